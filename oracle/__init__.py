@@ -1,0 +1,226 @@
+"""fp64 CPU oracle of the Kalman Linear Attention filter.
+
+TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the CPU-baseline
+leg of the benchmark may import this package; the product path never does, and
+it shares no code with the GPU kernels.
+
+The arithmetic lives in ``kla_oracle.c`` (plain sequential C, double precision):
+each (batch, head, key slot, value channel) runs the scalar information filter
+of Theorems 1 and 2 token after token, and the readout contracts over the key
+slot as in Algorithm 1.  This module only marshals numpy arrays.
+
+Shapes follow the row-major ``[B, T, H, *]`` layout of the product:
+``q, k, a, p`` are ``[B, T, H, dk]``, ``v`` is ``[B, T, H, dv]``.  The value
+precision ``r`` may be ``[B, T, H]`` (one precision per token and head, the
+product's layout) or ``[B, T, H, dv]`` (one per value channel, the literal
+shape in Algorithm 1).  In the first case results come back in the product's
+shapes: ``yvar [B, T, H]``, ``lamT [B, H, dk]``, ``dr [B, T, H]`` and
+``dlam0 [B, H, dk]``; the per-channel copies of the precision, which then all
+coincide, are reduced (the final precision reads channel 0; the gradient of an
+initial precision shared by all channels is the sum over channels).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "_kla_oracle.so")
+_lib = None
+
+_D = ctypes.POINTER(ctypes.c_double)
+_I = ctypes.c_int
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _b
+        _b.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.kla_oracle_forward.argtypes = [_I] * 5 + [_D] * 12 + [_I]
+    lib.kla_oracle_backward.argtypes = [_I] * 5 + [_D] * 19 + [_I]
+    lib.kla_oracle_decode_step.argtypes = [_I] * 4 + [_D] * 10
+    lib.kla_oracle_trace.argtypes = [_I] * 3 + [_D] * 9
+    lib.kla_oracle_mobius_matrix.argtypes = [ctypes.c_double] * 4 + [_D]
+    lib.kla_oracle_mobius_compose.argtypes = [_D] * 3
+    lib.kla_oracle_mobius_apply.argtypes = [_D, ctypes.c_double]
+    lib.kla_oracle_mobius_apply.restype = ctypes.c_double
+    lib.kla_oracle_affine_compose.argtypes = [_I] + [_D] * 6
+    for fn in ("kla_oracle_forward", "kla_oracle_backward", "kla_oracle_decode_step",
+               "kla_oracle_trace", "kla_oracle_mobius_matrix", "kla_oracle_mobius_compose",
+               "kla_oracle_affine_compose"):
+        getattr(lib, fn).restype = None
+    _lib = lib
+    return lib
+
+
+def _c(x) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _ptr(x: Optional[np.ndarray]):
+    if x is None:
+        return ctypes.cast(None, _D)
+    return x.ctypes.data_as(_D)
+
+
+def default_threads() -> int:
+    try:
+        return max(1, len(os.sched_getaffinity(0)))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+def _prep(q, k, v, a, p, r, lam0, eta0):
+    q, k, v, a, p, r = (_c(x) for x in (q, k, v, a, p, r))
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    per_head = r.ndim == 3
+    if per_head:
+        r = _c(np.broadcast_to(r[..., None], (B, T, H, dv)))
+    if lam0 is not None:
+        lam0 = _c(lam0)
+        if lam0.ndim == 3:
+            lam0 = _c(np.broadcast_to(lam0[..., None], (B, H, dk, dv)))
+    if eta0 is not None:
+        eta0 = _c(eta0)
+    return q, k, v, a, p, r, lam0, eta0, (B, T, H, dk, dv), per_head
+
+
+def forward(q, k, v, a, p, r, lam0=None, eta0=None, nthreads: Optional[int] = None) -> dict:
+    """Sequential filter over the whole sequence; returns y, yvar, lamT, etaT."""
+    lib = _load()
+    q, k, v, a, p, r, lam0, eta0, (B, T, H, dk, dv), per_head = _prep(q, k, v, a, p, r, lam0, eta0)
+    y = np.empty((B, T, H, dv))
+    yvar = np.empty((B, T, H, dv))
+    lamT = np.empty((B, H, dk, dv))
+    etaT = np.empty((B, H, dk, dv))
+    lib.kla_oracle_forward(B, T, H, dk, dv, _ptr(q), _ptr(k), _ptr(v), _ptr(a), _ptr(p), _ptr(r),
+                           _ptr(lam0), _ptr(eta0), _ptr(y), _ptr(yvar), _ptr(lamT), _ptr(etaT),
+                           nthreads or default_threads())
+    if per_head:
+        yvar = yvar[..., 0].copy()
+        lamT = lamT[..., 0].copy()
+    return {"y": y, "yvar": yvar, "lamT": lamT, "etaT": etaT}
+
+
+def backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None,
+             nthreads: Optional[int] = None) -> dict:
+    """Exact reverse-mode gradient of ``forward``'s y, lamT and etaT."""
+    lib = _load()
+    lam0_in_shape = None if lam0 is None else np.asarray(lam0).shape
+    q, k, v, a, p, r, lam0, eta0, (B, T, H, dk, dv), per_head = _prep(q, k, v, a, p, r, lam0, eta0)
+    dy = _c(dy)
+    if dlamT is not None:
+        dlamT = _c(dlamT)
+        if dlamT.ndim == 3:
+            # the final precision is shared by all channels: seed channel 0 only
+            full = np.zeros((B, H, dk, dv))
+            full[..., 0] = dlamT
+            dlamT = full
+    if detaT is not None:
+        detaT = _c(detaT)
+    out = {n: np.empty((B, T, H, dk)) for n in ("dq", "dk", "da", "dp")}
+    out["dv"] = np.empty((B, T, H, dv))
+    out["dr"] = np.empty((B, T, H, dv))
+    dlam0 = np.empty((B, H, dk, dv))
+    deta0 = np.empty((B, H, dk, dv))
+    lib.kla_oracle_backward(B, T, H, dk, dv, _ptr(q), _ptr(k), _ptr(v), _ptr(a), _ptr(p), _ptr(r),
+                            _ptr(lam0), _ptr(eta0), _ptr(dy), _ptr(dlamT), _ptr(detaT),
+                            _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["da"]),
+                            _ptr(out["dp"]), _ptr(out["dr"]), _ptr(dlam0), _ptr(deta0),
+                            nthreads or default_threads())
+    if per_head:
+        out["dr"] = out["dr"].sum(-1)
+    if lam0_in_shape is not None and len(lam0_in_shape) == 3:
+        dlam0 = dlam0.sum(-1)
+    out["dlam0"] = dlam0
+    out["deta0"] = deta0
+    return out
+
+
+def decode_step(q, k, v, a, p, r, lam, eta) -> dict:
+    """One recurrent step on a carried belief; inputs ``[S, H, *]``.
+
+    ``lam`` may be ``[S, H, dk]`` (shared over channels) or ``[S, H, dk, dv]``.
+    Returns new copies: y, yvar, lam, eta (input arrays are not modified)."""
+    lib = _load()
+    q, k, v, a, p, r = (_c(x) for x in (q, k, v, a, p, r))
+    S, H, dk = k.shape
+    dv = v.shape[-1]
+    per_head = r.ndim == 2
+    if per_head:
+        r = _c(np.broadcast_to(r[..., None], (S, H, dv)))
+    lam = _c(lam).copy()
+    lam_per_slot = lam.ndim == 3
+    if lam_per_slot:
+        lam = _c(np.broadcast_to(lam[..., None], (S, H, dk, dv)))
+    eta = _c(eta).copy()
+    y = np.empty((S, H, dv))
+    yvar = np.empty((S, H, dv))
+    lib.kla_oracle_decode_step(S, H, dk, dv, _ptr(q), _ptr(k), _ptr(v), _ptr(a), _ptr(p), _ptr(r),
+                               _ptr(lam), _ptr(eta), _ptr(y), _ptr(yvar))
+    if per_head:
+        yvar = yvar[..., 0].copy()
+    if lam_per_slot:
+        lam = lam[..., 0].copy()
+    return {"y": y, "yvar": yvar, "lam": lam, "eta": eta}
+
+
+def trace(k, v, a, p, r, lam0=None, eta0=None) -> tuple[np.ndarray, np.ndarray]:
+    """Whole (lam, eta) trajectory of one sequence: k, a, p [T, dk]; v, r [T, dv].
+
+    Returns two ``[T+1, dk, dv]`` arrays; row 0 is the prior belief."""
+    lib = _load()
+    k, v, a, p, r = (_c(x) for x in (k, v, a, p, r))
+    T, dk = k.shape
+    dv = v.shape[1]
+    lam0 = None if lam0 is None else _c(np.broadcast_to(lam0, (dk, dv)))
+    eta0 = None if eta0 is None else _c(np.broadcast_to(eta0, (dk, dv)))
+    lt = np.empty((T + 1, dk, dv))
+    et = np.empty((T + 1, dk, dv))
+    lib.kla_oracle_trace(T, dk, dv, _ptr(k), _ptr(v), _ptr(a), _ptr(p), _ptr(r),
+                         _ptr(lam0), _ptr(eta0), _ptr(lt), _ptr(et))
+    return lt, et
+
+
+def mobius_matrix(k: float, a: float, p: float, r: float) -> np.ndarray:
+    """Per-token 2x2 Moebius matrix of the precision update (Theorem 1)."""
+    M = np.empty(4)
+    _load().kla_oracle_mobius_matrix(float(k), float(a), float(p), float(r), _ptr(M))
+    return M.reshape(2, 2)
+
+
+def mobius_compose(M2, M1) -> np.ndarray:
+    """``M2`` after ``M1`` (Corollary 1)."""
+    A, Bm, out = _c(M2).reshape(4), _c(M1).reshape(4), np.empty(4)
+    _load().kla_oracle_mobius_compose(_ptr(A), _ptr(Bm), _ptr(out))
+    return out.reshape(2, 2)
+
+
+def mobius_apply(M, lam: float) -> float:
+    return float(_load().kla_oracle_mobius_apply(_ptr(_c(M).reshape(4)), float(lam)))
+
+
+def affine_compose(f2, b2, f1, b1) -> tuple[np.ndarray, np.ndarray]:
+    """``(f2, b2)`` after ``(f1, b1)`` for a diagonal gate f over the rows of b (Corollary 2)."""
+    b1 = _c(b1)
+    b2 = _c(b2)
+    shape = np.broadcast_shapes(b1.shape, b2.shape)
+    f1 = _c(np.broadcast_to(np.asarray(f1, dtype=np.float64).reshape(
+        np.asarray(f1).shape + (1,) * (len(shape) - np.ndim(f1))), shape))
+    f2 = _c(np.broadcast_to(np.asarray(f2, dtype=np.float64).reshape(
+        np.asarray(f2).shape + (1,) * (len(shape) - np.ndim(f2))), shape))
+    b1 = _c(np.broadcast_to(b1, shape))
+    b2 = _c(np.broadcast_to(b2, shape))
+    fo = np.empty(shape)
+    bo = np.empty(shape)
+    _load().kla_oracle_affine_compose(int(np.prod(shape)), _ptr(f2), _ptr(b2), _ptr(f1), _ptr(b1),
+                                      _ptr(fo), _ptr(bo))
+    return fo, bo
