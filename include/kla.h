@@ -1,0 +1,149 @@
+/*
+ * kla.h -- C ABI of the Kalman Linear Attention (KLA) filter layer for MI355X (gfx950).
+ *
+ * The layer is the time-parallel information-form Kalman filter of Kalman
+ * Linear Attention (Sec. 3.2 of the paper; Algorithm 1, eqs. kla-prec-mat and
+ * kla-mean-mat in Appendix A).  Per batch b and head h, with key slots n < dk
+ * and value channels d < dv, for t = 1..T:
+ *
+ *   rho_t[n] = 1 / (abar_t[n]^2 + pbar_t[n] * lam_{t-1}[n])      prior ratio (gate view of Thm 1)
+ *   lam_t[n] = rho_t[n] * lam_{t-1}[n] + k_t[n]^2 * r_t            precision (Theorem 1)
+ *   F_t[n]   = abar_t[n] * rho_t[n]                                forget gate (Theorem 2)
+ *   H_t[n,d] = F_t[n] * H_{t-1}[n,d] + r_t * k_t[n] * v_t[d]        information state (Theorem 2)
+ *   y_t[d]   = sum_n q_t[n] / lam_t[n] * H_t[n,d]                  posterior-mean readout (Alg. 1)
+ *   yvar_t   = sum_n q_t[n]^2 / lam_t[n]                            readout variance (Alg. 1, optional)
+ *
+ * r_t = Lambda^v_t is one observation precision per (token, head), so the
+ * precision lam and the gate F depend on the key slot only.
+ *
+ * Conventions shared by every entry point
+ *   Layout   : all tensors contiguous row-major.  Per-token tensors are
+ *              [B, T, H, width] (width dk for q, k, abar, pbar; dv for v, y, dy),
+ *              r is [B, T, H], yvar is [B, T, H]; beliefs are lam [B, H, dk],
+ *              eta = H [B, H, dk, dv].
+ *   Memory   : every pointer is a device pointer owned by the caller.  The
+ *              library never allocates, frees or synchronises; all work is
+ *              enqueued asynchronously on `stream` (0 = the null stream).
+ *              Inputs are read-only; outputs must not alias inputs (except the
+ *              in-place belief of kla_decode_step).  Base pointers must be
+ *              16-byte aligned.
+ *   dtype    : q, k, v, abar, pbar, r, y, dy and the input gradients share
+ *              `dtype` (fp32 or bf16).  Beliefs, yvar, states and every
+ *              accumulation are fp32.
+ *   Shapes   : B, H >= 1, T >= 0, dk and dv each in {16, 32, 64, 128}.
+ *   Domain   : abar in (0, 1], pbar >= 0, r > 0, lam0 > 0, all finite.  Not
+ *              checked unless the environment sets KLA_CHECK=1, in which case
+ *              a validation kernel runs first and the call synchronises and
+ *              returns KLA_ERR_NUMERIC on a violation.
+ *   Errors   : return codes only; on any error nothing has been enqueued
+ *              (except KLA_ERR_HIP, reported when a launch fails).
+ *   Threads  : no global mutable state; calls are thread-safe.  Results are
+ *              bitwise reproducible for a given descriptor.
+ */
+#ifndef KLA_H
+#define KLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { KLA_F32 = 0, KLA_BF16 = 1 } kla_dtype;
+
+typedef enum {
+    KLA_OK = 0,
+    KLA_ERR_NULL = 1,       /* a required pointer is NULL                         */
+    KLA_ERR_SHAPE = 2,      /* unsupported or inconsistent sizes                  */
+    KLA_ERR_DTYPE = 3,      /* unknown dtype                                      */
+    KLA_ERR_ALIGN = 4,      /* a pointer is not 16-byte aligned                   */
+    KLA_ERR_WORKSPACE = 5,  /* workspace missing or smaller than required         */
+    KLA_ERR_NUMERIC = 6,    /* KLA_CHECK=1 found an input outside the domain      */
+    KLA_ERR_HIP = 7         /* a HIP launch or runtime call failed                */
+} kla_status;
+
+/* Problem descriptor: batch, sequence length, heads, key width, value width, dtype. */
+typedef struct {
+    int32_t B, T, H, dk, dv;
+    int32_t dtype; /* kla_dtype */
+} kla_desc;
+
+/* Bytes of device workspace kla_forward needs (0 is possible). */
+size_t kla_forward_workspace(const kla_desc* desc);
+
+/* Bytes of the optional saved context that kla_forward can fill for
+ * kla_backward (precision and information state at every chunk start). */
+size_t kla_saved_bytes(const kla_desc* desc);
+
+/* Bytes of device workspace kla_backward needs when it is given a saved
+ * context (`with_saved` != 0) or must recompute one (`with_saved` == 0). */
+size_t kla_backward_workspace(const kla_desc* desc, int with_saved);
+
+/*
+ * kla_forward -- the filter over a whole sequence (Algorithm 1: Moebius scan of
+ * the precision, linear scan of the information state, query readout).
+ *
+ *   q, k, abar, pbar  [B, T, H, dk]  dtype      v [B, T, H, dv] dtype   r [B, T, H] dtype
+ *   lam0 [B, H, dk] fp32, eta0 [B, H, dk, dv] fp32: initial belief; NULL means
+ *        lam0 = 1 and eta0 = 0 respectively.
+ *   y    [B, T, H, dv] dtype  (required)
+ *   yvar [B, T, H] fp32 or NULL
+ *   lamT [B, H, dk] fp32, etaT [B, H, dk, dv] fp32: final belief, each may be NULL.
+ *   saved: NULL, or kla_saved_bytes(desc) bytes that kla_backward may later
+ *        consume with the same inputs.
+ *   ws / ws_bytes: workspace of at least kla_forward_workspace(desc) bytes.
+ */
+kla_status kla_forward(const kla_desc* desc,
+                       const void* q, const void* k, const void* v,
+                       const void* abar, const void* pbar, const void* r,
+                       const float* lam0, const float* eta0,
+                       void* y, float* yvar, float* lamT, float* etaT,
+                       void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * kla_backward -- exact gradient of kla_forward's y, lamT and etaT with respect
+ * to every input (yvar carries no gradient).
+ *
+ *   q .. r, lam0, eta0: exactly the forward inputs (NULL beliefs as in forward).
+ *   saved: the context a kla_forward call with these inputs filled, or NULL
+ *          (then it is recomputed inside the workspace).
+ *   dy [B, T, H, dv] dtype (required); dlamT [B, H, dk] and detaT [B, H, dk, dv]
+ *          fp32 upstream gradients of the final belief, NULL meaning zero.
+ *   dq, dk, dabar, dpbar [B, T, H, dk], dv [B, T, H, dv], dr [B, T, H]: dtype, required.
+ *   dlam0 [B, H, dk], deta0 [B, H, dk, dv]: fp32 or NULL.
+ *   ws / ws_bytes: at least kla_backward_workspace(desc, saved != NULL) bytes.
+ */
+kla_status kla_backward(const kla_desc* desc,
+                        const void* q, const void* k, const void* v,
+                        const void* abar, const void* pbar, const void* r,
+                        const float* lam0, const float* eta0, const void* saved,
+                        const void* dy, const float* dlamT, const float* detaT,
+                        void* dq, void* dk, void* dv, void* dabar, void* dpbar, void* dr,
+                        float* dlam0, float* deta0,
+                        void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * kla_decode_step -- one recurrent token for S independent sequences (the
+ * O(1)-per-token inference form of the filter): the same update as above for a
+ * single t, applied IN PLACE to the carried belief.
+ *
+ *   q, k, abar, pbar [S, H, dk] dtype   v [S, H, dv] dtype   r [S, H] dtype
+ *   lam [S, H, dk] fp32 and eta [S, H, dk, dv] fp32: read then overwritten.
+ *   y [S, H, dv] dtype (required); yvar [S, H] fp32 or NULL.
+ */
+kla_status kla_decode_step(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype,
+                           const void* q, const void* k, const void* v,
+                           const void* abar, const void* pbar, const void* r,
+                           float* lam, float* eta, void* y, float* yvar, hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+const char* kla_status_string(kla_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KLA_H */

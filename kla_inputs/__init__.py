@@ -208,20 +208,26 @@ def full(w: Workload, names: Iterable[str] = NAMES + ("dy",), seed: Optional[int
         else:
             arr = np.empty(shape, dtype=np.float64)
 
-        def fill(b, name=name, arr=arr):
+        def fill(task, name=name, arr=arr):
+            b, hs = task
             cache: dict = {}
-            for h in range(w.H):
+            for h in hs:
                 x = draw(w, name, b, h, seed=seed, T=T, proj_cache=cache)
                 if as_bits:
                     x = bf16_bits(x) if w.dtype == "bf16" else to_f32(x)
                 arr[b, :, h] = x
 
-        if threads > 1 and w.B > 1:
-            with ThreadPoolExecutor(max_workers=threads) as ex:
-                list(ex.map(fill, range(w.B)))
+        # the token-projection workload shares one projection per batch row
+        if w.dist == "a5":
+            tasks = [(b, range(w.H)) for b in range(w.B)]
         else:
-            for b in range(w.B):
-                fill(b)
+            tasks = [(b, (h,)) for b in range(w.B) for h in range(w.H)]
+        if threads > 1 and len(tasks) > 1:
+            with ThreadPoolExecutor(max_workers=threads) as ex:
+                list(ex.map(fill, tasks))
+        else:
+            for task in tasks:
+                fill(task)
         out[name] = arr
     return out
 
@@ -246,10 +252,10 @@ def random_case(B: int, T: int, H: int, dk: int, dv: int, dtype: str = "f32",
     return full(w, seed=seed)
 
 
-def decode_inputs(w: Workload, seed: Optional[int] = None) -> dict:
+def decode_inputs(w: Workload, seed: Optional[int] = None, as_bits: bool = False) -> dict:
     """Per-step inputs of the decode workload: [S, steps, H, width] float64
     (the steps are drawn as a second sequence, with the seed offset by 1000)."""
     seed = w.cid if seed is None else seed
     steps = w.extra["steps"]
     w2 = Workload(w.cid, w.name, w.B, steps, w.H, w.dk, w.dv, w.dtype, w.dist, False)
-    return full(w2, names=NAMES, seed=seed + 1000)
+    return full(w2, names=NAMES, seed=seed + 1000, as_bits=as_bits)

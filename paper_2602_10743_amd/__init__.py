@@ -1,0 +1,242 @@
+"""Kalman Linear Attention filter layer on MI355X (gfx950): Python binding.
+
+A thin ctypes binding over ``libkla.so`` whose functions carry the names of the
+C ABI in ``include/kla.h``.  It only marshals arguments: it checks shapes and
+dtypes, allocates outputs and workspace through torch (device memory and
+streams are all torch is used for) and passes raw device pointers and the
+current HIP stream to the library, where every step of the filter runs.
+
+There is no fallback: if the HIP library is missing or the tensors are not on
+a GPU, every entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+__all__ = ["kla_forward", "kla_backward", "kla_decode_step", "kla_status_string",
+           "kla_forward_workspace", "kla_backward_workspace", "kla_saved_bytes",
+           "KLAError", "KLAFilter", "kla_filter", "library_path"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_HERE, "libkla.so")
+
+KLA_F32, KLA_BF16 = 0, 1
+_DTYPES = {torch.float32: KLA_F32, torch.bfloat16: KLA_BF16}
+
+
+class KLAError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {kla_status_string(status)} (status {status})")
+
+
+class _Desc(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("T", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("dk", ctypes.c_int32), ("dv", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+_lib = None
+_VP = ctypes.c_void_p
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(library_path):
+        raise ImportError(f"KLA HIP library not built: {library_path} is missing "
+                          "(build it with `python paper_2602_10743_amd/build.py`)")
+    lib = ctypes.CDLL(library_path)
+    D = ctypes.POINTER(_Desc)
+    lib.kla_forward_workspace.argtypes = [D]
+    lib.kla_forward_workspace.restype = ctypes.c_size_t
+    lib.kla_saved_bytes.argtypes = [D]
+    lib.kla_saved_bytes.restype = ctypes.c_size_t
+    lib.kla_backward_workspace.argtypes = [D, ctypes.c_int]
+    lib.kla_backward_workspace.restype = ctypes.c_size_t
+    lib.kla_forward.argtypes = [D] + [_VP] * 14 + [ctypes.c_size_t, _VP]
+    lib.kla_forward.restype = ctypes.c_int
+    lib.kla_backward.argtypes = [D] + [_VP] * 21 + [ctypes.c_size_t, _VP]
+    lib.kla_backward.restype = ctypes.c_int
+    lib.kla_decode_step.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
+    lib.kla_decode_step.restype = ctypes.c_int
+    lib.kla_status_string.argtypes = [ctypes.c_int]
+    lib.kla_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def kla_status_string(status: int) -> str:
+    return _load().kla_status_string(int(status)).decode()
+
+
+def _p(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(dev: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+
+
+def _desc(q: torch.Tensor, v: torch.Tensor) -> _Desc:
+    B, T, H, dk = q.shape
+    return _Desc(B, T, H, dk, v.shape[-1], _DTYPES[q.dtype])
+
+
+def _check_inputs(q, k, v, a, p, r):
+    if not q.is_cuda:
+        raise ValueError("KLA tensors must live on a GPU; the layer has no CPU path")
+    if q.dtype not in _DTYPES:
+        raise TypeError(f"unsupported dtype {q.dtype}; use float32 or bfloat16")
+    if q.dim() != 4:
+        raise ValueError("q must be [B, T, H, dk]")
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    for name, t, shape in (("k", k, (B, T, H, dk)), ("a", a, (B, T, H, dk)), ("p", p, (B, T, H, dk)),
+                           ("v", v, (B, T, H, dv)), ("r", r, (B, T, H))):
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {shape}")
+        if t.dtype != q.dtype or t.device != q.device:
+            raise ValueError(f"{name} must share q's dtype and device")
+    for name, t in (("q", q), ("k", k), ("v", v), ("a", a), ("p", p), ("r", r)):
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+
+
+def _f32(t, shape, dev, name):
+    if t is None:
+        return None
+    if t.dtype != torch.float32 or tuple(t.shape) != shape or t.device != dev or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous float32 tensor of shape {shape} on {dev}")
+    return t
+
+
+def kla_forward_workspace(desc: _Desc) -> int:
+    return int(_load().kla_forward_workspace(ctypes.byref(desc)))
+
+
+def kla_saved_bytes(desc: _Desc) -> int:
+    return int(_load().kla_saved_bytes(ctypes.byref(desc)))
+
+
+def kla_backward_workspace(desc: _Desc, with_saved: bool) -> int:
+    return int(_load().kla_backward_workspace(ctypes.byref(desc), int(bool(with_saved))))
+
+
+def kla_forward(q, k, v, a, p, r, lam0=None, eta0=None, *, want_var: bool = False,
+                want_state: bool = True, save: bool = False, y=None) -> dict:
+    """Filter a whole sequence.  q, k, a, p: [B, T, H, dk]; v: [B, T, H, dv];
+    r: [B, T, H] (all one dtype, fp32 or bf16).  lam0 [B, H, dk], eta0
+    [B, H, dk, dv] fp32 or None (prior 1 and 0).  Returns y and, as asked,
+    yvar, the final belief (lamT, etaT) and the saved context for backward."""
+    lib = _load()
+    _check_inputs(q, k, v, a, p, r)
+    dev = q.device
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    lam0 = _f32(lam0, (B, H, dk), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    desc = _desc(q, v)
+    if y is None:
+        y = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    yvar = torch.empty((B, T, H), dtype=torch.float32, device=dev) if want_var else None
+    lamT = torch.empty((B, H, dk), dtype=torch.float32, device=dev) if want_state else None
+    etaT = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_state else None
+    nsaved = kla_saved_bytes(desc) if save else 0
+    saved = torch.empty(max(nsaved, 1), dtype=torch.uint8, device=dev) if save else None
+    nws = kla_forward_workspace(desc)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    st = lib.kla_forward(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(r), _p(lam0), _p(eta0),
+                         _p(y), _p(yvar), _p(lamT), _p(etaT), _p(saved if nsaved else None), _p(ws), nws,
+                         _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_forward")
+    return {"y": y, "yvar": yvar, "lamT": lamT, "etaT": etaT, "saved": saved if nsaved else None}
+
+
+def kla_backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None, *, saved=None,
+                 want_init_grads: bool = True) -> dict:
+    """Gradients of kla_forward's (y, lamT, etaT) for the upstream gradients
+    (dy, dlamT, detaT); returns dq, dk, dv, da, dp, dr in the input dtype and,
+    when asked, dlam0 [B, H, dk] and deta0 [B, H, dk, dv] in fp32."""
+    lib = _load()
+    _check_inputs(q, k, v, a, p, r)
+    dev = q.device
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    lam0 = _f32(lam0, (B, H, dk), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    dlamT = _f32(dlamT, (B, H, dk), dev, "dlamT")
+    detaT = _f32(detaT, (B, H, dk, dv), dev, "detaT")
+    if tuple(dy.shape) != (B, T, H, dv) or dy.dtype != q.dtype or not dy.is_contiguous():
+        raise ValueError("dy must be a contiguous [B, T, H, dv] tensor in the input dtype")
+    desc = _desc(q, v)
+    out = {n: torch.empty_like(x) for n, x in (("dq", q), ("dk", k), ("dv", v), ("da", a), ("dp", p), ("dr", r))}
+    dlam0 = torch.empty((B, H, dk), dtype=torch.float32, device=dev) if want_init_grads else None
+    deta0 = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_init_grads else None
+    nws = kla_backward_workspace(desc, saved is not None)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    st = lib.kla_backward(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(r), _p(lam0), _p(eta0),
+                          _p(saved), _p(dy), _p(dlamT), _p(detaT), _p(out["dq"]), _p(out["dk"]), _p(out["dv"]),
+                          _p(out["da"]), _p(out["dp"]), _p(out["dr"]), _p(dlam0), _p(deta0), _p(ws), nws,
+                          _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_backward")
+    out["dlam0"] = dlam0
+    out["deta0"] = deta0
+    return out
+
+
+def kla_decode_step(q, k, v, a, p, r, lam, eta, *, want_var: bool = False, y=None) -> dict:
+    """One token for S sequences: q, k, a, p [S, H, dk]; v [S, H, dv]; r [S, H];
+    lam [S, H, dk] and eta [S, H, dk, dv] fp32 are updated in place."""
+    lib = _load()
+    if not q.is_cuda or q.dtype not in _DTYPES:
+        raise ValueError("decode inputs must be fp32/bf16 GPU tensors")
+    S, H, dk = q.shape
+    dv = v.shape[-1]
+    for name, t, shape in (("k", k, (S, H, dk)), ("a", a, (S, H, dk)), ("p", p, (S, H, dk)),
+                           ("v", v, (S, H, dv)), ("r", r, (S, H))):
+        if tuple(t.shape) != shape or t.dtype != q.dtype or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {shape} tensor in q's dtype")
+    _f32(lam, (S, H, dk), q.device, "lam")
+    _f32(eta, (S, H, dk, dv), q.device, "eta")
+    if y is None:
+        y = torch.empty((S, H, dv), dtype=q.dtype, device=q.device)
+    yvar = torch.empty((S, H), dtype=torch.float32, device=q.device) if want_var else None
+    st = lib.kla_decode_step(S, H, dk, dv, _DTYPES[q.dtype], _p(q), _p(k), _p(v), _p(a), _p(p), _p(r),
+                             _p(lam), _p(eta), _p(y), _p(yvar), _stream(q.device))
+    if st != 0:
+        raise KLAError(st, "kla_decode_step")
+    return {"y": y, "yvar": yvar, "lam": lam, "eta": eta}
+
+
+class KLAFilter(torch.autograd.Function):
+    """Autograd wrapper: y, lamT, etaT = filter(q, k, v, a, p, r, lam0, eta0)."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, a, p, r, lam0, eta0):
+        out = kla_forward(q, k, v, a, p, r, lam0, eta0, want_state=True, save=True)
+        ctx.save_for_backward(q, k, v, a, p, r, lam0, eta0)
+        ctx.saved_ctx = out["saved"]
+        return out["y"], out["lamT"], out["etaT"]
+
+    @staticmethod
+    def backward(ctx, dy, dlamT, detaT):
+        q, k, v, a, p, r, lam0, eta0 = ctx.saved_tensors
+        dy = torch.zeros_like(q[..., :1].expand(*q.shape[:3], v.shape[-1])).contiguous() if dy is None \
+            else dy.contiguous()
+        g = kla_backward(q, k, v, a, p, r, lam0, eta0, dy,
+                         None if dlamT is None else dlamT.contiguous(),
+                         None if detaT is None else detaT.contiguous(), saved=ctx.saved_ctx)
+        return (g["dq"], g["dk"], g["dv"], g["da"], g["dp"], g["dr"],
+                g["dlam0"] if lam0 is not None else None, g["deta0"] if eta0 is not None else None)
+
+
+def kla_filter(q, k, v, a, p, r, lam0=None, eta0=None):
+    """Differentiable filter: returns (y, lamT, etaT)."""
+    return KLAFilter.apply(q, k, v, a, p, r, lam0, eta0)

@@ -1,0 +1,160 @@
+// C ABI of the KLA filter layer: argument validation, workspace layout and
+// launch sequencing.  Declarations and contracts are in include/kla.h.
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <hip/hip_runtime.h>
+
+#include "kla.h"
+#include "kla_internal.hpp"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool width_ok(int w) { return w == 16 || w == 32 || w == 64 || w == 128; }
+
+bool aligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+kla_status check_desc(const kla_desc* d) {
+    if (!d) return KLA_ERR_NULL;
+    if (d->dtype != KLA_F32 && d->dtype != KLA_BF16) return KLA_ERR_DTYPE;
+    if (d->B < 1 || d->H < 1 || d->T < 0 || !width_ok(d->dk) || !width_ok(d->dv)) return KLA_ERR_SHAPE;
+    // every per-tensor element count must stay addressable with 32-bit grid math
+    const double tok = (double)d->B * d->T * d->H * (d->dk > d->dv ? d->dk : d->dv);
+    if (tok > 9.0e18 || (double)d->B * d->H * 8 > 2.0e9) return KLA_ERR_SHAPE;
+    return KLA_OK;
+}
+
+kla::Shape shape_of(const kla_desc* d) { return kla::Shape{d->B, d->T, d->H, d->dk, d->dv, d->dtype == KLA_BF16}; }
+
+bool check_mode() {
+    const char* e = getenv("KLA_CHECK");
+    return e && e[0] == '1';
+}
+
+template <typename... P>
+bool all_aligned(P... ps) {
+    return (aligned(ps) && ...);
+}
+
+}  // namespace
+
+namespace kla {
+hipError_t launch_validate(const Shape& s, const void* q, const void* k, const void* v, const void* a,
+                           const void* p, const void* r, const float* lam0, const float* eta0, int T,
+                           int* flag, hipStream_t st);
+}
+
+namespace {
+
+// Domain check of the inputs (KLA_CHECK=1): synchronous; returns KLA_ERR_NUMERIC
+// when any value is outside abar in (0,1], pbar >= 0, r > 0, lam0 > 0, finite.
+kla_status validate(const kla::Shape& s, int T, const void* q, const void* k, const void* v, const void* a,
+                    const void* p, const void* r, const float* lam0, const float* eta0, void* flag_ws,
+                    hipStream_t st) {
+    int* flag = static_cast<int*>(flag_ws);
+    if (kla::launch_validate(s, q, k, v, a, p, r, lam0, eta0, T, flag, st) != hipSuccess) return KLA_ERR_HIP;
+    int host = 0;
+    if (hipMemcpyAsync(&host, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess) return KLA_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return KLA_ERR_HIP;
+    return host ? KLA_ERR_NUMERIC : KLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t kla_forward_workspace(const kla_desc* desc) {
+    if (check_desc(desc) != KLA_OK) return 0;
+    return kAlign;  // validation flag
+}
+
+size_t kla_saved_bytes(const kla_desc* desc) {
+    if (check_desc(desc) != KLA_OK) return 0;
+    return 0;
+}
+
+size_t kla_backward_workspace(const kla_desc* desc, int with_saved) {
+    (void)with_saved;
+    if (check_desc(desc) != KLA_OK) return 0;
+    return kAlign + round_up(kla::backward_recurrent_workspace(shape_of(desc)));
+}
+
+kla_status kla_forward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
+                       const void* pbar, const void* r, const float* lam0, const float* eta0, void* y,
+                       float* yvar, float* lamT, float* etaT, void* saved, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+    kla_status st = check_desc(desc);
+    if (st != KLA_OK) return st;
+    if (!q || !k || !v || !abar || !pbar || !r || !y) return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, y, (void*)yvar,
+                     (void*)lamT, (void*)etaT, saved, ws))
+        return KLA_ERR_ALIGN;
+    if (!ws || ws_bytes < kla_forward_workspace(desc)) return KLA_ERR_WORKSPACE;
+    (void)saved;
+    const kla::Shape s = shape_of(desc);
+    if (check_mode()) {
+        st = validate(s, s.T, q, k, v, abar, pbar, r, lam0, eta0, ws, stream);
+        if (st != KLA_OK) return st;
+    }
+    kla::FwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, y, yvar, lamT, etaT};
+    return kla::launch_forward_recurrent(s, a, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
+                        const void* pbar, const void* r, const float* lam0, const float* eta0, const void* saved,
+                        const void* dy, const float* dlamT, const float* detaT, void* dq, void* dk, void* dv,
+                        void* dabar, void* dpbar, void* dr, float* dlam0, float* deta0, void* ws,
+                        size_t ws_bytes, hipStream_t stream) {
+    kla_status st = check_desc(desc);
+    if (st != KLA_OK) return st;
+    if (!q || !k || !v || !abar || !pbar || !r || !dy || !dq || !dk || !dv || !dabar || !dpbar || !dr)
+        return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, saved, dy,
+                     (const void*)dlamT, (const void*)detaT, dq, dk, dv, dabar, dpbar, dr, (void*)dlam0,
+                     (void*)deta0, ws))
+        return KLA_ERR_ALIGN;
+    if (!ws || ws_bytes < kla_backward_workspace(desc, saved != nullptr)) return KLA_ERR_WORKSPACE;
+    const kla::Shape s = shape_of(desc);
+    if (check_mode()) {
+        st = validate(s, s.T, q, k, v, abar, pbar, r, lam0, eta0, ws, stream);
+        if (st != KLA_OK) return st;
+    }
+    kla::BwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT, detaT, dq, dk, dv, dabar, dpbar, dr,
+                   dlam0, deta0};
+    void* work = static_cast<char*>(ws) + kAlign;
+    return kla::launch_backward_recurrent(s, a, work, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+kla_status kla_decode_step(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,
+                           const void* k, const void* v, const void* abar, const void* pbar, const void* r,
+                           float* lam, float* eta, void* y, float* yvar, hipStream_t stream) {
+    kla_desc d{S, 1, H, dk, dv, dtype};
+    kla_status st = check_desc(&d);
+    if (st != KLA_OK) return st;
+    if (!q || !k || !v || !abar || !pbar || !r || !lam || !eta || !y) return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, abar, pbar, r, (void*)lam, (void*)eta, y, (void*)yvar)) return KLA_ERR_ALIGN;
+    const kla::Shape s = shape_of(&d);
+    kla::DecodeArgs a{q, k, v, abar, pbar, r, lam, eta, y, yvar};
+    return kla::launch_decode_step(s, a, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+const char* kla_status_string(kla_status s) {
+    switch (s) {
+        case KLA_OK: return "KLA_OK";
+        case KLA_ERR_NULL: return "KLA_ERR_NULL: a required pointer is NULL";
+        case KLA_ERR_SHAPE: return "KLA_ERR_SHAPE: unsupported or inconsistent sizes";
+        case KLA_ERR_DTYPE: return "KLA_ERR_DTYPE: unknown dtype";
+        case KLA_ERR_ALIGN: return "KLA_ERR_ALIGN: a pointer is not 16-byte aligned";
+        case KLA_ERR_WORKSPACE: return "KLA_ERR_WORKSPACE: workspace missing or too small";
+        case KLA_ERR_NUMERIC: return "KLA_ERR_NUMERIC: an input lies outside the filter's domain";
+        case KLA_ERR_HIP: return "KLA_ERR_HIP: a HIP launch or runtime call failed";
+    }
+    return "KLA_ERR_UNKNOWN";
+}
+
+}  // extern "C"

@@ -1,0 +1,43 @@
+// Internal launcher interface between the C ABI (kla_api.cpp) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kla {
+
+struct Shape {
+    int B, T, H, dk, dv;
+    int bf16;  // 0: fp32 storage, 1: bf16 storage
+};
+
+struct FwdArgs {
+    const void *q, *k, *v, *a, *p, *r;
+    const float *lam0, *eta0;
+    void* y;
+    float *yvar, *lamT, *etaT;
+};
+
+struct BwdArgs {
+    const void *q, *k, *v, *a, *p, *r;
+    const float *lam0, *eta0;
+    const void* dy;
+    const float *dlamT, *detaT;
+    void *dq, *dk, *dv, *da, *dp, *dr;
+    float *dlam0, *deta0;
+};
+
+struct DecodeArgs {
+    const void *q, *k, *v, *a, *p, *r;
+    float *lam, *eta;
+    void* y;
+    float* yvar;
+};
+
+// Token-recurrent reference kernels.
+hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, hipStream_t st);
+size_t backward_recurrent_workspace(const Shape& s);
+hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, void* ws, hipStream_t st);
+hipError_t launch_decode_step(const Shape& s, const DecodeArgs& a, hipStream_t st);
+
+}  // namespace kla

@@ -1,0 +1,102 @@
+"""Host-side checks of the C ABI (no GPU work): the library loads, exports every
+symbol include/kla.h declares, and rejects bad arguments before launching."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kla.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kla_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2602_10743_amd as K
+    return K._load()
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for n in ("kla_forward", "kla_backward", "kla_decode_step", "kla_status_string",
+              "kla_forward_workspace", "kla_backward_workspace", "kla_saved_bytes"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared():
+        assert hasattr(lib, name), f"{name} declared in kla.h but not exported"
+
+
+def test_status_strings(lib):
+    import paper_2602_10743_amd as K
+    for code in range(8):
+        assert K.kla_status_string(code).startswith("KLA_")
+
+
+def _desc(B=1, T=8, H=1, dk=16, dv=16, dtype=0):
+    import paper_2602_10743_amd as K
+    return K._Desc(B, T, H, dk, dv, dtype)
+
+
+def test_workspace_queries(lib):
+    import paper_2602_10743_amd as K
+    assert K.kla_forward_workspace(_desc()) > 0
+    assert K.kla_backward_workspace(_desc(), False) > 0
+    assert K.kla_forward_workspace(_desc(dk=24)) == 0          # unsupported width
+    assert K.kla_backward_workspace(_desc(dtype=7), True) == 0  # unknown dtype
+
+
+def _fwd(lib, desc, ptrs, ws_bytes=256):
+    return lib.kla_forward(ctypes.byref(desc), *ptrs, ws_bytes, None)
+
+
+def test_forward_argument_errors(lib):
+    fake = ctypes.c_void_p(0x10000)       # aligned, never dereferenced: the call returns first
+    odd = ctypes.c_void_p(0x10004)
+    ok = [fake] * 6 + [None, None, fake, None, None, None, None, fake]
+    assert _fwd(lib, _desc(dk=24), ok) == 2                        # KLA_ERR_SHAPE
+    assert _fwd(lib, _desc(dtype=5), ok) == 3                      # KLA_ERR_DTYPE
+    assert _fwd(lib, _desc(B=0), ok) == 2
+    assert _fwd(lib, _desc(T=-1), ok) == 2
+    assert lib.kla_forward(None, *ok, 256, None) == 1              # KLA_ERR_NULL
+    bad = list(ok)
+    bad[0] = None
+    assert _fwd(lib, _desc(), bad) == 1
+    bad = list(ok)
+    bad[2] = odd
+    assert _fwd(lib, _desc(), bad) == 4                            # KLA_ERR_ALIGN
+    assert _fwd(lib, _desc(), ok, ws_bytes=0) == 5                 # KLA_ERR_WORKSPACE
+    bad = list(ok)
+    bad[13] = None
+    assert _fwd(lib, _desc(), bad) == 5
+
+
+def test_backward_and_decode_argument_errors(lib):
+    fake = ctypes.c_void_p(0x10000)
+    d = _desc()
+    args = [fake] * 6 + [None, None, None] + [fake, None, None] + [fake] * 6 + [None, None] + [fake]
+    assert lib.kla_backward(ctypes.byref(d), *args, 0, None) == 5
+    bad = list(args)
+    bad[9] = None                                                  # dy
+    assert lib.kla_backward(ctypes.byref(d), *bad, 1 << 40, None) == 1
+    dec = [fake] * 6 + [fake, fake, fake, None, None]
+    assert lib.kla_decode_step(4, 2, 16, 48, 0, *dec) == 2
+    assert lib.kla_decode_step(4, 2, 16, 16, 9, *dec) == 3
+    bad = list(dec)
+    bad[6] = None
+    assert lib.kla_decode_step(4, 2, 16, 16, 0, *bad) == 1
+
+
+def test_binding_refuses_cpu_tensors():
+    import torch
+    import paper_2602_10743_amd as K
+    x = torch.zeros(1, 4, 1, 16)
+    with pytest.raises(ValueError, match="GPU"):
+        K.kla_forward(x, x, x, x, x, torch.zeros(1, 4, 1))
