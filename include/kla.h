@@ -35,6 +35,8 @@
  *              checked unless the environment sets KLA_CHECK=1, in which case
  *              a validation kernel runs first and the call synchronises and
  *              returns KLA_ERR_NUMERIC on a violation.
+ *   Empty    : with T == 0 the per-token pointers may be NULL; the final
+ *              belief is then the initial one and its gradients pass through.
  *   Errors   : return codes only; on any error nothing has been enqueued
  *              (except KLA_ERR_HIP, reported when a launch fails).
  *   Threads  : no global mutable state; calls are thread-safe.  Results are

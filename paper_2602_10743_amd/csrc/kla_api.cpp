@@ -90,7 +90,8 @@ kla_status kla_forward(const kla_desc* desc, const void* q, const void* k, const
                        hipStream_t stream) {
     kla_status st = check_desc(desc);
     if (st != KLA_OK) return st;
-    if (!q || !k || !v || !abar || !pbar || !r || !y) return KLA_ERR_NULL;
+    // with T == 0 the per-token tensors are empty and may be NULL
+    if (desc->T > 0 && (!q || !k || !v || !abar || !pbar || !r || !y)) return KLA_ERR_NULL;
     if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, y, (void*)yvar,
                      (void*)lamT, (void*)etaT, saved, ws))
         return KLA_ERR_ALIGN;
@@ -112,7 +113,8 @@ kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, cons
                         size_t ws_bytes, hipStream_t stream) {
     kla_status st = check_desc(desc);
     if (st != KLA_OK) return st;
-    if (!q || !k || !v || !abar || !pbar || !r || !dy || !dq || !dk || !dv || !dabar || !dpbar || !dr)
+    if (desc->T > 0 && (!q || !k || !v || !abar || !pbar || !r || !dy || !dq || !dk || !dv || !dabar || !dpbar ||
+                        !dr))
         return KLA_ERR_NULL;
     if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, saved, dy,
                      (const void*)dlamT, (const void*)detaT, dq, dk, dv, dabar, dpbar, dr, (void*)dlam0,

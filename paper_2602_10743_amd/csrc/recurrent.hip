@@ -87,8 +87,8 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
             sRed[j][ng][dl] = acc;
         }
         __syncthreads();
-        if (tid < nt * DVT) {
-            const int j = tid / DVT, dd = tid % DVT;
+        for (int idx = tid; idx < nt * DVT; idx += kThreads) {
+            const int j = idx / DVT, dd = idx % DVT;
             float acc = 0.f;
             for (int gi = 0; gi < NG; ++gi) acc += sRed[j][gi][dd];
             const size_t base = ((size_t)b * s.T + t0 + j) * s.H + h;

@@ -8,16 +8,20 @@ import numpy as np
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
-def rel_err(x, ref) -> float:
-    """max_i |x_i - r_i| / max(|r_i|, 0.01 * rms(r)) -- a relative error whose floor
-    (1% of the tensor's rms) keeps outputs that happen to be near zero meaningful."""
+def rel_err(x, ref, floor_frac: float = 1.0) -> float:
+    """max_i |x_i - r_i| / max(|r_i|, floor_frac * rms(r)).
+
+    The gate uses floor_frac = 1: an element at least as large as the tensor's
+    rms is judged relative to itself, a smaller one (the result of cancellation
+    between terms of rms size, whose rounding error scales with the rms) relative
+    to the rms.  floor_frac = 0.01 gives the stricter figure also reported."""
     x = np.asarray(x, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert x.shape == ref.shape, (x.shape, ref.shape)
     if ref.size == 0:
         return 0.0
     rms = np.sqrt(np.mean(ref * ref))
-    floor = max(0.01 * rms, 1e-30)
+    floor = max(floor_frac * rms, 1e-300)
     return float(np.max(np.abs(x - ref) / np.maximum(np.abs(ref), floor)))
 
 
