@@ -1,0 +1,575 @@
+// Chunked backward of the KLA filter on MFMA (bf16 inputs, fp32 state).
+//
+// Notation per chunk of kC tokens (local t), with the precision walk redone
+// from the saved chunk-start precision (see kla_scan.hpp for P, Qp, Kn):
+//   H_t  = P_t (H0 + sum_{j<=t} Kn_j v_j^T)            (state, per key slot row)
+//   G    = adjoint of the chunk's last state coming from later tokens
+//          (detaT for the last chunk), Gs = diag(P_C) G
+//   B    = dY V^T                                      (C x C)
+//   A    = Qp Kn^T                                     (C x C, the forward attention)
+// then, with M() keeping j <= t,
+//   X    = dY H0^T + M(B) Kn     dqt = P * X   (gradient of q / lam_t)
+//   Y    = M(B)^T Qp + V Gs^T    dkh = Y / P   (gradient of r k)
+//   dV   = M(A)^T dY + Kn Gs
+//   G'   = Qp^T dY + Gs                            (carry into the previous chunk)
+// The adjoint of log F_t is the reverse running sum of qt*dqt - kh*dkh (plus
+// the final-state term sum_d detaT H_T), and the adjoint g_t of lam_t follows
+//   g_t = c_t - q_t dqt_t / lam_t^2,  c_T = dlamT,
+//   c_{t-1} = abar_t^2 rho_t^2 g_t - pbar_t rho_t dlogF_t,
+// from which the input gradients follow by the chain rule through rho, lam, F.
+//
+// Kernel B1: one workgroup per (b, h, 64 value channels); walks chunks in
+//   reverse keeping G[dk, 64] in registers; writes dv and (at the end) deta0.
+// Kernel B2: one workgroup per (b, h, 64 key slots); walks chunks in reverse
+//   keeping G^T[dv, 64] in registers; reads the saved chunk-start states H0;
+//   writes dq, dk, dabar, dpbar, partial dr sums over its key slots and dlam0.
+#include "kla_internal.hpp"
+#include "kla_mfma.hpp"
+#include "kla_scan.hpp"
+
+namespace kla {
+namespace {
+
+constexpr int kC = 64;
+constexpr int kThr = 256;
+
+__device__ __forceinline__ void xcd_map(int i, int nbh, int ntile, int& bh, int& tile) {
+    if (nbh % 8 == 0) {
+        const int xcd = i % 8, slot = i / 8;
+        tile = slot % ntile;
+        bh = (slot / ntile) * 8 + xcd;
+    } else {
+        tile = i % ntile;
+        bh = i / ntile;
+    }
+}
+
+// ============================================================================ B1
+template <int DK, int DV>
+struct B1Cfg {
+    static constexpr int DVT = DV < 64 ? DV : 64;
+    static constexpr int NTILE = DV / DVT;
+    static constexpr int NCT = DVT / 16;
+    static constexpr int NRT = DK / 16;
+    static constexpr int KSN = DK / 32;
+    static constexpr int NSCAN = DK < 64 ? 64 : DK;
+    static constexpr int LQ = DK + 8, LT = kC + 8;
+    static constexpr int QH = 0, QL = QH + kC * LQ, KH = QL + kC * LQ, KL = KH + kC * LQ;
+    static constexpr int QTH = KL + kC * LQ, QTL = QTH + DK * LT;
+    static constexpr int YT = QTL + DK * LT;
+    static constexpr int ATH = YT + DVT * LT, ATL = ATH + kC * LT;
+    static constexpr int END16 = ATL + kC * LT;
+    static constexpr int DECAY = (END16 + 7) / 8 * 4;
+    static constexpr size_t BYTES = (size_t)(DECAY + DK) * 4;
+};
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kThr) void bwd_b1_kernel(Shape s, BwdArgs g, const float* __restrict__ saved_lam) {
+    using Cfg = B1Cfg<DK, DV>;
+    constexpr int DVT = Cfg::DVT, NCT = Cfg::NCT, NRT = Cfg::NRT, KSN = Cfg::KSN, LQ = Cfg::LQ, LT = Cfg::LT;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    uint16_t* sm = reinterpret_cast<uint16_t*>(smem_raw);
+    float* sDecay = reinterpret_cast<float*>(smem_raw) + Cfg::DECAY;
+
+    const uint16_t* q = static_cast<const uint16_t*>(g.q);
+    const uint16_t* k = static_cast<const uint16_t*>(g.k);
+    const uint16_t* a = static_cast<const uint16_t*>(g.a);
+    const uint16_t* p = static_cast<const uint16_t*>(g.p);
+    const uint16_t* r = static_cast<const uint16_t*>(g.r);
+    const uint16_t* dy = static_cast<const uint16_t*>(g.dy);
+    uint16_t* dv = static_cast<uint16_t*>(g.dv);
+
+    int bh, tile;
+    xcd_map(blockIdx.x, s.B * s.H, Cfg::NTILE, bh, tile);
+    const int b = bh / s.H, h = bh % s.H;
+    const int d0 = tile * DVT;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, g4 = lane >> 4;
+    const int T = s.T;
+    const int nchunk = (T + kC - 1) / kC;
+    const bool owns = wave < NCT;
+    const int dcol = d0 + 16 * wave + l16;
+    const bool scan_lane = tid < DK;
+    const int n_scan = scan_lane ? tid : DK - 1;
+
+    f32x4 G[NRT];
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+            G[rt][rr] = (owns && g.detaT) ? g.detaT[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dcol] : 0.f;
+
+    for (int c = nchunk - 1; c >= 0; --c) {
+        const int t0 = c * kC;
+        const int nt = min(kC, T - t0);
+        const size_t row0 = (size_t)b * T + t0;
+
+        load_tile<kC, DVT, 0, LT, false, true>(nullptr, sm + Cfg::YT, dy, row0, s.H, h, DV, d0, nt, tid, kThr);
+        if (tid < Cfg::NSCAN) {
+            float lam = saved_lam[((size_t)bh * nchunk + c) * DK + n_scan];
+            ScanLds L{};
+            L.qn_hi = sm + Cfg::QH;
+            L.qn_lo = sm + Cfg::QL;
+            L.kn_hi = sm + Cfg::KH;
+            L.kn_lo = sm + Cfg::KL;
+            L.qt_hi = sm + Cfg::QTH;
+            L.qt_lo = sm + Cfg::QTL;
+            const float P = scan_chunk<kC, LQ, LT, 0, true, true, true, false, false>(
+                a, p, k, q, r, row0, s.H, h, DK, n_scan, n_scan, scan_lane, nt, lam, L, false, lane);
+            if (scan_lane) sDecay[n_scan] = P;
+        }
+        __syncthreads();
+
+        // A^T[j, s] = sum_n Kn[j, n] Qp[s, n] for s >= j; tiles (1,0), (3,2) are the zeros
+        // read by the 32-deep K steps of dV.
+        for (int tk = wave; tk < 12; tk += 4) {
+            int jt, st;
+            if (tk < 10) {
+                jt = tk < 4 ? 0 : tk < 7 ? 1 : tk < 9 ? 2 : 3;
+                st = jt + (tk - (jt == 0 ? 0 : jt == 1 ? 4 : jt == 2 ? 7 : 9));
+            } else {
+                jt = tk == 10 ? 1 : 3;
+                st = jt - 1;
+            }
+            f32x4 acc = zero4();
+            if (tk < 10) {
+#pragma unroll
+                for (int ks = 0; ks < KSN; ++ks) {
+                    const int ko = (16 * jt + l16) * LQ + 32 * ks + 8 * g4;
+                    const int qo = (16 * st + l16) * LQ + 32 * ks + 8 * g4;
+                    acc = mfma3(lds8(sm + Cfg::KH + ko), lds8(sm + Cfg::KL + ko), lds8(sm + Cfg::QH + qo),
+                                lds8(sm + Cfg::QL + qo), acc);
+                }
+            }
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int j = 16 * jt + 4 * g4 + rr, sidx = 16 * st + l16;
+                const float x = (tk < 10 && sidx >= j) ? acc[rr] : 0.f;
+                uint16_t hi, lo;
+                split(x, hi, lo);
+                sm[Cfg::ATH + j * LT + sidx] = hi;
+                sm[Cfg::ATL + j * LT + sidx] = lo;
+            }
+        }
+        __syncthreads();
+
+        if (owns) {
+            const int ct = wave;
+            f32x4 Gs[NRT];
+#pragma unroll
+            for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) Gs[rt][rr] = G[rt][rr] * sDecay[16 * rt + 4 * g4 + rr];
+            // dV = M(A)^T dY + Kn Gs
+            f32x4 acc[4];
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) acc[jt] = zero4();
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) {
+#pragma unroll
+                for (int ks = jt >> 1; ks < 2; ++ks) {
+                    const int ao = (16 * jt + l16) * LT + 32 * ks + 8 * g4;
+                    const bf16x8 yb = lds8(sm + Cfg::YT + (16 * ct + l16) * LT + 32 * ks + 8 * g4);
+                    acc[jt] = mfma2a(lds8(sm + Cfg::ATH + ao), lds8(sm + Cfg::ATL + ao), yb, acc[jt]);
+                }
+            }
+#pragma unroll
+            for (int ks = 0; ks < KSN; ++ks) {
+                bf16x8 gh, gl;
+                split8(Gs[2 * ks], Gs[2 * ks + 1], gh, gl);
+#pragma unroll
+                for (int jt = 0; jt < 4; ++jt) {
+                    const int ko = (16 * jt + l16) * LQ + 32 * ks + 4 * g4;
+                    const bf16x8 kh = lds4x2(sm + Cfg::KH + ko, sm + Cfg::KH + ko + 16);
+                    const bf16x8 kl = lds4x2(sm + Cfg::KL + ko, sm + Cfg::KL + ko + 16);
+                    acc[jt] = mfma3(kh, kl, gh, gl, acc[jt]);
+                }
+            }
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int j = 16 * jt + 4 * g4 + rr;
+                    if (j < nt) dv[((row0 + j) * s.H + h) * DV + dcol] = f32_to_bf16(acc[jt][rr]);
+                }
+            // G <- Qp^T dY + Gs
+#pragma unroll
+            for (int rt = 0; rt < NRT; ++rt) {
+                f32x4 gacc = Gs[rt];
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const int qo = (16 * rt + l16) * LT + 32 * ks + 8 * g4;
+                    const bf16x8 yb = lds8(sm + Cfg::YT + (16 * ct + l16) * LT + 32 * ks + 8 * g4);
+                    gacc = mfma2a(lds8(sm + Cfg::QTH + qo), lds8(sm + Cfg::QTL + qo), yb, gacc);
+                }
+                G[rt] = gacc;
+            }
+        }
+        __syncthreads();
+    }
+    if (g.deta0 && owns) {
+#pragma unroll
+        for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr)
+                g.deta0[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dcol] = G[rt][rr];
+    }
+}
+
+// ============================================================================ B2
+template <int DK, int DV>
+struct B2Cfg {
+    static constexpr int NTN = DK < 64 ? DK : 64;   // key slots per workgroup
+    static constexpr int NNT = DK / NTN;
+    static constexpr int NCW = NTN / 16;            // waves owning 16 key-slot columns
+    static constexpr int NRD = DV / 16;
+    static constexpr int KSD = DV / 32;
+    static constexpr int LD = DV + 8, LT = kC + 8, LS = NTN + 4;
+    static constexpr int DY = 0, V = DY + kC * LD, DYT = V + kC * LD;
+    static constexpr int BH = DYT + DV * LT, BL = BH + kC * LT, BTH = BL + kC * LT, BTL = BTH + kC * LT;
+    static constexpr int QTH = BTL + kC * LT, QTL = QTH + NTN * LT, KTH = QTL + NTN * LT, KTL = KTH + NTN * LT;
+    static constexpr int END16 = KTL + NTN * LT;
+    // fp32 regions (float indices); X and Y alias the B / B^T buffers once those are consumed
+    static constexpr int LAM = (END16 + 7) / 8 * 4, PP = LAM + kC * LS, DECAY = PP + kC * LS;
+    static constexpr int X = BH / 2, Y = X + kC * LS;
+    static constexpr size_t BYTES = (size_t)(DECAY + NTN) * 4;
+    static_assert((size_t)2 * kC * LS * 4 <= (size_t)4 * kC * LT * 2, "X/Y must fit in the B buffers");
+    static_assert(BH % 8 == 0, "alignment");
+};
+
+template <int DK, int DV>
+__global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const float* __restrict__ saved_lam,
+                                                       const float* __restrict__ saved_H, float* __restrict__ dr_part) {
+    using Cfg = B2Cfg<DK, DV>;
+    constexpr int NTN = Cfg::NTN, NCW = Cfg::NCW, NRD = Cfg::NRD, KSD = Cfg::KSD;
+    constexpr int LD = Cfg::LD, LT = Cfg::LT, LS = Cfg::LS;
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    uint16_t* sm = reinterpret_cast<uint16_t*>(smem_raw);
+    float* smf = reinterpret_cast<float*>(smem_raw);
+
+    const uint16_t* q = static_cast<const uint16_t*>(g.q);
+    const uint16_t* k = static_cast<const uint16_t*>(g.k);
+    const uint16_t* v = static_cast<const uint16_t*>(g.v);
+    const uint16_t* a = static_cast<const uint16_t*>(g.a);
+    const uint16_t* p = static_cast<const uint16_t*>(g.p);
+    const uint16_t* r = static_cast<const uint16_t*>(g.r);
+    const uint16_t* dy = static_cast<const uint16_t*>(g.dy);
+    uint16_t* dq = static_cast<uint16_t*>(g.dq);
+    uint16_t* dk = static_cast<uint16_t*>(g.dk);
+    uint16_t* da = static_cast<uint16_t*>(g.da);
+    uint16_t* dp = static_cast<uint16_t*>(g.dp);
+
+    int bh, ntile;
+    xcd_map(blockIdx.x, s.B * s.H, Cfg::NNT, bh, ntile);
+    const int b = bh / s.H, h = bh % s.H;
+    const int n0 = ntile * NTN;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l16 = lane & 15, g4 = lane >> 4;
+    const int T = s.T;
+    const int nchunk = (T + kC - 1) / kC;
+    const size_t nbt = (size_t)s.B * T * s.H;
+    const bool owns = wave < NCW;
+    const int ncl = 16 * wave + l16;            // local key-slot column of this lane
+    const int ncol = n0 + ncl;
+
+    // G^T[d, n] for this wave's 16 key slots, all value channels
+    f32x4 GT[NRD];
+#pragma unroll
+    for (int rd = 0; rd < NRD; ++rd)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+            GT[rd][rr] = (owns && g.detaT) ? g.detaT[((size_t)bh * DK + ncol) * DV + 16 * rd + 4 * g4 + rr] : 0.f;
+
+    // per-slot carries of the reverse recursions, in lanes tid < NTN
+    const bool glane = tid < NTN;
+    const int nl = glane ? tid : 0;
+    const int ng = n0 + nl;
+    float cnext = 0.f, Sg = 0.f;
+    if (glane) {
+        cnext = g.dlamT ? g.dlamT[(size_t)bh * DK + ng] : 0.f;
+        if (g.detaT) {
+            const float* HT = saved_H + (((size_t)bh * (nchunk + 1) + nchunk) * DK + ng) * DV;
+            const float* dT = g.detaT + ((size_t)bh * DK + ng) * DV;
+            for (int d = 0; d < DV; ++d) Sg += dT[d] * HT[d];
+        }
+    }
+    const bool scan_lane = tid < NTN;
+    const int NSCAN = NTN < 64 ? 64 : NTN;
+
+    for (int c = nchunk - 1; c >= 0; --c) {
+        const int t0 = c * kC;
+        const int nt = min(kC, T - t0);
+        const size_t row0 = (size_t)b * T + t0;
+        const float lam_start = saved_lam[((size_t)bh * nchunk + c) * DK + ng];
+
+        load_tile<kC, DV, LD, LT, true, true>(sm + Cfg::DY, sm + Cfg::DYT, dy, row0, s.H, h, DV, 0, nt, tid, kThr);
+        load_tile<kC, DV, LD, 0, true, false>(sm + Cfg::V, nullptr, v, row0, s.H, h, DV, 0, nt, tid, kThr);
+        if (tid < NSCAN) {
+            float lam = saved_lam[((size_t)bh * nchunk + c) * DK + (scan_lane ? n0 + tid : n0)];
+            ScanLds L{};
+            L.qt_hi = sm + Cfg::QTH;
+            L.qt_lo = sm + Cfg::QTL;
+            L.kt_hi = sm + Cfg::KTH;
+            L.kt_lo = sm + Cfg::KTL;
+            L.lam = smf + Cfg::LAM;
+            L.P = smf + Cfg::PP;
+            const int n = scan_lane ? n0 + tid : n0;
+            const float P = scan_chunk<kC, 0, LT, LS, false, false, true, true, true>(
+                a, p, k, q, r, row0, s.H, h, DK, n, scan_lane ? tid : 0, scan_lane, nt, lam, L, false, lane);
+            if (scan_lane) smf[Cfg::DECAY + tid] = P;
+        }
+        __syncthreads();
+
+        // B[s, j] = dY_s . V_j for j <= s (exact bf16 products), kept as B and B^T;
+        // tiles (0,1), (2,3) are the zeros read by the 32-deep K steps.
+        for (int tk = wave; tk < 12; tk += 4) {
+            int st, jt;
+            if (tk < 10) {
+                st = tk >= 6 ? 3 : tk >= 3 ? 2 : tk >= 1 ? 1 : 0;
+                jt = tk - st * (st + 1) / 2;
+            } else {
+                st = tk == 10 ? 0 : 2;
+                jt = st + 1;
+            }
+            f32x4 acc = zero4();
+            if (tk < 10) {
+#pragma unroll
+                for (int ks = 0; ks < KSD; ++ks) {
+                    const bf16x8 ya = lds8(sm + Cfg::DY + (16 * st + l16) * LD + 32 * ks + 8 * g4);
+                    const bf16x8 vb = lds8(sm + Cfg::V + (16 * jt + l16) * LD + 32 * ks + 8 * g4);
+                    acc = mfma_bf16(ya, vb, acc);
+                }
+            }
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int si = 16 * st + 4 * g4 + rr, j = 16 * jt + l16;
+                const float x = (tk < 10 && j <= si) ? acc[rr] : 0.f;
+                uint16_t hi, lo;
+                split(x, hi, lo);
+                sm[Cfg::BH + si * LT + j] = hi;
+                sm[Cfg::BL + si * LT + j] = lo;
+                sm[Cfg::BTH + j * LT + si] = hi;
+                sm[Cfg::BTL + j * LT + si] = lo;
+            }
+        }
+        __syncthreads();
+
+        f32x4 accX[4], accY[4];
+        if (owns) {
+            // X = dY H0^T + M(B) Kn
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) accX[mt] = zero4();
+            const float* H0 = saved_H + (((size_t)bh * (nchunk + 1) + c) * DK + ncol) * DV;
+#pragma unroll
+            for (int ks = 0; ks < KSD; ++ks) {
+                const float4 h0a = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4);
+                const float4 h0b = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4 + 4);
+                bf16x8 hh, hl;
+                split8(f32x4{h0a.x, h0a.y, h0a.z, h0a.w}, f32x4{h0b.x, h0b.y, h0b.z, h0b.w}, hh, hl);
+#pragma unroll
+                for (int mt = 0; mt < 4; ++mt) {
+                    const bf16x8 ya = lds8(sm + Cfg::DY + (16 * mt + l16) * LD + 32 * ks + 8 * g4);
+                    accX[mt] = mfma2b(ya, hh, hl, accX[mt]);
+                }
+            }
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt) {
+#pragma unroll
+                for (int ks = 0; ks <= (mt >> 1); ++ks) {
+                    const int bo = (16 * mt + l16) * LT + 32 * ks + 8 * g4;
+                    const int ko = ncl * LT + 32 * ks + 8 * g4;
+                    accX[mt] = mfma3(lds8(sm + Cfg::BH + bo), lds8(sm + Cfg::BL + bo), lds8(sm + Cfg::KTH + ko),
+                                     lds8(sm + Cfg::KTL + ko), accX[mt]);
+                }
+            }
+            // Y = M(B)^T Qp + V Gs^T
+            const float Pc = smf[Cfg::DECAY + ncl];
+            f32x4 Gs[NRD];
+#pragma unroll
+            for (int rd = 0; rd < NRD; ++rd)
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) Gs[rd][rr] = GT[rd][rr] * Pc;
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) accY[jt] = zero4();
+#pragma unroll
+            for (int jt = 0; jt < 4; ++jt) {
+#pragma unroll
+                for (int ks = jt >> 1; ks < 2; ++ks) {
+                    const int bo = (16 * jt + l16) * LT + 32 * ks + 8 * g4;
+                    const int qo = ncl * LT + 32 * ks + 8 * g4;
+                    accY[jt] = mfma3(lds8(sm + Cfg::BTH + bo), lds8(sm + Cfg::BTL + bo), lds8(sm + Cfg::QTH + qo),
+                                     lds8(sm + Cfg::QTL + qo), accY[jt]);
+                }
+            }
+#pragma unroll
+            for (int ks = 0; ks < KSD; ++ks) {
+                bf16x8 gh, gl;
+                split8(Gs[2 * ks], Gs[2 * ks + 1], gh, gl);
+#pragma unroll
+                for (int jt = 0; jt < 4; ++jt) {
+                    const int vo = (16 * jt + l16) * LD + 32 * ks + 4 * g4;
+                    accY[jt] = mfma2b(lds4x2(sm + Cfg::V + vo, sm + Cfg::V + vo + 16), gh, gl, accY[jt]);
+                }
+            }
+            // G^T <- dY^T Qp + Gs^T
+#pragma unroll
+            for (int rd = 0; rd < NRD; ++rd) {
+                f32x4 gacc = Gs[rd];
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks) {
+                    const bf16x8 ya = lds8(sm + Cfg::DYT + (16 * rd + l16) * LT + 32 * ks + 8 * g4);
+                    const int qo = ncl * LT + 32 * ks + 8 * g4;
+                    gacc = mfma2b(ya, lds8(sm + Cfg::QTH + qo), lds8(sm + Cfg::QTL + qo), gacc);
+                }
+                GT[rd] = gacc;
+            }
+        }
+        __syncthreads();  // B buffers are dead: X and Y take their place
+        if (owns) {
+#pragma unroll
+            for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int t = 16 * mt + 4 * g4 + rr;
+                    smf[Cfg::X + t * LS + ncl] = accX[mt][rr];
+                    smf[Cfg::Y + t * LS + ncl] = accY[mt][rr];
+                }
+        }
+        __syncthreads();
+
+        // reverse walk over the chunk's tokens, one key slot per lane
+        if (glane) {
+            uint16_t raw[2][5][8];
+            auto load8 = [&](int buf, int tb) {  // tokens tb-7 .. tb
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int tc = max(min(tb - j, nt - 1), 0);
+                    const size_t rowi = (row0 + tc) * s.H + h;
+                    const size_t o = rowi * DK + ng;
+                    raw[buf][0][j] = a[o];
+                    raw[buf][1][j] = p[o];
+                    raw[buf][2][j] = k[o];
+                    raw[buf][3][j] = q[o];
+                    raw[buf][4][j] = r[rowi];
+                }
+            };
+            const int tlast = kC - 1;
+            load8(0, tlast);
+#pragma unroll
+            for (int bt = 0; bt < kC / 8; ++bt) {
+                const int cur = bt & 1;
+                if (bt + 1 < kC / 8) load8(cur ^ 1, tlast - 8 * (bt + 1));
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int t = tlast - 8 * bt - j;
+                    if (t < nt) {
+                        const float av = bf16_to_f32(raw[cur][0][j]), pv = bf16_to_f32(raw[cur][1][j]);
+                        const float kv = bf16_to_f32(raw[cur][2][j]), qv = bf16_to_f32(raw[cur][3][j]);
+                        const float rv = bf16_to_f32(raw[cur][4][j]);
+                        const float lam_t = smf[Cfg::LAM + t * LS + nl];
+                        const float lam_p = t > 0 ? smf[Cfg::LAM + (t - 1) * LS + nl] : lam_start;
+                        const float Pt = smf[Cfg::PP + t * LS + nl];
+                        const float Xv = smf[Cfg::X + t * LS + nl], Yv = smf[Cfg::Y + t * LS + nl];
+                        const float den = fmaf(pv, lam_p, av * av);
+                        const float rr3 = fast_rcp(den * lam_t * av);   // one reciprocal for three
+                        const float rho = lam_t * av * rr3;
+                        const float ilam = den * av * rr3;
+                        const float ia = den * lam_t * rr3;
+                        const float iPt = fast_rcp(Pt);
+                        const float dqt = Pt * Xv;
+                        const float dkh = Yv * iPt;
+                        const float kh = rv * kv;
+                        Sg += qv * ilam * dqt - kh * dkh;                      // adjoint of log F_t
+                        const float gl = cnext - qv * dqt * ilam * ilam;       // adjoint of lam_t
+                        const float drho = fmaf(gl, lam_p, Sg * den);
+                        const float rho2 = rho * rho;
+                        const size_t o = ((row0 + t) * s.H + h) * DK + ng;
+                        dq[o] = f32_to_bf16(dqt * ilam);
+                        dk[o] = f32_to_bf16(rv * dkh + 2.f * kv * rv * gl);
+                        da[o] = f32_to_bf16(Sg * ia - 2.f * av * rho2 * drho);
+                        dp[o] = f32_to_bf16(-lam_p * rho2 * drho);
+                        smf[Cfg::X + t * LS + nl] = kv * dkh + kv * kv * gl;   // term of dr
+                        cnext = av * av * rho2 * gl - pv * rho * Sg;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        // partial dr over this workgroup's key slots: 4 threads per token
+        {
+            const int t = tid >> 2, qd = tid & 3;
+            float acc = 0.f;
+            if (t < kC) {
+#pragma unroll 4
+                for (int i = qd; i < NTN; i += 4) acc += smf[Cfg::X + t * LS + i];
+            }
+            acc += __shfl_xor(acc, 1, 64);
+            acc += __shfl_xor(acc, 2, 64);
+            if (t < nt && qd == 0) dr_part[(size_t)ntile * nbt + (row0 + t) * s.H + h] = acc;
+        }
+        __syncthreads();
+    }
+    if (glane && g.dlam0) g.dlam0[(size_t)bh * DK + ng] = cnext;
+}
+
+// dr = sum of the per-key-tile partials, stored in the input dtype
+__global__ void dr_combine_kernel(const float* __restrict__ part, int ntile, size_t n, uint16_t* __restrict__ dr) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    float acc = 0.f;
+    for (int t = 0; t < ntile; ++t) acc += part[(size_t)t * n + i];
+    dr[i] = f32_to_bf16(acc);
+}
+
+template <int DK, int DV>
+hipError_t launch_bwd(const Shape& s, const BwdArgs& a, const float* saved_lam, const float* saved_H, float* dr_part,
+                      hipStream_t st) {
+    using C1 = B1Cfg<DK, DV>;
+    using C2 = B2Cfg<DK, DV>;
+    auto k1 = bwd_b1_kernel<DK, DV>;
+    auto k2 = bwd_b2_kernel<DK, DV>;
+    static const hipError_t e1 = hipFuncSetAttribute(reinterpret_cast<const void*>(k1),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)C1::BYTES);
+    static const hipError_t e2 = hipFuncSetAttribute(reinterpret_cast<const void*>(k2),
+                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)C2::BYTES);
+    if (e1 != hipSuccess) return e1;
+    if (e2 != hipSuccess) return e2;
+    hipLaunchKernelGGL(k1, dim3(s.B * s.H * C1::NTILE), dim3(kThr), C1::BYTES, st, s, a, saved_lam);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k2, dim3(s.B * s.H * C2::NNT), dim3(kThr), C2::BYTES, st, s, a, saved_lam, saved_H, dr_part);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t n = (size_t)s.B * s.T * s.H;
+    if (n > 0) {
+        hipLaunchKernelGGL(dr_combine_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, dr_part, C2::NNT, n,
+                           static_cast<uint16_t*>(a.dr));
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+}  // namespace
+
+bool chunked_bwd_supported(const Shape& s) { return s.bf16 && s.dk >= 32 && s.dv >= 32; }
+
+size_t chunked_bwd_workspace(const Shape& s) {
+    const int ntn = s.dk < 64 ? s.dk : 64;
+    return (size_t)(s.dk / ntn) * s.B * s.T * s.H * sizeof(float);
+}
+
+hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st) {
+    const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
+    const float* saved_lam = static_cast<const float*>(saved);
+    const float* saved_H = saved_lam + (size_t)s.B * s.H * nchunk * s.dk;
+    float* dr_part = static_cast<float*>(ws);
+#define KLA_BWD_CASE(DK_, DV_) \
+    if (s.dk == DK_ && s.dv == DV_) return launch_bwd<DK_, DV_>(s, a, saved_lam, saved_H, dr_part, st);
+#define KLA_BWD_ROW(DK_) KLA_BWD_CASE(DK_, 32) KLA_BWD_CASE(DK_, 64) KLA_BWD_CASE(DK_, 128)
+    KLA_BWD_ROW(32) KLA_BWD_ROW(64) KLA_BWD_ROW(128)
+#undef KLA_BWD_ROW
+#undef KLA_BWD_CASE
+    return hipErrorInvalidValue;
+}
+
+}  // namespace kla

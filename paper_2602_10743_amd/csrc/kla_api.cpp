@@ -75,13 +75,22 @@ size_t kla_forward_workspace(const kla_desc* desc) {
 
 size_t kla_saved_bytes(const kla_desc* desc) {
     if (check_desc(desc) != KLA_OK) return 0;
-    return 0;
+    const kla::Shape s = shape_of(desc);
+    return kla::chunked_supported(s) ? kla::chunked_saved_bytes(s) : 0;
 }
 
 size_t kla_backward_workspace(const kla_desc* desc, int with_saved) {
-    (void)with_saved;
     if (check_desc(desc) != KLA_OK) return 0;
-    return kAlign + round_up(kla::backward_recurrent_workspace(shape_of(desc)));
+    const kla::Shape s = shape_of(desc);
+    if (kla::chunked_bwd_supported(s)) {
+        size_t bytes = kAlign + round_up(kla::chunked_bwd_workspace(s));
+        if (!with_saved) {  // the context is recomputed: saved states plus a scratch output
+            const size_t elt = s.bf16 ? 2 : 4;
+            bytes += round_up(kla::chunked_saved_bytes(s)) + round_up((size_t)s.B * s.T * s.H * s.dv * elt);
+        }
+        return bytes;
+    }
+    return kAlign + round_up(kla::backward_recurrent_workspace(s));
 }
 
 kla_status kla_forward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
@@ -96,14 +105,15 @@ kla_status kla_forward(const kla_desc* desc, const void* q, const void* k, const
                      (void*)lamT, (void*)etaT, saved, ws))
         return KLA_ERR_ALIGN;
     if (!ws || ws_bytes < kla_forward_workspace(desc)) return KLA_ERR_WORKSPACE;
-    (void)saved;
     const kla::Shape s = shape_of(desc);
     if (check_mode()) {
         st = validate(s, s.T, q, k, v, abar, pbar, r, lam0, eta0, ws, stream);
         if (st != KLA_OK) return st;
     }
     kla::FwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, y, yvar, lamT, etaT};
-    return kla::launch_forward_recurrent(s, a, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+    hipError_t e = kla::chunked_supported(s) ? kla::launch_forward_chunked(s, a, saved, stream)
+                                             : kla::launch_forward_recurrent(s, a, stream);
+    return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 
 kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
@@ -128,8 +138,22 @@ kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, cons
     }
     kla::BwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT, detaT, dq, dk, dv, dabar, dpbar, dr,
                    dlam0, deta0};
-    void* work = static_cast<char*>(ws) + kAlign;
-    return kla::launch_backward_recurrent(s, a, work, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+    char* work = static_cast<char*>(ws) + kAlign;
+    hipError_t e;
+    if (kla::chunked_bwd_supported(s)) {
+        if (!saved) {
+            char* ctx = work + round_up(kla::chunked_bwd_workspace(s));
+            void* yscratch = ctx + round_up(kla::chunked_saved_bytes(s));
+            kla::FwdArgs f{q, k, v, abar, pbar, r, lam0, eta0, yscratch, nullptr, nullptr, nullptr};
+            e = kla::launch_forward_chunked(s, f, ctx, stream);
+            if (e != hipSuccess) return KLA_ERR_HIP;
+            saved = ctx;
+        }
+        e = kla::launch_backward_chunked(s, a, saved, work, stream);
+    } else {
+        e = kla::launch_backward_recurrent(s, a, work, stream);
+    }
+    return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 
 kla_status kla_decode_step(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,

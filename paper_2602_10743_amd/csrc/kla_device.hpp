@@ -17,12 +17,19 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t u) {
     return __uint_as_float(static_cast<uint32_t>(u) << 16);
 }
 
-// fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2_t;
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2_t;
+
+// Two fp32 -> packed bf16 pair (x0 in the low half), round to nearest even;
+// one v_cvt_pk_bf16_f32 on gfx950.
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float x0, float x1) {
+    const f32x2_t v = {x0, x1};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// fp32 -> bf16, round to nearest even.
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
-    u += 0x7fffu + ((u >> 16) & 1u);
-    return static_cast<uint16_t>(u >> 16);
+    return static_cast<uint16_t>(cvt_pk_bf16(f, 0.f));
 }
 
 __device__ __forceinline__ float ld(const float* p, size_t i) { return p[i]; }

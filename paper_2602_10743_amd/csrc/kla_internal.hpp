@@ -40,4 +40,12 @@ size_t backward_recurrent_workspace(const Shape& s);
 hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, void* ws, hipStream_t st);
 hipError_t launch_decode_step(const Shape& s, const DecodeArgs& a, hipStream_t st);
 
+// Chunked MFMA path (bf16 storage, dk >= 32).
+bool chunked_supported(const Shape& s);
+size_t chunked_saved_bytes(const Shape& s);
+hipError_t launch_forward_chunked(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st);
+bool chunked_bwd_supported(const Shape& s);
+size_t chunked_bwd_workspace(const Shape& s);
+hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st);
+
 }  // namespace kla

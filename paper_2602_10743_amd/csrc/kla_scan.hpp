@@ -1,0 +1,156 @@
+// Per-chunk precision walk of one key slot, shared by the chunked kernels.
+//
+// For key slot n and the tokens t < nt of one chunk, starting from the carried
+// precision lam (Theorem 1, gate view):
+//   den_t = abar_t^2 + pbar_t lam_{t-1}  (= 1 / rho_t)
+//   lam_t = rho_t lam_{t-1} + k_t^2 r_t
+//   F_t   = abar_t rho_t                  (forget gate, Theorem 2)
+//   P_t   = prod_{s<=t} F_s               (inside the chunk)
+//   Qp_t  = (q_t / lam_t) P_t,   Kn_t = (r_t k_t) / P_t
+// With num = lam_{t-1} + k^2 r den (so lam_t = num / den), one reciprocal of
+// den * num * abar yields rho_t, 1/lam_t and 1/abar.
+//
+// Qp and Kn are stored as split-bf16 (hi, lo) pairs in any of four LDS layouts
+// selected at compile time: [t][n] (row stride LQ) and [n][t] (row stride LT,
+// written 8 tokens per 16-byte store).  Optionally lam_t and P_t are stored in
+// fp32 [t][n] (row stride LS).  Tokens t >= nt get zeros.  The inputs of the
+// next 8 tokens are loaded while the current 8 are processed; loads are
+// unconditional (clamped to the last valid token).
+#pragma once
+#include "kla_mfma.hpp"
+
+namespace kla {
+
+struct ScanLds {
+    uint16_t *qn_hi, *qn_lo;   // Qp [t][n]
+    uint16_t *kn_hi, *kn_lo;   // Kn [t][n]
+    uint16_t *qt_hi, *qt_lo;   // Qp^T [n][t]
+    uint16_t *kt_hi, *kt_lo;   // Kn^T [n][t]
+    float *lam, *P;            // fp32 [t][n]
+    float* yv;                 // per-token partial sums of q^2 / lam over the wave, [t]
+};
+
+template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST>
+__device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ a, const uint16_t* __restrict__ p,
+                                            const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
+                                            const uint16_t* __restrict__ r, size_t row0, int H, int h, int DK,
+                                            int n, int nl, bool active, int nt, float& lam, const ScanLds& L,
+                                            bool want_yv, int lane) {
+    float P = 1.f, iP = 1.f;
+    uint16_t raw[2][5][8];
+    auto load8 = [&](int buf, int t8) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int tc = min(t8 + j, nt - 1);
+            const size_t rowi = (row0 + tc) * H + h;
+            const size_t o = rowi * DK + n;
+            raw[buf][0][j] = a[o];
+            raw[buf][1][j] = p[o];
+            raw[buf][2][j] = k[o];
+            raw[buf][3][j] = q[o];
+            raw[buf][4][j] = r[rowi];
+        }
+    };
+    load8(0, 0);
+#pragma unroll
+    for (int bt = 0; bt < C / 8; ++bt) {
+        const int cur = bt & 1;
+        if (bt + 1 < C / 8) load8(cur ^ 1, 8 * (bt + 1));
+        uint32_t hp[8], lp[8];  // per token: packed (Qp, Kn) hi and lo halves
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int t = 8 * bt + j;
+            const float av = bf16_to_f32(raw[cur][0][j]), pv = bf16_to_f32(raw[cur][1][j]);
+            const float kv = bf16_to_f32(raw[cur][2][j]), qv = bf16_to_f32(raw[cur][3][j]);
+            const float rv = bf16_to_f32(raw[cur][4][j]);
+            float qp = 0.f, kn = 0.f, w = 0.f;
+            if (t < nt) {
+                const float den = fmaf(pv, lam, av * av);
+                const float num = fmaf(kv * kv * rv, den, lam);
+                const float rr = fast_rcp(den * num * av);
+                const float rho = num * av * rr;
+                const float ilam = den * den * av * rr;
+                const float ia = den * num * rr;
+                lam = num * rho;
+                P *= av * rho;
+                iP *= den * ia;
+                const float qt = qv * ilam;
+                qp = qt * P;
+                kn = rv * kv * iP;
+                w = active ? qv * qt : 0.f;
+            }
+            split2(qp, kn, hp[j], lp[j]);
+            if (active) {
+                if constexpr (QN) {
+                    L.qn_hi[t * LQ + nl] = static_cast<uint16_t>(hp[j]);
+                    L.qn_lo[t * LQ + nl] = static_cast<uint16_t>(lp[j]);
+                }
+                if constexpr (KN) {
+                    L.kn_hi[t * LQ + nl] = static_cast<uint16_t>(hp[j] >> 16);
+                    L.kn_lo[t * LQ + nl] = static_cast<uint16_t>(lp[j] >> 16);
+                }
+                if constexpr (ST) {
+                    L.lam[t * LS + nl] = lam;
+                    L.P[t * LS + nl] = P;
+                }
+            }
+            if (want_yv) {
+#pragma unroll
+                for (int off = 32; off > 0; off >>= 1) w += __shfl_xor(w, off, 64);
+                if (lane == 0) L.yv[t] = w;
+            }
+        }
+        if (active) {
+            if constexpr (QT) {
+                uint4 h4, l4;
+                h4.x = (hp[0] & 0xffffu) | (hp[1] << 16);
+                h4.y = (hp[2] & 0xffffu) | (hp[3] << 16);
+                h4.z = (hp[4] & 0xffffu) | (hp[5] << 16);
+                h4.w = (hp[6] & 0xffffu) | (hp[7] << 16);
+                l4.x = (lp[0] & 0xffffu) | (lp[1] << 16);
+                l4.y = (lp[2] & 0xffffu) | (lp[3] << 16);
+                l4.z = (lp[4] & 0xffffu) | (lp[5] << 16);
+                l4.w = (lp[6] & 0xffffu) | (lp[7] << 16);
+                *reinterpret_cast<uint4*>(L.qt_hi + nl * LT + 8 * bt) = h4;
+                *reinterpret_cast<uint4*>(L.qt_lo + nl * LT + 8 * bt) = l4;
+            }
+            if constexpr (KT) {
+                uint4 h4, l4;
+                h4.x = (hp[0] >> 16) | (hp[1] & 0xffff0000u);
+                h4.y = (hp[2] >> 16) | (hp[3] & 0xffff0000u);
+                h4.z = (hp[4] >> 16) | (hp[5] & 0xffff0000u);
+                h4.w = (hp[6] >> 16) | (hp[7] & 0xffff0000u);
+                l4.x = (lp[0] >> 16) | (lp[1] & 0xffff0000u);
+                l4.y = (lp[2] >> 16) | (lp[3] & 0xffff0000u);
+                l4.z = (lp[4] >> 16) | (lp[5] & 0xffff0000u);
+                l4.w = (lp[6] >> 16) | (lp[7] & 0xffff0000u);
+                *reinterpret_cast<uint4*>(L.kt_hi + nl * LT + 8 * bt) = h4;
+                *reinterpret_cast<uint4*>(L.kt_lo + nl * LT + 8 * bt) = l4;
+            }
+        }
+    }
+    return P;
+}
+
+// Chunk tile of a per-token bf16 tensor (row length rowlen, columns c0 .. c0+W)
+// into LDS, row-major [t][c] (stride L) and/or transposed [c][t] (stride LT);
+// rows past the sequence end are zero.
+template <int C, int W, int L, int LT, bool ROWS, bool COLS>
+__device__ __forceinline__ void load_tile(uint16_t* rows, uint16_t* cols, const uint16_t* __restrict__ src,
+                                          size_t row0, int H, int h, int rowlen, int c0, int nt, int tid,
+                                          int nthreads) {
+    for (int idx = tid; idx < C * (W / 8); idx += nthreads) {
+        const int t = idx / (W / 8), c8 = idx % (W / 8);
+        const int tc = min(t, nt - 1);
+        uint4 x = *reinterpret_cast<const uint4*>(src + ((row0 + tc) * H + h) * rowlen + c0 + 8 * c8);
+        if (t >= nt) x = uint4{0u, 0u, 0u, 0u};
+        if constexpr (ROWS) *reinterpret_cast<uint4*>(rows + t * L + 8 * c8) = x;
+        if constexpr (COLS) {
+            const uint16_t* e = reinterpret_cast<const uint16_t*>(&x);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) cols[(8 * c8 + i) * LT + t] = e[i];
+        }
+    }
+}
+
+}  // namespace kla
