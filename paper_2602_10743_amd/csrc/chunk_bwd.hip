@@ -155,11 +155,11 @@ __global__ __launch_bounds__(kThr) void bwd_b1_kernel(Shape s, BwdArgs g, const 
 
         if (owns) {
             const int ct = wave;
-            f32x4 Gs[NRT];
+            // G <- diag(P_C) G in place (Gs of the notation above)
 #pragma unroll
             for (int rt = 0; rt < NRT; ++rt)
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr) Gs[rt][rr] = G[rt][rr] * sDecay[16 * rt + 4 * g4 + rr];
+                for (int rr = 0; rr < 4; ++rr) G[rt][rr] *= sDecay[16 * rt + 4 * g4 + rr];
             // dV = M(A)^T dY + Kn Gs
             f32x4 acc[4];
 #pragma unroll
@@ -176,7 +176,7 @@ __global__ __launch_bounds__(kThr) void bwd_b1_kernel(Shape s, BwdArgs g, const 
 #pragma unroll
             for (int ks = 0; ks < KSN; ++ks) {
                 bf16x8 gh, gl;
-                split8(Gs[2 * ks], Gs[2 * ks + 1], gh, gl);
+                split8(G[2 * ks], G[2 * ks + 1], gh, gl);
 #pragma unroll
                 for (int jt = 0; jt < 4; ++jt) {
                     const int ko = (16 * jt + l16) * LQ + 32 * ks + 4 * g4;
@@ -195,7 +195,7 @@ __global__ __launch_bounds__(kThr) void bwd_b1_kernel(Shape s, BwdArgs g, const 
             // G <- Qp^T dY + Gs
 #pragma unroll
             for (int rt = 0; rt < NRT; ++rt) {
-                f32x4 gacc = Gs[rt];
+                f32x4 gacc = G[rt];
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
                     const int qo = (16 * rt + l16) * LT + 32 * ks + 8 * g4;
@@ -384,11 +384,10 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
             }
             // Y = M(B)^T Qp + V Gs^T
             const float Pc = smf[Cfg::DECAY + ncl];
-            f32x4 Gs[NRD];
 #pragma unroll
             for (int rd = 0; rd < NRD; ++rd)
 #pragma unroll
-                for (int rr = 0; rr < 4; ++rr) Gs[rd][rr] = GT[rd][rr] * Pc;
+                for (int rr = 0; rr < 4; ++rr) GT[rd][rr] *= Pc;   // Gs^T in place
 #pragma unroll
             for (int jt = 0; jt < 4; ++jt) accY[jt] = zero4();
 #pragma unroll
@@ -404,7 +403,7 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
 #pragma unroll
             for (int ks = 0; ks < KSD; ++ks) {
                 bf16x8 gh, gl;
-                split8(Gs[2 * ks], Gs[2 * ks + 1], gh, gl);
+                split8(GT[2 * ks], GT[2 * ks + 1], gh, gl);
 #pragma unroll
                 for (int jt = 0; jt < 4; ++jt) {
                     const int vo = (16 * jt + l16) * LD + 32 * ks + 4 * g4;
@@ -414,7 +413,7 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
             // G^T <- dY^T Qp + Gs^T
 #pragma unroll
             for (int rd = 0; rd < NRD; ++rd) {
-                f32x4 gacc = Gs[rd];
+                f32x4 gacc = GT[rd];
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
                     const bf16x8 ya = lds8(sm + Cfg::DYT + (16 * rd + l16) * LT + 32 * ks + 8 * g4);
@@ -439,35 +438,35 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
 
         // reverse walk over the chunk's tokens, one key slot per lane
         if (glane) {
-            uint16_t raw[2][5][8];
-            auto load8 = [&](int buf, int tb) {  // tokens tb-7 .. tb
+            struct GBatch {
+                uint16_t v[5][4];
+            };
+            auto loadb = [&](GBatch& bb, int tb) {  // tokens tb, tb-1, tb-2, tb-3
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
+                for (int j = 0; j < 4; ++j) {
                     const int tc = max(min(tb - j, nt - 1), 0);
                     const size_t rowi = (row0 + tc) * s.H + h;
                     const size_t o = rowi * DK + ng;
-                    raw[buf][0][j] = a[o];
-                    raw[buf][1][j] = p[o];
-                    raw[buf][2][j] = k[o];
-                    raw[buf][3][j] = q[o];
-                    raw[buf][4][j] = r[rowi];
+                    bb.v[0][j] = a[o];
+                    bb.v[1][j] = p[o];
+                    bb.v[2][j] = k[o];
+                    bb.v[3][j] = q[o];
+                    bb.v[4][j] = r[rowi];
                 }
             };
-            const int tlast = kC - 1;
-            load8(0, tlast);
+            auto stepb = [&](const GBatch& bb, int tb) {
 #pragma unroll
-            for (int bt = 0; bt < kC / 8; ++bt) {
-                const int cur = bt & 1;
-                if (bt + 1 < kC / 8) load8(cur ^ 1, tlast - 8 * (bt + 1));
-#pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int t = tlast - 8 * bt - j;
+                for (int j = 0; j < 4; ++j) {
+                    const int t = tb - j;
+                    const uint16_t raw0 = bb.v[0][j], raw1 = bb.v[1][j], raw2 = bb.v[2][j], raw3 = bb.v[3][j],
+                                   raw4 = bb.v[4][j];
                     if (t < nt) {
-                        const float av = bf16_to_f32(raw[cur][0][j]), pv = bf16_to_f32(raw[cur][1][j]);
-                        const float kv = bf16_to_f32(raw[cur][2][j]), qv = bf16_to_f32(raw[cur][3][j]);
-                        const float rv = bf16_to_f32(raw[cur][4][j]);
+                        const float av = bf16_to_f32(raw0), pv = bf16_to_f32(raw1);
+                        const float kv = bf16_to_f32(raw2), qv = bf16_to_f32(raw3);
+                        const float rv = bf16_to_f32(raw4);
                         const float lam_t = smf[Cfg::LAM + t * LS + nl];
-                        const float lam_p = t > 0 ? smf[Cfg::LAM + (t - 1) * LS + nl] : lam_start;
+                        const float lam_pl = smf[Cfg::LAM + max(t - 1, 0) * LS + nl];
+                        const float lam_p = t > 0 ? lam_pl : lam_start;
                         const float Pt = smf[Cfg::PP + t * LS + nl];
                         const float Xv = smf[Cfg::X + t * LS + nl], Yv = smf[Cfg::Y + t * LS + nl];
                         const float den = fmaf(pv, lam_p, av * av);
@@ -492,6 +491,15 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
                         cnext = av * av * rho2 * gl - pv * rho * Sg;
                     }
                 }
+            };
+            GBatch b0, b1;
+            loadb(b0, kC - 1);
+#pragma unroll 1
+            for (int tb = kC - 1; tb >= 0; tb -= 8) {
+                loadb(b1, tb - 4);
+                stepb(b0, tb);
+                if (tb - 8 >= 0) loadb(b0, tb - 8);
+                stepb(b1, tb - 4);
             }
         }
         __syncthreads();

@@ -14,7 +14,7 @@
 // selected at compile time: [t][n] (row stride LQ) and [n][t] (row stride LT,
 // written 8 tokens per 16-byte store).  Optionally lam_t and P_t are stored in
 // fp32 [t][n] (row stride LS).  Tokens t >= nt get zeros.  The inputs of the
-// next 8 tokens are loaded while the current 8 are processed; loads are
+// next 4 tokens are loaded while the current 4 are processed; loads are
 // unconditional (clamped to the last valid token).
 #pragma once
 #include "kla_mfma.hpp"
@@ -31,38 +31,43 @@ struct ScanLds {
 };
 
 template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST>
-__device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ a, const uint16_t* __restrict__ p,
-                                            const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
-                                            const uint16_t* __restrict__ r, size_t row0, int H, int h, int DK,
-                                            int n, int nl, bool active, int nt, float& lam, const ScanLds& L,
-                                            bool want_yv, int lane) {
+struct ChunkScan {
+    // raw bf16 inputs of 4 tokens: abar, pbar, k, q, r
+    struct Batch {
+        uint16_t v[5][4];
+    };
+
+    const uint16_t *a, *p, *k, *q, *r;
+    size_t row0;
+    int H, h, DK, n, nl, nt, lane;
+    bool active, want_yv;
+    ScanLds L;
     float P = 1.f, iP = 1.f;
-    uint16_t raw[2][5][8];
-    auto load8 = [&](int buf, int t8) {
+    uint32_t hp[8], lp[8];  // the current 8 tokens: packed (Qp, Kn) hi and lo halves
+
+    __device__ __forceinline__ void load(Batch& b, int t4) const {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int tc = min(t8 + j, nt - 1);
+        for (int j = 0; j < 4; ++j) {
+            const int tc = min(t4 + j, nt - 1);
             const size_t rowi = (row0 + tc) * H + h;
             const size_t o = rowi * DK + n;
-            raw[buf][0][j] = a[o];
-            raw[buf][1][j] = p[o];
-            raw[buf][2][j] = k[o];
-            raw[buf][3][j] = q[o];
-            raw[buf][4][j] = r[rowi];
+            b.v[0][j] = a[o];
+            b.v[1][j] = p[o];
+            b.v[2][j] = k[o];
+            b.v[3][j] = q[o];
+            b.v[4][j] = r[rowi];
         }
-    };
-    load8(0, 0);
+    }
+
+    // tokens t4 .. t4+3 into slots OFF .. OFF+3 of the current group of 8
+    template <int OFF>
+    __device__ __forceinline__ void step(const Batch& b, int t4, float& lam) {
 #pragma unroll
-    for (int bt = 0; bt < C / 8; ++bt) {
-        const int cur = bt & 1;
-        if (bt + 1 < C / 8) load8(cur ^ 1, 8 * (bt + 1));
-        uint32_t hp[8], lp[8];  // per token: packed (Qp, Kn) hi and lo halves
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int t = 8 * bt + j;
-            const float av = bf16_to_f32(raw[cur][0][j]), pv = bf16_to_f32(raw[cur][1][j]);
-            const float kv = bf16_to_f32(raw[cur][2][j]), qv = bf16_to_f32(raw[cur][3][j]);
-            const float rv = bf16_to_f32(raw[cur][4][j]);
+        for (int j = 0; j < 4; ++j) {
+            const int t = t4 + j;
+            const float av = bf16_to_f32(b.v[0][j]), pv = bf16_to_f32(b.v[1][j]);
+            const float kv = bf16_to_f32(b.v[2][j]), qv = bf16_to_f32(b.v[3][j]);
+            const float rv = bf16_to_f32(b.v[4][j]);
             float qp = 0.f, kn = 0.f, w = 0.f;
             if (t < nt) {
                 const float den = fmaf(pv, lam, av * av);
@@ -79,15 +84,15 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ a, cons
                 kn = rv * kv * iP;
                 w = active ? qv * qt : 0.f;
             }
-            split2(qp, kn, hp[j], lp[j]);
+            split2(qp, kn, hp[OFF + j], lp[OFF + j]);
             if (active) {
                 if constexpr (QN) {
-                    L.qn_hi[t * LQ + nl] = static_cast<uint16_t>(hp[j]);
-                    L.qn_lo[t * LQ + nl] = static_cast<uint16_t>(lp[j]);
+                    L.qn_hi[t * LQ + nl] = static_cast<uint16_t>(hp[OFF + j]);
+                    L.qn_lo[t * LQ + nl] = static_cast<uint16_t>(lp[OFF + j]);
                 }
                 if constexpr (KN) {
-                    L.kn_hi[t * LQ + nl] = static_cast<uint16_t>(hp[j] >> 16);
-                    L.kn_lo[t * LQ + nl] = static_cast<uint16_t>(lp[j] >> 16);
+                    L.kn_hi[t * LQ + nl] = static_cast<uint16_t>(hp[OFF + j] >> 16);
+                    L.kn_lo[t * LQ + nl] = static_cast<uint16_t>(lp[OFF + j] >> 16);
                 }
                 if constexpr (ST) {
                     L.lam[t * LS + nl] = lam;
@@ -100,36 +105,66 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ a, cons
                 if (lane == 0) L.yv[t] = w;
             }
         }
-        if (active) {
-            if constexpr (QT) {
-                uint4 h4, l4;
-                h4.x = (hp[0] & 0xffffu) | (hp[1] << 16);
-                h4.y = (hp[2] & 0xffffu) | (hp[3] << 16);
-                h4.z = (hp[4] & 0xffffu) | (hp[5] << 16);
-                h4.w = (hp[6] & 0xffffu) | (hp[7] << 16);
-                l4.x = (lp[0] & 0xffffu) | (lp[1] << 16);
-                l4.y = (lp[2] & 0xffffu) | (lp[3] << 16);
-                l4.z = (lp[4] & 0xffffu) | (lp[5] << 16);
-                l4.w = (lp[6] & 0xffffu) | (lp[7] << 16);
-                *reinterpret_cast<uint4*>(L.qt_hi + nl * LT + 8 * bt) = h4;
-                *reinterpret_cast<uint4*>(L.qt_lo + nl * LT + 8 * bt) = l4;
-            }
-            if constexpr (KT) {
-                uint4 h4, l4;
-                h4.x = (hp[0] >> 16) | (hp[1] & 0xffff0000u);
-                h4.y = (hp[2] >> 16) | (hp[3] & 0xffff0000u);
-                h4.z = (hp[4] >> 16) | (hp[5] & 0xffff0000u);
-                h4.w = (hp[6] >> 16) | (hp[7] & 0xffff0000u);
-                l4.x = (lp[0] >> 16) | (lp[1] & 0xffff0000u);
-                l4.y = (lp[2] >> 16) | (lp[3] & 0xffff0000u);
-                l4.z = (lp[4] >> 16) | (lp[5] & 0xffff0000u);
-                l4.w = (lp[6] >> 16) | (lp[7] & 0xffff0000u);
-                *reinterpret_cast<uint4*>(L.kt_hi + nl * LT + 8 * bt) = h4;
-                *reinterpret_cast<uint4*>(L.kt_lo + nl * LT + 8 * bt) = l4;
-            }
+    }
+
+    // the transposed rows [n][t8 .. t8+7], one 16-byte store each
+    __device__ __forceinline__ void store8(int t8) const {
+        if (!active) return;
+        if constexpr (QT) {
+            uint4 h4, l4;
+            h4.x = (hp[0] & 0xffffu) | (hp[1] << 16);
+            h4.y = (hp[2] & 0xffffu) | (hp[3] << 16);
+            h4.z = (hp[4] & 0xffffu) | (hp[5] << 16);
+            h4.w = (hp[6] & 0xffffu) | (hp[7] << 16);
+            l4.x = (lp[0] & 0xffffu) | (lp[1] << 16);
+            l4.y = (lp[2] & 0xffffu) | (lp[3] << 16);
+            l4.z = (lp[4] & 0xffffu) | (lp[5] << 16);
+            l4.w = (lp[6] & 0xffffu) | (lp[7] << 16);
+            *reinterpret_cast<uint4*>(L.qt_hi + nl * LT + t8) = h4;
+            *reinterpret_cast<uint4*>(L.qt_lo + nl * LT + t8) = l4;
+        }
+        if constexpr (KT) {
+            uint4 h4, l4;
+            h4.x = (hp[0] >> 16) | (hp[1] & 0xffff0000u);
+            h4.y = (hp[2] >> 16) | (hp[3] & 0xffff0000u);
+            h4.z = (hp[4] >> 16) | (hp[5] & 0xffff0000u);
+            h4.w = (hp[6] >> 16) | (hp[7] & 0xffff0000u);
+            l4.x = (lp[0] >> 16) | (lp[1] & 0xffff0000u);
+            l4.y = (lp[2] >> 16) | (lp[3] & 0xffff0000u);
+            l4.z = (lp[4] >> 16) | (lp[5] & 0xffff0000u);
+            l4.w = (lp[6] >> 16) | (lp[7] & 0xffff0000u);
+            *reinterpret_cast<uint4*>(L.kt_hi + nl * LT + t8) = h4;
+            *reinterpret_cast<uint4*>(L.kt_lo + nl * LT + t8) = l4;
         }
     }
-    return P;
+
+    // Walk the chunk from the carried lam; returns P at the chunk end.  The loop
+    // over groups of 8 tokens is a runtime loop (LDS addresses advance with it
+    // instead of being materialised per token); the loads of the next 4 tokens
+    // are in flight while the current 4 are processed.
+    __device__ __forceinline__ float run(float& lam) {
+        Batch b0, b1;
+        load(b0, 0);
+#pragma unroll 1
+        for (int t8 = 0; t8 < C; t8 += 8) {
+            load(b1, t8 + 4);
+            step<0>(b0, t8, lam);
+            if (t8 + 8 < C) load(b0, t8 + 8);
+            step<4>(b1, t8 + 4, lam);
+            store8(t8);
+        }
+        return P;
+    }
+};
+
+template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST>
+__device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ a, const uint16_t* __restrict__ p,
+                                            const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
+                                            const uint16_t* __restrict__ r, size_t row0, int H, int h, int DK,
+                                            int n, int nl, bool active, int nt, float& lam, const ScanLds& L,
+                                            bool want_yv, int lane) {
+    ChunkScan<C, LQ, LT, LS, QN, KN, QT, KT, ST> sc{a, p, k, q, r, row0, H, h, DK, n, nl, nt, lane, active, want_yv, L};
+    return sc.run(lam);
 }
 
 // Chunk tile of a per-token bf16 tensor (row length rowlen, columns c0 .. c0+W)
