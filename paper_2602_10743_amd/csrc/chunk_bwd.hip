@@ -61,6 +61,7 @@ struct B1Cfg {
     static constexpr int END16 = ATL + kC * LT;
     static constexpr int DECAY = (END16 + 7) / 8 * 4;
     static constexpr size_t BYTES = (size_t)(DECAY + DK) * 4;
+    static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
 };
 
 template <int DK, int DV>
@@ -231,9 +232,13 @@ struct B2Cfg {
     static constexpr int END16 = KTL + NTN * LT;
     // fp32 regions (float indices); X and Y alias the B / B^T buffers once those are consumed
     static constexpr int LAM = (END16 + 7) / 8 * 4, PP = LAM + kC * LS, DECAY = PP + kC * LS;
+    // per-quarter affine summaries [4][4][NTN] alias the dY tile, dead by then
+    static constexpr int QS = DY / 2;
     static constexpr int X = BH / 2, Y = X + kC * LS;
     static constexpr size_t BYTES = (size_t)(DECAY + NTN) * 4;
     static_assert((size_t)2 * kC * LS * 4 <= (size_t)4 * kC * LT * 2, "X/Y must fit in the B buffers");
+    static_assert((size_t)16 * NTN * 4 <= (size_t)kC * LD * 2, "quarter summaries must fit in the dY tile");
+    static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
     static_assert(BH % 8 == 0, "alignment");
 };
 
@@ -280,9 +285,9 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
         for (int rr = 0; rr < 4; ++rr)
             GT[rd][rr] = (owns && g.detaT) ? g.detaT[((size_t)bh * DK + ncol) * DV + 16 * rd + 4 * g4 + rr] : 0.f;
 
-    // per-slot carries of the reverse recursions, in lanes tid < NTN
-    const bool glane = tid < NTN;
-    const int nl = glane ? tid : 0;
+    // per-slot carries of the reverse recursions, kept (identically) by lane nl of every wave
+    const bool glane = lane < NTN;
+    const int nl = glane ? lane : 0;
     const int ng = n0 + nl;
     float cnext = 0.f, Sg = 0.f;
     if (glane) {
@@ -314,7 +319,7 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
             L.lam = smf + Cfg::LAM;
             L.P = smf + Cfg::PP;
             const int n = scan_lane ? n0 + tid : n0;
-            const float P = scan_chunk<kC, 0, LT, LS, false, false, true, true, true>(
+            const float P = scan_chunk<kC, 0, LT, LS, false, false, true, true, true, 4>(
                 a, p, k, q, r, row0, s.H, h, DK, n, scan_lane ? tid : 0, scan_lane, nt, lam, L, false, lane);
             if (scan_lane) smf[Cfg::DECAY + tid] = P;
         }
@@ -436,70 +441,120 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
         }
         __syncthreads();
 
-        // reverse walk over the chunk's tokens, one key slot per lane
-        if (glane) {
-            struct GBatch {
-                uint16_t v[5][4];
+        // Reverse walk over the chunk's tokens, split into four 16-token quarters,
+        // one per wave (lane = key slot).  With u_t = qt dqt - kh dkh and
+        // w_t = q dqt / lam_t^2, the log-gate adjoint is S_t = S_in + sum_{s>=t} u_s
+        // and the precision-adjoint carry obeys c_{t-1} = alpha_t (c_t - w_t) -
+        // pbar_t rho_t S_t (alpha = abar^2 rho^2), affine in the quarter's incoming
+        // (c_in, S_in).  Pass 1 composes each quarter into c_out = A c_in + B +
+        // Gam S_in and S_out = S_in + U; the quarters are chained through LDS;
+        // pass 2 re-walks each quarter from its incoming carries and writes the
+        // gradients.
+        if (lane < NTN) {
+            const int tq1 = 16 * wave + 15;       // last token of this wave's quarter
+            struct GIn {
+                float av, pv, kv, qv, rv, lam_t, lam_p, Pt, Xv, Yv;
             };
-            auto loadb = [&](GBatch& bb, int tb) {  // tokens tb, tb-1, tb-2, tb-3
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int tc = max(min(tb - j, nt - 1), 0);
-                    const size_t rowi = (row0 + tc) * s.H + h;
-                    const size_t o = rowi * DK + ng;
-                    bb.v[0][j] = a[o];
-                    bb.v[1][j] = p[o];
-                    bb.v[2][j] = k[o];
-                    bb.v[3][j] = q[o];
-                    bb.v[4][j] = r[rowi];
+            auto fetch = [&](int t) {
+                GIn x;
+                const int tc = min(t, nt - 1);
+                const size_t rowi = (row0 + tc) * s.H + h;
+                const size_t o = rowi * DK + ng;
+                x.av = bf16_to_f32(a[o]);
+                x.pv = bf16_to_f32(p[o]);
+                x.kv = bf16_to_f32(k[o]);
+                x.qv = bf16_to_f32(q[o]);
+                x.rv = bf16_to_f32(r[rowi]);
+                x.lam_t = smf[Cfg::LAM + t * LS + nl];
+                const float lp = smf[Cfg::LAM + max(t - 1, 0) * LS + nl];
+                x.lam_p = t > 0 ? lp : lam_start;
+                x.Pt = smf[Cfg::PP + t * LS + nl];
+                x.Xv = smf[Cfg::X + t * LS + nl];
+                x.Yv = smf[Cfg::Y + t * LS + nl];
+                return x;
+            };
+            // pass 1: affine summary of the quarter
+            float A = 1.f, Bc = 0.f, Gam = 0.f, U = 0.f;
+#pragma unroll 4
+            for (int t = tq1; t > tq1 - 16; --t) {
+                if (t >= nt) continue;
+                const GIn x = fetch(t);
+                const float den = fmaf(x.pv, x.lam_p, x.av * x.av);
+                const float rr3 = fast_rcp(den * x.lam_t);
+                const float rho = x.lam_t * rr3, ilam = den * rr3;
+                const float dqt = x.Pt * x.Xv, dkh = x.Yv * fast_rcp(x.Pt);
+                U += x.qv * ilam * dqt - x.rv * x.kv * dkh;           // L_t (local suffix sum)
+                const float w = x.qv * dqt * ilam * ilam;
+                const float alpha = x.av * x.av * rho * rho, prho = x.pv * rho;
+                Bc = alpha * (Bc - w) - prho * U;
+                A *= alpha;
+                Gam = alpha * Gam - prho;
+            }
+            smf[Cfg::QS + (wave * 4 + 0) * NTN + nl] = A;
+            smf[Cfg::QS + (wave * 4 + 1) * NTN + nl] = Bc;
+            smf[Cfg::QS + (wave * 4 + 2) * NTN + nl] = Gam;
+            smf[Cfg::QS + (wave * 4 + 3) * NTN + nl] = U;
+        }
+        __syncthreads();  // quarter summaries visible to every wave
+        if (lane < NTN) {
+            const int tq1 = 16 * wave + 15;
+            float c_in = cnext, S_in = Sg;
+            for (int w2 = 3; w2 > wave; --w2) {
+                const float A2 = smf[Cfg::QS + (w2 * 4 + 0) * NTN + nl];
+                const float B2 = smf[Cfg::QS + (w2 * 4 + 1) * NTN + nl];
+                const float G2 = smf[Cfg::QS + (w2 * 4 + 2) * NTN + nl];
+                const float U2 = smf[Cfg::QS + (w2 * 4 + 3) * NTN + nl];
+                c_in = A2 * c_in + B2 + G2 * S_in;
+                S_in += U2;
+            }
+            // carries into the previous chunk: through all four quarters
+            {
+                float c_all = cnext, S_all = Sg;
+                for (int w2 = 3; w2 >= 0; --w2) {
+                    const float A2 = smf[Cfg::QS + (w2 * 4 + 0) * NTN + nl];
+                    const float B2 = smf[Cfg::QS + (w2 * 4 + 1) * NTN + nl];
+                    const float G2 = smf[Cfg::QS + (w2 * 4 + 2) * NTN + nl];
+                    const float U2 = smf[Cfg::QS + (w2 * 4 + 3) * NTN + nl];
+                    c_all = A2 * c_all + B2 + G2 * S_all;
+                    S_all += U2;
                 }
-            };
-            auto stepb = [&](const GBatch& bb, int tb) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int t = tb - j;
-                    const uint16_t raw0 = bb.v[0][j], raw1 = bb.v[1][j], raw2 = bb.v[2][j], raw3 = bb.v[3][j],
-                                   raw4 = bb.v[4][j];
-                    if (t < nt) {
-                        const float av = bf16_to_f32(raw0), pv = bf16_to_f32(raw1);
-                        const float kv = bf16_to_f32(raw2), qv = bf16_to_f32(raw3);
-                        const float rv = bf16_to_f32(raw4);
-                        const float lam_t = smf[Cfg::LAM + t * LS + nl];
-                        const float lam_pl = smf[Cfg::LAM + max(t - 1, 0) * LS + nl];
-                        const float lam_p = t > 0 ? lam_pl : lam_start;
-                        const float Pt = smf[Cfg::PP + t * LS + nl];
-                        const float Xv = smf[Cfg::X + t * LS + nl], Yv = smf[Cfg::Y + t * LS + nl];
-                        const float den = fmaf(pv, lam_p, av * av);
-                        const float rr3 = fast_rcp(den * lam_t * av);   // one reciprocal for three
-                        const float rho = lam_t * av * rr3;
-                        const float ilam = den * av * rr3;
-                        const float ia = den * lam_t * rr3;
-                        const float iPt = fast_rcp(Pt);
-                        const float dqt = Pt * Xv;
-                        const float dkh = Yv * iPt;
-                        const float kh = rv * kv;
-                        Sg += qv * ilam * dqt - kh * dkh;                      // adjoint of log F_t
-                        const float gl = cnext - qv * dqt * ilam * ilam;       // adjoint of lam_t
-                        const float drho = fmaf(gl, lam_p, Sg * den);
-                        const float rho2 = rho * rho;
-                        const size_t o = ((row0 + t) * s.H + h) * DK + ng;
-                        dq[o] = f32_to_bf16(dqt * ilam);
-                        dk[o] = f32_to_bf16(rv * dkh + 2.f * kv * rv * gl);
-                        da[o] = f32_to_bf16(Sg * ia - 2.f * av * rho2 * drho);
-                        dp[o] = f32_to_bf16(-lam_p * rho2 * drho);
-                        smf[Cfg::X + t * LS + nl] = kv * dkh + kv * kv * gl;   // term of dr
-                        cnext = av * av * rho2 * gl - pv * rho * Sg;
-                    }
-                }
-            };
-            GBatch b0, b1;
-            loadb(b0, kC - 1);
-#pragma unroll 1
-            for (int tb = kC - 1; tb >= 0; tb -= 8) {
-                loadb(b1, tb - 4);
-                stepb(b0, tb);
-                if (tb - 8 >= 0) loadb(b0, tb - 8);
-                stepb(b1, tb - 4);
+                cnext = c_all;
+                Sg = S_all;
+            }
+            // pass 2: gradients of the quarter's tokens
+            float c = c_in, S = S_in;
+#pragma unroll 4
+            for (int t = tq1; t > tq1 - 16; --t) {
+                if (t >= nt) continue;
+                const int tc = t;
+                const size_t rowi = (row0 + tc) * s.H + h;
+                const size_t o = rowi * DK + ng;
+                const float av = bf16_to_f32(a[o]), pv = bf16_to_f32(p[o]);
+                const float kv = bf16_to_f32(k[o]), qv = bf16_to_f32(q[o]);
+                const float rv = bf16_to_f32(r[rowi]);
+                const float lam_t = smf[Cfg::LAM + t * LS + nl];
+                const float lpl = smf[Cfg::LAM + max(t - 1, 0) * LS + nl];
+                const float lam_p = t > 0 ? lpl : lam_start;
+                const float Pt = smf[Cfg::PP + t * LS + nl];
+                const float Xv = smf[Cfg::X + t * LS + nl], Yv = smf[Cfg::Y + t * LS + nl];
+                const float den = fmaf(pv, lam_p, av * av);
+                const float rr3 = fast_rcp(den * lam_t * av);   // one reciprocal for three
+                const float rho = lam_t * av * rr3;
+                const float ilam = den * av * rr3;
+                const float ia = den * lam_t * rr3;
+                const float dqt = Pt * Xv;
+                const float dkh = Yv * fast_rcp(Pt);
+                const float kh = rv * kv;
+                S += qv * ilam * dqt - kh * dkh;                      // adjoint of log F_t
+                const float gl = c - qv * dqt * ilam * ilam;          // adjoint of lam_t
+                const float drho = fmaf(gl, lam_p, S * den);
+                const float rho2 = rho * rho;
+                dq[o] = f32_to_bf16(dqt * ilam);
+                dk[o] = f32_to_bf16(rv * dkh + 2.f * kv * rv * gl);
+                da[o] = f32_to_bf16(S * ia - 2.f * av * rho2 * drho);
+                dp[o] = f32_to_bf16(-lam_p * rho2 * drho);
+                smf[Cfg::X + t * LS + nl] = kv * dkh + kv * kv * gl;   // term of dr
+                c = av * av * rho2 * gl - pv * rho * S;
             }
         }
         __syncthreads();
@@ -517,7 +572,7 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
         }
         __syncthreads();
     }
-    if (glane && g.dlam0) g.dlam0[(size_t)bh * DK + ng] = cnext;
+    if (wave == 0 && glane && g.dlam0) g.dlam0[(size_t)bh * DK + ng] = cnext;
 }
 
 // dr = sum of the per-key-tile partials, stored in the input dtype

@@ -48,6 +48,7 @@ struct FwdCfg {
     static constexpr int YV = DECAY + DK;                  // [2][kC] floats
     static constexpr size_t BYTES = (size_t)(YV + 2 * kC) * 4;
     static_assert(DK >= 32 && DK % 32 == 0, "chunked path needs dk >= 32");
+    static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
 };
 
 template <int DK, int DV>

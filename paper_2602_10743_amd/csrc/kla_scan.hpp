@@ -14,7 +14,7 @@
 // selected at compile time: [t][n] (row stride LQ) and [n][t] (row stride LT,
 // written 8 tokens per 16-byte store).  Optionally lam_t and P_t are stored in
 // fp32 [t][n] (row stride LS).  Tokens t >= nt get zeros.  The inputs of the
-// next 4 tokens are loaded while the current 4 are processed; loads are
+// next NB tokens are loaded while the current NB are processed; loads are
 // unconditional (clamped to the last valid token).
 #pragma once
 #include "kla_mfma.hpp"
@@ -30,11 +30,12 @@ struct ScanLds {
     float* yv;                 // per-token partial sums of q^2 / lam over the wave, [t]
 };
 
-template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST>
+template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST, int NB>
 struct ChunkScan {
-    // raw bf16 inputs of 4 tokens: abar, pbar, k, q, r
+    static_assert(NB == 4 || NB == 8, "batches of 4 or 8 tokens");
+    // raw bf16 inputs of NB tokens: abar, pbar, k, q, r
     struct Batch {
-        uint16_t v[5][4];
+        uint16_t v[5][NB];
     };
 
     const uint16_t *a, *p, *k, *q, *r;
@@ -47,7 +48,7 @@ struct ChunkScan {
 
     __device__ __forceinline__ void load(Batch& b, int t4) const {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < NB; ++j) {
             const int tc = min(t4 + j, nt - 1);
             const size_t rowi = (row0 + tc) * H + h;
             const size_t o = rowi * DK + n;
@@ -59,11 +60,11 @@ struct ChunkScan {
         }
     }
 
-    // tokens t4 .. t4+3 into slots OFF .. OFF+3 of the current group of 8
+    // tokens t4 .. t4+NB-1 into slots OFF .. OFF+NB-1 of the current group of 8
     template <int OFF>
     __device__ __forceinline__ void step(const Batch& b, int t4, float& lam) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < NB; ++j) {
             const int t = t4 + j;
             const float av = bf16_to_f32(b.v[0][j]), pv = bf16_to_f32(b.v[1][j]);
             const float kv = bf16_to_f32(b.v[2][j]), qv = bf16_to_f32(b.v[3][j]);
@@ -145,25 +146,37 @@ struct ChunkScan {
     __device__ __forceinline__ float run(float& lam) {
         Batch b0, b1;
         load(b0, 0);
+        if constexpr (NB == 4) {
 #pragma unroll 1
-        for (int t8 = 0; t8 < C; t8 += 8) {
-            load(b1, t8 + 4);
-            step<0>(b0, t8, lam);
-            if (t8 + 8 < C) load(b0, t8 + 8);
-            step<4>(b1, t8 + 4, lam);
-            store8(t8);
+            for (int t8 = 0; t8 < C; t8 += 8) {
+                load(b1, t8 + 4);
+                step<0>(b0, t8, lam);
+                if (t8 + 8 < C) load(b0, t8 + 8);
+                step<4>(b1, t8 + 4, lam);
+                store8(t8);
+            }
+        } else {
+#pragma unroll 1
+            for (int t16 = 0; t16 < C; t16 += 16) {
+                load(b1, t16 + 8);
+                step<0>(b0, t16, lam);
+                store8(t16);
+                if (t16 + 16 < C) load(b0, t16 + 16);
+                step<0>(b1, t16 + 8, lam);
+                store8(t16 + 8);
+            }
         }
         return P;
     }
 };
 
-template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST>
+template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST, int NB = 8>
 __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ a, const uint16_t* __restrict__ p,
                                             const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
                                             const uint16_t* __restrict__ r, size_t row0, int H, int h, int DK,
                                             int n, int nl, bool active, int nt, float& lam, const ScanLds& L,
                                             bool want_yv, int lane) {
-    ChunkScan<C, LQ, LT, LS, QN, KN, QT, KT, ST> sc{a, p, k, q, r, row0, H, h, DK, n, nl, nt, lane, active, want_yv, L};
+    ChunkScan<C, LQ, LT, LS, QN, KN, QT, KT, ST, NB> sc{a, p, k, q, r, row0, H, h, DK, n, nl, nt, lane, active, want_yv, L};
     return sc.run(lam);
 }
 
