@@ -100,12 +100,24 @@ __global__ __launch_bounds__(kThr) void bwd_b1_kernel(Shape s, BwdArgs g, const 
         for (int rr = 0; rr < 4; ++rr)
             G[rt][rr] = (owns && g.detaT) ? g.detaT[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dcol] : 0.f;
 
+    // the previous chunk's dY tile and first scan inputs are in flight during a chunk
+    TileStage<kC, DVT, kThr> ystage;
+    ScanPrefetch<8> spre;
+    if (nchunk > 0) {
+        const int cl = nchunk - 1;
+        const size_t r0 = (size_t)b * T + (size_t)cl * kC;
+        const int ntl = T - cl * kC;
+        ystage.load(dy, r0, s.H, h, DV, d0, ntl, tid);
+        if (tid < Cfg::NSCAN) scan_prefetch<8>(spre, a, p, k, q, r, r0, s.H, h, DK, n_scan, ntl);
+    }
+
     for (int c = nchunk - 1; c >= 0; --c) {
         const int t0 = c * kC;
         const int nt = min(kC, T - t0);
         const size_t row0 = (size_t)b * T + t0;
 
-        load_tile<kC, DVT, 0, LT, false, true>(nullptr, sm + Cfg::YT, dy, row0, s.H, h, DV, d0, nt, tid, kThr);
+        ystage.template store<0, LT, false, true>(nullptr, sm + Cfg::YT, tid);
+        if (c > 0) ystage.load(dy, row0 - kC, s.H, h, DV, d0, kC, tid);   // earlier chunks are full
         if (tid < Cfg::NSCAN) {
             float lam = saved_lam[((size_t)bh * nchunk + c) * DK + n_scan];
             ScanLds L{};
@@ -115,9 +127,10 @@ __global__ __launch_bounds__(kThr) void bwd_b1_kernel(Shape s, BwdArgs g, const 
             L.kn_lo = sm + Cfg::KL;
             L.qt_hi = sm + Cfg::QTH;
             L.qt_lo = sm + Cfg::QTL;
-            const float P = scan_chunk<kC, LQ, LT, 0, true, true, true, false, false>(
-                a, p, k, q, r, row0, s.H, h, DK, n_scan, n_scan, scan_lane, nt, lam, L, false, lane);
+            const float P = scan_chunk<kC, LQ, LT, 0, true, true, true, false, false, 8>(
+                a, p, k, q, r, row0, s.H, h, DK, n_scan, n_scan, scan_lane, nt, lam, L, lane, spre);
             if (scan_lane) sDecay[n_scan] = P;
+            if (c > 0) scan_prefetch<8>(spre, a, p, k, q, r, row0 - kC, s.H, h, DK, n_scan, kC);
         }
         __syncthreads();
 
@@ -301,15 +314,45 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
     const bool scan_lane = tid < NTN;
     const int NSCAN = NTN < 64 ? 64 : NTN;
 
+    // the previous chunk's dY / V tiles, first scan inputs and saved state rows are
+    // in flight while a chunk is processed
+    TileStage<kC, DV, kThr> ystage, vstage;
+    ScanPrefetch<4> spre;
+    float4 h0pre[KSD][2];
+    auto load_h0 = [&](int cc) {
+        const float* H0 = saved_H + (((size_t)bh * (nchunk + 1) + cc) * DK + ncol) * DV;
+#pragma unroll
+        for (int ks = 0; ks < KSD; ++ks) {
+            h0pre[ks][0] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4);
+            h0pre[ks][1] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4 + 4);
+        }
+    };
+    if (nchunk > 0) {
+        const int cl = nchunk - 1;
+        const size_t r0 = (size_t)b * T + (size_t)cl * kC;
+        const int ntl = T - cl * kC;
+        ystage.load(dy, r0, s.H, h, DV, 0, ntl, tid);
+        vstage.load(v, r0, s.H, h, DV, 0, ntl, tid);
+        if (wave == 0) scan_prefetch<4>(spre, a, p, k, q, r, r0, s.H, h, DK, scan_lane ? n0 + tid : n0, ntl);
+        if (owns) load_h0(cl);
+    }
+
     for (int c = nchunk - 1; c >= 0; --c) {
         const int t0 = c * kC;
         const int nt = min(kC, T - t0);
         const size_t row0 = (size_t)b * T + t0;
         const float lam_start = saved_lam[((size_t)bh * nchunk + c) * DK + ng];
 
-        load_tile<kC, DV, LD, LT, true, true>(sm + Cfg::DY, sm + Cfg::DYT, dy, row0, s.H, h, DV, 0, nt, tid, kThr);
-        load_tile<kC, DV, LD, 0, true, false>(sm + Cfg::V, nullptr, v, row0, s.H, h, DV, 0, nt, tid, kThr);
-        if (tid < NSCAN) {
+        ystage.template store<LD, LT, true, true>(sm + Cfg::DY, sm + Cfg::DYT, tid);
+        vstage.template store<LD, 0, true, false>(sm + Cfg::V, nullptr, tid);
+        if (c > 0) {  // earlier chunks are full
+            ystage.load(dy, row0 - kC, s.H, h, DV, 0, kC, tid);
+            vstage.load(v, row0 - kC, s.H, h, DV, 0, kC, tid);
+        }
+        __syncthreads();
+
+        if (wave == 0) {
+            // precision walk of this workgroup's key slots
             float lam = saved_lam[((size_t)bh * nchunk + c) * DK + (scan_lane ? n0 + tid : n0)];
             ScanLds L{};
             L.qt_hi = sm + Cfg::QTH;
@@ -320,41 +363,41 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
             L.P = smf + Cfg::PP;
             const int n = scan_lane ? n0 + tid : n0;
             const float P = scan_chunk<kC, 0, LT, LS, false, false, true, true, true, 4>(
-                a, p, k, q, r, row0, s.H, h, DK, n, scan_lane ? tid : 0, scan_lane, nt, lam, L, false, lane);
+                a, p, k, q, r, row0, s.H, h, DK, n, scan_lane ? tid : 0, scan_lane, nt, lam, L, lane, spre);
             if (scan_lane) smf[Cfg::DECAY + tid] = P;
-        }
-        __syncthreads();
-
-        // B[s, j] = dY_s . V_j for j <= s (exact bf16 products), kept as B and B^T;
-        // tiles (0,1), (2,3) are the zeros read by the 32-deep K steps.
-        for (int tk = wave; tk < 12; tk += 4) {
-            int st, jt;
-            if (tk < 10) {
-                st = tk >= 6 ? 3 : tk >= 3 ? 2 : tk >= 1 ? 1 : 0;
-                jt = tk - st * (st + 1) / 2;
-            } else {
-                st = tk == 10 ? 0 : 2;
-                jt = st + 1;
-            }
-            f32x4 acc = zero4();
-            if (tk < 10) {
-#pragma unroll
-                for (int ks = 0; ks < KSD; ++ks) {
-                    const bf16x8 ya = lds8(sm + Cfg::DY + (16 * st + l16) * LD + 32 * ks + 8 * g4);
-                    const bf16x8 vb = lds8(sm + Cfg::V + (16 * jt + l16) * LD + 32 * ks + 8 * g4);
-                    acc = mfma_bf16(ya, vb, acc);
+            if (c > 0) scan_prefetch<4>(spre, a, p, k, q, r, row0 - kC, s.H, h, DK, n, kC);
+        } else {
+            // meanwhile B[s, j] = dY_s . V_j for j <= s (exact bf16 products), kept as B and
+            // B^T; tiles (0,1), (2,3) are the zeros read by the 32-deep K steps.
+            for (int tk = wave - 1; tk < 12; tk += 3) {
+                int st, jt;
+                if (tk < 10) {
+                    st = tk >= 6 ? 3 : tk >= 3 ? 2 : tk >= 1 ? 1 : 0;
+                    jt = tk - st * (st + 1) / 2;
+                } else {
+                    st = tk == 10 ? 0 : 2;
+                    jt = st + 1;
                 }
-            }
+                f32x4 acc = zero4();
+                if (tk < 10) {
 #pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                const int si = 16 * st + 4 * g4 + rr, j = 16 * jt + l16;
-                const float x = (tk < 10 && j <= si) ? acc[rr] : 0.f;
-                uint16_t hi, lo;
-                split(x, hi, lo);
-                sm[Cfg::BH + si * LT + j] = hi;
-                sm[Cfg::BL + si * LT + j] = lo;
-                sm[Cfg::BTH + j * LT + si] = hi;
-                sm[Cfg::BTL + j * LT + si] = lo;
+                    for (int ks = 0; ks < KSD; ++ks) {
+                        const bf16x8 ya = lds8(sm + Cfg::DY + (16 * st + l16) * LD + 32 * ks + 8 * g4);
+                        const bf16x8 vb = lds8(sm + Cfg::V + (16 * jt + l16) * LD + 32 * ks + 8 * g4);
+                        acc = mfma_bf16(ya, vb, acc);
+                    }
+                }
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    const int si = 16 * st + 4 * g4 + rr, j = 16 * jt + l16;
+                    const float x = (tk < 10 && j <= si) ? acc[rr] : 0.f;
+                    uint16_t hi, lo;
+                    split(x, hi, lo);
+                    sm[Cfg::BH + si * LT + j] = hi;
+                    sm[Cfg::BL + si * LT + j] = lo;
+                    sm[Cfg::BTH + j * LT + si] = hi;
+                    sm[Cfg::BTL + j * LT + si] = lo;
+                }
             }
         }
         __syncthreads();
@@ -364,11 +407,9 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
             // X = dY H0^T + M(B) Kn
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) accX[mt] = zero4();
-            const float* H0 = saved_H + (((size_t)bh * (nchunk + 1) + c) * DK + ncol) * DV;
 #pragma unroll
             for (int ks = 0; ks < KSD; ++ks) {
-                const float4 h0a = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4);
-                const float4 h0b = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4 + 4);
+                const float4 h0a = h0pre[ks][0], h0b = h0pre[ks][1];
                 bf16x8 hh, hl;
                 split8(f32x4{h0a.x, h0a.y, h0a.z, h0a.w}, f32x4{h0b.x, h0b.y, h0b.z, h0b.w}, hh, hl);
 #pragma unroll
@@ -377,6 +418,7 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
                     accX[mt] = mfma2b(ya, hh, hl, accX[mt]);
                 }
             }
+            if (c > 0) load_h0(c - 1);
 #pragma unroll
             for (int mt = 0; mt < 4; ++mt) {
 #pragma unroll

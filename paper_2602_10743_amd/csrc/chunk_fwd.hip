@@ -51,7 +51,7 @@ struct FwdCfg {
     static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
 };
 
-template <int DK, int DV>
+template <int DK, int DV, bool YV>
 __global__ __launch_bounds__(kThreadsC) void fwd_chunk_kernel(Shape s, FwdArgs g, float* saved_lam,
                                                               float* saved_H) {
     using Cfg = FwdCfg<DK, DV>;
@@ -91,7 +91,7 @@ __global__ __launch_bounds__(kThreadsC) void fwd_chunk_kernel(Shape s, FwdArgs g
     const int l16 = lane & 15, g4 = lane >> 4;
     const int T = s.T;
     const int nchunk = (T + kC - 1) / kC;
-    const bool want_yvar = g.yvar != nullptr && tile == 0;
+    const bool want_yvar = YV && tile == 0;
 
     // state tile owned by this wave: rows n (all), columns d0 + 16*wave .. +15
     f32x4 Hs[NRT];
@@ -110,10 +110,21 @@ __global__ __launch_bounds__(kThreadsC) void fwd_chunk_kernel(Shape s, FwdArgs g
     float lam = 1.f;
     if (scan_lane && g.lam0) lam = g.lam0[(size_t)bh * DK + tid];
 
+    // the next chunk's value tile and first scan inputs are in flight during a chunk
+    TileStage<kC, DVT, kThreadsC> vstage;
+    ScanPrefetch<8> spre;
+    const int n_scan = scan_lane ? tid : DK - 1;
+    if (nchunk > 0) {
+        const int nt0 = min(kC, T);
+        vstage.load(v, (size_t)b * T, s.H, h, DV, d0, nt0, tid);
+        if (tid < Cfg::NSCAN) scan_prefetch<8>(spre, a, p, k, q, r, (size_t)b * T, s.H, h, DK, n_scan, nt0);
+    }
+
     for (int c = 0; c < nchunk; ++c) {
         const int t0 = c * kC;
         const int nt = min(kC, T - t0);
         const size_t row0 = (size_t)b * T + t0;   // token index of t0 within batch b
+        const int ntn = min(kC, T - t0 - kC);      // tokens of the next chunk (if any)
 
         if (saved_H) {
             if (scan_lane) saved_lam[((size_t)bh * nchunk + c) * DK + tid] = lam;
@@ -126,8 +137,9 @@ __global__ __launch_bounds__(kThreadsC) void fwd_chunk_kernel(Shape s, FwdArgs g
             }
         }
 
-        // ---- value tile, transposed into [d][t]
-        load_tile<kC, DVT, 0, LT, false, true>(nullptr, sm + Cfg::VT, v, row0, s.H, h, DV, d0, nt, tid, kThreadsC);
+        // ---- value tile, transposed into [d][t]; then the next chunk's is requested
+        vstage.template store<0, LT, false, true>(nullptr, sm + Cfg::VT, tid);
+        if (c + 1 < nchunk) vstage.load(v, row0 + kC, s.H, h, DV, d0, ntn, tid);
 
         // ---- precision walk, one key slot per lane
         if (tid < Cfg::NSCAN) {
@@ -139,10 +151,10 @@ __global__ __launch_bounds__(kThreadsC) void fwd_chunk_kernel(Shape s, FwdArgs g
             L.kt_hi = sm + Cfg::KTH;
             L.kt_lo = sm + Cfg::KTL;
             L.yv = sYV + wave * kC;
-            const int n = scan_lane ? tid : DK - 1;
-            const float P = scan_chunk<kC, LQ, LT, 0, true, true, false, true, false>(
-                a, p, k, q, r, row0, s.H, h, DK, n, n, scan_lane, nt, lam, L, want_yvar, lane);
-            if (scan_lane) sDecay[n] = P;
+            const float P = scan_chunk<kC, LQ, LT, 0, true, true, false, true, false, 8, YV>(
+                a, p, k, q, r, row0, s.H, h, DK, n_scan, n_scan, scan_lane, nt, lam, L, lane, spre);
+            if (scan_lane) sDecay[n_scan] = P;
+            if (c + 1 < nchunk) scan_prefetch<8>(spre, a, p, k, q, r, row0 + kC, s.H, h, DK, n_scan, ntn);
         }
         __syncthreads();
 
@@ -253,10 +265,10 @@ __global__ __launch_bounds__(kThreadsC) void fwd_chunk_kernel(Shape s, FwdArgs g
     }
 }
 
-template <int DK, int DV>
-hipError_t launch_fwd(const Shape& s, const FwdArgs& a, float* saved_lam, float* saved_H, hipStream_t st) {
+template <int DK, int DV, bool YV>
+hipError_t launch_fwd_v(const Shape& s, const FwdArgs& a, float* saved_lam, float* saved_H, hipStream_t st) {
     using Cfg = FwdCfg<DK, DV>;
-    auto kern = fwd_chunk_kernel<DK, DV>;
+    auto kern = fwd_chunk_kernel<DK, DV, YV>;
     // more than 64 KiB of LDS must be opted into once per kernel (thread-safe static init)
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)Cfg::BYTES);
@@ -264,6 +276,13 @@ hipError_t launch_fwd(const Shape& s, const FwdArgs& a, float* saved_lam, float*
     const unsigned grid = (unsigned)(s.B * s.H * Cfg::NTILE);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreadsC), Cfg::BYTES, st, s, a, saved_lam, saved_H);
     return hipGetLastError();
+}
+
+// the readout variance adds a cross-lane sum per token, so it is a separate instantiation
+template <int DK, int DV>
+hipError_t launch_fwd(const Shape& s, const FwdArgs& a, float* saved_lam, float* saved_H, hipStream_t st) {
+    return a.yvar ? launch_fwd_v<DK, DV, true>(s, a, saved_lam, saved_H, st)
+                  : launch_fwd_v<DK, DV, false>(s, a, saved_lam, saved_H, st);
 }
 
 }  // namespace

@@ -13,7 +13,8 @@
 // Qp and Kn are stored as split-bf16 (hi, lo) pairs in any of four LDS layouts
 // selected at compile time: [t][n] (row stride LQ) and [n][t] (row stride LT,
 // written 8 tokens per 16-byte store).  Optionally lam_t and P_t are stored in
-// fp32 [t][n] (row stride LS).  Tokens t >= nt get zeros.  The inputs of the
+// fp32 [t][n] (row stride LS), and (YV) the per-token wave sums of q^2/lam.
+// Tokens t >= nt get zeros.  The inputs of the
 // next NB tokens are loaded while the current NB are processed; loads are
 // unconditional (clamped to the last valid token).
 #pragma once
@@ -30,7 +31,7 @@ struct ScanLds {
     float* yv;                 // per-token partial sums of q^2 / lam over the wave, [t]
 };
 
-template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST, int NB>
+template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST, int NB, bool YV>
 struct ChunkScan {
     static_assert(NB == 4 || NB == 8, "batches of 4 or 8 tokens");
     // raw bf16 inputs of NB tokens: abar, pbar, k, q, r
@@ -41,7 +42,7 @@ struct ChunkScan {
     const uint16_t *a, *p, *k, *q, *r;
     size_t row0;
     int H, h, DK, n, nl, nt, lane;
-    bool active, want_yv;
+    bool active;
     ScanLds L;
     float P = 1.f, iP = 1.f;
     uint32_t hp[8], lp[8];  // the current 8 tokens: packed (Qp, Kn) hi and lo halves
@@ -100,7 +101,7 @@ struct ChunkScan {
                     L.P[t * LS + nl] = P;
                 }
             }
-            if (want_yv) {
+            if constexpr (YV) {
 #pragma unroll
                 for (int off = 32; off > 0; off >>= 1) w += __shfl_xor(w, off, 64);
                 if (lane == 0) L.yv[t] = w;
@@ -143,9 +144,9 @@ struct ChunkScan {
     // over groups of 8 tokens is a runtime loop (LDS addresses advance with it
     // instead of being materialised per token); the loads of the next 4 tokens
     // are in flight while the current 4 are processed.
-    __device__ __forceinline__ float run(float& lam) {
-        Batch b0, b1;
-        load(b0, 0);
+    // b0 holds the chunk's first NB tokens, loaded in advance by the caller.
+    __device__ __forceinline__ float run(float& lam, const Batch& first) {
+        Batch b0 = first, b1;
         if constexpr (NB == 4) {
 #pragma unroll 1
             for (int t8 = 0; t8 < C; t8 += 8) {
@@ -170,15 +171,80 @@ struct ChunkScan {
     }
 };
 
-template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST, int NB = 8>
+// First NB tokens of a chunk for key slot n, issued ahead of the chunk's walk.
+template <int NB>
+struct ScanPrefetch {
+    uint16_t v[5][NB];
+};
+
+template <int NB>
+__device__ __forceinline__ void scan_prefetch(ScanPrefetch<NB>& b, const uint16_t* __restrict__ a,
+                                              const uint16_t* __restrict__ p, const uint16_t* __restrict__ k,
+                                              const uint16_t* __restrict__ q, const uint16_t* __restrict__ r,
+                                              size_t row0, int H, int h, int DK, int n, int nt) {
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+        const int tc = min(j, nt - 1);
+        const size_t rowi = (row0 + tc) * H + h;
+        const size_t o = rowi * DK + n;
+        b.v[0][j] = a[o];
+        b.v[1][j] = p[o];
+        b.v[2][j] = k[o];
+        b.v[3][j] = q[o];
+        b.v[4][j] = r[rowi];
+    }
+}
+
+template <int C, int LQ, int LT, int LS, bool QN, bool KN, bool QT, bool KT, bool ST, int NB, bool YV = false>
 __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ a, const uint16_t* __restrict__ p,
                                             const uint16_t* __restrict__ k, const uint16_t* __restrict__ q,
                                             const uint16_t* __restrict__ r, size_t row0, int H, int h, int DK,
                                             int n, int nl, bool active, int nt, float& lam, const ScanLds& L,
-                                            bool want_yv, int lane) {
-    ChunkScan<C, LQ, LT, LS, QN, KN, QT, KT, ST, NB> sc{a, p, k, q, r, row0, H, h, DK, n, nl, nt, lane, active, want_yv, L};
-    return sc.run(lam);
+                                            int lane, const ScanPrefetch<NB>& first) {
+    using S = ChunkScan<C, LQ, LT, LS, QN, KN, QT, KT, ST, NB, YV>;
+    S sc{a, p, k, q, r, row0, H, h, DK, n, nl, nt, lane, active, L};
+    typename S::Batch b0;
+#pragma unroll
+    for (int i = 0; i < 5; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) b0.v[i][j] = first.v[i][j];
+    return sc.run(lam, b0);
 }
+
+// Register-staged copy of a chunk tile of a per-token bf16 tensor (row length
+// rowlen, columns c0 .. c0+W): issued one chunk ahead, written to LDS later.
+template <int C, int W, int NTHR>
+struct TileStage {
+    static constexpr int PER = (C * (W / 8) + NTHR - 1) / NTHR;
+    uint4 x[PER];
+    __device__ __forceinline__ void load(const uint16_t* __restrict__ src, size_t row0, int H, int h, int rowlen,
+                                         int c0, int nt, int tid) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * NTHR;
+            const int t = idx / (W / 8), c8 = idx % (W / 8);
+            const int tc = min(t, nt - 1);
+            x[i] = *reinterpret_cast<const uint4*>(src + ((row0 + tc) * H + h) * rowlen + c0 + 8 * c8);
+            if (t >= nt) x[i] = uint4{0u, 0u, 0u, 0u};
+        }
+    }
+    // rows [t][c] with stride L and/or transposed [c][t] with stride LT
+    template <int L, int LT, bool ROWS, bool COLS>
+    __device__ __forceinline__ void store(uint16_t* rows, uint16_t* cols, int tid) const {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * NTHR;
+            if (PER * NTHR != C * (W / 8) && idx >= C * (W / 8)) break;
+            const int t = idx / (W / 8), c8 = idx % (W / 8);
+            if constexpr (ROWS) *reinterpret_cast<uint4*>(rows + t * L + 8 * c8) = x[i];
+            if constexpr (COLS) {
+                const uint16_t* e = reinterpret_cast<const uint16_t*>(&x[i]);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) cols[(8 * c8 + j) * LT + t] = e[j];
+            }
+        }
+    }
+};
 
 // Chunk tile of a per-token bf16 tensor (row length rowlen, columns c0 .. c0+W)
 // into LDS, row-major [t][c] (stride L) and/or transposed [c][t] (stride LT);
