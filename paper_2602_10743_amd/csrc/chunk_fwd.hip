@@ -1,67 +1,159 @@
 // Chunked forward of the KLA filter on MFMA (bf16 inputs, fp32 state).
 //
-// The sequence is cut into chunks of kC = 64 tokens.  Within a chunk, for each
-// key slot n, the precision path (Theorem 1, gate view) is walked token by
-// token from the carried lam, giving the gate F_t = abar_t rho_t (Theorem 2),
-// its running product P_t = prod_{s<=t} F_s inside the chunk, the effective
-// query qt_t = q_t / lam_t and the evidence key kh_t = r_t k_t.  With
-//   Qp[t, n] = qt_t[n] P_t[n],   Kn[t, n] = kh_t[n] / P_t[n]
-// the information-state recursion over the chunk is exactly
+// The sequence is cut into chunks of kC = 32 tokens.  Within a chunk, for each
+// key slot n, the precision path (Theorem 1) is walked token by token in
+// homogeneous coordinates.  The Moebius update
+//   lam_t = (lam + phi (abar^2 + pbar lam)) / (abar^2 + pbar lam),  phi = k^2 r,
+// acts linearly on (x, z) with lam = x / z:
+//   z_t = pbar_t x_{t-1} + abar_t^2 z_{t-1}     (so rho_t = z_{t-1} / z_t)
+//   x_t = x_{t-1} + phi_t z_t
+// and, with A_t = prod_{s<=t} abar_s, the running product of the forget gates
+// F = abar rho (Theorem 2) inside the chunk is P_t = A_t / z_t (x = lam, z = 1,
+// A = 1 at the chunk start).  With one reciprocal R = 1 / (x_t A_t) per token,
+//   Qp[t, n] = (q_t / lam_t) P_t = q_t A_t (A_t R)
+//   Kn[t, n] = (r_t k_t) / P_t   = r_t k_t z_t (x_t R)
+// and the information-state recursion over the chunk is exactly
 //   y    = mask(Qp Kn^T) V + Qp H                       (readout, Algorithm 1)
 //   H   <- diag(P_C) (H + Kn^T V)                       (state at the chunk end)
 // (the unrolled "attention matrix" of the paper's appendix, restricted to a
-// chunk, plus the carried state).  The four contractions run on
+// chunk, plus the carried state).  The contractions run on
 // v_mfma_f32_16x16x32_bf16 with split-bf16 operands for the fp32 factors
-// (see kla_mfma.hpp), accumulating in fp32.
+// (kla_mfma.hpp), accumulating in fp32.
 //
-// One workgroup (4 waves) per (batch, head, 64-wide value tile) walks the
-// chunks in order with the state tile H[dk, 64] in registers: wave w owns the
-// 16 value channels 16w..16w+15 of the tile for the readout and the state.
-// Requirement (documented in the ABI): inside one chunk the product of gates
-// P_t stays within fp32 range for every key slot.
+// One workgroup per (batch, head, value tile of up to 64 channels), with two
+// kinds of waves that work one chunk apart through a double-buffered LDS
+// exchange and one barrier per chunk:
+//   scan waves (64 key slots each) walk chunk c and write Qp and Kn ([t][n]),
+//     Kn^T ([n][t]), the chunk decay P_C and the variance partials into buffer
+//     c & 1; their inputs are staged through LDS one chunk ahead with 16-byte
+//     loads;
+//   MFMA waves (32 value channels each, the state H[dk, 32] in registers)
+//     meanwhile consume chunk c - 1: attention tiles, readout, y, state update.
+// Requirement (documented in the ABI): inside one chunk, prod abar,
+// prod (abar^2 + pbar lam) and lam prod (abar^2 + pbar lam) stay in fp32 range.
+#include "kla_buf.hpp"
 #include "kla_internal.hpp"
 #include "kla_mfma.hpp"
-#include "kla_scan.hpp"
 
 namespace kla {
 namespace {
 
-constexpr int kC = 64;
-constexpr int kThreadsC = 256;
+constexpr int kC = 32;         // tokens per chunk
+constexpr int kSaveEvery = 2;  // the saved context holds every second chunk start (64-token chunks)
 
 template <int DK, int DV>
 struct FwdCfg {
-    static constexpr int DVT = DV < 64 ? DV : 64;
+    static constexpr int DVT = DV < 64 ? DV : 64;    // value channels per workgroup
     static constexpr int NTILE = DV / DVT;
-    static constexpr int NCT = DVT / 16;
+    static constexpr int DCW = DVT < 32 ? DVT : 32;  // value channels per MFMA wave
+    static constexpr int NDT = DCW / 16;
+    static constexpr int NMW = DVT / DCW;            // MFMA waves
+    static constexpr int SW = DK < 64 ? DK : 64;     // key slots per scan wave
+    static constexpr int NSW = DK / SW;              // scan waves
+    static constexpr int NTHR = 64 * (NSW + NMW);
     static constexpr int NRT = DK / 16;
     static constexpr int KSN = DK / 32;
-    static constexpr int NSCAN = DK < 64 ? 64 : DK;   // threads running the precision scan
-    static constexpr int LQ = DK + 8;                  // row stride of [t][n] buffers
-    static constexpr int LT = kC + 8;                  // row stride of [n][t], [d][t], [i][j]
-    static constexpr int QH = 0, QL = QH + kC * LQ, KH = QL + kC * LQ, KL = KH + kC * LQ;
-    static constexpr int KTH = KL + kC * LQ, KTL = KTH + DK * LT;
-    static constexpr int VT = KTL + DK * LT;
-    static constexpr int AH = VT + DVT * LT, AL = AH + kC * LT;
-    static constexpr int END16 = AL + kC * LT;
-    static constexpr int DECAY = (END16 + 7) / 8 * 4;      // float index
-    static constexpr int YV = DECAY + DK;                  // [2][kC] floats
-    static constexpr size_t BYTES = (size_t)(YV + 2 * kC) * 4;
+    static constexpr int LQ = DK + 8;                // row stride of [t][n] (halfwords)
+    static constexpr int LT = kC + 8;                // row stride of [n][t] and [d][t] (halfwords)
+    // one exchange buffer (byte offsets)
+    static constexpr int QH = 0, QL = QH + kC * LQ * 2, KH = QL + kC * LQ * 2, KL = KH + kC * LQ * 2;
+    static constexpr int KTH = KL + kC * LQ * 2, KTL = KTH + DK * LT * 2;
+    static constexpr int DEC = KTL + DK * LT * 2;    // P_C [DK] fp32
+    static constexpr int YVP = DEC + DK * 4;         // variance partials [NSW][kC] fp32
+    static constexpr int BUF = (YVP + NSW * kC * 4 + 15) / 16 * 16;
+    static constexpr int VT = 2 * BUF;               // per MFMA wave: V^T [DCW][LT]
+    static constexpr int STG = VT + NMW * DCW * LT * 2;  // per scan wave: abar, pbar, k, q [4][kC][SW]
+    static constexpr int BYTES = STG + NSW * 4 * kC * SW * 2;
+    static constexpr int SPL = kC * SW / 8 / 64;     // 16-byte staging loads per lane and tensor
+    static constexpr int VPL = kC * DCW / 8 / 64;    // 16-byte V loads per lane
     static_assert(DK >= 32 && DK % 32 == 0, "chunked path needs dk >= 32");
+    static_assert(SPL >= 1 && VPL >= 1, "tile sizes");
     static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
 };
 
+// Outputs of the precision walk in one exchange buffer.
+struct ScanOut {
+    uint16_t *qh, *ql, *kh, *kl;   // [t][n]
+    uint32_t *kth, *ktl;           // [n][t] as packed pairs
+    float* yv;                     // per-token wave sums of q^2 / lam
+};
+
+// Walk the tokens of one chunk for key slot n (lane), from the staged inputs.
+// FULL: all kC tokens are valid (no per-token guards).
+template <int SW, int LQ, int LT, bool YV, bool FULL>
+__device__ __forceinline__ void scan_tokens(const uint16_t* __restrict__ stg, int sl, float rvc, int nt, bool active,
+                                            int n, float& x, float& z, float& A, const ScanOut& o) {
+#pragma unroll
+    for (int t8 = 0; t8 < kC; t8 += 8) {
+        uint32_t kth[4], ktl[4];
+#pragma unroll
+        for (int j2 = 0; j2 < 4; ++j2) {
+            float qp2[2], kn2[2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const int t = t8 + 2 * j2 + e;
+                const float av = bf16_to_f32(stg[(0 * kC + t) * SW + sl]);
+                const float pv = bf16_to_f32(stg[(1 * kC + t) * SW + sl]);
+                const float kv = bf16_to_f32(stg[(2 * kC + t) * SW + sl]);
+                const float qv = bf16_to_f32(stg[(3 * kC + t) * SW + sl]);
+                const float rv = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rvc), t));
+                const float kr = kv * rv;
+                const float zn = fmaf(pv, x, av * av * z);
+                const float xn = fmaf(kr * kv, zn, x);
+                const float An = A * av;
+                const float R = fast_rcp(xn * An);
+                const float AR = An * R;   // 1 / x_t
+                float qp = (qv * An) * AR;
+                float kn = (kr * zn) * (xn * R);
+                float w = 0.f;
+                if constexpr (YV) w = qv * qv * zn * AR;   // q^2 / lam_t
+                if (FULL || t < nt) {
+                    x = xn;
+                    z = zn;
+                    A = An;
+                } else {
+                    qp = 0.f;
+                    kn = 0.f;
+                    w = 0.f;
+                }
+                qp2[e] = qp;
+                kn2[e] = kn;
+                if constexpr (YV) {
+                    const float ws = wave_sum(active ? w : 0.f);
+                    if (sl == 0) o.yv[t] = ws;
+                }
+            }
+            uint32_t qh, ql, kh, kl;
+            split2(qp2[0], qp2[1], qh, ql);
+            split2(kn2[0], kn2[1], kh, kl);
+            const int t = t8 + 2 * j2;
+            if (active) {
+                o.qh[t * LQ + n] = static_cast<uint16_t>(qh);
+                o.qh[(t + 1) * LQ + n] = static_cast<uint16_t>(qh >> 16);
+                o.ql[t * LQ + n] = static_cast<uint16_t>(ql);
+                o.ql[(t + 1) * LQ + n] = static_cast<uint16_t>(ql >> 16);
+                o.kh[t * LQ + n] = static_cast<uint16_t>(kh);
+                o.kh[(t + 1) * LQ + n] = static_cast<uint16_t>(kh >> 16);
+                o.kl[t * LQ + n] = static_cast<uint16_t>(kl);
+                o.kl[(t + 1) * LQ + n] = static_cast<uint16_t>(kl >> 16);
+            }
+            kth[j2] = kh;
+            ktl[j2] = kl;
+        }
+        if (active) {
+            *reinterpret_cast<uint4*>(o.kth + (n * LT + t8) / 2) = uint4{kth[0], kth[1], kth[2], kth[3]};
+            *reinterpret_cast<uint4*>(o.ktl + (n * LT + t8) / 2) = uint4{ktl[0], ktl[1], ktl[2], ktl[3]};
+        }
+    }
+}
+
 template <int DK, int DV, bool YV>
-__global__ __launch_bounds__(kThreadsC) void fwd_chunk_kernel(Shape s, FwdArgs g, float* saved_lam,
-                                                              float* saved_H) {
+__global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape s, FwdArgs g, float* saved_lam,
+                                                                         float* saved_H) {
     using Cfg = FwdCfg<DK, DV>;
-    constexpr int DVT = Cfg::DVT, NTILE = Cfg::NTILE, NCT = Cfg::NCT, NRT = Cfg::NRT, KSN = Cfg::KSN;
-    constexpr int LQ = Cfg::LQ, LT = Cfg::LT;
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    uint16_t* sm = reinterpret_cast<uint16_t*>(smem_raw);
-    float* smf = reinterpret_cast<float*>(smem_raw);
-    float* sDecay = smf + Cfg::DECAY;
-    float* sYV = smf + Cfg::YV;
+    constexpr int DVT = Cfg::DVT, NTILE = Cfg::NTILE, DCW = Cfg::DCW, NDT = Cfg::NDT, NSW = Cfg::NSW;
+    constexpr int SW = Cfg::SW, NRT = Cfg::NRT, KSN = Cfg::KSN, LQ = Cfg::LQ, LT = Cfg::LT;
+    extern __shared__ __align__(16) unsigned char smem[];
 
     const uint16_t* q = static_cast<const uint16_t*>(g.q);
     const uint16_t* k = static_cast<const uint16_t*>(g.k);
@@ -86,182 +178,251 @@ __global__ __launch_bounds__(kThreadsC) void fwd_chunk_kernel(Shape s, FwdArgs g
         }
     }
     const int b = bh / s.H, h = bh % s.H;
-    const int d0 = tile * DVT;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int H = s.H, T = s.T;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform role
     const int l16 = lane & 15, g4 = lane >> 4;
-    const int T = s.T;
     const int nchunk = (T + kC - 1) / kC;
-    const bool want_yvar = YV && tile == 0;
+    const int nsave = (T + kC * kSaveEvery - 1) / (kC * kSaveEvery);
+    const size_t seq0 = (size_t)b * T;   // token index of this sequence's first token
 
-    // state tile owned by this wave: rows n (all), columns d0 + 16*wave .. +15
-    f32x4 Hs[NRT];
-    const bool owns_cols = wave < NCT;
-    const int dcol = d0 + 16 * wave + l16;
-#pragma unroll
-    for (int rt = 0; rt < NRT; ++rt) {
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-            const int n = 16 * rt + 4 * g4 + rr;
-            Hs[rt][rr] = (owns_cols && g.eta0) ? g.eta0[((size_t)bh * DK + n) * DV + dcol] : 0.f;
-        }
-    }
-    // precision lane n = tid (threads tid < DK)
-    const bool scan_lane = tid < DK;
-    float lam = 1.f;
-    if (scan_lane && g.lam0) lam = g.lam0[(size_t)bh * DK + tid];
+    if (wave < NSW) {
+        // ================================================================ scan waves
+        const bool active = lane < SW;
+        const int sl = active ? lane : 0;     // slot within this wave's staged rows
+        const int n = wave * SW + sl;
+        float x = (active && g.lam0) ? g.lam0[(size_t)bh * DK + n] : 1.f;   // lam at the chunk start
+        const uint16_t* stg = reinterpret_cast<const uint16_t*>(smem + Cfg::STG) + wave * 4 * kC * SW;
+        uint16_t* stg_w = reinterpret_cast<uint16_t*>(smem + Cfg::STG) + wave * 4 * kC * SW;
+        const uint32_t tok_bytes = (uint32_t)H * DK * 2;
 
-    // the next chunk's value tile and first scan inputs are in flight during a chunk
-    TileStage<kC, DVT, kThreadsC> vstage;
-    ScanPrefetch<8> spre;
-    const int n_scan = scan_lane ? tid : DK - 1;
-    if (nchunk > 0) {
-        const int nt0 = min(kC, T);
-        vstage.load(v, (size_t)b * T, s.H, h, DV, d0, nt0, tid);
-        if (tid < Cfg::NSCAN) scan_prefetch<8>(spre, a, p, k, q, r, (size_t)b * T, s.H, h, DK, n_scan, nt0);
-    }
-
-    for (int c = 0; c < nchunk; ++c) {
-        const int t0 = c * kC;
-        const int nt = min(kC, T - t0);
-        const size_t row0 = (size_t)b * T + t0;   // token index of t0 within batch b
-        const int ntn = min(kC, T - t0 - kC);      // tokens of the next chunk (if any)
-
-        if (saved_H) {
-            if (scan_lane) saved_lam[((size_t)bh * nchunk + c) * DK + tid] = lam;
-            if (owns_cols) {
-                float* dst = saved_H + ((size_t)bh * (nchunk + 1) + c) * DK * DV;
+        // 16-byte loads of one chunk's abar, pbar, k, q rows of this wave's slots:
+        // lane -> (token t, 8 slots); r as one value per lane (token = lane)
+        uint4 stv[4][Cfg::SPL];
+        float rv_lane = 0.f;
+        auto issue = [&](int c) {
+            const int t0 = c * kC, nt = min(kC, T - t0);
+            const size_t e0 = ((seq0 + t0) * H + h) * DK + wave * SW;
+            const uint32_t bytes = (uint32_t)((nt - 1) * H * DK + SW) * 2;
+            const uint16_t* src[4] = {a, p, k, q};
 #pragma unroll
-                for (int rt = 0; rt < NRT; ++rt)
+            for (int ti = 0; ti < 4; ++ti) {
+                const rsrc_t rs = make_rsrc(src[ti] + e0, bytes);
 #pragma unroll
-                    for (int rr = 0; rr < 4; ++rr) dst[(16 * rt + 4 * g4 + rr) * DV + dcol] = Hs[rt][rr];
+                for (int i = 0; i < Cfg::SPL; ++i) {
+                    const int idx = lane + 64 * i;
+                    const int t = idx / (SW / 8), c8 = idx % (SW / 8);
+                    stv[ti][i] = buf_ld128(rs, (uint32_t)t * tok_bytes + c8 * 16, 0);   // rows t >= nt read as 0
+                }
             }
-        }
+            const rsrc_t rr = make_rsrc(r + (seq0 + t0) * H + h, (uint32_t)((nt - 1) * H + 1) * 2);
+            rv_lane = bf16_to_f32(buf_ld16(rr, (uint32_t)(lane < kC ? lane : kC) * H * 2, 0));
+        };
+        if (nchunk > 0) issue(0);
 
-        // ---- value tile, transposed into [d][t]; then the next chunk's is requested
-        vstage.template store<0, LT, false, true>(nullptr, sm + Cfg::VT, tid);
-        if (c + 1 < nchunk) vstage.load(v, row0 + kC, s.H, h, DV, d0, ntn, tid);
+        for (int c = 0; c <= nchunk; ++c) {
+            if (c < nchunk) {
+                const int nt = min(kC, T - c * kC);
+                if (saved_lam && c % kSaveEvery == 0 && active)
+                    saved_lam[((size_t)bh * nsave + c / kSaveEvery) * DK + n] = x;
+#pragma unroll
+                for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+                    for (int i = 0; i < Cfg::SPL; ++i)
+                        *reinterpret_cast<uint4*>(stg_w + ti * kC * SW + (lane + 64 * i) * 8) = stv[ti][i];
+                const float rvc = rv_lane;
+                if (c + 1 < nchunk) issue(c + 1);
 
-        // ---- precision walk, one key slot per lane
-        if (tid < Cfg::NSCAN) {
-            ScanLds L{};
-            L.qn_hi = sm + Cfg::QH;
-            L.qn_lo = sm + Cfg::QL;
-            L.kn_hi = sm + Cfg::KH;
-            L.kn_lo = sm + Cfg::KL;
-            L.kt_hi = sm + Cfg::KTH;
-            L.kt_lo = sm + Cfg::KTL;
-            L.yv = sYV + wave * kC;
-            const float P = scan_chunk<kC, LQ, LT, 0, true, true, false, true, false, 8, YV>(
-                a, p, k, q, r, row0, s.H, h, DK, n_scan, n_scan, scan_lane, nt, lam, L, lane, spre);
-            if (scan_lane) sDecay[n_scan] = P;
-            if (c + 1 < nchunk) scan_prefetch<8>(spre, a, p, k, q, r, row0 + kC, s.H, h, DK, n_scan, ntn);
-        }
-        __syncthreads();
-
-        // ---- attention tiles A[i, j] = sum_n Qp[i, n] Kn[j, n], j <= i, shared through LDS
-        for (int tk = wave; tk < 12; tk += 4) {
-            int it, jt;
-            if (tk < 10) {
-                it = tk >= 6 ? 3 : tk >= 3 ? 2 : tk >= 1 ? 1 : 0;
-                jt = tk - it * (it + 1) / 2;
-            } else {  // upper tiles read by the 32-deep K steps: zero them
-                it = tk == 10 ? 0 : 2;
-                jt = it + 1;
+                unsigned char* buf = smem + (c & 1) * Cfg::BUF;
+                ScanOut o;
+                o.qh = reinterpret_cast<uint16_t*>(buf + Cfg::QH);
+                o.ql = reinterpret_cast<uint16_t*>(buf + Cfg::QL);
+                o.kh = reinterpret_cast<uint16_t*>(buf + Cfg::KH);
+                o.kl = reinterpret_cast<uint16_t*>(buf + Cfg::KL);
+                o.kth = reinterpret_cast<uint32_t*>(buf + Cfg::KTH);
+                o.ktl = reinterpret_cast<uint32_t*>(buf + Cfg::KTL);
+                o.yv = reinterpret_cast<float*>(buf + Cfg::YVP) + wave * kC;
+                float z = 1.f, A = 1.f;
+                if (nt == kC)
+                    scan_tokens<SW, LQ, LT, YV, true>(stg, sl, rvc, nt, active, n, x, z, A, o);
+                else
+                    scan_tokens<SW, LQ, LT, YV, false>(stg, sl, rvc, nt, active, n, x, z, A, o);
+                const float iz = fast_rcp(z);
+                x *= iz;   // lam at the chunk end
+                if (active) reinterpret_cast<float*>(buf + Cfg::DEC)[n] = A * iz;
             }
-            f32x4 acc = zero4();
-            if (tk < 10) {
+            __syncthreads();
+        }
+        if (g.lamT && active && tile == 0) g.lamT[(size_t)bh * DK + n] = x;
+    } else {
+        // ================================================================ MFMA waves
+        const int m = wave - NSW;
+        const int dm0 = tile * DVT + m * DCW;   // first value channel of this wave
+        uint16_t* sVT = reinterpret_cast<uint16_t*>(smem + Cfg::VT) + m * DCW * LT;
+
+        // state H[n, d] for n = 16 rt + 4 g4 + rr, d = dm0 + 16 dt + l16
+        f32x4 Hs[NRT][NDT];
+#pragma unroll
+        for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr)
+                    Hs[rt][dt][rr] =
+                        g.eta0 ? g.eta0[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dm0 + 16 * dt + l16] : 0.f;
+
+        uint4 vst[Cfg::VPL];
+        auto issue_v = [&](int c) {
+            const int t0 = c * kC, nt = min(kC, T - t0);
+            const rsrc_t rs = make_rsrc(v + ((seq0 + t0) * H + h) * DV + dm0, (uint32_t)((nt - 1) * H * DV + DCW) * 2);
+#pragma unroll
+            for (int i = 0; i < Cfg::VPL; ++i) {
+                const int idx = lane + 64 * i;
+                const int t = idx / (DCW / 8), c8 = idx % (DCW / 8);
+                vst[i] = buf_ld128(rs, ((uint32_t)t * H * DV + c8 * 8) * 2, 0);   // rows t >= nt read as 0
+            }
+        };
+        auto save_state = [&](int slot) {
+            float* dst = saved_H + ((size_t)bh * (nsave + 1) + slot) * DK * DV;
+#pragma unroll
+            for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr)
+                        dst[(16 * rt + 4 * g4 + rr) * DV + dm0 + 16 * dt + l16] = Hs[rt][dt][rr];
+        };
+        if (nchunk > 0) issue_v(0);
+
+        for (int c = 0; c <= nchunk; ++c) {
+            const int cc = c - 1;   // the chunk consumed in this round
+            if (cc >= 0) {
+                const int nt = min(kC, T - cc * kC);
+                const size_t row0 = seq0 + (size_t)cc * kC;
+                if (saved_H && cc % kSaveEvery == 0) save_state(cc / kSaveEvery);
+
+                // V^T [d][t] of this wave's channels (private to the wave); then the next chunk's V
+#pragma unroll
+                for (int i = 0; i < Cfg::VPL; ++i) {
+                    const int idx = lane + 64 * i;
+                    const int t = idx / (DCW / 8), c8 = idx % (DCW / 8);
+                    const uint16_t* e = reinterpret_cast<const uint16_t*>(&vst[i]);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) sVT[(8 * c8 + j) * LT + t] = e[j];
+                }
+                if (cc + 1 < nchunk) issue_v(cc + 1);
+
+                const unsigned char* buf = smem + (cc & 1) * Cfg::BUF;
+                const uint16_t* sQH = reinterpret_cast<const uint16_t*>(buf + Cfg::QH);
+                const uint16_t* sQL = reinterpret_cast<const uint16_t*>(buf + Cfg::QL);
+                const uint16_t* sKH = reinterpret_cast<const uint16_t*>(buf + Cfg::KH);
+                const uint16_t* sKL = reinterpret_cast<const uint16_t*>(buf + Cfg::KL);
+                const uint16_t* sKTH = reinterpret_cast<const uint16_t*>(buf + Cfg::KTH);
+                const uint16_t* sKTL = reinterpret_cast<const uint16_t*>(buf + Cfg::KTL);
+                const float* sDec = reinterpret_cast<const float*>(buf + Cfg::DEC);
+
+                // ---- S^T[j, i] = sum_n Kn[j, n] Qp[i, n], tiles (jt, it) = (0,0), (0,1), (1,1)
+                f32x4 S00 = zero4(), S01 = zero4(), S11 = zero4();
 #pragma unroll
                 for (int ks = 0; ks < KSN; ++ks) {
-                    const int qo = (16 * it + l16) * LQ + 32 * ks + 8 * g4;
-                    const int ko = (16 * jt + l16) * LQ + 32 * ks + 8 * g4;
-                    acc = mfma3(lds8(sm + Cfg::QH + qo), lds8(sm + Cfg::QL + qo), lds8(sm + Cfg::KH + ko),
-                                lds8(sm + Cfg::KL + ko), acc);
+                    const int o0 = l16 * LQ + 32 * ks + 8 * g4, o1 = o0 + 16 * LQ;
+                    const bf16x8 k0h = lds8(sKH + o0), k0l = lds8(sKL + o0);
+                    const bf16x8 k1h = lds8(sKH + o1), k1l = lds8(sKL + o1);
+                    const bf16x8 q0h = lds8(sQH + o0), q0l = lds8(sQL + o0);
+                    const bf16x8 q1h = lds8(sQH + o1), q1l = lds8(sQL + o1);
+                    S00 = mfma3(k0h, k0l, q0h, q0l, S00);
+                    S01 = mfma3(k0h, k0l, q1h, q1l, S01);
+                    S11 = mfma3(k1h, k1l, q1h, q1l, S11);
+                }
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {   // causal mask j <= i inside the diagonal tiles
+                    if (4 * g4 + rr > l16) {
+                        S00[rr] = 0.f;
+                        S11[rr] = 0.f;
+                    }
+                }
+                // B operands over the 32-deep contraction j (rows {4g..4g+3} and {16+4g..16+4g+3})
+                bf16x8 sbh[2], sbl[2];
+                split8(S00, zero4(), sbh[0], sbl[0]);
+                split8(S01, S11, sbh[1], sbl[1]);
+
+                // ---- y^T[d, i] = sum_j V^T[d, j] S^T[j, i] + sum_n H^T[d, n] Qp^T[n, i]
+                f32x4 yacc[NDT][2];
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) {
+                    const int vo = (16 * dt + l16) * LT + 4 * g4;
+                    const bf16x8 va = lds4x2(sVT + vo, sVT + vo + 16);
+#pragma unroll
+                    for (int it = 0; it < 2; ++it) yacc[dt][it] = mfma2b(va, sbh[it], sbl[it], zero4());
+                }
+#pragma unroll
+                for (int ks = 0; ks < KSN; ++ks) {
+                    bf16x8 qbh[2], qbl[2];
+#pragma unroll
+                    for (int it = 0; it < 2; ++it) {
+                        const int qo = (16 * it + l16) * LQ + 32 * ks + 4 * g4;
+                        qbh[it] = lds4x2(sQH + qo, sQH + qo + 16);
+                        qbl[it] = lds4x2(sQL + qo, sQL + qo + 16);
+                    }
+#pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt) {
+                        bf16x8 hh, hl;
+                        split8(Hs[2 * ks][dt], Hs[2 * ks + 1][dt], hh, hl);
+#pragma unroll
+                        for (int it = 0; it < 2; ++it) yacc[dt][it] = mfma3(hh, hl, qbh[it], qbl[it], yacc[dt][it]);
+                    }
+                }
+                // y[t, d .. d+3] for t = 16 it + l16, d = dm0 + 16 dt + 4 g4
+#pragma unroll
+                for (int it = 0; it < 2; ++it) {
+                    const int t = 16 * it + l16;
+                    if (t < nt) {
+#pragma unroll
+                        for (int dt = 0; dt < NDT; ++dt) {
+                            const uint2 pk{cvt_pk_bf16(yacc[dt][it][0], yacc[dt][it][1]),
+                                           cvt_pk_bf16(yacc[dt][it][2], yacc[dt][it][3])};
+                            *reinterpret_cast<uint2*>(y + ((row0 + t) * H + h) * DV + dm0 + 16 * dt + 4 * g4) = pk;
+                        }
+                    }
+                }
+
+                // ---- state: H <- diag(P_C) (H + Kn^T V)
+#pragma unroll
+                for (int rt = 0; rt < NRT; ++rt) {
+                    const int ko = (16 * rt + l16) * LT + 8 * g4;
+                    const bf16x8 kth = lds8(sKTH + ko), ktl = lds8(sKTL + ko);
+                    const float4 dec = *reinterpret_cast<const float4*>(sDec + 16 * rt + 4 * g4);
+#pragma unroll
+                    for (int dt = 0; dt < NDT; ++dt) {
+                        const f32x4 hacc = mfma2a(kth, ktl, lds8(sVT + (16 * dt + l16) * LT + 8 * g4), Hs[rt][dt]);
+                        Hs[rt][dt][0] = hacc[0] * dec.x;
+                        Hs[rt][dt][1] = hacc[1] * dec.y;
+                        Hs[rt][dt][2] = hacc[2] * dec.z;
+                        Hs[rt][dt][3] = hacc[3] * dec.w;
+                    }
+                }
+
+                if (YV && tile == 0 && m == 0 && lane < nt) {
+                    const float* yv = reinterpret_cast<const float*>(buf + Cfg::YVP);
+                    float acc = 0.f;
+#pragma unroll
+                    for (int w2 = 0; w2 < NSW; ++w2) acc += yv[w2 * kC + lane];
+                    g.yvar[(row0 + lane) * H + h] = acc;
                 }
             }
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                const int i = 16 * it + 4 * g4 + rr, j = 16 * jt + l16;
-                const float x = (tk < 10 && j <= i) ? acc[rr] : 0.f;
-                uint16_t hi, lo;
-                split(x, hi, lo);
-                sm[Cfg::AH + i * LT + j] = hi;
-                sm[Cfg::AL + i * LT + j] = lo;
-            }
+            __syncthreads();
         }
-        __syncthreads();
 
-        if (want_yvar && tid < nt) {
-            float acc = 0.f;
-            for (int w2 = 0; w2 < (Cfg::NSCAN + 63) / 64; ++w2) acc += sYV[w2 * kC + tid];
-            g.yvar[(row0 + tid) * s.H + h] = acc;
+        if (saved_H) save_state(nsave);   // the final state closes the saved sequence
+        if (g.etaT) {
+#pragma unroll
+            for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr)
+                        g.etaT[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dm0 + 16 * dt + l16] = Hs[rt][dt][rr];
         }
-
-        if (owns_cols) {
-            const int ct = wave;
-            // ---- readout: y = mask(A) V + Qp H
-            f32x4 acc[4];
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) acc[mt] = zero4();
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt) {
-#pragma unroll
-                for (int ks = 0; ks <= (mt >> 1); ++ks) {
-                    const int ao = (16 * mt + l16) * LT + 32 * ks + 8 * g4;
-                    const bf16x8 vb = lds8(sm + Cfg::VT + (16 * ct + l16) * LT + 32 * ks + 8 * g4);
-                    acc[mt] = mfma2a(lds8(sm + Cfg::AH + ao), lds8(sm + Cfg::AL + ao), vb, acc[mt]);
-                }
-            }
-#pragma unroll
-            for (int ks = 0; ks < KSN; ++ks) {
-                bf16x8 hh, hl;
-                split8(Hs[2 * ks], Hs[2 * ks + 1], hh, hl);
-#pragma unroll
-                for (int mt = 0; mt < 4; ++mt) {
-                    const int qo = (16 * mt + l16) * LQ + 32 * ks + 4 * g4;
-                    const bf16x8 qh = lds4x2(sm + Cfg::QH + qo, sm + Cfg::QH + qo + 16);
-                    const bf16x8 ql = lds4x2(sm + Cfg::QL + qo, sm + Cfg::QL + qo + 16);
-                    acc[mt] = mfma3(qh, ql, hh, hl, acc[mt]);
-                }
-            }
-#pragma unroll
-            for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    const int t = 16 * mt + 4 * g4 + rr;
-                    if (t < nt) y[((row0 + t) * s.H + h) * DV + dcol] = f32_to_bf16(acc[mt][rr]);
-                }
-
-            // ---- state: H <- diag(P_C) (H + Kn^T V)
-#pragma unroll
-            for (int rt = 0; rt < NRT; ++rt) {
-                f32x4 hacc = Hs[rt];
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const int ko = (16 * rt + l16) * LT + 32 * ks + 8 * g4;
-                    const bf16x8 vb = lds8(sm + Cfg::VT + (16 * ct + l16) * LT + 32 * ks + 8 * g4);
-                    hacc = mfma2a(lds8(sm + Cfg::KTH + ko), lds8(sm + Cfg::KTL + ko), vb, hacc);
-                }
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) Hs[rt][rr] = hacc[rr] * sDecay[16 * rt + 4 * g4 + rr];
-            }
-        }
-        __syncthreads();
-    }
-
-    if (saved_H && owns_cols) {  // the final state closes the saved sequence of chunk-start states
-        float* dst = saved_H + ((size_t)bh * (nchunk + 1) + nchunk) * DK * DV;
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt)
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr) dst[(16 * rt + 4 * g4 + rr) * DV + dcol] = Hs[rt][rr];
-    }
-    if (g.lamT && scan_lane && tile == 0) g.lamT[(size_t)bh * DK + tid] = lam;
-    if (g.etaT && owns_cols) {
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt)
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-                g.etaT[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dcol] = Hs[rt][rr];
     }
 }
 
@@ -271,10 +432,10 @@ hipError_t launch_fwd_v(const Shape& s, const FwdArgs& a, float* saved_lam, floa
     auto kern = fwd_chunk_kernel<DK, DV, YV>;
     // more than 64 KiB of LDS must be opted into once per kernel (thread-safe static init)
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)Cfg::BYTES);
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::BYTES);
     if (attr != hipSuccess) return attr;
     const unsigned grid = (unsigned)(s.B * s.H * Cfg::NTILE);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(kThreadsC), Cfg::BYTES, st, s, a, saved_lam, saved_H);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(Cfg::NTHR), Cfg::BYTES, st, s, a, saved_lam, saved_H);
     return hipGetLastError();
 }
 
@@ -289,20 +450,21 @@ hipError_t launch_fwd(const Shape& s, const FwdArgs& a, float* saved_lam, float*
 
 bool chunked_supported(const Shape& s) { return s.bf16 && s.dk >= 32; }
 
-// Saved context: lam at every chunk start [BH][nchunk][dk], then the information
-// state at every chunk start and after the last token [BH][nchunk+1][dk][dv].
+// Saved context over 64-token chunks: lam at every chunk start [BH][nsave][dk],
+// then the information state at every chunk start and after the last token
+// [BH][nsave+1][dk][dv].
 size_t chunked_saved_bytes(const Shape& s) {
-    const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
-    return (size_t)s.B * s.H * s.dk * (nchunk + (nchunk + 1) * (size_t)s.dv) * sizeof(float);
+    const size_t nsave = (size_t)(s.T + kC * kSaveEvery - 1) / (kC * kSaveEvery);
+    return (size_t)s.B * s.H * s.dk * (nsave + (nsave + 1) * (size_t)s.dv) * sizeof(float);
 }
 
 hipError_t launch_forward_chunked(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st) {
     float* saved_lam = nullptr;
     float* saved_H = nullptr;
     if (saved) {
-        const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
+        const size_t nsave = (size_t)(s.T + kC * kSaveEvery - 1) / (kC * kSaveEvery);
         saved_lam = static_cast<float*>(saved);
-        saved_H = saved_lam + (size_t)s.B * s.H * nchunk * s.dk;
+        saved_H = saved_lam + (size_t)s.B * s.H * nsave * s.dk;
     }
 #define KLA_FWD_CASE(DK_, DV_) \
     if (s.dk == DK_ && s.dv == DV_) return launch_fwd<DK_, DV_>(s, a, saved_lam, saved_H, st);
