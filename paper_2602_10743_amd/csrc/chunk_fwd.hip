@@ -25,10 +25,14 @@
 // exchange and one barrier per chunk:
 //   scan waves (64 key slots each) walk chunk c and write Qp and Kn ([t][n]),
 //     Kn^T ([n][t]), the chunk decay P_C and the variance partials into buffer
-//     c & 1; their inputs are staged through LDS one chunk ahead with 16-byte
-//     loads;
+//     c & 1; their inputs arrive in LDS by direct 16-byte buffer loads, each
+//     block of tokens requested for chunk c + 1 as soon as chunk c has walked
+//     past it; they also bring chunk c's value tile into the buffer;
 //   MFMA waves (32 value channels each, the state H[dk, 32] in registers)
 //     meanwhile consume chunk c - 1: attention tiles, readout, y, state update.
+// All loads are issued by the scan waves, whose request stream is fixed, so
+// each wait names exactly the requests it needs (vmcnt counts in issue order);
+// the MFMA waves only store.
 // Requirement (documented in the ABI): inside one chunk, prod abar,
 // prod (abar^2 + pbar lam) and lam prod (abar^2 + pbar lam) stay in fp32 range.
 #include "kla_buf.hpp"
@@ -60,14 +64,20 @@ struct FwdCfg {
     static constexpr int KTH = KL + kC * LQ * 2, KTL = KTH + DK * LT * 2;
     static constexpr int DEC = KTL + DK * LT * 2;    // P_C [DK] fp32
     static constexpr int YVP = DEC + DK * 4;         // variance partials [NSW][kC] fp32
-    static constexpr int BUF = (YVP + NSW * kC * 4 + 15) / 16 * 16;
+    static constexpr int VS = (YVP + NSW * kC * 4 + 15) / 16 * 16;   // value tile [kC][DVT] bf16
+    static constexpr int BUF = VS + kC * DVT * 2;
+    static constexpr int NVL = kC * DVT * 2 / 1024;  // 1 KiB wave loads of the value tile
+    static constexpr int TPV = kC / NVL;             // tokens per value-tile load
     static constexpr int VT = 2 * BUF;               // per MFMA wave: V^T [DCW][LT]
-    static constexpr int STG = VT + NMW * DCW * LT * 2;  // per scan wave: abar, pbar, k, q [4][kC][SW]
-    static constexpr int BYTES = STG + NSW * 4 * kC * SW * 2;
-    static constexpr int SPL = kC * SW / 8 / 64;     // 16-byte staging loads per lane and tensor
-    static constexpr int VPL = kC * DCW / 8 / 64;    // 16-byte V loads per lane
+    // per scan wave: abar, pbar, k, q [4][kC][SW] bf16, then r [2][64] as zero-extended words
+    static constexpr int STG = VT + NMW * DCW * LT * 2;
+    static constexpr int STG_WAVE = 4 * kC * SW * 2 + 2 * 64 * 4;
+    static constexpr int BYTES = STG + NSW * STG_WAVE;
+    static constexpr int TPL = 512 / SW;             // tokens per 16-byte-per-lane load (one block)
+    static constexpr int NBLK = kC / TPL;
+    static constexpr int VPL = kC * DCW / 8 / 64;    // 16-byte V^T transposes per MFMA lane
     static_assert(DK >= 32 && DK % 32 == 0, "chunked path needs dk >= 32");
-    static_assert(SPL >= 1 && VPL >= 1, "tile sizes");
+    static_assert(NBLK >= 1 && VPL >= 1, "tile sizes");
     static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
 };
 
@@ -78,48 +88,76 @@ struct ScanOut {
     float* yv;                     // per-token wave sums of q^2 / lam
 };
 
-// Walk the tokens of one chunk for key slot n (lane), from the staged inputs.
-// FULL: all kC tokens are valid (no per-token guards).
-template <int SW, int LQ, int LT, bool YV, bool FULL>
-__device__ __forceinline__ void scan_tokens(const uint16_t* __restrict__ stg, int sl, float rvc, int nt, bool active,
-                                            int n, float& x, float& z, float& A, const ScanOut& o) {
+// Staged inputs of one group of 8 tokens for one key slot (raw bf16 / r words).
+struct ScanGroup {
+    uint32_t a[8], p[8], k[8], q[8];
+    uint4 r[2];
+};
+
+template <int SW>
+__device__ __forceinline__ void read_group(ScanGroup& gr, const uint16_t* __restrict__ stg,
+                                           const uint32_t* __restrict__ rw, int sl, int t8) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        gr.a[e] = stg[(0 * kC + t8 + e) * SW + sl];
+        gr.p[e] = stg[(1 * kC + t8 + e) * SW + sl];
+        gr.k[e] = stg[(2 * kC + t8 + e) * SW + sl];
+        gr.q[e] = stg[(3 * kC + t8 + e) * SW + sl];
+    }
+    gr.r[0] = *reinterpret_cast<const uint4*>(rw + t8);
+    gr.r[1] = *reinterpret_cast<const uint4*>(rw + t8 + 4);
+}
+
+// Walk the tokens of one chunk for key slot n (lane), from the staged inputs
+// (stg: [4][kC][SW] bf16; rw: r as words [kC]).  FULL: all kC tokens are valid
+// (no per-token guards).  The inputs of the next group of 8 tokens are read
+// from LDS before the current group is processed.  before(G) runs before group
+// G is read (the wait for its staged inputs); after(j) after token block j
+// (TPL tokens) is done (the request of the next chunk's block j).
+template <int SW, int TPL, int LQ, int LT, bool YV, bool FULL, class Before, class After>
+__device__ __forceinline__ void scan_tokens(const uint16_t* __restrict__ stg, const uint32_t* __restrict__ rw, int sl,
+                                            int nt, bool active, int n, float& x, float& z, float& A,
+                                            const ScanOut& o, Before before, After after) {
+    ScanGroup gr[2];
+    before(0);
+    read_group<SW>(gr[0], stg, rw, sl, 0);
 #pragma unroll
     for (int t8 = 0; t8 < kC; t8 += 8) {
+        const ScanGroup& cur = gr[(t8 / 8) & 1];
+        if (t8 + 8 < kC) {
+            before((t8 + 8) / 8);
+            read_group<SW>(gr[((t8 / 8) + 1) & 1], stg, rw, sl, t8 + 8);
+        }
         uint32_t kth[4], ktl[4];
 #pragma unroll
         for (int j2 = 0; j2 < 4; ++j2) {
             float qp2[2], kn2[2];
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
-                const int t = t8 + 2 * j2 + e;
-                const float av = bf16_to_f32(stg[(0 * kC + t) * SW + sl]);
-                const float pv = bf16_to_f32(stg[(1 * kC + t) * SW + sl]);
-                const float kv = bf16_to_f32(stg[(2 * kC + t) * SW + sl]);
-                const float qv = bf16_to_f32(stg[(3 * kC + t) * SW + sl]);
-                const float rv = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, rvc), t));
+                const int t = t8 + 2 * j2 + e, i = 2 * j2 + e;
+                const float av = __uint_as_float(cur.a[i] << 16);
+                const float pv = __uint_as_float(cur.p[i] << 16);
+                const float kv = __uint_as_float(cur.k[i] << 16);
+                const float qv = __uint_as_float(cur.q[i] << 16);
+                const uint32_t rword = i < 4 ? (&cur.r[0].x)[i] : (&cur.r[1].x)[i - 4];
+                const float rv = __uint_as_float(rword << 16);
                 const float kr = kv * rv;
                 const float zn = fmaf(pv, x, av * av * z);
                 const float xn = fmaf(kr * kv, zn, x);
                 const float An = A * av;
                 const float R = fast_rcp(xn * An);
                 const float AR = An * R;   // 1 / x_t
-                float qp = (qv * An) * AR;
-                float kn = (kr * zn) * (xn * R);
-                float w = 0.f;
-                if constexpr (YV) w = qv * qv * zn * AR;   // q^2 / lam_t
-                if (FULL || t < nt) {
-                    x = xn;
-                    z = zn;
-                    A = An;
-                } else {
-                    qp = 0.f;
-                    kn = 0.f;
-                    w = 0.f;
-                }
+                const bool ok = FULL || t < nt;
+                const float qp = ok ? (qv * An) * AR : 0.f;
+                const float kn = ok ? (kr * zn) * (xn * R) : 0.f;
+                x = ok ? xn : x;
+                z = ok ? zn : z;
+                A = ok ? An : A;
                 qp2[e] = qp;
                 kn2[e] = kn;
                 if constexpr (YV) {
-                    const float ws = wave_sum(active ? w : 0.f);
+                    const float w = (ok && active) ? qv * qv * zn * AR : 0.f;   // q^2 / lam_t
+                    const float ws = wave_sum(w);
                     if (sl == 0) o.yv[t] = ws;
                 }
             }
@@ -144,6 +182,7 @@ __device__ __forceinline__ void scan_tokens(const uint16_t* __restrict__ stg, in
             *reinterpret_cast<uint4*>(o.kth + (n * LT + t8) / 2) = uint4{kth[0], kth[1], kth[2], kth[3]};
             *reinterpret_cast<uint4*>(o.ktl + (n * LT + t8) / 2) = uint4{ktl[0], ktl[1], ktl[2], ktl[3]};
         }
+        if ((t8 + 8) % TPL == 0) after((t8 + 8) / TPL - 1);
     }
 }
 
@@ -192,46 +231,61 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
         const int sl = active ? lane : 0;     // slot within this wave's staged rows
         const int n = wave * SW + sl;
         float x = (active && g.lam0) ? g.lam0[(size_t)bh * DK + n] : 1.f;   // lam at the chunk start
-        const uint16_t* stg = reinterpret_cast<const uint16_t*>(smem + Cfg::STG) + wave * 4 * kC * SW;
-        uint16_t* stg_w = reinterpret_cast<uint16_t*>(smem + Cfg::STG) + wave * 4 * kC * SW;
+        unsigned char* stw = smem + Cfg::STG + wave * Cfg::STG_WAVE;
+        uint16_t* stg = reinterpret_cast<uint16_t*>(stw);
+        uint32_t* rw = reinterpret_cast<uint32_t*>(stw + 4 * kC * SW * 2);   // [2][64]
         const uint32_t tok_bytes = (uint32_t)H * DK * 2;
+        // lane -> (token within a block, 8 slots); the load of a block lands as [t][SW] rows
+        const uint32_t blk_voff = (uint32_t)(lane / (SW / 8)) * tok_bytes + (lane % (SW / 8)) * 16;
 
-        // 16-byte loads of one chunk's abar, pbar, k, q rows of this wave's slots:
-        // lane -> (token t, 8 slots); r as one value per lane (token = lane)
-        uint4 stv[4][Cfg::SPL];
-        float rv_lane = 0.f;
-        auto issue = [&](int c) {
-            const int t0 = c * kC, nt = min(kC, T - t0);
+        // buffer descriptors of chunk cn (empty past the sequence: such loads write zeros)
+        rsrc_t rs[4];
+        auto chunk_rsrc = [&](int cn) {
+            const int t0 = cn * kC, nt = min(kC, T - t0);
             const size_t e0 = ((seq0 + t0) * H + h) * DK + wave * SW;
-            const uint32_t bytes = (uint32_t)((nt - 1) * H * DK + SW) * 2;
-            const uint16_t* src[4] = {a, p, k, q};
-#pragma unroll
-            for (int ti = 0; ti < 4; ++ti) {
-                const rsrc_t rs = make_rsrc(src[ti] + e0, bytes);
-#pragma unroll
-                for (int i = 0; i < Cfg::SPL; ++i) {
-                    const int idx = lane + 64 * i;
-                    const int t = idx / (SW / 8), c8 = idx % (SW / 8);
-                    stv[ti][i] = buf_ld128(rs, (uint32_t)t * tok_bytes + c8 * 16, 0);   // rows t >= nt read as 0
-                }
-            }
-            const rsrc_t rr = make_rsrc(r + (seq0 + t0) * H + h, (uint32_t)((nt - 1) * H + 1) * 2);
-            rv_lane = bf16_to_f32(buf_ld16(rr, (uint32_t)(lane < kC ? lane : kC) * H * 2, 0));
+            const uint32_t bytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + SW) * 2 : 0u;
+            rs[0] = make_rsrc(a + e0, bytes);
+            rs[1] = make_rsrc(p + e0, bytes);
+            rs[2] = make_rsrc(k + e0, bytes);
+            rs[3] = make_rsrc(q + e0, bytes);
         };
-        if (nchunk > 0) issue(0);
+        auto issue_block = [&](int j) {
+#pragma unroll
+            for (int ti = 0; ti < 4; ++ti)
+                buf_ld128_lds(rs[ti], stg + (ti * kC + j * Cfg::TPL) * SW, blk_voff + (uint32_t)j * Cfg::TPL * tok_bytes);
+        };
+        // this wave's share of the value-tile loads of chunk cn (loads i = wave, wave + NSW, ...)
+        const int nvw = wave < Cfg::NVL ? (Cfg::NVL - wave + NSW - 1) / NSW : 0;
+        const uint32_t v_voff = (uint32_t)(lane / (DVT / 8)) * H * DV * 2 + (lane % (DVT / 8)) * 16;
+        auto issue_v = [&](int cn) {
+            const int t0 = cn * kC, nt = min(kC, T - t0);
+            const rsrc_t rv = make_rsrc(v + ((seq0 + t0) * H + h) * DV + tile * DVT,
+                                        nt > 0 ? (uint32_t)((nt - 1) * H * DV + DVT) * 2 : 0u);
+            unsigned char* vs = smem + (cn & 1) * Cfg::BUF + Cfg::VS;
+            for (int i = wave; i < Cfg::NVL; i += NSW)
+                buf_ld128_lds(rv, vs + i * 1024, v_voff + (uint32_t)(i * Cfg::TPV) * H * DV * 2);
+        };
+        auto issue_r = [&](int cn) {
+            const int t0 = cn * kC, nt = min(kC, T - t0);
+            const rsrc_t rr = make_rsrc(r + (seq0 + t0) * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
+            buf_ld16_lds(rr, rw + (cn & 1) * 64, (uint32_t)lane * H * 2);   // lanes >= nt read as 0
+        };
+        wait_vm_all();   // the carried lam is complete before the prefetch loop starts
+        if (nchunk > 0) {
+            chunk_rsrc(0);
+            issue_r(0);
+#pragma unroll
+            for (int j = 0; j < Cfg::NBLK; ++j) issue_block(j);
+        }
 
         for (int c = 0; c <= nchunk; ++c) {
             if (c < nchunk) {
                 const int nt = min(kC, T - c * kC);
+                issue_v(c);
+                issue_r(c + 1);
+                chunk_rsrc(c + 1);
                 if (saved_lam && c % kSaveEvery == 0 && active)
                     saved_lam[((size_t)bh * nsave + c / kSaveEvery) * DK + n] = x;
-#pragma unroll
-                for (int ti = 0; ti < 4; ++ti)
-#pragma unroll
-                    for (int i = 0; i < Cfg::SPL; ++i)
-                        *reinterpret_cast<uint4*>(stg_w + ti * kC * SW + (lane + 64 * i) * 8) = stv[ti][i];
-                const float rvc = rv_lane;
-                if (c + 1 < nchunk) issue(c + 1);
 
                 unsigned char* buf = smem + (c & 1) * Cfg::BUF;
                 ScanOut o;
@@ -242,17 +296,34 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                 o.kth = reinterpret_cast<uint32_t*>(buf + Cfg::KTH);
                 o.ktl = reinterpret_cast<uint32_t*>(buf + Cfg::KTL);
                 o.yv = reinterpret_cast<float*>(buf + Cfg::YVP) + wave * kC;
+                // Group G starting block j is read while block j - 1 is processed (after
+                // the next chunk's blocks before j - 1 went out).  Younger than block j's
+                // loads are then: its later blocks, this chunk's value-tile loads (nvw),
+                // r of the next chunk, possibly the saved-lam store, and those requests:
+                // 4 (NBLK - 1) + 1 + nvw for j = 0, 4 (NBLK - 2) + 1 + nvw otherwise.
+                auto before = [&](int G) {
+                    if (G == 0)
+                        wait_vm_le_rt<4 * (Cfg::NBLK - 1) + 1>(nvw);
+                    else if ((8 * G) % Cfg::TPL == 0)
+                        wait_vm_le_rt<4 * (Cfg::NBLK - 2) + 1>(nvw);
+                };
+                auto after = [&](int j) { issue_block(j); };
+                const uint32_t* rwc = rw + (c & 1) * 64;
                 float z = 1.f, A = 1.f;
                 if (nt == kC)
-                    scan_tokens<SW, LQ, LT, YV, true>(stg, sl, rvc, nt, active, n, x, z, A, o);
+                    scan_tokens<SW, Cfg::TPL, LQ, LT, YV, true>(stg, rwc, sl, nt, active, n, x, z, A, o, before, after);
                 else
-                    scan_tokens<SW, LQ, LT, YV, false>(stg, sl, rvc, nt, active, n, x, z, A, o);
+                    scan_tokens<SW, Cfg::TPL, LQ, LT, YV, false>(stg, rwc, sl, nt, active, n, x, z, A, o, before,
+                                                                after);
                 const float iz = fast_rcp(z);
                 x *= iz;   // lam at the chunk end
                 if (active) reinterpret_cast<float*>(buf + Cfg::DEC)[n] = A * iz;
+                // the value tile has landed (younger: r, the saved-lam store, NBLK blocks)
+                wait_vm_le<4 * Cfg::NBLK + 1>();
             }
-            __syncthreads();
+            barrier_lds();
         }
+        wait_vm_all();   // the requests for the chunk past the end have landed before exit
         if (g.lamT && active && tile == 0) g.lamT[(size_t)bh * DK + n] = x;
     } else {
         // ================================================================ MFMA waves
@@ -271,17 +342,6 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                     Hs[rt][dt][rr] =
                         g.eta0 ? g.eta0[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dm0 + 16 * dt + l16] : 0.f;
 
-        uint4 vst[Cfg::VPL];
-        auto issue_v = [&](int c) {
-            const int t0 = c * kC, nt = min(kC, T - t0);
-            const rsrc_t rs = make_rsrc(v + ((seq0 + t0) * H + h) * DV + dm0, (uint32_t)((nt - 1) * H * DV + DCW) * 2);
-#pragma unroll
-            for (int i = 0; i < Cfg::VPL; ++i) {
-                const int idx = lane + 64 * i;
-                const int t = idx / (DCW / 8), c8 = idx % (DCW / 8);
-                vst[i] = buf_ld128(rs, ((uint32_t)t * H * DV + c8 * 8) * 2, 0);   // rows t >= nt read as 0
-            }
-        };
         auto save_state = [&](int slot) {
             float* dst = saved_H + ((size_t)bh * (nsave + 1) + slot) * DK * DV;
 #pragma unroll
@@ -292,27 +352,25 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                     for (int rr = 0; rr < 4; ++rr)
                         dst[(16 * rt + 4 * g4 + rr) * DV + dm0 + 16 * dt + l16] = Hs[rt][dt][rr];
         };
-        if (nchunk > 0) issue_v(0);
-
         for (int c = 0; c <= nchunk; ++c) {
             const int cc = c - 1;   // the chunk consumed in this round
             if (cc >= 0) {
                 const int nt = min(kC, T - cc * kC);
                 const size_t row0 = seq0 + (size_t)cc * kC;
-                if (saved_H && cc % kSaveEvery == 0) save_state(cc / kSaveEvery);
-
-                // V^T [d][t] of this wave's channels (private to the wave); then the next chunk's V
+                const unsigned char* buf = smem + (cc & 1) * Cfg::BUF;
+                // V^T [d][t] of this wave's channels (private to the wave) from the value tile
+                const uint16_t* sVS = reinterpret_cast<const uint16_t*>(buf + Cfg::VS);
 #pragma unroll
                 for (int i = 0; i < Cfg::VPL; ++i) {
                     const int idx = lane + 64 * i;
                     const int t = idx / (DCW / 8), c8 = idx % (DCW / 8);
-                    const uint16_t* e = reinterpret_cast<const uint16_t*>(&vst[i]);
+                    const uint4 x4 = *reinterpret_cast<const uint4*>(sVS + t * DVT + m * DCW + 8 * c8);
+                    const uint16_t* e = reinterpret_cast<const uint16_t*>(&x4);
 #pragma unroll
                     for (int j = 0; j < 8; ++j) sVT[(8 * c8 + j) * LT + t] = e[j];
                 }
-                if (cc + 1 < nchunk) issue_v(cc + 1);
+                if (saved_H && cc % kSaveEvery == 0) save_state(cc / kSaveEvery);
 
-                const unsigned char* buf = smem + (cc & 1) * Cfg::BUF;
                 const uint16_t* sQH = reinterpret_cast<const uint16_t*>(buf + Cfg::QH);
                 const uint16_t* sQL = reinterpret_cast<const uint16_t*>(buf + Cfg::QL);
                 const uint16_t* sKH = reinterpret_cast<const uint16_t*>(buf + Cfg::KH);
@@ -410,7 +468,7 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                     g.yvar[(row0 + lane) * H + h] = acc;
                 }
             }
-            __syncthreads();
+            barrier_lds();
         }
 
         if (saved_H) save_state(nsave);   // the final state closes the saved sequence

@@ -24,6 +24,54 @@ __device__ __forceinline__ uint4 buf_ld128(rsrc_t r, uint32_t voff, uint32_t sof
     return uint4{v[0], v[1], v[2], v[3]};
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// Direct loads into LDS: lane i's 16 bytes land at dst + 16 i (one wave fills
+// 1 KiB contiguously); lanes whose offset lies past the buffer end write zeros.
+// The write completes with the wave's vector-memory counter, not lgkmcnt.
+__device__ __forceinline__ void buf_ld128_lds(rsrc_t r, void* dst, uint32_t voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)dst, 16, voff, 0, 0, 0);
+}
+
+// 2-byte variant: lane i's value lands zero-extended in the word at dst + 4 i.
+__device__ __forceinline__ void buf_ld16_lds(rsrc_t r, void* dst, uint32_t voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)dst, 2, voff, 0, 0, 0);
+}
+
+// s_waitcnt vmcnt(N): at most N vector memory accesses of this wave are still
+// outstanding (they complete in issue order).
+template <int N>
+__device__ __forceinline__ void wait_vm_le() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// vmcnt(BASE + extra) for a wave-uniform extra in [0, 8).
+template <int BASE>
+__device__ __forceinline__ void wait_vm_le_rt(int extra) {
+    switch (extra) {
+        case 0: wait_vm_le<BASE>(); break;
+        case 1: wait_vm_le<BASE + 1>(); break;
+        case 2: wait_vm_le<BASE + 2>(); break;
+        case 3: wait_vm_le<BASE + 3>(); break;
+        case 4: wait_vm_le<BASE + 4>(); break;
+        case 5: wait_vm_le<BASE + 5>(); break;
+        case 6: wait_vm_le<BASE + 6>(); break;
+        default: wait_vm_le<BASE + 7>(); break;
+    }
+}
+
+// s_waitcnt vmcnt(0): every vector memory access of this wave has completed.
+// Placed after loads whose results are carried into a prefetching loop, so the
+// loop body does not wait on them (and thereby on the prefetch) at first use.
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0xF70); }
+
+// Workgroup barrier that orders LDS only: waits for this wave's LDS accesses
+// (lgkmcnt) but leaves vector-memory requests in flight, so direct-to-LDS
+// prefetches and global stores may cross it.  Data those requests bring into
+// LDS is waited for by its consumer through vmcnt.
+__device__ __forceinline__ void barrier_lds() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 template <int CTRL, int ROW_MASK>
 __device__ __forceinline__ float dpp(float x) {
     return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, ROW_MASK,
