@@ -24,12 +24,13 @@
 // kinds of waves that work one chunk apart through a double-buffered LDS
 // exchange and one barrier per chunk:
 //   scan waves (64 key slots each) walk chunk c and write Qp and Kn ([t][n]),
-//     Kn^T ([n][t]), the chunk decay P_C and the variance partials into buffer
-//     c & 1; their inputs arrive in LDS by direct 16-byte buffer loads, each
+//     the chunk decay P_C and the variance partials into buffer c & 1; their inputs arrive in LDS by direct 16-byte buffer loads, each
 //     block of tokens requested for chunk c + 1 as soon as chunk c has walked
 //     past it; they also bring chunk c's value tile into the buffer;
 //   MFMA waves (32 value channels each, the state H[dk, 32] in registers)
-//     meanwhile consume chunk c - 1: attention tiles, readout, y, state update.
+//     meanwhile consume chunk c - 1: attention tiles, readout, y, state update;
+//     operands that run across the rows of a tile (Kn^T, V) are read with
+//     transposing LDS reads (lds_tr8), so each tile is stored once.
 // All loads are issued by the scan waves, whose request stream is fixed, so
 // each wait names exactly the requests it needs (vmcnt counts in issue order);
 // the MFMA waves only store.
@@ -58,33 +59,28 @@ struct FwdCfg {
     static constexpr int NRT = DK / 16;
     static constexpr int KSN = DK / 32;
     static constexpr int LQ = DK + 8;                // row stride of [t][n] (halfwords)
-    static constexpr int LT = kC + 8;                // row stride of [n][t] and [d][t] (halfwords)
     // one exchange buffer (byte offsets)
     static constexpr int QH = 0, QL = QH + kC * LQ * 2, KH = QL + kC * LQ * 2, KL = KH + kC * LQ * 2;
-    static constexpr int KTH = KL + kC * LQ * 2, KTL = KTH + DK * LT * 2;
-    static constexpr int DEC = KTL + DK * LT * 2;    // P_C [DK] fp32
+    static constexpr int DEC = KL + kC * LQ * 2;     // P_C [DK] fp32
     static constexpr int YVP = DEC + DK * 4;         // variance partials [NSW][kC] fp32
     static constexpr int VS = (YVP + NSW * kC * 4 + 15) / 16 * 16;   // value tile [kC][DVT] bf16
     static constexpr int BUF = VS + kC * DVT * 2;
     static constexpr int NVL = kC * DVT * 2 / 1024;  // 1 KiB wave loads of the value tile
     static constexpr int TPV = kC / NVL;             // tokens per value-tile load
-    static constexpr int VT = 2 * BUF;               // per MFMA wave: V^T [DCW][LT]
     // per scan wave: abar, pbar, k, q [4][kC][SW] bf16, then r [2][64] as zero-extended words
-    static constexpr int STG = VT + NMW * DCW * LT * 2;
+    static constexpr int STG = 2 * BUF;
     static constexpr int STG_WAVE = 4 * kC * SW * 2 + 2 * 64 * 4;
     static constexpr int BYTES = STG + NSW * STG_WAVE;
     static constexpr int TPL = 512 / SW;             // tokens per 16-byte-per-lane load (one block)
     static constexpr int NBLK = kC / TPL;
-    static constexpr int VPL = kC * DCW / 8 / 64;    // 16-byte V^T transposes per MFMA lane
     static_assert(DK >= 32 && DK % 32 == 0, "chunked path needs dk >= 32");
-    static_assert(NBLK >= 1 && VPL >= 1, "tile sizes");
+    static_assert(NBLK >= 1 && NVL >= 1, "tile sizes");
     static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
 };
 
 // Outputs of the precision walk in one exchange buffer.
 struct ScanOut {
     uint16_t *qh, *ql, *kh, *kl;   // [t][n]
-    uint32_t *kth, *ktl;           // [n][t] as packed pairs
     float* yv;                     // per-token wave sums of q^2 / lam
 };
 
@@ -114,7 +110,7 @@ __device__ __forceinline__ void read_group(ScanGroup& gr, const uint16_t* __rest
 // from LDS before the current group is processed.  before(G) runs before group
 // G is read (the wait for its staged inputs); after(j) after token block j
 // (TPL tokens) is done (the request of the next chunk's block j).
-template <int SW, int TPL, int LQ, int LT, bool YV, bool FULL, class Before, class After>
+template <int SW, int TPL, int LQ, bool YV, bool FULL, class Before, class After>
 __device__ __forceinline__ void scan_tokens(const uint16_t* __restrict__ stg, const uint32_t* __restrict__ rw, int sl,
                                             int nt, bool active, int n, float& x, float& z, float& A,
                                             const ScanOut& o, Before before, After after) {
@@ -128,7 +124,6 @@ __device__ __forceinline__ void scan_tokens(const uint16_t* __restrict__ stg, co
             before((t8 + 8) / 8);
             read_group<SW>(gr[((t8 / 8) + 1) & 1], stg, rw, sl, t8 + 8);
         }
-        uint32_t kth[4], ktl[4];
 #pragma unroll
         for (int j2 = 0; j2 < 4; ++j2) {
             float qp2[2], kn2[2];
@@ -175,12 +170,6 @@ __device__ __forceinline__ void scan_tokens(const uint16_t* __restrict__ stg, co
                 o.kl[t * LQ + n] = static_cast<uint16_t>(kl);
                 o.kl[(t + 1) * LQ + n] = static_cast<uint16_t>(kl >> 16);
             }
-            kth[j2] = kh;
-            ktl[j2] = kl;
-        }
-        if (active) {
-            *reinterpret_cast<uint4*>(o.kth + (n * LT + t8) / 2) = uint4{kth[0], kth[1], kth[2], kth[3]};
-            *reinterpret_cast<uint4*>(o.ktl + (n * LT + t8) / 2) = uint4{ktl[0], ktl[1], ktl[2], ktl[3]};
         }
         if ((t8 + 8) % TPL == 0) after((t8 + 8) / TPL - 1);
     }
@@ -191,7 +180,7 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                                                                          float* saved_H) {
     using Cfg = FwdCfg<DK, DV>;
     constexpr int DVT = Cfg::DVT, NTILE = Cfg::NTILE, DCW = Cfg::DCW, NDT = Cfg::NDT, NSW = Cfg::NSW;
-    constexpr int SW = Cfg::SW, NRT = Cfg::NRT, KSN = Cfg::KSN, LQ = Cfg::LQ, LT = Cfg::LT;
+    constexpr int SW = Cfg::SW, NRT = Cfg::NRT, KSN = Cfg::KSN, LQ = Cfg::LQ;
     extern __shared__ __align__(16) unsigned char smem[];
 
     const uint16_t* q = static_cast<const uint16_t*>(g.q);
@@ -293,8 +282,6 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                 o.ql = reinterpret_cast<uint16_t*>(buf + Cfg::QL);
                 o.kh = reinterpret_cast<uint16_t*>(buf + Cfg::KH);
                 o.kl = reinterpret_cast<uint16_t*>(buf + Cfg::KL);
-                o.kth = reinterpret_cast<uint32_t*>(buf + Cfg::KTH);
-                o.ktl = reinterpret_cast<uint32_t*>(buf + Cfg::KTL);
                 o.yv = reinterpret_cast<float*>(buf + Cfg::YVP) + wave * kC;
                 // Group G starting block j is read while block j - 1 is processed (after
                 // the next chunk's blocks before j - 1 went out).  Younger than block j's
@@ -311,10 +298,9 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                 const uint32_t* rwc = rw + (c & 1) * 64;
                 float z = 1.f, A = 1.f;
                 if (nt == kC)
-                    scan_tokens<SW, Cfg::TPL, LQ, LT, YV, true>(stg, rwc, sl, nt, active, n, x, z, A, o, before, after);
+                    scan_tokens<SW, Cfg::TPL, LQ, YV, true>(stg, rwc, sl, nt, active, n, x, z, A, o, before, after);
                 else
-                    scan_tokens<SW, Cfg::TPL, LQ, LT, YV, false>(stg, rwc, sl, nt, active, n, x, z, A, o, before,
-                                                                after);
+                    scan_tokens<SW, Cfg::TPL, LQ, YV, false>(stg, rwc, sl, nt, active, n, x, z, A, o, before, after);
                 const float iz = fast_rcp(z);
                 x *= iz;   // lam at the chunk end
                 if (active) reinterpret_cast<float*>(buf + Cfg::DEC)[n] = A * iz;
@@ -329,7 +315,7 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
         // ================================================================ MFMA waves
         const int m = wave - NSW;
         const int dm0 = tile * DVT + m * DCW;   // first value channel of this wave
-        uint16_t* sVT = reinterpret_cast<uint16_t*>(smem + Cfg::VT) + m * DCW * LT;
+        const int dl0 = m * DCW;                // its first column within the value tile
 
         // state H[n, d] for n = 16 rt + 4 g4 + rr, d = dm0 + 16 dt + l16
         f32x4 Hs[NRT][NDT];
@@ -358,25 +344,13 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                 const int nt = min(kC, T - cc * kC);
                 const size_t row0 = seq0 + (size_t)cc * kC;
                 const unsigned char* buf = smem + (cc & 1) * Cfg::BUF;
-                // V^T [d][t] of this wave's channels (private to the wave) from the value tile
-                const uint16_t* sVS = reinterpret_cast<const uint16_t*>(buf + Cfg::VS);
-#pragma unroll
-                for (int i = 0; i < Cfg::VPL; ++i) {
-                    const int idx = lane + 64 * i;
-                    const int t = idx / (DCW / 8), c8 = idx % (DCW / 8);
-                    const uint4 x4 = *reinterpret_cast<const uint4*>(sVS + t * DVT + m * DCW + 8 * c8);
-                    const uint16_t* e = reinterpret_cast<const uint16_t*>(&x4);
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) sVT[(8 * c8 + j) * LT + t] = e[j];
-                }
+                const uint16_t* sVS = reinterpret_cast<const uint16_t*>(buf + Cfg::VS);   // V [t][DVT]
                 if (saved_H && cc % kSaveEvery == 0) save_state(cc / kSaveEvery);
 
                 const uint16_t* sQH = reinterpret_cast<const uint16_t*>(buf + Cfg::QH);
                 const uint16_t* sQL = reinterpret_cast<const uint16_t*>(buf + Cfg::QL);
                 const uint16_t* sKH = reinterpret_cast<const uint16_t*>(buf + Cfg::KH);
                 const uint16_t* sKL = reinterpret_cast<const uint16_t*>(buf + Cfg::KL);
-                const uint16_t* sKTH = reinterpret_cast<const uint16_t*>(buf + Cfg::KTH);
-                const uint16_t* sKTL = reinterpret_cast<const uint16_t*>(buf + Cfg::KTL);
                 const float* sDec = reinterpret_cast<const float*>(buf + Cfg::DEC);
 
                 // ---- S^T[j, i] = sum_n Kn[j, n] Qp[i, n], tiles (jt, it) = (0,0), (0,1), (1,1)
@@ -408,8 +382,7 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                 f32x4 yacc[NDT][2];
 #pragma unroll
                 for (int dt = 0; dt < NDT; ++dt) {
-                    const int vo = (16 * dt + l16) * LT + 4 * g4;
-                    const bf16x8 va = lds4x2(sVT + vo, sVT + vo + 16);
+                    const bf16x8 va = lds_tr8(sVS, DVT, 4 * g4, 16 + 4 * g4, dl0 + 16 * dt, l16);
 #pragma unroll
                     for (int it = 0; it < 2; ++it) yacc[dt][it] = mfma2b(va, sbh[it], sbl[it], zero4());
                 }
@@ -445,14 +418,18 @@ __global__ __launch_bounds__((FwdCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape
                 }
 
                 // ---- state: H <- diag(P_C) (H + Kn^T V)
+                bf16x8 vb[NDT];   // V rows t = 8 g4 .. 8 g4 + 7 of column d
+#pragma unroll
+                for (int dt = 0; dt < NDT; ++dt) vb[dt] = lds_tr8(sVS, DVT, 8 * g4, 8 * g4 + 4, dl0 + 16 * dt, l16);
 #pragma unroll
                 for (int rt = 0; rt < NRT; ++rt) {
-                    const int ko = (16 * rt + l16) * LT + 8 * g4;
-                    const bf16x8 kth = lds8(sKTH + ko), ktl = lds8(sKTL + ko);
+                    // Kn^T rows n = 16 rt + l16, tokens 8 g4 .. 8 g4 + 7
+                    const bf16x8 kth = lds_tr8(sKH, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
+                    const bf16x8 ktl = lds_tr8(sKL, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
                     const float4 dec = *reinterpret_cast<const float4*>(sDec + 16 * rt + 4 * g4);
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt) {
-                        const f32x4 hacc = mfma2a(kth, ktl, lds8(sVT + (16 * dt + l16) * LT + 8 * g4), Hs[rt][dt]);
+                        const f32x4 hacc = mfma2a(kth, ktl, vb[dt], Hs[rt][dt]);
                         Hs[rt][dt][0] = hacc[0] * dec.x;
                         Hs[rt][dt][1] = hacc[1] * dec.y;
                         Hs[rt][dt][2] = hacc[2] * dec.z;

@@ -65,6 +65,25 @@ __device__ __forceinline__ uint32_t pack2(uint16_t lo16, uint16_t hi16) {
     return static_cast<uint32_t>(lo16) | (static_cast<uint32_t>(hi16) << 16);
 }
 
+typedef __attribute__((__vector_size__(4 * sizeof(__bf16)))) __bf16 bf16x4;
+typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4_t;
+
+// MFMA operand read across the rows of a row-major bf16 LDS array X (row
+// stride ld halfwords) with ds_read_b64_tr_b16: lane l (s = l % 16) receives
+//   X[rowA + j][col0 + s] for j = 0..3 and X[rowB + j][col0 + s] for j = 0..3.
+// Within each group of 16 lanes the instruction hands lane i element i % 4 of
+// the 8 bytes addressed by lane 4 j + i / 4, so lane s addresses row
+// rowA + s / 4 (resp. rowB + s / 4) at column col0 + 4 (s % 4).  Rows and
+// columns may differ between the lane groups (rowA, rowB are per lane).
+// col0 and ld must be multiples of 4 (8-byte aligned addresses).
+__device__ __forceinline__ bf16x8 lds_tr8(const uint16_t* X, int ld, int rowA, int rowB, int col0, int s) {
+    const uint16_t* p0 = X + (rowA + (s >> 2)) * ld + col0 + 4 * (s & 3);
+    const uint16_t* p1 = X + (rowB + (s >> 2)) * ld + col0 + 4 * (s & 3);
+    const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)p0);
+    const bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)p1);
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
 // fp32 -> (hi, lo) bf16 pair
 __device__ __forceinline__ void split(float x, uint16_t& hi, uint16_t& lo) {
     hi = f32_to_bf16(x);
