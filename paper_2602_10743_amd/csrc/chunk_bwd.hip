@@ -18,8 +18,7 @@
 //   c_{t-1} = abar_t^2 rho_t^2 g_t - pbar_t rho_t dlogF_t,
 // from which the input gradients follow by the chain rule through rho, lam, F.
 //
-// Kernel B1: one workgroup per (b, h, 64 value channels); walks chunks in
-//   reverse keeping G[dk, 64] in registers; writes dv and (at the end) deta0.
+// (dv and deta0 come from the value-side kernel in chunk_bwd_dv.hip.)
 // Kernel B2: one workgroup per (b, h, 64 key slots); walks chunks in reverse
 //   keeping G^T[dv, 64] in registers; reads the saved chunk-start states H0;
 //   writes dq, dk, dabar, dpbar, partial dr sums over its key slots and dlam0.
@@ -41,192 +40,6 @@ __device__ __forceinline__ void xcd_map(int i, int nbh, int ntile, int& bh, int&
     } else {
         tile = i % ntile;
         bh = i / ntile;
-    }
-}
-
-// ============================================================================ B1
-template <int DK, int DV>
-struct B1Cfg {
-    static constexpr int DVT = DV < 64 ? DV : 64;
-    static constexpr int NTILE = DV / DVT;
-    static constexpr int NCT = DVT / 16;
-    static constexpr int NRT = DK / 16;
-    static constexpr int KSN = DK / 32;
-    static constexpr int NSCAN = DK < 64 ? 64 : DK;
-    static constexpr int LQ = DK + 8, LT = kC + 8;
-    static constexpr int QH = 0, QL = QH + kC * LQ, KH = QL + kC * LQ, KL = KH + kC * LQ;
-    static constexpr int QTH = KL + kC * LQ, QTL = QTH + DK * LT;
-    static constexpr int YT = QTL + DK * LT;
-    static constexpr int ATH = YT + DVT * LT, ATL = ATH + kC * LT;
-    static constexpr int END16 = ATL + kC * LT;
-    static constexpr int DECAY = (END16 + 7) / 8 * 4;
-    static constexpr size_t BYTES = (size_t)(DECAY + DK) * 4;
-    static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
-};
-
-template <int DK, int DV>
-__global__ __launch_bounds__(kThr) void bwd_b1_kernel(Shape s, BwdArgs g, const float* __restrict__ saved_lam) {
-    using Cfg = B1Cfg<DK, DV>;
-    constexpr int DVT = Cfg::DVT, NCT = Cfg::NCT, NRT = Cfg::NRT, KSN = Cfg::KSN, LQ = Cfg::LQ, LT = Cfg::LT;
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    uint16_t* sm = reinterpret_cast<uint16_t*>(smem_raw);
-    float* sDecay = reinterpret_cast<float*>(smem_raw) + Cfg::DECAY;
-
-    const uint16_t* q = static_cast<const uint16_t*>(g.q);
-    const uint16_t* k = static_cast<const uint16_t*>(g.k);
-    const uint16_t* a = static_cast<const uint16_t*>(g.a);
-    const uint16_t* p = static_cast<const uint16_t*>(g.p);
-    const uint16_t* r = static_cast<const uint16_t*>(g.r);
-    const uint16_t* dy = static_cast<const uint16_t*>(g.dy);
-    uint16_t* dv = static_cast<uint16_t*>(g.dv);
-
-    int bh, tile;
-    xcd_map(blockIdx.x, s.B * s.H, Cfg::NTILE, bh, tile);
-    const int b = bh / s.H, h = bh % s.H;
-    const int d0 = tile * DVT;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int l16 = lane & 15, g4 = lane >> 4;
-    const int T = s.T;
-    const int nchunk = (T + kC - 1) / kC;
-    const bool owns = wave < NCT;
-    const int dcol = d0 + 16 * wave + l16;
-    const bool scan_lane = tid < DK;
-    const int n_scan = scan_lane ? tid : DK - 1;
-
-    f32x4 G[NRT];
-#pragma unroll
-    for (int rt = 0; rt < NRT; ++rt)
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr)
-            G[rt][rr] = (owns && g.detaT) ? g.detaT[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dcol] : 0.f;
-
-    // the previous chunk's dY tile and first scan inputs are in flight during a chunk
-    TileStage<kC, DVT, kThr> ystage;
-    ScanPrefetch<8> spre;
-    if (nchunk > 0) {
-        const int cl = nchunk - 1;
-        const size_t r0 = (size_t)b * T + (size_t)cl * kC;
-        const int ntl = T - cl * kC;
-        ystage.load(dy, r0, s.H, h, DV, d0, ntl, tid);
-        if (tid < Cfg::NSCAN) scan_prefetch<8>(spre, a, p, k, q, r, r0, s.H, h, DK, n_scan, ntl);
-    }
-
-    for (int c = nchunk - 1; c >= 0; --c) {
-        const int t0 = c * kC;
-        const int nt = min(kC, T - t0);
-        const size_t row0 = (size_t)b * T + t0;
-
-        ystage.template store<0, LT, false, true>(nullptr, sm + Cfg::YT, tid);
-        if (c > 0) ystage.load(dy, row0 - kC, s.H, h, DV, d0, kC, tid);   // earlier chunks are full
-        if (tid < Cfg::NSCAN) {
-            float lam = saved_lam[((size_t)bh * nchunk + c) * DK + n_scan];
-            ScanLds L{};
-            L.qn_hi = sm + Cfg::QH;
-            L.qn_lo = sm + Cfg::QL;
-            L.kn_hi = sm + Cfg::KH;
-            L.kn_lo = sm + Cfg::KL;
-            L.qt_hi = sm + Cfg::QTH;
-            L.qt_lo = sm + Cfg::QTL;
-            const float P = scan_chunk<kC, LQ, LT, 0, true, true, true, false, false, 8>(
-                a, p, k, q, r, row0, s.H, h, DK, n_scan, n_scan, scan_lane, nt, lam, L, lane, spre);
-            if (scan_lane) sDecay[n_scan] = P;
-            if (c > 0) scan_prefetch<8>(spre, a, p, k, q, r, row0 - kC, s.H, h, DK, n_scan, kC);
-        }
-        __syncthreads();
-
-        // A^T[j, s] = sum_n Kn[j, n] Qp[s, n] for s >= j; tiles (1,0), (3,2) are the zeros
-        // read by the 32-deep K steps of dV.
-        for (int tk = wave; tk < 12; tk += 4) {
-            int jt, st;
-            if (tk < 10) {
-                jt = tk < 4 ? 0 : tk < 7 ? 1 : tk < 9 ? 2 : 3;
-                st = jt + (tk - (jt == 0 ? 0 : jt == 1 ? 4 : jt == 2 ? 7 : 9));
-            } else {
-                jt = tk == 10 ? 1 : 3;
-                st = jt - 1;
-            }
-            f32x4 acc = zero4();
-            if (tk < 10) {
-#pragma unroll
-                for (int ks = 0; ks < KSN; ++ks) {
-                    const int ko = (16 * jt + l16) * LQ + 32 * ks + 8 * g4;
-                    const int qo = (16 * st + l16) * LQ + 32 * ks + 8 * g4;
-                    acc = mfma3(lds8(sm + Cfg::KH + ko), lds8(sm + Cfg::KL + ko), lds8(sm + Cfg::QH + qo),
-                                lds8(sm + Cfg::QL + qo), acc);
-                }
-            }
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                const int j = 16 * jt + 4 * g4 + rr, sidx = 16 * st + l16;
-                const float x = (tk < 10 && sidx >= j) ? acc[rr] : 0.f;
-                uint16_t hi, lo;
-                split(x, hi, lo);
-                sm[Cfg::ATH + j * LT + sidx] = hi;
-                sm[Cfg::ATL + j * LT + sidx] = lo;
-            }
-        }
-        __syncthreads();
-
-        if (owns) {
-            const int ct = wave;
-            // G <- diag(P_C) G in place (Gs of the notation above)
-#pragma unroll
-            for (int rt = 0; rt < NRT; ++rt)
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) G[rt][rr] *= sDecay[16 * rt + 4 * g4 + rr];
-            // dV = M(A)^T dY + Kn Gs
-            f32x4 acc[4];
-#pragma unroll
-            for (int jt = 0; jt < 4; ++jt) acc[jt] = zero4();
-#pragma unroll
-            for (int jt = 0; jt < 4; ++jt) {
-#pragma unroll
-                for (int ks = jt >> 1; ks < 2; ++ks) {
-                    const int ao = (16 * jt + l16) * LT + 32 * ks + 8 * g4;
-                    const bf16x8 yb = lds8(sm + Cfg::YT + (16 * ct + l16) * LT + 32 * ks + 8 * g4);
-                    acc[jt] = mfma2a(lds8(sm + Cfg::ATH + ao), lds8(sm + Cfg::ATL + ao), yb, acc[jt]);
-                }
-            }
-#pragma unroll
-            for (int ks = 0; ks < KSN; ++ks) {
-                bf16x8 gh, gl;
-                split8(G[2 * ks], G[2 * ks + 1], gh, gl);
-#pragma unroll
-                for (int jt = 0; jt < 4; ++jt) {
-                    const int ko = (16 * jt + l16) * LQ + 32 * ks + 4 * g4;
-                    const bf16x8 kh = lds4x2(sm + Cfg::KH + ko, sm + Cfg::KH + ko + 16);
-                    const bf16x8 kl = lds4x2(sm + Cfg::KL + ko, sm + Cfg::KL + ko + 16);
-                    acc[jt] = mfma3(kh, kl, gh, gl, acc[jt]);
-                }
-            }
-#pragma unroll
-            for (int jt = 0; jt < 4; ++jt)
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {
-                    const int j = 16 * jt + 4 * g4 + rr;
-                    if (j < nt) dv[((row0 + j) * s.H + h) * DV + dcol] = f32_to_bf16(acc[jt][rr]);
-                }
-            // G <- Qp^T dY + Gs
-#pragma unroll
-            for (int rt = 0; rt < NRT; ++rt) {
-                f32x4 gacc = G[rt];
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    const int qo = (16 * rt + l16) * LT + 32 * ks + 8 * g4;
-                    const bf16x8 yb = lds8(sm + Cfg::YT + (16 * ct + l16) * LT + 32 * ks + 8 * g4);
-                    gacc = mfma2a(lds8(sm + Cfg::QTH + qo), lds8(sm + Cfg::QTL + qo), yb, gacc);
-                }
-                G[rt] = gacc;
-            }
-        }
-        __syncthreads();
-    }
-    if (g.deta0 && owns) {
-#pragma unroll
-        for (int rt = 0; rt < NRT; ++rt)
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr)
-                g.deta0[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dcol] = G[rt][rr];
     }
 }
 
@@ -285,6 +98,7 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
     const int l16 = lane & 15, g4 = lane >> 4;
     const int T = s.T;
     const int nchunk = (T + kC - 1) / kC;
+    const int nchunk32 = (T + 31) / 32;   // the saved lam is kept per 32-token chunk
     const size_t nbt = (size_t)s.B * T * s.H;
     const bool owns = wave < NCW;
     const int ncl = 16 * wave + l16;            // local key-slot column of this lane
@@ -312,7 +126,6 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
         }
     }
     const bool scan_lane = tid < NTN;
-    const int NSCAN = NTN < 64 ? 64 : NTN;
 
     // the previous chunk's dY / V tiles, first scan inputs and saved state rows are
     // in flight while a chunk is processed
@@ -341,7 +154,7 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
         const int t0 = c * kC;
         const int nt = min(kC, T - t0);
         const size_t row0 = (size_t)b * T + t0;
-        const float lam_start = saved_lam[((size_t)bh * nchunk + c) * DK + ng];
+        const float lam_start = saved_lam[((size_t)bh * nchunk32 + 2 * c) * DK + ng];
 
         ystage.template store<LD, LT, true, true>(sm + Cfg::DY, sm + Cfg::DYT, tid);
         vstage.template store<LD, 0, true, false>(sm + Cfg::V, nullptr, tid);
@@ -353,7 +166,7 @@ __global__ __launch_bounds__(kThr) void bwd_b2_kernel(Shape s, BwdArgs g, const 
 
         if (wave == 0) {
             // precision walk of this workgroup's key slots
-            float lam = saved_lam[((size_t)bh * nchunk + c) * DK + (scan_lane ? n0 + tid : n0)];
+            float lam = saved_lam[((size_t)bh * nchunk32 + 2 * c) * DK + (scan_lane ? n0 + tid : n0)];
             ScanLds L{};
             L.qt_hi = sm + Cfg::QTH;
             L.qt_lo = sm + Cfg::QTL;
@@ -629,18 +442,12 @@ __global__ void dr_combine_kernel(const float* __restrict__ part, int ntile, siz
 template <int DK, int DV>
 hipError_t launch_bwd(const Shape& s, const BwdArgs& a, const float* saved_lam, const float* saved_H, float* dr_part,
                       hipStream_t st) {
-    using C1 = B1Cfg<DK, DV>;
     using C2 = B2Cfg<DK, DV>;
-    auto k1 = bwd_b1_kernel<DK, DV>;
     auto k2 = bwd_b2_kernel<DK, DV>;
-    static const hipError_t e1 = hipFuncSetAttribute(reinterpret_cast<const void*>(k1),
-                                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)C1::BYTES);
     static const hipError_t e2 = hipFuncSetAttribute(reinterpret_cast<const void*>(k2),
                                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)C2::BYTES);
-    if (e1 != hipSuccess) return e1;
     if (e2 != hipSuccess) return e2;
-    hipLaunchKernelGGL(k1, dim3(s.B * s.H * C1::NTILE), dim3(kThr), C1::BYTES, st, s, a, saved_lam);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_backward_dv(s, a, saved_lam, st);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(k2, dim3(s.B * s.H * C2::NNT), dim3(kThr), C2::BYTES, st, s, a, saved_lam, saved_H, dr_part);
     e = hipGetLastError();
@@ -664,9 +471,9 @@ size_t chunked_bwd_workspace(const Shape& s) {
 }
 
 hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st) {
-    const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
+    const size_t nchunk32 = (size_t)(s.T + 31) / 32;
     const float* saved_lam = static_cast<const float*>(saved);
-    const float* saved_H = saved_lam + (size_t)s.B * s.H * nchunk * s.dk;
+    const float* saved_H = saved_lam + (size_t)s.B * s.H * nchunk32 * s.dk;
     float* dr_part = static_cast<float*>(ws);
 #define KLA_BWD_CASE(DK_, DV_) \
     if (s.dk == DK_ && s.dv == DV_) return launch_bwd<DK_, DV_>(s, a, saved_lam, saved_H, dr_part, st);

@@ -38,6 +38,11 @@ __device__ __forceinline__ void buf_ld16_lds(rsrc_t r, void* dst, uint32_t voff)
     __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)dst, 2, voff, 0, 0, 0);
 }
 
+// 4-byte variant: lane i's word lands at dst + 4 i.
+__device__ __forceinline__ void buf_ld32_lds(rsrc_t r, void* dst, uint32_t voff) {
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void_t*)dst, 4, voff, 0, 0, 0);
+}
+
 // s_waitcnt vmcnt(N): at most N vector memory accesses of this wave are still
 // outstanding (they complete in issue order).
 template <int N>

@@ -47,5 +47,7 @@ hipError_t launch_forward_chunked(const Shape& s, const FwdArgs& a, void* saved,
 bool chunked_bwd_supported(const Shape& s);
 size_t chunked_bwd_workspace(const Shape& s);
 hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st);
+// value side of the chunked backward (dv, deta0); saved_lam: lam at every 32-token chunk start
+hipError_t launch_backward_dv(const Shape& s, const BwdArgs& a, const float* saved_lam, hipStream_t st);
 
 }  // namespace kla
