@@ -1,0 +1,559 @@
+// Chunked backward, key side: dq, dk, dabar, dpbar, dr and dlam0.
+//
+// Notation per chunk of kC = 32 tokens (local t), with P_t, Qp, Kn from the
+// precision walk (kla_chunk.hpp) redone from the saved chunk-start lam:
+//   H_t  = P_t (H0 + sum_{j<=t} Kn_j v_j^T)          (state rows, H0 = saved chunk-start state)
+//   G    = adjoint of the chunk's last state from later tokens (detaT for the
+//          last chunk), Gs = diag(P_C) G
+//   B    = dY V^T                                    (kC x kC)
+// then, with M() keeping j <= t,
+//   X    = dY H0^T + M(B) Kn     dqt = P X   (gradient of qt = q / lam_t)
+//   Y    = M(B)^T Qp + V Gs^T    dkh = Y / P (gradient of kh = r k)
+//   G'   = Qp^T dY + Gs                          (carried into the previous chunk)
+// The adjoint of log F_t is the reverse running sum S_t of qt dqt - kh dkh (plus
+// the final-state term sum_d detaT H_T), and the adjoint c of lam follows
+//   g_t = c_t - q_t dqt_t / lam_t^2,    c_T = dlamT,
+//   c_{t-1} = abar_t^2 rho_t^2 g_t - pbar_t rho_t S_t,
+// from which the input gradients follow by the chain rule through rho, lam, F
+// (Theorem 1's update, differentiated by hand):
+//   dq = dqt / lam,  dk = r dkh + 2 k r g,  dr = sum_n (k dkh + k^2 g),
+//   drho = g lam_{t-1} + S / rho,  dabar = S / abar - 2 abar rho^2 drho,
+//   dpbar = -lam_{t-1} rho^2 drho,  dlam0 = c after the first token.
+//
+// One workgroup per (batch, head, 64 key slots) of NW waves; wave w owns the 16
+// key slots n0 + 16 w .. + 15 and does all of their work itself, sharing only
+// the dY / V tiles and nothing else:
+//   walk   lanes = (slot nl = lane % 16, quarter q = lane / 16 of 8 tokens):
+//          the chain (lam, z, prod abar) up to the quarter, then its 8 tokens,
+//          writing Qp and Kn ([t][16], split bf16) and keeping lam_t, P_t;
+//   MFMA   B, B^T, X^T and Y^T for its slots and G^T[dv, 16] in registers;
+//   adjoint per lane: its quarter's tokens in reverse, once to summarise the
+//          quarter as an affine map of the incoming (c, S), then -- the
+//          quarters chained through LDS -- once more for the gradients.
+// The chunks are walked last to first.  The next chunk's inputs go straight into
+// LDS, requested between the MFMA work and the adjoint walk of a round; the
+// chunk's saved state rows come into registers at the start of its round.
+#include "kla_chunk.hpp"
+#include "kla_internal.hpp"
+
+namespace kla {
+namespace {
+
+template <int DK, int DV>
+struct DkCfg {
+    static constexpr int NW = DK / 16 < 4 ? DK / 16 : 4;   // waves, 16 key slots each
+    static constexpr int NTN = 16 * NW;                     // key slots per workgroup
+    static constexpr int NNT = DK / NTN;                    // workgroups per (b, h)
+    static constexpr int NTHR = 64 * NW;
+    static constexpr int KSD = DV / 32;                     // 32-deep steps over the value channels
+    static constexpr int NRD = DV / 16;                     // 16-row tiles over the value channels
+    static constexpr int CPR = DV / 8;                      // 16-byte chunks per dY / V row
+    static constexpr int TPV = 512 / DV;                    // rows per 1 KiB load of a dY / V tile
+    static constexpr int NVL = kC / TPV;                    // 1 KiB loads per dY / V tile
+    static constexpr int LQ2 = 24;                          // row stride of per-wave [t][16] bf16 tiles
+    static constexpr int LX = 20;                           // row stride of per-wave [t][16] fp32 tiles
+    // shared: dY and V tiles [2 buffers][2][kC][DV] (16-byte chunks swizzled by row)
+    static constexpr int TILE = kC * DV * 2;
+    static constexpr int WAVE0 = 2 * 2 * TILE;
+    // per wave (offsets from the wave's base)
+    static constexpr int STG = 0;                                   // [2][4][kC][16] bf16: abar, pbar, k, q
+    static constexpr int RW = STG + 2 * 4 * kC * 16 * 2;            // [2][64] r words
+    static constexpr int LW = RW + 2 * 64 * 4;                      // [2][64] chunk-start lam (lanes < 16)
+    static constexpr int QH = LW + 2 * 64 * 4;                      // Qp, Kn split bf16 [kC][LQ2]
+    static constexpr int QL = QH + kC * LQ2 * 2, KH = QL + kC * LQ2 * 2, KL = KH + kC * LQ2 * 2;
+    static constexpr int XT = KL + kC * LQ2 * 2, YT = XT + kC * LX * 4;   // X, Y fp32 [kC][LX]
+    static constexpr int QS = YT + kC * LX * 4;                     // quarter maps [4][4][16] fp32
+    static constexpr int PC = QS + 4 * 4 * 16 * 4;                  // chunk decay P_C [16] fp32
+    static constexpr int WAVE = (PC + 16 * 4 + 15) / 16 * 16;
+    static constexpr int BYTES = WAVE0 + NW * WAVE;   // dynamic part
+    // The gradient tiles dq, dk, dabar, dpbar [4][kC][16] bf16 and the dr terms
+    // [kC][17] fp32 of each wave live in separate static arrays: they are read
+    // back while the next chunk's direct-to-LDS loads are in flight, and as
+    // distinct objects they are seen not to alias those loads' destinations.
+    static constexpr int STATIC = NW * (4 * kC * 16 * 2 + kC * 17 * 4);
+    static_assert(DK >= 32 && DK % 16 == 0 && DV >= 32 && DV % 32 == 0, "backward tile sizes");
+    static_assert(NVL >= 1 && TPV * CPR == 64, "value tile loads");
+    static_assert(BYTES + STATIC <= 160 * 1024, "LDS budget of one workgroup");
+};
+
+// Element (row t, column d) of a swizzled [kC][DV] bf16 tile: the 16-byte chunk
+// d / 8 of row t sits at chunk (d / 8) ^ (t % CPR), so that 16 consecutive rows
+// read at one column fall into distinct banks.
+template <int DV>
+__device__ __forceinline__ const uint16_t* swz(const uint16_t* tile, int t, int d) {
+    constexpr int CPR = DV / 8;
+    return tile + t * DV + ((((d >> 3) ^ (t % CPR)) << 3) | (d & 7));
+}
+
+template <int DV>
+__device__ __forceinline__ bf16x8 lds8_swz(const uint16_t* tile, int t, int d0) {
+    return lds8(swz<DV>(tile, t, d0));
+}
+
+template <int DV>
+__device__ __forceinline__ bf16x8 lds4x2_swz(const uint16_t* tile, int t, int d0, int d1) {
+    return lds4x2(swz<DV>(tile, t, d0), swz<DV>(tile, t, d1));
+}
+
+// lds_tr8 over a swizzled tile: lane s receives tile[rowA + j][col0 + s] and
+// tile[rowB + j][col0 + s], j = 0..3 (col0 a multiple of 16)
+template <int DV>
+__device__ __forceinline__ bf16x8 lds_tr8_swz(const uint16_t* tile, int rowA, int rowB, int col0, int s) {
+    const int col = col0 + 4 * (s & 3);
+    const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)swz<DV>(tile, rowA + (s >> 2), col));
+    const bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)swz<DV>(tile, rowB + (s >> 2), col));
+    return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+__device__ __forceinline__ void buf_st128(uint4 v, rsrc_t r, uint32_t voff) {
+    typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+    __builtin_amdgcn_raw_buffer_store_b128(u32x4{v.x, v.y, v.z, v.w}, r, voff, 0, 0);
+}
+
+__device__ __forceinline__ void buf_st32(float v, rsrc_t r, uint32_t voff) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, 0, 0);
+}
+
+template <int DK, int DV>
+__global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, BwdArgs g,
+                                                                       const float* __restrict__ saved_lam,
+                                                                       const float* __restrict__ saved_H,
+                                                                       float* __restrict__ dr_part) {
+    using Cfg = DkCfg<DK, DV>;
+    constexpr int NW = Cfg::NW, KSD = Cfg::KSD, NRD = Cfg::NRD, LQ2 = Cfg::LQ2, LX = Cfg::LX;
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ __align__(16) uint16_t s_out[NW * 4 * kC * 16];
+    __shared__ __align__(16) float s_drc[NW * kC * 17];
+
+    const uint16_t* a = static_cast<const uint16_t*>(g.a);
+    const uint16_t* p = static_cast<const uint16_t*>(g.p);
+    const uint16_t* k = static_cast<const uint16_t*>(g.k);
+    const uint16_t* q = static_cast<const uint16_t*>(g.q);
+    const uint16_t* r = static_cast<const uint16_t*>(g.r);
+    const uint16_t* vv = static_cast<const uint16_t*>(g.v);
+    const uint16_t* dy = static_cast<const uint16_t*>(g.dy);
+
+    int bh, ntile;
+    xcd_tile_map(blockIdx.x, s.B * s.H, Cfg::NNT, bh, ntile);
+    const int b = bh / s.H, h = bh % s.H;
+    const int H = s.H, T = s.T;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int l16 = lane & 15, g4 = lane >> 4;   // MFMA lane coordinates; for the walks: slot, quarter
+    const int nl = l16, qq = g4;
+    const int n0w = ntile * Cfg::NTN + 16 * wave;   // this wave's first key slot
+    const int nchunk = (T + kC - 1) / kC;
+    const size_t seq0 = (size_t)b * T;
+    const size_t nbt = (size_t)s.B * T * H;
+    unsigned char* wb = smem + Cfg::WAVE0 + wave * Cfg::WAVE;
+    const uint32_t tok_k = (uint32_t)H * DK * 2;   // bytes between tokens of a [.., H, DK] tensor
+    const uint32_t tok_v = (uint32_t)H * DV * 2;
+
+    // ---- carries of the reverse recursions (the 4 quarter lanes of a slot hold the same values)
+    float cT = g.dlamT ? g.dlamT[(size_t)bh * DK + n0w + nl] : 0.f;
+    float ST = 0.f;
+    if (g.detaT) {   // final-state term sum_d detaT H_T, split over the quarter lanes
+        const float* HT = saved_H + (((size_t)bh * (nchunk + 1) + nchunk) * DK + n0w + nl) * DV;
+        const float* dT = g.detaT + ((size_t)bh * DK + n0w + nl) * DV;
+        for (int d = qq * (DV / 4); d < (qq + 1) * (DV / 4); ++d) ST += dT[d] * HT[d];
+    }
+    ST += __shfl_xor(ST, 16, 64);
+    ST += __shfl_xor(ST, 32, 64);
+
+    // G^T[d, n] for d = 16 rd + 4 g4 + rr, n = n0w + l16
+    f32x4 GT[NRD];
+#pragma unroll
+    for (int rd = 0; rd < NRD; ++rd)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr)
+            GT[rd][rr] = g.detaT ? g.detaT[((size_t)bh * DK + n0w + l16) * DV + 16 * rd + 4 * g4 + rr] : 0.f;
+
+    // ---- requests of chunk cn into buffer bb (chunks outside the sequence: empty, writing zeros)
+    auto issue = [&](int cn, int bb) {
+        const bool in = cn >= 0 && cn < nchunk;
+        const int t0 = in ? cn * kC : 0, nt = in ? min(kC, T - t0) : 0;
+        const size_t tok0 = seq0 + t0;
+        // abar, pbar, k, q of this wave's slots: one 1 KiB load each, lane -> (t = lane / 2, 8 slots)
+        const uint32_t kbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + 16) * 2 : 0u;
+        const size_t ek = (tok0 * H + h) * DK + n0w;
+        const uint32_t koff = (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16;
+        uint16_t* stg = reinterpret_cast<uint16_t*>(wb + Cfg::STG) + bb * 4 * kC * 16;
+        buf_ld128_lds(make_rsrc(a + ek, kbytes), stg + 0 * kC * 16, koff);
+        buf_ld128_lds(make_rsrc(p + ek, kbytes), stg + 1 * kC * 16, koff);
+        buf_ld128_lds(make_rsrc(k + ek, kbytes), stg + 2 * kC * 16, koff);
+        buf_ld128_lds(make_rsrc(q + ek, kbytes), stg + 3 * kC * 16, koff);
+        // r (lanes >= nt read as 0) and the chunk-start lam of the 16 slots
+        const rsrc_t rr = make_rsrc(r + tok0 * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
+        buf_ld16_lds(rr, wb + Cfg::RW + bb * 256, (uint32_t)lane * H * 2);
+        const rsrc_t rl = make_rsrc(saved_lam + ((size_t)bh * nchunk + (in ? cn : 0)) * DK + n0w, in ? 64u : 0u);
+        buf_ld32_lds(rl, wb + Cfg::LW + bb * 256, (uint32_t)lane * 4);
+        // this wave's share of the dY and V tiles (loads i = wave, wave + NW, ...), swizzled
+        const uint32_t vbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DV + DV) * 2 : 0u;
+        const size_t ev = (tok0 * H + h) * DV;
+        const rsrc_t ry = make_rsrc(dy + ev, vbytes), rv = make_rsrc(vv + ev, vbytes);
+        unsigned char* tiles = smem + bb * 2 * Cfg::TILE;
+        for (int i = wave; i < Cfg::NVL; i += NW) {
+            const int row = i * Cfg::TPV + lane / Cfg::CPR, pch = lane % Cfg::CPR;
+            const uint32_t off = (uint32_t)row * tok_v + (uint32_t)((pch ^ (row % Cfg::CPR)) * 16);
+            buf_ld128_lds(ry, tiles + i * 1024, off);
+            buf_ld128_lds(rv, tiles + Cfg::TILE + i * 1024, off);
+        }
+    };
+    wait_vm_all();   // the carries and G^T are complete before the request stream starts
+    if (nchunk > 0) issue(nchunk - 1, 0);
+
+    for (int it = 0; it < nchunk; ++it) {
+        const int c = nchunk - 1 - it, bb = it & 1;
+        const int nt = min(kC, T - c * kC);
+        const size_t row0 = seq0 + (size_t)c * kC;
+
+        // saved chunk-start state rows H0[n0w + l16][32 ks + 8 g4 .. + 7], used by X below
+        float4 h0[KSD][2];
+        {
+            const float* H0 = saved_H + (((size_t)bh * (nchunk + 1) + c) * DK + n0w + l16) * DV;
+#pragma unroll
+            for (int ks = 0; ks < KSD; ++ks) {
+                h0[ks][0] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4);
+                h0[ks][1] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4 + 4);
+            }
+        }
+        // this chunk's requests (issued last round) have landed: younger are only the last
+        // round's 5 stores and the 2 KSD state loads just issued
+        if (it == 0)
+            wait_vm_le<2 * KSD>();
+        else
+            wait_vm_le<5 + 2 * KSD>();
+        barrier_lds();   // every wave's share of the dY / V tiles is in
+
+        const uint16_t* sDY = reinterpret_cast<const uint16_t*>(smem + bb * 2 * Cfg::TILE);
+        const uint16_t* sV = sDY + kC * DV;
+        const uint16_t* stg = reinterpret_cast<const uint16_t*>(wb + Cfg::STG) + bb * 4 * kC * 16;
+        const uint32_t* rw = reinterpret_cast<const uint32_t*>(wb + Cfg::RW) + bb * 64;
+        uint16_t* sQH = reinterpret_cast<uint16_t*>(wb + Cfg::QH);
+        uint16_t* sQL = reinterpret_cast<uint16_t*>(wb + Cfg::QL);
+        uint16_t* sKH = reinterpret_cast<uint16_t*>(wb + Cfg::KH);
+        uint16_t* sKL = reinterpret_cast<uint16_t*>(wb + Cfg::KL);
+        float* sX = reinterpret_cast<float*>(wb + Cfg::XT);
+        float* sY = reinterpret_cast<float*>(wb + Cfg::YT);
+        float* sPC = reinterpret_cast<float*>(wb + Cfg::PC);
+        auto in_a = [&](int t) { return __uint_as_float((uint32_t)stg[(0 * kC + t) * 16 + nl] << 16); };
+        auto in_p = [&](int t) { return __uint_as_float((uint32_t)stg[(1 * kC + t) * 16 + nl] << 16); };
+        auto in_k = [&](int t) { return __uint_as_float((uint32_t)stg[(2 * kC + t) * 16 + nl] << 16); };
+        auto in_q = [&](int t) { return __uint_as_float((uint32_t)stg[(3 * kC + t) * 16 + nl] << 16); };
+        auto in_r = [&](int t) { return __uint_as_float(rw[t] << 16); };
+
+        // ================================================================ precision walk
+        // chain (x, z, A) from the chunk start to this lane's quarter (t < 8 qq, t < nt)
+        float x = reinterpret_cast<const float*>(wb + Cfg::LW)[bb * 64 + nl], z = 1.f, A = 1.f;
+#pragma unroll
+        for (int t = 0; t < 24; ++t) {
+            const float av = in_a(t), pv = in_p(t), kv = in_k(t), rv = in_r(t);
+            const float zn = fmaf(pv, x, av * av * z);
+            const float xn = fmaf(kv * kv * rv, zn, x);
+            const bool ok = t < 8 * qq && t < nt;
+            x = ok ? xn : x;
+            z = ok ? zn : z;
+            A = ok ? A * av : A;
+        }
+        const float lamq = x * fast_rcp(z);   // lam before the quarter's first token
+        float lam_r[8], P_r[8];
+#pragma unroll
+        for (int j2 = 0; j2 < 4; ++j2) {
+            float qp2[2], kn2[2];
+#pragma unroll
+            for (int e = 0; e < 2; ++e) {
+                const int j = 2 * j2 + e, t = 8 * qq + j;
+                const float av = in_a(t), pv = in_p(t), kv = in_k(t), qv = in_q(t), rv = in_r(t);
+                const float kr = kv * rv;
+                const float zn = fmaf(pv, x, av * av * z);
+                const float xn = fmaf(kr * kv, zn, x);
+                const float An = A * av;
+                const float R = fast_rcp(xn * An);
+                const float iz = fast_rcp(zn);
+                const bool ok = t < nt;
+                qp2[e] = ok ? (qv * An) * (An * R) : 0.f;
+                kn2[e] = ok ? (kr * zn) * (xn * R) : 0.f;
+                lam_r[j] = xn * iz;
+                P_r[j] = An * iz;
+                x = ok ? xn : x;
+                z = ok ? zn : z;
+                A = ok ? An : A;
+            }
+            uint32_t qh, ql, kh, kl;
+            split2(qp2[0], qp2[1], qh, ql);
+            split2(kn2[0], kn2[1], kh, kl);
+            const int t = 8 * qq + 2 * j2;
+            sQH[t * LQ2 + nl] = static_cast<uint16_t>(qh);
+            sQH[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(qh >> 16);
+            sQL[t * LQ2 + nl] = static_cast<uint16_t>(ql);
+            sQL[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(ql >> 16);
+            sKH[t * LQ2 + nl] = static_cast<uint16_t>(kh);
+            sKH[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(kh >> 16);
+            sKL[t * LQ2 + nl] = static_cast<uint16_t>(kl);
+            sKL[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(kl >> 16);
+        }
+        if (qq == 3) sPC[nl] = A * fast_rcp(z);   // the last quarter ends at the chunk end
+
+        // ================================================================ MFMA
+        // B[t, j] = dY_t . V_j (j <= t) and B^T, tiles (0,0), (1,0), (1,1) / (0,0), (0,1), (1,1)
+        f32x4 B00 = zero4(), B10 = zero4(), B11 = zero4(), T00 = zero4(), T01 = zero4(), T11 = zero4();
+        bf16x8 ya[KSD][2];
+#pragma unroll
+        for (int ks = 0; ks < KSD; ++ks) {
+            ya[ks][0] = lds8_swz<DV>(sDY, l16, 32 * ks + 8 * g4);
+            ya[ks][1] = lds8_swz<DV>(sDY, 16 + l16, 32 * ks + 8 * g4);
+            const bf16x8 v0 = lds8_swz<DV>(sV, l16, 32 * ks + 8 * g4);
+            const bf16x8 v1 = lds8_swz<DV>(sV, 16 + l16, 32 * ks + 8 * g4);
+            B00 = mfma_bf16(ya[ks][0], v0, B00);
+            B10 = mfma_bf16(ya[ks][1], v0, B10);
+            B11 = mfma_bf16(ya[ks][1], v1, B11);
+            T00 = mfma_bf16(v0, ya[ks][0], T00);
+            T01 = mfma_bf16(v0, ya[ks][1], T01);
+            T11 = mfma_bf16(v1, ya[ks][1], T11);
+        }
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+            if (l16 > 4 * g4 + rr) {   // B: row t = 4 g4 + rr, column j = l16, keep j <= t
+                B00[rr] = 0.f;
+                B11[rr] = 0.f;
+            }
+            if (4 * g4 + rr > l16) {   // B^T: row j, column t = l16, keep j <= t
+                T00[rr] = 0.f;
+                T11[rr] = 0.f;
+            }
+        }
+        // B operands: over t for Y (column j), over j for X (column t); rows {4g..}, {16+4g..}
+        bf16x8 bbh[2], bbl[2], bth[2], btl[2];
+        split8(B00, B10, bbh[0], bbl[0]);
+        split8(zero4(), B11, bbh[1], bbl[1]);
+        split8(T00, zero4(), bth[0], btl[0]);
+        split8(T01, T11, bth[1], btl[1]);
+
+        // X^T[n, t] = sum_d H0[n, d] dY^T[d, t] + sum_j Kn^T[n, j] B^T[j, t]
+        f32x4 xacc[2] = {zero4(), zero4()};
+#pragma unroll
+        for (int ks = 0; ks < KSD; ++ks) {
+            bf16x8 hh, hl;
+            split8(f32x4{h0[ks][0].x, h0[ks][0].y, h0[ks][0].z, h0[ks][0].w},
+                   f32x4{h0[ks][1].x, h0[ks][1].y, h0[ks][1].z, h0[ks][1].w}, hh, hl);
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) xacc[tt] = mfma2a(hh, hl, ya[ks][tt], xacc[tt]);
+        }
+        {
+            const bf16x8 knh = lds_tr8(sKH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+            const bf16x8 knl = lds_tr8(sKL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) xacc[tt] = mfma3(knh, knl, bth[tt], btl[tt], xacc[tt]);
+        }
+        // Y^T[n, j] = sum_t Qp^T[n, t] B[t, j] + sum_d Gs[n, d] V^T[d, j]
+        f32x4 yacc[2];
+        {
+            const bf16x8 qth = lds_tr8(sQH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+            const bf16x8 qtl = lds_tr8(sQL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+#pragma unroll
+            for (int jt = 0; jt < 2; ++jt) yacc[jt] = mfma3(qth, qtl, bbh[jt], bbl[jt], zero4());
+        }
+        const float pcn = sPC[l16];
+#pragma unroll
+        for (int rd = 0; rd < NRD; ++rd)
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) GT[rd][rr] *= pcn;   // Gs^T in place
+#pragma unroll
+        for (int ks = 0; ks < KSD; ++ks) {
+            bf16x8 gh, gl;
+            split8(GT[2 * ks], GT[2 * ks + 1], gh, gl);
+#pragma unroll
+            for (int jt = 0; jt < 2; ++jt) {
+                const bf16x8 vb = lds4x2_swz<DV>(sV, 16 * jt + l16, 32 * ks + 4 * g4, 32 * ks + 16 + 4 * g4);
+                yacc[jt] = mfma2a(gh, gl, vb, yacc[jt]);
+            }
+        }
+        // G^T <- dY^T Qp + Gs^T
+        {
+            const bf16x8 qbh = lds_tr8(sQH, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
+            const bf16x8 qbl = lds_tr8(sQL, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
+#pragma unroll
+            for (int rd = 0; rd < NRD; ++rd) {
+                const bf16x8 yt = lds_tr8_swz<DV>(sDY, 8 * g4, 8 * g4 + 4, 16 * rd, l16);
+                GT[rd] = mfma2b(yt, qbh, qbl, GT[rd]);
+            }
+        }
+        // X and Y to [t][n] for the adjoint walk
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt) {
+            *reinterpret_cast<float4*>(sX + (16 * tt + l16) * LX + 4 * g4) =
+                float4{xacc[tt][0], xacc[tt][1], xacc[tt][2], xacc[tt][3]};
+            *reinterpret_cast<float4*>(sY + (16 * tt + l16) * LX + 4 * g4) =
+                float4{yacc[tt][0], yacc[tt][1], yacc[tt][2], yacc[tt][3]};
+        }
+
+        // the next chunk's requests go out only now: the transposing LDS reads above
+        // would otherwise wait for them
+        issue(c - 1, bb ^ 1);
+
+        // ================================================================ adjoint walk
+        // pass 1: the quarter's tokens in reverse; per token the affine step
+        //   (c, S) -> (alpha (c - w) - beta (S + u), S + u)
+        // composed into c_out = Am c_in + Bm S_in + Cm, S_out = S_in + Dm
+        float u_[8], w_[8], al_[8], be_[8], dq_[8], rdk_[8], kr2_[8], ia_[8], a2r2_[8], lp_[8], den_[8], lpr2_[8],
+            kdk_[8], kk_[8];
+        float Am = 1.f, Bm = 0.f, Cm = 0.f, Dm = 0.f;
+#pragma unroll
+        for (int j = 7; j >= 0; --j) {
+            const int t = 8 * qq + j;
+            const float av = in_a(t), pv = in_p(t), kv = in_k(t), qv = in_q(t), rv = in_r(t);
+            const float lam_t = lam_r[j], lam_p = j > 0 ? lam_r[j - 1] : lamq, Pt = P_r[j];
+            const float Xv = sX[t * LX + nl], Yv = sY[t * LX + nl];
+            const float den = fmaf(pv, lam_p, av * av);
+            const float rr3 = fast_rcp(den * lam_t * av);   // one reciprocal for 1/den, 1/lam, 1/abar
+            const float rho = lam_t * av * rr3, ilam = den * av * rr3, ia = den * lam_t * rr3;
+            const float dqt = Pt * Xv, dkh = Yv * fast_rcp(Pt);
+            const float kh = rv * kv;
+            const float qtd = qv * ilam * dqt;
+            const bool ok = t < nt;
+            const float u = ok ? qtd - kh * dkh : 0.f;
+            const float w = ok ? qtd * ilam : 0.f;
+            const float rho2 = rho * rho;
+            const float al = ok ? av * av * rho2 : 1.f;
+            const float be = ok ? pv * rho : 0.f;
+            u_[j] = u;
+            w_[j] = w;
+            al_[j] = al;
+            be_[j] = be;
+            dq_[j] = dqt * ilam;
+            rdk_[j] = rv * dkh;
+            kr2_[j] = 2.f * kh;
+            ia_[j] = ia;
+            a2r2_[j] = 2.f * av * rho2;
+            lp_[j] = lam_p;
+            den_[j] = den;
+            lpr2_[j] = lam_p * rho2;
+            kdk_[j] = kv * dkh;
+            kk_[j] = kv * kv;
+            Cm = al * Cm - be * Dm - (al * w + be * u);
+            Bm = al * Bm - be;
+            Am = al * Am;
+            Dm = Dm + u;
+        }
+        float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
+        qs[(qq * 4 + 0) * 16 + nl] = Am;
+        qs[(qq * 4 + 1) * 16 + nl] = Bm;
+        qs[(qq * 4 + 2) * 16 + nl] = Cm;
+        qs[(qq * 4 + 3) * 16 + nl] = Dm;
+        // carries into this quarter (through the later quarters) and out of the chunk
+        float c_in = 0.f, S_in = 0.f;
+#pragma unroll
+        for (int q2 = 3; q2 >= 0; --q2) {
+            if (q2 == qq) {
+                c_in = cT;
+                S_in = ST;
+            }
+            const float A2 = qs[(q2 * 4 + 0) * 16 + nl], B2 = qs[(q2 * 4 + 1) * 16 + nl];
+            const float C2 = qs[(q2 * 4 + 2) * 16 + nl], D2 = qs[(q2 * 4 + 3) * 16 + nl];
+            const float cn = fmaf(A2, cT, fmaf(B2, ST, C2));
+            ST += D2;
+            cT = cn;
+        }
+        // pass 2: gradients of the quarter's tokens
+        uint16_t* so = s_out + wave * 4 * kC * 16;
+        float* drc = s_drc + wave * kC * 17;
+        float cc = c_in, SS = S_in;
+#pragma unroll
+        for (int j = 7; j >= 0; --j) {
+            const int t = 8 * qq + j;
+            SS += u_[j];
+            const float gl = cc - w_[j];
+            const float dkv = fmaf(kr2_[j], gl, rdk_[j]);
+            const float drho = fmaf(gl, lp_[j], SS * den_[j]);
+            const float dav = fmaf(-a2r2_[j], drho, SS * ia_[j]);
+            const float dpv = -lpr2_[j] * drho;
+            drc[t * 17 + nl] = fmaf(kk_[j], gl, kdk_[j]);
+            cc = fmaf(al_[j], gl, -be_[j] * SS);
+            const uint32_t pq = cvt_pk_bf16(dq_[j], dkv), pa = cvt_pk_bf16(dav, dpv);
+            so[(0 * kC + t) * 16 + nl] = static_cast<uint16_t>(pq);
+            so[(1 * kC + t) * 16 + nl] = static_cast<uint16_t>(pq >> 16);
+            so[(2 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa);
+            so[(3 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa >> 16);
+        }
+
+        // ---- stores: [t][16] rows of dq, dk, dabar, dpbar (lane -> t = lane / 2, 8 slots),
+        // and this wave's dr partial over its 16 slots (lane -> t)
+        {
+            const uint32_t kbytes = (uint32_t)((nt - 1) * H * DK + 16) * 2;
+            const size_t ek = (row0 * H + h) * DK + n0w;
+            const uint32_t koff = (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16;
+            const uint16_t* o = so + (lane >> 1) * 16 + (lane & 1) * 8;
+            buf_st128(*reinterpret_cast<const uint4*>(o + 0 * kC * 16),
+                      make_rsrc(static_cast<uint16_t*>(g.dq) + ek, kbytes), koff);
+            buf_st128(*reinterpret_cast<const uint4*>(o + 1 * kC * 16),
+                      make_rsrc(static_cast<uint16_t*>(g.dk) + ek, kbytes), koff);
+            buf_st128(*reinterpret_cast<const uint4*>(o + 2 * kC * 16),
+                      make_rsrc(static_cast<uint16_t*>(g.da) + ek, kbytes), koff);
+            buf_st128(*reinterpret_cast<const uint4*>(o + 3 * kC * 16),
+                      make_rsrc(static_cast<uint16_t*>(g.dp) + ek, kbytes), koff);
+            const int t = lane & 31;
+            float acc = 0.f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc += drc[t * 17 + i];
+            float* dst = dr_part + (size_t)(ntile * NW + wave) * nbt + row0 * H + h;
+            buf_st32(acc, make_rsrc(dst, (uint32_t)((nt - 1) * H + 1) * 4), (uint32_t)lane * H * 4);   // lanes >= nt: dropped
+        }
+    }
+    wait_vm_all();   // the requests for the chunk before the first have landed before exit
+    if (g.dlam0 && qq == 0) g.dlam0[(size_t)bh * DK + n0w + nl] = cT;
+}
+
+// dr = sum of the per-wave partials, stored in the input dtype
+__global__ void dr_combine_kernel(const float* __restrict__ part, int nparts, size_t n, uint16_t* __restrict__ dr) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    float acc = 0.f;
+    for (int t = 0; t < nparts; ++t) acc += part[(size_t)t * n + i];
+    dr[i] = f32_to_bf16(acc);
+}
+
+template <int DK, int DV>
+hipError_t launch_dk(const Shape& s, const BwdArgs& a, const float* saved_lam, const float* saved_H, float* dr_part,
+                     hipStream_t st) {
+    using Cfg = DkCfg<DK, DV>;
+    auto kern = bwd_dk_kernel<DK, DV>;
+    static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                       hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::BYTES);
+    if (attr != hipSuccess) return attr;
+    hipError_t e = launch_backward_dv(s, a, saved_lam, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, dim3((unsigned)(s.B * s.H * Cfg::NNT)), dim3(Cfg::NTHR), Cfg::BYTES, st, s, a,
+                       saved_lam, saved_H, dr_part);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const size_t n = (size_t)s.B * s.T * s.H;
+    if (n > 0) {
+        hipLaunchKernelGGL(dr_combine_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, dr_part,
+                           Cfg::NNT * Cfg::NW, n, static_cast<uint16_t*>(a.dr));
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+}  // namespace
+
+bool chunked_bwd_supported(const Shape& s) { return s.bf16 && s.dk >= 32 && s.dv >= 32; }
+
+// per-wave dr partials: dk / 16 of them per token
+size_t chunked_bwd_workspace(const Shape& s) { return (size_t)(s.dk / 16) * s.B * s.T * s.H * sizeof(float); }
+
+hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st) {
+    const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
+    const float* saved_lam = static_cast<const float*>(saved);
+    const float* saved_H = saved_lam + (size_t)s.B * s.H * nchunk * s.dk;
+    float* dr_part = static_cast<float*>(ws);
+#define KLA_DK_CASE(DK_, DV_) \
+    if (s.dk == DK_ && s.dv == DV_) return launch_dk<DK_, DV_>(s, a, saved_lam, saved_H, dr_part, st);
+#define KLA_DK_ROW(DK_) KLA_DK_CASE(DK_, 32) KLA_DK_CASE(DK_, 64) KLA_DK_CASE(DK_, 128)
+    KLA_DK_ROW(32) KLA_DK_ROW(64) KLA_DK_ROW(128)
+#undef KLA_DK_ROW
+#undef KLA_DK_CASE
+    return hipErrorInvalidValue;
+}
+
+}  // namespace kla

@@ -22,7 +22,7 @@
 namespace kla {
 namespace {
 
-constexpr int kSaveEvery = 2;   // the saved states are those at every second chunk start (64 tokens)
+constexpr int kSaveEvery = 1;   // the saved states are those at every chunk start
 
 template <int DK, int DV, bool YV>
 __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape s, FwdArgs g, float* saved_lam,
@@ -230,9 +230,9 @@ hipError_t launch_fwd(const Shape& s, const FwdArgs& a, float* saved_lam, float*
 
 bool chunked_supported(const Shape& s) { return s.bf16 && s.dk >= 32; }
 
-// Saved context: lam at every 32-token chunk start [BH][nchunk][dk], then the
-// information state at every 64-token boundary and after the last token
-// [BH][nsave+1][dk][dv] (nsave = ceil(T / 64)).
+// Saved context: lam at every chunk start [BH][nchunk][dk], then the
+// information state at every chunk start and after the last token
+// [BH][nchunk+1][dk][dv].
 size_t chunked_saved_bytes(const Shape& s) {
     const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
     const size_t nsave = (size_t)(s.T + kC * kSaveEvery - 1) / (kC * kSaveEvery);
