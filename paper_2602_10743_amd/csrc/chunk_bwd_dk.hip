@@ -24,8 +24,11 @@
 // key slots n0 + 16 w .. + 15 and does all of their work itself, sharing only
 // the dY / V tiles and nothing else:
 //   walk   lanes = (slot nl = lane % 16, quarter q = lane / 16 of 8 tokens):
-//          the chain (lam, z, prod abar) up to the quarter, then its 8 tokens,
-//          writing Qp and Kn ([t][16], split bf16) and keeping lam_t, P_t;
+//          each lane first forms its quarter's transfer -- the 2x2 map of
+//          (x, z) of Theorem 1 over 8 tokens, with prod abar -- and the
+//          quarters are chained through LDS; then it walks its 8 tokens from
+//          the quarter start, writing Qp and Kn ([t][16], split bf16) and
+//          keeping lam_t, P_t and the reciprocals the adjoint walk needs;
 //   MFMA   B, B^T, X^T and Y^T for its slots and G^T[dv, 16] in registers;
 //   adjoint per lane: its quarter's tokens in reverse, once to summarise the
 //          quarter as an affine map of the incoming (c, S), then -- the
@@ -62,8 +65,8 @@ struct DkCfg {
     static constexpr int QH = LW + 2 * 64 * 4;                      // Qp, Kn split bf16 [kC][LQ2]
     static constexpr int QL = QH + kC * LQ2 * 2, KH = QL + kC * LQ2 * 2, KL = KH + kC * LQ2 * 2;
     static constexpr int XT = KL + kC * LQ2 * 2, YT = XT + kC * LX * 4;   // X, Y fp32 [kC][LX]
-    static constexpr int QS = YT + kC * LX * 4;                     // quarter maps [4][4][16] fp32
-    static constexpr int PC = QS + 4 * 4 * 16 * 4;                  // chunk decay P_C [16] fp32
+    static constexpr int QS = YT + kC * LX * 4;                     // quarter maps [4][5][16] fp32
+    static constexpr int PC = QS + 4 * 5 * 16 * 4;                  // chunk decay P_C [16] fp32
     static constexpr int WAVE = (PC + 16 * 4 + 15) / 16 * 16;
     static constexpr int BYTES = WAVE0 + NW * WAVE;   // dynamic part
     // The gradient tiles dq, dk, dabar, dpbar [4][kC][16] bf16 and the dr terms
@@ -243,20 +246,48 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
         auto in_r = [&](int t) { return __uint_as_float(rw[t] << 16); };
 
         // ================================================================ precision walk
-        // chain (x, z, A) from the chunk start to this lane's quarter (t < 8 qq, t < nt)
+        // transfer of this lane's quarter: (x, z) -> M (x, z) over its valid tokens, as the
+        // images of (1, 0) and (0, 1), and the product of abar
+        float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
+        {
+            float x0 = 1.f, z0 = 0.f, x1 = 0.f, z1 = 1.f, Aq = 1.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int t = 8 * qq + j;
+                const float av = in_a(t), pv = in_p(t), kv = in_k(t), rv = in_r(t);
+                const float a2 = av * av, phi = kv * kv * rv;
+                const float z0n = fmaf(pv, x0, a2 * z0), z1n = fmaf(pv, x1, a2 * z1);
+                const bool ok = t < nt;
+                x0 = ok ? fmaf(phi, z0n, x0) : x0;
+                x1 = ok ? fmaf(phi, z1n, x1) : x1;
+                z0 = ok ? z0n : z0;
+                z1 = ok ? z1n : z1;
+                Aq = ok ? Aq * av : Aq;
+            }
+            qs[(qq * 5 + 0) * 16 + nl] = x0;
+            qs[(qq * 5 + 1) * 16 + nl] = z0;
+            qs[(qq * 5 + 2) * 16 + nl] = x1;
+            qs[(qq * 5 + 3) * 16 + nl] = z1;
+            qs[(qq * 5 + 4) * 16 + nl] = Aq;
+        }
+        // chain the earlier quarters from the chunk start (x, z, A) = (lam, 1, 1)
         float x = reinterpret_cast<const float*>(wb + Cfg::LW)[bb * 64 + nl], z = 1.f, A = 1.f;
 #pragma unroll
-        for (int t = 0; t < 24; ++t) {
-            const float av = in_a(t), pv = in_p(t), kv = in_k(t), rv = in_r(t);
-            const float zn = fmaf(pv, x, av * av * z);
-            const float xn = fmaf(kv * kv * rv, zn, x);
-            const bool ok = t < 8 * qq && t < nt;
-            x = ok ? xn : x;
-            z = ok ? zn : z;
-            A = ok ? A * av : A;
+        for (int q2 = 0; q2 < 3; ++q2) {
+            const float m00 = qs[(q2 * 5 + 0) * 16 + nl], m10 = qs[(q2 * 5 + 1) * 16 + nl];
+            const float m01 = qs[(q2 * 5 + 2) * 16 + nl], m11 = qs[(q2 * 5 + 3) * 16 + nl];
+            const float aq = qs[(q2 * 5 + 4) * 16 + nl];
+            const bool use = q2 < qq;
+            const float xn = fmaf(m00, x, m01 * z), zn = fmaf(m10, x, m11 * z);
+            x = use ? xn : x;
+            z = use ? zn : z;
+            A = use ? A * aq : A;
         }
-        const float lamq = x * fast_rcp(z);   // lam before the quarter's first token
-        float lam_r[8], P_r[8];
+        float izp = fast_rcp(z);              // 1 / z before the quarter's first token
+        const float lamq = x * izp;           // lam before the quarter's first token
+        // per token of the quarter: lam_t, P_t and, for the adjoint walk, 1/P_t, 1/lam_t,
+        // rho_t, 1/rho_t = abar^2 + pbar lam_{t-1}, 1/abar
+        float lam_r[8], P_r[8], iP_r[8], il_r[8], rho_r[8], den_r[8], ia_r[8];
 #pragma unroll
         for (int j2 = 0; j2 < 4; ++j2) {
             float qp2[2], kn2[2];
@@ -270,11 +301,18 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 const float An = A * av;
                 const float R = fast_rcp(xn * An);
                 const float iz = fast_rcp(zn);
+                const float AR = An * R, XR = xn * R;   // 1 / x_t, 1 / A_t
                 const bool ok = t < nt;
-                qp2[e] = ok ? (qv * An) * (An * R) : 0.f;
-                kn2[e] = ok ? (kr * zn) * (xn * R) : 0.f;
+                qp2[e] = ok ? (qv * An) * AR : 0.f;
+                kn2[e] = ok ? (kr * zn) * XR : 0.f;
                 lam_r[j] = xn * iz;
                 P_r[j] = An * iz;
+                iP_r[j] = zn * XR;
+                il_r[j] = zn * AR;
+                rho_r[j] = z * iz;
+                den_r[j] = zn * izp;
+                ia_r[j] = A * XR;
+                izp = iz;
                 x = ok ? xn : x;
                 z = ok ? zn : z;
                 A = ok ? An : A;
@@ -402,12 +440,10 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
         for (int j = 7; j >= 0; --j) {
             const int t = 8 * qq + j;
             const float av = in_a(t), pv = in_p(t), kv = in_k(t), qv = in_q(t), rv = in_r(t);
-            const float lam_t = lam_r[j], lam_p = j > 0 ? lam_r[j - 1] : lamq, Pt = P_r[j];
+            const float lam_p = j > 0 ? lam_r[j - 1] : lamq;
             const float Xv = sX[t * LX + nl], Yv = sY[t * LX + nl];
-            const float den = fmaf(pv, lam_p, av * av);
-            const float rr3 = fast_rcp(den * lam_t * av);   // one reciprocal for 1/den, 1/lam, 1/abar
-            const float rho = lam_t * av * rr3, ilam = den * av * rr3, ia = den * lam_t * rr3;
-            const float dqt = Pt * Xv, dkh = Yv * fast_rcp(Pt);
+            const float rho = rho_r[j], ilam = il_r[j], ia = ia_r[j], den = den_r[j];
+            const float dqt = P_r[j] * Xv, dkh = Yv * iP_r[j];
             const float kh = rv * kv;
             const float qtd = qv * ilam * dqt;
             const bool ok = t < nt;
@@ -435,11 +471,10 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             Am = al * Am;
             Dm = Dm + u;
         }
-        float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
-        qs[(qq * 4 + 0) * 16 + nl] = Am;
-        qs[(qq * 4 + 1) * 16 + nl] = Bm;
-        qs[(qq * 4 + 2) * 16 + nl] = Cm;
-        qs[(qq * 4 + 3) * 16 + nl] = Dm;
+        qs[(qq * 5 + 0) * 16 + nl] = Am;
+        qs[(qq * 5 + 1) * 16 + nl] = Bm;
+        qs[(qq * 5 + 2) * 16 + nl] = Cm;
+        qs[(qq * 5 + 3) * 16 + nl] = Dm;
         // carries into this quarter (through the later quarters) and out of the chunk
         float c_in = 0.f, S_in = 0.f;
 #pragma unroll
@@ -448,8 +483,8 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 c_in = cT;
                 S_in = ST;
             }
-            const float A2 = qs[(q2 * 4 + 0) * 16 + nl], B2 = qs[(q2 * 4 + 1) * 16 + nl];
-            const float C2 = qs[(q2 * 4 + 2) * 16 + nl], D2 = qs[(q2 * 4 + 3) * 16 + nl];
+            const float A2 = qs[(q2 * 5 + 0) * 16 + nl], B2 = qs[(q2 * 5 + 1) * 16 + nl];
+            const float C2 = qs[(q2 * 5 + 2) * 16 + nl], D2 = qs[(q2 * 5 + 3) * 16 + nl];
             const float cn = fmaf(A2, cT, fmaf(B2, ST, C2));
             ST += D2;
             cT = cn;
