@@ -5,11 +5,14 @@ one batch of the language-model layer workload (B=8, H=16, T=2048,
 d_k=d_v=128, bf16 inputs with fp32 state), inputs already resident in HBM.
 The value is token-heads (B*T*H) per second.
 
-Besides the JSON line's throughput it reports, for the dominant kernel call,
-the achieved fraction of the HBM roofline from the algorithmic bytes per
-call and that call's average duration taken with HIP events on the stream it
-runs on, and the fp64 oracle's throughput on the host cores over a bounded
-sample of the same workload.
+Besides the JSON line's throughput it reports, for the dominant call (the
+backward: kernels bwd_dv, bwd_dk and dr_combine), the achieved fraction of
+the HBM roofline from the algorithmic bytes per call and that call's average
+duration taken with HIP events on the stream it runs on; the measured HBM
+traffic of that call when profiles/lm_layer_traffic.md was taken from the
+current kernel sources (see paper_2602_10743_amd/traffic.py); and the fp64
+oracle's throughput on the host cores over a bounded sample of the same
+workload.
 """
 import argparse
 import json
@@ -63,6 +66,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run a plain elementwise copy of known size first (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the filter layer shards over (batch, head) with no "
@@ -81,6 +86,14 @@ def main():
          for n in bits}
     del bits
     stream = torch.cuda.current_stream(dev)
+    if args.copy_calibration:
+        from paper_2602_10743_amd.traffic import COPY_BYTES
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step(ev=None):
         if ev is not None:
@@ -113,6 +126,9 @@ def main():
     else:
         dom, ms, nbytes = "kla_forward", fwd_ms, fwd_b * th
     achieved = nbytes / (ms * 1e-3) / 1e9
+    from paper_2602_10743_amd.traffic import load_summary
+    measured = load_summary(os.path.join(ROOT, "profiles", "lm_layer_traffic.md"))
+    traffic = measured.get(dom) if measured else None
     res = {
         "metric": METRIC,
         "value": th / (ms_per_step * 1e-3),
@@ -129,7 +145,8 @@ def main():
         "config": {"workload": w.name, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv,
                    "pass": "fwd+bwd", "tokens_counted": "B*T*H"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "traffic_unit": "bytes per call", "algorithmic_bytes_per_call": nbytes,
                      "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
                      "algorithmic_bytes_per_token_head": {"fwd": fwd_b, "bwd": bwd_b}},
     }

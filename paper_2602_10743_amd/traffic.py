@@ -1,0 +1,136 @@
+"""HBM traffic of the KLA calls from two rocprofv3 counter runs of bench.py.
+
+FETCH_SIZE and WRITE_SIZE (KiB per dispatch) are collected in separate runs,
+each over a bench run with --copy-calibration, which adds a plain elementwise
+copy of COPY_BYTES (read) + COPY_BYTES (written).  The counters of that copy
+kernel give the scale from counter units to bytes; the scaled counters of the
+kernels of one forward call and one backward call are the measured traffic.
+The summary records a digest of the kernel sources; bench.py reports the
+traffic only while the sources still match it.
+
+Run from the repository root on the GPU machine (TMPDIR=/tmp):
+  rocprofv3 --pmc FETCH_SIZE --output-format csv -d D/fetch -o run -- \\
+      python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration
+  rocprofv3 --pmc WRITE_SIZE --output-format csv -d D/write -o run -- \\
+      python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration
+  python -m paper_2602_10743_amd.traffic D/fetch D/write > profiles/lm_layer_traffic.md
+"""
+import csv
+import glob
+import hashlib
+import os
+import re
+import sys
+from collections import defaultdict
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+COPY_BYTES = 256 << 20
+CALLS = {
+    "kla_forward": ("fwd_chunk_kernel",),
+    "kla_backward": ("bwd_dv_kernel", "bwd_dk_kernel", "dr_combine_kernel"),
+}
+SUMMARY_KEY = "traffic_bytes_per_call"
+
+
+def sources_digest() -> str:
+    """sha256 over the kernel sources (csrc/*.hip, *.hpp, *.cpp) in name order."""
+    h = hashlib.sha256()
+    for path in sorted(glob.glob(os.path.join(HERE, "csrc", "*"))):
+        if path.endswith((".hip", ".hpp", ".cpp", ".h")):
+            h.update(os.path.basename(path).encode())
+            with open(path, "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def _short(name: str) -> str:
+    return re.sub(r"\(.*", "", name.replace("void ", "").replace("kla::(anonymous namespace)::", ""))
+
+
+def _counter(run_dir: str, counter: str) -> dict:
+    """kernel short name -> list of per-dispatch counter values."""
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {run_dir}")
+    vals = defaultdict(dict)
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            key = (r.get("Dispatch_Id") or r.get("Correlation_Id"), _short(r["Kernel_Name"]))
+            vals[key[1]][key[0]] = vals[key[1]].get(key[0], 0.0) + float(r["Counter_Value"])
+    return {k: list(v.values()) for k, v in vals.items()}
+
+
+def _per_call(vals: dict, scale: float) -> dict:
+    out = {}
+    for call, kernels in CALLS.items():
+        total = 0.0
+        for kname in kernels:
+            hits = [v for k, v in vals.items() if k.startswith(kname)]
+            if not hits:
+                raise KeyError(f"kernel {kname} not in the counter run")
+            seq = hits[0]
+            total += sum(seq) / len(seq) * scale
+        out[call] = total
+    return out
+
+
+def summarise(fetch_dir: str, write_dir: str) -> str:
+    fetch = _counter(fetch_dir, "FETCH_SIZE")
+    write = _counter(write_dir, "WRITE_SIZE")
+    kla_names = tuple(k for ks in CALLS.values() for k in ks)
+    copies = [k for k in fetch if not k.startswith(kla_names)]
+    if not copies:
+        raise KeyError("no calibration copy kernel in the fetch run")
+    copy = max(copies, key=lambda k: max(fetch[k]))
+    f_fetch = COPY_BYTES / max(fetch[copy])          # bytes per counter unit
+    f_write = COPY_BYTES / max(write[copy])
+    rd = _per_call(fetch, f_fetch)
+    wr = _per_call(write, f_write)
+    lines = [
+        "# HBM traffic per call, lm-layer workload (B=8, T=2048, H=16, d=128, bf16)",
+        "",
+        "Counters: FETCH_SIZE and WRITE_SIZE from two separate `rocprofv3 --pmc` runs of",
+        "`python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration`, scaled by",
+        f"the calibration copy kernel `{copy}` ({COPY_BYTES} bytes read and written):",
+        f"fetch scale {f_fetch:.4f} bytes/unit, write scale {f_write:.4f} bytes/unit.",
+        "",
+        "| call | read bytes | written bytes | total |",
+        "|---|---|---|---|",
+    ]
+    for call in CALLS:
+        lines.append(f"| {call} | {rd[call]:.4g} | {wr[call]:.4g} | {rd[call] + wr[call]:.4g} |")
+    lines += [
+        "",
+        f"sources: {sources_digest()}",
+        f"{SUMMARY_KEY}: " + ", ".join(f"{c}={rd[c] + wr[c]:.6g}" for c in CALLS),
+        "",
+    ]
+    return "\n".join(lines)
+
+
+def load_summary(path: str):
+    """{call: bytes} from a summary written by summarise(), or None when the file
+    is missing or was taken from different kernel sources."""
+    if not os.path.exists(path):
+        return None
+    digest, values = None, None
+    for line in open(path):
+        if line.startswith("sources: "):
+            digest = line.split(":", 1)[1].strip()
+        elif line.startswith(SUMMARY_KEY + ": "):
+            values = {}
+            for item in line.split(":", 1)[1].split(","):
+                k, v = item.strip().split("=")
+                values[k] = float(v)
+    if digest != sources_digest() or values is None:
+        return None
+    return values
+
+
+if __name__ == "__main__":
+    if len(sys.argv) != 3:
+        print(__doc__, file=sys.stderr)
+        sys.exit(2)
+    print(summarise(sys.argv[1], sys.argv[2]))
