@@ -34,8 +34,10 @@
 //          quarter as an affine map of the incoming (c, S), then -- the
 //          quarters chained through LDS -- once more for the gradients.
 // The chunks are walked last to first.  The next chunk's inputs go straight into
-// LDS, requested between the MFMA work and the adjoint walk of a round; the
-// chunk's saved state rows come into registers at the start of its round.
+// LDS, requested during the first pass of a round's adjoint walk; the chunk's
+// saved state rows come into registers at the start of its round.
+#include <type_traits>
+
 #include "kla_chunk.hpp"
 #include "kla_internal.hpp"
 
@@ -76,6 +78,7 @@ struct DkCfg {
     static constexpr int STATIC = NW * (4 * kC * 16 * 2 + kC * 17 * 4);
     static_assert(DK >= 32 && DK % 16 == 0 && DV >= 32 && DV % 32 == 0, "backward tile sizes");
     static_assert(NVL >= 1 && TPV * CPR == 64, "value tile loads");
+    static_assert(6 + 2 * ((NVL + NW - 1) / NW) <= 16, "requests spread over 8 tokens, two each");
     static_assert(BYTES + STATIC <= 160 * 1024, "LDS budget of one workgroup");
 };
 
@@ -171,39 +174,41 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
         for (int rr = 0; rr < 4; ++rr)
             GT[rd][rr] = g.detaT ? g.detaT[((size_t)bh * DK + n0w + l16) * DV + 16 * rd + 4 * g4 + rr] : 0.f;
 
-    // ---- requests of chunk cn into buffer bb (chunks outside the sequence: empty, writing zeros)
-    auto issue = [&](int cn, int bb) {
+    // ---- requests of chunk cn into buffer bb (chunks outside the sequence: empty, writing
+    // zeros), one load per part so that they can be spread over a round:
+    //   0..3  abar, pbar, k, q of this wave's slots (1 KiB each, lane -> (t = lane / 2, 8 slots))
+    //   4, 5  r (lanes >= nt read as 0) and the chunk-start lam of the 16 slots
+    //   6..   this wave's share of the dY and V tiles (loads i = wave, wave + NW, ...), swizzled
+    const int nvw = wave < Cfg::NVL ? (Cfg::NVL - wave + NW - 1) / NW : 0;
+    const int nparts = 6 + 2 * nvw;
+    auto issue_part = [&](int cn, int bb, int part) {
         const bool in = cn >= 0 && cn < nchunk;
         const int t0 = in ? cn * kC : 0, nt = in ? min(kC, T - t0) : 0;
         const size_t tok0 = seq0 + t0;
-        // abar, pbar, k, q of this wave's slots: one 1 KiB load each, lane -> (t = lane / 2, 8 slots)
-        const uint32_t kbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + 16) * 2 : 0u;
-        const size_t ek = (tok0 * H + h) * DK + n0w;
-        const uint32_t koff = (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16;
-        uint16_t* stg = reinterpret_cast<uint16_t*>(wb + Cfg::STG) + bb * 4 * kC * 16;
-        buf_ld128_lds(make_rsrc(a + ek, kbytes), stg + 0 * kC * 16, koff);
-        buf_ld128_lds(make_rsrc(p + ek, kbytes), stg + 1 * kC * 16, koff);
-        buf_ld128_lds(make_rsrc(k + ek, kbytes), stg + 2 * kC * 16, koff);
-        buf_ld128_lds(make_rsrc(q + ek, kbytes), stg + 3 * kC * 16, koff);
-        // r (lanes >= nt read as 0) and the chunk-start lam of the 16 slots
-        const rsrc_t rr = make_rsrc(r + tok0 * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
-        buf_ld16_lds(rr, wb + Cfg::RW + bb * 256, (uint32_t)lane * H * 2);
-        const rsrc_t rl = make_rsrc(saved_lam + ((size_t)bh * nchunk + (in ? cn : 0)) * DK + n0w, in ? 64u : 0u);
-        buf_ld32_lds(rl, wb + Cfg::LW + bb * 256, (uint32_t)lane * 4);
-        // this wave's share of the dY and V tiles (loads i = wave, wave + NW, ...), swizzled
-        const uint32_t vbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DV + DV) * 2 : 0u;
-        const size_t ev = (tok0 * H + h) * DV;
-        const rsrc_t ry = make_rsrc(dy + ev, vbytes), rv = make_rsrc(vv + ev, vbytes);
-        unsigned char* tiles = smem + bb * 2 * Cfg::TILE;
-        for (int i = wave; i < Cfg::NVL; i += NW) {
+        if (part < 4) {
+            const uint16_t* src = part == 0 ? a : part == 1 ? p : part == 2 ? k : q;
+            const uint32_t kbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + 16) * 2 : 0u;
+            uint16_t* stg = reinterpret_cast<uint16_t*>(wb + Cfg::STG) + (bb * 4 + part) * kC * 16;
+            buf_ld128_lds(make_rsrc(src + (tok0 * H + h) * DK + n0w, kbytes), stg,
+                          (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16);
+        } else if (part == 4) {
+            const rsrc_t rr = make_rsrc(r + tok0 * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
+            buf_ld16_lds(rr, wb + Cfg::RW + bb * 256, (uint32_t)lane * H * 2);
+        } else if (part == 5) {
+            const rsrc_t rl = make_rsrc(saved_lam + ((size_t)bh * nchunk + (in ? cn : 0)) * DK + n0w, in ? 64u : 0u);
+            buf_ld32_lds(rl, wb + Cfg::LW + bb * 256, (uint32_t)lane * 4);
+        } else if (part < nparts) {
+            const int m = (part - 6) >> 1, i = wave + NW * m;
+            const uint32_t vbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DV + DV) * 2 : 0u;
+            const rsrc_t rv = make_rsrc(((part - 6) & 1 ? vv : dy) + (tok0 * H + h) * DV, vbytes);
             const int row = i * Cfg::TPV + lane / Cfg::CPR, pch = lane % Cfg::CPR;
             const uint32_t off = (uint32_t)row * tok_v + (uint32_t)((pch ^ (row % Cfg::CPR)) * 16);
-            buf_ld128_lds(ry, tiles + i * 1024, off);
-            buf_ld128_lds(rv, tiles + Cfg::TILE + i * 1024, off);
+            buf_ld128_lds(rv, smem + (bb * 2 + ((part - 6) & 1)) * Cfg::TILE + i * 1024, off);
         }
     };
     wait_vm_all();   // the carries and G^T are complete before the request stream starts
-    if (nchunk > 0) issue(nchunk - 1, 0);
+    if (nchunk > 0)
+        for (int part = 0; part < nparts; ++part) issue_part(nchunk - 1, 0, part);
 
     for (int it = 0; it < nchunk; ++it) {
         const int c = nchunk - 1 - it, bb = it & 1;
@@ -228,311 +233,321 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             wait_vm_le<5 + 2 * KSD>();
         barrier_lds();   // every wave's share of the dY / V tiles is in
 
-        const uint16_t* sDY = reinterpret_cast<const uint16_t*>(smem + bb * 2 * Cfg::TILE);
-        const uint16_t* sV = sDY + kC * DV;
-        const uint16_t* stg = reinterpret_cast<const uint16_t*>(wb + Cfg::STG) + bb * 4 * kC * 16;
-        const uint32_t* rw = reinterpret_cast<const uint32_t*>(wb + Cfg::RW) + bb * 64;
-        uint16_t* sQH = reinterpret_cast<uint16_t*>(wb + Cfg::QH);
-        uint16_t* sQL = reinterpret_cast<uint16_t*>(wb + Cfg::QL);
-        uint16_t* sKH = reinterpret_cast<uint16_t*>(wb + Cfg::KH);
-        uint16_t* sKL = reinterpret_cast<uint16_t*>(wb + Cfg::KL);
-        float* sX = reinterpret_cast<float*>(wb + Cfg::XT);
-        float* sY = reinterpret_cast<float*>(wb + Cfg::YT);
-        float* sPC = reinterpret_cast<float*>(wb + Cfg::PC);
-        auto in_a = [&](int t) { return __uint_as_float((uint32_t)stg[(0 * kC + t) * 16 + nl] << 16); };
-        auto in_p = [&](int t) { return __uint_as_float((uint32_t)stg[(1 * kC + t) * 16 + nl] << 16); };
-        auto in_k = [&](int t) { return __uint_as_float((uint32_t)stg[(2 * kC + t) * 16 + nl] << 16); };
-        auto in_q = [&](int t) { return __uint_as_float((uint32_t)stg[(3 * kC + t) * 16 + nl] << 16); };
-        auto in_r = [&](int t) { return __uint_as_float(rw[t] << 16); };
+        // the round's work; FULL: all kC tokens valid (no per-token guards)
+        auto round_body = [&](auto full_tag) {
+            constexpr bool FULL = decltype(full_tag)::value;
+            const uint16_t* sDY = reinterpret_cast<const uint16_t*>(smem + bb * 2 * Cfg::TILE);
+            const uint16_t* sV = sDY + kC * DV;
+            const uint16_t* stg = reinterpret_cast<const uint16_t*>(wb + Cfg::STG) + bb * 4 * kC * 16;
+            const uint32_t* rw = reinterpret_cast<const uint32_t*>(wb + Cfg::RW) + bb * 64;
+            uint16_t* sQH = reinterpret_cast<uint16_t*>(wb + Cfg::QH);
+            uint16_t* sQL = reinterpret_cast<uint16_t*>(wb + Cfg::QL);
+            uint16_t* sKH = reinterpret_cast<uint16_t*>(wb + Cfg::KH);
+            uint16_t* sKL = reinterpret_cast<uint16_t*>(wb + Cfg::KL);
+            float* sX = reinterpret_cast<float*>(wb + Cfg::XT);
+            float* sY = reinterpret_cast<float*>(wb + Cfg::YT);
+            float* sPC = reinterpret_cast<float*>(wb + Cfg::PC);
+            auto in_a = [&](int t) { return __uint_as_float((uint32_t)stg[(0 * kC + t) * 16 + nl] << 16); };
+            auto in_p = [&](int t) { return __uint_as_float((uint32_t)stg[(1 * kC + t) * 16 + nl] << 16); };
+            auto in_k = [&](int t) { return __uint_as_float((uint32_t)stg[(2 * kC + t) * 16 + nl] << 16); };
+            auto in_q = [&](int t) { return __uint_as_float((uint32_t)stg[(3 * kC + t) * 16 + nl] << 16); };
+            auto in_r = [&](int t) { return __uint_as_float(rw[t] << 16); };
 
-        // ================================================================ precision walk
-        // transfer of this lane's quarter: (x, z) -> M (x, z) over its valid tokens, as the
-        // images of (1, 0) and (0, 1), and the product of abar
-        float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
-        {
-            float x0 = 1.f, z0 = 0.f, x1 = 0.f, z1 = 1.f, Aq = 1.f;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
+            // ================================================================ MFMA, part 1
+            // B[t, j] = dY_t . V_j (j <= t) and B^T, tiles (0,0), (1,0), (1,1) / (0,0), (0,1), (1,1)
+            f32x4 B00 = zero4(), B10 = zero4(), B11 = zero4(), T00 = zero4(), T01 = zero4(), T11 = zero4();
+    #pragma unroll
+            for (int ks = 0; ks < KSD; ++ks) {
+                const bf16x8 ya0 = lds8_swz<DV>(sDY, l16, 32 * ks + 8 * g4);
+                const bf16x8 ya1 = lds8_swz<DV>(sDY, 16 + l16, 32 * ks + 8 * g4);
+                const bf16x8 v0 = lds8_swz<DV>(sV, l16, 32 * ks + 8 * g4);
+                const bf16x8 v1 = lds8_swz<DV>(sV, 16 + l16, 32 * ks + 8 * g4);
+                B00 = mfma_bf16(ya0, v0, B00);
+                B10 = mfma_bf16(ya1, v0, B10);
+                B11 = mfma_bf16(ya1, v1, B11);
+                T00 = mfma_bf16(v0, ya0, T00);
+                T01 = mfma_bf16(v0, ya1, T01);
+                T11 = mfma_bf16(v1, ya1, T11);
+            }
+    #pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                if (l16 > 4 * g4 + rr) {   // B: row t = 4 g4 + rr, column j = l16, keep j <= t
+                    B00[rr] = 0.f;
+                    B11[rr] = 0.f;
+                }
+                if (4 * g4 + rr > l16) {   // B^T: row j, column t = l16, keep j <= t
+                    T00[rr] = 0.f;
+                    T11[rr] = 0.f;
+                }
+            }
+            // B operands: over t for Y (column j), over j for X (column t); rows {4g..}, {16+4g..}
+            bf16x8 bbh[2], bbl[2], bth[2], btl[2];
+            split8(B00, B10, bbh[0], bbl[0]);
+            split8(zero4(), B11, bbh[1], bbl[1]);
+            split8(T00, zero4(), bth[0], btl[0]);
+            split8(T01, T11, bth[1], btl[1]);
+
+            // ================================================================ precision walk
+            // transfer of this lane's quarter: (x, z) -> M (x, z) over its valid tokens, as the
+            // images of (1, 0) and (0, 1), and the product of abar
+            float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
+            {
+                float x0 = 1.f, z0 = 0.f, x1 = 0.f, z1 = 1.f, Aq = 1.f;
+    #pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int t = 8 * qq + j;
+                    const float av = in_a(t), pv = in_p(t), kv = in_k(t), rv = in_r(t);
+                    const float a2 = av * av, phi = kv * kv * rv;
+                    const float z0n = fmaf(pv, x0, a2 * z0), z1n = fmaf(pv, x1, a2 * z1);
+                    const bool ok = FULL || t < nt;
+                    x0 = ok ? fmaf(phi, z0n, x0) : x0;
+                    x1 = ok ? fmaf(phi, z1n, x1) : x1;
+                    z0 = ok ? z0n : z0;
+                    z1 = ok ? z1n : z1;
+                    Aq = ok ? Aq * av : Aq;
+                }
+                qs[(qq * 5 + 0) * 16 + nl] = x0;
+                qs[(qq * 5 + 1) * 16 + nl] = z0;
+                qs[(qq * 5 + 2) * 16 + nl] = x1;
+                qs[(qq * 5 + 3) * 16 + nl] = z1;
+                qs[(qq * 5 + 4) * 16 + nl] = Aq;
+            }
+            // chain the earlier quarters from the chunk start (x, z, A) = (lam, 1, 1)
+            float x = reinterpret_cast<const float*>(wb + Cfg::LW)[bb * 64 + nl], z = 1.f, A = 1.f;
+    #pragma unroll
+            for (int q2 = 0; q2 < 3; ++q2) {
+                const float m00 = qs[(q2 * 5 + 0) * 16 + nl], m10 = qs[(q2 * 5 + 1) * 16 + nl];
+                const float m01 = qs[(q2 * 5 + 2) * 16 + nl], m11 = qs[(q2 * 5 + 3) * 16 + nl];
+                const float aq = qs[(q2 * 5 + 4) * 16 + nl];
+                const bool use = q2 < qq;
+                const float xn = fmaf(m00, x, m01 * z), zn = fmaf(m10, x, m11 * z);
+                x = use ? xn : x;
+                z = use ? zn : z;
+                A = use ? A * aq : A;
+            }
+            float izp = fast_rcp(z);              // 1 / z before the quarter's first token
+            const float lamq = x * izp;           // lam before the quarter's first token
+            // per token of the quarter: lam_t, P_t and, for the adjoint walk, 1/P_t, 1/lam_t,
+            // rho_t, 1/rho_t = abar^2 + pbar lam_{t-1}, 1/abar
+            float lam_r[8], P_r[8], iP_r[8], il_r[8], rho_r[8], den_r[8], ia_r[8];
+    #pragma unroll
+            for (int j2 = 0; j2 < 4; ++j2) {
+                float qp2[2], kn2[2];
+    #pragma unroll
+                for (int e = 0; e < 2; ++e) {
+                    const int j = 2 * j2 + e, t = 8 * qq + j;
+                    const float av = in_a(t), pv = in_p(t), kv = in_k(t), qv = in_q(t), rv = in_r(t);
+                    const float kr = kv * rv;
+                    const float zn = fmaf(pv, x, av * av * z);
+                    const float xn = fmaf(kr * kv, zn, x);
+                    const float An = A * av;
+                    const float R = fast_rcp(xn * An);
+                    const float iz = fast_rcp(zn);
+                    const float AR = An * R, XR = xn * R;   // 1 / x_t, 1 / A_t
+                    const bool ok = FULL || t < nt;
+                    qp2[e] = ok ? (qv * An) * AR : 0.f;
+                    kn2[e] = ok ? (kr * zn) * XR : 0.f;
+                    lam_r[j] = xn * iz;
+                    P_r[j] = An * iz;
+                    iP_r[j] = zn * XR;
+                    il_r[j] = zn * AR;
+                    rho_r[j] = z * iz;
+                    den_r[j] = zn * izp;
+                    ia_r[j] = A * XR;
+                    izp = iz;
+                    x = ok ? xn : x;
+                    z = ok ? zn : z;
+                    A = ok ? An : A;
+                }
+                uint32_t qh, ql, kh, kl;
+                split2(qp2[0], qp2[1], qh, ql);
+                split2(kn2[0], kn2[1], kh, kl);
+                const int t = 8 * qq + 2 * j2;
+                sQH[t * LQ2 + nl] = static_cast<uint16_t>(qh);
+                sQH[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(qh >> 16);
+                sQL[t * LQ2 + nl] = static_cast<uint16_t>(ql);
+                sQL[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(ql >> 16);
+                sKH[t * LQ2 + nl] = static_cast<uint16_t>(kh);
+                sKH[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(kh >> 16);
+                sKL[t * LQ2 + nl] = static_cast<uint16_t>(kl);
+                sKL[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(kl >> 16);
+            }
+            if (qq == 3) sPC[nl] = A * fast_rcp(z);   // the last quarter ends at the chunk end
+
+            // ================================================================ MFMA, part 2
+            // X^T[n, t] = sum_d H0[n, d] dY^T[d, t] + sum_j Kn^T[n, j] B^T[j, t]
+            f32x4 xacc[2] = {zero4(), zero4()};
+    #pragma unroll
+            for (int ks = 0; ks < KSD; ++ks) {
+                bf16x8 hh, hl;
+                split8(f32x4{h0[ks][0].x, h0[ks][0].y, h0[ks][0].z, h0[ks][0].w},
+                       f32x4{h0[ks][1].x, h0[ks][1].y, h0[ks][1].z, h0[ks][1].w}, hh, hl);
+    #pragma unroll
+                for (int tt = 0; tt < 2; ++tt)
+                    xacc[tt] = mfma2a(hh, hl, lds8_swz<DV>(sDY, 16 * tt + l16, 32 * ks + 8 * g4), xacc[tt]);
+            }
+            {
+                const bf16x8 knh = lds_tr8(sKH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+                const bf16x8 knl = lds_tr8(sKL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+    #pragma unroll
+                for (int tt = 0; tt < 2; ++tt) xacc[tt] = mfma3(knh, knl, bth[tt], btl[tt], xacc[tt]);
+            }
+            // Y^T[n, j] = sum_t Qp^T[n, t] B[t, j] + sum_d Gs[n, d] V^T[d, j]
+            f32x4 yacc[2];
+            {
+                const bf16x8 qth = lds_tr8(sQH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+                const bf16x8 qtl = lds_tr8(sQL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+    #pragma unroll
+                for (int jt = 0; jt < 2; ++jt) yacc[jt] = mfma3(qth, qtl, bbh[jt], bbl[jt], zero4());
+            }
+            const float pcn = sPC[l16];
+    #pragma unroll
+            for (int rd = 0; rd < NRD; ++rd)
+    #pragma unroll
+                for (int rr = 0; rr < 4; ++rr) GT[rd][rr] *= pcn;   // Gs^T in place
+    #pragma unroll
+            for (int ks = 0; ks < KSD; ++ks) {
+                bf16x8 gh, gl;
+                split8(GT[2 * ks], GT[2 * ks + 1], gh, gl);
+    #pragma unroll
+                for (int jt = 0; jt < 2; ++jt) {
+                    const bf16x8 vb = lds4x2_swz<DV>(sV, 16 * jt + l16, 32 * ks + 4 * g4, 32 * ks + 16 + 4 * g4);
+                    yacc[jt] = mfma2a(gh, gl, vb, yacc[jt]);
+                }
+            }
+            // G^T <- dY^T Qp + Gs^T
+            {
+                const bf16x8 qbh = lds_tr8(sQH, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
+                const bf16x8 qbl = lds_tr8(sQL, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
+    #pragma unroll
+                for (int rd = 0; rd < NRD; ++rd) {
+                    const bf16x8 yt = lds_tr8_swz<DV>(sDY, 8 * g4, 8 * g4 + 4, 16 * rd, l16);
+                    GT[rd] = mfma2b(yt, qbh, qbl, GT[rd]);
+                }
+            }
+            // X and Y to [t][n] for the adjoint walk
+    #pragma unroll
+            for (int tt = 0; tt < 2; ++tt) {
+                *reinterpret_cast<float4*>(sX + (16 * tt + l16) * LX + 4 * g4) =
+                    float4{xacc[tt][0], xacc[tt][1], xacc[tt][2], xacc[tt][3]};
+                *reinterpret_cast<float4*>(sY + (16 * tt + l16) * LX + 4 * g4) =
+                    float4{yacc[tt][0], yacc[tt][1], yacc[tt][2], yacc[tt][3]};
+            }
+
+            // ================================================================ adjoint walk
+            // pass 1: the quarter's tokens in reverse; per token the affine step
+            //   (c, S) -> (alpha (c - w) - beta (S + u), S + u)
+            // composed into c_out = Am c_in + Bm S_in + Cm, S_out = S_in + Dm
+            float u_[8], w_[8], al_[8], be_[8], dq_[8], rdk_[8], kr2_[8], ia_[8], a2r2_[8], lp_[8], den_[8], lpr2_[8],
+                kdk_[8], kk_[8];
+            float Am = 1.f, Bm = 0.f, Cm = 0.f, Dm = 0.f;
+    #pragma unroll
+            for (int j = 7; j >= 0; --j) {
                 const int t = 8 * qq + j;
-                const float av = in_a(t), pv = in_p(t), kv = in_k(t), rv = in_r(t);
-                const float a2 = av * av, phi = kv * kv * rv;
-                const float z0n = fmaf(pv, x0, a2 * z0), z1n = fmaf(pv, x1, a2 * z1);
-                const bool ok = t < nt;
-                x0 = ok ? fmaf(phi, z0n, x0) : x0;
-                x1 = ok ? fmaf(phi, z1n, x1) : x1;
-                z0 = ok ? z0n : z0;
-                z1 = ok ? z1n : z1;
-                Aq = ok ? Aq * av : Aq;
-            }
-            qs[(qq * 5 + 0) * 16 + nl] = x0;
-            qs[(qq * 5 + 1) * 16 + nl] = z0;
-            qs[(qq * 5 + 2) * 16 + nl] = x1;
-            qs[(qq * 5 + 3) * 16 + nl] = z1;
-            qs[(qq * 5 + 4) * 16 + nl] = Aq;
-        }
-        // chain the earlier quarters from the chunk start (x, z, A) = (lam, 1, 1)
-        float x = reinterpret_cast<const float*>(wb + Cfg::LW)[bb * 64 + nl], z = 1.f, A = 1.f;
-#pragma unroll
-        for (int q2 = 0; q2 < 3; ++q2) {
-            const float m00 = qs[(q2 * 5 + 0) * 16 + nl], m10 = qs[(q2 * 5 + 1) * 16 + nl];
-            const float m01 = qs[(q2 * 5 + 2) * 16 + nl], m11 = qs[(q2 * 5 + 3) * 16 + nl];
-            const float aq = qs[(q2 * 5 + 4) * 16 + nl];
-            const bool use = q2 < qq;
-            const float xn = fmaf(m00, x, m01 * z), zn = fmaf(m10, x, m11 * z);
-            x = use ? xn : x;
-            z = use ? zn : z;
-            A = use ? A * aq : A;
-        }
-        float izp = fast_rcp(z);              // 1 / z before the quarter's first token
-        const float lamq = x * izp;           // lam before the quarter's first token
-        // per token of the quarter: lam_t, P_t and, for the adjoint walk, 1/P_t, 1/lam_t,
-        // rho_t, 1/rho_t = abar^2 + pbar lam_{t-1}, 1/abar
-        float lam_r[8], P_r[8], iP_r[8], il_r[8], rho_r[8], den_r[8], ia_r[8];
-#pragma unroll
-        for (int j2 = 0; j2 < 4; ++j2) {
-            float qp2[2], kn2[2];
-#pragma unroll
-            for (int e = 0; e < 2; ++e) {
-                const int j = 2 * j2 + e, t = 8 * qq + j;
                 const float av = in_a(t), pv = in_p(t), kv = in_k(t), qv = in_q(t), rv = in_r(t);
-                const float kr = kv * rv;
-                const float zn = fmaf(pv, x, av * av * z);
-                const float xn = fmaf(kr * kv, zn, x);
-                const float An = A * av;
-                const float R = fast_rcp(xn * An);
-                const float iz = fast_rcp(zn);
-                const float AR = An * R, XR = xn * R;   // 1 / x_t, 1 / A_t
-                const bool ok = t < nt;
-                qp2[e] = ok ? (qv * An) * AR : 0.f;
-                kn2[e] = ok ? (kr * zn) * XR : 0.f;
-                lam_r[j] = xn * iz;
-                P_r[j] = An * iz;
-                iP_r[j] = zn * XR;
-                il_r[j] = zn * AR;
-                rho_r[j] = z * iz;
-                den_r[j] = zn * izp;
-                ia_r[j] = A * XR;
-                izp = iz;
-                x = ok ? xn : x;
-                z = ok ? zn : z;
-                A = ok ? An : A;
+                const float lam_p = j > 0 ? lam_r[j - 1] : lamq;
+                const float Xv = sX[t * LX + nl], Yv = sY[t * LX + nl];
+                const float rho = rho_r[j], ilam = il_r[j], ia = ia_r[j], den = den_r[j];
+                const float dqt = P_r[j] * Xv, dkh = Yv * iP_r[j];
+                const float kh = rv * kv;
+                const float qtd = qv * ilam * dqt;
+                const bool ok = FULL || t < nt;
+                const float u = ok ? qtd - kh * dkh : 0.f;
+                const float w = ok ? qtd * ilam : 0.f;
+                const float rho2 = rho * rho;
+                const float al = ok ? av * av * rho2 : 1.f;
+                const float be = ok ? pv * rho : 0.f;
+                u_[j] = u;
+                w_[j] = w;
+                al_[j] = al;
+                be_[j] = be;
+                dq_[j] = dqt * ilam;
+                rdk_[j] = rv * dkh;
+                kr2_[j] = 2.f * kh;
+                ia_[j] = ia;
+                a2r2_[j] = 2.f * av * rho2;
+                lp_[j] = lam_p;
+                den_[j] = den;
+                lpr2_[j] = lam_p * rho2;
+                kdk_[j] = kv * dkh;
+                kk_[j] = kv * kv;
+                Cm = al * Cm - be * Dm - (al * w + be * u);
+                Bm = al * Bm - be;
+                Am = al * Am;
+                Dm = Dm + u;
+                // the next chunk's requests, two per token: they go out only after the
+                // transposing LDS reads above (which would otherwise wait for them) and are
+                // spread so that the loads of the four waves do not queue up at once
+                issue_part(c - 1, bb ^ 1, 2 * (7 - j));
+                issue_part(c - 1, bb ^ 1, 2 * (7 - j) + 1);
             }
-            uint32_t qh, ql, kh, kl;
-            split2(qp2[0], qp2[1], qh, ql);
-            split2(kn2[0], kn2[1], kh, kl);
-            const int t = 8 * qq + 2 * j2;
-            sQH[t * LQ2 + nl] = static_cast<uint16_t>(qh);
-            sQH[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(qh >> 16);
-            sQL[t * LQ2 + nl] = static_cast<uint16_t>(ql);
-            sQL[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(ql >> 16);
-            sKH[t * LQ2 + nl] = static_cast<uint16_t>(kh);
-            sKH[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(kh >> 16);
-            sKL[t * LQ2 + nl] = static_cast<uint16_t>(kl);
-            sKL[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(kl >> 16);
-        }
-        if (qq == 3) sPC[nl] = A * fast_rcp(z);   // the last quarter ends at the chunk end
+            qs[(qq * 5 + 0) * 16 + nl] = Am;
+            qs[(qq * 5 + 1) * 16 + nl] = Bm;
+            qs[(qq * 5 + 2) * 16 + nl] = Cm;
+            qs[(qq * 5 + 3) * 16 + nl] = Dm;
+            // carries into this quarter (through the later quarters) and out of the chunk
+            float c_in = 0.f, S_in = 0.f;
+    #pragma unroll
+            for (int q2 = 3; q2 >= 0; --q2) {
+                if (q2 == qq) {
+                    c_in = cT;
+                    S_in = ST;
+                }
+                const float A2 = qs[(q2 * 5 + 0) * 16 + nl], B2 = qs[(q2 * 5 + 1) * 16 + nl];
+                const float C2 = qs[(q2 * 5 + 2) * 16 + nl], D2 = qs[(q2 * 5 + 3) * 16 + nl];
+                const float cn = fmaf(A2, cT, fmaf(B2, ST, C2));
+                ST += D2;
+                cT = cn;
+            }
+            // pass 2: gradients of the quarter's tokens
+            uint16_t* so = s_out + wave * 4 * kC * 16;
+            float* drc = s_drc + wave * kC * 17;
+            float cc = c_in, SS = S_in;
+    #pragma unroll
+            for (int j = 7; j >= 0; --j) {
+                const int t = 8 * qq + j;
+                SS += u_[j];
+                const float gl = cc - w_[j];
+                const float dkv = fmaf(kr2_[j], gl, rdk_[j]);
+                const float drho = fmaf(gl, lp_[j], SS * den_[j]);
+                const float dav = fmaf(-a2r2_[j], drho, SS * ia_[j]);
+                const float dpv = -lpr2_[j] * drho;
+                drc[t * 17 + nl] = fmaf(kk_[j], gl, kdk_[j]);
+                cc = fmaf(al_[j], gl, -be_[j] * SS);
+                const uint32_t pq = cvt_pk_bf16(dq_[j], dkv), pa = cvt_pk_bf16(dav, dpv);
+                so[(0 * kC + t) * 16 + nl] = static_cast<uint16_t>(pq);
+                so[(1 * kC + t) * 16 + nl] = static_cast<uint16_t>(pq >> 16);
+                so[(2 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa);
+                so[(3 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa >> 16);
+            }
 
-        // ================================================================ MFMA
-        // B[t, j] = dY_t . V_j (j <= t) and B^T, tiles (0,0), (1,0), (1,1) / (0,0), (0,1), (1,1)
-        f32x4 B00 = zero4(), B10 = zero4(), B11 = zero4(), T00 = zero4(), T01 = zero4(), T11 = zero4();
-        bf16x8 ya[KSD][2];
-#pragma unroll
-        for (int ks = 0; ks < KSD; ++ks) {
-            ya[ks][0] = lds8_swz<DV>(sDY, l16, 32 * ks + 8 * g4);
-            ya[ks][1] = lds8_swz<DV>(sDY, 16 + l16, 32 * ks + 8 * g4);
-            const bf16x8 v0 = lds8_swz<DV>(sV, l16, 32 * ks + 8 * g4);
-            const bf16x8 v1 = lds8_swz<DV>(sV, 16 + l16, 32 * ks + 8 * g4);
-            B00 = mfma_bf16(ya[ks][0], v0, B00);
-            B10 = mfma_bf16(ya[ks][1], v0, B10);
-            B11 = mfma_bf16(ya[ks][1], v1, B11);
-            T00 = mfma_bf16(v0, ya[ks][0], T00);
-            T01 = mfma_bf16(v0, ya[ks][1], T01);
-            T11 = mfma_bf16(v1, ya[ks][1], T11);
-        }
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-            if (l16 > 4 * g4 + rr) {   // B: row t = 4 g4 + rr, column j = l16, keep j <= t
-                B00[rr] = 0.f;
-                B11[rr] = 0.f;
+            // ---- stores: [t][16] rows of dq, dk, dabar, dpbar (lane -> t = lane / 2, 8 slots),
+            // and this wave's dr partial over its 16 slots (lane -> t)
+            {
+                const uint32_t kbytes = (uint32_t)((nt - 1) * H * DK + 16) * 2;
+                const size_t ek = (row0 * H + h) * DK + n0w;
+                const uint32_t koff = (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16;
+                const uint16_t* o = so + (lane >> 1) * 16 + (lane & 1) * 8;
+                buf_st128(*reinterpret_cast<const uint4*>(o + 0 * kC * 16),
+                          make_rsrc(static_cast<uint16_t*>(g.dq) + ek, kbytes), koff);
+                buf_st128(*reinterpret_cast<const uint4*>(o + 1 * kC * 16),
+                          make_rsrc(static_cast<uint16_t*>(g.dk) + ek, kbytes), koff);
+                buf_st128(*reinterpret_cast<const uint4*>(o + 2 * kC * 16),
+                          make_rsrc(static_cast<uint16_t*>(g.da) + ek, kbytes), koff);
+                buf_st128(*reinterpret_cast<const uint4*>(o + 3 * kC * 16),
+                          make_rsrc(static_cast<uint16_t*>(g.dp) + ek, kbytes), koff);
+                const int t = lane & 31;
+                float acc = 0.f;
+    #pragma unroll
+                for (int i = 0; i < 16; ++i) acc += drc[t * 17 + i];
+                float* dst = dr_part + (size_t)(ntile * NW + wave) * nbt + row0 * H + h;
+                buf_st32(acc, make_rsrc(dst, (uint32_t)((nt - 1) * H + 1) * 4), (uint32_t)lane * H * 4);   // lanes >= nt: dropped
             }
-            if (4 * g4 + rr > l16) {   // B^T: row j, column t = l16, keep j <= t
-                T00[rr] = 0.f;
-                T11[rr] = 0.f;
-            }
-        }
-        // B operands: over t for Y (column j), over j for X (column t); rows {4g..}, {16+4g..}
-        bf16x8 bbh[2], bbl[2], bth[2], btl[2];
-        split8(B00, B10, bbh[0], bbl[0]);
-        split8(zero4(), B11, bbh[1], bbl[1]);
-        split8(T00, zero4(), bth[0], btl[0]);
-        split8(T01, T11, bth[1], btl[1]);
-
-        // X^T[n, t] = sum_d H0[n, d] dY^T[d, t] + sum_j Kn^T[n, j] B^T[j, t]
-        f32x4 xacc[2] = {zero4(), zero4()};
-#pragma unroll
-        for (int ks = 0; ks < KSD; ++ks) {
-            bf16x8 hh, hl;
-            split8(f32x4{h0[ks][0].x, h0[ks][0].y, h0[ks][0].z, h0[ks][0].w},
-                   f32x4{h0[ks][1].x, h0[ks][1].y, h0[ks][1].z, h0[ks][1].w}, hh, hl);
-#pragma unroll
-            for (int tt = 0; tt < 2; ++tt) xacc[tt] = mfma2a(hh, hl, ya[ks][tt], xacc[tt]);
-        }
-        {
-            const bf16x8 knh = lds_tr8(sKH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
-            const bf16x8 knl = lds_tr8(sKL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
-#pragma unroll
-            for (int tt = 0; tt < 2; ++tt) xacc[tt] = mfma3(knh, knl, bth[tt], btl[tt], xacc[tt]);
-        }
-        // Y^T[n, j] = sum_t Qp^T[n, t] B[t, j] + sum_d Gs[n, d] V^T[d, j]
-        f32x4 yacc[2];
-        {
-            const bf16x8 qth = lds_tr8(sQH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
-            const bf16x8 qtl = lds_tr8(sQL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
-#pragma unroll
-            for (int jt = 0; jt < 2; ++jt) yacc[jt] = mfma3(qth, qtl, bbh[jt], bbl[jt], zero4());
-        }
-        const float pcn = sPC[l16];
-#pragma unroll
-        for (int rd = 0; rd < NRD; ++rd)
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr) GT[rd][rr] *= pcn;   // Gs^T in place
-#pragma unroll
-        for (int ks = 0; ks < KSD; ++ks) {
-            bf16x8 gh, gl;
-            split8(GT[2 * ks], GT[2 * ks + 1], gh, gl);
-#pragma unroll
-            for (int jt = 0; jt < 2; ++jt) {
-                const bf16x8 vb = lds4x2_swz<DV>(sV, 16 * jt + l16, 32 * ks + 4 * g4, 32 * ks + 16 + 4 * g4);
-                yacc[jt] = mfma2a(gh, gl, vb, yacc[jt]);
-            }
-        }
-        // G^T <- dY^T Qp + Gs^T
-        {
-            const bf16x8 qbh = lds_tr8(sQH, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
-            const bf16x8 qbl = lds_tr8(sQL, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
-#pragma unroll
-            for (int rd = 0; rd < NRD; ++rd) {
-                const bf16x8 yt = lds_tr8_swz<DV>(sDY, 8 * g4, 8 * g4 + 4, 16 * rd, l16);
-                GT[rd] = mfma2b(yt, qbh, qbl, GT[rd]);
-            }
-        }
-        // X and Y to [t][n] for the adjoint walk
-#pragma unroll
-        for (int tt = 0; tt < 2; ++tt) {
-            *reinterpret_cast<float4*>(sX + (16 * tt + l16) * LX + 4 * g4) =
-                float4{xacc[tt][0], xacc[tt][1], xacc[tt][2], xacc[tt][3]};
-            *reinterpret_cast<float4*>(sY + (16 * tt + l16) * LX + 4 * g4) =
-                float4{yacc[tt][0], yacc[tt][1], yacc[tt][2], yacc[tt][3]};
-        }
-
-        // the next chunk's requests go out only now: the transposing LDS reads above
-        // would otherwise wait for them
-        issue(c - 1, bb ^ 1);
-
-        // ================================================================ adjoint walk
-        // pass 1: the quarter's tokens in reverse; per token the affine step
-        //   (c, S) -> (alpha (c - w) - beta (S + u), S + u)
-        // composed into c_out = Am c_in + Bm S_in + Cm, S_out = S_in + Dm
-        float u_[8], w_[8], al_[8], be_[8], dq_[8], rdk_[8], kr2_[8], ia_[8], a2r2_[8], lp_[8], den_[8], lpr2_[8],
-            kdk_[8], kk_[8];
-        float Am = 1.f, Bm = 0.f, Cm = 0.f, Dm = 0.f;
-#pragma unroll
-        for (int j = 7; j >= 0; --j) {
-            const int t = 8 * qq + j;
-            const float av = in_a(t), pv = in_p(t), kv = in_k(t), qv = in_q(t), rv = in_r(t);
-            const float lam_p = j > 0 ? lam_r[j - 1] : lamq;
-            const float Xv = sX[t * LX + nl], Yv = sY[t * LX + nl];
-            const float rho = rho_r[j], ilam = il_r[j], ia = ia_r[j], den = den_r[j];
-            const float dqt = P_r[j] * Xv, dkh = Yv * iP_r[j];
-            const float kh = rv * kv;
-            const float qtd = qv * ilam * dqt;
-            const bool ok = t < nt;
-            const float u = ok ? qtd - kh * dkh : 0.f;
-            const float w = ok ? qtd * ilam : 0.f;
-            const float rho2 = rho * rho;
-            const float al = ok ? av * av * rho2 : 1.f;
-            const float be = ok ? pv * rho : 0.f;
-            u_[j] = u;
-            w_[j] = w;
-            al_[j] = al;
-            be_[j] = be;
-            dq_[j] = dqt * ilam;
-            rdk_[j] = rv * dkh;
-            kr2_[j] = 2.f * kh;
-            ia_[j] = ia;
-            a2r2_[j] = 2.f * av * rho2;
-            lp_[j] = lam_p;
-            den_[j] = den;
-            lpr2_[j] = lam_p * rho2;
-            kdk_[j] = kv * dkh;
-            kk_[j] = kv * kv;
-            Cm = al * Cm - be * Dm - (al * w + be * u);
-            Bm = al * Bm - be;
-            Am = al * Am;
-            Dm = Dm + u;
-        }
-        qs[(qq * 5 + 0) * 16 + nl] = Am;
-        qs[(qq * 5 + 1) * 16 + nl] = Bm;
-        qs[(qq * 5 + 2) * 16 + nl] = Cm;
-        qs[(qq * 5 + 3) * 16 + nl] = Dm;
-        // carries into this quarter (through the later quarters) and out of the chunk
-        float c_in = 0.f, S_in = 0.f;
-#pragma unroll
-        for (int q2 = 3; q2 >= 0; --q2) {
-            if (q2 == qq) {
-                c_in = cT;
-                S_in = ST;
-            }
-            const float A2 = qs[(q2 * 5 + 0) * 16 + nl], B2 = qs[(q2 * 5 + 1) * 16 + nl];
-            const float C2 = qs[(q2 * 5 + 2) * 16 + nl], D2 = qs[(q2 * 5 + 3) * 16 + nl];
-            const float cn = fmaf(A2, cT, fmaf(B2, ST, C2));
-            ST += D2;
-            cT = cn;
-        }
-        // pass 2: gradients of the quarter's tokens
-        uint16_t* so = s_out + wave * 4 * kC * 16;
-        float* drc = s_drc + wave * kC * 17;
-        float cc = c_in, SS = S_in;
-#pragma unroll
-        for (int j = 7; j >= 0; --j) {
-            const int t = 8 * qq + j;
-            SS += u_[j];
-            const float gl = cc - w_[j];
-            const float dkv = fmaf(kr2_[j], gl, rdk_[j]);
-            const float drho = fmaf(gl, lp_[j], SS * den_[j]);
-            const float dav = fmaf(-a2r2_[j], drho, SS * ia_[j]);
-            const float dpv = -lpr2_[j] * drho;
-            drc[t * 17 + nl] = fmaf(kk_[j], gl, kdk_[j]);
-            cc = fmaf(al_[j], gl, -be_[j] * SS);
-            const uint32_t pq = cvt_pk_bf16(dq_[j], dkv), pa = cvt_pk_bf16(dav, dpv);
-            so[(0 * kC + t) * 16 + nl] = static_cast<uint16_t>(pq);
-            so[(1 * kC + t) * 16 + nl] = static_cast<uint16_t>(pq >> 16);
-            so[(2 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa);
-            so[(3 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa >> 16);
-        }
-
-        // ---- stores: [t][16] rows of dq, dk, dabar, dpbar (lane -> t = lane / 2, 8 slots),
-        // and this wave's dr partial over its 16 slots (lane -> t)
-        {
-            const uint32_t kbytes = (uint32_t)((nt - 1) * H * DK + 16) * 2;
-            const size_t ek = (row0 * H + h) * DK + n0w;
-            const uint32_t koff = (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16;
-            const uint16_t* o = so + (lane >> 1) * 16 + (lane & 1) * 8;
-            buf_st128(*reinterpret_cast<const uint4*>(o + 0 * kC * 16),
-                      make_rsrc(static_cast<uint16_t*>(g.dq) + ek, kbytes), koff);
-            buf_st128(*reinterpret_cast<const uint4*>(o + 1 * kC * 16),
-                      make_rsrc(static_cast<uint16_t*>(g.dk) + ek, kbytes), koff);
-            buf_st128(*reinterpret_cast<const uint4*>(o + 2 * kC * 16),
-                      make_rsrc(static_cast<uint16_t*>(g.da) + ek, kbytes), koff);
-            buf_st128(*reinterpret_cast<const uint4*>(o + 3 * kC * 16),
-                      make_rsrc(static_cast<uint16_t*>(g.dp) + ek, kbytes), koff);
-            const int t = lane & 31;
-            float acc = 0.f;
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc += drc[t * 17 + i];
-            float* dst = dr_part + (size_t)(ntile * NW + wave) * nbt + row0 * H + h;
-            buf_st32(acc, make_rsrc(dst, (uint32_t)((nt - 1) * H + 1) * 4), (uint32_t)lane * H * 4);   // lanes >= nt: dropped
-        }
+        };
+        if (nt == kC)
+            round_body(std::true_type{});
+        else
+            round_body(std::false_type{});
     }
     wait_vm_all();   // the requests for the chunk before the first have landed before exit
     if (g.dlam0 && qq == 0) g.dlam0[(size_t)bh * DK + n0w + nl] = cT;
