@@ -22,8 +22,6 @@
 namespace kla {
 namespace {
 
-constexpr int kSaveEvery = 1;   // the saved states are those at every chunk start
-
 template <int DK, int DV, bool YV>
 __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape s, FwdArgs g, float* saved_lam,
                                                                          float* saved_H) {
@@ -48,7 +46,6 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform role
     const int l16 = lane & 15, g4 = lane >> 4;
     const int nchunk = (T + kC - 1) / kC;
-    const int nsave = (T + kC * kSaveEvery - 1) / (kC * kSaveEvery);
     const size_t seq0 = (size_t)b * T;   // token index of this sequence's first token
 
     if (wave < NSW) {
@@ -73,15 +70,14 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
                     Hs[rt][dt][rr] =
                         g.eta0 ? g.eta0[((size_t)bh * DK + 16 * rt + 4 * g4 + rr) * DV + dm0 + 16 * dt + l16] : 0.f;
 
-        auto save_state = [&](int slot) {
-            float* dst = saved_H + ((size_t)bh * (nsave + 1) + slot) * DK * DV;
+        // state rows 16 rt .. 16 rt + 15 (this wave's columns) into saved slot `slot`
+        auto save_rows = [&](int slot, int rt) {
+            float* dst = saved_H + ((size_t)bh * (nchunk + 1) + slot) * DK * DV;
 #pragma unroll
-            for (int rt = 0; rt < NRT; ++rt)
+            for (int dt = 0; dt < NDT; ++dt)
 #pragma unroll
-                for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-                    for (int rr = 0; rr < 4; ++rr)
-                        dst[(16 * rt + 4 * g4 + rr) * DV + dm0 + 16 * dt + l16] = Hs[rt][dt][rr];
+                for (int rr = 0; rr < 4; ++rr)
+                    dst[(16 * rt + 4 * g4 + rr) * DV + dm0 + 16 * dt + l16] = Hs[rt][dt][rr];
         };
         for (int c = 0; c <= nchunk; ++c) {
             const int cc = c - 1;   // the chunk consumed in this round
@@ -90,8 +86,6 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
                 const size_t row0 = seq0 + (size_t)cc * kC;
                 const unsigned char* buf = smem + (cc & 1) * Cfg::BUF;
                 const uint16_t* sVS = reinterpret_cast<const uint16_t*>(buf + Cfg::VS);   // V [t][DVT]
-                if (saved_H && cc % kSaveEvery == 0) save_state(cc / kSaveEvery);
-
                 const uint16_t* sQH = reinterpret_cast<const uint16_t*>(buf + Cfg::QH);
                 const uint16_t* sQL = reinterpret_cast<const uint16_t*>(buf + Cfg::QL);
                 const uint16_t* sKH = reinterpret_cast<const uint16_t*>(buf + Cfg::KH);
@@ -147,6 +141,12 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
 #pragma unroll
                         for (int it = 0; it < 2; ++it) yacc[dt][it] = mfma3(hh, hl, qbh[it], qbl[it], yacc[dt][it]);
                     }
+                    // the chunk-start state goes to the saved context a few rows at a time, between
+                    // the products, so that the stores of all workgroups do not come in one burst
+                    if (saved_H) {
+                        save_rows(cc, 2 * ks);
+                        save_rows(cc, 2 * ks + 1);
+                    }
                 }
                 // y[t, d .. d+3] for t = 16 it + l16, d = dm0 + 16 dt + 4 g4
 #pragma unroll
@@ -193,7 +193,9 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
             barrier_lds();
         }
 
-        if (saved_H) save_state(nsave);   // the final state closes the saved sequence
+        if (saved_H)   // the final state closes the saved sequence
+#pragma unroll
+            for (int rt = 0; rt < NRT; ++rt) save_rows(nchunk, rt);
         if (g.etaT) {
 #pragma unroll
             for (int rt = 0; rt < NRT; ++rt)
@@ -235,8 +237,7 @@ bool chunked_supported(const Shape& s) { return s.bf16 && s.dk >= 32; }
 // [BH][nchunk+1][dk][dv].
 size_t chunked_saved_bytes(const Shape& s) {
     const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
-    const size_t nsave = (size_t)(s.T + kC * kSaveEvery - 1) / (kC * kSaveEvery);
-    return (size_t)s.B * s.H * s.dk * (nchunk + (nsave + 1) * (size_t)s.dv) * sizeof(float);
+    return (size_t)s.B * s.H * s.dk * (nchunk + (nchunk + 1) * (size_t)s.dv) * sizeof(float);
 }
 
 hipError_t launch_forward_chunked(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st) {

@@ -83,6 +83,17 @@ __device__ __forceinline__ float dpp(float x) {
                                                                  0xf, false));
 }
 
+// Sums over the 32 lanes of each half of a wave (lanes 0..31 and 32..63) with
+// DPP moves; the total of a half lands in its upper 16 lanes (16..31, 48..63).
+__device__ __forceinline__ float half_sum(float x) {
+    x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
+    x += dpp<0x4E, 0xf>(x);    // quad_perm [2,3,0,1]
+    x += dpp<0x141, 0xf>(x);   // row_half_mirror
+    x += dpp<0x140, 0xf>(x);   // row_mirror: every lane of a row holds the row sum
+    x += dpp<0x142, 0xa>(x);   // row_bcast:15 into rows 1 and 3
+    return x;
+}
+
 // Sum over the 64 lanes of a wave with DPP moves (no LDS traffic); the total is
 // returned in every lane through lane 63.
 __device__ __forceinline__ float wave_sum(float x) {

@@ -7,26 +7,37 @@
 // acts linearly on (x, z) with lam = x / z:
 //   z_t = pbar_t x_{t-1} + abar_t^2 z_{t-1}     (so rho_t = z_{t-1} / z_t)
 //   x_t = x_{t-1} + phi_t z_t
-// and, with A_t = prod_{s<=t} abar_s, the running product of the forget gates
-// F = abar rho (Theorem 2) inside the chunk is P_t = A_t / z_t (x = lam, z = 1,
-// A = 1 at the chunk start).  With one reciprocal R = 1 / (x_t A_t) per token,
+// i.e. (x, z) is multiplied by Theorem 1's matrix [[1 + pbar phi, abar^2 phi],
+// [pbar, abar^2]].  With A_t = prod_{s<=t} abar_s, the running product of the
+// forget gates F = abar rho (Theorem 2) inside the chunk is P_t = A_t / z_t
+// (x = lam, z = 1, A = 1 at the chunk start).  With one reciprocal
+// R = 1 / (x_t A_t) per token,
 //   Qp[t, n] = (q_t / lam_t) P_t = q_t A_t (A_t R)
 //   Kn[t, n] = (r_t k_t) / P_t   = r_t k_t z_t (x_t R)
 // Requirement (documented in the ABI): inside one chunk, prod abar,
 // prod (abar^2 + pbar lam) and lam prod (abar^2 + pbar lam) stay in fp32 range.
 //
-// A workgroup runs NSW scan waves (64 key slots each) beside NMW MFMA waves
-// (32 value channels each).  Round i of the chunk loop: the scan waves walk
-// chunk c(i) into exchange buffer i & 1 -- Qp and Kn as split-bf16 [t][n]
-// tiles, the chunk decay P_C, optionally the per-token variance partials --
-// and bring that chunk's tile of a per-token value tensor (v or dy) into the
-// same buffer, while the MFMA waves consume buffer (i - 1) & 1.  One
-// LDS-ordering barrier ends each round.  The scan waves issue every load of
-// the workgroup, straight into LDS (16-byte buffer loads), and request each
-// token block of the next chunk as soon as the current chunk has walked past
-// it; since their request stream is fixed, each wait names exactly the
-// requests it needs.
+// A workgroup runs NSW scan waves (32 key slots each) beside NMW MFMA waves
+// (16 value channels each).  A scan-wave lane owns one key slot and one half of
+// the chunk (tokens 16 h .. 16 h + 15, h = lane / 32).  The second half needs
+// the state after token 15 before it can start, so each lane first composes
+// the 2x2 matrices of 8 tokens -- tokens 0..7 in half 0, 8..15 in half 1 --,
+// the half-1 lane takes its partner's product through a cross-lane exchange and
+// applies both to the chunk start (lam, 1); then both halves walk their 16
+// tokens side by side, and the half-1 lanes end at the chunk end.
+//
+// Round i of the chunk loop: the scan waves walk chunk c(i) into exchange
+// buffer i & 1 -- Qp and Kn as split-bf16 [t][n] tiles, the chunk decay P_C,
+// optionally the per-token variance partials -- and bring that chunk's tile of
+// a per-token value tensor (v or dy) into the same buffer, while the MFMA waves
+// consume buffer (i - 1) & 1.  One LDS-ordering barrier ends each round.  The
+// scan waves issue every load of the workgroup, straight into LDS (16-byte
+// buffer loads); their input staging is double-buffered: at the start of round
+// i they request all inputs of chunk c(i + 1) and then wait for those of chunk
+// c(i), requested one round earlier.
 #pragma once
+#include <type_traits>
+
 #include "kla_buf.hpp"
 #include "kla_mfma.hpp"
 
@@ -39,10 +50,10 @@ struct ChunkCfg {
     static constexpr int DK = DK_, DV = DV_;
     static constexpr int DVT = DV < 64 ? DV : 64;    // value channels per workgroup
     static constexpr int NTILE = DV / DVT;
-    static constexpr int DCW = DVT < 32 ? DVT : 32;  // value channels per MFMA wave
+    static constexpr int DCW = 16;                   // value channels per MFMA wave
     static constexpr int NDT = DCW / 16;
     static constexpr int NMW = DVT / DCW;            // MFMA waves
-    static constexpr int SW = DK < 64 ? DK : 64;     // key slots per scan wave
+    static constexpr int SW = 32;                    // key slots per scan wave
     static constexpr int NSW = DK / SW;              // scan waves
     static constexpr int NTHR = 64 * (NSW + NMW);
     static constexpr int NRT = DK / 16;
@@ -56,16 +67,15 @@ struct ChunkCfg {
     static constexpr int BUF = VS + kC * DVT * 2;
     static constexpr int NVL = kC * DVT * 2 / 1024;  // 1 KiB wave loads of the value tile
     static constexpr int TPV = kC / NVL;             // tokens per value-tile load
-    // per scan wave: abar, pbar, k, q [4][kC][SW] bf16, r [2][64] and the chunk-start
-    // lam [2][64] as words
+    // per scan wave: abar, pbar, k, q [2 buffers][4][kC][SW] bf16, then r [2][64] and the
+    // chunk-start lam [2][64] as words
     static constexpr int STG = 2 * BUF;
-    static constexpr int STG_R = 4 * kC * SW * 2, STG_L = STG_R + 2 * 64 * 4;
+    static constexpr int STG_IN = 4 * kC * SW * 2;   // one buffer of staged inputs
+    static constexpr int STG_R = 2 * STG_IN, STG_L = STG_R + 2 * 64 * 4;
     static constexpr int STG_WAVE = STG_L + 2 * 64 * 4;
     static constexpr int BYTES = STG + NSW * STG_WAVE;
-    static constexpr int TPL = 512 / SW;             // tokens per 16-byte-per-lane load (one block)
-    static constexpr int NBLK = kC / TPL;
     static_assert(DK >= 32 && DK % 32 == 0, "chunked path needs dk >= 32");
-    static_assert(NBLK >= 2 && NVL >= 1, "tile sizes");
+    static_assert(DVT % 16 == 0 && NVL >= 1 && NVL * TPV == kC, "value tile sizes");
     static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
 };
 
@@ -84,10 +94,11 @@ __device__ __forceinline__ void xcd_tile_map(int i, int nbh, int ntile, int& bh,
 // Outputs of the precision walk in one exchange buffer.
 struct ScanOut {
     uint16_t *qh, *ql, *kh, *kl;   // [t][n]
-    float* yv;                     // per-token wave sums of q^2 / lam
+    float* dec;                    // P_C [n]
+    float* yv;                     // per-token sums of q^2 / lam over this wave's slots
 };
 
-// Staged inputs of one group of 8 tokens for one key slot (raw bf16 / r words).
+// Staged inputs of 8 consecutive tokens for one key slot (raw bf16 / r words).
 struct ScanGroup {
     uint32_t a[8], p[8], k[8], q[8];
     uint4 r[2];
@@ -107,75 +118,107 @@ __device__ __forceinline__ void read_group(ScanGroup& gr, const uint16_t* __rest
     gr.r[1] = *reinterpret_cast<const uint4*>(rw + t8 + 4);
 }
 
-// Walk the tokens of one chunk for key slot n (lane), from the staged inputs
-// (stg: [4][kC][SW] bf16; rw: r as words [kC]).  FULL: all kC tokens are valid
-// (no per-token guards).  The inputs of the next group of 8 tokens are read
-// from LDS before the current group is processed.  before(G) runs before group
-// G is read (the wait for its staged inputs); after(j) after token block j
-// (TPL tokens) is done (the request of the next chunk's block j).
-template <int SW, int TPL, int LQ, bool YV, bool FULL, class Before, class After>
-__device__ __forceinline__ void scan_tokens(const uint16_t* __restrict__ stg, const uint32_t* __restrict__ rw, int sl,
-                                            int nt, bool active, int n, float& x, float& z, float& A,
-                                            const ScanOut& o, Before before, After after) {
-    ScanGroup gr[2];
-    before(0);
-    read_group<SW>(gr[0], stg, rw, sl, 0);
+__device__ __forceinline__ float bf16w(uint32_t w) { return __uint_as_float(w << 16); }
+
+// One chunk of the walk for key slot n (lane: slot sl, half hf) from the staged
+// inputs (stg: [4][kC][SW] bf16; rw: r as words [kC]), starting from the chunk-
+// start lam x.  FULL: all kC tokens are valid (no per-token guards).  Returns
+// the lam at the chunk end in every lane.
+template <int SW, int LQ, bool YV, bool FULL>
+__device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, const uint32_t* __restrict__ rw,
+                                            int sl, int hf, int n, int nt, float x, const ScanOut& o) {
+    // ---- the 2x2 product of this lane's 8 tokens 8 hf .. 8 hf + 7, as the images of
+    // (1, 0) and (0, 1), with the product of abar
+    float m00 = 1.f, m10 = 0.f, m01 = 0.f, m11 = 1.f, aq = 1.f;
+    {
+        float ta[8], tp[8], tk[8], tr[8];
 #pragma unroll
-    for (int t8 = 0; t8 < kC; t8 += 8) {
-        const ScanGroup& cur = gr[(t8 / 8) & 1];
-        if (t8 + 8 < kC) {
-            before((t8 + 8) / 8);
-            read_group<SW>(gr[((t8 / 8) + 1) & 1], stg, rw, sl, t8 + 8);
+        for (int j = 0; j < 8; ++j) {
+            const int t = 8 * hf + j;
+            ta[j] = bf16w(stg[(0 * kC + t) * SW + sl]);
+            tp[j] = bf16w(stg[(1 * kC + t) * SW + sl]);
+            tk[j] = bf16w(stg[(2 * kC + t) * SW + sl]);
+            tr[j] = bf16w(rw[t]);
         }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float a2 = ta[j] * ta[j], phi = tk[j] * tk[j] * tr[j];
+            const float z0 = fmaf(tp[j], m00, a2 * m10), z1 = fmaf(tp[j], m01, a2 * m11);
+            const float x0 = fmaf(phi, z0, m00), x1 = fmaf(phi, z1, m01);
+            const bool ok = FULL || 8 * hf + j < nt;
+            m00 = ok ? x0 : m00;
+            m10 = ok ? z0 : m10;
+            m01 = ok ? x1 : m01;
+            m11 = ok ? z1 : m11;
+            aq = ok ? aq * ta[j] : aq;
+        }
+    }
+    // ---- the start of this lane's half: (lam, 1, 1) in half 0; in half 1 the partner's
+    // product (tokens 0..7) and then its own (8..15) applied to (lam, 1)
+    const float p00 = __shfl_xor(m00, 32, 64), p10 = __shfl_xor(m10, 32, 64);
+    const float p01 = __shfl_xor(m01, 32, 64), p11 = __shfl_xor(m11, 32, 64);
+    const float pa = __shfl_xor(aq, 32, 64);
+    const float x8 = fmaf(p00, x, p01), z8 = fmaf(p10, x, p11);
+    float xw = hf ? fmaf(m00, x8, m01 * z8) : x;
+    float zw = hf ? fmaf(m10, x8, m11 * z8) : 1.f;
+    float Aw = hf ? aq * pa : 1.f;
+
+    // ---- walk tokens 16 hf .. 16 hf + 15 (inputs of the next 8 read before the current 8)
+    const int tb = 16 * hf;
+    ScanGroup gr[2];
+    read_group<SW>(gr[0], stg, rw, sl, tb);
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+        const ScanGroup& cur = gr[g];
+        if (g == 0) read_group<SW>(gr[1], stg, rw, sl, tb + 8);
 #pragma unroll
         for (int j2 = 0; j2 < 4; ++j2) {
             float qp2[2], kn2[2];
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
-                const int t = t8 + 2 * j2 + e, i = 2 * j2 + e;
-                const float av = __uint_as_float(cur.a[i] << 16);
-                const float pv = __uint_as_float(cur.p[i] << 16);
-                const float kv = __uint_as_float(cur.k[i] << 16);
-                const float qv = __uint_as_float(cur.q[i] << 16);
+                const int i = 2 * j2 + e, t = tb + 8 * g + i;
+                const float av = bf16w(cur.a[i]), pv = bf16w(cur.p[i]);
+                const float kv = bf16w(cur.k[i]), qv = bf16w(cur.q[i]);
                 const uint32_t rword = i < 4 ? (&cur.r[0].x)[i] : (&cur.r[1].x)[i - 4];
-                const float rv = __uint_as_float(rword << 16);
+                const float rv = bf16w(rword);
                 const float kr = kv * rv;
-                const float zn = fmaf(pv, x, av * av * z);
-                const float xn = fmaf(kr * kv, zn, x);
-                const float An = A * av;
+                const float zn = fmaf(pv, xw, av * av * zw);
+                const float xn = fmaf(kr * kv, zn, xw);
+                const float An = Aw * av;
                 const float R = fast_rcp(xn * An);
                 const float AR = An * R;   // 1 / x_t
                 const bool ok = FULL || t < nt;
-                const float qp = ok ? (qv * An) * AR : 0.f;
-                const float kn = ok ? (kr * zn) * (xn * R) : 0.f;
-                x = ok ? xn : x;
-                z = ok ? zn : z;
-                A = ok ? An : A;
-                qp2[e] = qp;
-                kn2[e] = kn;
+                qp2[e] = ok ? (qv * An) * AR : 0.f;
+                kn2[e] = ok ? (kr * zn) * (xn * R) : 0.f;
+                xw = ok ? xn : xw;
+                zw = ok ? zn : zw;
+                Aw = ok ? An : Aw;
                 if constexpr (YV) {
-                    const float w = (ok && active) ? qv * qv * zn * AR : 0.f;   // q^2 / lam_t
-                    const float ws = wave_sum(w);
-                    if (sl == 0) o.yv[t] = ws;
+                    const float w = ok ? qv * qv * zn * AR : 0.f;   // q^2 / lam_t
+                    const float ws = half_sum(w);
+                    if (sl == SW - 1) o.yv[t] = ws;
                 }
             }
             uint32_t qh, ql, kh, kl;
             split2(qp2[0], qp2[1], qh, ql);
             split2(kn2[0], kn2[1], kh, kl);
-            const int t = t8 + 2 * j2;
-            if (active) {
-                o.qh[t * LQ + n] = static_cast<uint16_t>(qh);
-                o.qh[(t + 1) * LQ + n] = static_cast<uint16_t>(qh >> 16);
-                o.ql[t * LQ + n] = static_cast<uint16_t>(ql);
-                o.ql[(t + 1) * LQ + n] = static_cast<uint16_t>(ql >> 16);
-                o.kh[t * LQ + n] = static_cast<uint16_t>(kh);
-                o.kh[(t + 1) * LQ + n] = static_cast<uint16_t>(kh >> 16);
-                o.kl[t * LQ + n] = static_cast<uint16_t>(kl);
-                o.kl[(t + 1) * LQ + n] = static_cast<uint16_t>(kl >> 16);
-            }
+            const int t = tb + 8 * g + 2 * j2;
+            o.qh[t * LQ + n] = static_cast<uint16_t>(qh);
+            o.qh[(t + 1) * LQ + n] = static_cast<uint16_t>(qh >> 16);
+            o.ql[t * LQ + n] = static_cast<uint16_t>(ql);
+            o.ql[(t + 1) * LQ + n] = static_cast<uint16_t>(ql >> 16);
+            o.kh[t * LQ + n] = static_cast<uint16_t>(kh);
+            o.kh[(t + 1) * LQ + n] = static_cast<uint16_t>(kh >> 16);
+            o.kl[t * LQ + n] = static_cast<uint16_t>(kl);
+            o.kl[(t + 1) * LQ + n] = static_cast<uint16_t>(kl >> 16);
         }
-        if ((t8 + 8) % TPL == 0) after((t8 + 8) / TPL - 1);
     }
+    // ---- the half-1 lanes stand at the chunk end; their lam goes to both halves
+    const float iz = fast_rcp(zw);
+    const float lam_end = xw * iz;
+    if (hf) o.dec[n] = Aw * iz;
+    const float other = __shfl_xor(lam_end, 32, 64);
+    return hf ? lam_end : other;
 }
 
 // Sequence and tensors of one scan-wave loop.
@@ -191,47 +234,53 @@ struct ScanSrc {
 // order is c = 0 .. nchunk-1 (REV = false: lam carried from lam_in, the
 // chunk-start lam stored to save_lam when given) or c = nchunk-1 .. 0 (REV:
 // the chunk-start lam read from lam_in [BH][nchunk][DK]).  Returns the lam
-// after the last walked token (forward order) for key slot wave * SW + lane.
+// after the last walked token (forward order) for key slot wave * SW + lane % SW.
 template <class Cfg, bool YV, bool REV>
 __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int lane, const ScanSrc& sc,
                                            const float* __restrict__ lam_in, float* __restrict__ save_lam) {
     constexpr int DK = Cfg::DK, DV = Cfg::DV, DVT = Cfg::DVT, SW = Cfg::SW, NSW = Cfg::NSW;
     constexpr int NL = REV ? 1 : 0;   // chunk-start lam requests per round
     const int H = sc.H, h = sc.h, T = sc.T, nchunk = sc.nchunk;
-    const bool active = lane < SW;
-    const int sl = active ? lane : 0;   // slot within this wave's staged rows
+    const int sl = lane % SW, hf = lane / SW;   // key slot within the wave, half of the chunk
     const int n = wave * SW + sl;
-    float x = 1.f;                      // lam at the chunk start
-    if (!REV && active && lam_in) x = lam_in[(size_t)sc.bh * DK + n];
+    float x = 1.f;                              // lam at the chunk start
+    if (!REV && lam_in) x = lam_in[(size_t)sc.bh * DK + n];
     unsigned char* stw = smem + Cfg::STG + wave * Cfg::STG_WAVE;
-    uint16_t* stg = reinterpret_cast<uint16_t*>(stw);
     uint32_t* rw = reinterpret_cast<uint32_t*>(stw + Cfg::STG_R);   // [2][64]
     float* lw = reinterpret_cast<float*>(stw + Cfg::STG_L);         // [2][64]
     const uint32_t tok_bytes = (uint32_t)H * DK * 2;
-    // lane -> (token within a block, 8 slots); the load of a block lands as [t][SW] rows
-    const uint32_t blk_voff = (uint32_t)(lane / (SW / 8)) * tok_bytes + (lane % (SW / 8)) * 16;
+    // lane -> (token lane / 4, 8 slots); a load of 16 tokens lands as [t][SW] rows
+    const uint32_t in_voff = (uint32_t)(lane >> 2) * tok_bytes + (lane & 3) * 16;
     auto chunk_of = [&](int it) { return REV ? nchunk - 1 - it : it; };
 
-    // buffer descriptors of chunk cn; chunks outside the sequence get empty
-    // descriptors, whose loads write zeros
-    rsrc_t rs[4];
-    auto chunk_rsrc = [&](int cn) {
+    // every input of chunk cn into staging buffer bb: abar, pbar, k, q (two loads of 16
+    // tokens each), r and, walking backwards, the chunk-start lam.  Chunks outside the
+    // sequence get empty descriptors, whose loads write zeros.
+    auto issue_inputs = [&](int cn, int bb) {
         const bool in = cn >= 0 && cn < nchunk;
         const int t0 = in ? cn * kC : 0, nt = in ? min(kC, T - t0) : 0;
         const size_t e0 = ((sc.seq0 + t0) * H + h) * DK + wave * SW;
         const uint32_t bytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + SW) * 2 : 0u;
-        rs[0] = make_rsrc(sc.a + e0, bytes);
-        rs[1] = make_rsrc(sc.p + e0, bytes);
-        rs[2] = make_rsrc(sc.k + e0, bytes);
-        rs[3] = make_rsrc(sc.q + e0, bytes);
-    };
-    auto issue_block = [&](int j) {
-#pragma unroll
-        for (int ti = 0; ti < 4; ++ti)
-            buf_ld128_lds(rs[ti], stg + (ti * kC + j * Cfg::TPL) * SW, blk_voff + (uint32_t)j * Cfg::TPL * tok_bytes);
+        uint16_t* stg = reinterpret_cast<uint16_t*>(stw) + bb * 4 * kC * SW;
+        auto one = [&](const uint16_t* src, int ti) {
+            const rsrc_t rs = make_rsrc(src + e0, bytes);
+            buf_ld128_lds(rs, stg + ti * kC * SW, in_voff);
+            buf_ld128_lds(rs, stg + (ti * kC + 16) * SW, in_voff + 16 * tok_bytes);
+        };
+        one(sc.a, 0);
+        one(sc.p, 1);
+        one(sc.k, 2);
+        one(sc.q, 3);
+        const rsrc_t rr = make_rsrc(sc.r + (sc.seq0 + t0) * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
+        buf_ld16_lds(rr, rw + bb * 64, (uint32_t)lane * H * 2);
+        if constexpr (REV) {
+            const rsrc_t rl = make_rsrc(lam_in + ((size_t)sc.bh * nchunk + (in ? cn : 0)) * DK + wave * SW,
+                                        in ? (uint32_t)SW * 4 : 0u);
+            buf_ld32_lds(rl, lw + bb * 64, (uint32_t)lane * 4);
+        }
     };
     // this wave's share of the value-tile loads (loads i = wave, wave + NSW, ...)
-    const int nvw = wave < Cfg::NVL ? (Cfg::NVL - wave + NSW - 1) / NSW : 0;
+    const int nvw = Cfg::NVL % NSW == 0 ? Cfg::NVL / NSW : wave < Cfg::NVL ? (Cfg::NVL - wave + NSW - 1) / NSW : 0;
     const uint32_t v_voff = (uint32_t)(lane / (DVT / 8)) * H * DV * 2 + (lane % (DVT / 8)) * 16;
     auto issue_tile = [&](int cn, int it) {
         const int t0 = cn * kC, nt = min(kC, T - t0);
@@ -241,34 +290,22 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
         for (int i = wave; i < Cfg::NVL; i += NSW)
             buf_ld128_lds(rv, vs + i * 1024, v_voff + (uint32_t)(i * Cfg::TPV) * H * DV * 2);
     };
-    // r of chunk cn (lanes >= nt read as 0) and, walking backwards, its start lam
-    auto issue_rl = [&](int cn, int it) {
-        const bool in = cn >= 0 && cn < nchunk;
-        const int t0 = in ? cn * kC : 0, nt = in ? min(kC, T - t0) : 0;
-        const rsrc_t rr = make_rsrc(sc.r + (sc.seq0 + t0) * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
-        buf_ld16_lds(rr, rw + (it & 1) * 64, (uint32_t)lane * H * 2);
-        if constexpr (REV) {
-            const rsrc_t rl = make_rsrc(lam_in + ((size_t)sc.bh * nchunk + (in ? cn : 0)) * DK + wave * SW,
-                                        in ? (uint32_t)SW * 4 : 0u);
-            buf_ld32_lds(rl, lw + (it & 1) * 64, (uint32_t)lane * 4);
-        }
-    };
+    // the chunk-start lam goes to save_lam (one store per round, issued by the whole wave)
+    const bool sl_store = !REV && save_lam != nullptr;
     wait_vm_all();   // the carried lam is complete before the prefetch loop starts
-    if (nchunk > 0) {
-        chunk_rsrc(chunk_of(0));
-        issue_rl(chunk_of(0), 0);
-#pragma unroll
-        for (int j = 0; j < Cfg::NBLK; ++j) issue_block(j);
-    }
+    if (nchunk > 0) issue_inputs(chunk_of(0), 0);
 
     for (int it = 0; it <= nchunk; ++it) {
         if (it < nchunk) {
-            const int c = chunk_of(it), cn = chunk_of(it + 1);
+            const int c = chunk_of(it), bb = it & 1;
             const int nt = min(kC, T - c * kC);
+            if (sl_store) save_lam[((size_t)sc.bh * nchunk + c) * DK + n] = x;
             issue_tile(c, it);
-            issue_rl(cn, it + 1);
-            chunk_rsrc(cn);
-            if (!REV && save_lam && active) save_lam[((size_t)sc.bh * nchunk + c) * DK + n] = x;
+            issue_inputs(chunk_of(it + 1), bb ^ 1);
+            // this chunk's inputs, requested one round earlier, have landed: younger are the
+            // requests just issued (the saved-lam store, the value-tile loads, 9 + NL staging loads)
+            wait_vm_le_rt<9 + NL>(nvw + (sl_store ? 1 : 0));
+            if constexpr (REV) x = lw[bb * 64 + sl];
 
             unsigned char* buf = smem + (it & 1) * Cfg::BUF;
             ScanOut o;
@@ -276,33 +313,16 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             o.ql = reinterpret_cast<uint16_t*>(buf + Cfg::QL);
             o.kh = reinterpret_cast<uint16_t*>(buf + Cfg::KH);
             o.kl = reinterpret_cast<uint16_t*>(buf + Cfg::KL);
+            o.dec = reinterpret_cast<float*>(buf + Cfg::DEC);
             o.yv = reinterpret_cast<float*>(buf + Cfg::YVP) + wave * kC;
-            // Group G starting block j is read while block j - 1 is processed (after
-            // the next chunk's blocks before j - 1 went out).  Younger than block j's
-            // loads are then: its later blocks, this chunk's value-tile loads (nvw),
-            // r (and lam) of the next chunk, possibly the saved-lam store, and those
-            // requests: 4 (NBLK - 1) + 1 + NL + nvw for j = 0, 4 (NBLK - 2) + 1 + NL +
-            // nvw otherwise.  The chunk-start lam was requested before block 0.
-            auto before = [&](int G) {
-                if (G == 0) {
-                    wait_vm_le_rt<4 * (Cfg::NBLK - 1) + 1 + NL>(nvw);
-                    if constexpr (REV) x = lw[(it & 1) * 64 + sl];
-                } else if ((8 * G) % Cfg::TPL == 0) {
-                    wait_vm_le_rt<4 * (Cfg::NBLK - 2) + 1 + NL>(nvw);
-                }
-            };
-            auto after = [&](int j) { issue_block(j); };
-            const uint32_t* rwc = rw + (it & 1) * 64;
-            float z = 1.f, A = 1.f;
+            const uint16_t* stg = reinterpret_cast<const uint16_t*>(stw) + bb * 4 * kC * SW;
+            const uint32_t* rwc = rw + bb * 64;
             if (nt == kC)
-                scan_tokens<SW, Cfg::TPL, Cfg::LQ, YV, true>(stg, rwc, sl, nt, active, n, x, z, A, o, before, after);
+                x = scan_chunk<SW, Cfg::LQ, YV, true>(stg, rwc, sl, hf, n, nt, x, o);
             else
-                scan_tokens<SW, Cfg::TPL, Cfg::LQ, YV, false>(stg, rwc, sl, nt, active, n, x, z, A, o, before, after);
-            const float iz = fast_rcp(z);
-            x *= iz;   // lam at the chunk end
-            if (active) reinterpret_cast<float*>(buf + Cfg::DEC)[n] = A * iz;
-            // the value tile has landed (younger: r, lam, the saved-lam store, NBLK blocks)
-            wait_vm_le<4 * Cfg::NBLK + 1 + NL>();
+                x = scan_chunk<SW, Cfg::LQ, YV, false>(stg, rwc, sl, hf, n, nt, x, o);
+            // the value tile has landed (younger: the 9 + NL staging loads)
+            wait_vm_le<9 + NL>();
         }
         barrier_lds();
     }
