@@ -20,22 +20,25 @@
 //   drho = g lam_{t-1} + S / rho,  dabar = S / abar - 2 abar rho^2 drho,
 //   dpbar = -lam_{t-1} rho^2 drho,  dlam0 = c after the first token.
 //
-// One workgroup per (batch, head, 64 key slots) of NW waves; wave w owns the 16
-// key slots n0 + 16 w .. + 15 and does all of their work itself, sharing only
-// the dY / V tiles and nothing else:
-//   walk   lanes = (slot nl = lane % 16, quarter q = lane / 16 of 8 tokens):
-//          each lane first forms its quarter's transfer -- the 2x2 map of
-//          (x, z) of Theorem 1 over 8 tokens, with prod abar -- and the
-//          quarters are chained through LDS; then it walks its 8 tokens from
-//          the quarter start, writing Qp and Kn ([t][16], split bf16) and
-//          keeping lam_t, P_t and the reciprocals the adjoint walk needs;
-//   MFMA   B, B^T, X^T and Y^T for its slots and G^T[dv, 16] in registers;
-//   adjoint per lane: its quarter's tokens in reverse, once to summarise the
-//          quarter as an affine map of the incoming (c, S), then -- the
-//          quarters chained through LDS -- once more for the gradients.
-// The chunks are walked last to first.  The next chunk's inputs go straight into
-// LDS, requested during the first pass of a round's adjoint walk; the chunk's
-// saved state rows come into registers at the start of its round.
+// One workgroup per (batch, head, 64 key slots); a pair of waves owns 16 key
+// slots n0 + 16 p .. + 15, and the pairs share only the dY / V tiles.  Wave e of
+// a pair takes the tokens 16 e .. 16 e + 15 of each chunk in the walks:
+//   walk   lanes = (slot nl = lane % 16, group g = lane / 16 of 4 tokens): each
+//          lane forms its group's transfer -- the 2x2 map of (x, z) of
+//          Theorem 1 over 4 tokens, with prod abar --, the eight groups of the
+//          chunk are chained through LDS, and each lane walks its 4 tokens from
+//          the group start, writing Qp and Kn ([t][16], split bf16) and keeping
+//          lam_t, P_t and the reciprocals the adjoint walk needs;
+//   MFMA   split by operand instead: wave 0 forms B^T and X^T (with the chunk's
+//          saved start state H0 in registers), wave 1 forms B and Y^T and
+//          carries G^T[dv, 16] in registers;
+//   adjoint per lane: its group's tokens in reverse, once to summarise the
+//          group as an affine map of the incoming (c, S), then -- the groups
+//          chained through LDS -- once more for the gradients.
+// The chunks are walked last to first, five LDS barriers per chunk separating
+// the phases.  The next chunk's inputs go straight into LDS, requested during
+// the first pass of a round's adjoint walk; the chunk's saved state rows come
+// into wave 0's registers at the start of its round.
 #include <type_traits>
 
 #include "kla_chunk.hpp"
@@ -46,8 +49,9 @@ namespace {
 
 template <int DK, int DV>
 struct DkCfg {
-    static constexpr int NW = DK / 16 < 4 ? DK / 16 : 4;   // waves, 16 key slots each
-    static constexpr int NTN = 16 * NW;                     // key slots per workgroup
+    static constexpr int NP = DK / 16 < 4 ? DK / 16 : 4;   // wave pairs, 16 key slots each
+    static constexpr int NW = 2 * NP;                       // waves
+    static constexpr int NTN = 16 * NP;                     // key slots per workgroup
     static constexpr int NNT = DK / NTN;                    // workgroups per (b, h)
     static constexpr int NTHR = 64 * NW;
     static constexpr int KSD = DV / 32;                     // 32-deep steps over the value channels
@@ -55,30 +59,31 @@ struct DkCfg {
     static constexpr int CPR = DV / 8;                      // 16-byte chunks per dY / V row
     static constexpr int TPV = 512 / DV;                    // rows per 1 KiB load of a dY / V tile
     static constexpr int NVL = kC / TPV;                    // 1 KiB loads per dY / V tile
-    static constexpr int LQ2 = 24;                          // row stride of per-wave [t][16] bf16 tiles
-    static constexpr int LX = 20;                           // row stride of per-wave [t][16] fp32 tiles
+    static constexpr int LQ2 = 24;                          // row stride of per-pair [t][16] bf16 tiles
+    static constexpr int LX = 20;                           // row stride of per-pair [t][16] fp32 tiles
+    static constexpr int NG = 8;                            // token groups per chunk (4 tokens each)
     // shared: dY and V tiles [2 buffers][2][kC][DV] (16-byte chunks swizzled by row)
     static constexpr int TILE = kC * DV * 2;
-    static constexpr int WAVE0 = 2 * 2 * TILE;
-    // per wave (offsets from the wave's base)
+    static constexpr int PAIR0 = 2 * 2 * TILE;
+    // per pair (offsets from the pair's base)
     static constexpr int STG = 0;                                   // [2][4][kC][16] bf16: abar, pbar, k, q
     static constexpr int RW = STG + 2 * 4 * kC * 16 * 2;            // [2][64] r words
     static constexpr int LW = RW + 2 * 64 * 4;                      // [2][64] chunk-start lam (lanes < 16)
     static constexpr int QH = LW + 2 * 64 * 4;                      // Qp, Kn split bf16 [kC][LQ2]
     static constexpr int QL = QH + kC * LQ2 * 2, KH = QL + kC * LQ2 * 2, KL = KH + kC * LQ2 * 2;
     static constexpr int XT = KL + kC * LQ2 * 2, YT = XT + kC * LX * 4;   // X, Y fp32 [kC][LX]
-    static constexpr int QS = YT + kC * LX * 4;                     // quarter maps [4][5][16] fp32
-    static constexpr int PC = QS + 4 * 5 * 16 * 4;                  // chunk decay P_C [16] fp32
-    static constexpr int WAVE = (PC + 16 * 4 + 15) / 16 * 16;
-    static constexpr int BYTES = WAVE0 + NW * WAVE;   // dynamic part
+    static constexpr int QS = YT + kC * LX * 4;                     // group maps [NG][5][16] fp32
+    static constexpr int PC = QS + NG * 5 * 16 * 4;                 // chunk decay P_C [16] fp32
+    static constexpr int PAIR = (PC + 16 * 4 + 15) / 16 * 16;
+    static constexpr int BYTES = PAIR0 + NP * PAIR;   // dynamic part
     // The gradient tiles dq, dk, dabar, dpbar [4][kC][16] bf16 and the dr terms
-    // [kC][17] fp32 of each wave live in separate static arrays: they are read
+    // [kC][17] fp32 of each pair live in separate static arrays: they are read
     // back while the next chunk's direct-to-LDS loads are in flight, and as
     // distinct objects they are seen not to alias those loads' destinations.
-    static constexpr int STATIC = NW * (4 * kC * 16 * 2 + kC * 17 * 4);
+    static constexpr int STATIC = NP * (4 * kC * 16 * 2 + kC * 17 * 4);
     static_assert(DK >= 32 && DK % 16 == 0 && DV >= 32 && DV % 32 == 0, "backward tile sizes");
     static_assert(NVL >= 1 && TPV * CPR == 64, "value tile loads");
-    static_assert(6 + 2 * ((NVL + NW - 1) / NW) <= 16, "requests spread over 8 tokens, two each");
+    static_assert(4 + 2 * ((NVL + NW - 1) / NW) <= 8, "requests spread over 4 tokens, two each");
     static_assert(BYTES + STATIC <= 160 * 1024, "LDS budget of one workgroup");
 };
 
@@ -126,10 +131,11 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                                                                        const float* __restrict__ saved_H,
                                                                        float* __restrict__ dr_part) {
     using Cfg = DkCfg<DK, DV>;
-    constexpr int NW = Cfg::NW, KSD = Cfg::KSD, NRD = Cfg::NRD, LQ2 = Cfg::LQ2, LX = Cfg::LX;
+    constexpr int NP = Cfg::NP, NW = Cfg::NW, KSD = Cfg::KSD, NRD = Cfg::NRD, LQ2 = Cfg::LQ2, LX = Cfg::LX;
+    constexpr int NG = Cfg::NG;
     extern __shared__ __align__(16) unsigned char smem[];
-    __shared__ __align__(16) uint16_t s_out[NW * 4 * kC * 16];
-    __shared__ __align__(16) float s_drc[NW * kC * 17];
+    __shared__ __align__(16) uint16_t s_out[NP * 4 * kC * 16];
+    __shared__ __align__(16) float s_drc[NP * kC * 17];
 
     const uint16_t* a = static_cast<const uint16_t*>(g.a);
     const uint16_t* p = static_cast<const uint16_t*>(g.p);
@@ -145,65 +151,70 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
     const int H = s.H, T = s.T;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int l16 = lane & 15, g4 = lane >> 4;   // MFMA lane coordinates; for the walks: slot, quarter
-    const int nl = l16, qq = g4;
-    const int n0w = ntile * Cfg::NTN + 16 * wave;   // this wave's first key slot
+    const int pr = wave % NP, e = wave / NP;     // pair, half of the chunk (a pair shares a SIMD)
+    const int l16 = lane & 15, g4 = lane >> 4;   // MFMA lane coordinates
+    const int nl = l16, gg = 4 * e + g4;         // walk lanes: slot, token group (tokens 4 gg .. 4 gg + 3)
+    const int n0w = ntile * Cfg::NTN + 16 * pr;  // the pair's first key slot
     const int nchunk = (T + kC - 1) / kC;
     const size_t seq0 = (size_t)b * T;
     const size_t nbt = (size_t)s.B * T * H;
-    unsigned char* wb = smem + Cfg::WAVE0 + wave * Cfg::WAVE;
+    unsigned char* wb = smem + Cfg::PAIR0 + pr * Cfg::PAIR;
     const uint32_t tok_k = (uint32_t)H * DK * 2;   // bytes between tokens of a [.., H, DK] tensor
     const uint32_t tok_v = (uint32_t)H * DV * 2;
 
-    // ---- carries of the reverse recursions (the 4 quarter lanes of a slot hold the same values)
+    // ---- carries of the reverse recursions (every lane of both waves holds its slot's values)
     float cT = g.dlamT ? g.dlamT[(size_t)bh * DK + n0w + nl] : 0.f;
     float ST = 0.f;
-    if (g.detaT) {   // final-state term sum_d detaT H_T, split over the quarter lanes
+    if (g.detaT) {   // final-state term sum_d detaT H_T, split over the four lane groups
         const float* HT = saved_H + (((size_t)bh * (nchunk + 1) + nchunk) * DK + n0w + nl) * DV;
         const float* dT = g.detaT + ((size_t)bh * DK + n0w + nl) * DV;
-        for (int d = qq * (DV / 4); d < (qq + 1) * (DV / 4); ++d) ST += dT[d] * HT[d];
+        for (int d = g4 * (DV / 4); d < (g4 + 1) * (DV / 4); ++d) ST += dT[d] * HT[d];
     }
     ST += __shfl_xor(ST, 16, 64);
     ST += __shfl_xor(ST, 32, 64);
 
-    // G^T[d, n] for d = 16 rd + 4 g4 + rr, n = n0w + l16
+    // G^T[d, n] for d = 16 rd + 4 g4 + rr, n = n0w + l16 (carried by wave 1 of the pair)
     f32x4 GT[NRD];
 #pragma unroll
     for (int rd = 0; rd < NRD; ++rd)
 #pragma unroll
         for (int rr = 0; rr < 4; ++rr)
-            GT[rd][rr] = g.detaT ? g.detaT[((size_t)bh * DK + n0w + l16) * DV + 16 * rd + 4 * g4 + rr] : 0.f;
+            GT[rd][rr] = (e == 1 && g.detaT) ? g.detaT[((size_t)bh * DK + n0w + l16) * DV + 16 * rd + 4 * g4 + rr] : 0.f;
 
     // ---- requests of chunk cn into buffer bb (chunks outside the sequence: empty, writing
     // zeros), one load per part so that they can be spread over a round:
-    //   0..3  abar, pbar, k, q of this wave's slots (1 KiB each, lane -> (t = lane / 2, 8 slots))
-    //   4, 5  r (lanes >= nt read as 0) and the chunk-start lam of the 16 slots
-    //   6..   this wave's share of the dY and V tiles (loads i = wave, wave + NW, ...), swizzled
+    //   wave 0: 0..3  abar, pbar, k, q of the pair's slots (1 KiB each, lane -> (t = lane / 2, 8 slots))
+    //   wave 1: 0, 1  r (lanes >= nt read as 0) and the chunk-start lam of the 16 slots
+    //   then this wave's share of the dY and V tiles (loads i = wave, wave + NW, ...), swizzled
+    const int nin = e == 0 ? 4 : 2;
     const int nvw = wave < Cfg::NVL ? (Cfg::NVL - wave + NW - 1) / NW : 0;
-    const int nparts = 6 + 2 * nvw;
+    const int nparts = nin + 2 * nvw;
     auto issue_part = [&](int cn, int bb, int part) {
         const bool in = cn >= 0 && cn < nchunk;
         const int t0 = in ? cn * kC : 0, nt = in ? min(kC, T - t0) : 0;
         const size_t tok0 = seq0 + t0;
-        if (part < 4) {
-            const uint16_t* src = part == 0 ? a : part == 1 ? p : part == 2 ? k : q;
-            const uint32_t kbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + 16) * 2 : 0u;
-            uint16_t* stg = reinterpret_cast<uint16_t*>(wb + Cfg::STG) + (bb * 4 + part) * kC * 16;
-            buf_ld128_lds(make_rsrc(src + (tok0 * H + h) * DK + n0w, kbytes), stg,
-                          (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16);
-        } else if (part == 4) {
-            const rsrc_t rr = make_rsrc(r + tok0 * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
-            buf_ld16_lds(rr, wb + Cfg::RW + bb * 256, (uint32_t)lane * H * 2);
-        } else if (part == 5) {
-            const rsrc_t rl = make_rsrc(saved_lam + ((size_t)bh * nchunk + (in ? cn : 0)) * DK + n0w, in ? 64u : 0u);
-            buf_ld32_lds(rl, wb + Cfg::LW + bb * 256, (uint32_t)lane * 4);
+        if (part < nin) {
+            if (e == 0) {
+                const uint16_t* src = part == 0 ? a : part == 1 ? p : part == 2 ? k : q;
+                const uint32_t kbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + 16) * 2 : 0u;
+                uint16_t* stg = reinterpret_cast<uint16_t*>(wb + Cfg::STG) + (bb * 4 + part) * kC * 16;
+                buf_ld128_lds(make_rsrc(src + (tok0 * H + h) * DK + n0w, kbytes), stg,
+                              (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16);
+            } else if (part == 0) {
+                const rsrc_t rr = make_rsrc(r + tok0 * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
+                buf_ld16_lds(rr, wb + Cfg::RW + bb * 256, (uint32_t)lane * H * 2);
+            } else {
+                const rsrc_t rl =
+                    make_rsrc(saved_lam + ((size_t)bh * nchunk + (in ? cn : 0)) * DK + n0w, in ? 64u : 0u);
+                buf_ld32_lds(rl, wb + Cfg::LW + bb * 256, (uint32_t)lane * 4);
+            }
         } else if (part < nparts) {
-            const int m = (part - 6) >> 1, i = wave + NW * m;
+            const int m = (part - nin) >> 1, i = wave + NW * m, sel = (part - nin) & 1;
             const uint32_t vbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DV + DV) * 2 : 0u;
-            const rsrc_t rv = make_rsrc(((part - 6) & 1 ? vv : dy) + (tok0 * H + h) * DV, vbytes);
+            const rsrc_t rv = make_rsrc((sel ? vv : dy) + (tok0 * H + h) * DV, vbytes);
             const int row = i * Cfg::TPV + lane / Cfg::CPR, pch = lane % Cfg::CPR;
             const uint32_t off = (uint32_t)row * tok_v + (uint32_t)((pch ^ (row % Cfg::CPR)) * 16);
-            buf_ld128_lds(rv, smem + (bb * 2 + ((part - 6) & 1)) * Cfg::TILE + i * 1024, off);
+            buf_ld128_lds(rv, smem + (bb * 2 + sel) * Cfg::TILE + i * 1024, off);
         }
     };
     wait_vm_all();   // the carries and G^T are complete before the request stream starts
@@ -215,27 +226,33 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
         const int nt = min(kC, T - c * kC);
         const size_t row0 = seq0 + (size_t)c * kC;
 
-        // saved chunk-start state rows H0[n0w + l16][32 ks + 8 g4 .. + 7], used by X below
-        float4 h0[KSD][2];
-        {
-            const float* H0 = saved_H + (((size_t)bh * (nchunk + 1) + c) * DK + n0w + l16) * DV;
-#pragma unroll
-            for (int ks = 0; ks < KSD; ++ks) {
-                h0[ks][0] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4);
-                h0[ks][1] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4 + 4);
-            }
-        }
-        // this chunk's requests (issued last round) have landed: younger are only the last
-        // round's 5 stores and the 2 KSD state loads just issued
-        if (it == 0)
-            wait_vm_le<2 * KSD>();
-        else
-            wait_vm_le<5 + 2 * KSD>();
-        barrier_lds();   // every wave's share of the dY / V tiles is in
-
-        // the round's work; FULL: all kC tokens valid (no per-token guards)
-        auto round_body = [&](auto full_tag) {
+        // the round's work for wave E of the pair; FULL: all kC tokens valid (no per-token guards)
+        auto round_body = [&](auto full_tag, auto role_tag) {
             constexpr bool FULL = decltype(full_tag)::value;
+            constexpr int E = decltype(role_tag)::value;
+            // saved chunk-start state rows H0[n0w + l16][32 ks + 8 g4 .. + 7] (wave 0, for X)
+            float4 h0[KSD][2];
+            if constexpr (E == 0) {
+                const float* H0 = saved_H + (((size_t)bh * (nchunk + 1) + c) * DK + n0w + l16) * DV;
+#pragma unroll
+                for (int ks = 0; ks < KSD; ++ks) {
+                    h0[ks][0] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4);
+                    h0[ks][1] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4 + 4);
+                }
+                // this chunk's requests (issued last round) have landed: younger are only the
+                // last round's 5 stores and the 2 KSD state loads just issued
+                if (it == 0)
+                    wait_vm_le<2 * KSD>();
+                else
+                    wait_vm_le<5 + 2 * KSD>();
+            } else {
+                if (it == 0)
+                    wait_vm_le<0>();
+                else
+                    wait_vm_le<5>();
+            }
+            barrier_lds();   // every wave's share of the dY / V tiles and staging is in
+
             const uint16_t* sDY = reinterpret_cast<const uint16_t*>(smem + bb * 2 * Cfg::TILE);
             const uint16_t* sV = sDY + kC * DV;
             const uint16_t* stg = reinterpret_cast<const uint16_t*>(wb + Cfg::STG) + bb * 4 * kC * 16;
@@ -247,55 +264,60 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             float* sX = reinterpret_cast<float*>(wb + Cfg::XT);
             float* sY = reinterpret_cast<float*>(wb + Cfg::YT);
             float* sPC = reinterpret_cast<float*>(wb + Cfg::PC);
+            float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
             auto in_a = [&](int t) { return __uint_as_float((uint32_t)stg[(0 * kC + t) * 16 + nl] << 16); };
             auto in_p = [&](int t) { return __uint_as_float((uint32_t)stg[(1 * kC + t) * 16 + nl] << 16); };
             auto in_k = [&](int t) { return __uint_as_float((uint32_t)stg[(2 * kC + t) * 16 + nl] << 16); };
             auto in_q = [&](int t) { return __uint_as_float((uint32_t)stg[(3 * kC + t) * 16 + nl] << 16); };
             auto in_r = [&](int t) { return __uint_as_float(rw[t] << 16); };
 
-            // ================================================================ MFMA, part 1
-            // B[t, j] = dY_t . V_j (j <= t) and B^T, tiles (0,0), (1,0), (1,1) / (0,0), (0,1), (1,1)
-            f32x4 B00 = zero4(), B10 = zero4(), B11 = zero4(), T00 = zero4(), T01 = zero4(), T11 = zero4();
-    #pragma unroll
-            for (int ks = 0; ks < KSD; ++ks) {
-                const bf16x8 ya0 = lds8_swz<DV>(sDY, l16, 32 * ks + 8 * g4);
-                const bf16x8 ya1 = lds8_swz<DV>(sDY, 16 + l16, 32 * ks + 8 * g4);
-                const bf16x8 v0 = lds8_swz<DV>(sV, l16, 32 * ks + 8 * g4);
-                const bf16x8 v1 = lds8_swz<DV>(sV, 16 + l16, 32 * ks + 8 * g4);
-                B00 = mfma_bf16(ya0, v0, B00);
-                B10 = mfma_bf16(ya1, v0, B10);
-                B11 = mfma_bf16(ya1, v1, B11);
-                T00 = mfma_bf16(v0, ya0, T00);
-                T01 = mfma_bf16(v0, ya1, T01);
-                T11 = mfma_bf16(v1, ya1, T11);
-            }
-    #pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                if (l16 > 4 * g4 + rr) {   // B: row t = 4 g4 + rr, column j = l16, keep j <= t
-                    B00[rr] = 0.f;
-                    B11[rr] = 0.f;
+            // ================================================================ phase 1
+            // wave 0: B^T[j, t] = V_j . dY_t (j <= t), tiles (0,0), (0,1), (1,1), as operands over j;
+            // wave 1: B[t, j] = dY_t . V_j (j <= t), tiles (0,0), (1,0), (1,1), as operands over t
+            bf16x8 boh[2], bol[2];
+            {
+                f32x4 c0 = zero4(), c1 = zero4(), c2 = zero4();
+#pragma unroll
+                for (int ks = 0; ks < KSD; ++ks) {
+                    const bf16x8 ya0 = lds8_swz<DV>(sDY, l16, 32 * ks + 8 * g4);
+                    const bf16x8 ya1 = lds8_swz<DV>(sDY, 16 + l16, 32 * ks + 8 * g4);
+                    const bf16x8 v0 = lds8_swz<DV>(sV, l16, 32 * ks + 8 * g4);
+                    const bf16x8 v1 = lds8_swz<DV>(sV, 16 + l16, 32 * ks + 8 * g4);
+                    if constexpr (E == 0) {
+                        c0 = mfma_bf16(v0, ya0, c0);
+                        c1 = mfma_bf16(v0, ya1, c1);
+                        c2 = mfma_bf16(v1, ya1, c2);
+                    } else {
+                        c0 = mfma_bf16(ya0, v0, c0);
+                        c1 = mfma_bf16(ya1, v0, c1);
+                        c2 = mfma_bf16(ya1, v1, c2);
+                    }
                 }
-                if (4 * g4 + rr > l16) {   // B^T: row j, column t = l16, keep j <= t
-                    T00[rr] = 0.f;
-                    T11[rr] = 0.f;
+#pragma unroll
+                for (int rr = 0; rr < 4; ++rr) {
+                    // B^T: row j = 4 g4 + rr, column t = l16; B: row t = 4 g4 + rr, column j = l16
+                    const bool drop = E == 0 ? 4 * g4 + rr > l16 : l16 > 4 * g4 + rr;
+                    if (drop) {
+                        c0[rr] = 0.f;
+                        c2[rr] = 0.f;
+                    }
+                }
+                // rows {4g..}, {16+4g..} of the contraction
+                if constexpr (E == 0) {
+                    split8(c0, zero4(), boh[0], bol[0]);
+                    split8(c1, c2, boh[1], bol[1]);
+                } else {
+                    split8(c0, c1, boh[0], bol[0]);
+                    split8(zero4(), c2, boh[1], bol[1]);
                 }
             }
-            // B operands: over t for Y (column j), over j for X (column t); rows {4g..}, {16+4g..}
-            bf16x8 bbh[2], bbl[2], bth[2], btl[2];
-            split8(B00, B10, bbh[0], bbl[0]);
-            split8(zero4(), B11, bbh[1], bbl[1]);
-            split8(T00, zero4(), bth[0], btl[0]);
-            split8(T01, T11, bth[1], btl[1]);
-
-            // ================================================================ precision walk
-            // transfer of this lane's quarter: (x, z) -> M (x, z) over its valid tokens, as the
+            // the transfer of this lane's group: (x, z) -> M (x, z) over its valid tokens, as the
             // images of (1, 0) and (0, 1), and the product of abar
-            float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
             {
                 float x0 = 1.f, z0 = 0.f, x1 = 0.f, z1 = 1.f, Aq = 1.f;
-    #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const int t = 8 * qq + j;
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int t = 4 * gg + j;
                     const float av = in_a(t), pv = in_p(t), kv = in_k(t), rv = in_r(t);
                     const float a2 = av * av, phi = kv * kv * rv;
                     const float z0n = fmaf(pv, x0, a2 * z0), z1n = fmaf(pv, x1, a2 * z1);
@@ -306,36 +328,39 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                     z1 = ok ? z1n : z1;
                     Aq = ok ? Aq * av : Aq;
                 }
-                qs[(qq * 5 + 0) * 16 + nl] = x0;
-                qs[(qq * 5 + 1) * 16 + nl] = z0;
-                qs[(qq * 5 + 2) * 16 + nl] = x1;
-                qs[(qq * 5 + 3) * 16 + nl] = z1;
-                qs[(qq * 5 + 4) * 16 + nl] = Aq;
+                qs[(gg * 5 + 0) * 16 + nl] = x0;
+                qs[(gg * 5 + 1) * 16 + nl] = z0;
+                qs[(gg * 5 + 2) * 16 + nl] = x1;
+                qs[(gg * 5 + 3) * 16 + nl] = z1;
+                qs[(gg * 5 + 4) * 16 + nl] = Aq;
             }
-            // chain the earlier quarters from the chunk start (x, z, A) = (lam, 1, 1)
+            barrier_lds();   // the group transfers of the chunk are in
+
+            // ================================================================ phase 2
+            // chain the earlier groups from the chunk start (x, z, A) = (lam, 1, 1)
             float x = reinterpret_cast<const float*>(wb + Cfg::LW)[bb * 64 + nl], z = 1.f, A = 1.f;
-    #pragma unroll
-            for (int q2 = 0; q2 < 3; ++q2) {
+#pragma unroll
+            for (int q2 = 0; q2 < NG - 1; ++q2) {
                 const float m00 = qs[(q2 * 5 + 0) * 16 + nl], m10 = qs[(q2 * 5 + 1) * 16 + nl];
                 const float m01 = qs[(q2 * 5 + 2) * 16 + nl], m11 = qs[(q2 * 5 + 3) * 16 + nl];
                 const float aq = qs[(q2 * 5 + 4) * 16 + nl];
-                const bool use = q2 < qq;
+                const bool use = q2 < gg;
                 const float xn = fmaf(m00, x, m01 * z), zn = fmaf(m10, x, m11 * z);
                 x = use ? xn : x;
                 z = use ? zn : z;
                 A = use ? A * aq : A;
             }
-            float izp = fast_rcp(z);              // 1 / z before the quarter's first token
-            const float lamq = x * izp;           // lam before the quarter's first token
-            // per token of the quarter: lam_t, P_t and, for the adjoint walk, 1/P_t, 1/lam_t,
+            float izp = fast_rcp(z);              // 1 / z before the group's first token
+            const float lamq = x * izp;           // lam before the group's first token
+            // per token of the group: lam_t, P_t and, for the adjoint walk, 1/P_t, 1/lam_t,
             // rho_t, 1/rho_t = abar^2 + pbar lam_{t-1}, 1/abar
-            float lam_r[8], P_r[8], iP_r[8], il_r[8], rho_r[8], den_r[8], ia_r[8];
-    #pragma unroll
-            for (int j2 = 0; j2 < 4; ++j2) {
+            float lam_r[4], P_r[4], iP_r[4], il_r[4], rho_r[4], den_r[4], ia_r[4];
+#pragma unroll
+            for (int j2 = 0; j2 < 2; ++j2) {
                 float qp2[2], kn2[2];
-    #pragma unroll
-                for (int e = 0; e < 2; ++e) {
-                    const int j = 2 * j2 + e, t = 8 * qq + j;
+#pragma unroll
+                for (int e2 = 0; e2 < 2; ++e2) {
+                    const int j = 2 * j2 + e2, t = 4 * gg + j;
                     const float av = in_a(t), pv = in_p(t), kv = in_k(t), qv = in_q(t), rv = in_r(t);
                     const float kr = kv * rv;
                     const float zn = fmaf(pv, x, av * av * z);
@@ -345,8 +370,8 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                     const float iz = fast_rcp(zn);
                     const float AR = An * R, XR = xn * R;   // 1 / x_t, 1 / A_t
                     const bool ok = FULL || t < nt;
-                    qp2[e] = ok ? (qv * An) * AR : 0.f;
-                    kn2[e] = ok ? (kr * zn) * XR : 0.f;
+                    qp2[e2] = ok ? (qv * An) * AR : 0.f;
+                    kn2[e2] = ok ? (kr * zn) * XR : 0.f;
                     lam_r[j] = xn * iz;
                     P_r[j] = An * iz;
                     iP_r[j] = zn * XR;
@@ -362,7 +387,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 uint32_t qh, ql, kh, kl;
                 split2(qp2[0], qp2[1], qh, ql);
                 split2(kn2[0], kn2[1], kh, kl);
-                const int t = 8 * qq + 2 * j2;
+                const int t = 4 * gg + 2 * j2;
                 sQH[t * LQ2 + nl] = static_cast<uint16_t>(qh);
                 sQH[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(qh >> 16);
                 sQL[t * LQ2 + nl] = static_cast<uint16_t>(ql);
@@ -372,78 +397,69 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 sKL[t * LQ2 + nl] = static_cast<uint16_t>(kl);
                 sKL[(t + 1) * LQ2 + nl] = static_cast<uint16_t>(kl >> 16);
             }
-            if (qq == 3) sPC[nl] = A * fast_rcp(z);   // the last quarter ends at the chunk end
+            if (gg == NG - 1) sPC[nl] = A * fast_rcp(z);   // the last group ends at the chunk end
+            barrier_lds();   // Qp, Kn of every token and P_C are in
 
-            // ================================================================ MFMA, part 2
-            // X^T[n, t] = sum_d H0[n, d] dY^T[d, t] + sum_j Kn^T[n, j] B^T[j, t]
-            f32x4 xacc[2] = {zero4(), zero4()};
-    #pragma unroll
-            for (int ks = 0; ks < KSD; ++ks) {
-                bf16x8 hh, hl;
-                split8(f32x4{h0[ks][0].x, h0[ks][0].y, h0[ks][0].z, h0[ks][0].w},
-                       f32x4{h0[ks][1].x, h0[ks][1].y, h0[ks][1].z, h0[ks][1].w}, hh, hl);
-    #pragma unroll
-                for (int tt = 0; tt < 2; ++tt)
-                    xacc[tt] = mfma2a(hh, hl, lds8_swz<DV>(sDY, 16 * tt + l16, 32 * ks + 8 * g4), xacc[tt]);
-            }
-            {
+            // ================================================================ phase 3
+            if constexpr (E == 0) {
+                // X^T[n, t] = sum_d H0[n, d] dY^T[d, t] + sum_j Kn^T[n, j] B^T[j, t]
+                f32x4 xacc[2] = {zero4(), zero4()};
+#pragma unroll
+                for (int ks = 0; ks < KSD; ++ks) {
+                    bf16x8 hh, hl;
+                    split8(f32x4{h0[ks][0].x, h0[ks][0].y, h0[ks][0].z, h0[ks][0].w},
+                           f32x4{h0[ks][1].x, h0[ks][1].y, h0[ks][1].z, h0[ks][1].w}, hh, hl);
+#pragma unroll
+                    for (int tt = 0; tt < 2; ++tt)
+                        xacc[tt] = mfma2a(hh, hl, lds8_swz<DV>(sDY, 16 * tt + l16, 32 * ks + 8 * g4), xacc[tt]);
+                }
                 const bf16x8 knh = lds_tr8(sKH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
                 const bf16x8 knl = lds_tr8(sKL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
-    #pragma unroll
-                for (int tt = 0; tt < 2; ++tt) xacc[tt] = mfma3(knh, knl, bth[tt], btl[tt], xacc[tt]);
-            }
-            // Y^T[n, j] = sum_t Qp^T[n, t] B[t, j] + sum_d Gs[n, d] V^T[d, j]
-            f32x4 yacc[2];
-            {
+#pragma unroll
+                for (int tt = 0; tt < 2; ++tt) {
+                    xacc[tt] = mfma3(knh, knl, boh[tt], bol[tt], xacc[tt]);
+                    *reinterpret_cast<float4*>(sX + (16 * tt + l16) * LX + 4 * g4) =
+                        float4{xacc[tt][0], xacc[tt][1], xacc[tt][2], xacc[tt][3]};
+                }
+            } else {
+                // Y^T[n, j] = sum_t Qp^T[n, t] B[t, j] + sum_d Gs[n, d] V^T[d, j]
+                f32x4 yacc[2];
                 const bf16x8 qth = lds_tr8(sQH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
                 const bf16x8 qtl = lds_tr8(sQL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
-    #pragma unroll
-                for (int jt = 0; jt < 2; ++jt) yacc[jt] = mfma3(qth, qtl, bbh[jt], bbl[jt], zero4());
-            }
-            const float pcn = sPC[l16];
-    #pragma unroll
-            for (int rd = 0; rd < NRD; ++rd)
-    #pragma unroll
-                for (int rr = 0; rr < 4; ++rr) GT[rd][rr] *= pcn;   // Gs^T in place
-    #pragma unroll
-            for (int ks = 0; ks < KSD; ++ks) {
-                bf16x8 gh, gl;
-                split8(GT[2 * ks], GT[2 * ks + 1], gh, gl);
-    #pragma unroll
-                for (int jt = 0; jt < 2; ++jt) {
-                    const bf16x8 vb = lds4x2_swz<DV>(sV, 16 * jt + l16, 32 * ks + 4 * g4, 32 * ks + 16 + 4 * g4);
-                    yacc[jt] = mfma2a(gh, gl, vb, yacc[jt]);
+#pragma unroll
+                for (int jt = 0; jt < 2; ++jt) yacc[jt] = mfma3(qth, qtl, boh[jt], bol[jt], zero4());
+                const float pcn = sPC[l16];
+#pragma unroll
+                for (int rd = 0; rd < NRD; ++rd)
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr) GT[rd][rr] *= pcn;   // Gs^T in place
+#pragma unroll
+                for (int ks = 0; ks < KSD; ++ks) {
+                    bf16x8 gh, gl;
+                    split8(GT[2 * ks], GT[2 * ks + 1], gh, gl);
+#pragma unroll
+                    for (int jt = 0; jt < 2; ++jt) {
+                        const bf16x8 vb = lds4x2_swz<DV>(sV, 16 * jt + l16, 32 * ks + 4 * g4, 32 * ks + 16 + 4 * g4);
+                        yacc[jt] = mfma2a(gh, gl, vb, yacc[jt]);
+                    }
                 }
+#pragma unroll
+                for (int jt = 0; jt < 2; ++jt)
+                    *reinterpret_cast<float4*>(sY + (16 * jt + l16) * LX + 4 * g4) =
+                        float4{yacc[jt][0], yacc[jt][1], yacc[jt][2], yacc[jt][3]};
             }
-            // G^T <- dY^T Qp + Gs^T
-            {
-                const bf16x8 qbh = lds_tr8(sQH, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
-                const bf16x8 qbl = lds_tr8(sQL, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
-    #pragma unroll
-                for (int rd = 0; rd < NRD; ++rd) {
-                    const bf16x8 yt = lds_tr8_swz<DV>(sDY, 8 * g4, 8 * g4 + 4, 16 * rd, l16);
-                    GT[rd] = mfma2b(yt, qbh, qbl, GT[rd]);
-                }
-            }
-            // X and Y to [t][n] for the adjoint walk
-    #pragma unroll
-            for (int tt = 0; tt < 2; ++tt) {
-                *reinterpret_cast<float4*>(sX + (16 * tt + l16) * LX + 4 * g4) =
-                    float4{xacc[tt][0], xacc[tt][1], xacc[tt][2], xacc[tt][3]};
-                *reinterpret_cast<float4*>(sY + (16 * tt + l16) * LX + 4 * g4) =
-                    float4{yacc[tt][0], yacc[tt][1], yacc[tt][2], yacc[tt][3]};
-            }
+            barrier_lds();   // X and Y of every token are in
 
-            // ================================================================ adjoint walk
-            // pass 1: the quarter's tokens in reverse; per token the affine step
+            // ================================================================ phase 4
+            // adjoint pass 1: the group's tokens in reverse; per token the affine step
             //   (c, S) -> (alpha (c - w) - beta (S + u), S + u)
             // composed into c_out = Am c_in + Bm S_in + Cm, S_out = S_in + Dm
-            float u_[8], w_[8], al_[8], be_[8], dq_[8], rdk_[8], kr2_[8], ia_[8], a2r2_[8], lp_[8], den_[8], lpr2_[8],
-                kdk_[8], kk_[8];
+            float u_[4], w_[4], al_[4], be_[4], dq_[4], rdk_[4], kr2_[4], ia_[4], a2r2_[4], lp_[4], den_[4], lpr2_[4],
+                kdk_[4], kk_[4];
             float Am = 1.f, Bm = 0.f, Cm = 0.f, Dm = 0.f;
-    #pragma unroll
-            for (int j = 7; j >= 0; --j) {
-                const int t = 8 * qq + j;
+#pragma unroll
+            for (int j = 3; j >= 0; --j) {
+                const int t = 4 * gg + j;
                 const float av = in_a(t), pv = in_p(t), kv = in_k(t), qv = in_q(t), rv = in_r(t);
                 const float lam_p = j > 0 ? lam_r[j - 1] : lamq;
                 const float Xv = sX[t * LX + nl], Yv = sY[t * LX + nl];
@@ -476,36 +492,48 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 Am = al * Am;
                 Dm = Dm + u;
                 // the next chunk's requests, two per token: they go out only after the
-                // transposing LDS reads above (which would otherwise wait for them) and are
-                // spread so that the loads of the four waves do not queue up at once
-                issue_part(c - 1, bb ^ 1, 2 * (7 - j));
-                issue_part(c - 1, bb ^ 1, 2 * (7 - j) + 1);
+                // transposing LDS reads above (which would otherwise wait for them)
+                issue_part(c - 1, bb ^ 1, 2 * (3 - j));
+                issue_part(c - 1, bb ^ 1, 2 * (3 - j) + 1);
             }
-            qs[(qq * 5 + 0) * 16 + nl] = Am;
-            qs[(qq * 5 + 1) * 16 + nl] = Bm;
-            qs[(qq * 5 + 2) * 16 + nl] = Cm;
-            qs[(qq * 5 + 3) * 16 + nl] = Dm;
-            // carries into this quarter (through the later quarters) and out of the chunk
+            if constexpr (E == 1) {
+                // G^T <- dY^T Qp + Gs^T
+                const bf16x8 qbh = lds_tr8(sQH, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
+                const bf16x8 qbl = lds_tr8(sQL, LQ2, 8 * g4, 8 * g4 + 4, 0, l16);
+#pragma unroll
+                for (int rd = 0; rd < NRD; ++rd) {
+                    const bf16x8 yt = lds_tr8_swz<DV>(sDY, 8 * g4, 8 * g4 + 4, 16 * rd, l16);
+                    GT[rd] = mfma2b(yt, qbh, qbl, GT[rd]);
+                }
+            }
+            qs[(gg * 4 + 0) * 16 + nl] = Am;   // the group transfers were read before the last barrier
+            qs[(gg * 4 + 1) * 16 + nl] = Bm;
+            qs[(gg * 4 + 2) * 16 + nl] = Cm;
+            qs[(gg * 4 + 3) * 16 + nl] = Dm;
+            barrier_lds();   // the group summaries are in
+
+            // ================================================================ phase 5
+            // carries into this group (through the later groups) and out of the chunk
             float c_in = 0.f, S_in = 0.f;
-    #pragma unroll
-            for (int q2 = 3; q2 >= 0; --q2) {
-                if (q2 == qq) {
+#pragma unroll
+            for (int q2 = NG - 1; q2 >= 0; --q2) {
+                if (q2 == gg) {
                     c_in = cT;
                     S_in = ST;
                 }
-                const float A2 = qs[(q2 * 5 + 0) * 16 + nl], B2 = qs[(q2 * 5 + 1) * 16 + nl];
-                const float C2 = qs[(q2 * 5 + 2) * 16 + nl], D2 = qs[(q2 * 5 + 3) * 16 + nl];
+                const float A2 = qs[(q2 * 4 + 0) * 16 + nl], B2 = qs[(q2 * 4 + 1) * 16 + nl];
+                const float C2 = qs[(q2 * 4 + 2) * 16 + nl], D2 = qs[(q2 * 4 + 3) * 16 + nl];
                 const float cn = fmaf(A2, cT, fmaf(B2, ST, C2));
                 ST += D2;
                 cT = cn;
             }
-            // pass 2: gradients of the quarter's tokens
-            uint16_t* so = s_out + wave * 4 * kC * 16;
-            float* drc = s_drc + wave * kC * 17;
+            // pass 2: gradients of the group's tokens
+            uint16_t* so = s_out + pr * 4 * kC * 16;
+            float* drc = s_drc + pr * kC * 17;
             float cc = c_in, SS = S_in;
-    #pragma unroll
-            for (int j = 7; j >= 0; --j) {
-                const int t = 8 * qq + j;
+#pragma unroll
+            for (int j = 3; j >= 0; --j) {
+                const int t = 4 * gg + j;
                 SS += u_[j];
                 const float gl = cc - w_[j];
                 const float dkv = fmaf(kr2_[j], gl, rdk_[j]);
@@ -521,13 +549,16 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 so[(3 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa >> 16);
             }
 
-            // ---- stores: [t][16] rows of dq, dk, dabar, dpbar (lane -> t = lane / 2, 8 slots),
-            // and this wave's dr partial over its 16 slots (lane -> t)
+            // ---- stores of this wave's 16 tokens: [t][16] rows of dq, dk, dabar, dpbar (lanes
+            // < 32: t = 16 E + lane / 2, 8 slots) and the pair's dr partial over its 16 slots
+            // (lanes < 16: t = 16 E + lane); the other lanes address the end of the range and
+            // are dropped, as are tokens past the sequence end
             {
+                const int tl = 16 * E + ((lane >> 1) & 15);
                 const uint32_t kbytes = (uint32_t)((nt - 1) * H * DK + 16) * 2;
                 const size_t ek = (row0 * H + h) * DK + n0w;
-                const uint32_t koff = (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16;
-                const uint16_t* o = so + (lane >> 1) * 16 + (lane & 1) * 8;
+                const uint32_t koff = lane < 32 ? (uint32_t)tl * tok_k + (lane & 1) * 16 : kbytes;
+                const uint16_t* o = so + tl * 16 + (lane & 1) * 8;
                 buf_st128(*reinterpret_cast<const uint4*>(o + 0 * kC * 16),
                           make_rsrc(static_cast<uint16_t*>(g.dq) + ek, kbytes), koff);
                 buf_st128(*reinterpret_cast<const uint4*>(o + 1 * kC * 16),
@@ -536,24 +567,32 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                           make_rsrc(static_cast<uint16_t*>(g.da) + ek, kbytes), koff);
                 buf_st128(*reinterpret_cast<const uint4*>(o + 3 * kC * 16),
                           make_rsrc(static_cast<uint16_t*>(g.dp) + ek, kbytes), koff);
-                const int t = lane & 31;
+                const int t = 16 * E + l16;
                 float acc = 0.f;
-    #pragma unroll
+#pragma unroll
                 for (int i = 0; i < 16; ++i) acc += drc[t * 17 + i];
-                float* dst = dr_part + (size_t)(ntile * NW + wave) * nbt + row0 * H + h;
-                buf_st32(acc, make_rsrc(dst, (uint32_t)((nt - 1) * H + 1) * 4), (uint32_t)lane * H * 4);   // lanes >= nt: dropped
+                float* dst = dr_part + (size_t)(ntile * NP + pr) * nbt + row0 * H + h;
+                const uint32_t dbytes = (uint32_t)((nt - 1) * H + 1) * 4;
+                buf_st32(acc, make_rsrc(dst, dbytes), lane < 16 ? (uint32_t)t * H * 4 : dbytes);
             }
         };
-        if (nt == kC)
-            round_body(std::true_type{});
-        else
-            round_body(std::false_type{});
+        if (e == 0) {
+            if (nt == kC)
+                round_body(std::true_type{}, std::integral_constant<int, 0>{});
+            else
+                round_body(std::false_type{}, std::integral_constant<int, 0>{});
+        } else {
+            if (nt == kC)
+                round_body(std::true_type{}, std::integral_constant<int, 1>{});
+            else
+                round_body(std::false_type{}, std::integral_constant<int, 1>{});
+        }
     }
     wait_vm_all();   // the requests for the chunk before the first have landed before exit
-    if (g.dlam0 && qq == 0) g.dlam0[(size_t)bh * DK + n0w + nl] = cT;
+    if (g.dlam0 && e == 0 && g4 == 0) g.dlam0[(size_t)bh * DK + n0w + nl] = cT;
 }
 
-// dr = sum of the per-wave partials, stored in the input dtype
+// dr = sum of the per-pair partials, stored in the input dtype
 __global__ void dr_combine_kernel(const float* __restrict__ part, int nparts, size_t n, uint16_t* __restrict__ dr) {
     const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= n) return;
@@ -579,7 +618,7 @@ hipError_t launch_dk(const Shape& s, const BwdArgs& a, const float* saved_lam, c
     const size_t n = (size_t)s.B * s.T * s.H;
     if (n > 0) {
         hipLaunchKernelGGL(dr_combine_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, dr_part,
-                           Cfg::NNT * Cfg::NW, n, static_cast<uint16_t*>(a.dr));
+                           Cfg::NNT * Cfg::NP, n, static_cast<uint16_t*>(a.dr));
         e = hipGetLastError();
     }
     return e;
@@ -589,7 +628,7 @@ hipError_t launch_dk(const Shape& s, const BwdArgs& a, const float* saved_lam, c
 
 bool chunked_bwd_supported(const Shape& s) { return s.bf16 && s.dk >= 32 && s.dv >= 32; }
 
-// per-wave dr partials: dk / 16 of them per token
+// per-pair dr partials: dk / 16 of them per token
 size_t chunked_bwd_workspace(const Shape& s) { return (size_t)(s.dk / 16) * s.B * s.T * s.H * sizeof(float); }
 
 hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st) {
