@@ -14,6 +14,12 @@ Run from the repository root on the GPU machine (TMPDIR=/tmp):
   rocprofv3 --pmc WRITE_SIZE --output-format csv -d D/write -o run -- \\
       python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration
   python -m paper_2602_10743_amd.traffic D/fetch D/write > profiles/lm_layer_traffic.md
+
+MFMA and VALU utilisation per kernel come from a third run:
+  rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU \\
+      GRBM_GUI_ACTIVE --output-format csv -d D/util -o run -- \\
+      python bench.py --steps 2 --warmup 1 --no-cpu-baseline
+  python -m paper_2602_10743_amd.traffic --util D/util > profiles/lm_layer_mfma_valu.md
 """
 import csv
 import glob
@@ -129,7 +135,69 @@ def load_summary(path: str):
     return values
 
 
+UTIL_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU", "GRBM_GUI_ACTIVE")
+NUM_SIMD = 1024          # 256 CUs x 4 SIMDs
+NUM_XCD = 8              # GRBM_GUI_ACTIVE comes summed over the accelerator dies
+BF16_PEAK = 2.5e15       # dense bf16 MFMA flop/s
+VALU_PEAK_INSTS = 256 * 4 * 2.4e9 / 4   # wave64 VALU instructions per second (one per 4 cycles per SIMD)
+
+
+def _rows(run_dir: str):
+    files = glob.glob(os.path.join(run_dir, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no counter_collection.csv under {run_dir}")
+    for f in files:
+        yield from csv.DictReader(open(f))
+
+
+def summarise_util(run_dir: str) -> str:
+    """MFMA busy fraction, bf16 MFMA flop rate and VALU issue per kernel from one
+    counter run with UTIL_COUNTERS; durations from the dispatch timestamps."""
+    acc = defaultdict(lambda: defaultdict(float))   # kernel -> counter -> sum over dispatches
+    dur = defaultdict(dict)                          # kernel -> dispatch -> ns
+    for r in _rows(run_dir):
+        k = _short(r["Kernel_Name"])
+        if not k.startswith(tuple(n for ns in CALLS.values() for n in ns)):
+            continue
+        d = r.get("Dispatch_Id") or r.get("Correlation_Id")
+        acc[k][r["Counter_Name"]] += float(r["Counter_Value"])
+        dur[k][d] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    lines = [
+        "# MFMA and VALU utilisation per kernel, lm-layer workload (B=8, T=2048, H=16, d=128, bf16)",
+        "",
+        "Command (repository root, one MI355X, TMPDIR=/tmp):",
+        "",
+        "    rocprofv3 --pmc " + " ".join(UTIL_COUNTERS) + " --output-format csv -d D/util -o run -- "
+        "python bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+        "    python -m paper_2602_10743_amd.traffic --util D/util",
+        "",
+        "Durations come from the dispatch timestamps of the same run.  MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / ",
+        f"{NUM_XCD} dies x {NUM_SIMD} SIMDs); bf16 rate = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16 / duration against",
+        f"{BF16_PEAK / 1e15:.1f} PFLOP/s; VALU issue = SQ_INSTS_VALU / duration against one wave64",
+        "instruction per 4 cycles per SIMD at 2.4 GHz.  The split-bf16 products count 2-3 MFMAs",
+        "per fp32-accurate product.",
+        "",
+        "| kernel | dispatches | avg us | MFMA busy | bf16 MFMA TFLOP/s | of peak | VALU Ginst/s | of peak |",
+        "|---|---|---|---|---|---|---|---|",
+    ]
+    for k in sorted(acc):
+        n = len(dur[k])
+        t = sum(dur[k].values()) / n * 1e-9
+        c = {name: v / n for name, v in acc[k].items()}
+        active = c.get("GRBM_GUI_ACTIVE", 1.0) / NUM_XCD
+        busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / max(active * NUM_SIMD, 1.0)
+        flops = 512.0 * c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) / t
+        valu = c.get("SQ_INSTS_VALU", 0.0) / t
+        lines.append(f"| {k} | {n} | {t * 1e6:.1f} | {100 * busy:.1f}% | {flops / 1e12:.1f} | "
+                     f"{100 * flops / BF16_PEAK:.1f}% | {valu / 1e9:.1f} | {100 * valu / VALU_PEAK_INSTS:.1f}% |")
+    lines.append("")
+    return "\n".join(lines)
+
+
 if __name__ == "__main__":
+    if len(sys.argv) == 3 and sys.argv[1] == "--util":
+        print(summarise_util(sys.argv[2]))
+        sys.exit(0)
     if len(sys.argv) != 3:
         print(__doc__, file=sys.stderr)
         sys.exit(2)
