@@ -71,7 +71,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the filter layer shards over (batch, head) with no "
-              "communication, so multi-GPU runs are not part of this build", file=sys.stderr)
+              "communication, and no multi-GPU path is implemented", file=sys.stderr)
         sys.exit(2)
 
     import torch
