@@ -55,6 +55,11 @@ SMALL = [  # B, T, H, dk, dv, dtype, dist
     (1, 200, 2, 128, 128, "bf16", "lm"),
     (1, 33, 2, 16, 128, "bf16", "c0"),
     (3, 129, 2, 128, 128, "f32", "lm"),
+    # chunked path at the other widths, partial chunks, a single short chunk, B*H not a multiple of 8
+    (1, 97, 3, 32, 64, "bf16", "lm"),
+    (2, 64, 1, 128, 32, "bf16", "lm"),
+    (1, 31, 1, 64, 128, "bf16", "lm"),
+    (3, 161, 1, 32, 32, "bf16", "c0"),
 ]
 
 
