@@ -2,7 +2,7 @@
  * kla.h -- C ABI of the Kalman Linear Attention (KLA) filter layer for MI355X (gfx950).
  *
  * The layer is the time-parallel information-form Kalman filter of Kalman
- * Linear Attention (Sec. 3.2 of the paper; Algorithm 1, eqs. kla-prec-mat and
+ * Linear Attention (Sec. 4.2 of the paper; Algorithm 1, eqs. kla-prec-mat and
  * kla-mean-mat in Appendix A).  Per batch b and head h, with key slots n < dk
  * and value channels d < dv, for t = 1..T:
  *

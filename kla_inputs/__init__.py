@@ -259,3 +259,27 @@ def decode_inputs(w: Workload, seed: Optional[int] = None, as_bits: bool = False
     steps = w.extra["steps"]
     w2 = Workload(w.cid, w.name, w.B, steps, w.H, w.dk, w.dv, w.dtype, w.dist, False)
     return full(w2, names=NAMES, seed=seed + 1000, as_bits=as_bits)
+
+
+OU_TENSOR_ID = {"a": 7, "p": 8, "delta": 9}
+
+
+def ou_params(H: int, dk: int, seed: int = 0) -> dict:
+    """Time-invariant OU parameters [H, dk] as float32 (the storage form; the
+    oracle widens them): step size delta log-uniform on [1e-3, 1e-1], mean
+    reversion a uniform on [1, 16], diffusion scale p = softplus(N(2, 1)).  The
+    resulting decays exp(-a delta) span about (0.2, 0.999), centred near 0.92."""
+    out = {}
+    for name, tid in OU_TENSOR_ID.items():
+        rows = []
+        for h in range(H):
+            g = _rng(seed, tid, 0, h)
+            if name == "delta":
+                x = np.exp(g.uniform(np.log(1e-3), np.log(1e-1), dk))
+            elif name == "a":
+                x = g.uniform(1.0, 16.0, dk)
+            else:
+                x = softplus(g.standard_normal(dk) + 2.0)
+            rows.append(x)
+        out[name] = to_f32(np.stack(rows))
+    return out

@@ -18,6 +18,12 @@ shapes: ``yvar [B, T, H]``, ``lamT [B, H, dk]``, ``dr [B, T, H]`` and
 ``dlam0 [B, H, dk]``; the per-channel copies of the precision, which then all
 coincide, are reduced (the final precision reads channel 0; the gradient of an
 initial precision shared by all channels is the sum over channels).
+
+The ``*_ou`` functions take the gates from time-invariant OU parameters
+``a, p, delta [H, dk]`` instead (Sec. 4.1, eq. discretisation): the exact
+discretisation is written out in numpy (fp64), broadcast over (b, t) and fed to
+the same filter; the parameter gradients are the per-token gate gradients summed
+over (b, t) and taken through the discretisation by the chain rule.
 """
 from __future__ import annotations
 
@@ -224,3 +230,72 @@ def affine_compose(f2, b2, f1, b1) -> tuple[np.ndarray, np.ndarray]:
     _load().kla_oracle_affine_compose(int(np.prod(shape)), _ptr(f2), _ptr(b2), _ptr(f1), _ptr(b1),
                                       _ptr(fo), _ptr(bo))
     return fo, bo
+
+
+# --------------------------------------------------------------------------------------
+# OU parameterisation (Sec. 4.1, eq. discretisation; Algorithm 1's OU-Discretisation
+# steps): time-invariant parameters a > 0 (mean reversion), p (diffusion scale) and
+# delta > 0 (step size), each [H, dk], define the decay and process-noise variance
+# shared by every token of every sequence:
+#   abar = exp(-a delta),    pbar = p^2 / (2 a) (1 - exp(-2 a delta)).
+# The filter is then the one above with abar_t = abar and pbar_t = pbar for all
+# (b, t); their gradients are the sums over (b, t) of the per-token ones, taken
+# through the discretisation by the chain rule.
+
+def ou_discretise(a, p, delta) -> tuple[np.ndarray, np.ndarray]:
+    """Decay abar and process-noise variance pbar of the exactly discretised OU prior."""
+    a, p, delta = (_c(x) for x in (a, p, delta))
+    abar = np.exp(-a * delta)
+    pbar = p * p * (-np.expm1(-2.0 * a * delta)) / (2.0 * a)
+    return abar, pbar
+
+
+def ou_discretise_vjp(a, p, delta, g_abar, g_pbar) -> tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Gradients (da, dp, ddelta) of a loss whose gradients with respect to abar and
+    pbar are g_abar and g_pbar (all [H, dk]).
+
+    With E = exp(-2 a delta) = abar^2 and s = (1 - E) / (2 a), so that pbar = p^2 s:
+      d abar / d a = -delta abar,   d abar / d delta = -a abar,
+      d s / d a = (delta E - s) / a,   d s / d delta = E."""
+    a, p, delta, g_abar, g_pbar = (_c(x) for x in (a, p, delta, g_abar, g_pbar))
+    abar = np.exp(-a * delta)
+    E = abar * abar
+    s = -np.expm1(-2.0 * a * delta) / (2.0 * a)
+    da = g_abar * (-delta * abar) + g_pbar * p * p * (delta * E - s) / a
+    dp = g_pbar * 2.0 * p * s
+    ddelta = g_abar * (-a * abar) + g_pbar * p * p * E
+    return da, dp, ddelta
+
+
+def _ou_tokens(a, p, delta, B, T):
+    abar, pbar = ou_discretise(a, p, delta)
+    shape = (B, T) + abar.shape
+    return _c(np.broadcast_to(abar, shape)), _c(np.broadcast_to(pbar, shape))
+
+
+def forward_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, nthreads: Optional[int] = None) -> dict:
+    """``forward`` with the gates of the OU parameters a, p, delta [H, dk]."""
+    B, T = np.shape(k)[:2]
+    abar, pbar = _ou_tokens(a, p, delta, B, T)
+    return forward(q, k, v, abar, pbar, r, lam0, eta0, nthreads=nthreads)
+
+
+def backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=None,
+                nthreads: Optional[int] = None) -> dict:
+    """Gradient of ``forward_ou``: dq, dk, dv, dr, dlam0, deta0 as in ``backward``, and
+    da, dp, ddelta [H, dk] for the OU parameters."""
+    B, T = np.shape(k)[:2]
+    abar, pbar = _ou_tokens(a, p, delta, B, T)
+    out = backward(q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT, detaT, nthreads=nthreads)
+    g_abar = out.pop("da").sum(axis=(0, 1))
+    g_pbar = out.pop("dp").sum(axis=(0, 1))
+    out["da"], out["dp"], out["ddelta"] = ou_discretise_vjp(a, p, delta, g_abar, g_pbar)
+    return out
+
+
+def decode_step_ou(q, k, v, a, p, delta, r, lam, eta) -> dict:
+    """``decode_step`` with the gates of the OU parameters a, p, delta [H, dk]."""
+    abar, pbar = ou_discretise(a, p, delta)
+    S = np.shape(k)[0]
+    shape = (S,) + abar.shape
+    return decode_step(q, k, v, np.broadcast_to(abar, shape), np.broadcast_to(pbar, shape), r, lam, eta)

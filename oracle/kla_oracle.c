@@ -5,7 +5,7 @@
  * calls this file; only the test-suite, the smoke check and the CPU baseline
  * leg of the benchmark do.  It shares no code with the GPU path.
  *
- * What it computes (paper: Sec. 3.2 "Parallel Inference via Moebius and Affine
+ * What it computes (paper: Sec. 4.2 "Parallel Inference via Moebius and Affine
  * Scans", Theorem 1 with its gate view, Theorem 2, and Appendix A's state-
  * expanded matrix form, eqs. kla-prec-mat / kla-mean-mat, with the readout
  * of Algorithm 1):

@@ -12,7 +12,7 @@
 //
 // One workgroup per (batch, head, value tile of up to 64 channels).  The scan
 // waves redo the precision walk of each chunk from its saved start lam and
-// stage the chunk's dY tile; the MFMA waves (32 value channels each, G[dk, 32]
+// stage the chunk's dY tile; the MFMA waves (16 value channels each, G[dk, 16]
 // in registers) consume the previous round's chunk:
 //   dV^T[d, j] = sum_i dY^T[d, i] A[i, j] + sum_n Gs^T[d, n] Kn^T[n, j]
 //   G[n, d]   += sum_t Qp^T[n, t] dY[t, d]

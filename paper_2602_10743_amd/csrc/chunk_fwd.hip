@@ -11,7 +11,7 @@
 // (kla_mfma.hpp), accumulating in fp32.
 //
 // One workgroup per (batch, head, value tile of up to 64 channels): scan waves
-// walk chunk c while MFMA waves (32 value channels each, the state H[dk, 32]
+// walk chunk c while MFMA waves (16 value channels each, the state H[dk, 16]
 // in registers) consume chunk c - 1 -- attention tiles, readout, y, state
 // update; operands that run across the rows of a tile (Kn^T, V) are read with
 // transposing LDS reads (lds_tr8), so each tile is stored once.  The MFMA
