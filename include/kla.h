@@ -141,6 +141,53 @@ kla_status kla_decode_step(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t
                            const void* abar, const void* pbar, const void* r,
                            float* lam, float* eta, void* y, float* yvar, hipStream_t stream);
 
+/*
+ * OU gates (Sec. 4.1, eq. discretisation; Algorithm 1's OU-Discretisation
+ * steps).  The layer can take its decay and process noise from time-invariant
+ * parameters of an Ornstein-Uhlenbeck prior instead of per-token tensors: for
+ * head h and key slot n, mean reversion a > 0, diffusion scale p and step size
+ * delta > 0 give, for every token of every sequence,
+ *
+ *   abar[h,n] = exp(-a delta),   pbar[h,n] = p^2 (1 - exp(-2 a delta)) / (2 a)
+ *
+ * (formed in fp64 on the device, then rounded to fp32).  a, p, delta are
+ * [H, dk] fp32 device arrays; every other argument is as in the entry point of
+ * the same name above.  The gate gradients, summed over (b, t), reach the
+ * parameters by the chain rule: da, dp, ddelta are [H, dk] fp32, overwritten.
+ * Domain under KLA_CHECK=1: a > 0, delta > 0, p finite (and the rest as above).
+ */
+
+/* Workspace of kla_backward_ou: kla_backward_workspace plus the per-part token
+ * sums of the two gate gradients. */
+size_t kla_backward_ou_workspace(const kla_desc* desc, int with_saved);
+
+/* kla_forward with OU gates; its saved context serves kla_backward_ou. */
+kla_status kla_forward_ou(const kla_desc* desc,
+                          const void* q, const void* k, const void* v,
+                          const float* a, const float* p, const float* delta, const void* r,
+                          const float* lam0, const float* eta0,
+                          void* y, float* yvar, float* lamT, float* etaT,
+                          void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* kla_backward with OU gates: dq, dk, dv, dr (dtype), dlam0, deta0 as there, and
+ * the parameter gradients da, dp, ddelta [H, dk] fp32 (required).
+ * ws_bytes >= kla_backward_ou_workspace(desc, saved != NULL). */
+kla_status kla_backward_ou(const kla_desc* desc,
+                           const void* q, const void* k, const void* v,
+                           const float* a, const float* p, const float* delta, const void* r,
+                           const float* lam0, const float* eta0, const void* saved,
+                           const void* dy, const float* dlamT, const float* detaT,
+                           void* dq, void* dk, void* dv, float* da, float* dp, float* ddelta, void* dr,
+                           float* dlam0, float* deta0,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* kla_decode_step with OU gates (a, p, delta [H, dk] fp32, shared by the S
+ * sequences). */
+kla_status kla_decode_step_ou(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype,
+                              const void* q, const void* k, const void* v,
+                              const float* a, const float* p, const float* delta, const void* r,
+                              float* lam, float* eta, void* y, float* yvar, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char* kla_status_string(kla_status status);
 

@@ -19,7 +19,8 @@ import torch
 
 __all__ = ["kla_forward", "kla_backward", "kla_decode_step", "kla_status_string",
            "kla_forward_workspace", "kla_backward_workspace", "kla_saved_bytes",
-           "KLAError", "KLAFilter", "kla_filter", "library_path"]
+           "kla_forward_ou", "kla_backward_ou", "kla_decode_step_ou", "kla_backward_ou_workspace",
+           "KLAError", "KLAFilter", "kla_filter", "KLAFilterOU", "kla_filter_ou", "library_path"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 library_path = os.path.join(_HERE, "libkla.so")
@@ -64,6 +65,14 @@ def _load():
     lib.kla_backward.restype = ctypes.c_int
     lib.kla_decode_step.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
     lib.kla_decode_step.restype = ctypes.c_int
+    lib.kla_backward_ou_workspace.argtypes = [D, ctypes.c_int]
+    lib.kla_backward_ou_workspace.restype = ctypes.c_size_t
+    lib.kla_forward_ou.argtypes = [D] + [_VP] * 15 + [ctypes.c_size_t, _VP]
+    lib.kla_forward_ou.restype = ctypes.c_int
+    lib.kla_backward_ou.argtypes = [D] + [_VP] * 23 + [ctypes.c_size_t, _VP]
+    lib.kla_backward_ou.restype = ctypes.c_int
+    lib.kla_decode_step_ou.argtypes = [ctypes.c_int32] * 5 + [_VP] * 12
+    lib.kla_decode_step_ou.restype = ctypes.c_int
     lib.kla_status_string.argtypes = [ctypes.c_int]
     lib.kla_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -240,3 +249,147 @@ class KLAFilter(torch.autograd.Function):
 def kla_filter(q, k, v, a, p, r, lam0=None, eta0=None):
     """Differentiable filter: returns (y, lamT, etaT)."""
     return KLAFilter.apply(q, k, v, a, p, r, lam0, eta0)
+
+
+# ---- OU gates: time-invariant a, p, delta [H, dk] fp32 in place of per-token abar, pbar
+
+def _check_ou(a, p, delta, H, dk, dev):
+    for name, t in (("a", a), ("p", p), ("delta", delta)):
+        _f32(t, (H, dk), dev, name)
+
+
+def _check_inputs_ou(q, k, v, r):
+    if not q.is_cuda:
+        raise ValueError("KLA tensors must live on a GPU; the layer has no CPU path")
+    if q.dtype not in _DTYPES:
+        raise TypeError(f"unsupported dtype {q.dtype}; use float32 or bfloat16")
+    if q.dim() != 4:
+        raise ValueError("q must be [B, T, H, dk]")
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    for name, t, shape in (("k", k, (B, T, H, dk)), ("v", v, (B, T, H, dv)), ("r", r, (B, T, H))):
+        if tuple(t.shape) != shape:
+            raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {shape}")
+        if t.dtype != q.dtype or t.device != q.device:
+            raise ValueError(f"{name} must share q's dtype and device")
+    for name, t in (("q", q), ("k", k), ("v", v), ("r", r)):
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+
+
+def kla_backward_ou_workspace(desc: _Desc, with_saved: bool) -> int:
+    return int(_load().kla_backward_ou_workspace(ctypes.byref(desc), int(bool(with_saved))))
+
+
+def kla_forward_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, *, want_var: bool = False,
+                   want_state: bool = True, save: bool = False, y=None) -> dict:
+    """kla_forward with the gates of the OU parameters a, p, delta [H, dk] fp32."""
+    lib = _load()
+    _check_inputs_ou(q, k, v, r)
+    dev = q.device
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    _check_ou(a, p, delta, H, dk, dev)
+    lam0 = _f32(lam0, (B, H, dk), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    desc = _desc(q, v)
+    if y is None:
+        y = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    yvar = torch.empty((B, T, H), dtype=torch.float32, device=dev) if want_var else None
+    lamT = torch.empty((B, H, dk), dtype=torch.float32, device=dev) if want_state else None
+    etaT = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_state else None
+    nsaved = kla_saved_bytes(desc) if save else 0
+    saved = torch.empty(max(nsaved, 1), dtype=torch.uint8, device=dev) if save else None
+    nws = kla_forward_workspace(desc)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    st = lib.kla_forward_ou(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(delta), _p(r), _p(lam0),
+                            _p(eta0), _p(y), _p(yvar), _p(lamT), _p(etaT), _p(saved if nsaved else None), _p(ws),
+                            nws, _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_forward_ou")
+    return {"y": y, "yvar": yvar, "lamT": lamT, "etaT": etaT, "saved": saved if nsaved else None}
+
+
+def kla_backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=None, *, saved=None,
+                    want_init_grads: bool = True) -> dict:
+    """Gradients of kla_forward_ou: dq, dk, dv, dr in the input dtype; da, dp,
+    ddelta [H, dk] fp32; dlam0, deta0 in fp32 when asked."""
+    lib = _load()
+    _check_inputs_ou(q, k, v, r)
+    dev = q.device
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    _check_ou(a, p, delta, H, dk, dev)
+    lam0 = _f32(lam0, (B, H, dk), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    dlamT = _f32(dlamT, (B, H, dk), dev, "dlamT")
+    detaT = _f32(detaT, (B, H, dk, dv), dev, "detaT")
+    if tuple(dy.shape) != (B, T, H, dv) or dy.dtype != q.dtype or not dy.is_contiguous():
+        raise ValueError("dy must be a contiguous [B, T, H, dv] tensor in the input dtype")
+    desc = _desc(q, v)
+    out = {n: torch.empty_like(x) for n, x in (("dq", q), ("dk", k), ("dv", v), ("dr", r))}
+    for n in ("da", "dp", "ddelta"):
+        out[n] = torch.empty((H, dk), dtype=torch.float32, device=dev)
+    dlam0 = torch.empty((B, H, dk), dtype=torch.float32, device=dev) if want_init_grads else None
+    deta0 = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_init_grads else None
+    nws = kla_backward_ou_workspace(desc, saved is not None)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    st = lib.kla_backward_ou(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(delta), _p(r), _p(lam0),
+                             _p(eta0), _p(saved), _p(dy), _p(dlamT), _p(detaT), _p(out["dq"]), _p(out["dk"]),
+                             _p(out["dv"]), _p(out["da"]), _p(out["dp"]), _p(out["ddelta"]), _p(out["dr"]),
+                             _p(dlam0), _p(deta0), _p(ws), nws, _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_backward_ou")
+    out["dlam0"] = dlam0
+    out["deta0"] = deta0
+    return out
+
+
+def kla_decode_step_ou(q, k, v, a, p, delta, r, lam, eta, *, want_var: bool = False, y=None) -> dict:
+    """kla_decode_step with the gates of the OU parameters a, p, delta [H, dk] fp32."""
+    lib = _load()
+    if not q.is_cuda or q.dtype not in _DTYPES:
+        raise ValueError("decode inputs must be fp32/bf16 GPU tensors")
+    S, H, dk = q.shape
+    dv = v.shape[-1]
+    for name, t, shape in (("k", k, (S, H, dk)), ("v", v, (S, H, dv)), ("r", r, (S, H))):
+        if tuple(t.shape) != shape or t.dtype != q.dtype or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {shape} tensor in q's dtype")
+    _check_ou(a, p, delta, H, dk, q.device)
+    _f32(lam, (S, H, dk), q.device, "lam")
+    _f32(eta, (S, H, dk, dv), q.device, "eta")
+    if y is None:
+        y = torch.empty((S, H, dv), dtype=q.dtype, device=q.device)
+    yvar = torch.empty((S, H), dtype=torch.float32, device=q.device) if want_var else None
+    st = lib.kla_decode_step_ou(S, H, dk, dv, _DTYPES[q.dtype], _p(q), _p(k), _p(v), _p(a), _p(p), _p(delta),
+                                _p(r), _p(lam), _p(eta), _p(y), _p(yvar), _stream(q.device))
+    if st != 0:
+        raise KLAError(st, "kla_decode_step_ou")
+    return {"y": y, "yvar": yvar, "lam": lam, "eta": eta}
+
+
+class KLAFilterOU(torch.autograd.Function):
+    """Autograd wrapper: y, lamT, etaT = filter(q, k, v, a, p, delta, r, lam0, eta0) with OU gates."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, a, p, delta, r, lam0, eta0):
+        out = kla_forward_ou(q, k, v, a, p, delta, r, lam0, eta0, want_state=True, save=True)
+        ctx.save_for_backward(q, k, v, a, p, delta, r, lam0, eta0)
+        ctx.saved_ctx = out["saved"]
+        return out["y"], out["lamT"], out["etaT"]
+
+    @staticmethod
+    def backward(ctx, dy, dlamT, detaT):
+        q, k, v, a, p, delta, r, lam0, eta0 = ctx.saved_tensors
+        dy = torch.zeros_like(q[..., :1].expand(*q.shape[:3], v.shape[-1])).contiguous() if dy is None \
+            else dy.contiguous()
+        g = kla_backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy,
+                            None if dlamT is None else dlamT.contiguous(),
+                            None if detaT is None else detaT.contiguous(), saved=ctx.saved_ctx)
+        return (g["dq"], g["dk"], g["dv"], g["da"], g["dp"], g["ddelta"], g["dr"],
+                g["dlam0"] if lam0 is not None else None, g["deta0"] if eta0 is not None else None)
+
+
+def kla_filter_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None):
+    """Differentiable filter with OU gates: returns (y, lamT, etaT)."""
+    return KLAFilterOU.apply(q, k, v, a, p, delta, r, lam0, eta0)

@@ -39,6 +39,11 @@
 // the phases.  The next chunk's inputs go straight into LDS, requested during
 // the first pass of a round's adjoint walk; the chunk's saved state rows come
 // into wave 0's registers at the start of its round.
+//
+// TI (gates from OU parameters, the same for every token of a key slot): abar
+// and pbar are formed once per lane and not loaded; dabar and dpbar are not
+// stored per token but summed over the lane's tokens, one part per (batch row,
+// wave of the pair), for the parameter gradients.
 #include <type_traits>
 
 #include "kla_chunk.hpp"
@@ -125,7 +130,7 @@ __device__ __forceinline__ void buf_st32(float v, rsrc_t r, uint32_t voff) {
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, 0, 0);
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool TI>
 __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, BwdArgs g,
                                                                        const float* __restrict__ saved_lam,
                                                                        const float* __restrict__ saved_H,
@@ -133,6 +138,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
     using Cfg = DkCfg<DK, DV>;
     constexpr int NP = Cfg::NP, NW = Cfg::NW, KSD = Cfg::KSD, NRD = Cfg::NRD, LQ2 = Cfg::LQ2, LX = Cfg::LX;
     constexpr int NG = Cfg::NG;
+    constexpr int NST = TI ? 3 : 5;   // gradient stores per round: dq, dk(, dabar, dpbar) and dr
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ __align__(16) uint16_t s_out[NP * 4 * kC * 16];
     __shared__ __align__(16) float s_drc[NP * kC * 17];
@@ -172,6 +178,12 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
     }
     ST += __shfl_xor(ST, 16, 64);
     ST += __shfl_xor(ST, 32, 64);
+    // time-invariant gates of the slot and the lane's sums of their gradients
+    float ca = 0.f, cp = 0.f, sum_da = 0.f, sum_dp = 0.f;
+    if constexpr (TI) {
+        const int o = h * DK + n0w + nl;
+        ou_gates(g.ou_a[o], g.ou_p[o], g.ou_d[o], ca, cp);
+    }
 
     // G^T[d, n] for d = 16 rd + 4 g4 + rr, n = n0w + l16 (carried by wave 1 of the pair)
     f32x4 GT[NRD];
@@ -183,10 +195,11 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
 
     // ---- requests of chunk cn into buffer bb (chunks outside the sequence: empty, writing
     // zeros), one load per part so that they can be spread over a round:
-    //   wave 0: 0..3  abar, pbar, k, q of the pair's slots (1 KiB each, lane -> (t = lane / 2, 8 slots))
+    //   wave 0: 0..3  abar, pbar, k, q of the pair's slots (1 KiB each, lane -> (t = lane / 2, 8 slots));
+    //                 TI: 0, 1  k, q
     //   wave 1: 0, 1  r (lanes >= nt read as 0) and the chunk-start lam of the 16 slots
     //   then this wave's share of the dY and V tiles (loads i = wave, wave + NW, ...), swizzled
-    const int nin = e == 0 ? 4 : 2;
+    const int nin = e == 0 && !TI ? 4 : 2;
     const int nvw = wave < Cfg::NVL ? (Cfg::NVL - wave + NW - 1) / NW : 0;
     const int nparts = nin + 2 * nvw;
     auto issue_part = [&](int cn, int bb, int part) {
@@ -195,9 +208,10 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
         const size_t tok0 = seq0 + t0;
         if (part < nin) {
             if (e == 0) {
-                const uint16_t* src = part == 0 ? a : part == 1 ? p : part == 2 ? k : q;
+                const int slot = TI ? part + 2 : part;   // staging slots: abar, pbar, k, q
+                const uint16_t* src = slot == 0 ? a : slot == 1 ? p : slot == 2 ? k : q;
                 const uint32_t kbytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + 16) * 2 : 0u;
-                uint16_t* stg = reinterpret_cast<uint16_t*>(wb + Cfg::STG) + (bb * 4 + part) * kC * 16;
+                uint16_t* stg = reinterpret_cast<uint16_t*>(wb + Cfg::STG) + (bb * 4 + slot) * kC * 16;
                 buf_ld128_lds(make_rsrc(src + (tok0 * H + h) * DK + n0w, kbytes), stg,
                               (uint32_t)(lane >> 1) * tok_k + (lane & 1) * 16);
             } else if (part == 0) {
@@ -240,16 +254,16 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                     h0[ks][1] = *reinterpret_cast<const float4*>(H0 + 32 * ks + 8 * g4 + 4);
                 }
                 // this chunk's requests (issued last round) have landed: younger are only the
-                // last round's 5 stores and the 2 KSD state loads just issued
+                // last round's NST stores and the 2 KSD state loads just issued
                 if (it == 0)
                     wait_vm_le<2 * KSD>();
                 else
-                    wait_vm_le<5 + 2 * KSD>();
+                    wait_vm_le<NST + 2 * KSD>();
             } else {
                 if (it == 0)
                     wait_vm_le<0>();
                 else
-                    wait_vm_le<5>();
+                    wait_vm_le<NST>();
             }
             barrier_lds();   // every wave's share of the dY / V tiles and staging is in
 
@@ -265,8 +279,12 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             float* sY = reinterpret_cast<float*>(wb + Cfg::YT);
             float* sPC = reinterpret_cast<float*>(wb + Cfg::PC);
             float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
-            auto in_a = [&](int t) { return __uint_as_float((uint32_t)stg[(0 * kC + t) * 16 + nl] << 16); };
-            auto in_p = [&](int t) { return __uint_as_float((uint32_t)stg[(1 * kC + t) * 16 + nl] << 16); };
+            auto in_a = [&](int t) {
+                return TI ? ca : __uint_as_float((uint32_t)stg[(0 * kC + t) * 16 + nl] << 16);
+            };
+            auto in_p = [&](int t) {
+                return TI ? cp : __uint_as_float((uint32_t)stg[(1 * kC + t) * 16 + nl] << 16);
+            };
             auto in_k = [&](int t) { return __uint_as_float((uint32_t)stg[(2 * kC + t) * 16 + nl] << 16); };
             auto in_q = [&](int t) { return __uint_as_float((uint32_t)stg[(3 * kC + t) * 16 + nl] << 16); };
             auto in_r = [&](int t) { return __uint_as_float(rw[t] << 16); };
@@ -542,11 +560,19 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 const float dpv = -lpr2_[j] * drho;
                 drc[t * 17 + nl] = fmaf(kk_[j], gl, kdk_[j]);
                 cc = fmaf(al_[j], gl, -be_[j] * SS);
-                const uint32_t pq = cvt_pk_bf16(dq_[j], dkv), pa = cvt_pk_bf16(dav, dpv);
+                const uint32_t pq = cvt_pk_bf16(dq_[j], dkv);
                 so[(0 * kC + t) * 16 + nl] = static_cast<uint16_t>(pq);
                 so[(1 * kC + t) * 16 + nl] = static_cast<uint16_t>(pq >> 16);
-                so[(2 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa);
-                so[(3 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa >> 16);
+                if constexpr (TI) {
+                    if (FULL || t < nt) {
+                        sum_da += dav;
+                        sum_dp += dpv;
+                    }
+                } else {
+                    const uint32_t pa = cvt_pk_bf16(dav, dpv);
+                    so[(2 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa);
+                    so[(3 * kC + t) * 16 + nl] = static_cast<uint16_t>(pa >> 16);
+                }
             }
 
             // ---- stores of this wave's 16 tokens: [t][16] rows of dq, dk, dabar, dpbar (lanes
@@ -563,10 +589,12 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                           make_rsrc(static_cast<uint16_t*>(g.dq) + ek, kbytes), koff);
                 buf_st128(*reinterpret_cast<const uint4*>(o + 1 * kC * 16),
                           make_rsrc(static_cast<uint16_t*>(g.dk) + ek, kbytes), koff);
-                buf_st128(*reinterpret_cast<const uint4*>(o + 2 * kC * 16),
-                          make_rsrc(static_cast<uint16_t*>(g.da) + ek, kbytes), koff);
-                buf_st128(*reinterpret_cast<const uint4*>(o + 3 * kC * 16),
-                          make_rsrc(static_cast<uint16_t*>(g.dp) + ek, kbytes), koff);
+                if constexpr (!TI) {
+                    buf_st128(*reinterpret_cast<const uint4*>(o + 2 * kC * 16),
+                              make_rsrc(static_cast<uint16_t*>(g.da) + ek, kbytes), koff);
+                    buf_st128(*reinterpret_cast<const uint4*>(o + 3 * kC * 16),
+                              make_rsrc(static_cast<uint16_t*>(g.dp) + ek, kbytes), koff);
+                }
                 const int t = 16 * E + l16;
                 float acc = 0.f;
 #pragma unroll
@@ -590,6 +618,18 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
     }
     wait_vm_all();   // the requests for the chunk before the first have landed before exit
     if (g.dlam0 && e == 0 && g4 == 0) g.dlam0[(size_t)bh * DK + n0w + nl] = cT;
+    if constexpr (TI) {   // part e * B + b of the token sums: the wave's four token groups added
+        sum_da += __shfl_xor(sum_da, 16, 64);
+        sum_da += __shfl_xor(sum_da, 32, 64);
+        sum_dp += __shfl_xor(sum_dp, 16, 64);
+        sum_dp += __shfl_xor(sum_dp, 32, 64);
+        if (g4 == 0) {
+            const size_t np = (size_t)2 * s.B * H * DK;
+            const size_t o = ((size_t)(e * s.B + b) * H + h) * DK + n0w + nl;
+            g.ou_part[o] = sum_da;
+            g.ou_part[np + o] = sum_dp;
+        }
+    }
 }
 
 // dr = sum of the per-pair partials, stored in the input dtype
@@ -601,11 +641,11 @@ __global__ void dr_combine_kernel(const float* __restrict__ part, int nparts, si
     dr[i] = f32_to_bf16(acc);
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool TI>
 hipError_t launch_dk(const Shape& s, const BwdArgs& a, const float* saved_lam, const float* saved_H, float* dr_part,
                      hipStream_t st) {
     using Cfg = DkCfg<DK, DV>;
-    auto kern = bwd_dk_kernel<DK, DV>;
+    auto kern = bwd_dk_kernel<DK, DV, TI>;
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::BYTES);
     if (attr != hipSuccess) return attr;
@@ -628,6 +668,9 @@ hipError_t launch_dk(const Shape& s, const BwdArgs& a, const float* saved_lam, c
 
 bool chunked_bwd_supported(const Shape& s) { return s.bf16 && s.dk >= 32 && s.dv >= 32; }
 
+// one part per (wave of a pair, batch row)
+int chunked_ou_parts(const Shape& s) { return 2 * s.B; }
+
 // per-pair dr partials: dk / 16 of them per token
 size_t chunked_bwd_workspace(const Shape& s) { return (size_t)(s.dk / 16) * s.B * s.T * s.H * sizeof(float); }
 
@@ -636,8 +679,10 @@ hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void*
     const float* saved_lam = static_cast<const float*>(saved);
     const float* saved_H = saved_lam + (size_t)s.B * s.H * nchunk * s.dk;
     float* dr_part = static_cast<float*>(ws);
-#define KLA_DK_CASE(DK_, DV_) \
-    if (s.dk == DK_ && s.dv == DV_) return launch_dk<DK_, DV_>(s, a, saved_lam, saved_H, dr_part, st);
+#define KLA_DK_CASE(DK_, DV_)                                                      \
+    if (s.dk == DK_ && s.dv == DV_)                                                \
+        return a.ou_a ? launch_dk<DK_, DV_, true>(s, a, saved_lam, saved_H, dr_part, st) \
+                      : launch_dk<DK_, DV_, false>(s, a, saved_lam, saved_H, dr_part, st);
 #define KLA_DK_ROW(DK_) KLA_DK_CASE(DK_, 32) KLA_DK_CASE(DK_, 64) KLA_DK_CASE(DK_, 128)
     KLA_DK_ROW(32) KLA_DK_ROW(64) KLA_DK_ROW(128)
 #undef KLA_DK_ROW

@@ -24,7 +24,7 @@
 namespace kla {
 namespace {
 
-template <int DK, int DV>
+template <int DK, int DV, bool TI>
 __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void bwd_dv_kernel(Shape s, BwdArgs g,
                                                                           const float* __restrict__ saved_lam) {
     using Cfg = ChunkCfg<DK, DV>;
@@ -46,8 +46,8 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void bwd_dv_kernel(Shape 
         const ScanSrc sc{static_cast<const uint16_t*>(g.a), static_cast<const uint16_t*>(g.p),
                          static_cast<const uint16_t*>(g.k), static_cast<const uint16_t*>(g.q),
                          static_cast<const uint16_t*>(g.r), static_cast<const uint16_t*>(g.dy),
-                         tile * DVT, seq0, H, h, T, nchunk, bh};
-        scan_wave<Cfg, false, true>(smem, wave, lane, sc, saved_lam, nullptr);
+                         tile * DVT, seq0, H, h, T, nchunk, bh, g.ou_a, g.ou_p, g.ou_d};
+        scan_wave<Cfg, false, true, TI>(smem, wave, lane, sc, saved_lam, nullptr);
         return;
     }
 
@@ -185,10 +185,10 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void bwd_dv_kernel(Shape 
     }
 }
 
-template <int DK, int DV>
+template <int DK, int DV, bool TI>
 hipError_t launch_dv(const Shape& s, const BwdArgs& a, const float* saved_lam, hipStream_t st) {
     using Cfg = ChunkCfg<DK, DV>;
-    auto kern = bwd_dv_kernel<DK, DV>;
+    auto kern = bwd_dv_kernel<DK, DV, TI>;
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::BYTES);
     if (attr != hipSuccess) return attr;
@@ -200,8 +200,10 @@ hipError_t launch_dv(const Shape& s, const BwdArgs& a, const float* saved_lam, h
 }  // namespace
 
 hipError_t launch_backward_dv(const Shape& s, const BwdArgs& a, const float* saved_lam, hipStream_t st) {
-#define KLA_DV_CASE(DK_, DV_) \
-    if (s.dk == DK_ && s.dv == DV_) return launch_dv<DK_, DV_>(s, a, saved_lam, st);
+#define KLA_DV_CASE(DK_, DV_)                                          \
+    if (s.dk == DK_ && s.dv == DV_)                                    \
+        return a.ou_a ? launch_dv<DK_, DV_, true>(s, a, saved_lam, st) \
+                      : launch_dv<DK_, DV_, false>(s, a, saved_lam, st);
 #define KLA_DV_ROW(DK_) KLA_DV_CASE(DK_, 32) KLA_DV_CASE(DK_, 64) KLA_DV_CASE(DK_, 128)
     KLA_DV_ROW(32) KLA_DV_ROW(64) KLA_DV_ROW(128)
 #undef KLA_DV_ROW

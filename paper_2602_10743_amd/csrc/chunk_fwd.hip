@@ -15,14 +15,15 @@
 // in registers) consume chunk c - 1 -- attention tiles, readout, y, state
 // update; operands that run across the rows of a tile (Kn^T, V) are read with
 // transposing LDS reads (lds_tr8), so each tile is stored once.  The MFMA
-// waves only store; all loads come from the scan waves.
+// waves only store; all loads come from the scan waves.  TI: the gates come
+// from OU parameters (time-invariant per key slot) instead of per-token tensors.
 #include "kla_chunk.hpp"
 #include "kla_internal.hpp"
 
 namespace kla {
 namespace {
 
-template <int DK, int DV, bool YV>
+template <int DK, int DV, bool YV, bool TI>
 __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape s, FwdArgs g, float* saved_lam,
                                                                          float* saved_H) {
     using Cfg = ChunkCfg<DK, DV>;
@@ -50,8 +51,8 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
 
     if (wave < NSW) {
         // ================================================================ scan waves
-        const ScanSrc sc{a, p, k, q, r, v, tile * DVT, seq0, H, h, T, nchunk, bh};
-        const float x = scan_wave<Cfg, YV, false>(smem, wave, lane, sc, g.lam0, saved_lam);
+        const ScanSrc sc{a, p, k, q, r, v, tile * DVT, seq0, H, h, T, nchunk, bh, g.ou_a, g.ou_p, g.ou_d};
+        const float x = scan_wave<Cfg, YV, false, TI>(smem, wave, lane, sc, g.lam0, saved_lam);
         if (g.lamT && lane < SW && tile == 0) g.lamT[(size_t)bh * DK + wave * SW + lane] = x;
     } else {
         // ================================================================ MFMA waves
@@ -208,10 +209,10 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
     }
 }
 
-template <int DK, int DV, bool YV>
+template <int DK, int DV, bool YV, bool TI>
 hipError_t launch_fwd_v(const Shape& s, const FwdArgs& a, float* saved_lam, float* saved_H, hipStream_t st) {
     using Cfg = ChunkCfg<DK, DV>;
-    auto kern = fwd_chunk_kernel<DK, DV, YV>;
+    auto kern = fwd_chunk_kernel<DK, DV, YV, TI>;
     // more than 64 KiB of LDS must be opted into once per kernel (thread-safe static init)
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::BYTES);
@@ -221,11 +222,15 @@ hipError_t launch_fwd_v(const Shape& s, const FwdArgs& a, float* saved_lam, floa
     return hipGetLastError();
 }
 
-// the readout variance adds a cross-lane sum per token, so it is a separate instantiation
+// the readout variance adds a cross-lane sum per token, so it is a separate
+// instantiation, as are the time-invariant gates
 template <int DK, int DV>
 hipError_t launch_fwd(const Shape& s, const FwdArgs& a, float* saved_lam, float* saved_H, hipStream_t st) {
-    return a.yvar ? launch_fwd_v<DK, DV, true>(s, a, saved_lam, saved_H, st)
-                  : launch_fwd_v<DK, DV, false>(s, a, saved_lam, saved_H, st);
+    if (a.ou_a)
+        return a.yvar ? launch_fwd_v<DK, DV, true, true>(s, a, saved_lam, saved_H, st)
+                      : launch_fwd_v<DK, DV, false, true>(s, a, saved_lam, saved_H, st);
+    return a.yvar ? launch_fwd_v<DK, DV, true, false>(s, a, saved_lam, saved_H, st)
+                  : launch_fwd_v<DK, DV, false, false>(s, a, saved_lam, saved_H, st);
 }
 
 }  // namespace

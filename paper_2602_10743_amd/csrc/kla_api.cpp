@@ -46,18 +46,21 @@ bool all_aligned(P... ps) {
 namespace kla {
 hipError_t launch_validate(const Shape& s, const void* q, const void* k, const void* v, const void* a,
                            const void* p, const void* r, const float* lam0, const float* eta0, int T,
-                           int* flag, hipStream_t st);
+                           int* flag, hipStream_t st, const float* ou_a, const float* ou_p, const float* ou_d);
 }
 
 namespace {
 
 // Domain check of the inputs (KLA_CHECK=1): synchronous; returns KLA_ERR_NUMERIC
-// when any value is outside abar in (0,1], pbar >= 0, r > 0, lam0 > 0, finite.
+// when any value is outside abar in (0,1], pbar >= 0, r > 0, lam0 > 0, finite
+// (OU parameters: a > 0, delta > 0, p finite).
 kla_status validate(const kla::Shape& s, int T, const void* q, const void* k, const void* v, const void* a,
                     const void* p, const void* r, const float* lam0, const float* eta0, void* flag_ws,
-                    hipStream_t st) {
+                    hipStream_t st, const float* ou_a = nullptr, const float* ou_p = nullptr,
+                    const float* ou_d = nullptr) {
     int* flag = static_cast<int*>(flag_ws);
-    if (kla::launch_validate(s, q, k, v, a, p, r, lam0, eta0, T, flag, st) != hipSuccess) return KLA_ERR_HIP;
+    if (kla::launch_validate(s, q, k, v, a, p, r, lam0, eta0, T, flag, st, ou_a, ou_p, ou_d) != hipSuccess)
+        return KLA_ERR_HIP;
     int host = 0;
     if (hipMemcpyAsync(&host, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess) return KLA_ERR_HIP;
     if (hipStreamSynchronize(st) != hipSuccess) return KLA_ERR_HIP;
@@ -93,58 +96,71 @@ size_t kla_backward_workspace(const kla_desc* desc, int with_saved) {
     return kAlign + round_up(kla::backward_recurrent_workspace(s));
 }
 
-kla_status kla_forward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
-                       const void* pbar, const void* r, const float* lam0, const float* eta0, void* y,
-                       float* yvar, float* lamT, float* etaT, void* saved, void* ws, size_t ws_bytes,
-                       hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The forward behind both gate forms: per-token abar / pbar in a.a, a.p, or OU
+// parameters in a.ou_a, a.ou_p, a.ou_d.
+kla_status forward_impl(const kla_desc* desc, const kla::FwdArgs& a, bool ou, void* saved, void* ws,
+                        size_t ws_bytes, hipStream_t stream) {
     kla_status st = check_desc(desc);
     if (st != KLA_OK) return st;
+    if (ou && (!a.ou_a || !a.ou_p || !a.ou_d)) return KLA_ERR_NULL;
     // with T == 0 the per-token tensors are empty and may be NULL
-    if (desc->T > 0 && (!q || !k || !v || !abar || !pbar || !r || !y)) return KLA_ERR_NULL;
-    if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, y, (void*)yvar,
-                     (void*)lamT, (void*)etaT, saved, ws))
+    if (desc->T > 0 && (!a.q || !a.k || !a.v || (!ou && (!a.a || !a.p)) || !a.r || !a.y)) return KLA_ERR_NULL;
+    if (!all_aligned(a.q, a.k, a.v, a.a, a.p, a.r, (const void*)a.lam0, (const void*)a.eta0, a.y, (void*)a.yvar,
+                     (void*)a.lamT, (void*)a.etaT, saved, ws, (const void*)a.ou_a, (const void*)a.ou_p,
+                     (const void*)a.ou_d))
         return KLA_ERR_ALIGN;
     if (!ws || ws_bytes < kla_forward_workspace(desc)) return KLA_ERR_WORKSPACE;
     const kla::Shape s = shape_of(desc);
     if (check_mode()) {
-        st = validate(s, s.T, q, k, v, abar, pbar, r, lam0, eta0, ws, stream);
+        st = validate(s, s.T, a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, ws, stream, a.ou_a, a.ou_p, a.ou_d);
         if (st != KLA_OK) return st;
     }
-    kla::FwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, y, yvar, lamT, etaT};
     hipError_t e = kla::chunked_supported(s) ? kla::launch_forward_chunked(s, a, saved, stream)
                                              : kla::launch_forward_recurrent(s, a, stream);
     return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 
-kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
-                        const void* pbar, const void* r, const float* lam0, const float* eta0, const void* saved,
-                        const void* dy, const float* dlamT, const float* detaT, void* dq, void* dk, void* dv,
-                        void* dabar, void* dpbar, void* dr, float* dlam0, float* deta0, void* ws,
-                        size_t ws_bytes, hipStream_t stream) {
+int ou_parts(const kla::Shape& s) {
+    return kla::chunked_bwd_supported(s) ? kla::chunked_ou_parts(s) : kla::recurrent_ou_parts(s);
+}
+
+// The backward behind both gate forms.  With OU parameters the gate gradients
+// are summed into parts at the end of the workspace and reduced into the
+// parameter gradients da, dp, dd.
+kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const void* saved, float* da, float* dp,
+                         float* dd, void* ws, size_t ws_bytes, hipStream_t stream) {
     kla_status st = check_desc(desc);
     if (st != KLA_OK) return st;
-    if (desc->T > 0 && (!q || !k || !v || !abar || !pbar || !r || !dy || !dq || !dk || !dv || !dabar || !dpbar ||
-                        !dr))
+    if (ou && (!a.ou_a || !a.ou_p || !a.ou_d || !da || !dp || !dd)) return KLA_ERR_NULL;
+    if (desc->T > 0 && (!a.q || !a.k || !a.v || (!ou && (!a.a || !a.p)) || !a.r || !a.dy || !a.dq || !a.dk ||
+                        !a.dv || (!ou && (!a.da || !a.dp)) || !a.dr))
         return KLA_ERR_NULL;
-    if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, saved, dy,
-                     (const void*)dlamT, (const void*)detaT, dq, dk, dv, dabar, dpbar, dr, (void*)dlam0,
-                     (void*)deta0, ws))
+    if (!all_aligned(a.q, a.k, a.v, a.a, a.p, a.r, (const void*)a.lam0, (const void*)a.eta0, saved, a.dy,
+                     (const void*)a.dlamT, (const void*)a.detaT, a.dq, a.dk, a.dv, a.da, a.dp, a.dr,
+                     (void*)a.dlam0, (void*)a.deta0, ws, (const void*)a.ou_a, (const void*)a.ou_p,
+                     (const void*)a.ou_d, (void*)da, (void*)dp, (void*)dd))
         return KLA_ERR_ALIGN;
-    if (!ws || ws_bytes < kla_backward_workspace(desc, saved != nullptr)) return KLA_ERR_WORKSPACE;
+    const size_t need = ou ? kla_backward_ou_workspace(desc, saved != nullptr)
+                           : kla_backward_workspace(desc, saved != nullptr);
+    if (!ws || ws_bytes < need) return KLA_ERR_WORKSPACE;
     const kla::Shape s = shape_of(desc);
     if (check_mode()) {
-        st = validate(s, s.T, q, k, v, abar, pbar, r, lam0, eta0, ws, stream);
+        st = validate(s, s.T, a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, ws, stream, a.ou_a, a.ou_p, a.ou_d);
         if (st != KLA_OK) return st;
     }
-    kla::BwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT, detaT, dq, dk, dv, dabar, dpbar, dr,
-                   dlam0, deta0};
+    if (ou) a.ou_part = reinterpret_cast<float*>(static_cast<char*>(ws) + kla_backward_workspace(desc, saved != nullptr));
     char* work = static_cast<char*>(ws) + kAlign;
     hipError_t e;
     if (kla::chunked_bwd_supported(s)) {
         if (!saved) {
             char* ctx = work + round_up(kla::chunked_bwd_workspace(s));
             void* yscratch = ctx + round_up(kla::chunked_saved_bytes(s));
-            kla::FwdArgs f{q, k, v, abar, pbar, r, lam0, eta0, yscratch, nullptr, nullptr, nullptr};
+            kla::FwdArgs f{a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, yscratch, nullptr, nullptr, nullptr,
+                           a.ou_a, a.ou_p, a.ou_d};
             e = kla::launch_forward_chunked(s, f, ctx, stream);
             if (e != hipSuccess) return KLA_ERR_HIP;
             saved = ctx;
@@ -153,20 +169,86 @@ kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, cons
     } else {
         e = kla::launch_backward_recurrent(s, a, work, stream);
     }
+    if (e == hipSuccess && ou)
+        e = kla::launch_ou_param_grads(s.H, s.dk, ou_parts(s), a.ou_part, a.ou_a, a.ou_p, a.ou_d, da, dp, dd, stream);
     return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+kla_status decode_impl(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const kla::DecodeArgs& a,
+                       bool ou, hipStream_t stream) {
+    kla_desc d{S, 1, H, dk, dv, dtype};
+    kla_status st = check_desc(&d);
+    if (st != KLA_OK) return st;
+    if (!a.q || !a.k || !a.v || (!ou && (!a.a || !a.p)) || !a.r || !a.lam || !a.eta || !a.y) return KLA_ERR_NULL;
+    if (ou && (!a.ou_a || !a.ou_p || !a.ou_d)) return KLA_ERR_NULL;
+    if (!all_aligned(a.q, a.k, a.v, a.a, a.p, a.r, (void*)a.lam, (void*)a.eta, a.y, (void*)a.yvar,
+                     (const void*)a.ou_a, (const void*)a.ou_p, (const void*)a.ou_d))
+        return KLA_ERR_ALIGN;
+    return kla::launch_decode_step(shape_of(&d), a, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+kla_status kla_forward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
+                       const void* pbar, const void* r, const float* lam0, const float* eta0, void* y,
+                       float* yvar, float* lamT, float* etaT, void* saved, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+    return forward_impl(desc, kla::FwdArgs{q, k, v, abar, pbar, r, lam0, eta0, y, yvar, lamT, etaT}, false, saved,
+                        ws, ws_bytes, stream);
+}
+
+kla_status kla_forward_ou(const kla_desc* desc, const void* q, const void* k, const void* v, const float* a,
+                          const float* p, const float* delta, const void* r, const float* lam0, const float* eta0,
+                          void* y, float* yvar, float* lamT, float* etaT, void* saved, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
+    return forward_impl(desc,
+                        kla::FwdArgs{q, k, v, nullptr, nullptr, r, lam0, eta0, y, yvar, lamT, etaT, a, p, delta},
+                        true, saved, ws, ws_bytes, stream);
+}
+
+kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
+                        const void* pbar, const void* r, const float* lam0, const float* eta0, const void* saved,
+                        const void* dy, const float* dlamT, const float* detaT, void* dq, void* dk, void* dv,
+                        void* dabar, void* dpbar, void* dr, float* dlam0, float* deta0, void* ws,
+                        size_t ws_bytes, hipStream_t stream) {
+    const kla::BwdArgs a{q,  k,  v,  abar,  pbar,  r,  lam0, eta0,  dy, dlamT,
+                         detaT, dq, dk, dv, dabar, dpbar, dr, dlam0, deta0};
+    return backward_impl(desc, a, false, saved, nullptr, nullptr, nullptr, ws, ws_bytes, stream);
+}
+
+size_t kla_backward_ou_workspace(const kla_desc* desc, int with_saved) {
+    if (check_desc(desc) != KLA_OK) return 0;
+    const kla::Shape s = shape_of(desc);
+    return kla_backward_workspace(desc, with_saved) + round_up((size_t)2 * ou_parts(s) * s.H * s.dk * sizeof(float));
+}
+
+kla_status kla_backward_ou(const kla_desc* desc, const void* q, const void* k, const void* v, const float* a,
+                           const float* p, const float* delta, const void* r, const float* lam0, const float* eta0,
+                           const void* saved, const void* dy, const float* dlamT, const float* detaT, void* dq,
+                           void* dk, void* dv, float* da, float* dp, float* ddelta, void* dr, float* dlam0,
+                           float* deta0, void* ws, size_t ws_bytes, hipStream_t stream) {
+    kla::BwdArgs g{q,  k,  v,       nullptr, nullptr, r,  lam0,  eta0,  dy, dlamT,
+                   detaT, dq, dk, dv, nullptr, nullptr, dr, dlam0, deta0};
+    g.ou_a = a;
+    g.ou_p = p;
+    g.ou_d = delta;
+    return backward_impl(desc, g, true, saved, da, dp, ddelta, ws, ws_bytes, stream);
 }
 
 kla_status kla_decode_step(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,
                            const void* k, const void* v, const void* abar, const void* pbar, const void* r,
                            float* lam, float* eta, void* y, float* yvar, hipStream_t stream) {
-    kla_desc d{S, 1, H, dk, dv, dtype};
-    kla_status st = check_desc(&d);
-    if (st != KLA_OK) return st;
-    if (!q || !k || !v || !abar || !pbar || !r || !lam || !eta || !y) return KLA_ERR_NULL;
-    if (!all_aligned(q, k, v, abar, pbar, r, (void*)lam, (void*)eta, y, (void*)yvar)) return KLA_ERR_ALIGN;
-    const kla::Shape s = shape_of(&d);
-    kla::DecodeArgs a{q, k, v, abar, pbar, r, lam, eta, y, yvar};
-    return kla::launch_decode_step(s, a, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+    return decode_impl(S, H, dk, dv, dtype, kla::DecodeArgs{q, k, v, abar, pbar, r, lam, eta, y, yvar}, false,
+                       stream);
+}
+
+kla_status kla_decode_step_ou(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,
+                              const void* k, const void* v, const float* a, const float* p, const float* delta,
+                              const void* r, float* lam, float* eta, void* y, float* yvar, hipStream_t stream) {
+    return decode_impl(S, H, dk, dv, dtype,
+                       kla::DecodeArgs{q, k, v, nullptr, nullptr, r, lam, eta, y, yvar, a, p, delta}, true, stream);
 }
 
 const char* kla_status_string(kla_status s) {

@@ -35,6 +35,10 @@
 // buffer loads); their input staging is double-buffered: at the start of round
 // i they request all inputs of chunk c(i + 1) and then wait for those of chunk
 // c(i), requested one round earlier.
+//
+// TI (time-invariant gates, from the OU parameters of Sec. 4.1): abar and pbar
+// are the same for every token of a key slot; each lane forms them once and the
+// staging carries only k, q and r.
 #pragma once
 #include <type_traits>
 
@@ -98,19 +102,22 @@ struct ScanOut {
     float* yv;                     // per-token sums of q^2 / lam over this wave's slots
 };
 
-// Staged inputs of 8 consecutive tokens for one key slot (raw bf16 / r words).
+// Staged inputs of 8 consecutive tokens for one key slot (raw bf16 / r words;
+// a and p unused with time-invariant gates).
 struct ScanGroup {
     uint32_t a[8], p[8], k[8], q[8];
     uint4 r[2];
 };
 
-template <int SW>
+template <int SW, bool TI>
 __device__ __forceinline__ void read_group(ScanGroup& gr, const uint16_t* __restrict__ stg,
                                            const uint32_t* __restrict__ rw, int sl, int t8) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-        gr.a[e] = stg[(0 * kC + t8 + e) * SW + sl];
-        gr.p[e] = stg[(1 * kC + t8 + e) * SW + sl];
+        if constexpr (!TI) {
+            gr.a[e] = stg[(0 * kC + t8 + e) * SW + sl];
+            gr.p[e] = stg[(1 * kC + t8 + e) * SW + sl];
+        }
         gr.k[e] = stg[(2 * kC + t8 + e) * SW + sl];
         gr.q[e] = stg[(3 * kC + t8 + e) * SW + sl];
     }
@@ -122,11 +129,13 @@ __device__ __forceinline__ float bf16w(uint32_t w) { return __uint_as_float(w <<
 
 // One chunk of the walk for key slot n (lane: slot sl, half hf) from the staged
 // inputs (stg: [4][kC][SW] bf16; rw: r as words [kC]), starting from the chunk-
-// start lam x.  FULL: all kC tokens are valid (no per-token guards).  Returns
-// the lam at the chunk end in every lane.
-template <int SW, int LQ, bool YV, bool FULL>
+// start lam x.  FULL: all kC tokens are valid (no per-token guards).  TI: the
+// gates are the lane's ca, cp for every token.  Returns the lam at the chunk end
+// in every lane.
+template <int SW, int LQ, bool YV, bool FULL, bool TI>
 __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, const uint32_t* __restrict__ rw,
-                                            int sl, int hf, int n, int nt, float x, const ScanOut& o) {
+                                            int sl, int hf, int n, int nt, float x, const ScanOut& o, float ca,
+                                            float cp) {
     // ---- the 2x2 product of this lane's 8 tokens 8 hf .. 8 hf + 7, as the images of
     // (1, 0) and (0, 1), with the product of abar
     float m00 = 1.f, m10 = 0.f, m01 = 0.f, m11 = 1.f, aq = 1.f;
@@ -135,8 +144,8 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int t = 8 * hf + j;
-            ta[j] = bf16w(stg[(0 * kC + t) * SW + sl]);
-            tp[j] = bf16w(stg[(1 * kC + t) * SW + sl]);
+            ta[j] = TI ? ca : bf16w(stg[(0 * kC + t) * SW + sl]);
+            tp[j] = TI ? cp : bf16w(stg[(1 * kC + t) * SW + sl]);
             tk[j] = bf16w(stg[(2 * kC + t) * SW + sl]);
             tr[j] = bf16w(rw[t]);
         }
@@ -166,18 +175,18 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
     // ---- walk tokens 16 hf .. 16 hf + 15 (inputs of the next 8 read before the current 8)
     const int tb = 16 * hf;
     ScanGroup gr[2];
-    read_group<SW>(gr[0], stg, rw, sl, tb);
+    read_group<SW, TI>(gr[0], stg, rw, sl, tb);
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
         const ScanGroup& cur = gr[g];
-        if (g == 0) read_group<SW>(gr[1], stg, rw, sl, tb + 8);
+        if (g == 0) read_group<SW, TI>(gr[1], stg, rw, sl, tb + 8);
 #pragma unroll
         for (int j2 = 0; j2 < 4; ++j2) {
             float qp2[2], kn2[2];
 #pragma unroll
             for (int e = 0; e < 2; ++e) {
                 const int i = 2 * j2 + e, t = tb + 8 * g + i;
-                const float av = bf16w(cur.a[i]), pv = bf16w(cur.p[i]);
+                const float av = TI ? ca : bf16w(cur.a[i]), pv = TI ? cp : bf16w(cur.p[i]);
                 const float kv = bf16w(cur.k[i]), qv = bf16w(cur.q[i]);
                 const uint32_t rword = i < 4 ? (&cur.r[0].x)[i] : (&cur.r[1].x)[i - 4];
                 const float rv = bf16w(rword);
@@ -228,6 +237,7 @@ struct ScanSrc {
     int tcol0;                            // first column of the value tile
     size_t seq0;                          // b * T
     int H, h, T, nchunk, bh;
+    const float *oa = nullptr, *op = nullptr, *od = nullptr;   // OU parameters [H, DK] (TI)
 };
 
 // The scan-wave loop: nchunk + 1 rounds, each ended by barrier_lds().  The walk
@@ -235,16 +245,19 @@ struct ScanSrc {
 // chunk-start lam stored to save_lam when given) or c = nchunk-1 .. 0 (REV:
 // the chunk-start lam read from lam_in [BH][nchunk][DK]).  Returns the lam
 // after the last walked token (forward order) for key slot wave * SW + lane % SW.
-template <class Cfg, bool YV, bool REV>
+template <class Cfg, bool YV, bool REV, bool TI>
 __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int lane, const ScanSrc& sc,
                                            const float* __restrict__ lam_in, float* __restrict__ save_lam) {
     constexpr int DK = Cfg::DK, DV = Cfg::DV, DVT = Cfg::DVT, SW = Cfg::SW, NSW = Cfg::NSW;
-    constexpr int NL = REV ? 1 : 0;   // chunk-start lam requests per round
+    constexpr int NL = REV ? 1 : 0;    // chunk-start lam requests per round
+    constexpr int NI = TI ? 4 : 8;     // staging loads of the per-token key-side inputs per round
     const int H = sc.H, h = sc.h, T = sc.T, nchunk = sc.nchunk;
     const int sl = lane % SW, hf = lane / SW;   // key slot within the wave, half of the chunk
     const int n = wave * SW + sl;
     float x = 1.f;                              // lam at the chunk start
     if (!REV && lam_in) x = lam_in[(size_t)sc.bh * DK + n];
+    float ca = 0.f, cp = 0.f;                   // time-invariant gates of slot n
+    if constexpr (TI) ou_gates(sc.oa[h * DK + n], sc.op[h * DK + n], sc.od[h * DK + n], ca, cp);
     unsigned char* stw = smem + Cfg::STG + wave * Cfg::STG_WAVE;
     uint32_t* rw = reinterpret_cast<uint32_t*>(stw + Cfg::STG_R);   // [2][64]
     float* lw = reinterpret_cast<float*>(stw + Cfg::STG_L);         // [2][64]
@@ -267,8 +280,10 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             buf_ld128_lds(rs, stg + ti * kC * SW, in_voff);
             buf_ld128_lds(rs, stg + (ti * kC + 16) * SW, in_voff + 16 * tok_bytes);
         };
-        one(sc.a, 0);
-        one(sc.p, 1);
+        if constexpr (!TI) {
+            one(sc.a, 0);
+            one(sc.p, 1);
+        }
         one(sc.k, 2);
         one(sc.q, 3);
         const rsrc_t rr = make_rsrc(sc.r + (sc.seq0 + t0) * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
@@ -303,8 +318,9 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             issue_tile(c, it);
             issue_inputs(chunk_of(it + 1), bb ^ 1);
             // this chunk's inputs, requested one round earlier, have landed: younger are the
-            // requests just issued (the saved-lam store, the value-tile loads, 9 + NL staging loads)
-            wait_vm_le_rt<9 + NL>(nvw + (sl_store ? 1 : 0));
+            // requests just issued (the saved-lam store, the value-tile loads, NI + 1 + NL
+            // staging loads)
+            wait_vm_le_rt<NI + 1 + NL>(nvw + (sl_store ? 1 : 0));
             if constexpr (REV) x = lw[bb * 64 + sl];
 
             unsigned char* buf = smem + (it & 1) * Cfg::BUF;
@@ -318,11 +334,11 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             const uint16_t* stg = reinterpret_cast<const uint16_t*>(stw) + bb * 4 * kC * SW;
             const uint32_t* rwc = rw + bb * 64;
             if (nt == kC)
-                x = scan_chunk<SW, Cfg::LQ, YV, true>(stg, rwc, sl, hf, n, nt, x, o);
+                x = scan_chunk<SW, Cfg::LQ, YV, true, TI>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
             else
-                x = scan_chunk<SW, Cfg::LQ, YV, false>(stg, rwc, sl, hf, n, nt, x, o);
-            // the value tile has landed (younger: the 9 + NL staging loads)
-            wait_vm_le<9 + NL>();
+                x = scan_chunk<SW, Cfg::LQ, YV, false, TI>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
+            // the value tile has landed (younger: the NI + 1 + NL staging loads)
+            wait_vm_le<NI + 1 + NL>();
         }
         barrier_lds();
     }

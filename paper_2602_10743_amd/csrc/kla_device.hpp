@@ -32,6 +32,15 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     return static_cast<uint16_t>(cvt_pk_bf16(f, 0.f));
 }
 
+// Gates of the exactly discretised OU prior (Sec. 4.1, eq. discretisation) for
+// mean reversion a > 0, diffusion scale p and step delta > 0, formed in fp64:
+//   abar = exp(-a delta),  pbar = p^2 (1 - exp(-2 a delta)) / (2 a).
+__device__ __forceinline__ void ou_gates(float a, float p, float delta, float& abar, float& pbar) {
+    const double ad = (double)a * (double)delta;
+    abar = (float)exp(-ad);
+    pbar = (float)((double)p * (double)p * -expm1(-2.0 * ad) / (2.0 * (double)a));
+}
+
 __device__ __forceinline__ float ld(const float* p, size_t i) { return p[i]; }
 __device__ __forceinline__ float ld(const uint16_t* p, size_t i) { return bf16_to_f32(p[i]); }
 __device__ __forceinline__ void st(float* p, size_t i, float x) { p[i] = x; }

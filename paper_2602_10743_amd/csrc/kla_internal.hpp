@@ -11,11 +11,15 @@ struct Shape {
     int bf16;  // 0: fp32 storage, 1: bf16 storage
 };
 
+// Gates: per token (a, p: abar, pbar [B, T, H, dk] in the storage type) or, when
+// ou_a is set, time-invariant from the OU parameters ou_a, ou_p, ou_d [H, dk] fp32
+// (a and p unused).
 struct FwdArgs {
     const void *q, *k, *v, *a, *p, *r;
     const float *lam0, *eta0;
     void* y;
     float *yvar, *lamT, *etaT;
+    const float *ou_a = nullptr, *ou_p = nullptr, *ou_d = nullptr;
 };
 
 struct BwdArgs {
@@ -25,6 +29,10 @@ struct BwdArgs {
     const float *dlamT, *detaT;
     void *dq, *dk, *dv, *da, *dp, *dr;
     float *dlam0, *deta0;
+    const float *ou_a = nullptr, *ou_p = nullptr, *ou_d = nullptr;
+    // OU gates: per-part sums over tokens of the abar and pbar gradients,
+    // [2][nparts][H][dk] fp32 (da, dp unused)
+    float* ou_part = nullptr;
 };
 
 struct DecodeArgs {
@@ -32,6 +40,7 @@ struct DecodeArgs {
     float *lam, *eta;
     void* y;
     float* yvar;
+    const float *ou_a = nullptr, *ou_p = nullptr, *ou_d = nullptr;
 };
 
 // Token-recurrent reference kernels.
@@ -49,5 +58,12 @@ size_t chunked_bwd_workspace(const Shape& s);
 hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st);
 // value side of the chunked backward (dv, deta0); saved_lam: lam at every 32-token chunk start
 hipError_t launch_backward_dv(const Shape& s, const BwdArgs& a, const float* saved_lam, hipStream_t st);
+// token-sum parts of the OU gate gradients that the chunked / recurrent backward leave
+int chunked_ou_parts(const Shape& s);
+int recurrent_ou_parts(const Shape& s);
+
+// OU gates: gradients of the parameters from the per-part gate-gradient sums
+hipError_t launch_ou_param_grads(int H, int dk, int nparts, const float* part, const float* a, const float* p,
+                                 const float* d, float* da, float* dp, float* dd, hipStream_t st);
 
 }  // namespace kla

@@ -4,6 +4,9 @@
 // precision, Theorem 2 for the information state, Algorithm 1 readout), with
 // the d_k x d_v state held in registers across the token loop.  They are the
 // reference HIP path of the library and the decode step's implementation.
+// With OU parameters (ou_a set) every token of a head shares the gates of its
+// key slot, formed once per lane; the backward then sums the gate gradients of
+// a lane over its tokens into one part per batch row.
 #include "kla_device.hpp"
 #include "kla_internal.hpp"
 
@@ -53,13 +56,16 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
     }
     float lam = 1.f;
     if (tid < DK && g.lam0) lam = g.lam0[(size_t)bh * DK + tid];
+    const bool ou = g.ou_a != nullptr;
+    float oa = 0.f, op = 0.f;
+    if (ou && tid < DK) ou_gates(g.ou_a[h * DK + tid], g.ou_p[h * DK + tid], g.ou_d[h * DK + tid], oa, op);
 
     for (int t0 = 0; t0 < s.T; t0 += kTB) {
         const int nt = min(kTB, s.T - t0);
         if (tid < DK) {
             for (int j = 0; j < nt; ++j) {
                 const size_t base = ((size_t)b * s.T + t0 + j) * s.H + h;
-                const float at = ld(a, base * DK + tid), pt = ld(p, base * DK + tid);
+                const float at = ou ? oa : ld(a, base * DK + tid), pt = ou ? op : ld(p, base * DK + tid);
                 const float kt = ld(k, base * DK + tid), qt = ld(q, base * DK + tid);
                 const float rt = ld(r, base);
                 const float rho = 1.f / (at * at + pt * lam);
@@ -137,10 +143,14 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     for (int i = 0; i < DPER; ++i)
         Hs[i] = g.eta0 ? g.eta0[((size_t)bh * DK + n) * DV + dl + i * DL] : 0.f;
     float lam = g.lam0 ? g.lam0[(size_t)bh * DK + n] : 1.f;
+    const bool ou = g.ou_a != nullptr;
+    float oa = 0.f, op = 0.f;
+    if (ou) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], oa, op);
 
     for (int t = 0; t < s.T; ++t) {
         const size_t base = ((size_t)b * s.T + t) * s.H + h;
-        const float at = ld(a, base * DK + n), pt = ld(p, base * DK + n), kt = ld(k, base * DK + n);
+        const float at = ou ? oa : ld(a, base * DK + n), pt = ou ? op : ld(p, base * DK + n);
+        const float kt = ld(k, base * DK + n);
         const float rt = ld(r, base);
         const float rho = 1.f / (at * at + pt * lam);
         const float F = at * rho, kh = rt * kt;
@@ -220,9 +230,12 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
 
     // per-slot scalars, live in threads tid < DK
     float Fnext = 1.f, cnext = 0.f, Sg = 0.f;
+    const bool ou = g.ou_a != nullptr;
+    float oa = 0.f, op = 0.f, sum_da = 0.f, sum_dp = 0.f;
     if (tid < DK) {
         cnext = g.dlamT ? g.dlamT[(size_t)bh * DK + tid] : 0.f;
         Sg = wPT[(size_t)bh * DK + tid];
+        if (ou) ou_gates(g.ou_a[h * DK + tid], g.ou_p[h * DK + tid], g.ou_d[h * DK + tid], oa, op);
     }
 
     for (int t = s.T - 1; t >= 0; --t) {
@@ -266,7 +279,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
         if (tid < DK) {
             float dkh = 0.f;
             for (int i = 0; i < DVT; ++i) dkh += sPK[tid][i];
-            const float at = ld(a, base * DK + tid), pt = ld(p, base * DK + tid);
+            const float at = ou ? oa : ld(a, base * DK + tid), pt = ou ? op : ld(p, base * DK + tid);
             const float lprev = t > 0 ? wlam[(base - s.H) * DK + tid] : (g.lam0 ? g.lam0[(size_t)bh * DK + tid] : 1.f);
             const float qtl = sQt[tid], kh = sKh[tid];
             Sg += qtl * dqt - kh * dkh;                       // dG_t
@@ -275,8 +288,14 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
             const float drho = gl * lprev + Sg / rho;
             st(dq, base * DK + tid, dqt / lam_t);
             st(dk, base * DK + tid, rt * dkh + 2.f * kt * rt * gl);
-            st(da, base * DK + tid, Sg / at - 2.f * at * rho * rho * drho);
-            st(dp, base * DK + tid, -lprev * rho * rho * drho);
+            const float dav = Sg / at - 2.f * at * rho * rho * drho, dpv = -lprev * rho * rho * drho;
+            if (ou) {
+                sum_da += dav;
+                sum_dp += dpv;
+            } else {
+                st(da, base * DK + tid, dav);
+                st(dp, base * DK + tid, dpv);
+            }
             sDR[tid] = kt * dkh + kt * kt * gl;
             cnext = at * at * rho * rho * gl - pt * rho * Sg;
             Fnext = at * rho;
@@ -294,6 +313,11 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
         }
     }
     if (tid < DK && g.dlam0) g.dlam0[(size_t)bh * DK + tid] = cnext;
+    if (ou && tid < DK) {   // part b of the token sums
+        const size_t np = (size_t)s.B * s.H * DK;
+        g.ou_part[(size_t)bh * DK + tid] = sum_da;
+        g.ou_part[np + (size_t)bh * DK + tid] = sum_dp;
+    }
     __syncthreads();
     if (tid < DK) sFn[tid] = Fnext;
     __syncthreads();
@@ -332,7 +356,15 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(int H, DecodeArgs g) {
     const int tid = threadIdx.x;
     if (tid < DK) {
         const size_t o = sh * DK + tid;
-        const float at = ld(a, o), pt = ld(p, o), kt = ld(k, o), qt = ld(q, o), rt = ld(r, sh);
+        float at, pt;
+        if (g.ou_a) {
+            const int oh = (int)(sh % H) * DK + tid;
+            ou_gates(g.ou_a[oh], g.ou_p[oh], g.ou_d[oh], at, pt);
+        } else {
+            at = ld(a, o);
+            pt = ld(p, o);
+        }
+        const float kt = ld(k, o), qt = ld(q, o), rt = ld(r, sh);
         const float lam = g.lam[o];
         const float rho = 1.f / (at * at + pt * lam);
         const float ln = rho * lam + kt * kt * rt;
@@ -443,6 +475,9 @@ struct DecL {
 hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, hipStream_t st) {
     return dispatch<FwdL>(s, a, st);
 }
+
+// one part per batch row: the recurrent backward walks a whole (b, h) in one workgroup
+int recurrent_ou_parts(const Shape& s) { return s.B; }
 
 size_t backward_recurrent_workspace(const Shape& s) {
     const size_t ntok = (size_t)s.B * s.T * s.H * s.dk;

@@ -100,3 +100,44 @@ def test_binding_refuses_cpu_tensors():
     x = torch.zeros(1, 4, 1, 16)
     with pytest.raises(ValueError, match="GPU"):
         K.kla_forward(x, x, x, x, x, torch.zeros(1, 4, 1))
+
+
+def test_ou_entry_points_declared_and_sized(lib):
+    import paper_2602_10743_amd as K
+    names = _declared()
+    for n in ("kla_forward_ou", "kla_backward_ou", "kla_decode_step_ou", "kla_backward_ou_workspace"):
+        assert n in names
+    for d in (_desc(), _desc(B=3, T=70, H=2, dk=64, dv=32, dtype=1)):
+        # the OU backward adds the per-part gate-gradient sums to the plain workspace
+        for saved in (False, True):
+            assert K.kla_backward_ou_workspace(d, saved) > K.kla_backward_workspace(d, saved)
+    assert K.kla_backward_ou_workspace(_desc(dk=24), False) == 0
+
+
+def test_ou_argument_errors(lib):
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10004)
+    d = _desc()
+    # q k v a p delta r lam0 eta0 y yvar lamT etaT saved ws
+    ok = [fake] * 7 + [None, None, fake, None, None, None, None, fake]
+    assert lib.kla_forward_ou(ctypes.byref(_desc(dk=24)), *ok, 256, None) == 2
+    for i in (3, 4, 5):                                            # a, p, delta
+        bad = list(ok)
+        bad[i] = None
+        assert lib.kla_forward_ou(ctypes.byref(d), *bad, 256, None) == 1
+    bad = list(ok)
+    bad[5] = odd
+    assert lib.kla_forward_ou(ctypes.byref(d), *bad, 256, None) == 4
+    assert lib.kla_forward_ou(ctypes.byref(d), *ok, 0, None) == 5
+    # q k v a p delta r lam0 eta0 saved dy dlamT detaT dq dk dv da dp ddelta dr dlam0 deta0 ws
+    bwd = [fake] * 7 + [None, None, None] + [fake, None, None] + [fake] * 7 + [None, None] + [fake]
+    assert lib.kla_backward_ou(ctypes.byref(d), *bwd, 0, None) == 5
+    for i in (16, 17, 18):                                         # da, dp, ddelta
+        bad = list(bwd)
+        bad[i] = None
+        assert lib.kla_backward_ou(ctypes.byref(d), *bad, 1 << 40, None) == 1
+    dec = [fake] * 7 + [fake, fake, fake, None, None]
+    assert lib.kla_decode_step_ou(4, 2, 16, 48, 0, *dec) == 2
+    bad = list(dec)
+    bad[5] = None
+    assert lib.kla_decode_step_ou(4, 2, 16, 16, 0, *bad) == 1
