@@ -13,6 +13,10 @@ traffic of that call when profiles/lm_layer_traffic.md was taken from the
 current kernel sources (see paper_2602_10743_amd/traffic.py); and the fp64
 oracle's throughput on the host cores over a bounded sample of the same
 workload.
+
+With --ou the same shape runs with OU gates instead (kla_forward_ou /
+kla_backward_ou: time-invariant a, p, delta [H, dk] in place of the per-token
+abar and pbar tensors); its traffic summary is profiles/lm_layer_ou_traffic.md.
 """
 import argparse
 import json
@@ -30,33 +34,58 @@ METRIC = "KLA layer fwd+bwd tokens/sec (B·T·H, d=128) on 1 MI355X; % of HBM/MF
 HBM_PEAK_GBS = 8000.0
 
 
-def algorithmic_bytes(w, s):
+def algorithmic_bytes(w, s, ou=False):
     """Per token-head: forward reads q,k,abar,pbar (dk each), v (dv), r (1) and
-    writes y (dv); backward reads those plus dy and writes the six gradients."""
-    fwd = (4 * w.dk + w.dv + 1) * s + w.dv * s
-    bwd = 2 * (4 * w.dk + w.dv + 1) * s + w.dv * s
+    writes y (dv); backward reads those plus dy and writes the six gradients.
+    With OU gates there are no per-token abar, pbar or their gradients (the
+    [H, dk] parameters and their gradients are a fixed few KiB per call)."""
+    nk = 2 if ou else 4
+    fwd = (nk * w.dk + w.dv + 1) * s + w.dv * s
+    bwd = 2 * (nk * w.dk + w.dv + 1) * s + w.dv * s
     return fwd, bwd
 
 
-def cpu_baseline(w, budget_s: float):
-    """fp64 oracle (forward + backward) on a few sampled (b, h) sequences."""
+def cpu_baseline(w, budget_s: float, ou=None):
+    """fp64 oracle (forward + backward) on a few sampled (b, h) sequences.  With
+    OU parameters ``ou`` the sample is every batch row of as many heads as fit
+    (the parameters are per head), the oracle called once per head."""
     import kla_inputs as K
     import oracle
     threads = oracle.default_threads()
-    pairs = [(b, h) for b in range(w.B) for h in range(w.H)]
-    g = np.random.default_rng(0)
-    g.shuffle(pairs)
-    n = max(1, min(4 * threads, len(pairs)))
-    sample = sorted(pairs[:n])
-    sl = K.pairs_slice(w, sample)
-    t0 = time.perf_counter()
-    oracle.forward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["r"], nthreads=threads)
-    t1 = time.perf_counter()
-    oracle.backward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["r"], None, None, sl["dy"], nthreads=threads)
-    t2 = time.perf_counter()
-    th = len(sample) * w.T
-    return {"value": th / (t2 - t0), "unit": "tokens/s", "cores": min(threads, len(sample)), "kind": "oracle",
-            "sample": f"{len(sample)} (batch, head) sequences of T={w.T} (fwd {t1 - t0:.1f}s + bwd {t2 - t1:.1f}s)"}
+    n = max(1, min(4 * threads, w.B * w.H))
+    if ou is None:
+        pairs = [(b, h) for b in range(w.B) for h in range(w.H)]
+        g = np.random.default_rng(0)
+        g.shuffle(pairs)
+        groups = [sorted(pairs[:n])]
+    else:
+        groups = [[(b, h) for b in range(w.B)] for h in range(max(1, n // w.B))]
+    tf = tb = 0.0
+    count = 0
+    for sample in groups:
+        sl = K.pairs_slice(w, sample)
+        t0 = time.perf_counter()
+        if ou is None:
+            oracle.forward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["r"], nthreads=threads)
+        else:
+            h = sample[0][1]
+            hp = {k: np.asarray(v[h:h + 1], dtype=np.float64) for k, v in ou.items()}
+            oracle.forward_ou(sl["q"], sl["k"], sl["v"], hp["a"], hp["p"], hp["delta"], sl["r"], nthreads=threads)
+        t1 = time.perf_counter()
+        if ou is None:
+            oracle.backward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["r"], None, None, sl["dy"],
+                            nthreads=threads)
+        else:
+            oracle.backward_ou(sl["q"], sl["k"], sl["v"], hp["a"], hp["p"], hp["delta"], sl["r"], None, None,
+                               sl["dy"], nthreads=threads)
+        t2 = time.perf_counter()
+        tf += t1 - t0
+        tb += t2 - t1
+        count += len(sample)
+    th = count * w.T
+    return {"value": th / (tf + tb), "unit": "tokens/s", "cores": min(threads, max(len(s) for s in groups)),
+            "kind": "oracle",
+            "sample": f"{count} (batch, head) sequences of T={w.T} (fwd {tf:.1f}s + bwd {tb:.1f}s)"}
 
 
 def main():
@@ -68,6 +97,8 @@ def main():
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain elementwise copy of known size first (counter calibration)")
+    ap.add_argument("--ou", action="store_true",
+                    help="OU gates: time-invariant (a, p, delta) instead of per-token abar, pbar")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the filter layer shards over (batch, head) with no "
@@ -81,10 +112,13 @@ def main():
     w = K.WORKLOADS[2]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    bits = K.full(w, as_bits=True)
+    names = ("q", "k", "v", "r", "dy") if args.ou else K.NAMES + ("dy",)
+    bits = K.full(w, names=names, as_bits=True)
     x = {n: torch.from_numpy(np.ascontiguousarray(bits[n].view(np.int16))).view(torch.bfloat16).to(dev)
          for n in bits}
     del bits
+    ou_np = K.ou_params(w.H, w.dk, seed=w.cid) if args.ou else None
+    ou = {n: torch.from_numpy(v).to(dev) for n, v in ou_np.items()} if args.ou else None
     stream = torch.cuda.current_stream(dev)
     if args.copy_calibration:
         from paper_2602_10743_amd.traffic import COPY_BYTES
@@ -98,11 +132,19 @@ def main():
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], want_state=False, save=True)
+        if ou is None:
+            out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], want_state=False, save=True)
+        else:
+            out = kla.kla_forward_ou(x["q"], x["k"], x["v"], ou["a"], ou["p"], ou["delta"], x["r"],
+                                     want_state=False, save=True)
         if ev is not None:
             ev[1].record(stream)
-        kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], None, None, x["dy"],
-                         saved=out["saved"], want_init_grads=False)
+        if ou is None:
+            kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], None, None, x["dy"],
+                             saved=out["saved"], want_init_grads=False)
+        else:
+            kla.kla_backward_ou(x["q"], x["k"], x["v"], ou["a"], ou["p"], ou["delta"], x["r"], None, None,
+                                x["dy"], saved=out["saved"], want_init_grads=False)
         if ev is not None:
             ev[2].record(stream)
 
@@ -120,14 +162,15 @@ def main():
     bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     ms_per_step = wall * 1e3 / args.steps
     th = w.token_heads
-    fwd_b, bwd_b = algorithmic_bytes(w, 2)
+    fwd_b, bwd_b = algorithmic_bytes(w, 2, ou=args.ou)
+    sfx = "_ou" if args.ou else ""
     if bwd_ms >= fwd_ms:
-        dom, ms, nbytes = "kla_backward", bwd_ms, bwd_b * th
+        dom, ms, nbytes = "kla_backward" + sfx, bwd_ms, bwd_b * th
     else:
-        dom, ms, nbytes = "kla_forward", fwd_ms, fwd_b * th
+        dom, ms, nbytes = "kla_forward" + sfx, fwd_ms, fwd_b * th
     achieved = nbytes / (ms * 1e-3) / 1e9
     from paper_2602_10743_amd.traffic import load_summary
-    measured = load_summary(os.path.join(ROOT, "profiles", "lm_layer_traffic.md"))
+    measured = load_summary(os.path.join(ROOT, "profiles", f"lm_layer{sfx}_traffic.md"))
     traffic = measured.get(dom) if measured else None
     res = {
         "metric": METRIC,
@@ -142,8 +185,9 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv,
-                   "pass": "fwd+bwd", "tokens_counted": "B*T*H"},
+        "config": {"workload": w.name + sfx, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv,
+                   "pass": "fwd+bwd", "gates": "ou (a, p, delta per head and key slot)" if args.ou else "per token",
+                   "tokens_counted": "B*T*H"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "traffic_unit": "bytes per call", "algorithmic_bytes_per_call": nbytes,
@@ -151,7 +195,7 @@ def main():
                      "algorithmic_bytes_per_token_head": {"fwd": fwd_b, "bwd": bwd_b}},
     }
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_budget, ou=ou_np)
     print(json.dumps(res), flush=True)
 
 

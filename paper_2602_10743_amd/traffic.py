@@ -15,6 +15,9 @@ Run from the repository root on the GPU machine (TMPDIR=/tmp):
       python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration
   python -m paper_2602_10743_amd.traffic D/fetch D/write > profiles/lm_layer_traffic.md
 
+With OU gates: the same two runs with `bench.py ... --ou`, then
+  python -m paper_2602_10743_amd.traffic D/fetch D/write --ou > profiles/lm_layer_ou_traffic.md
+
 MFMA and VALU utilisation per kernel come from a third run:
   rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU \\
       GRBM_GUI_ACTIVE --output-format csv -d D/util -o run -- \\
@@ -34,6 +37,10 @@ COPY_BYTES = 256 << 20
 CALLS = {
     "kla_forward": ("fwd_chunk_kernel",),
     "kla_backward": ("bwd_dv_kernel", "bwd_dk_kernel", "dr_combine_kernel"),
+}
+CALLS_OU = {
+    "kla_forward_ou": ("fwd_chunk_kernel",),
+    "kla_backward_ou": ("bwd_dv_kernel", "bwd_dk_kernel", "dr_combine_kernel", "ou_param_grads_kernel"),
 }
 SUMMARY_KEY = "traffic_bytes_per_call"
 
@@ -68,9 +75,9 @@ def _counter(run_dir: str, counter: str) -> dict:
     return {k: list(v.values()) for k, v in vals.items()}
 
 
-def _per_call(vals: dict, scale: float) -> dict:
+def _per_call(vals: dict, scale: float, calls: dict) -> dict:
     out = {}
-    for call, kernels in CALLS.items():
+    for call, kernels in calls.items():
         total = 0.0
         for kname in kernels:
             hits = [v for k, v in vals.items() if k.startswith(kname)]
@@ -82,35 +89,38 @@ def _per_call(vals: dict, scale: float) -> dict:
     return out
 
 
-def summarise(fetch_dir: str, write_dir: str) -> str:
+def summarise(fetch_dir: str, write_dir: str, ou: bool = False) -> str:
+    calls = CALLS_OU if ou else CALLS
+    flag = " --ou" if ou else ""
     fetch = _counter(fetch_dir, "FETCH_SIZE")
     write = _counter(write_dir, "WRITE_SIZE")
-    kla_names = tuple(k for ks in CALLS.values() for k in ks)
+    kla_names = tuple(k for ks in calls.values() for k in ks)
     copies = [k for k in fetch if not k.startswith(kla_names)]
     if not copies:
         raise KeyError("no calibration copy kernel in the fetch run")
     copy = max(copies, key=lambda k: max(fetch[k]))
     f_fetch = COPY_BYTES / max(fetch[copy])          # bytes per counter unit
     f_write = COPY_BYTES / max(write[copy])
-    rd = _per_call(fetch, f_fetch)
-    wr = _per_call(write, f_write)
+    rd = _per_call(fetch, f_fetch, calls)
+    wr = _per_call(write, f_write, calls)
     lines = [
-        "# HBM traffic per call, lm-layer workload (B=8, T=2048, H=16, d=128, bf16)",
+        "# HBM traffic per call, lm-layer workload (B=8, T=2048, H=16, d=128, bf16"
+        + (", OU gates)" if ou else ")"),
         "",
         "Counters: FETCH_SIZE and WRITE_SIZE from two separate `rocprofv3 --pmc` runs of",
-        "`python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration`, scaled by",
+        f"`python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration{flag}`, scaled by",
         f"the calibration copy kernel `{copy}` ({COPY_BYTES} bytes read and written):",
         f"fetch scale {f_fetch:.4f} bytes/unit, write scale {f_write:.4f} bytes/unit.",
         "",
         "| call | read bytes | written bytes | total |",
         "|---|---|---|---|",
     ]
-    for call in CALLS:
+    for call in calls:
         lines.append(f"| {call} | {rd[call]:.4g} | {wr[call]:.4g} | {rd[call] + wr[call]:.4g} |")
     lines += [
         "",
         f"sources: {sources_digest()}",
-        f"{SUMMARY_KEY}: " + ", ".join(f"{c}={rd[c] + wr[c]:.6g}" for c in CALLS),
+        f"{SUMMARY_KEY}: " + ", ".join(f"{c}={rd[c] + wr[c]:.6g}" for c in calls),
         "",
     ]
     return "\n".join(lines)
@@ -157,7 +167,7 @@ def summarise_util(run_dir: str) -> str:
     dur = defaultdict(dict)                          # kernel -> dispatch -> ns
     for r in _rows(run_dir):
         k = _short(r["Kernel_Name"])
-        if not k.startswith(tuple(n for ns in CALLS.values() for n in ns)):
+        if not k.startswith(tuple(n for ns in list(CALLS.values()) + list(CALLS_OU.values()) for n in ns)):
             continue
         d = r.get("Dispatch_Id") or r.get("Correlation_Id")
         acc[k][r["Counter_Name"]] += float(r["Counter_Value"])
@@ -198,7 +208,9 @@ if __name__ == "__main__":
     if len(sys.argv) == 3 and sys.argv[1] == "--util":
         print(summarise_util(sys.argv[2]))
         sys.exit(0)
-    if len(sys.argv) != 3:
+    ou = "--ou" in sys.argv[1:]
+    args = [a for a in sys.argv[1:] if a != "--ou"]
+    if len(args) != 2:
         print(__doc__, file=sys.stderr)
         sys.exit(2)
-    print(summarise(sys.argv[1], sys.argv[2]))
+    print(summarise(args[0], args[1], ou=ou))
