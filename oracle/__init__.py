@@ -50,7 +50,7 @@ def _load():
         _b.build()
     lib = ctypes.CDLL(_LIB_PATH)
     lib.kla_oracle_forward.argtypes = [_I] * 5 + [_D] * 12 + [_I]
-    lib.kla_oracle_backward.argtypes = [_I] * 5 + [_D] * 19 + [_I]
+    lib.kla_oracle_backward.argtypes = [_I] * 5 + [_D] * 20 + [_I]
     lib.kla_oracle_decode_step.argtypes = [_I] * 4 + [_D] * 10
     lib.kla_oracle_trace.argtypes = [_I] * 3 + [_D] * 9
     lib.kla_oracle_mobius_matrix.argtypes = [ctypes.c_double] * 4 + [_D]
@@ -117,12 +117,20 @@ def forward(q, k, v, a, p, r, lam0=None, eta0=None, nthreads: Optional[int] = No
 
 
 def backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None,
-             nthreads: Optional[int] = None) -> dict:
-    """Exact reverse-mode gradient of ``forward``'s y, lamT and etaT."""
+             nthreads: Optional[int] = None, dyvar=None) -> dict:
+    """Exact reverse-mode gradient of ``forward``'s y, lamT, etaT and (with
+    ``dyvar``, shaped like ``forward``'s yvar) yvar."""
     lib = _load()
     lam0_in_shape = None if lam0 is None else np.asarray(lam0).shape
     q, k, v, a, p, r, lam0, eta0, (B, T, H, dk, dv), per_head = _prep(q, k, v, a, p, r, lam0, eta0)
     dy = _c(dy)
+    if dyvar is not None:
+        dyvar = _c(dyvar)
+        if per_head:
+            # the per-head variance is channel 0 of the per-channel one: seed channel 0 only
+            full = np.zeros((B, T, H, dv))
+            full[..., 0] = dyvar
+            dyvar = full
     if dlamT is not None:
         dlamT = _c(dlamT)
         if dlamT.ndim == 3:
@@ -138,7 +146,7 @@ def backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None,
     dlam0 = np.empty((B, H, dk, dv))
     deta0 = np.empty((B, H, dk, dv))
     lib.kla_oracle_backward(B, T, H, dk, dv, _ptr(q), _ptr(k), _ptr(v), _ptr(a), _ptr(p), _ptr(r),
-                            _ptr(lam0), _ptr(eta0), _ptr(dy), _ptr(dlamT), _ptr(detaT),
+                            _ptr(lam0), _ptr(eta0), _ptr(dy), _ptr(dyvar), _ptr(dlamT), _ptr(detaT),
                             _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["da"]),
                             _ptr(out["dp"]), _ptr(out["dr"]), _ptr(dlam0), _ptr(deta0),
                             nthreads or default_threads())
@@ -281,12 +289,12 @@ def forward_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, nthreads: Optional
 
 
 def backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=None,
-                nthreads: Optional[int] = None) -> dict:
+                nthreads: Optional[int] = None, dyvar=None) -> dict:
     """Gradient of ``forward_ou``: dq, dk, dv, dr, dlam0, deta0 as in ``backward``, and
     da, dp, ddelta [H, dk] for the OU parameters."""
     B, T = np.shape(k)[:2]
     abar, pbar = _ou_tokens(a, p, delta, B, T)
-    out = backward(q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT, detaT, nthreads=nthreads)
+    out = backward(q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT, detaT, nthreads=nthreads, dyvar=dyvar)
     g_abar = out.pop("da").sum(axis=(0, 1))
     g_pbar = out.pop("dp").sum(axis=(0, 1))
     out["da"], out["dp"], out["ddelta"] = ou_discretise_vjp(a, p, delta, g_abar, g_pbar)

@@ -33,7 +33,10 @@
  * sum over n, the adjoint of each scalar filter's mean is known up front
  * (dL/dmu_t[n,d] = q_t[n] * dy_t[d]), so each (n, d) filter is differentiated
  * on its own: one forward sweep storing its (lam, eta) trajectory, then one
- * reverse sweep.
+ * reverse sweep.  The readout variance is differentiable too (the Monte Carlo
+ * readout of the paper's appendix samples through it): an upstream gradient
+ * dyvar_t[d] adds 2 q dyvar / lam to dq and -q^2 dyvar / lam^2 to the adjoint
+ * of lam_t.
  *
  * Layouts (all row-major, contiguous, double):
  *   q, k, a, p  [B, T, H, dk]       v, Lv, y, yvar, dy   [B, T, H, dv]
@@ -51,7 +54,7 @@ typedef struct {
     const double *lam0, *eta0;
     double *y, *yvar, *lamT, *etaT;
     /* backward only */
-    const double *dy, *dlamT, *detaT;
+    const double *dy, *dyvar, *dlamT, *detaT;
     double *dq, *dk_, *dv_, *da, *dp, *dr, *dlam0, *deta0;
     /* work distribution */
     int next;                 /* next (b,h) pair to take */
@@ -154,6 +157,12 @@ static void backward_filter(const job_t* J, int b, int h, int n, int d, double* 
         double dmu = q * g;
         ge += dmu / lc;
         gl -= dmu * ec / (lc * lc);
+        /* readout variance yvar_t[d] += q^2 / lam */
+        if (J->dyvar) {
+            double gv = J->dyvar[iv];
+            J->dq[ik] += 2.0 * q * gv / lc;
+            gl -= q * q * gv / (lc * lc);
+        }
         /* eta_t = f * eta_{t-1} + k r v,  f = a * rho */
         double den = a * a + p * lp, rho = 1.0 / den, f = a * rho;
         double df = ge * ep;
@@ -221,21 +230,21 @@ void kla_oracle_forward(int B, int T, int H, int dk, int dv,
     run(&J, forward_worker, nthreads);
 }
 
-/* Gradients are written (not accumulated) into dq..dr, dlam0, deta0; dlamT /
- * detaT NULL mean zero upstream gradient of the final belief; dlam0 / deta0
- * may be NULL.  The forward readout yvar carries no gradient. */
+/* Gradients are written (not accumulated) into dq..dr, dlam0, deta0; dyvar
+ * (upstream gradient of yvar, [B, T, H, dv]), dlamT and detaT NULL mean zero;
+ * dlam0 / deta0 may be NULL. */
 void kla_oracle_backward(int B, int T, int H, int dk, int dv,
                          const double* q, const double* k, const double* v,
                          const double* a, const double* p, const double* r,
                          const double* lam0, const double* eta0,
-                         const double* dy, const double* dlamT, const double* detaT,
+                         const double* dy, const double* dyvar, const double* dlamT, const double* detaT,
                          double* dq, double* dk_, double* dv_, double* da, double* dp, double* dr,
                          double* dlam0, double* deta0, int nthreads) {
     job_t J;
     memset(&J, 0, sizeof J);
     J.B = B; J.T = T; J.H = H; J.dk = dk; J.dv = dv;
     J.q = q; J.k = k; J.v = v; J.a = a; J.p = p; J.r = r;
-    J.lam0 = lam0; J.eta0 = eta0; J.dy = dy; J.dlamT = dlamT; J.detaT = detaT;
+    J.lam0 = lam0; J.eta0 = eta0; J.dy = dy; J.dyvar = dyvar; J.dlamT = dlamT; J.detaT = detaT;
     J.dq = dq; J.dk_ = dk_; J.dv_ = dv_; J.da = da; J.dp = dp; J.dr = dr;
     J.dlam0 = dlam0; J.deta0 = deta0;
     size_t nk = (size_t)B * T * H * dk, nv = (size_t)B * T * H * dv;

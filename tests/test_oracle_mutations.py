@@ -28,6 +28,8 @@ MUTATIONS = {
     "bwd_noise_grad_wrong_index": ("J->dp[ik] += dden * lp;", "J->dp[ik] += dden * lc;"),
     "bwd_key_grad_missing_factor": ("J->dk_[ik] += gl * 2.0 * k * r;", "J->dk_[ik] += gl * k * r;"),
     "bwd_gate_adjoint_dropped": ("gl_prev += dden * p;", "gl_prev += 0.0;"),
+    "bwd_variance_query_factor": ("J->dq[ik] += 2.0 * q * gv / lc;", "J->dq[ik] += q * gv / lc;"),
+    "bwd_variance_precision_power": ("gl -= q * q * gv / (lc * lc);", "gl -= q * q * gv / lc;"),
 }
 
 
@@ -87,13 +89,15 @@ def _fd_battery(orc) -> bool:
     dy = g.standard_normal((B, T, H, dv))
     dlamT = g.standard_normal((B, H, dk))
     detaT = g.standard_normal((B, H, dk, dv))
+    dyvar = g.standard_normal((B, T, H))
 
     def loss():
         o = orc.forward(inp["q"], inp["k"], inp["v"], inp["a"], inp["p"], inp["r"], inp["lam0"], inp["eta0"])
-        return (o["y"] * dy).sum() + (o["lamT"] * dlamT).sum() + (o["etaT"] * detaT).sum()
+        return ((o["y"] * dy).sum() + (o["lamT"] * dlamT).sum() + (o["etaT"] * detaT).sum()
+                + (o["yvar"] * dyvar).sum())
 
     gr = orc.backward(inp["q"], inp["k"], inp["v"], inp["a"], inp["p"], inp["r"], inp["lam0"], inp["eta0"],
-                      dy, dlamT, detaT)
+                      dy, dlamT, detaT, dyvar=dyvar)
     ok = True
     for name, gname in (("q", "dq"), ("k", "dk"), ("v", "dv"), ("a", "da"), ("p", "dp"), ("r", "dr"),
                         ("lam0", "dlam0"), ("eta0", "deta0")):

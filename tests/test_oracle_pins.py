@@ -375,10 +375,11 @@ def test_per_head_precision_keeps_channels_identical():
 
 
 # --------------------------------------------- backward: finite differences
-def _loss(inp, dy, dlamT, detaT):
+def _loss(inp, dy, dlamT, detaT, dyvar):
     out = oracle.forward(inp["q"], inp["k"], inp["v"], inp["a"], inp["p"], inp["r"],
                          inp["lam0"], inp["eta0"])
-    return (out["y"] * dy).sum() + (out["lamT"] * dlamT).sum() + (out["etaT"] * detaT).sum()
+    return ((out["y"] * dy).sum() + (out["lamT"] * dlamT).sum() + (out["etaT"] * detaT).sum()
+            + (out["yvar"] * dyvar).sum())
 
 
 @pytest.mark.parametrize("per_head", [False, True])
@@ -392,15 +393,17 @@ def test_backward_matches_central_differences(per_head):
         inp["r"] = 0.2 + g.random((B, T, H))
         inp["lam0"] = 0.5 + g.random((B, H, dk))
         dlamT = g.standard_normal((B, H, dk))
+        dyvar = g.standard_normal((B, T, H))
     else:
         inp["r"] = 0.2 + g.random((B, T, H, dv))
         inp["lam0"] = 0.5 + g.random((B, H, dk, dv))
         dlamT = g.standard_normal((B, H, dk, dv))
+        dyvar = g.standard_normal((B, T, H, dv))
     inp["eta0"] = g.standard_normal((B, H, dk, dv))
     dy = g.standard_normal((B, T, H, dv))
     detaT = g.standard_normal((B, H, dk, dv))
     gr = oracle.backward(inp["q"], inp["k"], inp["v"], inp["a"], inp["p"], inp["r"],
-                         inp["lam0"], inp["eta0"], dy, dlamT, detaT)
+                         inp["lam0"], inp["eta0"], dy, dlamT, detaT, dyvar=dyvar)
     names = {"q": "dq", "k": "dk", "v": "dv", "a": "da", "p": "dp", "r": "dr",
              "lam0": "dlam0", "eta0": "deta0"}
     h = 1e-6
@@ -410,9 +413,9 @@ def test_backward_matches_central_differences(per_head):
         for idx in np.ndindex(x.shape):
             old = x[idx]
             x[idx] = old + h
-            lp = _loss(inp, dy, dlamT, detaT)
+            lp = _loss(inp, dy, dlamT, detaT, dyvar)
             x[idx] = old - h
-            lm = _loss(inp, dy, dlamT, detaT)
+            lm = _loss(inp, dy, dlamT, detaT, dyvar)
             x[idx] = old
             fd[idx] = (lp - lm) / (2 * h)
         assert gr[gname].shape == x.shape, gname
