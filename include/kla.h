@@ -106,14 +106,17 @@ kla_status kla_forward(const kla_desc* desc,
                        void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
- * kla_backward -- exact gradient of kla_forward's y, lamT and etaT with respect
- * to every input (yvar carries no gradient).
+ * kla_backward -- exact gradient of kla_forward's y, yvar, lamT and etaT with
+ * respect to every input.
  *
  *   q .. r, lam0, eta0: exactly the forward inputs (NULL beliefs as in forward).
  *   saved: the context a kla_forward call with these inputs filled, or NULL
  *          (then it is recomputed inside the workspace).
- *   dy [B, T, H, dv] dtype (required); dlamT [B, H, dk] and detaT [B, H, dk, dv]
- *          fp32 upstream gradients of the final belief, NULL meaning zero.
+ *   dy [B, T, H, dv] dtype (required); dyvar [B, T, H] fp32, the upstream
+ *          gradient of the readout variance (the Monte Carlo readout of the
+ *          paper's appendix, eq. nmll, samples through it), NULL meaning zero;
+ *          dlamT [B, H, dk] and detaT [B, H, dk, dv] fp32 upstream gradients of
+ *          the final belief, NULL meaning zero.
  *   dq, dk, dabar, dpbar [B, T, H, dk], dv [B, T, H, dv], dr [B, T, H]: dtype, required.
  *   dlam0 [B, H, dk], deta0 [B, H, dk, dv]: fp32 or NULL.
  *   ws / ws_bytes: at least kla_backward_workspace(desc, saved != NULL) bytes.
@@ -122,7 +125,7 @@ kla_status kla_backward(const kla_desc* desc,
                         const void* q, const void* k, const void* v,
                         const void* abar, const void* pbar, const void* r,
                         const float* lam0, const float* eta0, const void* saved,
-                        const void* dy, const float* dlamT, const float* detaT,
+                        const void* dy, const float* dyvar, const float* dlamT, const float* detaT,
                         void* dq, void* dk, void* dv, void* dabar, void* dpbar, void* dr,
                         float* dlam0, float* deta0,
                         void* ws, size_t ws_bytes, hipStream_t stream);
@@ -176,7 +179,7 @@ kla_status kla_backward_ou(const kla_desc* desc,
                            const void* q, const void* k, const void* v,
                            const float* a, const float* p, const float* delta, const void* r,
                            const float* lam0, const float* eta0, const void* saved,
-                           const void* dy, const float* dlamT, const float* detaT,
+                           const void* dy, const float* dyvar, const float* dlamT, const float* detaT,
                            void* dq, void* dk, void* dv, float* da, float* dp, float* ddelta, void* dr,
                            float* dlam0, float* deta0,
                            void* ws, size_t ws_bytes, hipStream_t stream);

@@ -61,7 +61,7 @@ def _load():
     lib.kla_backward_workspace.restype = ctypes.c_size_t
     lib.kla_forward.argtypes = [D] + [_VP] * 14 + [ctypes.c_size_t, _VP]
     lib.kla_forward.restype = ctypes.c_int
-    lib.kla_backward.argtypes = [D] + [_VP] * 21 + [ctypes.c_size_t, _VP]
+    lib.kla_backward.argtypes = [D] + [_VP] * 22 + [ctypes.c_size_t, _VP]
     lib.kla_backward.restype = ctypes.c_int
     lib.kla_decode_step.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
     lib.kla_decode_step.restype = ctypes.c_int
@@ -69,7 +69,7 @@ def _load():
     lib.kla_backward_ou_workspace.restype = ctypes.c_size_t
     lib.kla_forward_ou.argtypes = [D] + [_VP] * 15 + [ctypes.c_size_t, _VP]
     lib.kla_forward_ou.restype = ctypes.c_int
-    lib.kla_backward_ou.argtypes = [D] + [_VP] * 23 + [ctypes.c_size_t, _VP]
+    lib.kla_backward_ou.argtypes = [D] + [_VP] * 24 + [ctypes.c_size_t, _VP]
     lib.kla_backward_ou.restype = ctypes.c_int
     lib.kla_decode_step_ou.argtypes = [ctypes.c_int32] * 5 + [_VP] * 12
     lib.kla_decode_step_ou.restype = ctypes.c_int
@@ -168,10 +168,11 @@ def kla_forward(q, k, v, a, p, r, lam0=None, eta0=None, *, want_var: bool = Fals
 
 
 def kla_backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None, *, saved=None,
-                 want_init_grads: bool = True) -> dict:
-    """Gradients of kla_forward's (y, lamT, etaT) for the upstream gradients
-    (dy, dlamT, detaT); returns dq, dk, dv, da, dp, dr in the input dtype and,
-    when asked, dlam0 [B, H, dk] and deta0 [B, H, dk, dv] in fp32."""
+                 want_init_grads: bool = True, dyvar=None) -> dict:
+    """Gradients of kla_forward's (y, yvar, lamT, etaT) for the upstream gradients
+    (dy, dyvar [B, T, H] fp32 or None, dlamT, detaT); returns dq, dk, dv, da, dp,
+    dr in the input dtype and, when asked, dlam0 [B, H, dk] and deta0
+    [B, H, dk, dv] in fp32."""
     lib = _load()
     _check_inputs(q, k, v, a, p, r)
     dev = q.device
@@ -181,6 +182,7 @@ def kla_backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None, *, sa
     eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
     dlamT = _f32(dlamT, (B, H, dk), dev, "dlamT")
     detaT = _f32(detaT, (B, H, dk, dv), dev, "detaT")
+    dyvar = _f32(dyvar, (B, T, H), dev, "dyvar")
     if tuple(dy.shape) != (B, T, H, dv) or dy.dtype != q.dtype or not dy.is_contiguous():
         raise ValueError("dy must be a contiguous [B, T, H, dv] tensor in the input dtype")
     desc = _desc(q, v)
@@ -190,7 +192,7 @@ def kla_backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None, *, sa
     nws = kla_backward_workspace(desc, saved is not None)
     ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
     st = lib.kla_backward(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(r), _p(lam0), _p(eta0),
-                          _p(saved), _p(dy), _p(dlamT), _p(detaT), _p(out["dq"]), _p(out["dk"]), _p(out["dv"]),
+                          _p(saved), _p(dy), _p(dyvar), _p(dlamT), _p(detaT), _p(out["dq"]), _p(out["dk"]), _p(out["dv"]),
                           _p(out["da"]), _p(out["dp"]), _p(out["dr"]), _p(dlam0), _p(deta0), _p(ws), nws,
                           _stream(dev))
     if st != 0:
@@ -224,31 +226,44 @@ def kla_decode_step(q, k, v, a, p, r, lam, eta, *, want_var: bool = False, y=Non
     return {"y": y, "yvar": yvar, "lam": lam, "eta": eta}
 
 
+def _split_grads(q, v, want_var, grads):
+    """Upstream gradients of (y[, yvar], lamT, etaT) as contiguous tensors or None."""
+    if want_var:
+        dy, dyvar, dlamT, detaT = grads
+    else:
+        (dy, dlamT, detaT), dyvar = grads, None
+    dy = torch.zeros_like(q[..., :1].expand(*q.shape[:3], v.shape[-1])).contiguous() if dy is None \
+        else dy.contiguous()
+    c = lambda t: None if t is None else t.contiguous()
+    return dy, c(dyvar), c(dlamT), c(detaT)
+
+
 class KLAFilter(torch.autograd.Function):
-    """Autograd wrapper: y, lamT, etaT = filter(q, k, v, a, p, r, lam0, eta0)."""
+    """Autograd wrapper: y[, yvar], lamT, etaT = filter(q, k, v, a, p, r, lam0, eta0)."""
 
     @staticmethod
-    def forward(ctx, q, k, v, a, p, r, lam0, eta0):
-        out = kla_forward(q, k, v, a, p, r, lam0, eta0, want_state=True, save=True)
+    def forward(ctx, want_var, q, k, v, a, p, r, lam0, eta0):
+        out = kla_forward(q, k, v, a, p, r, lam0, eta0, want_var=want_var, want_state=True, save=True)
         ctx.save_for_backward(q, k, v, a, p, r, lam0, eta0)
         ctx.saved_ctx = out["saved"]
+        ctx.want_var = want_var
+        if want_var:
+            return out["y"], out["yvar"], out["lamT"], out["etaT"]
         return out["y"], out["lamT"], out["etaT"]
 
     @staticmethod
-    def backward(ctx, dy, dlamT, detaT):
+    def backward(ctx, *grads):
         q, k, v, a, p, r, lam0, eta0 = ctx.saved_tensors
-        dy = torch.zeros_like(q[..., :1].expand(*q.shape[:3], v.shape[-1])).contiguous() if dy is None \
-            else dy.contiguous()
-        g = kla_backward(q, k, v, a, p, r, lam0, eta0, dy,
-                         None if dlamT is None else dlamT.contiguous(),
-                         None if detaT is None else detaT.contiguous(), saved=ctx.saved_ctx)
-        return (g["dq"], g["dk"], g["dv"], g["da"], g["dp"], g["dr"],
+        dy, dyvar, dlamT, detaT = _split_grads(q, v, ctx.want_var, grads)
+        g = kla_backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT, detaT, saved=ctx.saved_ctx, dyvar=dyvar)
+        return (None, g["dq"], g["dk"], g["dv"], g["da"], g["dp"], g["dr"],
                 g["dlam0"] if lam0 is not None else None, g["deta0"] if eta0 is not None else None)
 
 
-def kla_filter(q, k, v, a, p, r, lam0=None, eta0=None):
-    """Differentiable filter: returns (y, lamT, etaT)."""
-    return KLAFilter.apply(q, k, v, a, p, r, lam0, eta0)
+def kla_filter(q, k, v, a, p, r, lam0=None, eta0=None, *, want_var: bool = False):
+    """Differentiable filter: returns (y, lamT, etaT), or (y, yvar, lamT, etaT)
+    with want_var (the readout variance then carries a gradient too)."""
+    return KLAFilter.apply(bool(want_var), q, k, v, a, p, r, lam0, eta0)
 
 
 # ---- OU gates: time-invariant a, p, delta [H, dk] fp32 in place of per-token abar, pbar
@@ -311,9 +326,9 @@ def kla_forward_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, *, want_var: b
 
 
 def kla_backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=None, *, saved=None,
-                    want_init_grads: bool = True) -> dict:
-    """Gradients of kla_forward_ou: dq, dk, dv, dr in the input dtype; da, dp,
-    ddelta [H, dk] fp32; dlam0, deta0 in fp32 when asked."""
+                    want_init_grads: bool = True, dyvar=None) -> dict:
+    """Gradients of kla_forward_ou (dyvar as in kla_backward): dq, dk, dv, dr in
+    the input dtype; da, dp, ddelta [H, dk] fp32; dlam0, deta0 in fp32 when asked."""
     lib = _load()
     _check_inputs_ou(q, k, v, r)
     dev = q.device
@@ -324,6 +339,7 @@ def kla_backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=N
     eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
     dlamT = _f32(dlamT, (B, H, dk), dev, "dlamT")
     detaT = _f32(detaT, (B, H, dk, dv), dev, "detaT")
+    dyvar = _f32(dyvar, (B, T, H), dev, "dyvar")
     if tuple(dy.shape) != (B, T, H, dv) or dy.dtype != q.dtype or not dy.is_contiguous():
         raise ValueError("dy must be a contiguous [B, T, H, dv] tensor in the input dtype")
     desc = _desc(q, v)
@@ -335,7 +351,8 @@ def kla_backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=N
     nws = kla_backward_ou_workspace(desc, saved is not None)
     ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
     st = lib.kla_backward_ou(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(delta), _p(r), _p(lam0),
-                             _p(eta0), _p(saved), _p(dy), _p(dlamT), _p(detaT), _p(out["dq"]), _p(out["dk"]),
+                             _p(eta0), _p(saved), _p(dy), _p(dyvar), _p(dlamT), _p(detaT), _p(out["dq"]),
+                             _p(out["dk"]),
                              _p(out["dv"]), _p(out["da"]), _p(out["dp"]), _p(out["ddelta"]), _p(out["dr"]),
                              _p(dlam0), _p(deta0), _p(ws), nws, _stream(dev))
     if st != 0:
@@ -369,27 +386,29 @@ def kla_decode_step_ou(q, k, v, a, p, delta, r, lam, eta, *, want_var: bool = Fa
 
 
 class KLAFilterOU(torch.autograd.Function):
-    """Autograd wrapper: y, lamT, etaT = filter(q, k, v, a, p, delta, r, lam0, eta0) with OU gates."""
+    """Autograd wrapper: y[, yvar], lamT, etaT = filter(q, k, v, a, p, delta, r, lam0, eta0) with OU gates."""
 
     @staticmethod
-    def forward(ctx, q, k, v, a, p, delta, r, lam0, eta0):
-        out = kla_forward_ou(q, k, v, a, p, delta, r, lam0, eta0, want_state=True, save=True)
+    def forward(ctx, want_var, q, k, v, a, p, delta, r, lam0, eta0):
+        out = kla_forward_ou(q, k, v, a, p, delta, r, lam0, eta0, want_var=want_var, want_state=True, save=True)
         ctx.save_for_backward(q, k, v, a, p, delta, r, lam0, eta0)
         ctx.saved_ctx = out["saved"]
+        ctx.want_var = want_var
+        if want_var:
+            return out["y"], out["yvar"], out["lamT"], out["etaT"]
         return out["y"], out["lamT"], out["etaT"]
 
     @staticmethod
-    def backward(ctx, dy, dlamT, detaT):
+    def backward(ctx, *grads):
         q, k, v, a, p, delta, r, lam0, eta0 = ctx.saved_tensors
-        dy = torch.zeros_like(q[..., :1].expand(*q.shape[:3], v.shape[-1])).contiguous() if dy is None \
-            else dy.contiguous()
-        g = kla_backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy,
-                            None if dlamT is None else dlamT.contiguous(),
-                            None if detaT is None else detaT.contiguous(), saved=ctx.saved_ctx)
-        return (g["dq"], g["dk"], g["dv"], g["da"], g["dp"], g["ddelta"], g["dr"],
+        dy, dyvar, dlamT, detaT = _split_grads(q, v, ctx.want_var, grads)
+        g = kla_backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT, detaT, saved=ctx.saved_ctx,
+                            dyvar=dyvar)
+        return (None, g["dq"], g["dk"], g["dv"], g["da"], g["dp"], g["ddelta"], g["dr"],
                 g["dlam0"] if lam0 is not None else None, g["deta0"] if eta0 is not None else None)
 
 
-def kla_filter_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None):
-    """Differentiable filter with OU gates: returns (y, lamT, etaT)."""
-    return KLAFilterOU.apply(q, k, v, a, p, delta, r, lam0, eta0)
+def kla_filter_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, *, want_var: bool = False):
+    """Differentiable filter with OU gates: returns (y, lamT, etaT), or
+    (y, yvar, lamT, etaT) with want_var."""
+    return KLAFilterOU.apply(bool(want_var), q, k, v, a, p, delta, r, lam0, eta0)

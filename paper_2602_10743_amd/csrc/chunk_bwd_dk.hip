@@ -19,6 +19,9 @@
 //   dq = dqt / lam,  dk = r dkh + 2 k r g,  dr = sum_n (k dkh + k^2 g),
 //   drho = g lam_{t-1} + S / rho,  dabar = S / abar - 2 abar rho^2 drho,
 //   dpbar = -lam_{t-1} rho^2 drho,  dlam0 = c after the first token.
+// An upstream gradient gv_t of the readout variance yvar_t = sum_n q^2 / lam_t
+// adds 2 q gv / lam to dq and -q^2 gv / lam^2 to g_t (YG instantiations; the
+// others leave out its load and arithmetic).
 //
 // One workgroup per (batch, head, 64 key slots); a pair of waves owns 16 key
 // slots n0 + 16 p .. + 15, and the pairs share only the dY / V tiles.  Wave e of
@@ -74,7 +77,8 @@ struct DkCfg {
     static constexpr int STG = 0;                                   // [2][4][kC][16] bf16: abar, pbar, k, q
     static constexpr int RW = STG + 2 * 4 * kC * 16 * 2;            // [2][64] r words
     static constexpr int LW = RW + 2 * 64 * 4;                      // [2][64] chunk-start lam (lanes < 16)
-    static constexpr int QH = LW + 2 * 64 * 4;                      // Qp, Kn split bf16 [kC][LQ2]
+    static constexpr int GV = LW + 2 * 64 * 4;                      // [2][64] yvar gradient (fp32)
+    static constexpr int QH = GV + 2 * 64 * 4;                      // Qp, Kn split bf16 [kC][LQ2]
     static constexpr int QL = QH + kC * LQ2 * 2, KH = QL + kC * LQ2 * 2, KL = KH + kC * LQ2 * 2;
     static constexpr int XT = KL + kC * LQ2 * 2, YT = XT + kC * LX * 4;   // X, Y fp32 [kC][LX]
     static constexpr int QS = YT + kC * LX * 4;                     // group maps [NG][5][16] fp32
@@ -89,6 +93,7 @@ struct DkCfg {
     static_assert(DK >= 32 && DK % 16 == 0 && DV >= 32 && DV % 32 == 0, "backward tile sizes");
     static_assert(NVL >= 1 && TPV * CPR == 64, "value tile loads");
     static_assert(4 + 2 * ((NVL + NW - 1) / NW) <= 8, "requests spread over 4 tokens, two each");
+    static_assert(3 + 2 * ((NVL + NW - 1) / NW) <= 8, "requests spread over 4 tokens, two each");
     static_assert(BYTES + STATIC <= 160 * 1024, "LDS budget of one workgroup");
 };
 
@@ -130,7 +135,7 @@ __device__ __forceinline__ void buf_st32(float v, rsrc_t r, uint32_t voff) {
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, voff, 0, 0);
 }
 
-template <int DK, int DV, bool TI>
+template <int DK, int DV, bool TI, bool YG>
 __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, BwdArgs g,
                                                                        const float* __restrict__ saved_lam,
                                                                        const float* __restrict__ saved_H,
@@ -197,9 +202,10 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
     // zeros), one load per part so that they can be spread over a round:
     //   wave 0: 0..3  abar, pbar, k, q of the pair's slots (1 KiB each, lane -> (t = lane / 2, 8 slots));
     //                 TI: 0, 1  k, q
-    //   wave 1: 0, 1  r (lanes >= nt read as 0) and the chunk-start lam of the 16 slots
+    //   wave 1: 0..2  r (lanes >= nt read as 0), the chunk-start lam of the 16 slots and (YG)
+    //                 the yvar gradient
     //   then this wave's share of the dY and V tiles (loads i = wave, wave + NW, ...), swizzled
-    const int nin = e == 0 && !TI ? 4 : 2;
+    const int nin = e == 0 ? (TI ? 2 : 4) : (YG ? 3 : 2);
     const int nvw = wave < Cfg::NVL ? (Cfg::NVL - wave + NW - 1) / NW : 0;
     const int nparts = nin + 2 * nvw;
     auto issue_part = [&](int cn, int bb, int part) {
@@ -217,6 +223,9 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             } else if (part == 0) {
                 const rsrc_t rr = make_rsrc(r + tok0 * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
                 buf_ld16_lds(rr, wb + Cfg::RW + bb * 256, (uint32_t)lane * H * 2);
+            } else if (part == 2) {
+                const rsrc_t rv = make_rsrc(g.dyvar + tok0 * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 4 : 0u);
+                buf_ld32_lds(rv, wb + Cfg::GV + bb * 256, (uint32_t)lane * H * 4);
             } else {
                 const rsrc_t rl =
                     make_rsrc(saved_lam + ((size_t)bh * nchunk + (in ? cn : 0)) * DK + n0w, in ? 64u : 0u);
@@ -288,6 +297,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             auto in_k = [&](int t) { return __uint_as_float((uint32_t)stg[(2 * kC + t) * 16 + nl] << 16); };
             auto in_q = [&](int t) { return __uint_as_float((uint32_t)stg[(3 * kC + t) * 16 + nl] << 16); };
             auto in_r = [&](int t) { return __uint_as_float(rw[t] << 16); };
+            const float* gvw = reinterpret_cast<const float*>(wb + Cfg::GV) + bb * 64;
 
             // ================================================================ phase 1
             // wave 0: B^T[j, t] = V_j . dY_t (j <= t), tiles (0,0), (0,1), (1,1), as operands over j;
@@ -484,10 +494,10 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 const float rho = rho_r[j], ilam = il_r[j], ia = ia_r[j], den = den_r[j];
                 const float dqt = P_r[j] * Xv, dkh = Yv * iP_r[j];
                 const float kh = rv * kv;
-                const float qtd = qv * ilam * dqt;
+                const float qi = qv * ilam, qg = YG ? qv * gvw[t] : 0.f;
                 const bool ok = FULL || t < nt;
-                const float u = ok ? qtd - kh * dkh : 0.f;
-                const float w = ok ? qtd * ilam : 0.f;
+                const float u = ok ? qi * dqt - kh * dkh : 0.f;
+                const float w = ok ? qi * (dqt + qg) * ilam : 0.f;
                 const float rho2 = rho * rho;
                 const float al = ok ? av * av * rho2 : 1.f;
                 const float be = ok ? pv * rho : 0.f;
@@ -495,7 +505,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 w_[j] = w;
                 al_[j] = al;
                 be_[j] = be;
-                dq_[j] = dqt * ilam;
+                dq_[j] = fmaf(2.f, qg, dqt) * ilam;
                 rdk_[j] = rv * dkh;
                 kr2_[j] = 2.f * kh;
                 ia_[j] = ia;
@@ -641,11 +651,11 @@ __global__ void dr_combine_kernel(const float* __restrict__ part, int nparts, si
     dr[i] = f32_to_bf16(acc);
 }
 
-template <int DK, int DV, bool TI>
+template <int DK, int DV, bool TI, bool YG>
 hipError_t launch_dk(const Shape& s, const BwdArgs& a, const float* saved_lam, const float* saved_H, float* dr_part,
                      hipStream_t st) {
     using Cfg = DkCfg<DK, DV>;
-    auto kern = bwd_dk_kernel<DK, DV, TI>;
+    auto kern = bwd_dk_kernel<DK, DV, TI, YG>;
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::BYTES);
     if (attr != hipSuccess) return attr;
@@ -679,10 +689,14 @@ hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void*
     const float* saved_lam = static_cast<const float*>(saved);
     const float* saved_H = saved_lam + (size_t)s.B * s.H * nchunk * s.dk;
     float* dr_part = static_cast<float*>(ws);
-#define KLA_DK_CASE(DK_, DV_)                                                      \
-    if (s.dk == DK_ && s.dv == DV_)                                                \
-        return a.ou_a ? launch_dk<DK_, DV_, true>(s, a, saved_lam, saved_H, dr_part, st) \
-                      : launch_dk<DK_, DV_, false>(s, a, saved_lam, saved_H, dr_part, st);
+#define KLA_DK_CASE(DK_, DV_)                                                    \
+    if (s.dk == DK_ && s.dv == DV_) {                                            \
+        if (a.dyvar)                                                             \
+            return a.ou_a ? launch_dk<DK_, DV_, true, true>(s, a, saved_lam, saved_H, dr_part, st) \
+                          : launch_dk<DK_, DV_, false, true>(s, a, saved_lam, saved_H, dr_part, st); \
+        return a.ou_a ? launch_dk<DK_, DV_, true, false>(s, a, saved_lam, saved_H, dr_part, st)     \
+                      : launch_dk<DK_, DV_, false, false>(s, a, saved_lam, saved_H, dr_part, st);    \
+    }
 #define KLA_DK_ROW(DK_) KLA_DK_CASE(DK_, 32) KLA_DK_CASE(DK_, 64) KLA_DK_CASE(DK_, 128)
     KLA_DK_ROW(32) KLA_DK_ROW(64) KLA_DK_ROW(128)
 #undef KLA_DK_ROW

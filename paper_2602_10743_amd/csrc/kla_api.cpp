@@ -140,7 +140,7 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
                         !a.dv || (!ou && (!a.da || !a.dp)) || !a.dr))
         return KLA_ERR_NULL;
     if (!all_aligned(a.q, a.k, a.v, a.a, a.p, a.r, (const void*)a.lam0, (const void*)a.eta0, saved, a.dy,
-                     (const void*)a.dlamT, (const void*)a.detaT, a.dq, a.dk, a.dv, a.da, a.dp, a.dr,
+                     (const void*)a.dyvar, (const void*)a.dlamT, (const void*)a.detaT, a.dq, a.dk, a.dv, a.da, a.dp, a.dr,
                      (void*)a.dlam0, (void*)a.deta0, ws, (const void*)a.ou_a, (const void*)a.ou_p,
                      (const void*)a.ou_d, (void*)da, (void*)dp, (void*)dd))
         return KLA_ERR_ALIGN;
@@ -210,11 +210,12 @@ kla_status kla_forward_ou(const kla_desc* desc, const void* q, const void* k, co
 
 kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
                         const void* pbar, const void* r, const float* lam0, const float* eta0, const void* saved,
-                        const void* dy, const float* dlamT, const float* detaT, void* dq, void* dk, void* dv,
-                        void* dabar, void* dpbar, void* dr, float* dlam0, float* deta0, void* ws,
-                        size_t ws_bytes, hipStream_t stream) {
-    const kla::BwdArgs a{q,  k,  v,  abar,  pbar,  r,  lam0, eta0,  dy, dlamT,
-                         detaT, dq, dk, dv, dabar, dpbar, dr, dlam0, deta0};
+                        const void* dy, const float* dyvar, const float* dlamT, const float* detaT, void* dq,
+                        void* dk, void* dv, void* dabar, void* dpbar, void* dr, float* dlam0, float* deta0,
+                        void* ws, size_t ws_bytes, hipStream_t stream) {
+    kla::BwdArgs a{q,  k,  v,  abar,  pbar,  r,  lam0, eta0,  dy, dlamT,
+                   detaT, dq, dk, dv, dabar, dpbar, dr, dlam0, deta0};
+    a.dyvar = dyvar;
     return backward_impl(desc, a, false, saved, nullptr, nullptr, nullptr, ws, ws_bytes, stream);
 }
 
@@ -226,14 +227,15 @@ size_t kla_backward_ou_workspace(const kla_desc* desc, int with_saved) {
 
 kla_status kla_backward_ou(const kla_desc* desc, const void* q, const void* k, const void* v, const float* a,
                            const float* p, const float* delta, const void* r, const float* lam0, const float* eta0,
-                           const void* saved, const void* dy, const float* dlamT, const float* detaT, void* dq,
-                           void* dk, void* dv, float* da, float* dp, float* ddelta, void* dr, float* dlam0,
-                           float* deta0, void* ws, size_t ws_bytes, hipStream_t stream) {
+                           const void* saved, const void* dy, const float* dyvar, const float* dlamT,
+                           const float* detaT, void* dq, void* dk, void* dv, float* da, float* dp, float* ddelta,
+                           void* dr, float* dlam0, float* deta0, void* ws, size_t ws_bytes, hipStream_t stream) {
     kla::BwdArgs g{q,  k,  v,       nullptr, nullptr, r,  lam0,  eta0,  dy, dlamT,
                    detaT, dq, dk, dv, nullptr, nullptr, dr, dlam0, deta0};
     g.ou_a = a;
     g.ou_p = p;
     g.ou_d = delta;
+    g.dyvar = dyvar;
     return backward_impl(desc, g, true, saved, da, dp, ddelta, ws, ws_bytes, stream);
 }
 

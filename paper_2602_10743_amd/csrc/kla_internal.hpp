@@ -33,6 +33,7 @@ struct BwdArgs {
     // OU gates: per-part sums over tokens of the abar and pbar gradients,
     // [2][nparts][H][dk] fp32 (da, dp unused)
     float* ou_part = nullptr;
+    const float* dyvar = nullptr;   // upstream gradient of yvar [B, T, H] fp32, or none
 };
 
 struct DecodeArgs {

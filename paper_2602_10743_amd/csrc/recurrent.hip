@@ -186,7 +186,8 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
 //   dH_t   = F_{t+1} dH_{t+1} + qt_t dy_t^T          (dH_T starts at detaT)
 //   dkh_t  = dH_t v_t,  dv_t = dH_t^T kh_t
 //   dG_t   = PT + sum_{s>=t} (qt_s dqt_s - kh_s dkh_s)
-//   g_t    = c_t - q_t dqt_t / lam_t^2,  c_T = dlamT,
+//   g_t    = c_t - q_t (dqt_t + q_t gv_t) / lam_t^2,  c_T = dlamT,
+//            (gv_t: upstream gradient of the readout variance, zero if none)
 //   c_{t-1}= abar_t^2 rho_t^2 g_t - pbar_t rho_t dG_t
 // and the input gradients follow by the chain rule through rho, lam and F.
 template <typename S, int DK, int DV>
@@ -282,11 +283,12 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
             const float at = ou ? oa : ld(a, base * DK + tid), pt = ou ? op : ld(p, base * DK + tid);
             const float lprev = t > 0 ? wlam[(base - s.H) * DK + tid] : (g.lam0 ? g.lam0[(size_t)bh * DK + tid] : 1.f);
             const float qtl = sQt[tid], kh = sKh[tid];
+            const float qg = g.dyvar ? qt * g.dyvar[base] : 0.f;
             Sg += qtl * dqt - kh * dkh;                       // dG_t
             const float rho = 1.f / (at * at + pt * lprev);
-            const float gl = cnext - qt * dqt / (lam_t * lam_t);  // g_t
+            const float gl = cnext - qt * (dqt + qg) / (lam_t * lam_t);  // g_t
             const float drho = gl * lprev + Sg / rho;
-            st(dq, base * DK + tid, dqt / lam_t);
+            st(dq, base * DK + tid, (dqt + 2.f * qg) / lam_t);
             st(dk, base * DK + tid, rt * dkh + 2.f * kt * rt * gl);
             const float dav = Sg / at - 2.f * at * rho * rho * drho, dpv = -lprev * rho * rho * drho;
             if (ou) {

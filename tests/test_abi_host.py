@@ -81,7 +81,8 @@ def test_forward_argument_errors(lib):
 def test_backward_and_decode_argument_errors(lib):
     fake = ctypes.c_void_p(0x10000)
     d = _desc()
-    args = [fake] * 6 + [None, None, None] + [fake, None, None] + [fake] * 6 + [None, None] + [fake]
+    # q k v a p r lam0 eta0 saved dy dyvar dlamT detaT dq dk dv da dp dr dlam0 deta0 ws
+    args = [fake] * 6 + [None, None, None] + [fake, None, None, None] + [fake] * 6 + [None, None] + [fake]
     assert lib.kla_backward(ctypes.byref(d), *args, 0, None) == 5
     bad = list(args)
     bad[9] = None                                                  # dy
@@ -129,10 +130,10 @@ def test_ou_argument_errors(lib):
     bad[5] = odd
     assert lib.kla_forward_ou(ctypes.byref(d), *bad, 256, None) == 4
     assert lib.kla_forward_ou(ctypes.byref(d), *ok, 0, None) == 5
-    # q k v a p delta r lam0 eta0 saved dy dlamT detaT dq dk dv da dp ddelta dr dlam0 deta0 ws
-    bwd = [fake] * 7 + [None, None, None] + [fake, None, None] + [fake] * 7 + [None, None] + [fake]
+    # q k v a p delta r lam0 eta0 saved dy dyvar dlamT detaT dq dk dv da dp ddelta dr dlam0 deta0 ws
+    bwd = [fake] * 7 + [None, None, None] + [fake, None, None, None] + [fake] * 7 + [None, None] + [fake]
     assert lib.kla_backward_ou(ctypes.byref(d), *bwd, 0, None) == 5
-    for i in (16, 17, 18):                                         # da, dp, ddelta
+    for i in (17, 18, 19):                                         # da, dp, ddelta
         bad = list(bwd)
         bad[i] = None
         assert lib.kla_backward_ou(ctypes.byref(d), *bad, 1 << 40, None) == 1

@@ -92,14 +92,15 @@ def test_backward_small(kla, B, T, H, dk, dv, dtype, dist):
     g = np.random.default_rng(T)
     dlamT = g.standard_normal((B, H, dk)).astype(np.float32).astype(np.float64)
     detaT = g.standard_normal((B, H, dk, dv)).astype(np.float32).astype(np.float64)
+    dyvar = g.standard_normal((B, T, H)).astype(np.float32).astype(np.float64)
     log(f"backward small B{B} T{T} H{H} dk{dk} dv{dv} {dtype}")
     x = _dev_inputs(case, dtype)
     f32 = lambda a: torch.tensor(a, dtype=torch.float32, device=DEV)
     gr = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), x["dy"],
-                          f32(dlamT), f32(detaT))
+                          f32(dlamT), f32(detaT), dyvar=f32(dyvar))
     torch.cuda.synchronize()
     ref = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0,
-                          case["dy"], dlamT, detaT)
+                          case["dy"], dlamT, detaT, dyvar=dyvar)
     rep = []
     for n in ("dq", "dk", "dv", "da", "dp", "dr"):
         _check(n, to_np(gr[n]), ref[n], TOL[dtype], rep)
@@ -181,10 +182,12 @@ def test_autograd_wrapper(kla):
     case = K.random_case(1, 50, 2, 32, 32, "f32", seed=2)
     x = {n: to_torch(case[n], "f32", DEV).requires_grad_(True) for n in K.NAMES}
     log("autograd")
-    y, lamT, etaT = kla.kla_filter(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"])
+    y, yvar, lamT, etaT = kla.kla_filter(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], want_var=True)
     dy = to_torch(case["dy"], "f32", DEV)
-    (y * dy).sum().backward()
-    ref = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], None, None, case["dy"])
+    gv = np.random.default_rng(3).standard_normal((1, 50, 2)).astype(np.float32).astype(np.float64)
+    ((y * dy).sum() + (yvar * to_torch(gv, "f32", DEV)).sum()).backward()
+    ref = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], None, None, case["dy"],
+                          dyvar=gv)
     for n, gn in (("q", "dq"), ("k", "dk"), ("v", "dv"), ("a", "da"), ("p", "dp"), ("r", "dr")):
         assert rel_err(to_np(x[n].grad), ref[gn]) <= TOL["f32"], n
 

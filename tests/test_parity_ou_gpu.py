@@ -78,19 +78,20 @@ def test_ou_forward_backward_small(kla, B, T, H, dk, dv, dtype, dist):
     g = np.random.default_rng(T + 3)
     dlamT = g.standard_normal((B, H, dk)).astype(np.float32).astype(np.float64)
     detaT = g.standard_normal((B, H, dk, dv)).astype(np.float32).astype(np.float64)
+    dyvar = g.standard_normal((B, T, H)).astype(np.float32).astype(np.float64)
     log(f"ou small B{B} T{T} H{H} dk{dk} dv{dv} {dtype}")
     x = {n: to_torch(case[n], dtype, DEV) for n in TOKEN_NAMES}
     out = kla.kla_forward_ou(x["q"], x["k"], x["v"], P["a"], P["p"], P["delta"], x["r"], _f32(lam0), _f32(eta0),
                              want_var=True, save=True)
     gr = kla.kla_backward_ou(x["q"], x["k"], x["v"], P["a"], P["p"], P["delta"], x["r"], _f32(lam0), _f32(eta0),
-                             x["dy"], _f32(dlamT), _f32(detaT), saved=out["saved"])
+                             x["dy"], _f32(dlamT), _f32(detaT), saved=out["saved"], dyvar=_f32(dyvar))
     # the backward without a saved context recomputes it and must agree bit for bit
     gr2 = kla.kla_backward_ou(x["q"], x["k"], x["v"], P["a"], P["p"], P["delta"], x["r"], _f32(lam0),
-                              _f32(eta0), x["dy"], _f32(dlamT), _f32(detaT))
+                              _f32(eta0), x["dy"], _f32(dlamT), _f32(detaT), dyvar=_f32(dyvar))
     torch.cuda.synchronize()
     ref = oracle.forward_ou(case["q"], case["k"], case["v"], Pd["a"], Pd["p"], Pd["delta"], case["r"], lam0, eta0)
     rg = oracle.backward_ou(case["q"], case["k"], case["v"], Pd["a"], Pd["p"], Pd["delta"], case["r"], lam0, eta0,
-                            case["dy"], dlamT, detaT)
+                            case["dy"], dlamT, detaT, dyvar=dyvar)
     tol = TOL[dtype]
     rep = []
     _check("y", to_np(out["y"]), K.quantise(ref["y"], dtype), tol, rep)
@@ -170,9 +171,12 @@ def test_ou_autograd_wrapper(kla):
     x = {n: to_torch(case[n], "bf16", DEV) for n in TOKEN_NAMES}
     P, _ = _ou(H, dk, seed=21)
     leaves = {n: P[n].clone().requires_grad_(True) for n in ("a", "p", "delta")}
-    y, lamT, etaT = kla.kla_filter_ou(x["q"], x["k"], x["v"], leaves["a"], leaves["p"], leaves["delta"], x["r"])
-    y.backward(x["dy"])
-    gr = kla.kla_backward_ou(x["q"], x["k"], x["v"], P["a"], P["p"], P["delta"], x["r"], None, None, x["dy"])
+    y, yvar, lamT, etaT = kla.kla_filter_ou(x["q"], x["k"], x["v"], leaves["a"], leaves["p"], leaves["delta"],
+                                            x["r"], want_var=True)
+    gv = torch.randn(yvar.shape, generator=torch.Generator().manual_seed(4)).to(DEV)
+    torch.autograd.backward([y, yvar], [x["dy"], gv])
+    gr = kla.kla_backward_ou(x["q"], x["k"], x["v"], P["a"], P["p"], P["delta"], x["r"], None, None, x["dy"],
+                             _f32(np.zeros((B, H, dk))), _f32(np.zeros((B, H, dk, dv))), dyvar=gv)
     torch.cuda.synchronize()
     for n, g in (("a", "da"), ("p", "dp"), ("delta", "ddelta")):
         assert torch.equal(leaves[n].grad, gr[g]), n
