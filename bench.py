@@ -17,6 +17,11 @@ workload.
 With --ou the same shape runs with OU gates instead (kla_forward_ou /
 kla_backward_ou: time-invariant a, p, delta [H, dk] in place of the per-token
 abar and pbar tensors); its traffic summary is profiles/lm_layer_ou_traffic.md.
+
+With --pc it times the forward of the per-channel-precision variant
+(kla_forward_pc: r drawn per value channel, precision and gates per (key slot,
+value channel)), an elementwise scan bound by VALU issue; its roofline is the
+chip's fp32 VALU issue rate (see ALU_SLOTS_PER_ELEMENT).
 """
 import argparse
 import json
@@ -32,6 +37,15 @@ import numpy as np
 
 METRIC = "KLA layer fwd+bwd tokens/sec (B·T·H, d=128) on 1 MI355X; % of HBM/MFMA roofline"
 HBM_PEAK_GBS = 8000.0
+# fp32 VALU issue of the chip: 256 CUs x 4 SIMDs, one wave64 instruction (64 lanes) per 4
+# cycles per SIMD at 2.4 GHz, i.e. 16 lane-operations per cycle per SIMD (packed fp32 unused)
+VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
+# issue slots of one element update of the per-channel scan, with the per-token products
+# abar^2, k^2, q^2 and r v shared by a row or column: den = abar^2 + pbar lam (1), k^2 r (1),
+# num = lam + k^2 r den (1), den num (1), its reciprocal R (quarter rate: 4), 1/den = num R and
+# lam_t = num / den (2), 1/lam_t = den^2 R (2), the gate abar / den (1), k r v (1), eta_t (1),
+# eta_t / lam_t (1) and the two readout sums (2)
+ALU_SLOTS_PER_ELEMENT = 18
 
 
 def algorithmic_bytes(w, s, ou=False):
@@ -43,6 +57,72 @@ def algorithmic_bytes(w, s, ou=False):
     fwd = (nk * w.dk + w.dv + 1) * s + w.dv * s
     bwd = 2 * (nk * w.dk + w.dv + 1) * s + w.dv * s
     return fwd, bwd
+
+
+def cpu_baseline_pc(w):
+    """fp64 oracle forward of the per-channel workload on a few sampled sequences."""
+    import kla_inputs as K
+    import oracle
+    threads = oracle.default_threads()
+    pairs = [(b, h) for b in range(w.B) for h in range(w.H)]
+    np.random.default_rng(0).shuffle(pairs)
+    sample = sorted(pairs[:max(1, min(8 * threads, len(pairs)))])
+    sl = K.pairs_slice(w, sample, names=("q", "k", "v", "a", "p", "rc"))
+    t0 = time.perf_counter()
+    oracle.forward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["rc"], nthreads=threads)
+    t1 = time.perf_counter()
+    return {"value": len(sample) * w.T / (t1 - t0), "unit": "tokens/s", "cores": min(threads, len(sample)),
+            "kind": "oracle", "sample": f"{len(sample)} (batch, head) sequences of T={w.T}, forward ({t1 - t0:.1f}s)"}
+
+
+def bench_pc(args, w, dev):
+    """Forward of the per-channel-precision variant at the LM-layer shape."""
+    import torch
+    import kla_inputs as K
+    import paper_2602_10743_amd as kla
+    names = ("q", "k", "v", "a", "p", "rc")
+    bits = K.full(w, names=names, as_bits=True)
+    x = {n: torch.from_numpy(np.ascontiguousarray(bits[n].view(np.int16))).view(torch.bfloat16).to(dev)
+         for n in bits}
+    del bits
+    stream = torch.cuda.current_stream(dev)
+    y = torch.empty_like(x["v"])
+
+    def step():
+        kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], want_state=False, y=y)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    t0 = time.perf_counter()
+    ev[0].record(stream)
+    for _ in range(args.steps):
+        step()
+    ev[1].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    ms = ev[0].elapsed_time(ev[1]) / args.steps
+    th = w.token_heads
+    elements = th * w.dk * w.dv
+    achieved = elements * ALU_SLOTS_PER_ELEMENT / (ms * 1e-3)
+    res = {
+        "metric": METRIC, "value": th / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name + "_pc", "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv,
+                   "pass": "fwd", "precision": "per value channel (bf16 inputs, fp32 scan)",
+                   "tokens_counted": "B*T*H"},
+        "roofline": {"bound": "alu", "kernel": "kla_forward_pc", "achieved": achieved / 1e12,
+                     "peak": VALU_LANE_OPS / 1e12, "unit": "T lane-ops/s",
+                     "frac": achieved / VALU_LANE_OPS, "traffic": None,
+                     "element_updates_per_call": elements, "slots_per_element": ALU_SLOTS_PER_ELEMENT,
+                     "fwd_ms": ms},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline_pc(w)
+    print(json.dumps(res), flush=True)
 
 
 def cpu_baseline(w, budget_s: float, ou=None):
@@ -99,6 +179,8 @@ def main():
                     help="run a plain elementwise copy of known size first (counter calibration)")
     ap.add_argument("--ou", action="store_true",
                     help="OU gates: time-invariant (a, p, delta) instead of per-token abar, pbar")
+    ap.add_argument("--pc", action="store_true",
+                    help="forward of the per-channel-precision variant (elementwise scan)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the filter layer shards over (batch, head) with no "
@@ -112,6 +194,9 @@ def main():
     w = K.WORKLOADS[2]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.pc:
+        bench_pc(args, w, dev)
+        return
     names = ("q", "k", "v", "r", "dy") if args.ou else K.NAMES + ("dy",)
     bits = K.full(w, names=names, as_bits=True)
     x = {n: torch.from_numpy(np.ascontiguousarray(bits[n].view(np.int16))).view(torch.bfloat16).to(dev)

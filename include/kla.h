@@ -191,6 +191,35 @@ kla_status kla_decode_step_ou(int32_t S, int32_t H, int32_t dk, int32_t dv, int3
                               const float* a, const float* p, const float* delta, const void* r,
                               float* lam, float* eta, void* y, float* yvar, hipStream_t stream);
 
+/*
+ * Per-channel precision (Algorithm 1 with Lambda^v of shape (B, T, 1, D)): one
+ * observation precision per value channel, r_t[d], so that the precision and
+ * the forget gate are dk x dv arrays per head (eqs. kla-prec-mat and
+ * kla-mean-mat elementwise):
+ *
+ *   rho_t[n,d] = 1 / (abar_t[n]^2 + pbar_t[n] lam_{t-1}[n,d])
+ *   lam_t[n,d] = rho_t[n,d] lam_{t-1}[n,d] + k_t[n]^2 r_t[d]
+ *   H_t[n,d]   = abar_t[n] rho_t[n,d] H_{t-1}[n,d] + k_t[n] r_t[d] v_t[d]
+ *   y_t[d]     = sum_n q_t[n] H_t[n,d] / lam_t[n,d]
+ *   yvar_t[d]  = sum_n q_t[n]^2 / lam_t[n,d]
+ *
+ * Shapes differ from the entry points above only in: r [B, T, H, dv] (decode:
+ * [S, H, dv]) in dtype; lam0, lamT, decode lam [.., H, dk, dv] fp32; yvar
+ * [B, T, H, dv] fp32 (decode: [S, H, dv]).  Workspace: kla_forward_workspace.
+ * Every other convention is as above.
+ */
+kla_status kla_forward_pc(const kla_desc* desc,
+                          const void* q, const void* k, const void* v,
+                          const void* abar, const void* pbar, const void* r,
+                          const float* lam0, const float* eta0,
+                          void* y, float* yvar, float* lamT, float* etaT,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+kla_status kla_decode_step_pc(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype,
+                              const void* q, const void* k, const void* v,
+                              const void* abar, const void* pbar, const void* r,
+                              float* lam, float* eta, void* y, float* yvar, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char* kla_status_string(kla_status status);
 

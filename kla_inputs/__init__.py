@@ -26,9 +26,9 @@ from typing import Iterable, Optional
 
 import numpy as np
 
-TENSOR_ID = {"q": 0, "k": 1, "v": 2, "a": 3, "p": 4, "r": 5, "dy": 6}
+TENSOR_ID = {"q": 0, "k": 1, "v": 2, "a": 3, "p": 4, "r": 5, "dy": 6, "rc": 10}
 KEY_DIM = ("q", "k", "a", "p")          # [B, T, H, dk]
-VAL_DIM = ("v", "dy")                   # [B, T, H, dv]
+VAL_DIM = ("v", "dy", "rc")             # [B, T, H, dv]; rc: one observation precision per value channel
 NAMES = ("q", "k", "v", "a", "p", "r")
 
 
@@ -118,7 +118,7 @@ def _draw_iid(w: Workload, name: str, b: int, h: int, T: int, seed: int) -> np.n
             return sigmoid(z + 2.0)
         if name == "p":
             return softplus(z - 2.0)
-        return softplus(z)                      # r
+        return softplus(z)                      # r, rc
     # language-model distributions (also the long-context stress)
     if name == "k":
         return z / np.linalg.norm(z, axis=1, keepdims=True)
@@ -129,7 +129,7 @@ def _draw_iid(w: Workload, name: str, b: int, h: int, T: int, seed: int) -> np.n
         return sigmoid(z + shift)
     if name == "p":
         return softplus(z - 3.0)
-    return softplus(z)                          # r
+    return softplus(z)                          # r, rc
 
 
 @lru_cache(maxsize=4)

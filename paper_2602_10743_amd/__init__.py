@@ -20,6 +20,7 @@ import torch
 __all__ = ["kla_forward", "kla_backward", "kla_decode_step", "kla_status_string",
            "kla_forward_workspace", "kla_backward_workspace", "kla_saved_bytes",
            "kla_forward_ou", "kla_backward_ou", "kla_decode_step_ou", "kla_backward_ou_workspace",
+           "kla_forward_pc", "kla_decode_step_pc",
            "KLAError", "KLAFilter", "kla_filter", "KLAFilterOU", "kla_filter_ou", "library_path"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -73,6 +74,10 @@ def _load():
     lib.kla_backward_ou.restype = ctypes.c_int
     lib.kla_decode_step_ou.argtypes = [ctypes.c_int32] * 5 + [_VP] * 12
     lib.kla_decode_step_ou.restype = ctypes.c_int
+    lib.kla_forward_pc.argtypes = [D] + [_VP] * 13 + [ctypes.c_size_t, _VP]
+    lib.kla_forward_pc.restype = ctypes.c_int
+    lib.kla_decode_step_pc.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
+    lib.kla_decode_step_pc.restype = ctypes.c_int
     lib.kla_status_string.argtypes = [ctypes.c_int]
     lib.kla_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -412,3 +417,64 @@ def kla_filter_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, *, want_var: bo
     """Differentiable filter with OU gates: returns (y, lamT, etaT), or
     (y, yvar, lamT, etaT) with want_var."""
     return KLAFilterOU.apply(bool(want_var), q, k, v, a, p, delta, r, lam0, eta0)
+
+
+# ---- per-channel precision: r [B, T, H, dv], beliefs [B, H, dk, dv]
+
+def kla_forward_pc(q, k, v, a, p, r, lam0=None, eta0=None, *, want_var: bool = False,
+                   want_state: bool = True, y=None) -> dict:
+    """Filter with one observation precision per value channel: q, k, a, p
+    [B, T, H, dk]; v, r [B, T, H, dv] (one dtype); lam0, eta0 [B, H, dk, dv] fp32
+    or None.  Returns y and, as asked, yvar [B, T, H, dv] and lamT, etaT
+    [B, H, dk, dv]."""
+    lib = _load()
+    if not q.is_cuda:
+        raise ValueError("KLA tensors must live on a GPU; the layer has no CPU path")
+    if q.dtype not in _DTYPES or q.dim() != 4:
+        raise ValueError("q must be a [B, T, H, dk] float32 or bfloat16 tensor")
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    for name, t, shape in (("k", k, (B, T, H, dk)), ("a", a, (B, T, H, dk)), ("p", p, (B, T, H, dk)),
+                           ("v", v, (B, T, H, dv)), ("r", r, (B, T, H, dv))):
+        if tuple(t.shape) != shape or t.dtype != q.dtype or t.device != q.device or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {shape} tensor in q's dtype")
+    dev = q.device
+    lam0 = _f32(lam0, (B, H, dk, dv), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    desc = _desc(q, v)
+    if y is None:
+        y = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    yvar = torch.empty((B, T, H, dv), dtype=torch.float32, device=dev) if want_var else None
+    lamT = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_state else None
+    etaT = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_state else None
+    nws = kla_forward_workspace(desc)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    st = lib.kla_forward_pc(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(r), _p(lam0), _p(eta0),
+                            _p(y), _p(yvar), _p(lamT), _p(etaT), _p(ws), nws, _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_forward_pc")
+    return {"y": y, "yvar": yvar, "lamT": lamT, "etaT": etaT}
+
+
+def kla_decode_step_pc(q, k, v, a, p, r, lam, eta, *, want_var: bool = False, y=None) -> dict:
+    """One token with per-channel precision: q, k, a, p [S, H, dk]; v, r [S, H, dv];
+    lam, eta [S, H, dk, dv] fp32 updated in place."""
+    lib = _load()
+    if not q.is_cuda or q.dtype not in _DTYPES:
+        raise ValueError("decode inputs must be fp32/bf16 GPU tensors")
+    S, H, dk = q.shape
+    dv = v.shape[-1]
+    for name, t, shape in (("k", k, (S, H, dk)), ("a", a, (S, H, dk)), ("p", p, (S, H, dk)),
+                           ("v", v, (S, H, dv)), ("r", r, (S, H, dv))):
+        if tuple(t.shape) != shape or t.dtype != q.dtype or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {shape} tensor in q's dtype")
+    _f32(lam, (S, H, dk, dv), q.device, "lam")
+    _f32(eta, (S, H, dk, dv), q.device, "eta")
+    if y is None:
+        y = torch.empty((S, H, dv), dtype=q.dtype, device=q.device)
+    yvar = torch.empty((S, H, dv), dtype=torch.float32, device=q.device) if want_var else None
+    st = lib.kla_decode_step_pc(S, H, dk, dv, _DTYPES[q.dtype], _p(q), _p(k), _p(v), _p(a), _p(p), _p(r),
+                                _p(lam), _p(eta), _p(y), _p(yvar), _stream(q.device))
+    if st != 0:
+        raise KLAError(st, "kla_decode_step_pc")
+    return {"y": y, "yvar": yvar, "lam": lam, "eta": eta}

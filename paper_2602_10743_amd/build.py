@@ -24,7 +24,7 @@ FLAGS = [
     "-ffp-contract=fast", "-munsafe-fp-atomics",
     "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function",
 ]
-SOURCES = ["kla_api.cpp", "recurrent.hip", "validate.hip", "ou.hip", "chunk_fwd.hip", "chunk_bwd_dv.hip",
+SOURCES = ["kla_api.cpp", "recurrent.hip", "validate.hip", "ou.hip", "pc.hip", "chunk_fwd.hip", "chunk_bwd_dv.hip",
            "chunk_bwd_dk.hip"]
 
 

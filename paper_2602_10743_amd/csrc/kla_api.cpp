@@ -46,7 +46,8 @@ bool all_aligned(P... ps) {
 namespace kla {
 hipError_t launch_validate(const Shape& s, const void* q, const void* k, const void* v, const void* a,
                            const void* p, const void* r, const float* lam0, const float* eta0, int T,
-                           int* flag, hipStream_t st, const float* ou_a, const float* ou_p, const float* ou_d);
+                           int* flag, hipStream_t st, const float* ou_a, const float* ou_p, const float* ou_d,
+                           bool per_channel);
 }
 
 namespace {
@@ -57,9 +58,10 @@ namespace {
 kla_status validate(const kla::Shape& s, int T, const void* q, const void* k, const void* v, const void* a,
                     const void* p, const void* r, const float* lam0, const float* eta0, void* flag_ws,
                     hipStream_t st, const float* ou_a = nullptr, const float* ou_p = nullptr,
-                    const float* ou_d = nullptr) {
+                    const float* ou_d = nullptr, bool per_channel = false) {
     int* flag = static_cast<int*>(flag_ws);
-    if (kla::launch_validate(s, q, k, v, a, p, r, lam0, eta0, T, flag, st, ou_a, ou_p, ou_d) != hipSuccess)
+    if (kla::launch_validate(s, q, k, v, a, p, r, lam0, eta0, T, flag, st, ou_a, ou_p, ou_d, per_channel) !=
+        hipSuccess)
         return KLA_ERR_HIP;
     int host = 0;
     if (hipMemcpyAsync(&host, flag, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess) return KLA_ERR_HIP;
@@ -237,6 +239,37 @@ kla_status kla_backward_ou(const kla_desc* desc, const void* q, const void* k, c
     g.ou_d = delta;
     g.dyvar = dyvar;
     return backward_impl(desc, g, true, saved, da, dp, ddelta, ws, ws_bytes, stream);
+}
+
+kla_status kla_forward_pc(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
+                          const void* pbar, const void* r, const float* lam0, const float* eta0, void* y,
+                          float* yvar, float* lamT, float* etaT, void* ws, size_t ws_bytes, hipStream_t stream) {
+    kla_status st = check_desc(desc);
+    if (st != KLA_OK) return st;
+    if (desc->T > 0 && (!q || !k || !v || !abar || !pbar || !r || !y)) return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, y, (void*)yvar, (void*)lamT,
+                     (void*)etaT, ws))
+        return KLA_ERR_ALIGN;
+    if (!ws || ws_bytes < kla_forward_workspace(desc)) return KLA_ERR_WORKSPACE;
+    const kla::Shape s = shape_of(desc);
+    if (check_mode()) {
+        st = validate(s, s.T, q, k, v, abar, pbar, r, lam0, eta0, ws, stream, nullptr, nullptr, nullptr, true);
+        if (st != KLA_OK) return st;
+    }
+    const kla::FwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, y, yvar, lamT, etaT};
+    return kla::launch_forward_pc(s, a, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+kla_status kla_decode_step_pc(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,
+                              const void* k, const void* v, const void* abar, const void* pbar, const void* r,
+                              float* lam, float* eta, void* y, float* yvar, hipStream_t stream) {
+    kla_desc d{S, 1, H, dk, dv, dtype};
+    kla_status st = check_desc(&d);
+    if (st != KLA_OK) return st;
+    if (!q || !k || !v || !abar || !pbar || !r || !lam || !eta || !y) return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, abar, pbar, r, (void*)lam, (void*)eta, y, (void*)yvar)) return KLA_ERR_ALIGN;
+    const kla::DecodeArgs a{q, k, v, abar, pbar, r, lam, eta, y, yvar};
+    return kla::launch_decode_pc(shape_of(&d), a, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 
 kla_status kla_decode_step(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,

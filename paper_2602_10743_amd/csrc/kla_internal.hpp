@@ -63,6 +63,10 @@ hipError_t launch_backward_dv(const Shape& s, const BwdArgs& a, const float* sav
 int chunked_ou_parts(const Shape& s);
 int recurrent_ou_parts(const Shape& s);
 
+// Per-channel precision (r [B, T, H, dv], beliefs [B, H, dk, dv]): elementwise scan and decode.
+hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, hipStream_t st);
+hipError_t launch_decode_pc(const Shape& s, const DecodeArgs& a, hipStream_t st);
+
 // OU gates: gradients of the parameters from the per-part gate-gradient sums
 hipError_t launch_ou_param_grads(int H, int dk, int nparts, const float* part, const float* a, const float* p,
                                  const float* d, float* da, float* dp, float* dd, hipStream_t st);

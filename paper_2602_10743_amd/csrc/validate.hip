@@ -53,17 +53,20 @@ __global__ __launch_bounds__(256) void validate_kernel(size_t nk, size_t nv, siz
 
 hipError_t launch_validate(const Shape& s, const void* q, const void* k, const void* v, const void* a,
                            const void* p, const void* r, const float* lam0, const float* eta0, int T,
-                           int* flag, hipStream_t st, const float* ou_a, const float* ou_p, const float* ou_d) {
+                           int* flag, hipStream_t st, const float* ou_a, const float* ou_p, const float* ou_d,
+                           bool per_channel) {
     hipLaunchKernelGGL(zero_flag, dim3(1), dim3(64), 0, st, flag);
     const size_t tok = (size_t)s.B * T * s.H;
-    const size_t nk = tok * s.dk, nv = tok * s.dv, nb = (size_t)s.B * s.H * s.dk, ne = nb * s.dv;
+    const size_t nk = tok * s.dk, nv = tok * s.dv, ne = (size_t)s.B * s.H * s.dk * s.dv;
+    // per-channel precision: r [B, T, H, dv] and lam0 [B, H, dk, dv]
+    const size_t nr = per_channel ? nv : tok, nb = per_channel ? ne : (size_t)s.B * s.H * s.dk;
     const size_t nou = (size_t)s.H * s.dk;
     const unsigned grid = 1024;
     if (s.bf16)
-        hipLaunchKernelGGL(validate_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, nk, nv, tok, nb, ne, q, k, v, a,
+        hipLaunchKernelGGL(validate_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, nk, nv, nr, nb, ne, q, k, v, a,
                            p, r, lam0, eta0, nou, ou_a, ou_p, ou_d, flag);
     else
-        hipLaunchKernelGGL(validate_kernel<f32_t>, dim3(grid), dim3(256), 0, st, nk, nv, tok, nb, ne, q, k, v, a,
+        hipLaunchKernelGGL(validate_kernel<f32_t>, dim3(grid), dim3(256), 0, st, nk, nv, nr, nb, ne, q, k, v, a,
                            p, r, lam0, eta0, nou, ou_a, ou_p, ou_d, flag);
     return hipGetLastError();
 }

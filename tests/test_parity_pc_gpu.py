@@ -1,0 +1,158 @@
+"""GPU parity of the per-channel-precision entry points (kla_forward_pc,
+kla_decode_step_pc) against the fp64 oracle, which runs every (n, d) filter
+with its own precision (r [B, T, H, dv], beliefs [B, H, dk, dv]).
+
+Small shapes are compared over whole tensors; the language-model shape
+(B8 T2048 H16 d128 bf16, r drawn per value channel) runs at full size and is
+compared on sampled (batch, head) sequences.
+"""
+import numpy as np
+import pytest
+
+import kla_inputs as K
+import oracle
+from kla_testutil import TOL, bits_to_torch, log, rel_err, to_np, to_torch
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+NAMES = ("q", "k", "v", "a", "p", "rc")
+
+
+@pytest.fixture(scope="module")
+def kla():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_10743_amd as lib
+    lib._load()
+    return lib
+
+
+def _check(name, got, ref, tol, report):
+    e = rel_err(got, ref)
+    report.append(f"{name}={e:.2e}(1%floor {rel_err(got, ref, 0.01):.1e})")
+    assert np.all(np.isfinite(got)), f"{name} has non-finite values"
+    assert e <= tol, f"{name}: rel err {e:.3e} > {tol:.0e}"
+
+
+def _f32(a):
+    return torch.tensor(np.asarray(a), dtype=torch.float32, device=DEV)
+
+
+def _case(B, T, H, dk, dv, dtype, seed, dist):
+    w = K.Workload(0, "custom", B, T, H, dk, dv, dtype, dist, False)
+    return K.full(w, names=NAMES, seed=seed)
+
+
+PC_SMALL = [  # B, T, H, dk, dv, dtype, dist
+    (2, 100, 3, 16, 16, "f32", "c0"),
+    (1, 77, 2, 32, 64, "f32", "lm"),
+    (3, 41, 1, 128, 16, "f32", "lm"),
+    (2, 130, 2, 64, 32, "bf16", "lm"),
+    (1, 70, 2, 128, 128, "bf16", "lm"),
+    (1, 33, 1, 16, 128, "bf16", "c0"),
+]
+
+
+@pytest.mark.parametrize("B,T,H,dk,dv,dtype,dist", PC_SMALL)
+@pytest.mark.parametrize("init", [False, True])
+def test_pc_forward_small(kla, B, T, H, dk, dv, dtype, dist, init):
+    case = _case(B, T, H, dk, dv, dtype, seed=T * 5 + dk, dist=dist)
+    lam0 = eta0 = None
+    if init:
+        g = np.random.default_rng(T)
+        lam0 = (0.5 + g.random((B, H, dk, dv))).astype(np.float32).astype(np.float64)
+        eta0 = g.standard_normal((B, H, dk, dv)).astype(np.float32).astype(np.float64)
+    log(f"pc forward B{B} T{T} H{H} dk{dk} dv{dv} {dtype} init={init}")
+    x = {n: to_torch(case[n], dtype, DEV) for n in NAMES}
+    out = kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"],
+                             None if lam0 is None else _f32(lam0), None if eta0 is None else _f32(eta0),
+                             want_var=True)
+    torch.cuda.synchronize()
+    ref = oracle.forward(case["q"], case["k"], case["v"], case["a"], case["p"], case["rc"], lam0, eta0)
+    tol = TOL[dtype]
+    rep = []
+    _check("y", to_np(out["y"]), K.quantise(ref["y"], dtype), tol, rep)
+    _check("yvar", to_np(out["yvar"]), ref["yvar"], TOL["f32"], rep)
+    _check("lamT", to_np(out["lamT"]), ref["lamT"], TOL["f32"], rep)
+    _check("etaT", to_np(out["etaT"]), ref["etaT"], TOL["f32"], rep)
+    assert np.all(to_np(out["lamT"]) > 0) and np.all(to_np(out["yvar"]) > 0)
+    log("  " + " ".join(rep))
+
+
+def test_pc_empty_sequence(kla):
+    B, H, dk, dv = 2, 2, 32, 16
+    g = np.random.default_rng(1)
+    lam0 = (0.5 + g.random((B, H, dk, dv))).astype(np.float32)
+    eta0 = g.standard_normal((B, H, dk, dv)).astype(np.float32)
+    for tdt in (torch.float32, torch.bfloat16):
+        e = lambda *s: torch.empty(s, dtype=tdt, device=DEV)
+        log(f"pc edge T=0 {tdt}")
+        out = kla.kla_forward_pc(e(B, 0, H, dk), e(B, 0, H, dk), e(B, 0, H, dv), e(B, 0, H, dk), e(B, 0, H, dk),
+                                 e(B, 0, H, dv), _f32(lam0), _f32(eta0))
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(to_np(out["lamT"]), lam0)
+        np.testing.assert_array_equal(to_np(out["etaT"]), eta0)
+
+
+def test_pc_decode_steps_equal_forward(kla):
+    S, H, dk, dv, steps = 6, 2, 64, 32, 5
+    case = _case(S, steps, H, dk, dv, "f32", seed=23, dist="lm")
+    g = np.random.default_rng(2)
+    lam = (0.5 + g.random((S, H, dk, dv))).astype(np.float32).astype(np.float64)
+    eta = g.standard_normal((S, H, dk, dv)).astype(np.float32).astype(np.float64)
+    lam_d, eta_d = _f32(lam), _f32(eta)
+    rep = []
+    for t in range(steps):
+        x = {n: to_torch(np.ascontiguousarray(case[n][:, t]), "f32", DEV) for n in NAMES}
+        log(f"pc decode step {t}")
+        out = kla.kla_decode_step_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], lam_d, eta_d, want_var=True)
+        torch.cuda.synchronize()
+        ref = oracle.decode_step(case["q"][:, t], case["k"][:, t], case["v"][:, t], case["a"][:, t],
+                                 case["p"][:, t], case["rc"][:, t], lam, eta)
+        lam, eta = ref["lam"], ref["eta"]
+        for n, got, want in (("y", out["y"], ref["y"]), ("yvar", out["yvar"], ref["yvar"]),
+                             ("lam", lam_d, lam), ("eta", eta_d, eta)):
+            _check(f"{n}{t}", to_np(got), want, TOL["f32"], rep)
+    log("  pc decode: " + " ".join(rep))
+
+
+def test_pc_check_mode_rejects_bad_channel_precision(kla, monkeypatch):
+    monkeypatch.setenv("KLA_CHECK", "1")
+    B, T, H, dk, dv = 1, 20, 2, 32, 64
+    case = _case(B, T, H, dk, dv, "f32", seed=4, dist="lm")
+    x = {n: to_torch(case[n], "f32", DEV) for n in NAMES}
+    kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"])   # in the domain
+    bad = x["rc"].clone()
+    bad[0, T - 1, H - 1, dv - 1] = -1.0   # the last element: the check must cover every channel
+    log("pc check mode: r < 0 in the last channel")
+    with pytest.raises(kla.KLAError, match="NUMERIC"):
+        kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], bad)
+
+
+def test_pc_lm_layer_full_size(kla):
+    """B8 T2048 H16 d128 bf16 with r per value channel, sampled sequences."""
+    w = K.WORKLOADS[2]
+    log(f"pc lm layer B{w.B} T{w.T} H{w.H} d{w.dk}: generating inputs")
+    bits = K.full(w, names=NAMES, as_bits=True)
+    x = {n: bits_to_torch(bits[n], DEV) for n in bits}
+    del bits
+    log("pc lm layer: forward on GPU")
+    out = kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], want_var=True)
+    torch.cuda.synchronize()
+    pairs = [(0, 0), (w.B - 1, w.H - 1), (3, 9)]
+    log(f"pc lm layer: oracle on pairs {pairs}")
+    sl = K.pairs_slice(w, pairs, names=NAMES)
+    ref = oracle.forward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["rc"])
+    bi = [b for b, _ in pairs]
+    hi = [h for _, h in pairs]
+    tol = TOL[w.dtype]
+    rep = []
+    _check("y", to_np(out["y"][bi, :, hi]), K.quantise(ref["y"][:, :, 0], w.dtype), tol, rep)
+    _check("yvar", to_np(out["yvar"][bi, :, hi]), ref["yvar"][:, :, 0], tol, rep)
+    _check("lamT", to_np(out["lamT"][bi, hi]), ref["lamT"][:, 0], tol, rep)
+    _check("etaT", to_np(out["etaT"][bi, hi]), ref["etaT"][:, 0], tol, rep)
+    assert torch.all(out["lamT"] > 0) and torch.all(out["yvar"] > 0)
+    assert torch.isfinite(out["y"].float()).all()
+    log("  pc lm layer: " + " ".join(rep))
