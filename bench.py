@@ -18,10 +18,10 @@ With --ou the same shape runs with OU gates instead (kla_forward_ou /
 kla_backward_ou: time-invariant a, p, delta [H, dk] in place of the per-token
 abar and pbar tensors); its traffic summary is profiles/lm_layer_ou_traffic.md.
 
-With --pc it times the forward of the per-channel-precision variant
-(kla_forward_pc: r drawn per value channel, precision and gates per (key slot,
-value channel)), an elementwise scan bound by VALU issue; its roofline is the
-chip's fp32 VALU issue rate (see ALU_SLOTS_PER_ELEMENT).
+With --pc it times forward + backward of the per-channel-precision variant
+(kla_forward_pc / kla_backward_pc: r drawn per value channel, precision and
+gates per (key slot, value channel)), elementwise scans bound by VALU issue;
+their roofline is the chip's fp32 VALU issue rate (see ALU_SLOTS_*).
 """
 import argparse
 import json
@@ -46,6 +46,10 @@ VALU_LANE_OPS = 256 * 4 * 16 * 2.4e9
 # lam_t = num / den (2), 1/lam_t = den^2 R (2), the gate abar / den (1), k r v (1), eta_t (1),
 # eta_t / lam_t (1) and the two readout sums (2)
 ALU_SLOTS_PER_ELEMENT = 18
+# backward, per element and token: the recomputed update (13 slots: the forward's without the
+# readouts) and the adjoint step as written in pc.hip with the same sharing (38 slots, one
+# quarter-rate reciprocal of lam_t den among them)
+ALU_SLOTS_BWD_PER_ELEMENT = 51
 
 
 def algorithmic_bytes(w, s, ou=False):
@@ -60,19 +64,22 @@ def algorithmic_bytes(w, s, ou=False):
 
 
 def cpu_baseline_pc(w):
-    """fp64 oracle forward of the per-channel workload on a few sampled sequences."""
+    """fp64 oracle forward + backward of the per-channel workload on a few sampled sequences."""
     import kla_inputs as K
     import oracle
     threads = oracle.default_threads()
     pairs = [(b, h) for b in range(w.B) for h in range(w.H)]
     np.random.default_rng(0).shuffle(pairs)
-    sample = sorted(pairs[:max(1, min(8 * threads, len(pairs)))])
-    sl = K.pairs_slice(w, sample, names=("q", "k", "v", "a", "p", "rc"))
+    sample = sorted(pairs[:max(1, min(2 * threads, len(pairs)))])
+    sl = K.pairs_slice(w, sample, names=("q", "k", "v", "a", "p", "rc", "dy"))
     t0 = time.perf_counter()
     oracle.forward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["rc"], nthreads=threads)
     t1 = time.perf_counter()
-    return {"value": len(sample) * w.T / (t1 - t0), "unit": "tokens/s", "cores": min(threads, len(sample)),
-            "kind": "oracle", "sample": f"{len(sample)} (batch, head) sequences of T={w.T}, forward ({t1 - t0:.1f}s)"}
+    oracle.backward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["rc"], None, None, sl["dy"], nthreads=threads)
+    t2 = time.perf_counter()
+    return {"value": len(sample) * w.T / (t2 - t0), "unit": "tokens/s", "cores": min(threads, len(sample)),
+            "kind": "oracle",
+            "sample": f"{len(sample)} (batch, head) sequences of T={w.T} (fwd {t1 - t0:.1f}s + bwd {t2 - t1:.1f}s)"}
 
 
 def bench_pc(args, w, dev):
@@ -80,7 +87,7 @@ def bench_pc(args, w, dev):
     import torch
     import kla_inputs as K
     import paper_2602_10743_amd as kla
-    names = ("q", "k", "v", "a", "p", "rc")
+    names = ("q", "k", "v", "a", "p", "rc", "dy")
     bits = K.full(w, names=names, as_bits=True)
     x = {n: torch.from_numpy(np.ascontiguousarray(bits[n].view(np.int16))).view(torch.bfloat16).to(dev)
          for n in bits}
@@ -88,37 +95,45 @@ def bench_pc(args, w, dev):
     stream = torch.cuda.current_stream(dev)
     y = torch.empty_like(x["v"])
 
-    def step():
-        kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], want_state=False, y=y)
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        out = kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], want_state=False, save=True, y=y)
+        if ev is not None:
+            ev[1].record(stream)
+        kla.kla_backward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], None, None, x["dy"],
+                            saved=out["saved"], want_init_grads=False)
+        if ev is not None:
+            ev[2].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     t0 = time.perf_counter()
-    ev[0].record(stream)
-    for _ in range(args.steps):
-        step()
-    ev[1].record(stream)
+    for i in range(args.steps):
+        step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
-    ms = ev[0].elapsed_time(ev[1]) / args.steps
+    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     th = w.token_heads
     elements = th * w.dk * w.dv
-    achieved = elements * ALU_SLOTS_PER_ELEMENT / (ms * 1e-3)
+    achieved = elements * ALU_SLOTS_BWD_PER_ELEMENT / (bwd_ms * 1e-3)
     res = {
         "metric": METRIC, "value": th / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": w.name + "_pc", "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv,
-                   "pass": "fwd", "precision": "per value channel (bf16 inputs, fp32 scan)",
+                   "pass": "fwd+bwd", "precision": "per value channel (bf16 inputs, fp32 scan)",
                    "tokens_counted": "B*T*H"},
-        "roofline": {"bound": "alu", "kernel": "kla_forward_pc", "achieved": achieved / 1e12,
+        "roofline": {"bound": "alu", "kernel": "kla_backward_pc", "achieved": achieved / 1e12,
                      "peak": VALU_LANE_OPS / 1e12, "unit": "T lane-ops/s",
                      "frac": achieved / VALU_LANE_OPS, "traffic": None,
-                     "element_updates_per_call": elements, "slots_per_element": ALU_SLOTS_PER_ELEMENT,
-                     "fwd_ms": ms},
+                     "element_updates_per_call": elements, "slots_per_element": ALU_SLOTS_BWD_PER_ELEMENT,
+                     "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
+                     "fwd_frac": elements * ALU_SLOTS_PER_ELEMENT / (fwd_ms * 1e-3) / VALU_LANE_OPS},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline_pc(w)

@@ -203,17 +203,33 @@ kla_status kla_decode_step_ou(int32_t S, int32_t H, int32_t dk, int32_t dv, int3
  *   y_t[d]     = sum_n q_t[n] H_t[n,d] / lam_t[n,d]
  *   yvar_t[d]  = sum_n q_t[n]^2 / lam_t[n,d]
  *
- * Shapes differ from the entry points above only in: r [B, T, H, dv] (decode:
- * [S, H, dv]) in dtype; lam0, lamT, decode lam [.., H, dk, dv] fp32; yvar
- * [B, T, H, dv] fp32 (decode: [S, H, dv]).  Workspace: kla_forward_workspace.
+ * Shapes differ from the entry points above only in: r, dr, dyvar [B, T, H, dv]
+ * (decode: r [S, H, dv]) in dtype (dyvar fp32); lam0, lamT, dlamT, dlam0 and
+ * decode lam [.., H, dk, dv] fp32; yvar [B, T, H, dv] fp32 (decode: [S, H, dv]).
+ * The saved context holds the belief every 8 tokens (kla_saved_pc_bytes);
+ * forward workspace: kla_forward_workspace, backward: kla_backward_pc_workspace.
  * Every other convention is as above.
  */
+size_t kla_saved_pc_bytes(const kla_desc* desc);
+size_t kla_backward_pc_workspace(const kla_desc* desc, int with_saved);
+
 kla_status kla_forward_pc(const kla_desc* desc,
                           const void* q, const void* k, const void* v,
                           const void* abar, const void* pbar, const void* r,
                           const float* lam0, const float* eta0,
                           void* y, float* yvar, float* lamT, float* etaT,
-                          void* ws, size_t ws_bytes, hipStream_t stream);
+                          void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Exact gradient of kla_forward_pc's y, yvar, lamT and etaT (arguments as in
+ * kla_backward, with the per-channel shapes above). */
+kla_status kla_backward_pc(const kla_desc* desc,
+                           const void* q, const void* k, const void* v,
+                           const void* abar, const void* pbar, const void* r,
+                           const float* lam0, const float* eta0, const void* saved,
+                           const void* dy, const float* dyvar, const float* dlamT, const float* detaT,
+                           void* dq, void* dk, void* dv, void* dabar, void* dpbar, void* dr,
+                           float* dlam0, float* deta0,
+                           void* ws, size_t ws_bytes, hipStream_t stream);
 
 kla_status kla_decode_step_pc(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype,
                               const void* q, const void* k, const void* v,

@@ -20,7 +20,7 @@ import torch
 __all__ = ["kla_forward", "kla_backward", "kla_decode_step", "kla_status_string",
            "kla_forward_workspace", "kla_backward_workspace", "kla_saved_bytes",
            "kla_forward_ou", "kla_backward_ou", "kla_decode_step_ou", "kla_backward_ou_workspace",
-           "kla_forward_pc", "kla_decode_step_pc",
+           "kla_forward_pc", "kla_backward_pc", "kla_decode_step_pc",
            "KLAError", "KLAFilter", "kla_filter", "KLAFilterOU", "kla_filter_ou", "library_path"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -74,8 +74,14 @@ def _load():
     lib.kla_backward_ou.restype = ctypes.c_int
     lib.kla_decode_step_ou.argtypes = [ctypes.c_int32] * 5 + [_VP] * 12
     lib.kla_decode_step_ou.restype = ctypes.c_int
-    lib.kla_forward_pc.argtypes = [D] + [_VP] * 13 + [ctypes.c_size_t, _VP]
+    lib.kla_forward_pc.argtypes = [D] + [_VP] * 14 + [ctypes.c_size_t, _VP]
     lib.kla_forward_pc.restype = ctypes.c_int
+    lib.kla_backward_pc.argtypes = [D] + [_VP] * 22 + [ctypes.c_size_t, _VP]
+    lib.kla_backward_pc.restype = ctypes.c_int
+    lib.kla_saved_pc_bytes.argtypes = [D]
+    lib.kla_saved_pc_bytes.restype = ctypes.c_size_t
+    lib.kla_backward_pc_workspace.argtypes = [D, ctypes.c_int]
+    lib.kla_backward_pc_workspace.restype = ctypes.c_size_t
     lib.kla_decode_step_pc.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
     lib.kla_decode_step_pc.restype = ctypes.c_int
     lib.kla_status_string.argtypes = [ctypes.c_int]
@@ -421,13 +427,7 @@ def kla_filter_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, *, want_var: bo
 
 # ---- per-channel precision: r [B, T, H, dv], beliefs [B, H, dk, dv]
 
-def kla_forward_pc(q, k, v, a, p, r, lam0=None, eta0=None, *, want_var: bool = False,
-                   want_state: bool = True, y=None) -> dict:
-    """Filter with one observation precision per value channel: q, k, a, p
-    [B, T, H, dk]; v, r [B, T, H, dv] (one dtype); lam0, eta0 [B, H, dk, dv] fp32
-    or None.  Returns y and, as asked, yvar [B, T, H, dv] and lamT, etaT
-    [B, H, dk, dv]."""
-    lib = _load()
+def _check_pc(q, k, v, a, p, r):
     if not q.is_cuda:
         raise ValueError("KLA tensors must live on a GPU; the layer has no CPU path")
     if q.dtype not in _DTYPES or q.dim() != 4:
@@ -438,6 +438,18 @@ def kla_forward_pc(q, k, v, a, p, r, lam0=None, eta0=None, *, want_var: bool = F
                            ("v", v, (B, T, H, dv)), ("r", r, (B, T, H, dv))):
         if tuple(t.shape) != shape or t.dtype != q.dtype or t.device != q.device or not t.is_contiguous():
             raise ValueError(f"{name} must be a contiguous {shape} tensor in q's dtype")
+
+
+def kla_forward_pc(q, k, v, a, p, r, lam0=None, eta0=None, *, want_var: bool = False,
+                   want_state: bool = True, save: bool = False, y=None) -> dict:
+    """Filter with one observation precision per value channel: q, k, a, p
+    [B, T, H, dk]; v, r [B, T, H, dv] (one dtype); lam0, eta0 [B, H, dk, dv] fp32
+    or None.  Returns y and, as asked, yvar [B, T, H, dv], lamT, etaT
+    [B, H, dk, dv] and the saved context (belief checkpoints) for kla_backward_pc."""
+    lib = _load()
+    _check_pc(q, k, v, a, p, r)
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
     dev = q.device
     lam0 = _f32(lam0, (B, H, dk, dv), dev, "lam0")
     eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
@@ -447,13 +459,51 @@ def kla_forward_pc(q, k, v, a, p, r, lam0=None, eta0=None, *, want_var: bool = F
     yvar = torch.empty((B, T, H, dv), dtype=torch.float32, device=dev) if want_var else None
     lamT = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_state else None
     etaT = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_state else None
+    nsaved = int(lib.kla_saved_pc_bytes(ctypes.byref(desc))) if save else 0
+    saved = torch.empty(max(nsaved, 1), dtype=torch.uint8, device=dev) if save else None
     nws = kla_forward_workspace(desc)
     ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
     st = lib.kla_forward_pc(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(r), _p(lam0), _p(eta0),
-                            _p(y), _p(yvar), _p(lamT), _p(etaT), _p(ws), nws, _stream(dev))
+                            _p(y), _p(yvar), _p(lamT), _p(etaT), _p(saved if nsaved else None), _p(ws), nws,
+                            _stream(dev))
     if st != 0:
         raise KLAError(st, "kla_forward_pc")
-    return {"y": y, "yvar": yvar, "lamT": lamT, "etaT": etaT}
+    return {"y": y, "yvar": yvar, "lamT": lamT, "etaT": etaT, "saved": saved if nsaved else None}
+
+
+def kla_backward_pc(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None, *, saved=None,
+                    want_init_grads: bool = True, dyvar=None) -> dict:
+    """Gradients of kla_forward_pc's (y, yvar, lamT, etaT): dq, dk, da, dp
+    [B, T, H, dk] and dv, dr [B, T, H, dv] in the input dtype; dlam0, deta0
+    [B, H, dk, dv] fp32 when asked.  dyvar [B, T, H, dv], dlamT, detaT
+    [B, H, dk, dv] fp32 or None."""
+    lib = _load()
+    _check_pc(q, k, v, a, p, r)
+    dev = q.device
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    lam0 = _f32(lam0, (B, H, dk, dv), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    dlamT = _f32(dlamT, (B, H, dk, dv), dev, "dlamT")
+    detaT = _f32(detaT, (B, H, dk, dv), dev, "detaT")
+    dyvar = _f32(dyvar, (B, T, H, dv), dev, "dyvar")
+    if tuple(dy.shape) != (B, T, H, dv) or dy.dtype != q.dtype or not dy.is_contiguous():
+        raise ValueError("dy must be a contiguous [B, T, H, dv] tensor in the input dtype")
+    desc = _desc(q, v)
+    out = {n: torch.empty_like(x) for n, x in (("dq", q), ("dk", k), ("dv", v), ("da", a), ("dp", p), ("dr", r))}
+    dlam0 = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_init_grads else None
+    deta0 = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_init_grads else None
+    nws = int(lib.kla_backward_pc_workspace(ctypes.byref(desc), int(saved is not None)))
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    st = lib.kla_backward_pc(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(r), _p(lam0), _p(eta0),
+                             _p(saved), _p(dy), _p(dyvar), _p(dlamT), _p(detaT), _p(out["dq"]), _p(out["dk"]),
+                             _p(out["dv"]), _p(out["da"]), _p(out["dp"]), _p(out["dr"]), _p(dlam0), _p(deta0),
+                             _p(ws), nws, _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_backward_pc")
+    out["dlam0"] = dlam0
+    out["deta0"] = deta0
+    return out
 
 
 def kla_decode_step_pc(q, k, v, a, p, r, lam, eta, *, want_var: bool = False, y=None) -> dict:

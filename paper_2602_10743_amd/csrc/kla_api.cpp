@@ -241,14 +241,31 @@ kla_status kla_backward_ou(const kla_desc* desc, const void* q, const void* k, c
     return backward_impl(desc, g, true, saved, da, dp, ddelta, ws, ws_bytes, stream);
 }
 
+size_t kla_saved_pc_bytes(const kla_desc* desc) {
+    if (check_desc(desc) != KLA_OK) return 0;
+    return kla::pc_saved_bytes(shape_of(desc));
+}
+
+size_t kla_backward_pc_workspace(const kla_desc* desc, int with_saved) {
+    if (check_desc(desc) != KLA_OK) return 0;
+    const kla::Shape s = shape_of(desc);
+    size_t bytes = kAlign + round_up(kla::pc_bwd_workspace(s));
+    if (!with_saved) {  // the checkpoints are recomputed: saved context plus a scratch output
+        const size_t elt = s.bf16 ? 2 : 4;
+        bytes += round_up(kla::pc_saved_bytes(s)) + round_up((size_t)s.B * s.T * s.H * s.dv * elt);
+    }
+    return bytes;
+}
+
 kla_status kla_forward_pc(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
                           const void* pbar, const void* r, const float* lam0, const float* eta0, void* y,
-                          float* yvar, float* lamT, float* etaT, void* ws, size_t ws_bytes, hipStream_t stream) {
+                          float* yvar, float* lamT, float* etaT, void* saved, void* ws, size_t ws_bytes,
+                          hipStream_t stream) {
     kla_status st = check_desc(desc);
     if (st != KLA_OK) return st;
     if (desc->T > 0 && (!q || !k || !v || !abar || !pbar || !r || !y)) return KLA_ERR_NULL;
     if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, y, (void*)yvar, (void*)lamT,
-                     (void*)etaT, ws))
+                     (void*)etaT, saved, ws))
         return KLA_ERR_ALIGN;
     if (!ws || ws_bytes < kla_forward_workspace(desc)) return KLA_ERR_WORKSPACE;
     const kla::Shape s = shape_of(desc);
@@ -257,7 +274,43 @@ kla_status kla_forward_pc(const kla_desc* desc, const void* q, const void* k, co
         if (st != KLA_OK) return st;
     }
     const kla::FwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, y, yvar, lamT, etaT};
-    return kla::launch_forward_pc(s, a, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+    return kla::launch_forward_pc(s, a, static_cast<float*>(saved), stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+kla_status kla_backward_pc(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
+                           const void* pbar, const void* r, const float* lam0, const float* eta0, const void* saved,
+                           const void* dy, const float* dyvar, const float* dlamT, const float* detaT, void* dq,
+                           void* dk, void* dv, void* dabar, void* dpbar, void* dr, float* dlam0, float* deta0,
+                           void* ws, size_t ws_bytes, hipStream_t stream) {
+    kla_status st = check_desc(desc);
+    if (st != KLA_OK) return st;
+    if (desc->T > 0 && (!q || !k || !v || !abar || !pbar || !r || !dy || !dq || !dk || !dv || !dabar || !dpbar ||
+                        !dr))
+        return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, abar, pbar, r, (const void*)lam0, (const void*)eta0, saved, dy, (const void*)dyvar,
+                     (const void*)dlamT, (const void*)detaT, dq, dk, dv, dabar, dpbar, dr, (void*)dlam0,
+                     (void*)deta0, ws))
+        return KLA_ERR_ALIGN;
+    if (!ws || ws_bytes < kla_backward_pc_workspace(desc, saved != nullptr)) return KLA_ERR_WORKSPACE;
+    const kla::Shape s = shape_of(desc);
+    if (check_mode()) {
+        st = validate(s, s.T, q, k, v, abar, pbar, r, lam0, eta0, ws, stream, nullptr, nullptr, nullptr, true);
+        if (st != KLA_OK) return st;
+    }
+    char* work = static_cast<char*>(ws) + kAlign;
+    float* kpart = reinterpret_cast<float*>(work);
+    if (!saved) {
+        char* ctx = work + round_up(kla::pc_bwd_workspace(s));
+        void* yscratch = ctx + round_up(kla::pc_saved_bytes(s));
+        const kla::FwdArgs f{q, k, v, abar, pbar, r, lam0, eta0, yscratch, nullptr, nullptr, nullptr};
+        if (kla::launch_forward_pc(s, f, reinterpret_cast<float*>(ctx), stream) != hipSuccess) return KLA_ERR_HIP;
+        saved = ctx;
+    }
+    kla::BwdArgs a{q,  k,  v,  abar,  pbar,  r,  lam0, eta0,  dy, dlamT,
+                   detaT, dq, dk, dv, dabar, dpbar, dr, dlam0, deta0};
+    a.dyvar = dyvar;
+    return kla::launch_backward_pc(s, a, static_cast<const float*>(saved), kpart, stream) == hipSuccess ? KLA_OK
+                                                                                                      : KLA_ERR_HIP;
 }
 
 kla_status kla_decode_step_pc(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,

@@ -64,7 +64,11 @@ int chunked_ou_parts(const Shape& s);
 int recurrent_ou_parts(const Shape& s);
 
 // Per-channel precision (r [B, T, H, dv], beliefs [B, H, dk, dv]): elementwise scan and decode.
-hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, hipStream_t st);
+// ck: NULL or pc_saved_bytes of belief checkpoints for launch_backward_pc; kpart: pc_bwd_workspace bytes
+hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, float* ck, hipStream_t st);
+size_t pc_saved_bytes(const Shape& s);
+size_t pc_bwd_workspace(const Shape& s);
+hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const float* ck, float* kpart, hipStream_t st);
 hipError_t launch_decode_pc(const Shape& s, const DecodeArgs& a, hipStream_t st);
 
 // OU gates: gradients of the parameters from the per-part gate-gradient sums

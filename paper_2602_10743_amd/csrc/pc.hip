@@ -14,6 +14,24 @@
 // Per element and token one reciprocal serves both quotients: with
 // den = abar^2 + pbar lam and num = lam + k^2 r den (so lam_t = num / den),
 //   R = 1 / (den num),  1 / den = num R,  1 / lam_t = den^2 R.
+//
+// Backward: the exact reverse-mode derivative of each element's recursion (the
+// per-element form of the adjoint in the oracle), with lam and H of every
+// token recomputed in registers from checkpoints the forward stores every
+// kCK tokens.  Per element and token, with ge, gl the adjoints of H_t and lam_t
+// (gy = dy_t[d], gv = dyvar_t[d], mu = H_t / lam_t):
+//   dq[n] += mu gy + 2 q gv / lam_t
+//   ge    += q gy / lam_t,   gl -= (q gy mu + q^2 gv / lam_t) / lam_t
+//   rho = 1 / (abar^2 + pbar lam_{t-1}),  f = abar rho,  df = ge H_{t-1}
+//   dk[n] += ge r v + 2 gl k r,  dr[d] += ge k v + gl k^2,  dv[d] += ge k r
+//   drho = df abar + gl lam_{t-1},  dden = -drho rho^2
+//   dabar[n] += df rho + 2 abar dden,  dpbar[n] += dden lam_{t-1}
+//   ge <- f ge,  gl <- gl rho + pbar dden
+// and after the first token dlam0 = gl, deta0 = ge.  The sums over n (dv, dr)
+// are completed inside the workgroup, which holds every key slot of its
+// channels; the sums over d (dq, dk, dabar, dpbar) inside the workgroup over
+// its channels, then across the channel tiles by pc_key_combine_kernel, in a
+// fixed order (the results are bitwise reproducible).
 #include "kla_buf.hpp"
 #include "kla_device.hpp"
 #include "kla_internal.hpp"
@@ -23,6 +41,7 @@ namespace {
 
 constexpr int kNG = 8;    // lanes sharing one value channel, each with every 8th key slot
 constexpr int kTB = 16;   // tokens per staged block
+constexpr int kCK = 8;    // tokens between checkpoints of the belief (saved context)
 
 __device__ __forceinline__ float sum8(float x) {   // over the 8 lanes of a channel
     x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
@@ -37,7 +56,7 @@ __device__ __forceinline__ float sum8(float x) {   // over the 8 lanes of a chan
 // (r, v as [t][c]) are staged in LDS, the elements are updated, the partial
 // readouts summed over the 8 lanes of a channel and y, yvar written from LDS.
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s, FwdArgs g) {
+__global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s, FwdArgs g, float* ck) {
     using T_ = typename storage<S>::type;
     constexpr int CT = DV < 32 ? DV : 32;
     constexpr int NTHR = kNG * CT;
@@ -61,6 +80,10 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
         lam[i] = g.lam0 ? g.lam0[o] : 1.f;
         eta[i] = g.eta0 ? g.eta0[o] : 0.f;
     }
+    // checkpoints: the belief before tokens 0, kCK, 2 kCK, ... as lam [BH][nseg][DK][DV] then eta
+    const int nseg = (s.T + kCK - 1) / kCK;
+    float* ck_lam = ck;
+    float* ck_eta = ck ? ck + (size_t)s.B * s.H * nseg * DK * DV : nullptr;
     for (int t0 = 0; t0 < s.T; t0 += kTB) {
         const int nt = min(kTB, s.T - t0);
         for (int idx = tid; idx < nt * DK; idx += NTHR) {
@@ -75,6 +98,14 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
         }
         __syncthreads();
         for (int t = 0; t < nt; ++t) {
+            if (ck && (t0 + t) % kCK == 0) {
+#pragma unroll
+                for (int i = 0; i < NPER; ++i) {
+                    const size_t o = (((size_t)bh * nseg + (t0 + t) / kCK) * DK + ng + kNG * i) * DV + d;
+                    ck_lam[o] = lam[i];
+                    ck_eta[o] = eta[i];
+                }
+            }
             const float2 rv = s_v[t][c];
             const float krv_s = rv.x * rv.y;   // r v: the evidence k r v over k
             float ya = 0.f, wa = 0.f;
@@ -211,10 +242,219 @@ hipError_t dispatch_pc(const Shape& s, A&&... args) {
 
 template <typename S, int DK, int DV>
 struct FwdPc {
-    static hipError_t run(const Shape& s, const FwdArgs& a, hipStream_t st) {
+    static hipError_t run(const Shape& s, const FwdArgs& a, float* ck, hipStream_t st) {
         constexpr int CT = DV < 32 ? DV : 32;
         hipLaunchKernelGGL((fwd_pc_kernel<S, DK, DV>), dim3((unsigned)(s.B * s.H * (DV / CT))), dim3(kNG * CT), 0,
-                           st, s, a);
+                           st, s, a, ck);
+        return hipGetLastError();
+    }
+};
+
+// ----------------------------------------------------------------------------
+// Backward.  One workgroup per (b, h, CB value channels: 32, 16 at dk = 128); LPC lanes per channel
+// (32, or 16 at dk = 16), lane l owning key slots l % LPC + LPC i of channel
+// l / LPC.  Segments of kCK tokens are taken last to first: stage the segment's
+// inputs, recompute lam and H of its tokens from the checkpoint into registers,
+// then walk its tokens in reverse.  Per token the channel sums (dv, dr) are
+// completed by DPP over the LPC lanes of a channel; the key-slot sums (dq, dk,
+// dabar, dpbar) are added over the channels of a wave by lane shuffles and over
+// the waves through a double-buffered LDS slot, and stored as this tile's part.
+// At dk = 128 a lane's 4 elements keep 72 trajectory values in registers, so the
+// workgroup takes 16 channels (2 waves per SIMD, room for them) instead of 32.
+template <int DK, int DV>
+struct PcLanes {
+    static constexpr int LPC = DK < 32 ? DK : 32;
+    static constexpr int NPER = DK / LPC;
+    static constexpr int CBMAX = DK == 128 ? 16 : 32;
+    static constexpr int CB = DV < CBMAX ? DV : CBMAX;
+    static constexpr int NTHR = LPC * CB;
+};
+
+template <typename S, int DK, int DV>
+__global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s, BwdArgs g, const float* ck,
+                                                                        float* kpart) {
+    using T_ = typename storage<S>::type;
+    constexpr int LPC = PcLanes<DK, DV>::LPC, NPER = PcLanes<DK, DV>::NPER;
+    constexpr int CB = PcLanes<DK, DV>::CB;
+    constexpr int NTHR = LPC * CB, NW = NTHR / 64;
+    static_assert(NTHR % 64 == 0 && (LPC == 16 || LPC == 32), "lane layout");
+    __shared__ float4 s_k[kCK][DK];        // abar, pbar, k, q
+    __shared__ float4 s_c[kCK][CB];        // r, v, dy, dyvar
+    __shared__ float2 s_o[kCK][CB];        // dv, dr
+    __shared__ float s_red[2][NW][4][DK];  // per-wave key-slot sums of dq, dk, dabar, dpbar
+
+    const T_ *q = static_cast<const T_*>(g.q), *k = static_cast<const T_*>(g.k), *v = static_cast<const T_*>(g.v);
+    const T_ *a = static_cast<const T_*>(g.a), *p = static_cast<const T_*>(g.p), *r = static_cast<const T_*>(g.r);
+    const T_* dy = static_cast<const T_*>(g.dy);
+    T_* dv_out = static_cast<T_*>(g.dv);
+    T_* dr_out = static_cast<T_*>(g.dr);
+    const int ntile = DV / CB;
+    const int bh = blockIdx.x / ntile, tile = blockIdx.x % ntile, d0 = tile * CB;
+    const int b = bh / s.H, h = bh % s.H;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int ln = tid % LPC, c = tid / LPC, d = d0 + c;
+    const int T = s.T, nseg = (T + kCK - 1) / kCK;
+    const size_t nck = (size_t)s.B * s.H * nseg * DK * DV;
+    const size_t nkey = (size_t)s.B * T * s.H * DK;
+
+    float ge[NPER], gl[NPER];
+#pragma unroll
+    for (int i = 0; i < NPER; ++i) {
+        const size_t o = ((size_t)bh * DK + ln + LPC * i) * DV + d;
+        ge[i] = g.detaT ? g.detaT[o] : 0.f;
+        gl[i] = g.dlamT ? g.dlamT[o] : 0.f;
+    }
+    for (int sg = nseg - 1; sg >= 0; --sg) {
+        const int t0 = sg * kCK, nt = min(kCK, T - t0);
+        __syncthreads();   // the previous segment's staging and outputs are no longer read
+        for (int idx = tid; idx < nt * DK; idx += NTHR) {
+            const int t = idx / DK, n = idx % DK;
+            const size_t o = (((size_t)b * T + t0 + t) * s.H + h) * DK + n;
+            s_k[t][n] = make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
+        }
+        for (int idx = tid; idx < nt * CB; idx += NTHR) {
+            const int t = idx / CB, cc = idx % CB;
+            const size_t tok = ((size_t)b * T + t0 + t) * s.H + h;
+            const size_t o = tok * DV + d0 + cc;
+            s_c[t][cc] = make_float4(ld(r, o), ld(v, o), ld(dy, o), g.dyvar ? g.dyvar[o] : 0.f);
+        }
+        // lam and H before each token of the segment and after its last
+        float lt[kCK + 1][NPER], et[kCK + 1][NPER];
+#pragma unroll
+        for (int i = 0; i < NPER; ++i) {
+            const size_t o = (((size_t)bh * nseg + sg) * DK + ln + LPC * i) * DV + d;
+            lt[0][i] = ck[o];
+            et[0][i] = ck[nck + o];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kCK; ++j) {
+            const bool ok = j < nt;
+            const float4 cv = s_c[ok ? j : 0][c];
+            const float krv = cv.x * cv.y;
+#pragma unroll
+            for (int i = 0; i < NPER; ++i) {
+                const float4 in = s_k[ok ? j : 0][ln + LPC * i];
+                const float den = fmaf(in.y, lt[j][i], in.x * in.x);
+                const float num = fmaf(in.z * in.z * cv.x, den, lt[j][i]);
+                const float R = __builtin_amdgcn_rcpf(den * num);
+                const float iden = num * R;
+                lt[j + 1][i] = ok ? num * iden : lt[j][i];
+                et[j + 1][i] = ok ? fmaf(in.x * iden, et[j][i], in.z * krv) : et[j][i];
+            }
+        }
+        // reverse over the segment's tokens
+#pragma unroll
+        for (int j = kCK - 1; j >= 0; --j) {
+            if (j >= nt) continue;   // uniform: the tail of the last segment
+            const float4 cv = s_c[j][c];   // r, v, gy, gv
+            float kq[4][NPER];             // this lane's dq, dk, dabar, dpbar of token j
+            float cdv = 0.f, cdr = 0.f;
+#pragma unroll
+            for (int i = 0; i < NPER; ++i) {
+                const float4 in = s_k[j][ln + LPC * i];   // abar, pbar, k, q
+                const float av = in.x, pv = in.y, kv = in.z, qv = in.w;
+                const float lp = lt[j][i], lc = lt[j + 1][i], ep = et[j][i], ec = et[j + 1][i];
+                const float den = fmaf(pv, lp, av * av);
+                const float R = __builtin_amdgcn_rcpf(lc * den);
+                const float ilc = den * R, rho = lc * R;
+                const float mu = ec * ilc;
+                const float qgy = qv * cv.z;
+                kq[0][i] = fmaf(mu, cv.z, 2.f * qv * cv.w * ilc);
+                float gei = fmaf(qgy, ilc, ge[i]);
+                float gli = gl[i] - fmaf(qgy, mu, qv * qv * cv.w * ilc) * ilc;
+                const float df = gei * ep;
+                const float kr = kv * cv.x;
+                kq[1][i] = fmaf(gei, cv.x * cv.y, 2.f * gli * kr);
+                cdr = fmaf(gei, kv * cv.y, fmaf(gli, kv * kv, cdr));
+                cdv = fmaf(gei, kr, cdv);
+                const float drho = fmaf(df, av, gli * lp);
+                const float dden = -drho * rho * rho;
+                kq[2][i] = fmaf(df, rho, 2.f * av * dden);
+                kq[3][i] = dden * lp;
+                ge[i] = av * rho * gei;
+                gl[i] = fmaf(gli, rho, pv * dden);
+            }
+            // channel sums over the LPC lanes of the channel
+            if constexpr (LPC == 32) {
+                cdv = half_sum(cdv);
+                cdr = half_sum(cdr);
+            } else {
+                cdv += dpp<0xB1, 0xf>(cdv);
+                cdv += dpp<0x4E, 0xf>(cdv);
+                cdv += dpp<0x141, 0xf>(cdv);
+                cdv += dpp<0x140, 0xf>(cdv);
+                cdr += dpp<0xB1, 0xf>(cdr);
+                cdr += dpp<0x4E, 0xf>(cdr);
+                cdr += dpp<0x141, 0xf>(cdr);
+                cdr += dpp<0x140, 0xf>(cdr);
+            }
+            if (ln == LPC - 1) s_o[j][c] = make_float2(cdv, cdr);
+            // key-slot sums: over the channels of this wave, then through LDS over the waves
+            float* slot = &s_red[j & 1][wave][0][0];
+#pragma unroll
+            for (int qi = 0; qi < 4; ++qi)
+#pragma unroll
+                for (int i = 0; i < NPER; ++i) {
+                    float x = kq[qi][i];
+#pragma unroll
+                    for (int m = LPC; m < 64; m *= 2) x += __shfl_xor(x, m, 64);
+                    if (lane < LPC) slot[qi * DK + ln + LPC * i] = x;
+                }
+            __syncthreads();
+            const size_t tk = ((size_t)b * T + t0 + j) * s.H + h;
+            for (int idx = tid; idx < 4 * DK; idx += NTHR) {
+                float acc = 0.f;
+#pragma unroll
+                for (int w = 0; w < NW; ++w) acc += (&s_red[j & 1][w][0][0])[idx];
+                const int qi = idx / DK, n = idx % DK;
+                kpart[((size_t)tile * 4 + qi) * nkey + tk * DK + n] = acc;
+            }
+        }
+        __syncthreads();
+        for (int idx = tid; idx < nt * CB; idx += NTHR) {
+            const int t = idx / CB, cc = idx % CB;
+            const size_t o = (((size_t)b * T + t0 + t) * s.H + h) * DV + d0 + cc;
+            st(dv_out, o, s_o[t][cc].x);
+            st(dr_out, o, s_o[t][cc].y);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < NPER; ++i) {
+        const size_t o = ((size_t)bh * DK + ln + LPC * i) * DV + d;
+        if (g.dlam0) g.dlam0[o] = gl[i];
+        if (g.deta0) g.deta0[o] = ge[i];
+    }
+}
+
+// dq, dk, dabar, dpbar = sums of the channel tiles' parts, in the input dtype
+template <typename S>
+__global__ __launch_bounds__(256) void pc_key_combine_kernel(const float* __restrict__ kpart, int ntile, size_t n,
+                                                             BwdArgs g) {
+    using T_ = typename storage<S>::type;
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    T_* out[4] = {static_cast<T_*>(g.dq), static_cast<T_*>(g.dk), static_cast<T_*>(g.da), static_cast<T_*>(g.dp)};
+#pragma unroll
+    for (int qi = 0; qi < 4; ++qi) {
+        float acc = 0.f;
+        for (int t = 0; t < ntile; ++t) acc += kpart[((size_t)t * 4 + qi) * n + i];
+        st(out[qi], i, acc);
+    }
+}
+
+template <typename S, int DK, int DV>
+struct BwdPc {
+    static hipError_t run(const Shape& s, const BwdArgs& a, const float* ck, float* kpart, hipStream_t st) {
+        constexpr int CB = PcLanes<DK, DV>::CB;
+        constexpr int NTHR = PcLanes<DK, DV>::NTHR;
+        hipLaunchKernelGGL((bwd_pc_kernel<S, DK, DV>), dim3((unsigned)(s.B * s.H * (DV / CB))), dim3(NTHR), 0, st,
+                           s, a, ck, kpart);
+        hipError_t e = hipGetLastError();
+        const size_t n = (size_t)s.B * s.T * s.H * DK;
+        if (e != hipSuccess || n == 0) return e;
+        hipLaunchKernelGGL(pc_key_combine_kernel<S>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, kpart,
+                           DV / CB, n, a);
         return hipGetLastError();
     }
 };
@@ -229,7 +469,24 @@ struct DecPc {
 
 }  // namespace
 
-hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, hipStream_t st) { return dispatch_pc<FwdPc>(s, a, st); }
+hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, float* ck, hipStream_t st) {
+    return dispatch_pc<FwdPc>(s, a, ck, st);
+}
+
+size_t pc_saved_bytes(const Shape& s) {
+    const size_t nseg = (size_t)(s.T + kCK - 1) / kCK;
+    return 2 * (size_t)s.B * s.H * nseg * s.dk * s.dv * sizeof(float);
+}
+
+size_t pc_bwd_workspace(const Shape& s) {
+    const int cbmax = s.dk == 128 ? 16 : 32;
+    const int cb = s.dv < cbmax ? s.dv : cbmax;
+    return (size_t)(s.dv / cb) * 4 * s.B * s.T * s.H * s.dk * sizeof(float);
+}
+
+hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const float* ck, float* kpart, hipStream_t st) {
+    return dispatch_pc<BwdPc>(s, a, ck, kpart, st);
+}
 
 hipError_t launch_decode_pc(const Shape& s, const DecodeArgs& a, hipStream_t st) {
     return dispatch_pc<DecPc>(s, a, st);

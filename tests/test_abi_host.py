@@ -142,3 +142,29 @@ def test_ou_argument_errors(lib):
     bad = list(dec)
     bad[5] = None
     assert lib.kla_decode_step_ou(4, 2, 16, 16, 0, *bad) == 1
+
+
+def test_per_channel_entry_points(lib):
+    import paper_2602_10743_amd as K
+    names = _declared()
+    for n in ("kla_forward_pc", "kla_backward_pc", "kla_decode_step_pc", "kla_saved_pc_bytes",
+              "kla_backward_pc_workspace"):
+        assert n in names
+    d = _desc(B=2, T=20, H=3, dk=32, dv=16)
+    # the saved context holds lam and eta at every 8th token: 3 checkpoints of [B, H, dk, dv]
+    assert lib.kla_saved_pc_bytes(ctypes.byref(d)) == 2 * 2 * 3 * 3 * 32 * 16 * 4
+    assert lib.kla_backward_pc_workspace(ctypes.byref(d), 0) > lib.kla_backward_pc_workspace(ctypes.byref(d), 1)
+    fake = ctypes.c_void_p(0x10000)
+    # q k v a p r lam0 eta0 y yvar lamT etaT saved ws
+    fwd = [fake] * 6 + [None, None, fake, None, None, None, None, fake]
+    assert lib.kla_forward_pc(ctypes.byref(_desc(dk=24)), *fwd, 256, None) == 2
+    bad = list(fwd)
+    bad[5] = None                                                  # r
+    assert lib.kla_forward_pc(ctypes.byref(d), *bad, 256, None) == 1
+    assert lib.kla_forward_pc(ctypes.byref(d), *fwd, 0, None) == 5
+    # q k v a p r lam0 eta0 saved dy dyvar dlamT detaT dq dk dv da dp dr dlam0 deta0 ws
+    bwd = [fake] * 6 + [None, None, None] + [fake, None, None, None] + [fake] * 6 + [None, None] + [fake]
+    assert lib.kla_backward_pc(ctypes.byref(d), *bwd, 0, None) == 5
+    bad = list(bwd)
+    bad[18] = None                                                 # dr
+    assert lib.kla_backward_pc(ctypes.byref(d), *bad, 1 << 40, None) == 1

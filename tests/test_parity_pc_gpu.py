@@ -1,5 +1,5 @@
 """GPU parity of the per-channel-precision entry points (kla_forward_pc,
-kla_decode_step_pc) against the fp64 oracle, which runs every (n, d) filter
+kla_backward_pc, kla_decode_step_pc) against the fp64 oracle, which runs every (n, d) filter
 with its own precision (r [B, T, H, dv], beliefs [B, H, dk, dv]).
 
 Small shapes are compared over whole tensors; the language-model shape
@@ -81,6 +81,37 @@ def test_pc_forward_small(kla, B, T, H, dk, dv, dtype, dist, init):
     log("  " + " ".join(rep))
 
 
+@pytest.mark.parametrize("B,T,H,dk,dv,dtype,dist", PC_SMALL)
+def test_pc_backward_small(kla, B, T, H, dk, dv, dtype, dist):
+    case = _case(B, T, H, dk, dv, dtype, seed=T * 3 + dv, dist=dist)
+    g = np.random.default_rng(T + 11)
+    q32 = lambda x: x.astype(np.float32).astype(np.float64)
+    lam0 = q32(0.5 + g.random((B, H, dk, dv)))
+    eta0 = q32(g.standard_normal((B, H, dk, dv)))
+    dlamT = q32(g.standard_normal((B, H, dk, dv)))
+    detaT = q32(g.standard_normal((B, H, dk, dv)))
+    dyvar = q32(g.standard_normal((B, T, H, dv)))
+    dy = K.quantise(g.standard_normal((B, T, H, dv)), dtype)
+    log(f"pc backward B{B} T{T} H{H} dk{dk} dv{dv} {dtype}")
+    x = {n: to_torch(case[n], dtype, DEV) for n in NAMES}
+    dyt = to_torch(dy, dtype, DEV)
+    out = kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], _f32(lam0), _f32(eta0), save=True)
+    gr = kla.kla_backward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], _f32(lam0), _f32(eta0), dyt,
+                             _f32(dlamT), _f32(detaT), saved=out["saved"], dyvar=_f32(dyvar))
+    gr2 = kla.kla_backward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], _f32(lam0), _f32(eta0), dyt,
+                              _f32(dlamT), _f32(detaT), dyvar=_f32(dyvar))
+    torch.cuda.synchronize()
+    ref = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["rc"], lam0, eta0, dy,
+                          dlamT, detaT, dyvar=dyvar)
+    tol = TOL[dtype]
+    rep = []
+    for n in ("dq", "dk", "dv", "da", "dp", "dr", "dlam0", "deta0"):
+        _check(n, to_np(gr[n]), ref[n], tol, rep)
+    for n in ("dq", "dk", "dv", "da", "dp", "dr", "dlam0", "deta0"):
+        assert torch.equal(gr[n], gr2[n]), f"{n} differs between saved and recomputed context"
+    log("  " + " ".join(rep))
+
+
 def test_pc_empty_sequence(kla):
     B, H, dk, dv = 2, 2, 32, 16
     g = np.random.default_rng(1)
@@ -138,13 +169,17 @@ def test_pc_lm_layer_full_size(kla):
     bits = K.full(w, names=NAMES, as_bits=True)
     x = {n: bits_to_torch(bits[n], DEV) for n in bits}
     del bits
-    log("pc lm layer: forward on GPU")
-    out = kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], want_var=True)
+    dyb = bits_to_torch(K.full(w, names=("dy",), as_bits=True)["dy"], DEV)
+    log("pc lm layer: forward and backward on GPU")
+    out = kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], want_var=True, save=True)
+    gr = kla.kla_backward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], None, None, dyb,
+                             saved=out["saved"], want_init_grads=False)
     torch.cuda.synchronize()
-    pairs = [(0, 0), (w.B - 1, w.H - 1), (3, 9)]
+    pairs = [(0, 0), (w.B - 1, w.H - 1)]
     log(f"pc lm layer: oracle on pairs {pairs}")
-    sl = K.pairs_slice(w, pairs, names=NAMES)
+    sl = K.pairs_slice(w, pairs, names=NAMES + ("dy",))
     ref = oracle.forward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["rc"])
+    rg = oracle.backward(sl["q"], sl["k"], sl["v"], sl["a"], sl["p"], sl["rc"], None, None, sl["dy"])
     bi = [b for b, _ in pairs]
     hi = [h for _, h in pairs]
     tol = TOL[w.dtype]
@@ -153,6 +188,9 @@ def test_pc_lm_layer_full_size(kla):
     _check("yvar", to_np(out["yvar"][bi, :, hi]), ref["yvar"][:, :, 0], tol, rep)
     _check("lamT", to_np(out["lamT"][bi, hi]), ref["lamT"][:, 0], tol, rep)
     _check("etaT", to_np(out["etaT"][bi, hi]), ref["etaT"][:, 0], tol, rep)
+    for n in ("dq", "dk", "dv", "da", "dp", "dr"):
+        _check(n, to_np(gr[n][bi, :, hi]), rg[n][:, :, 0], tol, rep)
+        assert torch.isfinite(gr[n].float()).all(), n
     assert torch.all(out["lamT"] > 0) and torch.all(out["yvar"] > 0)
     assert torch.isfinite(out["y"].float()).all()
     log("  pc lm layer: " + " ".join(rep))
