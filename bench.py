@@ -22,6 +22,11 @@ With --pc it times forward + backward of the per-channel-precision variant
 (kla_forward_pc / kla_backward_pc: r drawn per value channel, precision and
 gates per (key slot, value channel)), elementwise scans bound by VALU issue;
 their roofline is the chip's fp32 VALU issue rate (see ALU_SLOTS_*).
+
+With --block it times the block scaffolding around the layer at the same shape,
+forward + backward: the causal conv1d + SiLU over the C = H dk channels, the
+RMS QK-norm of q and of k (rows of dk) and the SiLU gate of the output, all
+HBM-bound; the roofline object is for the dominant kernel call.
 """
 import argparse
 import json
@@ -140,6 +145,79 @@ def bench_pc(args, w, dev):
     print(json.dumps(res), flush=True)
 
 
+def bench_block(args, w, dev):
+    """Conv + SiLU, QK-norm (q and k) and gate, forward + backward, at the LM-layer shape."""
+    import torch
+    import paper_2602_10743_amd as kla
+    B, T, H, d = w.B, w.T, w.H, w.dk
+    C = H * d
+    gen = torch.Generator(device=dev).manual_seed(0)
+    r = lambda *s: torch.randn(*s, generator=gen, device=dev).to(torch.bfloat16)
+    x, du, q, k, y, z, g = r(B, T, C), r(B, T, C), r(B, T, H, d), r(B, T, H, d), r(B, T, C), r(B, T, C), r(B, T, C)
+    cw = torch.randn(C, 4, generator=gen, device=dev) * 0.5
+    cb = torch.randn(C, generator=gen, device=dev)
+    nw = torch.ones(d, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    calls = {}
+
+    def timed(name, fn):
+        if name not in calls:
+            calls[name] = []
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        out = fn()
+        e1.record(stream)
+        calls[name].append((e0, e1))
+        return out
+
+    def step():
+        timed("conv_fwd", lambda: kla.kla_conv_silu_forward(x, cw, cb))
+        timed("conv_bwd", lambda: kla.kla_conv_silu_backward(x, cw, cb, du))
+        for nm, t in (("q", q), ("k", k)):
+            out, rstd = timed("norm_fwd", lambda: kla.kla_qk_norm_forward(t, nw, 1e-6))
+            timed("norm_bwd", lambda: kla.kla_qk_norm_backward(t, nw, rstd, out))
+        timed("gate_fwd", lambda: kla.kla_gate_forward(y, z))
+        timed("gate_bwd", lambda: kla.kla_gate_backward(y, z, g))
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    calls.clear()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = {n: float(np.mean([a.elapsed_time(b) for a, b in v])) for n, v in calls.items()}
+    th = w.token_heads
+    s = 2
+    # algorithmic bytes per call (bf16 tensors; fp32 row statistics and weights are negligible)
+    nbytes = {"conv_fwd": 2 * B * T * C * s, "conv_bwd": 3 * B * T * C * s,
+              "norm_fwd": 2 * th * d * s + th * 4, "norm_bwd": 3 * th * d * s + th * 4,
+              "gate_fwd": 3 * B * T * C * s, "gate_bwd": 5 * B * T * C * s}
+    dom = max(ms, key=lambda n: ms[n] * calls_per_step(n))
+    achieved = nbytes[dom] / (ms[dom] * 1e-3) / 1e9
+    ms_per_step = wall * 1e3 / args.steps
+    res = {
+        "metric": METRIC, "value": th / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name + "_block_scaffolding", "B": B, "T": T, "H": H, "dk": d, "C": C,
+                   "pass": "fwd+bwd", "ops": "conv1d(k=4)+silu, rms qk-norm of q and k, silu gate",
+                   "tokens_counted": "B*T*H"},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_call": nbytes[dom],
+                     "per_call_ms": ms,
+                     "per_call_frac": {n: nbytes[n] / (ms[n] * 1e-3) / 1e9 / HBM_PEAK_GBS for n in ms}},
+    }
+    print(json.dumps(res), flush=True)
+
+
+def calls_per_step(name):
+    return 2 if name.startswith("norm") else 1
+
+
 def cpu_baseline(w, budget_s: float, ou=None):
     """fp64 oracle (forward + backward) on a few sampled (b, h) sequences.  With
     OU parameters ``ou`` the sample is every batch row of as many heads as fit
@@ -195,7 +273,9 @@ def main():
     ap.add_argument("--ou", action="store_true",
                     help="OU gates: time-invariant (a, p, delta) instead of per-token abar, pbar")
     ap.add_argument("--pc", action="store_true",
-                    help="forward of the per-channel-precision variant (elementwise scan)")
+                    help="per-channel-precision variant (elementwise scans), forward + backward")
+    ap.add_argument("--block", action="store_true",
+                    help="block scaffolding around the layer (conv + SiLU, QK-norm, gate), forward + backward")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the filter layer shards over (batch, head) with no "
@@ -211,6 +291,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.pc:
         bench_pc(args, w, dev)
+        return
+    if args.block:
+        bench_block(args, w, dev)
         return
     names = ("q", "k", "v", "r", "dy") if args.ou else K.NAMES + ("dy",)
     bits = K.full(w, names=names, as_bits=True)

@@ -236,6 +236,43 @@ kla_status kla_decode_step_pc(int32_t S, int32_t H, int32_t dk, int32_t dv, int3
                               const void* abar, const void* pbar, const void* r,
                               float* lam, float* eta, void* y, float* yvar, hipStream_t stream);
 
+/*
+ * Block scaffolding around the layer (the Mamba-style block of Sec. 4.4 and
+ * Appendix A): a causal depthwise 1D convolution of kernel size 4 fused with
+ * SiLU, QK-norm, and the SiLU output gate.  The paper fixes no details beyond
+ * that; the definitions implemented are:
+ *
+ *   conv:  u[b,t,c] = silu(bias[c] + sum_{j<4} w[c,j] x[b,t-3+j,c])   (x = 0 before t = 0;
+ *          tap 3 is the current token)                      x, u [B, T, C] dtype; w [C, 4] fp32;
+ *                                                           bias [C] fp32 or NULL
+ *   norm:  out = x / sqrt(mean_row(x^2) + eps) * w           rows of n in {16, 32, 64, 128}
+ *          (one head's q or k of one token), w [n] fp32 shared by the rows; rstd [rows] fp32
+ *          receives 1 / sqrt(mean(x^2) + eps) for the backward (may be NULL in the forward)
+ *   gate:  out = y * silu(z)                                 y, z, out [n] dtype
+ *
+ * silu(s) = s / (1 + exp(-s)).  C must be a multiple of 8 (bf16) or 4 (fp32),
+ * as must the gate's n; pointers 16-byte aligned.  Weight gradients (dw,
+ * dbias) are overwritten and summed over (b, t) or rows in a fixed order through
+ * the workspace.  Every other convention of this header applies.
+ */
+size_t kla_conv_silu_workspace(int32_t B, int32_t T, int32_t C);
+kla_status kla_conv_silu_forward(int32_t B, int32_t T, int32_t C, int32_t dtype, const void* x, const float* w,
+                                 const float* bias, void* u, hipStream_t stream);
+kla_status kla_conv_silu_backward(int32_t B, int32_t T, int32_t C, int32_t dtype, const void* x, const float* w,
+                                  const float* bias, const void* du, void* dx, float* dw, float* dbias,
+                                  void* ws, size_t ws_bytes, hipStream_t stream);
+
+size_t kla_qk_norm_workspace(int32_t n);
+kla_status kla_qk_norm_forward(int64_t rows, int32_t n, int32_t dtype, const void* x, const float* w, float eps,
+                               void* out, float* rstd, hipStream_t stream);
+kla_status kla_qk_norm_backward(int64_t rows, int32_t n, int32_t dtype, const void* x, const float* w,
+                                const float* rstd, const void* dout, void* dx, float* dw,
+                                void* ws, size_t ws_bytes, hipStream_t stream);
+
+kla_status kla_gate_forward(int64_t n, int32_t dtype, const void* y, const void* z, void* out, hipStream_t stream);
+kla_status kla_gate_backward(int64_t n, int32_t dtype, const void* y, const void* z, const void* dout,
+                             void* dy, void* dz, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char* kla_status_string(kla_status status);
 

@@ -21,6 +21,8 @@ __all__ = ["kla_forward", "kla_backward", "kla_decode_step", "kla_status_string"
            "kla_forward_workspace", "kla_backward_workspace", "kla_saved_bytes",
            "kla_forward_ou", "kla_backward_ou", "kla_decode_step_ou", "kla_backward_ou_workspace",
            "kla_forward_pc", "kla_backward_pc", "kla_decode_step_pc",
+           "kla_conv_silu_forward", "kla_conv_silu_backward", "kla_qk_norm_forward", "kla_qk_norm_backward",
+           "kla_gate_forward", "kla_gate_backward",
            "KLAError", "KLAFilter", "kla_filter", "KLAFilterOU", "kla_filter_ou", "library_path"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -82,6 +84,20 @@ def _load():
     lib.kla_saved_pc_bytes.restype = ctypes.c_size_t
     lib.kla_backward_pc_workspace.argtypes = [D, ctypes.c_int]
     lib.kla_backward_pc_workspace.restype = ctypes.c_size_t
+    i32, i64 = ctypes.c_int32, ctypes.c_int64
+    lib.kla_conv_silu_workspace.argtypes = [i32] * 3
+    lib.kla_conv_silu_workspace.restype = ctypes.c_size_t
+    lib.kla_conv_silu_forward.argtypes = [i32] * 4 + [_VP] * 5
+    lib.kla_conv_silu_backward.argtypes = [i32] * 4 + [_VP] * 8 + [ctypes.c_size_t, _VP]
+    lib.kla_qk_norm_workspace.argtypes = [i32]
+    lib.kla_qk_norm_workspace.restype = ctypes.c_size_t
+    lib.kla_qk_norm_forward.argtypes = [i64, i32, i32, _VP, _VP, ctypes.c_float, _VP, _VP, _VP]
+    lib.kla_qk_norm_backward.argtypes = [i64, i32, i32] + [_VP] * 7 + [ctypes.c_size_t, _VP]
+    lib.kla_gate_forward.argtypes = [i64, i32] + [_VP] * 4
+    lib.kla_gate_backward.argtypes = [i64, i32] + [_VP] * 6
+    for fn in ("kla_conv_silu_forward", "kla_conv_silu_backward", "kla_qk_norm_forward", "kla_qk_norm_backward",
+               "kla_gate_forward", "kla_gate_backward"):
+        getattr(lib, fn).restype = ctypes.c_int
     lib.kla_decode_step_pc.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
     lib.kla_decode_step_pc.restype = ctypes.c_int
     lib.kla_status_string.argtypes = [ctypes.c_int]
@@ -528,3 +544,110 @@ def kla_decode_step_pc(q, k, v, a, p, r, lam, eta, *, want_var: bool = False, y=
     if st != 0:
         raise KLAError(st, "kla_decode_step_pc")
     return {"y": y, "yvar": yvar, "lam": lam, "eta": eta}
+
+
+# ---- block scaffolding: causal conv1d (k = 4) + SiLU, RMS QK-norm, SiLU gate
+
+def _dense(t, name, dtype=None):
+    if not t.is_cuda or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous GPU tensor")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}")
+    return t
+
+
+def kla_conv_silu_forward(x, w, bias=None):
+    """u = silu(causal depthwise conv of x [B, T, C] with w [C, 4] (tap 3 = current token) + bias [C])."""
+    lib = _load()
+    _dense(x, "x")
+    B, T, C = x.shape
+    _f32(w, (C, 4), x.device, "w")
+    _f32(bias, (C,), x.device, "bias")
+    u = torch.empty_like(x)
+    st = lib.kla_conv_silu_forward(B, T, C, _DTYPES[x.dtype], _p(x), _p(w), _p(bias), _p(u), _stream(x.device))
+    if st != 0:
+        raise KLAError(st, "kla_conv_silu_forward")
+    return u
+
+
+def kla_conv_silu_backward(x, w, bias, du):
+    """(dx, dw, dbias) of kla_conv_silu_forward; dbias is None without a bias."""
+    lib = _load()
+    _dense(x, "x")
+    B, T, C = x.shape
+    _dense(du, "du", x.dtype)
+    _f32(w, (C, 4), x.device, "w")
+    _f32(bias, (C,), x.device, "bias")
+    dx = torch.empty_like(x)
+    dw = torch.empty((C, 4), dtype=torch.float32, device=x.device)
+    db = torch.empty((C,), dtype=torch.float32, device=x.device) if bias is not None else None
+    nws = int(lib.kla_conv_silu_workspace(B, T, C))
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=x.device)
+    st = lib.kla_conv_silu_backward(B, T, C, _DTYPES[x.dtype], _p(x), _p(w), _p(bias), _p(du), _p(dx), _p(dw),
+                                    _p(db), _p(ws), nws, _stream(x.device))
+    if st != 0:
+        raise KLAError(st, "kla_conv_silu_backward")
+    return dx, dw, db
+
+
+def kla_qk_norm_forward(x, w, eps: float = 1e-6):
+    """RMS normalisation of the rows (last dimension n) of x with weight w [n]; returns (out, rstd)."""
+    lib = _load()
+    _dense(x, "x")
+    n = x.shape[-1]
+    rows = x.numel() // max(n, 1)
+    _f32(w, (n,), x.device, "w")
+    out = torch.empty_like(x)
+    rstd = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device)
+    st = lib.kla_qk_norm_forward(rows, n, _DTYPES[x.dtype], _p(x), _p(w), float(eps), _p(out), _p(rstd),
+                                 _stream(x.device))
+    if st != 0:
+        raise KLAError(st, "kla_qk_norm_forward")
+    return out, rstd
+
+
+def kla_qk_norm_backward(x, w, rstd, dout):
+    """(dx, dw) of kla_qk_norm_forward."""
+    lib = _load()
+    _dense(x, "x")
+    n = x.shape[-1]
+    rows = x.numel() // max(n, 1)
+    _f32(w, (n,), x.device, "w")
+    _f32(rstd, tuple(x.shape[:-1]), x.device, "rstd")
+    _dense(dout, "dout", x.dtype)
+    dx = torch.empty_like(x)
+    dw = torch.empty((n,), dtype=torch.float32, device=x.device)
+    nws = int(lib.kla_qk_norm_workspace(n))
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=x.device)
+    st = lib.kla_qk_norm_backward(rows, n, _DTYPES[x.dtype], _p(x), _p(w), _p(rstd), _p(dout), _p(dx), _p(dw),
+                                  _p(ws), nws, _stream(x.device))
+    if st != 0:
+        raise KLAError(st, "kla_qk_norm_backward")
+    return dx, dw
+
+
+def kla_gate_forward(y, z):
+    """y * silu(z), elementwise."""
+    lib = _load()
+    _dense(y, "y")
+    _dense(z, "z", y.dtype)
+    out = torch.empty_like(y)
+    st = lib.kla_gate_forward(y.numel(), _DTYPES[y.dtype], _p(y), _p(z), _p(out), _stream(y.device))
+    if st != 0:
+        raise KLAError(st, "kla_gate_forward")
+    return out
+
+
+def kla_gate_backward(y, z, dout):
+    """(dy, dz) of kla_gate_forward."""
+    lib = _load()
+    _dense(y, "y")
+    _dense(z, "z", y.dtype)
+    _dense(dout, "dout", y.dtype)
+    dy = torch.empty_like(y)
+    dz = torch.empty_like(y)
+    st = lib.kla_gate_backward(y.numel(), _DTYPES[y.dtype], _p(y), _p(z), _p(dout), _p(dy), _p(dz),
+                               _stream(y.device))
+    if st != 0:
+        raise KLAError(st, "kla_gate_backward")
+    return dy, dz

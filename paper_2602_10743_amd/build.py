@@ -24,8 +24,8 @@ FLAGS = [
     "-ffp-contract=fast", "-munsafe-fp-atomics",
     "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function",
 ]
-SOURCES = ["kla_api.cpp", "recurrent.hip", "validate.hip", "ou.hip", "pc.hip", "chunk_fwd.hip", "chunk_bwd_dv.hip",
-           "chunk_bwd_dk.hip"]
+SOURCES = ["kla_api.cpp", "recurrent.hip", "validate.hip", "ou.hip", "pc.hip", "block.hip", "chunk_fwd.hip",
+           "chunk_bwd_dv.hip", "chunk_bwd_dk.hip"]
 
 
 def _hipcc() -> str:

@@ -339,6 +339,82 @@ kla_status kla_decode_step_ou(int32_t S, int32_t H, int32_t dk, int32_t dv, int3
                        kla::DecodeArgs{q, k, v, nullptr, nullptr, r, lam, eta, y, yvar, a, p, delta}, true, stream);
 }
 
+// ---------------------------------------------------------------- block scaffolding
+
+size_t kla_conv_silu_workspace(int32_t B, int32_t T, int32_t C) {
+    if (B < 1 || T < 0 || C < 1) return 0;
+    return kla::conv_parts_bytes(B, T, C);
+}
+
+kla_status kla_conv_silu_forward(int32_t B, int32_t T, int32_t C, int32_t dtype, const void* x, const float* w,
+                                 const float* bias, void* u, hipStream_t stream) {
+    if (dtype != KLA_F32 && dtype != KLA_BF16) return KLA_ERR_DTYPE;
+    if (B < 1 || T < 0 || C < 1 || C % kla::block_vec(dtype == KLA_BF16) != 0) return KLA_ERR_SHAPE;
+    if (!w || (T > 0 && (!x || !u))) return KLA_ERR_NULL;
+    if (!all_aligned(x, (const void*)w, (const void*)bias, u)) return KLA_ERR_ALIGN;
+    return kla::launch_conv_fwd(B, T, C, dtype == KLA_BF16, x, w, bias, u, stream) == hipSuccess ? KLA_OK
+                                                                                                 : KLA_ERR_HIP;
+}
+
+kla_status kla_conv_silu_backward(int32_t B, int32_t T, int32_t C, int32_t dtype, const void* x, const float* w,
+                                  const float* bias, const void* du, void* dx, float* dw, float* dbias, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+    if (dtype != KLA_F32 && dtype != KLA_BF16) return KLA_ERR_DTYPE;
+    if (B < 1 || T < 0 || C < 1 || C % kla::block_vec(dtype == KLA_BF16) != 0) return KLA_ERR_SHAPE;
+    if (!w || !dw || (T > 0 && (!x || !du || !dx))) return KLA_ERR_NULL;
+    if (!all_aligned(x, (const void*)w, (const void*)bias, du, dx, (void*)dw, (void*)dbias, ws)) return KLA_ERR_ALIGN;
+    if (!ws || ws_bytes < kla_conv_silu_workspace(B, T, C)) return KLA_ERR_WORKSPACE;
+    return kla::launch_conv_bwd(B, T, C, dtype == KLA_BF16, x, w, bias, du, dx, dw, dbias, static_cast<float*>(ws),
+                                stream) == hipSuccess
+               ? KLA_OK
+               : KLA_ERR_HIP;
+}
+
+size_t kla_qk_norm_workspace(int32_t n) { return width_ok(n) ? kla::norm_parts_bytes(n) : 0; }
+
+kla_status kla_qk_norm_forward(int64_t rows, int32_t n, int32_t dtype, const void* x, const float* w, float eps,
+                               void* out, float* rstd, hipStream_t stream) {
+    if (dtype != KLA_F32 && dtype != KLA_BF16) return KLA_ERR_DTYPE;
+    if (rows < 0 || !width_ok(n) || !(eps >= 0.f)) return KLA_ERR_SHAPE;
+    if (!w || (rows > 0 && (!x || !out))) return KLA_ERR_NULL;
+    if (!all_aligned(x, (const void*)w, out, (void*)rstd)) return KLA_ERR_ALIGN;
+    return kla::launch_norm_fwd((size_t)rows, n, dtype == KLA_BF16, x, w, eps, out, rstd, stream) == hipSuccess
+               ? KLA_OK
+               : KLA_ERR_HIP;
+}
+
+kla_status kla_qk_norm_backward(int64_t rows, int32_t n, int32_t dtype, const void* x, const float* w,
+                                const float* rstd, const void* dout, void* dx, float* dw, void* ws, size_t ws_bytes,
+                                hipStream_t stream) {
+    if (dtype != KLA_F32 && dtype != KLA_BF16) return KLA_ERR_DTYPE;
+    if (rows < 0 || !width_ok(n)) return KLA_ERR_SHAPE;
+    if (!w || !dw || (rows > 0 && (!x || !rstd || !dout || !dx))) return KLA_ERR_NULL;
+    if (!all_aligned(x, (const void*)w, (const void*)rstd, dout, dx, (void*)dw, ws)) return KLA_ERR_ALIGN;
+    if (!ws || ws_bytes < kla_qk_norm_workspace(n)) return KLA_ERR_WORKSPACE;
+    return kla::launch_norm_bwd((size_t)rows, n, dtype == KLA_BF16, x, w, rstd, dout, dx, dw, static_cast<float*>(ws),
+                                stream) == hipSuccess
+               ? KLA_OK
+               : KLA_ERR_HIP;
+}
+
+kla_status kla_gate_forward(int64_t n, int32_t dtype, const void* y, const void* z, void* out, hipStream_t stream) {
+    if (dtype != KLA_F32 && dtype != KLA_BF16) return KLA_ERR_DTYPE;
+    if (n < 0 || n % kla::block_vec(dtype == KLA_BF16) != 0) return KLA_ERR_SHAPE;
+    if (n > 0 && (!y || !z || !out)) return KLA_ERR_NULL;
+    if (!all_aligned(y, z, out)) return KLA_ERR_ALIGN;
+    return kla::launch_gate_fwd((size_t)n, dtype == KLA_BF16, y, z, out, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+kla_status kla_gate_backward(int64_t n, int32_t dtype, const void* y, const void* z, const void* dout, void* dy,
+                             void* dz, hipStream_t stream) {
+    if (dtype != KLA_F32 && dtype != KLA_BF16) return KLA_ERR_DTYPE;
+    if (n < 0 || n % kla::block_vec(dtype == KLA_BF16) != 0) return KLA_ERR_SHAPE;
+    if (n > 0 && (!y || !z || !dout || !dy || !dz)) return KLA_ERR_NULL;
+    if (!all_aligned(y, z, dout, dy, dz)) return KLA_ERR_ALIGN;
+    return kla::launch_gate_bwd((size_t)n, dtype == KLA_BF16, y, z, dout, dy, dz, stream) == hipSuccess ? KLA_OK
+                                                                                                      : KLA_ERR_HIP;
+}
+
 const char* kla_status_string(kla_status s) {
     switch (s) {
         case KLA_OK: return "KLA_OK";

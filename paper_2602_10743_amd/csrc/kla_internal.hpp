@@ -71,6 +71,22 @@ size_t pc_bwd_workspace(const Shape& s);
 hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const float* ck, float* kpart, hipStream_t st);
 hipError_t launch_decode_pc(const Shape& s, const DecodeArgs& a, hipStream_t st);
 
+// Block scaffolding: causal conv1d (k = 4) + SiLU, RMS QK-norm, SiLU gate.
+int block_vec(bool bf16);   // elements per 16-byte vector
+size_t conv_parts_bytes(int B, int T, int C);
+size_t norm_parts_bytes(int n);
+hipError_t launch_conv_fwd(int B, int T, int C, bool bf16, const void* x, const float* w, const float* bias, void* u,
+                           hipStream_t st);
+hipError_t launch_conv_bwd(int B, int T, int C, bool bf16, const void* x, const float* w, const float* bias,
+                           const void* du, void* dx, float* dw, float* dbias, float* part, hipStream_t st);
+hipError_t launch_norm_fwd(size_t rows, int n, bool bf16, const void* x, const float* w, float eps, void* out,
+                           float* rstd, hipStream_t st);
+hipError_t launch_norm_bwd(size_t rows, int n, bool bf16, const void* x, const float* w, const float* rstd,
+                           const void* dout, void* dx, float* dw, float* part, hipStream_t st);
+hipError_t launch_gate_fwd(size_t n, bool bf16, const void* y, const void* z, void* out, hipStream_t st);
+hipError_t launch_gate_bwd(size_t n, bool bf16, const void* y, const void* z, const void* dout, void* dy, void* dz,
+                           hipStream_t st);
+
 // OU gates: gradients of the parameters from the per-part gate-gradient sums
 hipError_t launch_ou_param_grads(int H, int dk, int nparts, const float* part, const float* a, const float* p,
                                  const float* d, float* da, float* dp, float* dd, hipStream_t st);

@@ -168,3 +168,23 @@ def test_per_channel_entry_points(lib):
     bad = list(bwd)
     bad[18] = None                                                 # dr
     assert lib.kla_backward_pc(ctypes.byref(d), *bad, 1 << 40, None) == 1
+
+
+def test_block_scaffolding_entry_points(lib):
+    names = _declared()
+    for n in ("kla_conv_silu_forward", "kla_conv_silu_backward", "kla_conv_silu_workspace", "kla_qk_norm_forward",
+              "kla_qk_norm_backward", "kla_qk_norm_workspace", "kla_gate_forward", "kla_gate_backward"):
+        assert n in names
+    fake = ctypes.c_void_p(0x10000)
+    odd = ctypes.c_void_p(0x10004)
+    assert lib.kla_conv_silu_forward(2, 10, 12, 1, fake, fake, None, fake, None) == 2    # C % 8 for bf16
+    assert lib.kla_conv_silu_forward(2, 10, 16, 3, fake, fake, None, fake, None) == 3    # dtype
+    assert lib.kla_conv_silu_forward(2, 10, 16, 1, None, fake, None, fake, None) == 1    # x
+    assert lib.kla_conv_silu_forward(2, 10, 16, 1, odd, fake, None, fake, None) == 4     # alignment
+    assert lib.kla_conv_silu_backward(2, 10, 16, 1, fake, fake, None, fake, fake, fake, None, fake, 0, None) == 5
+    assert lib.kla_conv_silu_workspace(2, 130, 16) == 2 * 3 * 16 * 5 * 4   # one part per 64 tokens
+    assert lib.kla_qk_norm_forward(10, 24, 1, fake, fake, ctypes.c_float(1e-6), fake, None, None) == 2
+    assert lib.kla_qk_norm_forward(10, 32, 1, fake, None, ctypes.c_float(1e-6), fake, None, None) == 1
+    assert lib.kla_qk_norm_backward(10, 32, 1, fake, fake, fake, fake, fake, fake, fake, 0, None) == 5
+    assert lib.kla_gate_forward(12, 1, fake, fake, fake, None) == 2                       # n % 8 for bf16
+    assert lib.kla_gate_backward(16, 1, fake, fake, None, fake, fake, None) == 1
