@@ -131,6 +131,40 @@ def test_empty_and_single_token(kla):
             np.testing.assert_allclose(to_np(out["y"]), ref["y"], rtol=1e-5, atol=1e-6)
 
 
+@pytest.mark.parametrize("T", [0, 1, 32, 33])
+def test_chunked_edges(kla, T):
+    """The chunked bf16 path with no token, one token, exactly one chunk and one chunk plus a token,
+    with an initial belief and gradients of the final belief."""
+    B, H, dk, dv = 2, 2, 64, 32
+    case = K.random_case(B, T, H, dk, dv, "bf16", seed=50 + T, dist="lm")
+    lam0, eta0 = _random_belief(B, H, dk, dv, 9)
+    g = np.random.default_rng(T)
+    dlamT = g.standard_normal((B, H, dk)).astype(np.float32).astype(np.float64)
+    detaT = g.standard_normal((B, H, dk, dv)).astype(np.float32).astype(np.float64)
+    log(f"chunked edge T={T}")
+    x = _dev_inputs(case, "bf16")
+    f32 = lambda a: torch.tensor(a, dtype=torch.float32, device=DEV)
+    out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), want_var=True,
+                          save=True)
+    gr = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), x["dy"],
+                          f32(dlamT), f32(detaT), saved=out["saved"])
+    torch.cuda.synchronize()
+    ref = oracle.forward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0)
+    rg = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0,
+                         case["dy"], dlamT, detaT)
+    rep = []
+    tol = TOL["bf16"]
+    _check("lamT", to_np(out["lamT"]), ref["lamT"], TOL["f32"], rep)
+    _check("etaT", to_np(out["etaT"]), ref["etaT"], tol, rep)
+    _check("dlam0", to_np(gr["dlam0"]), rg["dlam0"], tol, rep)
+    _check("deta0", to_np(gr["deta0"]), rg["deta0"], tol, rep)
+    if T:
+        _check("y", to_np(out["y"]), K.quantise(ref["y"], "bf16"), tol, rep)
+        for n in ("dq", "dk", "dv", "da", "dp", "dr"):
+            _check(n, to_np(gr[n]), rg[n], tol, rep)
+    log("  " + " ".join(rep))
+
+
 def test_bitwise_deterministic(kla):
     case = K.random_case(2, 300, 4, 128, 128, "bf16", seed=9, dist="lm")
     x = _dev_inputs(case, "bf16")
