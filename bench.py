@@ -23,6 +23,11 @@ With --pc it times forward + backward of the per-channel-precision variant
 gates per (key slot, value channel)), elementwise scans bound by VALU issue;
 their roofline is the chip's fp32 VALU issue rate (see ALU_SLOTS_*).
 
+With --decode it times kla_decode_step on the decode workload (S = 512
+sequences, H = 16, d = 128, fp32 belief of 512 MiB updated in place), HBM-bound
+on the belief; --decode --pc times kla_decode_step_pc (per-channel precision:
+the precision is a second dk x dv array per head).
+
 With --block it times the block scaffolding around the layer at the same shape,
 forward + backward: the causal conv1d + SiLU over the C = H dk channels, the
 RMS QK-norm of q and of k (rows of dk) and the SiLU gate of the output, all
@@ -214,6 +219,64 @@ def bench_block(args, w, dev):
     print(json.dumps(res), flush=True)
 
 
+def bench_decode(args, dev):
+    """kla_decode_step (or kla_decode_step_pc) at the decode workload's shape, belief resident in HBM."""
+    import torch
+    import kla_inputs as K
+    import paper_2602_10743_amd as kla
+    w = K.WORKLOADS[4]
+    S, H, dk, dv = w.B, w.H, w.dk, w.dv
+    gen = torch.Generator(device=dev).manual_seed(0)
+    steps_in = 8   # distinct per-step inputs, cycled
+    n = lambda *sh: torch.randn(*sh, generator=gen, device=dev)
+    sp = lambda *sh: torch.nn.functional.softplus(n(*sh))
+    xs = []
+    for _ in range(steps_in):
+        k = n(S, H, dk)
+        xs.append({"q": n(S, H, dk), "k": k / k.norm(dim=-1, keepdim=True), "v": n(S, H, dv),
+                   "a": torch.sigmoid(n(S, H, dk) + 3.0), "p": sp(S, H, dk) * 0.05,
+                   "r": sp(S, H, dv) if args.pc else sp(S, H)})
+    lam = 1.0 + torch.rand((S, H, dk, dv) if args.pc else (S, H, dk), generator=gen, device=dev)
+    eta = n(S, H, dk, dv)
+    y = torch.empty((S, H, dv), device=dev)
+    fn = kla.kla_decode_step_pc if args.pc else kla.kla_decode_step
+    stream = torch.cuda.current_stream(dev)
+
+    def step(i):
+        x = xs[i % steps_in]
+        fn(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], lam, eta, y=y)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    # per (sequence, head): read and write the fp32 belief, read the fp32 inputs, write y
+    belief = (2 * dk * dv if args.pc else dk * dv + dk)
+    inputs = 4 * dk + dv + (dv if args.pc else 1)
+    nbytes = S * H * (8 * belief + 4 * inputs + 4 * dv)
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    res = {
+        "metric": METRIC, "value": S * H / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name + ("_pc" if args.pc else ""), "S": S, "H": H, "dk": dk, "dv": dv,
+                   "pass": "decode step", "tokens_counted": "S*H per step"},
+        "roofline": {"bound": "hbm", "kernel": "kla_decode_step_pc" if args.pc else "kla_decode_step",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes_per_call": nbytes, "call_ms": ms},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def calls_per_step(name):
     return 2 if name.startswith("norm") else 1
 
@@ -274,6 +337,8 @@ def main():
                     help="OU gates: time-invariant (a, p, delta) instead of per-token abar, pbar")
     ap.add_argument("--pc", action="store_true",
                     help="per-channel-precision variant (elementwise scans), forward + backward")
+    ap.add_argument("--decode", action="store_true",
+                    help="decode step on the decode workload (with --pc: per-channel precision)")
     ap.add_argument("--block", action="store_true",
                     help="block scaffolding around the layer (conv + SiLU, QK-norm, gate), forward + backward")
     args = ap.parse_args()
@@ -289,6 +354,9 @@ def main():
     w = K.WORKLOADS[2]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.decode:
+        bench_decode(args, dev)
+        return
     if args.pc:
         bench_pc(args, w, dev)
         return
