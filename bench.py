@@ -28,6 +28,10 @@ sequences, H = 16, d = 128, fp32 belief of 512 MiB updated in place), HBM-bound
 on the belief; --decode --pc times kla_decode_step_pc (per-channel precision:
 the precision is a second dk x dv array per head).
 
+With --long it times the forward of the long-context workload (B = 1, H = 16,
+T = 65536, d = 128, bf16; heads 8..15 with slow decay), which has only 16
+sequences to spread over the chip.
+
 With --block it times the block scaffolding around the layer at the same shape,
 forward + backward: the causal conv1d + SiLU over the C = H dk channels, the
 RMS QK-norm of q and of k (rows of dk) and the SiLU gate of the output, all
@@ -277,6 +281,50 @@ def bench_decode(args, dev):
     print(json.dumps(res), flush=True)
 
 
+def bench_long(args, dev):
+    """kla_forward (no saved context) on the long-context workload."""
+    import torch
+    import kla_inputs as K
+    import paper_2602_10743_amd as kla
+    w = K.WORKLOADS[3]
+    bits = K.full(w, names=K.NAMES, as_bits=True)
+    x = {n: torch.from_numpy(np.ascontiguousarray(bits[n].view(np.int16))).view(torch.bfloat16).to(dev)
+         for n in bits}
+    del bits
+    stream = torch.cuda.current_stream(dev)
+    y = torch.empty_like(x["v"])
+
+    def step():
+        kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], want_state=True, y=y)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1) / args.steps
+    th = w.token_heads
+    fwd_b, _ = algorithmic_bytes(w, 2)
+    achieved = fwd_b * th / (ms * 1e-3) / 1e9
+    res = {
+        "metric": METRIC, "value": th / (wall / args.steps), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv, "pass": "fwd",
+                   "tokens_counted": "B*T*H"},
+        "roofline": {"bound": "hbm", "kernel": "kla_forward", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_call": fwd_b * th, "call_ms": ms},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def calls_per_step(name):
     return 2 if name.startswith("norm") else 1
 
@@ -339,6 +387,7 @@ def main():
                     help="per-channel-precision variant (elementwise scans), forward + backward")
     ap.add_argument("--decode", action="store_true",
                     help="decode step on the decode workload (with --pc: per-channel precision)")
+    ap.add_argument("--long", action="store_true", help="forward of the long-context workload")
     ap.add_argument("--block", action="store_true",
                     help="block scaffolding around the layer (conv + SiLU, QK-norm, gate), forward + backward")
     args = ap.parse_args()
@@ -356,6 +405,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.decode:
         bench_decode(args, dev)
+        return
+    if args.long:
+        bench_long(args, dev)
         return
     if args.pc:
         bench_pc(args, w, dev)

@@ -23,7 +23,7 @@
 namespace kla {
 namespace {
 
-template <int DK, int DV, bool YV, bool TI>
+template <int DK, int DV, bool YV, bool TI, bool NOY>
 __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Shape s, FwdArgs g, float* saved_lam,
                                                                          float* saved_H) {
     using Cfg = ChunkCfg<DK, DV>;
@@ -93,72 +93,74 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
                 const uint16_t* sKL = reinterpret_cast<const uint16_t*>(buf + Cfg::KL);
                 const float* sDec = reinterpret_cast<const float*>(buf + Cfg::DEC);
 
-                // ---- S^T[j, i] = sum_n Kn[j, n] Qp[i, n], tiles (jt, it) = (0,0), (0,1), (1,1)
-                f32x4 S00 = zero4(), S01 = zero4(), S11 = zero4();
+                if constexpr (!NOY) {   // the readout (skipped when only the final state is asked for)
+                    // ---- S^T[j, i] = sum_n Kn[j, n] Qp[i, n], tiles (jt, it) = (0,0), (0,1), (1,1)
+                    f32x4 S00 = zero4(), S01 = zero4(), S11 = zero4();
 #pragma unroll
-                for (int ks = 0; ks < KSN; ++ks) {
-                    const int o0 = l16 * LQ + 32 * ks + 8 * g4, o1 = o0 + 16 * LQ;
-                    const bf16x8 k0h = lds8(sKH + o0), k0l = lds8(sKL + o0);
-                    const bf16x8 k1h = lds8(sKH + o1), k1l = lds8(sKL + o1);
-                    const bf16x8 q0h = lds8(sQH + o0), q0l = lds8(sQL + o0);
-                    const bf16x8 q1h = lds8(sQH + o1), q1l = lds8(sQL + o1);
-                    S00 = mfma3(k0h, k0l, q0h, q0l, S00);
-                    S01 = mfma3(k0h, k0l, q1h, q1l, S01);
-                    S11 = mfma3(k1h, k1l, q1h, q1l, S11);
-                }
-#pragma unroll
-                for (int rr = 0; rr < 4; ++rr) {   // causal mask j <= i inside the diagonal tiles
-                    if (4 * g4 + rr > l16) {
-                        S00[rr] = 0.f;
-                        S11[rr] = 0.f;
+                    for (int ks = 0; ks < KSN; ++ks) {
+                        const int o0 = l16 * LQ + 32 * ks + 8 * g4, o1 = o0 + 16 * LQ;
+                        const bf16x8 k0h = lds8(sKH + o0), k0l = lds8(sKL + o0);
+                        const bf16x8 k1h = lds8(sKH + o1), k1l = lds8(sKL + o1);
+                        const bf16x8 q0h = lds8(sQH + o0), q0l = lds8(sQL + o0);
+                        const bf16x8 q1h = lds8(sQH + o1), q1l = lds8(sQL + o1);
+                        S00 = mfma3(k0h, k0l, q0h, q0l, S00);
+                        S01 = mfma3(k0h, k0l, q1h, q1l, S01);
+                        S11 = mfma3(k1h, k1l, q1h, q1l, S11);
                     }
-                }
-                // B operands over the 32-deep contraction j (rows {4g..4g+3} and {16+4g..16+4g+3})
-                bf16x8 sbh[2], sbl[2];
-                split8(S00, zero4(), sbh[0], sbl[0]);
-                split8(S01, S11, sbh[1], sbl[1]);
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr) {   // causal mask j <= i inside the diagonal tiles
+                        if (4 * g4 + rr > l16) {
+                            S00[rr] = 0.f;
+                            S11[rr] = 0.f;
+                        }
+                    }
+                    // B operands over the 32-deep contraction j (rows {4g..4g+3} and {16+4g..16+4g+3})
+                    bf16x8 sbh[2], sbl[2];
+                    split8(S00, zero4(), sbh[0], sbl[0]);
+                    split8(S01, S11, sbh[1], sbl[1]);
 
-                // ---- y^T[d, i] = sum_j V^T[d, j] S^T[j, i] + sum_n H^T[d, n] Qp^T[n, i]
-                f32x4 yacc[NDT][2];
-#pragma unroll
-                for (int dt = 0; dt < NDT; ++dt) {
-                    const bf16x8 va = lds_tr8(sVS, DVT, 4 * g4, 16 + 4 * g4, dl0 + 16 * dt, l16);
-#pragma unroll
-                    for (int it = 0; it < 2; ++it) yacc[dt][it] = mfma2b(va, sbh[it], sbl[it], zero4());
-                }
-#pragma unroll
-                for (int ks = 0; ks < KSN; ++ks) {
-                    bf16x8 qbh[2], qbl[2];
-#pragma unroll
-                    for (int it = 0; it < 2; ++it) {
-                        const int qo = (16 * it + l16) * LQ + 32 * ks + 4 * g4;
-                        qbh[it] = lds4x2(sQH + qo, sQH + qo + 16);
-                        qbl[it] = lds4x2(sQL + qo, sQL + qo + 16);
-                    }
+                    // ---- y^T[d, i] = sum_j V^T[d, j] S^T[j, i] + sum_n H^T[d, n] Qp^T[n, i]
+                    f32x4 yacc[NDT][2];
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt) {
-                        bf16x8 hh, hl;
-                        split8(Hs[2 * ks][dt], Hs[2 * ks + 1][dt], hh, hl);
+                        const bf16x8 va = lds_tr8(sVS, DVT, 4 * g4, 16 + 4 * g4, dl0 + 16 * dt, l16);
 #pragma unroll
-                        for (int it = 0; it < 2; ++it) yacc[dt][it] = mfma3(hh, hl, qbh[it], qbl[it], yacc[dt][it]);
+                        for (int it = 0; it < 2; ++it) yacc[dt][it] = mfma2b(va, sbh[it], sbl[it], zero4());
                     }
-                    // the chunk-start state goes to the saved context a few rows at a time, between
-                    // the products, so that the stores of all workgroups do not come in one burst
-                    if (saved_H) {
-                        save_rows(cc, 2 * ks);
-                        save_rows(cc, 2 * ks + 1);
-                    }
-                }
-                // y[t, d .. d+3] for t = 16 it + l16, d = dm0 + 16 dt + 4 g4
 #pragma unroll
-                for (int it = 0; it < 2; ++it) {
-                    const int t = 16 * it + l16;
-                    if (t < nt) {
+                    for (int ks = 0; ks < KSN; ++ks) {
+                        bf16x8 qbh[2], qbl[2];
+#pragma unroll
+                        for (int it = 0; it < 2; ++it) {
+                            const int qo = (16 * it + l16) * LQ + 32 * ks + 4 * g4;
+                            qbh[it] = lds4x2(sQH + qo, sQH + qo + 16);
+                            qbl[it] = lds4x2(sQL + qo, sQL + qo + 16);
+                        }
 #pragma unroll
                         for (int dt = 0; dt < NDT; ++dt) {
-                            const uint2 pk{cvt_pk_bf16(yacc[dt][it][0], yacc[dt][it][1]),
-                                           cvt_pk_bf16(yacc[dt][it][2], yacc[dt][it][3])};
-                            *reinterpret_cast<uint2*>(y + ((row0 + t) * H + h) * DV + dm0 + 16 * dt + 4 * g4) = pk;
+                            bf16x8 hh, hl;
+                            split8(Hs[2 * ks][dt], Hs[2 * ks + 1][dt], hh, hl);
+#pragma unroll
+                            for (int it = 0; it < 2; ++it) yacc[dt][it] = mfma3(hh, hl, qbh[it], qbl[it], yacc[dt][it]);
+                        }
+                        // the chunk-start state goes to the saved context a few rows at a time, between
+                        // the products, so that the stores of all workgroups do not come in one burst
+                        if (saved_H) {
+                            save_rows(cc, 2 * ks);
+                            save_rows(cc, 2 * ks + 1);
+                        }
+                    }
+                    // y[t, d .. d+3] for t = 16 it + l16, d = dm0 + 16 dt + 4 g4
+#pragma unroll
+                    for (int it = 0; it < 2; ++it) {
+                        const int t = 16 * it + l16;
+                        if (t < nt) {
+#pragma unroll
+                            for (int dt = 0; dt < NDT; ++dt) {
+                                const uint2 pk{cvt_pk_bf16(yacc[dt][it][0], yacc[dt][it][1]),
+                                               cvt_pk_bf16(yacc[dt][it][2], yacc[dt][it][3])};
+                                *reinterpret_cast<uint2*>(y + ((row0 + t) * H + h) * DV + dm0 + 16 * dt + 4 * g4) = pk;
+                            }
                         }
                     }
                 }
@@ -209,10 +211,10 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
     }
 }
 
-template <int DK, int DV, bool YV, bool TI>
+template <int DK, int DV, bool YV, bool TI, bool NOY = false>
 hipError_t launch_fwd_v(const Shape& s, const FwdArgs& a, float* saved_lam, float* saved_H, hipStream_t st) {
     using Cfg = ChunkCfg<DK, DV>;
-    auto kern = fwd_chunk_kernel<DK, DV, YV, TI>;
+    auto kern = fwd_chunk_kernel<DK, DV, YV, TI, NOY>;
     // more than 64 KiB of LDS must be opted into once per kernel (thread-safe static init)
     static const hipError_t attr = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                        hipFuncAttributeMaxDynamicSharedMemorySize, Cfg::BYTES);
@@ -223,9 +225,11 @@ hipError_t launch_fwd_v(const Shape& s, const FwdArgs& a, float* saved_lam, floa
 }
 
 // the readout variance adds a cross-lane sum per token, so it is a separate
-// instantiation, as are the time-invariant gates
+// instantiation, as are the time-invariant gates and the state-only pass (no y:
+// the segment-parallel forward's first pass)
 template <int DK, int DV>
 hipError_t launch_fwd(const Shape& s, const FwdArgs& a, float* saved_lam, float* saved_H, hipStream_t st) {
+    if (!a.y) return launch_fwd_v<DK, DV, false, false, true>(s, a, nullptr, nullptr, st);
     if (a.ou_a)
         return a.yvar ? launch_fwd_v<DK, DV, true, true>(s, a, saved_lam, saved_H, st)
                       : launch_fwd_v<DK, DV, false, true>(s, a, saved_lam, saved_H, st);

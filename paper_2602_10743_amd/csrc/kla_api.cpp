@@ -75,7 +75,8 @@ extern "C" {
 
 size_t kla_forward_workspace(const kla_desc* desc) {
     if (check_desc(desc) != KLA_OK) return 0;
-    return kAlign;  // validation flag
+    // validation flag, then the segment-parallel forward's carries when the shape takes it
+    return kAlign + round_up(kla::forward_segmented_workspace(shape_of(desc)));
 }
 
 size_t kla_saved_bytes(const kla_desc* desc) {
@@ -121,8 +122,12 @@ kla_status forward_impl(const kla_desc* desc, const kla::FwdArgs& a, bool ou, vo
         st = validate(s, s.T, a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, ws, stream, a.ou_a, a.ou_p, a.ou_d);
         if (st != KLA_OK) return st;
     }
-    hipError_t e = kla::chunked_supported(s) ? kla::launch_forward_chunked(s, a, saved, stream)
-                                             : kla::launch_forward_recurrent(s, a, stream);
+    hipError_t e;
+    if (!saved && !ou && kla::forward_segments(s) > 1)
+        e = kla::launch_forward_segmented(s, a, static_cast<char*>(ws) + kAlign, stream);
+    else
+        e = kla::chunked_supported(s) ? kla::launch_forward_chunked(s, a, saved, stream)
+                                      : kla::launch_forward_recurrent(s, a, stream);
     return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 

@@ -57,6 +57,11 @@ hipError_t launch_forward_chunked(const Shape& s, const FwdArgs& a, void* saved,
 bool chunked_bwd_supported(const Shape& s);
 size_t chunked_bwd_workspace(const Shape& s);
 hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st);
+// Segment-parallel chunked forward for few long sequences (no saved context): the number of
+// segments (1: not used), its workspace and launch.
+int forward_segments(const Shape& s);
+size_t forward_segmented_workspace(const Shape& s);
+hipError_t launch_forward_segmented(const Shape& s, const FwdArgs& a, void* ws, hipStream_t st);
 // value side of the chunked backward (dv, deta0); saved_lam: lam at every 32-token chunk start
 hipError_t launch_backward_dv(const Shape& s, const BwdArgs& a, const float* saved_lam, hipStream_t st);
 // token-sum parts of the OU gate gradients that the chunked / recurrent backward leave

@@ -165,6 +165,31 @@ def test_chunked_edges(kla, T):
     log("  " + " ".join(rep))
 
 
+@pytest.mark.parametrize("init", [False, True])
+def test_segment_parallel_forward(kla, init):
+    """Few long sequences take the segment-parallel forward (no saved context); it must agree with
+    the oracle and with the one-pass chunked forward (taken when a saved context is asked for)."""
+    B, T, H, dk, dv = 1, 8192, 2, 64, 64
+    case = K.random_case(B, T, H, dk, dv, "bf16", seed=77, dist="lm")
+    lam0, eta0 = _random_belief(B, H, dk, dv, 78) if init else (None, None)
+    log(f"segment-parallel forward B{B} T{T} H{H} d{dk} init={init}")
+    x = _dev_inputs(case, "bf16")
+    f32 = lambda a: None if a is None else torch.tensor(a, dtype=torch.float32, device=DEV)
+    seg = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), want_var=True)
+    one = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), want_var=True,
+                          save=True)
+    torch.cuda.synchronize()
+    ref = oracle.forward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0)
+    rep = []
+    tol = TOL["bf16"]
+    for name, out in (("seg", seg), ("one", one)):
+        _check(f"{name}.y", to_np(out["y"]), K.quantise(ref["y"], "bf16"), tol, rep)
+        _check(f"{name}.yvar", to_np(out["yvar"]), ref["yvar"], TOL["f32"], rep)
+        _check(f"{name}.lamT", to_np(out["lamT"]), ref["lamT"], TOL["f32"], rep)
+        _check(f"{name}.etaT", to_np(out["etaT"]), ref["etaT"], tol, rep)
+    log("  " + " ".join(rep))
+
+
 def test_bitwise_deterministic(kla):
     case = K.random_case(2, 300, 4, 128, 128, "bf16", seed=9, dist="lm")
     x = _dev_inputs(case, "bf16")
