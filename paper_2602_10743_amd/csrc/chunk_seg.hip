@@ -4,10 +4,12 @@
 // of the chip idle.  The sequence is cut into NS equal segments and both
 // recursions are carried across segment boundaries by their composition laws
 // (Corollaries 1 and 2):
-//   1. per piece of SUB tokens and key slot, the product of Theorem 1's 2x2
-//      matrices over the piece's tokens (seg_prec_kernel), with prod abar;
-//   2. a scan over the pieces gives the precision at every segment start and
-//      the segment's gate product P_s = prod_t F_t (seg_lam_scan_kernel);
+//   1. per piece of up to 256 tokens and key slot, the product of Theorem 1's
+//      2x2 matrices over the piece's tokens (seg_prec_kernel), with prod abar,
+//      then the product over each segment's pieces (seg_compose_kernel);
+//   2. an exclusive scan over the segments gives the precision at every
+//      segment start and the segment's gate product P_s = prod_t F_t
+//      (seg_lam_scan_kernel);
 //   3. the chunked forward over every segment at once from those precisions
 //      and a zero state gives the state each segment adds on its own, U_s;
 //   4. an exclusive scan of H_{s+1} = diag(P_s) H_s + U_s gives the state at
@@ -67,9 +69,37 @@ __global__ __launch_bounds__(DK) void seg_prec_kernel(int T, int H, int NP, cons
     o[4 * DK + n] = A;
 }
 
+// Per (b, h, segment, key slot): the product of the segment's PPS piece matrices
+// (later pieces on the left) with their abar products, rescaled by the largest
+// entry after each piece; written over the segment's first piece.
+__global__ __launch_bounds__(256) void seg_compose_kernel(int nbh, int DK, int NS, int PPS, float* __restrict__ mseg) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= nbh * NS * DK) return;
+    const int n = i % DK, seg = (i / DK) % NS, bh = i / (DK * NS);
+    float* m0 = mseg + ((size_t)bh * NS * PPS + (size_t)seg * PPS) * 5 * DK;
+    float x0 = m0[0 * DK + n], z0 = m0[1 * DK + n], x1 = m0[2 * DK + n], z1 = m0[3 * DK + n], A = m0[4 * DK + n];
+    for (int u = 1; u < PPS; ++u) {
+        const float* m = m0 + (size_t)u * 5 * DK;
+        const float mx0 = m[0 * DK + n], mz0 = m[1 * DK + n], mx1 = m[2 * DK + n], mz1 = m[3 * DK + n];
+        const float nx0 = fmaf(mx0, x0, mx1 * z0), nz0 = fmaf(mz0, x0, mz1 * z0);
+        const float nx1 = fmaf(mx0, x1, mx1 * z1), nz1 = fmaf(mz0, x1, mz1 * z1);
+        A *= m[4 * DK + n];
+        const float sc = 1.f / fmaxf(fmaxf(fabsf(nx0), fabsf(nz0)), fmaxf(fabsf(nx1), fabsf(nz1)));
+        x0 = nx0 * sc;
+        z0 = nz0 * sc;
+        x1 = nx1 * sc;
+        z1 = nz1 * sc;
+        A *= sc;
+    }
+    m0[0 * DK + n] = x0;
+    m0[1 * DK + n] = z0;
+    m0[2 * DK + n] = x1;
+    m0[3 * DK + n] = z1;
+    m0[4 * DK + n] = A;
+}
+
 // Per (b, h, key slot): lam at every segment start (virtual layout
-// [(b NS + s) H + h][DK]), each segment's gate product (over its PPS pieces),
-// and the final lam.
+// [(b NS + s) H + h][DK]), each segment's gate product, and the final lam.
 __global__ __launch_bounds__(256) void seg_lam_scan_kernel(int B, int H, int DK, int NS, int PPS,
                                                            const float* __restrict__ mseg,
                                                            const float* __restrict__ lam0, float* __restrict__ lam_start,
@@ -81,15 +111,11 @@ __global__ __launch_bounds__(256) void seg_lam_scan_kernel(int B, int H, int DK,
     for (int s = 0; s < NS; ++s) {
         const size_t v = ((size_t)b * NS + s) * H + h;
         lam_start[v * DK + n] = lam;
-        float P = 1.f;
-        for (int u = 0; u < PPS; ++u) {
-            const float* m = mseg + ((size_t)bh * NS * PPS + (size_t)s * PPS + u) * 5 * DK;
-            const float x = fmaf(m[0 * DK + n], lam, m[2 * DK + n]);
-            const float z = fmaf(m[1 * DK + n], lam, m[3 * DK + n]);
-            P *= m[4 * DK + n] / z;
-            lam = x / z;
-        }
-        pseg[v * DK + n] = P;
+        const float* m = mseg + ((size_t)bh * NS * PPS + (size_t)s * PPS) * 5 * DK;   // the composed segment
+        const float x = fmaf(m[0 * DK + n], lam, m[2 * DK + n]);
+        const float z = fmaf(m[1 * DK + n], lam, m[3 * DK + n]);
+        pseg[v * DK + n] = m[4 * DK + n] / z;
+        lam = x / z;
     }
     if (lamT) lamT[i] = lam;
 }
@@ -167,6 +193,9 @@ hipError_t launch_forward_segmented(const Shape& s, const FwdArgs& a, void* ws, 
 #undef KLA_SEG_PREC
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(seg_compose_kernel, dim3((unsigned)((nbh * ns * s.dk + 255) / 256)), dim3(256), 0, st, nbh,
+                       s.dk, ns, pps, mseg);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     hipLaunchKernelGGL(seg_lam_scan_kernel, dim3((unsigned)((nbh * s.dk + 255) / 256)), dim3(256), 0, st, s.B, s.H,
                        s.dk, ns, pps, mseg, a.lam0, lam_start, pseg, a.lamT);
     if ((e = hipGetLastError()) != hipSuccess) return e;

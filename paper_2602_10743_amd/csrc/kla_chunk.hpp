@@ -38,7 +38,8 @@
 //
 // TI (time-invariant gates, from the OU parameters of Sec. 4.1): abar and pbar
 // are the same for every token of a key slot; each lane forms them once and the
-// staging carries only k, q and r.
+// staging carries only k, q and r.  NOQ (a pass that only carries the state):
+// the query is neither staged nor turned into Qp.
 #pragma once
 #include <type_traits>
 
@@ -109,7 +110,7 @@ struct ScanGroup {
     uint4 r[2];
 };
 
-template <int SW, bool TI>
+template <int SW, bool TI, bool NOQ>
 __device__ __forceinline__ void read_group(ScanGroup& gr, const uint16_t* __restrict__ stg,
                                            const uint32_t* __restrict__ rw, int sl, int t8) {
 #pragma unroll
@@ -119,7 +120,7 @@ __device__ __forceinline__ void read_group(ScanGroup& gr, const uint16_t* __rest
             gr.p[e] = stg[(1 * kC + t8 + e) * SW + sl];
         }
         gr.k[e] = stg[(2 * kC + t8 + e) * SW + sl];
-        gr.q[e] = stg[(3 * kC + t8 + e) * SW + sl];
+        if constexpr (!NOQ) gr.q[e] = stg[(3 * kC + t8 + e) * SW + sl];
     }
     gr.r[0] = *reinterpret_cast<const uint4*>(rw + t8);
     gr.r[1] = *reinterpret_cast<const uint4*>(rw + t8 + 4);
@@ -132,7 +133,7 @@ __device__ __forceinline__ float bf16w(uint32_t w) { return __uint_as_float(w <<
 // start lam x.  FULL: all kC tokens are valid (no per-token guards).  TI: the
 // gates are the lane's ca, cp for every token.  Returns the lam at the chunk end
 // in every lane.
-template <int SW, int LQ, bool YV, bool FULL, bool TI>
+template <int SW, int LQ, bool YV, bool FULL, bool TI, bool NOQ>
 __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, const uint32_t* __restrict__ rw,
                                             int sl, int hf, int n, int nt, float x, const ScanOut& o, float ca,
                                             float cp) {
@@ -175,11 +176,11 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
     // ---- walk tokens 16 hf .. 16 hf + 15 (inputs of the next 8 read before the current 8)
     const int tb = 16 * hf;
     ScanGroup gr[2];
-    read_group<SW, TI>(gr[0], stg, rw, sl, tb);
+    read_group<SW, TI, NOQ>(gr[0], stg, rw, sl, tb);
 #pragma unroll
     for (int g = 0; g < 2; ++g) {
         const ScanGroup& cur = gr[g];
-        if (g == 0) read_group<SW, TI>(gr[1], stg, rw, sl, tb + 8);
+        if (g == 0) read_group<SW, TI, NOQ>(gr[1], stg, rw, sl, tb + 8);
 #pragma unroll
         for (int j2 = 0; j2 < 4; ++j2) {
             float qp2[2], kn2[2];
@@ -187,7 +188,7 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
             for (int e = 0; e < 2; ++e) {
                 const int i = 2 * j2 + e, t = tb + 8 * g + i;
                 const float av = TI ? ca : bf16w(cur.a[i]), pv = TI ? cp : bf16w(cur.p[i]);
-                const float kv = bf16w(cur.k[i]), qv = bf16w(cur.q[i]);
+                const float kv = bf16w(cur.k[i]), qv = NOQ ? 0.f : bf16w(cur.q[i]);
                 const uint32_t rword = i < 4 ? (&cur.r[0].x)[i] : (&cur.r[1].x)[i - 4];
                 const float rv = bf16w(rword);
                 const float kr = kv * rv;
@@ -209,13 +210,15 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
                 }
             }
             uint32_t qh, ql, kh, kl;
-            split2(qp2[0], qp2[1], qh, ql);
+            if constexpr (!NOQ) split2(qp2[0], qp2[1], qh, ql);
             split2(kn2[0], kn2[1], kh, kl);
             const int t = tb + 8 * g + 2 * j2;
-            o.qh[t * LQ + n] = static_cast<uint16_t>(qh);
-            o.qh[(t + 1) * LQ + n] = static_cast<uint16_t>(qh >> 16);
-            o.ql[t * LQ + n] = static_cast<uint16_t>(ql);
-            o.ql[(t + 1) * LQ + n] = static_cast<uint16_t>(ql >> 16);
+            if constexpr (!NOQ) {
+                o.qh[t * LQ + n] = static_cast<uint16_t>(qh);
+                o.qh[(t + 1) * LQ + n] = static_cast<uint16_t>(qh >> 16);
+                o.ql[t * LQ + n] = static_cast<uint16_t>(ql);
+                o.ql[(t + 1) * LQ + n] = static_cast<uint16_t>(ql >> 16);
+            }
             o.kh[t * LQ + n] = static_cast<uint16_t>(kh);
             o.kh[(t + 1) * LQ + n] = static_cast<uint16_t>(kh >> 16);
             o.kl[t * LQ + n] = static_cast<uint16_t>(kl);
@@ -245,12 +248,14 @@ struct ScanSrc {
 // chunk-start lam stored to save_lam when given) or c = nchunk-1 .. 0 (REV:
 // the chunk-start lam read from lam_in [BH][nchunk][DK]).  Returns the lam
 // after the last walked token (forward order) for key slot wave * SW + lane % SW.
-template <class Cfg, bool YV, bool REV, bool TI>
+template <class Cfg, bool YV, bool REV, bool TI, bool NOQ = false>
 __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int lane, const ScanSrc& sc,
                                            const float* __restrict__ lam_in, float* __restrict__ save_lam) {
     constexpr int DK = Cfg::DK, DV = Cfg::DV, DVT = Cfg::DVT, SW = Cfg::SW, NSW = Cfg::NSW;
     constexpr int NL = REV ? 1 : 0;    // chunk-start lam requests per round
-    constexpr int NI = TI ? 4 : 8;     // staging loads of the per-token key-side inputs per round
+    // staging loads of the per-token key-side inputs per round: two per staged tensor
+    constexpr int NI = 2 * ((TI ? 0 : 2) + 1 + (NOQ ? 0 : 1));
+    static_assert(!(NOQ && YV), "the readout variance needs the query");
     const int H = sc.H, h = sc.h, T = sc.T, nchunk = sc.nchunk;
     const int sl = lane % SW, hf = lane / SW;   // key slot within the wave, half of the chunk
     const int n = wave * SW + sl;
@@ -285,7 +290,7 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             one(sc.p, 1);
         }
         one(sc.k, 2);
-        one(sc.q, 3);
+        if constexpr (!NOQ) one(sc.q, 3);
         const rsrc_t rr = make_rsrc(sc.r + (sc.seq0 + t0) * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
         buf_ld16_lds(rr, rw + bb * 64, (uint32_t)lane * H * 2);
         if constexpr (REV) {
@@ -334,9 +339,9 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             const uint16_t* stg = reinterpret_cast<const uint16_t*>(stw) + bb * 4 * kC * SW;
             const uint32_t* rwc = rw + bb * 64;
             if (nt == kC)
-                x = scan_chunk<SW, Cfg::LQ, YV, true, TI>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
+                x = scan_chunk<SW, Cfg::LQ, YV, true, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
             else
-                x = scan_chunk<SW, Cfg::LQ, YV, false, TI>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
+                x = scan_chunk<SW, Cfg::LQ, YV, false, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
             // the value tile has landed (younger: the NI + 1 + NL staging loads)
             wait_vm_le<NI + 1 + NL>();
         }
