@@ -45,14 +45,20 @@ CALLS_OU = {
 SUMMARY_KEY = "traffic_bytes_per_call"
 
 
+# the sources the measured calls are built from: the ABI layer, the shared
+# headers and the chunked kernels (and the OU parameter gradients)
+DIGEST_SOURCES = ("kla_api.cpp", "kla_internal.hpp", "kla_device.hpp", "kla_buf.hpp", "kla_mfma.hpp",
+                  "kla_chunk.hpp", "chunk_fwd.hip", "chunk_bwd_dv.hip", "chunk_bwd_dk.hip", "ou.hip",
+                  "validate.hip")
+
+
 def sources_digest() -> str:
-    """sha256 over the kernel sources (csrc/*.hip, *.hpp, *.cpp) in name order."""
+    """sha256 over the sources of the measured kernels, in name order."""
     h = hashlib.sha256()
-    for path in sorted(glob.glob(os.path.join(HERE, "csrc", "*"))):
-        if path.endswith((".hip", ".hpp", ".cpp", ".h")):
-            h.update(os.path.basename(path).encode())
-            with open(path, "rb") as f:
-                h.update(f.read())
+    for name in sorted(DIGEST_SOURCES):
+        h.update(name.encode())
+        with open(os.path.join(HERE, "csrc", name), "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 
