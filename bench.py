@@ -32,6 +32,9 @@ With --long it times the forward of the long-context workload (B = 1, H = 16,
 T = 65536, d = 128, bf16; heads 8..15 with slow decay), which has only 16
 sequences to spread over the chip.
 
+With --a5 it times forward + backward of the state-tracking workload (B = 64,
+H = 4, T = 512, d = 32, fp32 inputs: the token-recurrent kernels).
+
 With --block it times the block scaffolding around the layer at the same shape,
 forward + backward: the causal conv1d + SiLU over the C = H dk channels, the
 RMS QK-norm of q and of k (rows of dk) and the SiLU gate of the output, all
@@ -281,6 +284,57 @@ def bench_decode(args, dev):
     print(json.dumps(res), flush=True)
 
 
+def bench_a5(args, dev):
+    """kla_forward (saving the context) + kla_backward on the state-tracking workload (fp32)."""
+    import torch
+    import kla_inputs as K
+    import paper_2602_10743_amd as kla
+    w = K.WORKLOADS[1]
+    bits = K.full(w, as_bits=True)
+    x = {n: torch.from_numpy(np.ascontiguousarray(bits[n])).to(dev) for n in bits}
+    del bits
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], want_state=False, save=True)
+        if ev is not None:
+            ev[1].record(stream)
+        kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], None, None, x["dy"],
+                         saved=out["saved"], want_init_grads=False)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fwd_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    bwd_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    th = w.token_heads
+    fwd_b, bwd_b = algorithmic_bytes(w, 4)
+    dom, ms, nbytes = ("kla_backward", bwd_ms, bwd_b * th) if bwd_ms >= fwd_ms else ("kla_forward", fwd_ms, fwd_b * th)
+    achieved = nbytes / (ms * 1e-3) / 1e9
+    res = {
+        "metric": METRIC, "value": th / (wall / args.steps), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv, "pass": "fwd+bwd",
+                   "tokens_counted": "B*T*H"},
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes_per_call": nbytes,
+                     "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
+                     "note": "the working set fits the 256 MB last-level cache: cache-assisted"},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def bench_long(args, dev):
     """kla_forward (no saved context) on the long-context workload."""
     import torch
@@ -388,6 +442,7 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="decode step on the decode workload (with --pc: per-channel precision)")
     ap.add_argument("--long", action="store_true", help="forward of the long-context workload")
+    ap.add_argument("--a5", action="store_true", help="fwd+bwd of the state-tracking workload (fp32)")
     ap.add_argument("--block", action="store_true",
                     help="block scaffolding around the layer (conv + SiLU, QK-norm, gate), forward + backward")
     args = ap.parse_args()
@@ -408,6 +463,9 @@ def main():
         return
     if args.long:
         bench_long(args, dev)
+        return
+    if args.a5:
+        bench_a5(args, dev)
         return
     if args.pc:
         bench_pc(args, w, dev)

@@ -7,6 +7,7 @@
 // With OU parameters (ou_a set) every token of a head shares the gates of its
 // key slot, formed once per lane; the backward then sums the gate gradients of
 // a lane over its tokens into one part per batch row.
+#include "kla_buf.hpp"
 #include "kla_device.hpp"
 #include "kla_internal.hpp"
 
@@ -14,22 +15,86 @@ namespace kla {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTB = 16;  // tokens per LDS block in the forward
+constexpr int kTB = 16;  // tokens per staged block (forward, sweep 1)
+
+// Per-token inputs reach the kernels in blocks of ROWS tokens, staged in LDS as
+// rows of floats.  A Part is one tensor's W values per token: each thread
+// fetches elements tid + kThreads m of the next block into registers while the
+// current block is worked on, and writes them to their LDS columns once that
+// block is done, so a token's loads never wait in its recursion.  The kernels
+// synchronise with barrier_lds (LDS ordering only): a full __syncthreads would
+// wait for the prefetch at the first barrier after it is issued.
+template <int ROWS, int W>
+struct Part {
+    static constexpr int N = (ROWS * W + kThreads - 1) / kThreads;
+    float x[N];
+    // rows j < nt (nt >= 1): element c of row j at x0[j * ts + c].  Rows past nt and
+    // elements past the block re-read the last valid element: they are never used,
+    // and the loads stay unconditional, so nothing waits for them before the commit.
+    template <typename T>
+    __device__ __forceinline__ void fetch(const T* x0, int ts, int nt) {
+#pragma unroll
+        for (int m = 0; m < N; ++m) {
+            const int e = min((int)threadIdx.x + kThreads * m, ROWS * W - 1);
+            const int j = min(e / W, nt - 1), c = e % W;
+            x[m] = ld(x0, (size_t)(j * ts + c));
+        }
+    }
+    // row j of the block into dst[j * ROW + c0 + c]
+    template <int ROW>
+    __device__ __forceinline__ void commit(float* dst, int c0) const {
+#pragma unroll
+        for (int m = 0; m < N; ++m) {
+            const int e = (int)threadIdx.x + kThreads * m;
+            const int j = e / W, c = e % W;
+            if (e < ROWS * W) dst[j * ROW + c0 + c] = x[m];
+        }
+    }
+};
+
+// Reciprocal on v_rcp_f32 (about 1 ulp), as in the chunked kernels: the IEEE division
+// sequence would lengthen the per-token precision chain several times over.
+__device__ __forceinline__ float rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
+// Sum over groups of W consecutive lanes with DPP moves.  W = 16: every lane of
+// a 16-lane row holds the row sum.  W = 32: the sum of each half wave lands in
+// its upper 16 lanes (16..31, 48..63).
+template <int W>
+__device__ __forceinline__ float group_sum(float x) {
+    static_assert(W == 16 || W == 32, "group width");
+    x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
+    x += dpp<0x4E, 0xf>(x);    // quad_perm [2,3,0,1]
+    x += dpp<0x141, 0xf>(x);   // row_half_mirror
+    x += dpp<0x140, 0xf>(x);   // row_mirror
+    if constexpr (W == 32) x += dpp<0x142, 0xa>(x);   // row_bcast:15 into rows 1 and 3
+    return x;
+}
+
+// value channels per forward workgroup: 16, so that even a small head spreads over
+// several workgroups (each walks the precision of the head itself)
+template <int DV>
+constexpr int kFwdDVT = DV < 16 ? DV : 16;
 
 // ----------------------------------------------------------------------------
 // Forward.  One workgroup per (b, h, value tile of DVT channels).  Threads
 // tid < DK own the precision lane n = tid; every thread owns H[n, d] for
-// n = ng + i*NG and one channel d = d0 + dl.
+// n = ng + i*NG and one channel d = d0 + dl.  Per block of kTB tokens: the
+// precision lanes walk the block and leave F, r k, q / lam and q^2 / lam in the
+// staged rows; then every thread updates its state entries over the block and
+// the readout partials are summed.
 template <typename S, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArgs g) {
     using T_ = typename storage<S>::type;
-    constexpr int DVT = DV < 32 ? DV : 32;
+    constexpr int DVT = kFwdDVT<DV>;
     constexpr int NTILE = DV / DVT;
     constexpr int NG = kThreads / DVT;
     constexpr int NPER = DK / NG > 0 ? DK / NG : 1;
     static_assert(DK % NG == 0 || NG > DK, "key width must be a multiple of the n-groups");
+    // staged row of a token: abar, pbar, k, q [DK] each, this tile's v [DVT], r
+    constexpr int CA = 0, CP = DK, CK = 2 * DK, CQ = 3 * DK, CV = 4 * DK, CR = CV + DVT, ROW = CR + 1;
+    constexpr int NY = (kTB * DVT + kThreads - 1) / kThreads;   // outputs per thread and block
 
-    __shared__ float sF[kTB][DK], sKh[kTB][DK], sQt[kTB][DK], sW[kTB][DK];
+    __shared__ float sIn[kTB * ROW];
     __shared__ float sRed[kTB][NG][DVT];
 
     const T_* q = static_cast<const T_*>(g.q);
@@ -47,6 +112,7 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
     const int dl = tid % DVT, ng = tid / DVT;
     const int d = tile * DVT + dl;
     const bool owns = ng < DK;  // with NG > DK some n-groups are idle
+    const size_t row0 = (size_t)b * s.T;
 
     float Hs[NPER];
 #pragma unroll
@@ -60,53 +126,114 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
     float oa = 0.f, op = 0.f;
     if (ou && tid < DK) ou_gates(g.ou_a[h * DK + tid], g.ou_p[h * DK + tid], g.ou_d[h * DK + tid], oa, op);
 
-    for (int t0 = 0; t0 < s.T; t0 += kTB) {
-        const int nt = min(kTB, s.T - t0);
+    Part<kTB, DK> xa, xp, xk, xq;
+    Part<kTB, DVT> xv;
+    Part<kTB, 1> xr;
+    // with OU gates the abar / pbar columns are filled from k and not used
+    const T_* ga = ou ? k : a;
+    const T_* gp = ou ? k : p;
+    auto fetch = [&](int t) {
+        const int nt = min(kTB, s.T - t);
+        const size_t o = (row0 + t) * s.H + h;
+        xa.fetch(ga + o * DK, s.H * DK, nt);
+        xp.fetch(gp + o * DK, s.H * DK, nt);
+        xk.fetch(k + o * DK, s.H * DK, nt);
+        xq.fetch(q + o * DK, s.H * DK, nt);
+        xv.fetch(v + o * DV + tile * DVT, s.H * DV, nt);
+        xr.fetch(r + o, s.H, nt);
+    };
+    auto commit = [&]() {
+        wait_vm_all();   // the prefetch has landed (and stores issued before it are done)
+        xa.template commit<ROW>(sIn, CA);
+        xp.template commit<ROW>(sIn, CP);
+        xk.template commit<ROW>(sIn, CK);
+        xq.template commit<ROW>(sIn, CQ);
+        xv.template commit<ROW>(sIn, CV);
+        xr.template commit<ROW>(sIn, CR);
+    };
+
+    // Block blk is worked on from LDS while block blk + 1 is in registers; after its
+    // outputs are formed, block blk + 1 goes to LDS, the outputs are stored and block
+    // blk + 2 is fetched.  The fetch comes last: rewriting a register that an in-flight
+    // store reads waits for that store, and with the loads issued after the stores such a
+    // wait does not also wait for the prefetch.  Fetches past the end fetch the last block
+    // again (unused), so they stay unconditional.
+    const int nblk = (s.T + kTB - 1) / kTB;
+    wait_vm_all();   // the initial state is in: no first-use wait inside the loop
+    if (nblk > 0) {
+        fetch(0);
+        commit();
+        fetch(min(1, nblk - 1) * kTB);
+    }
+    barrier_lds();
+    for (int blk = 0; blk < nblk; ++blk) {
+        const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
         if (tid < DK) {
-            for (int j = 0; j < nt; ++j) {
-                const size_t base = ((size_t)b * s.T + t0 + j) * s.H + h;
-                const float at = ou ? oa : ld(a, base * DK + tid), pt = ou ? op : ld(p, base * DK + tid);
-                const float kt = ld(k, base * DK + tid), qt = ld(q, base * DK + tid);
-                const float rt = ld(r, base);
-                const float rho = 1.f / (at * at + pt * lam);
-                sF[j][tid] = at * rho;
-                lam = rho * lam + kt * kt * rt;
-                const float inv = 1.f / lam;
-                sKh[j][tid] = rt * kt;
-                sQt[j][tid] = qt * inv;
-                sW[j][tid] = qt * qt * inv;
-            }
-        }
-        __syncthreads();
-        for (int j = 0; j < nt; ++j) {
-            const size_t base = ((size_t)b * s.T + t0 + j) * s.H + h;
-            const float vd = ld(v, base * DV + d);
-            float acc = 0.f;
 #pragma unroll
-            for (int i = 0; i < NPER; ++i) {
-                const int n = ng + i * NG;
-                if (owns) {
-                    Hs[i] = sF[j][n] * Hs[i] + sKh[j][n] * vd;
-                    acc += sQt[j][n] * Hs[i];
+            for (int j = 0; j < kTB; ++j) {
+                if (j < nt) {
+                    float* row = sIn + j * ROW;
+                    const float ra = row[CA + tid], rp = row[CP + tid];
+                    const float at = ou ? oa : ra, pt = ou ? op : rp;
+                    const float kt = row[CK + tid], qt = row[CQ + tid], rt = row[CR];
+                    const float rho = rcp(at * at + pt * lam);
+                    lam = rho * lam + kt * kt * rt;
+                    const float inv = rcp(lam);
+                    row[CA + tid] = at * rho;
+                    row[CP + tid] = rt * kt;
+                    row[CK + tid] = qt * inv;
+                    row[CQ + tid] = qt * qt * inv;
                 }
             }
-            sRed[j][ng][dl] = acc;
         }
-        __syncthreads();
-        for (int idx = tid; idx < nt * DVT; idx += kThreads) {
-            const int j = idx / DVT, dd = idx % DVT;
+        barrier_lds();
+#pragma unroll 2
+        for (int j = 0; j < kTB; ++j) {
+            if (j < nt) {
+                const float* row = sIn + j * ROW;
+                const float vd = row[CV + dl];
+                float acc = 0.f;
+#pragma unroll
+                for (int i = 0; i < NPER; ++i) {
+                    const int n = ng + i * NG;
+                    if (owns) {
+                        Hs[i] = row[CA + n] * Hs[i] + row[CP + n] * vd;
+                        acc += row[CK + n] * Hs[i];
+                    }
+                }
+                sRed[j][ng][dl] = acc;
+            }
+        }
+        barrier_lds();
+        // the block's outputs are formed in registers and stored after the commit, whose wait
+        // then covers the prefetch only
+        float yo[NY], yvo = 0.f;
+#pragma unroll
+        for (int u = 0; u < NY; ++u) {
+            const int idx = tid + kThreads * u, j = idx / DVT, dd = idx % DVT;
             float acc = 0.f;
-            for (int gi = 0; gi < NG; ++gi) acc += sRed[j][gi][dd];
-            const size_t base = ((size_t)b * s.T + t0 + j) * s.H + h;
-            st(y, base * DV + tile * DVT + dd, acc);
+            if (j < nt) {
+#pragma unroll
+                for (int gi = 0; gi < NG; ++gi) acc += sRed[j][gi][dd];
+            }
+            yo[u] = acc;
         }
-        if (tile == 0 && g.yvar && tid >= kThreads - kTB && tid - (kThreads - kTB) < nt) {
-            const int j = tid - (kThreads - kTB);
-            float acc = 0.f;
-            for (int n = 0; n < DK; ++n) acc += sW[j][n];
-            g.yvar[((size_t)b * s.T + t0 + j) * s.H + h] = acc;
+        const int jv = tid - (kThreads - kTB);   // the token whose readout variance this thread sums
+        const bool wv = tile == 0 && g.yvar && jv >= 0 && jv < nt;
+        if (wv) {
+#pragma unroll
+            for (int n = 0; n < DK; ++n) yvo += sIn[jv * ROW + CQ + n];
         }
-        __syncthreads();
+        barrier_lds();
+        commit();
+#pragma unroll
+        for (int u = 0; u < NY; ++u) {
+            const int idx = tid + kThreads * u, j = idx / DVT, dd = idx % DVT;
+            if (j < nt) st(y, ((row0 + t0 + j) * s.H + h) * DV + tile * DVT + dd, yo[u]);
+        }
+        if (wv) g.yvar[(row0 + t0 + jv) * s.H + h] = yvo;
+        fetch(min(blk + 2, nblk - 1) * kTB);
+        barrier_lds();
     }
     if (tile == 0 && g.lamT && tid < DK) g.lamT[(size_t)bh * DK + tid] = lam;
     if (g.etaT && owns) {
@@ -125,6 +252,11 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
                                                                float* wdqt, float* wPT) {
     using T_ = typename storage<S>::type;
     constexpr int NT = 16, DL = 16, DPER = DV / DL;
+    static_assert(DL == kTB, "lane j of a slot's row holds token j of the block");
+    // staged row of a token: abar, pbar, k of this workgroup's NT key slots, v [DV], dy [DV], r
+    constexpr int CA = 0, CP = NT, CK = 2 * NT, CV = 3 * NT, CD = CV + DV, CR = CD + DV, ROW = CR + 1;
+    __shared__ float sIn[kTB * ROW];
+
     const T_* k = static_cast<const T_*>(g.k);
     const T_* v = static_cast<const T_*>(g.v);
     const T_* a = static_cast<const T_*>(g.a);
@@ -133,10 +265,11 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     const T_* dy = static_cast<const T_*>(g.dy);
 
     const int ntile = DK / NT;
-    const int bh = blockIdx.x / ntile, nt = blockIdx.x % ntile;
+    const int bh = blockIdx.x / ntile, ktile = blockIdx.x % ntile;
     const int b = bh / s.H, h = bh % s.H;
     const int tid = threadIdx.x;
-    const int n = nt * NT + tid / DL, dl = tid % DL;
+    const int nl = tid / DL, n = ktile * NT + nl, dl = tid % DL;
+    const size_t row0 = (size_t)b * s.T;
 
     float Hs[DPER];
 #pragma unroll
@@ -147,35 +280,83 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     float oa = 0.f, op = 0.f;
     if (ou) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], oa, op);
 
-    for (int t = 0; t < s.T; ++t) {
-        const size_t base = ((size_t)b * s.T + t) * s.H + h;
-        const float at = ou ? oa : ld(a, base * DK + n), pt = ou ? op : ld(p, base * DK + n);
-        const float kt = ld(k, base * DK + n);
-        const float rt = ld(r, base);
-        const float rho = 1.f / (at * at + pt * lam);
-        const float F = at * rho, kh = rt * kt;
-        lam = rho * lam + kt * kt * rt;
-        float acc = 0.f;
+    Part<kTB, NT> xa, xp, xk;
+    Part<kTB, DV> xv, xdy;
+    Part<kTB, 1> xr;
+    // with OU gates the abar / pbar columns are filled from k and not used
+    const T_* ga = ou ? k : a;
+    const T_* gp = ou ? k : p;
+    auto fetch = [&](int t) {
+        const int nt = min(kTB, s.T - t);
+        const size_t o = (row0 + t) * s.H + h;
+        xa.fetch(ga + o * DK + ktile * NT, s.H * DK, nt);
+        xp.fetch(gp + o * DK + ktile * NT, s.H * DK, nt);
+        xk.fetch(k + o * DK + ktile * NT, s.H * DK, nt);
+        xv.fetch(v + o * DV, s.H * DV, nt);
+        xdy.fetch(dy + o * DV, s.H * DV, nt);
+        xr.fetch(r + o, s.H, nt);
+    };
+    auto commit = [&]() {
+        wait_vm_all();   // the prefetch has landed (and stores issued before it are done)
+        xa.template commit<ROW>(sIn, CA);
+        xp.template commit<ROW>(sIn, CP);
+        xk.template commit<ROW>(sIn, CK);
+        xv.template commit<ROW>(sIn, CV);
+        xdy.template commit<ROW>(sIn, CD);
+        xr.template commit<ROW>(sIn, CR);
+    };
+
+    // blocks staged as in the forward: blk from LDS, blk + 1 in registers
+    const int nblk = (s.T + kTB - 1) / kTB;
+    wait_vm_all();   // the initial state is in: no first-use wait inside the loop
+    if (nblk > 0) {
+        fetch(0);
+        commit();
+        fetch(min(1, nblk - 1) * kTB);
+    }
+    barrier_lds();
+    for (int blk = 0; blk < nblk; ++blk) {
+        const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
+        float olam = 0.f, odqt = 0.f;
+#pragma unroll 2
+        for (int j = 0; j < kTB; ++j) {
+            if (j < nt) {
+                const float* row = sIn + j * ROW;
+                const float ra = row[CA + nl], rp = row[CP + nl];
+                const float at = ou ? oa : ra, pt = ou ? op : rp;
+                const float kt = row[CK + nl], rt = row[CR];
+                const float rho = rcp(at * at + pt * lam);
+                const float F = at * rho, kh = rt * kt;
+                lam = rho * lam + kt * kt * rt;
+                float acc = 0.f;
 #pragma unroll
-        for (int i = 0; i < DPER; ++i) {
-            const size_t o = base * DV + dl + i * DL;
-            Hs[i] = F * Hs[i] + kh * ld(v, o);
-            acc += Hs[i] * ld(dy, o);
+                for (int i = 0; i < DPER; ++i) {
+                    Hs[i] = F * Hs[i] + kh * row[CV + dl + i * DL];
+                    acc += Hs[i] * row[CD + dl + i * DL];
+                }
+                acc = group_sum<16>(acc);
+                if (dl == j) {   // lane j of the slot's row keeps token j's results
+                    olam = lam;
+                    odqt = acc;
+                }
+            }
         }
-#pragma unroll
-        for (int off = DL / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, DL);
-        if (dl == 0) {
-            wlam[base * DK + n] = lam;
-            wdqt[base * DK + n] = acc;
+        barrier_lds();
+        commit();
+        if (dl < nt) {
+            const size_t o = ((row0 + t0 + dl) * s.H + h) * DK + n;
+            wlam[o] = olam;
+            wdqt[o] = odqt;
         }
+        fetch(min(blk + 2, nblk - 1) * kTB);
+        barrier_lds();
     }
     float acc = 0.f;
     if (g.detaT) {
 #pragma unroll
         for (int i = 0; i < DPER; ++i) acc += g.detaT[((size_t)bh * DK + n) * DV + dl + i * DL] * Hs[i];
     }
-#pragma unroll
-    for (int off = DL / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off, DL);
+    acc = group_sum<16>(acc);
     if (dl == 0) wPT[(size_t)bh * DK + n] = acc;
 }
 
@@ -190,17 +371,54 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
 //            (gv_t: upstream gradient of the readout variance, zero if none)
 //   c_{t-1}= abar_t^2 rho_t^2 g_t - pbar_t rho_t dG_t
 // and the input gradients follow by the chain rule through rho, lam and F.
+// Per block of TB tokens (latest block first):
+//   A  every (token, slot): rho, F, qt, kh and the coefficients of the c/g/dG
+//      recursion, in parallel;
+//   B  every thread: its dH entries over the block's tokens (latest first),
+//      with the dkh sums (DPP) and dv partials per token;
+//   C  one lane per slot: the dG / g / c recursion over the block;
+//   D  every (token, slot): dq, dk, dabar, dpbar and the dr terms; dv sums;
+//   E  dr sums, and the next block's inputs go to LDS.
+template <int DK, int DV>
+struct Sweep2Cfg {
+    static constexpr int DVT = DV < 32 ? DV : 32, NG = kThreads / DVT;
+    static constexpr int NPER = DK / NG, DPER = DV / DVT;
+    static_assert(NG <= DK && DK % NG == 0, "every thread owns dH entries");
+    // staged row of token t: lam_t, dqt_t, q, k, abar, pbar [DK] each; v, dy [DV]; r; the
+    // upstream gradient of the readout variance
+    static constexpr int CL = 0, CDQ = DK, CQ = 2 * DK, CK = 3 * DK, CA = 4 * DK, CP = 5 * DK;
+    static constexpr int CV = 6 * DK, CD = CV + DV, CR = CD + DV, CG = CR + 1, ROW = CG + 1;
+    static constexpr int TB = ROW * 16 * 4 <= 48 * 1024 ? 16 : 8;
+    // LDS, in floats: staged rows, then lam of the token before the block; {F_{t+1}, qt, kh,
+    // rho} and {(abar rho)^2, pbar rho, q (dqt + q gv) / lam^2, qt dqt} per (token, slot);
+    // dkh; dv partials per n-group; {dG, g} per (token, slot); dr terms; the carried forget
+    // gate (two buffers); per-thread OU sums
+    static constexpr int L_LP = TB * ROW, L_C0 = (L_LP + DK + 3) / 4 * 4, L_C1 = L_C0 + 4 * TB * DK;
+    static constexpr int L_PK = L_C1 + 4 * TB * DK, L_PV = L_PK + TB * DK, L_SG = L_PV + TB * NG * DV;
+    static constexpr int L_DR = L_SG + 2 * TB * DK, L_FC = L_DR + TB * DK, L_OU = L_FC + 2 * DK;
+    static constexpr size_t BYTES = (size_t)(L_OU + 2 * kThreads) * sizeof(float);
+    static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
+};
+
 template <typename S, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g, const float* wlam,
                                                                const float* wdqt, const float* wPT) {
     using T_ = typename storage<S>::type;
-    constexpr int DVT = DV < 32 ? DV : 32;
-    constexpr int NG = kThreads / DVT;
-    constexpr int NPER = DK / NG > 0 ? DK / NG : 1;
-    constexpr int DPER = DV / DVT;
-    __shared__ float sQt[DK], sKh[DK], sFn[DK], sV[DV], sDy[DV], sDR[DK];
-    __shared__ float sPK[DK][DVT + 1];
-    __shared__ float sPV[NG][DV];
+    using C = Sweep2Cfg<DK, DV>;
+    constexpr int DVT = C::DVT, NG = C::NG, NPER = C::NPER, DPER = C::DPER, TB = C::TB, ROW = C::ROW;
+    constexpr int ND = TB * DK / kThreads, NDV = (TB * DV + kThreads - 1) / kThreads;   // items per thread
+    static_assert(ND * kThreads == TB * DK, "(token, slot) items split evenly over the threads");
+    extern __shared__ __align__(16) float sm[];
+    float* sIn = sm;
+    float* sLP = sm + C::L_LP;    // [DK]
+    float* sC0 = sm + C::L_C0;    // [TB][DK][4]
+    float* sC1 = sm + C::L_C1;    // [TB][DK][4]
+    float* sPK = sm + C::L_PK;    // [TB][DK]
+    float* sPV = sm + C::L_PV;    // [TB][NG][DV]
+    float* sSG = sm + C::L_SG;    // [TB][DK][2]
+    float* sDR = sm + C::L_DR;    // [TB][DK]
+    float* sFC = sm + C::L_FC;    // [2][DK]
+    float* sOU = sm + C::L_OU;    // [2][kThreads]
 
     const T_* q = static_cast<const T_*>(g.q);
     const T_* k = static_cast<const T_*>(g.k);
@@ -220,116 +438,250 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
     const int b = bh / s.H, h = bh % s.H;
     const int tid = threadIdx.x;
     const int dl = tid % DVT, ng = tid / DVT;
-    const bool owns = ng < DK;
+    const int nme = tid % DK;   // the key slot of this thread's (token, slot) items
+    const size_t row0 = (size_t)b * s.T;
 
     float dH[NPER][DPER];
 #pragma unroll
     for (int i = 0; i < NPER; ++i)
 #pragma unroll
         for (int j = 0; j < DPER; ++j)
-            dH[i][j] = (owns && g.detaT) ? g.detaT[((size_t)bh * DK + ng + i * NG) * DV + dl + j * DVT] : 0.f;
+            dH[i][j] = g.detaT ? g.detaT[((size_t)bh * DK + ng + i * NG) * DV + dl + j * DVT] : 0.f;
 
-    // per-slot scalars, live in threads tid < DK
-    float Fnext = 1.f, cnext = 0.f, Sg = 0.f;
-    const bool ou = g.ou_a != nullptr;
-    float oa = 0.f, op = 0.f, sum_da = 0.f, sum_dp = 0.f;
+    // the dG / c recursion lives in threads tid < DK
+    float cnext = 0.f, Sg = 0.f;
     if (tid < DK) {
         cnext = g.dlamT ? g.dlamT[(size_t)bh * DK + tid] : 0.f;
         Sg = wPT[(size_t)bh * DK + tid];
-        if (ou) ou_gates(g.ou_a[h * DK + tid], g.ou_p[h * DK + tid], g.ou_d[h * DK + tid], oa, op);
+        sFC[DK + tid] = 1.f;   // no forget gate after the last token
     }
+    const bool ou = g.ou_a != nullptr;
+    float oa = 0.f, op = 0.f, sum_da = 0.f, sum_dp = 0.f;
+    if (ou) ou_gates(g.ou_a[h * DK + nme], g.ou_p[h * DK + nme], g.ou_d[h * DK + nme], oa, op);
 
-    for (int t = s.T - 1; t >= 0; --t) {
-        const size_t base = ((size_t)b * s.T + t) * s.H + h;
-        float lam_t = 0.f, dqt = 0.f, qt = 0.f, kt = 0.f, rt = 0.f;
-        if (tid < DK) {
-            lam_t = wlam[base * DK + tid];
-            dqt = wdqt[base * DK + tid];
-            qt = ld(q, base * DK + tid);
-            kt = ld(k, base * DK + tid);
-            rt = ld(r, base);
-            sQt[tid] = qt / lam_t;
-            sKh[tid] = rt * kt;
-            sFn[tid] = Fnext;
-        }
-        for (int i = tid; i < DV; i += kThreads) {
-            sV[i] = ld(v, base * DV + i);
-            sDy[i] = ld(dy, base * DV + i);
-        }
-        __syncthreads();
-        float pv[DPER];
-#pragma unroll
-        for (int j = 0; j < DPER; ++j) pv[j] = 0.f;
-#pragma unroll
-        for (int i = 0; i < NPER; ++i) {
-            const int n = ng + i * NG;
-            if (!owns) break;
-            float pk = 0.f;
-#pragma unroll
-            for (int j = 0; j < DPER; ++j) {
-                const int dd = dl + j * DVT;
-                dH[i][j] = sFn[n] * dH[i][j] + sQt[n] * sDy[dd];
-                pk += dH[i][j] * sV[dd];
-                pv[j] += dH[i][j] * sKh[n];
+    Part<TB, DK> xl, xdq, xq, xk, xa, xp;
+    Part<TB, DV> xv, xdy;
+    Part<TB, 1> xr, xg;
+    Part<1, DK> xlp;
+    // Loads stay unconditional: absent tensors are replaced by present ones whose values
+    // are not used (OU gates: abar / pbar columns from k; no readout-variance gradient:
+    // its column from lam, scaled by zero; no initial precision: token 0's lam_{t-1}
+    // from lam_0, replaced by 1 where it is read).
+    const T_* ga = ou ? k : a;
+    const T_* gp = ou ? k : p;
+    const float* gvar = g.dyvar ? g.dyvar : wlam;
+    const float gscale = g.dyvar ? 1.f : 0.f;
+    const float* glam0 = g.lam0 ? g.lam0 + (size_t)bh * DK : wlam + (row0 * s.H + h) * DK;
+    const bool lam0_one = g.lam0 == nullptr;
+    auto fetch = [&](int t) {
+        const int nt = min(TB, s.T - t);
+        const size_t o = (row0 + t) * s.H + h;
+        const int ts = s.H * DK;
+        xl.fetch(wlam + o * DK, ts, nt);
+        xdq.fetch(wdqt + o * DK, ts, nt);
+        xq.fetch(q + o * DK, ts, nt);
+        xk.fetch(k + o * DK, ts, nt);
+        xa.fetch(ga + o * DK, ts, nt);
+        xp.fetch(gp + o * DK, ts, nt);
+        xv.fetch(v + o * DV, s.H * DV, nt);
+        xdy.fetch(dy + o * DV, s.H * DV, nt);
+        xr.fetch(r + o, s.H, nt);
+        xg.fetch(gvar + (g.dyvar ? o : o * DK), g.dyvar ? s.H : ts, nt);
+        xlp.fetch(t > 0 ? wlam + (o - s.H) * DK : glam0, 0, 1);
+    };
+    auto commit = [&]() {
+        wait_vm_all();   // the prefetch has landed (and stores issued before it are done)
+        xl.template commit<ROW>(sIn, C::CL);
+        xdq.template commit<ROW>(sIn, C::CDQ);
+        xq.template commit<ROW>(sIn, C::CQ);
+        xk.template commit<ROW>(sIn, C::CK);
+        xa.template commit<ROW>(sIn, C::CA);
+        xp.template commit<ROW>(sIn, C::CP);
+        xv.template commit<ROW>(sIn, C::CV);
+        xdy.template commit<ROW>(sIn, C::CD);
+        xr.template commit<ROW>(sIn, C::CR);
+        xg.template commit<ROW>(sIn, C::CG);
+        xlp.template commit<DK>(sLP, 0);
+    };
+
+    // blocks staged as in the forward, latest first: blk from LDS, blk - 1 in registers
+    const int nblk = (s.T + TB - 1) / TB;
+    wait_vm_all();   // the initial state is in: no first-use wait inside the loop
+    if (nblk > 0) {
+        fetch((nblk - 1) * TB);
+        commit();
+        fetch(max(nblk - 2, 0) * TB);
+    }
+    int cur = 1;   // sFC buffer holding F of the token after the current block
+    barrier_lds();
+    for (int blk = nblk - 1; blk >= 0; --blk) {
+        const int t0 = blk * TB, nt = min(TB, s.T - t0);
+        // ---- A
+        for (int idx = tid; idx < TB * DK; idx += kThreads) {
+            const int j = idx / DK, n = idx % DK;
+            if (j < nt) {
+                const float* row = sIn + j * ROW;
+                const float lam = row[C::CL + n];
+                const float lp = j > 0 ? row[C::CL + n - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[n]);
+                const float dqt = row[C::CDQ + n], qv = row[C::CQ + n], kv = row[C::CK + n];
+                const float ra = row[C::CA + n], rp = row[C::CP + n];
+                const float at = ou ? oa : ra, pt = ou ? op : rp;
+                const float rt = row[C::CR], gv = gscale * row[C::CG];
+                const float rho = rcp(at * at + pt * lp);
+                const float il = rcp(lam), qtl = qv * il, F = at * rho;
+                float* c0 = sC0 + 4 * (j * DK + n);
+                c0[1] = qtl;
+                c0[2] = rt * kv;
+                c0[3] = rho;
+                if (j > 0) sC0[4 * ((j - 1) * DK + n)] = F;
+                else sFC[(cur ^ 1) * DK + n] = F;
+                if (j == nt - 1) c0[0] = sFC[cur * DK + n];
+                *reinterpret_cast<float4*>(sC1 + 4 * (j * DK + n)) =
+                    make_float4(F * F, pt * rho, qv * (dqt + qv * gv) * il * il, qtl * dqt);
             }
-            sPK[n][dl] = pk;
+        }
+        barrier_lds();
+        // ---- B
+#pragma unroll 2
+        for (int j = TB - 1; j >= 0; --j) {
+            if (j < nt) {
+                const float* row = sIn + j * ROW;
+                float dyd[DPER], vd[DPER], pv[DPER];
+#pragma unroll
+                for (int jd = 0; jd < DPER; ++jd) {
+                    dyd[jd] = row[C::CD + dl + jd * DVT];
+                    vd[jd] = row[C::CV + dl + jd * DVT];
+                    pv[jd] = 0.f;
+                }
+#pragma unroll
+                for (int i = 0; i < NPER; ++i) {
+                    const int n = ng + i * NG;
+                    const float4 co = *reinterpret_cast<const float4*>(sC0 + 4 * (j * DK + n));
+                    float pk = 0.f;
+#pragma unroll
+                    for (int jd = 0; jd < DPER; ++jd) {
+                        dH[i][jd] = co.x * dH[i][jd] + co.y * dyd[jd];
+                        pk += dH[i][jd] * vd[jd];
+                        pv[jd] += dH[i][jd] * co.z;
+                    }
+                    pk = group_sum<DVT>(pk);
+                    if (dl == DVT - 1) sPK[j * DK + n] = pk;
+                }
+#pragma unroll
+                for (int jd = 0; jd < DPER; ++jd) sPV[(j * NG + ng) * DV + dl + jd * DVT] = pv[jd];
+            }
+        }
+        barrier_lds();
+        // ---- C
+        if (tid < DK) {
+#pragma unroll 4
+            for (int j = TB - 1; j >= 0; --j) {
+                if (j < nt) {
+                    const float kh = sC0[4 * (j * DK + tid) + 2];
+                    const float4 c1 = *reinterpret_cast<const float4*>(sC1 + 4 * (j * DK + tid));
+                    const float dkh = sPK[j * DK + tid];
+                    Sg += c1.w - kh * dkh;   // dG_t
+                    const float gl = cnext - c1.z;   // g_t
+                    *reinterpret_cast<float2*>(sSG + 2 * (j * DK + tid)) = make_float2(Sg, gl);
+                    cnext = c1.x * gl - c1.y * Sg;
+                }
+            }
+        }
+        barrier_lds();
+        // ---- D (results in registers: they are stored after the commit, whose wait then
+        // covers the prefetch only)
+        float o_dq[ND], o_dk[ND], o_da[ND], o_dp[ND], o_dv[NDV];
+#pragma unroll
+        for (int u = 0; u < ND; ++u) {
+            const int idx = tid + kThreads * u, j = idx / DK, n = idx % DK;
+            const float* row = sIn + j * ROW;
+            const float lam = row[C::CL + n];
+            const float lp = j > 0 ? row[C::CL + n - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[n]);
+            const float dqt = row[C::CDQ + n], qv = row[C::CQ + n], kv = row[C::CK + n];
+            const float ra = row[C::CA + n], rp = row[C::CP + n];
+            const float at = ou ? oa : ra, pt = ou ? op : rp;
+            const float rt = row[C::CR], gv = gscale * row[C::CG];
+            const float rho = sC0[4 * (j * DK + n) + 3];
+            const float dkh = sPK[j * DK + n];
+            const float2 sg = *reinterpret_cast<const float2*>(sSG + 2 * (j * DK + n));
+            const float qg = qv * gv;
+            const float drho = sg.y * lp + sg.x * (at * at + pt * lp);
+            o_dq[u] = (dqt + 2.f * qg) * rcp(lam);
+            o_dk[u] = rt * dkh + 2.f * kv * rt * sg.y;
+            o_da[u] = sg.x * rcp(at) - 2.f * at * rho * rho * drho;
+            o_dp[u] = -lp * rho * rho * drho;
+            if (j < nt) {
+                if (ou) {
+                    sum_da += o_da[u];
+                    sum_dp += o_dp[u];
+                }
+                sDR[j * DK + n] = kv * dkh + kv * kv * sg.y;
+            }
         }
 #pragma unroll
-        for (int j = 0; j < DPER; ++j) sPV[ng][dl + j * DVT] = pv[j];
-        __syncthreads();
-        if (tid < DK) {
-            float dkh = 0.f;
-            for (int i = 0; i < DVT; ++i) dkh += sPK[tid][i];
-            const float at = ou ? oa : ld(a, base * DK + tid), pt = ou ? op : ld(p, base * DK + tid);
-            const float lprev = t > 0 ? wlam[(base - s.H) * DK + tid] : (g.lam0 ? g.lam0[(size_t)bh * DK + tid] : 1.f);
-            const float qtl = sQt[tid], kh = sKh[tid];
-            const float qg = g.dyvar ? qt * g.dyvar[base] : 0.f;
-            Sg += qtl * dqt - kh * dkh;                       // dG_t
-            const float rho = 1.f / (at * at + pt * lprev);
-            const float gl = cnext - qt * (dqt + qg) / (lam_t * lam_t);  // g_t
-            const float drho = gl * lprev + Sg / rho;
-            st(dq, base * DK + tid, (dqt + 2.f * qg) / lam_t);
-            st(dk, base * DK + tid, rt * dkh + 2.f * kt * rt * gl);
-            const float dav = Sg / at - 2.f * at * rho * rho * drho, dpv = -lprev * rho * rho * drho;
-            if (ou) {
-                sum_da += dav;
-                sum_dp += dpv;
-            } else {
-                st(da, base * DK + tid, dav);
-                st(dp, base * DK + tid, dpv);
+        for (int u = 0; u < NDV; ++u) {
+            const int idx = tid + kThreads * u, j = idx / DV, dd = idx % DV;
+            float acc = 0.f;
+            if (j < nt) {
+#pragma unroll
+                for (int gi = 0; gi < NG; ++gi) acc += sPV[(j * NG + gi) * DV + dd];
             }
-            sDR[tid] = kt * dkh + kt * kt * gl;
-            cnext = at * at * rho * rho * gl - pt * rho * Sg;
-            Fnext = at * rho;
+            o_dv[u] = acc;
         }
-        if (tid < DV) {
+        barrier_lds();
+        // ---- E
+        commit();
+#pragma unroll
+        for (int u = 0; u < ND; ++u) {
+            const int idx = tid + kThreads * u, j = idx / DK, n = idx % DK;
+            if (j < nt) {
+                const size_t o = ((row0 + t0 + j) * s.H + h) * DK + n;
+                st(dq, o, o_dq[u]);
+                st(dk, o, o_dk[u]);
+                if (!ou) {
+                    st(da, o, o_da[u]);
+                    st(dp, o, o_dp[u]);
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < NDV; ++u) {
+            const int idx = tid + kThreads * u, j = idx / DV, dd = idx % DV;
+            if (j < nt && idx < TB * DV) st(dv, ((row0 + t0 + j) * s.H + h) * DV + dd, o_dv[u]);
+        }
+        if (tid < nt) {
             float acc = 0.f;
-            for (int gi = 0; gi < NG && gi < DK; ++gi) acc += sPV[gi][tid];
-            st(dv, base * DV + tid, acc);
+#pragma unroll
+            for (int n = 0; n < DK; ++n) acc += sDR[tid * DK + n];
+            st(dr, (row0 + t0 + tid) * s.H + h, acc);
         }
-        __syncthreads();
-        if (tid == 0) {
-            float acc = 0.f;
-            for (int n = 0; n < DK; ++n) acc += sDR[n];
-            st(dr, base, acc);
-        }
+        fetch(max(blk - 2, 0) * TB);
+        cur ^= 1;
+        barrier_lds();
     }
     if (tid < DK && g.dlam0) g.dlam0[(size_t)bh * DK + tid] = cnext;
-    if (ou && tid < DK) {   // part b of the token sums
-        const size_t np = (size_t)s.B * s.H * DK;
-        g.ou_part[(size_t)bh * DK + tid] = sum_da;
-        g.ou_part[np + (size_t)bh * DK + tid] = sum_dp;
+    if (ou) {   // part b of the token sums: the threads of one slot are combined in order
+        sOU[tid] = sum_da;
+        sOU[kThreads + tid] = sum_dp;
+        barrier_lds();
+        if (tid < DK) {
+            float sa = 0.f, sp = 0.f;
+            for (int i = tid; i < kThreads; i += DK) {
+                sa += sOU[i];
+                sp += sOU[kThreads + i];
+            }
+            const size_t np = (size_t)s.B * s.H * DK;
+            g.ou_part[(size_t)bh * DK + tid] = sa;
+            g.ou_part[np + (size_t)bh * DK + tid] = sp;
+        }
     }
-    __syncthreads();
-    if (tid < DK) sFn[tid] = Fnext;
-    __syncthreads();
-    if (g.deta0 && owns) {
+    if (g.deta0) {   // sFC[cur] holds F of token 0
 #pragma unroll
         for (int i = 0; i < NPER; ++i)
 #pragma unroll
             for (int j = 0; j < DPER; ++j) {
                 const int n = ng + i * NG;
-                g.deta0[((size_t)bh * DK + n) * DV + dl + j * DVT] = sFn[n] * dH[i][j];
+                g.deta0[((size_t)bh * DK + n) * DV + dl + j * DVT] = sFC[cur * DK + n] * dH[i][j];
             }
     }
 }
@@ -440,7 +792,7 @@ hipError_t dispatch(const Shape& s, A&&... args) {
 template <typename S, int DK, int DV>
 struct FwdL {
     static hipError_t run(const Shape& s, const FwdArgs& a, hipStream_t st) {
-        constexpr int DVT = DV < 32 ? DV : 32;
+        constexpr int DVT = kFwdDVT<DV>;
         const unsigned grid = (unsigned)(s.B * s.H * (DV / DVT));
         hipLaunchKernelGGL((fwd_recurrent_kernel<S, DK, DV>), dim3(grid), dim3(kThreads), 0, st, s, a);
         return hipGetLastError();
@@ -458,8 +810,13 @@ struct BwdL {
                            s, a, wlam, wdqt, wPT);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL((bwd_sweep2_kernel<S, DK, DV>), dim3(s.B * s.H), dim3(kThreads), 0, st, s, a,
-                           wlam, wdqt, wPT);
+        auto kern = bwd_sweep2_kernel<S, DK, DV>;
+        constexpr size_t bytes = Sweep2Cfg<DK, DV>::BYTES;
+        // more than 64 KiB of LDS must be opted into once per kernel (thread-safe static init)
+        static const hipError_t attr =
+            hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+        if (attr != hipSuccess) return attr;
+        hipLaunchKernelGGL(kern, dim3(s.B * s.H), dim3(kThreads), bytes, st, s, a, wlam, wdqt, wPT);
         return hipGetLastError();
     }
 };
