@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
             }
         }
         barrier_lds();
-#pragma unroll 2
+#pragma unroll
         for (int j = 0; j < kTB; ++j) {
             if (j < nt) {
                 const float* row = sIn + j * ROW;
@@ -318,7 +318,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     for (int blk = 0; blk < nblk; ++blk) {
         const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
         float olam = 0.f, odqt = 0.f;
-#pragma unroll 2
+#pragma unroll
         for (int j = 0; j < kTB; ++j) {
             if (j < nt) {
                 const float* row = sIn + j * ROW;
@@ -542,7 +542,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
         }
         barrier_lds();
         // ---- B
-#pragma unroll 2
+#pragma unroll
         for (int j = TB - 1; j >= 0; --j) {
             if (j < nt) {
                 const float* row = sIn + j * ROW;
