@@ -55,6 +55,8 @@ SMALL = [  # B, T, H, dk, dv, dtype, dist
     (1, 200, 2, 128, 128, "bf16", "lm"),
     (1, 33, 2, 16, 128, "bf16", "c0"),
     (3, 129, 2, 128, 128, "f32", "lm"),
+    (2, 47, 2, 64, 64, "f32", "lm"),
+    (1, 9, 1, 16, 32, "f32", "c0"),
     # chunked path at the other widths, partial chunks, a single short chunk, B*H not a multiple of 8
     (1, 97, 3, 32, 64, "bf16", "lm"),
     (2, 64, 1, 128, 32, "bf16", "lm"),
@@ -106,6 +108,27 @@ def test_backward_small(kla, B, T, H, dk, dv, dtype, dist):
         _check(n, to_np(gr[n]), ref[n], TOL[dtype], rep)
     _check("dlam0", to_np(gr["dlam0"]), ref["dlam0"], TOL[dtype], rep)
     _check("deta0", to_np(gr["deta0"]), ref["deta0"], TOL[dtype], rep)
+    log("  " + " ".join(rep))
+
+
+@pytest.mark.parametrize("dk,dv", [(32, 32), (128, 16)])
+def test_backward_default_belief_ragged(kla, dk, dv):
+    """Token-recurrent path without an initial belief, final-belief gradients or a
+    variance gradient, at a length that leaves a partial block."""
+    B, T, H = 2, 37, 3
+    case = K.random_case(B, T, H, dk, dv, "f32", seed=dk + dv, dist="c0")
+    log(f"backward defaults B{B} T{T} H{H} dk{dk} dv{dv} f32")
+    x = _dev_inputs(case, "f32")
+    out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], want_var=True)
+    gr = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], None, None, x["dy"])
+    torch.cuda.synchronize()
+    ref = oracle.forward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"])
+    rg = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], None, None, case["dy"])
+    rep = []
+    _check("y", to_np(out["y"]), ref["y"], TOL["f32"], rep)
+    _check("yvar", to_np(out["yvar"]), ref["yvar"], TOL["f32"], rep)
+    for n in ("dq", "dk", "dv", "da", "dp", "dr"):
+        _check(n, to_np(gr[n]), rg[n], TOL["f32"], rep)
     log("  " + " ".join(rep))
 
 
