@@ -24,9 +24,9 @@ constexpr int kTB = 16;  // tokens per staged block (forward, sweep 1)
 // block is done, so a token's loads never wait in its recursion.  The kernels
 // synchronise with barrier_lds (LDS ordering only): a full __syncthreads would
 // wait for the prefetch at the first barrier after it is issued.
-template <int ROWS, int W>
+template <int ROWS, int W, int NT = kThreads>
 struct Part {
-    static constexpr int N = (ROWS * W + kThreads - 1) / kThreads;
+    static constexpr int N = (ROWS * W + NT - 1) / NT;
     float x[N];
     // rows j < nt (nt >= 1): element c of row j at x0[j * ts + c].  Rows past nt and
     // elements past the block re-read the last valid element: they are never used,
@@ -35,7 +35,7 @@ struct Part {
     __device__ __forceinline__ void fetch(const T* x0, int ts, int nt) {
 #pragma unroll
         for (int m = 0; m < N; ++m) {
-            const int e = min((int)threadIdx.x + kThreads * m, ROWS * W - 1);
+            const int e = min((int)threadIdx.x + NT * m, ROWS * W - 1);
             const int j = min(e / W, nt - 1), c = e % W;
             x[m] = ld(x0, (size_t)(j * ts + c));
         }
@@ -45,7 +45,7 @@ struct Part {
     __device__ __forceinline__ void commit(float* dst, int c0) const {
 #pragma unroll
         for (int m = 0; m < N; ++m) {
-            const int e = (int)threadIdx.x + kThreads * m;
+            const int e = (int)threadIdx.x + NT * m;
             const int j = e / W, c = e % W;
             if (e < ROWS * W) dst[j * ROW + c0 + c] = x[m];
         }
@@ -379,11 +379,11 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
 //   C  one lane per slot: the dG / g / c recursion over the block;
 //   D  every (token, slot): dq, dk, dabar, dpbar and the dr terms; dv sums;
 //   E  dr sums, and the next block's inputs go to LDS.
-template <int DK, int DV>
-struct Sweep2Cfg {
-    static constexpr int DVT = DV < 32 ? DV : 32, NG = kThreads / DVT;
-    static constexpr int NPER = DK / NG, DPER = DV / DVT;
-    static_assert(NG <= DK && DK % NG == 0, "every thread owns dH entries");
+template <int DK, int DV, int NTH_>
+struct Sweep2Lay {
+    static constexpr int NTH = NTH_;
+    static constexpr int DVT = DV < 32 ? DV : 32, NG = NTH / DVT;
+    static constexpr int NPER = DK / NG > 0 ? DK / NG : 1, DPER = DV / DVT;
     // staged row of token t: lam_t, dqt_t, q, k, abar, pbar [DK] each; v, dy [DV]; r; the
     // upstream gradient of the readout variance
     static constexpr int CL = 0, CDQ = DK, CQ = 2 * DK, CK = 3 * DK, CA = 4 * DK, CP = 5 * DK;
@@ -396,18 +396,26 @@ struct Sweep2Cfg {
     static constexpr int L_LP = TB * ROW, L_C0 = (L_LP + DK + 3) / 4 * 4, L_C1 = L_C0 + 4 * TB * DK;
     static constexpr int L_PK = L_C1 + 4 * TB * DK, L_PV = L_PK + TB * DK, L_SG = L_PV + TB * NG * DV;
     static constexpr int L_DR = L_SG + 2 * TB * DK, L_FC = L_DR + TB * DK, L_OU = L_FC + 2 * DK;
-    static constexpr size_t BYTES = (size_t)(L_OU + 2 * kThreads) * sizeof(float);
-    static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
+    static constexpr size_t BYTES = (size_t)(L_OU + 2 * NTH) * sizeof(float);
+    static constexpr bool fits = NG <= DK && DK % NG == 0 && (TB * DK) % NTH == 0 && BYTES <= 160 * 1024;
+};
+
+// 512 threads (two waves per SIMD, half the dH entries per thread) for heads of up to
+// 64 x 64 where the shape splits evenly over them and the LDS fits, else 256
+template <int DK, int DV>
+struct Sweep2Cfg : Sweep2Lay<DK, DV, (DK * DV <= 64 * 64 && Sweep2Lay<DK, DV, 512>::fits) ? 512 : 256> {
+    static_assert(Sweep2Lay<DK, DV, Sweep2Cfg::NTH>::fits, "every thread owns dH entries; LDS budget");
 };
 
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g, const float* wlam,
+__global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Shape s, BwdArgs g, const float* wlam,
                                                                const float* wdqt, const float* wPT) {
     using T_ = typename storage<S>::type;
     using C = Sweep2Cfg<DK, DV>;
     constexpr int DVT = C::DVT, NG = C::NG, NPER = C::NPER, DPER = C::DPER, TB = C::TB, ROW = C::ROW;
-    constexpr int ND = TB * DK / kThreads, NDV = (TB * DV + kThreads - 1) / kThreads;   // items per thread
-    static_assert(ND * kThreads == TB * DK, "(token, slot) items split evenly over the threads");
+    constexpr int NTH = C::NTH;
+    constexpr int ND = TB * DK / NTH, NDV = (TB * DV + NTH - 1) / NTH;   // items per thread
+    static_assert(ND * NTH == TB * DK, "(token, slot) items split evenly over the threads");
     extern __shared__ __align__(16) float sm[];
     float* sIn = sm;
     float* sLP = sm + C::L_LP;    // [DK]
@@ -418,7 +426,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
     float* sSG = sm + C::L_SG;    // [TB][DK][2]
     float* sDR = sm + C::L_DR;    // [TB][DK]
     float* sFC = sm + C::L_FC;    // [2][DK]
-    float* sOU = sm + C::L_OU;    // [2][kThreads]
+    float* sOU = sm + C::L_OU;    // [2][NTH]
 
     const T_* q = static_cast<const T_*>(g.q);
     const T_* k = static_cast<const T_*>(g.k);
@@ -459,10 +467,10 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
     float oa = 0.f, op = 0.f, sum_da = 0.f, sum_dp = 0.f;
     if (ou) ou_gates(g.ou_a[h * DK + nme], g.ou_p[h * DK + nme], g.ou_d[h * DK + nme], oa, op);
 
-    Part<TB, DK> xl, xdq, xq, xk, xa, xp;
-    Part<TB, DV> xv, xdy;
-    Part<TB, 1> xr, xg;
-    Part<1, DK> xlp;
+    Part<TB, DK, NTH> xl, xdq, xq, xk, xa, xp;
+    Part<TB, DV, NTH> xv, xdy;
+    Part<TB, 1, NTH> xr, xg;
+    Part<1, DK, NTH> xlp;
     // Loads stay unconditional: absent tensors are replaced by present ones whose values
     // are not used (OU gates: abar / pbar columns from k; no readout-variance gradient:
     // its column from lam, scaled by zero; no initial precision: token 0's lam_{t-1}
@@ -517,7 +525,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
     for (int blk = nblk - 1; blk >= 0; --blk) {
         const int t0 = blk * TB, nt = min(TB, s.T - t0);
         // ---- A
-        for (int idx = tid; idx < TB * DK; idx += kThreads) {
+        for (int idx = tid; idx < TB * DK; idx += NTH) {
             const int j = idx / DK, n = idx % DK;
             if (j < nt) {
                 const float* row = sIn + j * ROW;
@@ -593,7 +601,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
         float o_dq[ND], o_dk[ND], o_da[ND], o_dp[ND], o_dv[NDV];
 #pragma unroll
         for (int u = 0; u < ND; ++u) {
-            const int idx = tid + kThreads * u, j = idx / DK, n = idx % DK;
+            const int idx = tid + NTH * u, j = idx / DK, n = idx % DK;
             const float* row = sIn + j * ROW;
             const float lam = row[C::CL + n];
             const float lp = j > 0 ? row[C::CL + n - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[n]);
@@ -620,7 +628,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
         }
 #pragma unroll
         for (int u = 0; u < NDV; ++u) {
-            const int idx = tid + kThreads * u, j = idx / DV, dd = idx % DV;
+            const int idx = tid + NTH * u, j = idx / DV, dd = idx % DV;
             float acc = 0.f;
             if (j < nt) {
 #pragma unroll
@@ -633,7 +641,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
         commit();
 #pragma unroll
         for (int u = 0; u < ND; ++u) {
-            const int idx = tid + kThreads * u, j = idx / DK, n = idx % DK;
+            const int idx = tid + NTH * u, j = idx / DK, n = idx % DK;
             if (j < nt) {
                 const size_t o = ((row0 + t0 + j) * s.H + h) * DK + n;
                 st(dq, o, o_dq[u]);
@@ -646,7 +654,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
         }
 #pragma unroll
         for (int u = 0; u < NDV; ++u) {
-            const int idx = tid + kThreads * u, j = idx / DV, dd = idx % DV;
+            const int idx = tid + NTH * u, j = idx / DV, dd = idx % DV;
             if (j < nt && idx < TB * DV) st(dv, ((row0 + t0 + j) * s.H + h) * DV + dd, o_dv[u]);
         }
         if (tid < nt) {
@@ -662,13 +670,13 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep2_kernel(Shape s, BwdArgs g
     if (tid < DK && g.dlam0) g.dlam0[(size_t)bh * DK + tid] = cnext;
     if (ou) {   // part b of the token sums: the threads of one slot are combined in order
         sOU[tid] = sum_da;
-        sOU[kThreads + tid] = sum_dp;
+        sOU[NTH + tid] = sum_dp;
         barrier_lds();
         if (tid < DK) {
             float sa = 0.f, sp = 0.f;
-            for (int i = tid; i < kThreads; i += DK) {
+            for (int i = tid; i < NTH; i += DK) {
                 sa += sOU[i];
-                sp += sOU[kThreads + i];
+                sp += sOU[NTH + i];
             }
             const size_t np = (size_t)s.B * s.H * DK;
             g.ou_part[(size_t)bh * DK + tid] = sa;
@@ -816,7 +824,7 @@ struct BwdL {
         static const hipError_t attr =
             hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
         if (attr != hipSuccess) return attr;
-        hipLaunchKernelGGL(kern, dim3(s.B * s.H), dim3(kThreads), bytes, st, s, a, wlam, wdqt, wPT);
+        hipLaunchKernelGGL(kern, dim3(s.B * s.H), dim3(Sweep2Cfg<DK, DV>::NTH), bytes, st, s, a, wlam, wdqt, wPT);
         return hipGetLastError();
     }
 };
