@@ -74,6 +74,10 @@ __device__ __forceinline__ float group_sum(float x) {
 // several workgroups (each walks the precision of the head itself)
 template <int DV>
 constexpr int kFwdDVT = DV < 16 ? DV : 16;
+// threads per forward workgroup: 512 (two waves per SIMD) where the key width fills
+// them and the LDS fits
+template <int DK>
+constexpr int kFwdThreads = (DK >= 32 && DK <= 64) ? 512 : 256;
 
 // ----------------------------------------------------------------------------
 // Forward.  One workgroup per (b, h, value tile of DVT channels).  Threads
@@ -83,16 +87,17 @@ constexpr int kFwdDVT = DV < 16 ? DV : 16;
 // staged rows; then every thread updates its state entries over the block and
 // the readout partials are summed.
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArgs g) {
+__global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s, FwdArgs g) {
     using T_ = typename storage<S>::type;
+    constexpr int NTH = kFwdThreads<DK>;
     constexpr int DVT = kFwdDVT<DV>;
     constexpr int NTILE = DV / DVT;
-    constexpr int NG = kThreads / DVT;
+    constexpr int NG = NTH / DVT;
     constexpr int NPER = DK / NG > 0 ? DK / NG : 1;
     static_assert(DK % NG == 0 || NG > DK, "key width must be a multiple of the n-groups");
     // staged row of a token: abar, pbar, k, q [DK] each, this tile's v [DVT], r
     constexpr int CA = 0, CP = DK, CK = 2 * DK, CQ = 3 * DK, CV = 4 * DK, CR = CV + DVT, ROW = CR + 1;
-    constexpr int NY = (kTB * DVT + kThreads - 1) / kThreads;   // outputs per thread and block
+    constexpr int NY = (kTB * DVT + NTH - 1) / NTH;   // outputs per thread and block
 
     __shared__ float sIn[kTB * ROW];
     __shared__ float sRed[kTB][NG][DVT];
@@ -126,9 +131,9 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
     float oa = 0.f, op = 0.f;
     if (ou && tid < DK) ou_gates(g.ou_a[h * DK + tid], g.ou_p[h * DK + tid], g.ou_d[h * DK + tid], oa, op);
 
-    Part<kTB, DK> xa, xp, xk, xq;
-    Part<kTB, DVT> xv;
-    Part<kTB, 1> xr;
+    Part<kTB, DK, NTH> xa, xp, xk, xq;
+    Part<kTB, DVT, NTH> xv;
+    Part<kTB, 1, NTH> xr;
     // with OU gates the abar / pbar columns are filled from k and not used
     const T_* ga = ou ? k : a;
     const T_* gp = ou ? k : p;
@@ -210,7 +215,7 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
         float yo[NY], yvo = 0.f;
 #pragma unroll
         for (int u = 0; u < NY; ++u) {
-            const int idx = tid + kThreads * u, j = idx / DVT, dd = idx % DVT;
+            const int idx = tid + NTH * u, j = idx / DVT, dd = idx % DVT;
             float acc = 0.f;
             if (j < nt) {
 #pragma unroll
@@ -218,7 +223,7 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
             }
             yo[u] = acc;
         }
-        const int jv = tid - (kThreads - kTB);   // the token whose readout variance this thread sums
+        const int jv = tid - (NTH - kTB);   // the token whose readout variance this thread sums
         const bool wv = tile == 0 && g.yvar && jv >= 0 && jv < nt;
         if (wv) {
 #pragma unroll
@@ -228,7 +233,7 @@ __global__ __launch_bounds__(kThreads) void fwd_recurrent_kernel(Shape s, FwdArg
         commit();
 #pragma unroll
         for (int u = 0; u < NY; ++u) {
-            const int idx = tid + kThreads * u, j = idx / DVT, dd = idx % DVT;
+            const int idx = tid + NTH * u, j = idx / DVT, dd = idx % DVT;
             if (j < nt) st(y, ((row0 + t0 + j) * s.H + h) * DV + tile * DVT + dd, yo[u]);
         }
         if (wv) g.yvar[(row0 + t0 + jv) * s.H + h] = yvo;
@@ -802,7 +807,7 @@ struct FwdL {
     static hipError_t run(const Shape& s, const FwdArgs& a, hipStream_t st) {
         constexpr int DVT = kFwdDVT<DV>;
         const unsigned grid = (unsigned)(s.B * s.H * (DV / DVT));
-        hipLaunchKernelGGL((fwd_recurrent_kernel<S, DK, DV>), dim3(grid), dim3(kThreads), 0, st, s, a);
+        hipLaunchKernelGGL((fwd_recurrent_kernel<S, DK, DV>), dim3(grid), dim3(kFwdThreads<DK>), 0, st, s, a);
         return hipGetLastError();
     }
 };
