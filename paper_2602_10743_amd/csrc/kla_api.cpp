@@ -82,7 +82,7 @@ size_t kla_forward_workspace(const kla_desc* desc) {
 size_t kla_saved_bytes(const kla_desc* desc) {
     if (check_desc(desc) != KLA_OK) return 0;
     const kla::Shape s = shape_of(desc);
-    return kla::chunked_supported(s) ? kla::chunked_saved_bytes(s) : 0;
+    return kla::chunked_supported(s) ? kla::chunked_saved_bytes(s) : kla::recurrent_saved_bytes(s);
 }
 
 size_t kla_backward_workspace(const kla_desc* desc, int with_saved) {
@@ -127,7 +127,7 @@ kla_status forward_impl(const kla_desc* desc, const kla::FwdArgs& a, bool ou, vo
         e = kla::launch_forward_segmented(s, a, static_cast<char*>(ws) + kAlign, stream);
     else
         e = kla::chunked_supported(s) ? kla::launch_forward_chunked(s, a, saved, stream)
-                                      : kla::launch_forward_recurrent(s, a, stream);
+                                      : kla::launch_forward_recurrent(s, a, static_cast<float*>(saved), stream);
     return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 
@@ -174,7 +174,7 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
         }
         e = kla::launch_backward_chunked(s, a, saved, work, stream);
     } else {
-        e = kla::launch_backward_recurrent(s, a, work, stream);
+        e = kla::launch_backward_recurrent(s, a, static_cast<const float*>(saved), work, stream);
     }
     if (e == hipSuccess && ou)
         e = kla::launch_ou_param_grads(s.H, s.dk, ou_parts(s), a.ou_part, a.ou_a, a.ou_p, a.ou_d, da, dp, dd, stream);

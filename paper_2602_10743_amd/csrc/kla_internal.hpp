@@ -44,10 +44,13 @@ struct DecodeArgs {
     const float *ou_a = nullptr, *ou_p = nullptr, *ou_d = nullptr;
 };
 
-// Token-recurrent reference kernels.
-hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, hipStream_t st);
+// Token-recurrent kernels.  Their saved context is the precision trajectory
+// lam_t [B, T, H, dk] fp32 (saved_lam: NULL, or recurrent_saved_bytes(s) bytes).
+size_t recurrent_saved_bytes(const Shape& s);
+hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st);
 size_t backward_recurrent_workspace(const Shape& s);
-hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, void* ws, hipStream_t st);
+hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, const float* saved_lam, void* ws,
+                                     hipStream_t st);
 hipError_t launch_decode_step(const Shape& s, const DecodeArgs& a, hipStream_t st);
 
 // Chunked MFMA path (bf16 storage, dk >= 32).

@@ -70,6 +70,16 @@ __device__ __forceinline__ float group_sum(float x) {
     return x;
 }
 
+// Sum over groups of W consecutive lanes (W = 16 or 32), held by every lane of the
+// group: W = 32 exchanges the two row sums with a swizzle (lane l reads lane l ^ 16).
+template <int W>
+__device__ __forceinline__ float group_sum_all(float x) {
+    x = group_sum<16>(x);
+    if constexpr (W == 32)
+        x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+    return x;
+}
+
 // value channels per forward workgroup: 16, so that even a small head spreads over
 // several workgroups (each walks the precision of the head itself)
 template <int DV>
@@ -87,7 +97,7 @@ constexpr int kFwdThreads = (DK >= 32 && DK <= 64) ? 512 : 256;
 // staged rows; then every thread updates its state entries over the block and
 // the readout partials are summed.
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s, FwdArgs g) {
+__global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s, FwdArgs g, float* saved_lam) {
     using T_ = typename storage<S>::type;
     constexpr int NTH = kFwdThreads<DK>;
     constexpr int DVT = kFwdDVT<DV>;
@@ -173,41 +183,43 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
     barrier_lds();
     for (int blk = 0; blk < nblk; ++blk) {
         const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
+        float lsv[kTB];   // lam after each token of the block (the saved context)
+        // Token loops carry no branch: rows past nt (the ragged last block) are worked on
+        // as well, from the repeated last row, and only selects keep them out of the state.
         if (tid < DK) {
 #pragma unroll
             for (int j = 0; j < kTB; ++j) {
-                if (j < nt) {
-                    float* row = sIn + j * ROW;
-                    const float ra = row[CA + tid], rp = row[CP + tid];
-                    const float at = ou ? oa : ra, pt = ou ? op : rp;
-                    const float kt = row[CK + tid], qt = row[CQ + tid], rt = row[CR];
-                    const float rho = rcp(at * at + pt * lam);
-                    lam = rho * lam + kt * kt * rt;
-                    const float inv = rcp(lam);
-                    row[CA + tid] = at * rho;
-                    row[CP + tid] = rt * kt;
-                    row[CK + tid] = qt * inv;
-                    row[CQ + tid] = qt * qt * inv;
-                }
+                float* row = sIn + j * ROW;
+                const float ra = row[CA + tid], rp = row[CP + tid];
+                const float at = ou ? oa : ra, pt = ou ? op : rp;
+                const float kt = row[CK + tid], qt = row[CQ + tid], rt = row[CR];
+                const float rho = rcp(at * at + pt * lam);
+                const float ln = rho * lam + kt * kt * rt;
+                lam = j < nt ? ln : lam;
+                lsv[j] = ln;
+                const float inv = rcp(ln);
+                row[CA + tid] = at * rho;
+                row[CP + tid] = rt * kt;
+                row[CK + tid] = qt * inv;
+                row[CQ + tid] = qt * qt * inv;
             }
         }
         barrier_lds();
 #pragma unroll
         for (int j = 0; j < kTB; ++j) {
-            if (j < nt) {
-                const float* row = sIn + j * ROW;
-                const float vd = row[CV + dl];
-                float acc = 0.f;
+            const float* row = sIn + j * ROW;
+            const float vd = row[CV + dl];
+            float acc = 0.f;
 #pragma unroll
-                for (int i = 0; i < NPER; ++i) {
-                    const int n = ng + i * NG;
-                    if (owns) {
-                        Hs[i] = row[CA + n] * Hs[i] + row[CP + n] * vd;
-                        acc += row[CK + n] * Hs[i];
-                    }
+            for (int i = 0; i < NPER; ++i) {
+                const int n = ng + i * NG;
+                if (NG <= DK || owns) {
+                    const float hn = row[CA + n] * Hs[i] + row[CP + n] * vd;
+                    Hs[i] = j < nt ? hn : Hs[i];
+                    acc += row[CK + n] * hn;
                 }
-                sRed[j][ng][dl] = acc;
             }
+            sRed[j][ng][dl] = acc;
         }
         barrier_lds();
         // the block's outputs are formed in registers and stored after the commit, whose wait
@@ -237,6 +249,11 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
             if (j < nt) st(y, ((row0 + t0 + j) * s.H + h) * DV + tile * DVT + dd, yo[u]);
         }
         if (wv) g.yvar[(row0 + t0 + jv) * s.H + h] = yvo;
+        if (saved_lam && tile == 0 && tid < DK) {
+#pragma unroll
+            for (int j = 0; j < kTB; ++j)
+                if (j < nt) saved_lam[((row0 + t0 + j) * s.H + h) * DK + tid] = lsv[j];
+        }
         fetch(min(blk + 2, nblk - 1) * kTB);
         barrier_lds();
     }
@@ -252,15 +269,20 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
 // precision trajectory lam_t and dqt_t = H_t dy_t (the gradient of the
 // effective query q/lam_t), plus PT[n] = sum_d detaT[n,d] H_T[n,d].
 // One workgroup per (b, h, 16 key slots); 16 lanes split the value channels.
-template <typename S, int DK, int DV>
-__global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g, float* wlam,
+// SV: the forward saved lam_t (slam); every token's gates then follow from lam_{t-1}
+// without the serial precision walk, and lam_t is not written again.
+template <typename S, int DK, int DV, bool SV>
+__global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g, const float* slam, float* wlam,
                                                                float* wdqt, float* wPT) {
     using T_ = typename storage<S>::type;
     constexpr int NT = 16, DL = 16, DPER = DV / DL;
     static_assert(DL == kTB, "lane j of a slot's row holds token j of the block");
-    // staged row of a token: abar, pbar, k of this workgroup's NT key slots, v [DV], dy [DV], r
-    constexpr int CA = 0, CP = NT, CK = 2 * NT, CV = 3 * NT, CD = CV + DV, CR = CD + DV, ROW = CR + 1;
+    // staged row of a token: abar, pbar, k of this workgroup's NT key slots, v [DV], dy [DV], r, and
+    // with SV the saved lam of the NT slots
+    constexpr int CA = 0, CP = NT, CK = 2 * NT, CV = 3 * NT, CD = CV + DV, CR = CD + DV, CL = CR + 1;
+    constexpr int ROW = SV ? CL + NT : CR + 1;
     __shared__ float sIn[kTB * ROW];
+    __shared__ float sLP[NT];   // SV: lam of the token before the block
 
     const T_* k = static_cast<const T_*>(g.k);
     const T_* v = static_cast<const T_*>(g.v);
@@ -285,12 +307,15 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     float oa = 0.f, op = 0.f;
     if (ou) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], oa, op);
 
-    Part<kTB, NT> xa, xp, xk;
+    Part<kTB, NT> xa, xp, xk, xl;
     Part<kTB, DV> xv, xdy;
     Part<kTB, 1> xr;
-    // with OU gates the abar / pbar columns are filled from k and not used
+    Part<1, NT> xlp;
+    // with OU gates the abar / pbar columns are filled from k and not used; with SV and no
+    // initial precision, token 0's lam_{t-1} is read from the saved lam and replaced by 1
     const T_* ga = ou ? k : a;
     const T_* gp = ou ? k : p;
+    const bool lam0_one = g.lam0 == nullptr;
     auto fetch = [&](int t) {
         const int nt = min(kTB, s.T - t);
         const size_t o = (row0 + t) * s.H + h;
@@ -300,6 +325,12 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
         xv.fetch(v + o * DV, s.H * DV, nt);
         xdy.fetch(dy + o * DV, s.H * DV, nt);
         xr.fetch(r + o, s.H, nt);
+        if constexpr (SV) {
+            xl.fetch(slam + o * DK + ktile * NT, s.H * DK, nt);
+            const float* lp0 = t > 0 ? slam + (o - s.H) * DK
+                                     : (lam0_one ? slam + o * DK : g.lam0 + (size_t)bh * DK);
+            xlp.fetch(lp0 + ktile * NT, 0, 1);
+        }
     };
     auto commit = [&]() {
         wait_vm_all();   // the prefetch has landed (and stores issued before it are done)
@@ -309,6 +340,10 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
         xv.template commit<ROW>(sIn, CV);
         xdy.template commit<ROW>(sIn, CD);
         xr.template commit<ROW>(sIn, CR);
+        if constexpr (SV) {
+            xl.template commit<ROW>(sIn, CL);
+            xlp.template commit<NT>(sLP, 0);
+        }
     };
 
     // blocks staged as in the forward: blk from LDS, blk + 1 in registers
@@ -324,33 +359,35 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
         const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
         float olam = 0.f, odqt = 0.f;
 #pragma unroll
-        for (int j = 0; j < kTB; ++j) {
-            if (j < nt) {
-                const float* row = sIn + j * ROW;
-                const float ra = row[CA + nl], rp = row[CP + nl];
-                const float at = ou ? oa : ra, pt = ou ? op : rp;
-                const float kt = row[CK + nl], rt = row[CR];
-                const float rho = rcp(at * at + pt * lam);
-                const float F = at * rho, kh = rt * kt;
-                lam = rho * lam + kt * kt * rt;
-                float acc = 0.f;
+        for (int j = 0; j < kTB; ++j) {   // no branch: rows past nt only reach selects
+            const bool live = j < nt;
+            const float* row = sIn + j * ROW;
+            const float ra = row[CA + nl], rp = row[CP + nl];
+            const float at = ou ? oa : ra, pt = ou ? op : rp;
+            const float kt = row[CK + nl], rt = row[CR];
+            if constexpr (SV)   // lam_{t-1} from the saved trajectory
+                lam = j > 0 ? row[CL + nl - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[nl]);
+            const float rho = rcp(at * at + pt * lam);
+            const float F = at * rho, kh = rt * kt;
+            if constexpr (!SV) lam = live ? rho * lam + kt * kt * rt : lam;
+            float acc = 0.f;
 #pragma unroll
-                for (int i = 0; i < DPER; ++i) {
-                    Hs[i] = F * Hs[i] + kh * row[CV + dl + i * DL];
-                    acc += Hs[i] * row[CD + dl + i * DL];
-                }
-                acc = group_sum<16>(acc);
-                if (dl == j) {   // lane j of the slot's row keeps token j's results
-                    olam = lam;
-                    odqt = acc;
-                }
+            for (int i = 0; i < DPER; ++i) {
+                const float hn = F * Hs[i] + kh * row[CV + dl + i * DL];
+                Hs[i] = live ? hn : Hs[i];
+                acc += hn * row[CD + dl + i * DL];
+            }
+            acc = group_sum<16>(acc);
+            if (dl == j) {   // lane j of the slot's row keeps token j's results
+                olam = lam;
+                odqt = acc;
             }
         }
         barrier_lds();
         commit();
         if (dl < nt) {
             const size_t o = ((row0 + t0 + dl) * s.H + h) * DK + n;
-            wlam[o] = olam;
+            if constexpr (!SV) wlam[o] = olam;
             wdqt[o] = odqt;
         }
         fetch(min(blk + 2, nblk - 1) * kTB);
@@ -556,48 +593,47 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
         barrier_lds();
         // ---- B
 #pragma unroll
-        for (int j = TB - 1; j >= 0; --j) {
-            if (j < nt) {
-                const float* row = sIn + j * ROW;
-                float dyd[DPER], vd[DPER], pv[DPER];
+        for (int j = TB - 1; j >= 0; --j) {   // no branch: rows past nt only reach selects
+            const bool live = j < nt;
+            const float* row = sIn + j * ROW;
+            float dyd[DPER], vd[DPER], pv[DPER];
+#pragma unroll
+            for (int jd = 0; jd < DPER; ++jd) {
+                dyd[jd] = row[C::CD + dl + jd * DVT];
+                vd[jd] = row[C::CV + dl + jd * DVT];
+                pv[jd] = 0.f;
+            }
+#pragma unroll
+            for (int i = 0; i < NPER; ++i) {
+                const int n = ng + i * NG;
+                const float4 co = *reinterpret_cast<const float4*>(sC0 + 4 * (j * DK + n));
+                float pk = 0.f;
 #pragma unroll
                 for (int jd = 0; jd < DPER; ++jd) {
-                    dyd[jd] = row[C::CD + dl + jd * DVT];
-                    vd[jd] = row[C::CV + dl + jd * DVT];
-                    pv[jd] = 0.f;
+                    const float hn = co.x * dH[i][jd] + co.y * dyd[jd];
+                    dH[i][jd] = live ? hn : dH[i][jd];
+                    pk += hn * vd[jd];
+                    pv[jd] += hn * co.z;
                 }
-#pragma unroll
-                for (int i = 0; i < NPER; ++i) {
-                    const int n = ng + i * NG;
-                    const float4 co = *reinterpret_cast<const float4*>(sC0 + 4 * (j * DK + n));
-                    float pk = 0.f;
-#pragma unroll
-                    for (int jd = 0; jd < DPER; ++jd) {
-                        dH[i][jd] = co.x * dH[i][jd] + co.y * dyd[jd];
-                        pk += dH[i][jd] * vd[jd];
-                        pv[jd] += dH[i][jd] * co.z;
-                    }
-                    pk = group_sum<DVT>(pk);
-                    if (dl == DVT - 1) sPK[j * DK + n] = pk;
-                }
-#pragma unroll
-                for (int jd = 0; jd < DPER; ++jd) sPV[(j * NG + ng) * DV + dl + jd * DVT] = pv[jd];
+                sPK[j * DK + n] = group_sum_all<DVT>(pk);   // the same value from every lane of the group
             }
+#pragma unroll
+            for (int jd = 0; jd < DPER; ++jd) sPV[(j * NG + ng) * DV + dl + jd * DVT] = pv[jd];
         }
         barrier_lds();
         // ---- C
         if (tid < DK) {
-#pragma unroll 4
-            for (int j = TB - 1; j >= 0; --j) {
-                if (j < nt) {
-                    const float kh = sC0[4 * (j * DK + tid) + 2];
-                    const float4 c1 = *reinterpret_cast<const float4*>(sC1 + 4 * (j * DK + tid));
-                    const float dkh = sPK[j * DK + tid];
-                    Sg += c1.w - kh * dkh;   // dG_t
-                    const float gl = cnext - c1.z;   // g_t
-                    *reinterpret_cast<float2*>(sSG + 2 * (j * DK + tid)) = make_float2(Sg, gl);
-                    cnext = c1.x * gl - c1.y * Sg;
-                }
+#pragma unroll
+            for (int j = TB - 1; j >= 0; --j) {   // no branch: rows past nt only reach selects
+                const bool live = j < nt;
+                const float kh = sC0[4 * (j * DK + tid) + 2];
+                const float4 c1 = *reinterpret_cast<const float4*>(sC1 + 4 * (j * DK + tid));
+                const float dkh = sPK[j * DK + tid];
+                const float sg = Sg + (c1.w - kh * dkh);   // dG_t
+                const float gl = cnext - c1.z;              // g_t
+                *reinterpret_cast<float2*>(sSG + 2 * (j * DK + tid)) = make_float2(sg, gl);
+                Sg = live ? sg : Sg;
+                cnext = live ? c1.x * gl - c1.y * sg : cnext;
             }
         }
         barrier_lds();
@@ -804,23 +840,30 @@ hipError_t dispatch(const Shape& s, A&&... args) {
 
 template <typename S, int DK, int DV>
 struct FwdL {
-    static hipError_t run(const Shape& s, const FwdArgs& a, hipStream_t st) {
+    static hipError_t run(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st) {
         constexpr int DVT = kFwdDVT<DV>;
         const unsigned grid = (unsigned)(s.B * s.H * (DV / DVT));
-        hipLaunchKernelGGL((fwd_recurrent_kernel<S, DK, DV>), dim3(grid), dim3(kFwdThreads<DK>), 0, st, s, a);
+        hipLaunchKernelGGL((fwd_recurrent_kernel<S, DK, DV>), dim3(grid), dim3(kFwdThreads<DK>), 0, st, s, a,
+                           saved_lam);
         return hipGetLastError();
     }
 };
 
 template <typename S, int DK, int DV>
 struct BwdL {
-    static hipError_t run(const Shape& s, const BwdArgs& a, void* ws, hipStream_t st) {
+    static hipError_t run(const Shape& s, const BwdArgs& a, const float* saved_lam, void* ws, hipStream_t st) {
         const size_t ntok = (size_t)s.B * s.T * s.H * DK;
         float* wlam = static_cast<float*>(ws);
         float* wdqt = wlam + ntok;
         float* wPT = wdqt + ntok;
-        hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV>), dim3(s.B * s.H * (DK / 16)), dim3(kThreads), 0, st,
-                           s, a, wlam, wdqt, wPT);
+        const dim3 grid1(s.B * s.H * (DK / 16));
+        if (saved_lam)
+            hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV, true>), grid1, dim3(kThreads), 0, st, s, a, saved_lam,
+                               wlam, wdqt, wPT);
+        else
+            hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV, false>), grid1, dim3(kThreads), 0, st, s, a, nullptr,
+                               wlam, wdqt, wPT);
+        const float* lam_t = saved_lam ? saved_lam : wlam;
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         auto kern = bwd_sweep2_kernel<S, DK, DV>;
@@ -829,7 +872,7 @@ struct BwdL {
         static const hipError_t attr =
             hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
         if (attr != hipSuccess) return attr;
-        hipLaunchKernelGGL(kern, dim3(s.B * s.H), dim3(Sweep2Cfg<DK, DV>::NTH), bytes, st, s, a, wlam, wdqt, wPT);
+        hipLaunchKernelGGL(kern, dim3(s.B * s.H), dim3(Sweep2Cfg<DK, DV>::NTH), bytes, st, s, a, lam_t, wdqt, wPT);
         return hipGetLastError();
     }
 };
@@ -844,8 +887,10 @@ struct DecL {
 
 }  // namespace
 
-hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, hipStream_t st) {
-    return dispatch<FwdL>(s, a, st);
+size_t recurrent_saved_bytes(const Shape& s) { return (size_t)s.B * s.T * s.H * s.dk * sizeof(float); }
+
+hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st) {
+    return dispatch<FwdL>(s, a, saved_lam, st);
 }
 
 // one part per batch row: the recurrent backward walks a whole (b, h) in one workgroup
@@ -856,8 +901,9 @@ size_t backward_recurrent_workspace(const Shape& s) {
     return (2 * ntok + (size_t)s.B * s.H * s.dk) * sizeof(float);
 }
 
-hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, void* ws, hipStream_t st) {
-    return dispatch<BwdL>(s, a, ws, st);
+hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, const float* saved_lam, void* ws,
+                                     hipStream_t st) {
+    return dispatch<BwdL>(s, a, saved_lam, ws, st);
 }
 
 hipError_t launch_decode_step(const Shape& s, const DecodeArgs& a, hipStream_t st) {

@@ -88,18 +88,23 @@ def test_forward_small(kla, B, T, H, dk, dv, dtype, dist, init):
 
 
 @pytest.mark.parametrize("B,T,H,dk,dv,dtype,dist", SMALL)
-def test_backward_small(kla, B, T, H, dk, dv, dtype, dist):
+@pytest.mark.parametrize("with_saved", [False, True])
+def test_backward_small(kla, B, T, H, dk, dv, dtype, dist, with_saved):
     case = K.random_case(B, T, H, dk, dv, dtype, seed=T * 11 + dv, dist=dist)
     lam0, eta0 = _random_belief(B, H, dk, dv, T + 1)
     g = np.random.default_rng(T)
     dlamT = g.standard_normal((B, H, dk)).astype(np.float32).astype(np.float64)
     detaT = g.standard_normal((B, H, dk, dv)).astype(np.float32).astype(np.float64)
     dyvar = g.standard_normal((B, T, H)).astype(np.float32).astype(np.float64)
-    log(f"backward small B{B} T{T} H{H} dk{dk} dv{dv} {dtype}")
+    log(f"backward small B{B} T{T} H{H} dk{dk} dv{dv} {dtype} saved={with_saved}")
     x = _dev_inputs(case, dtype)
     f32 = lambda a: torch.tensor(a, dtype=torch.float32, device=DEV)
+    saved = None
+    if with_saved:   # the context a forward with the same inputs saved
+        saved = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0),
+                                save=True)["saved"]
     gr = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), x["dy"],
-                          f32(dlamT), f32(detaT), dyvar=f32(dyvar))
+                          f32(dlamT), f32(detaT), saved=saved, dyvar=f32(dyvar))
     torch.cuda.synchronize()
     ref = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0,
                           case["dy"], dlamT, detaT, dyvar=dyvar)
@@ -290,11 +295,13 @@ def _workload_parity(kla, cid, pairs_n, backward):
     x = {n: bits_to_torch(bits[n], DEV) for n in bits}
     del bits
     log(f"workload {cid}: forward on GPU")
-    out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], want_var=True)
+    # the launch configuration bench.py times: the forward saves its context for the backward
+    out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], want_var=True, save=backward)
     gr = None
     if backward:
         log(f"workload {cid}: backward on GPU")
-        gr = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], None, None, x["dy"])
+        gr = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], None, None, x["dy"],
+                              saved=out["saved"])
     torch.cuda.synchronize()
     pairs = _sample_pairs(w, pairs_n)
     log(f"workload {cid}: oracle on pairs {pairs}")
