@@ -282,7 +282,9 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     constexpr int CA = 0, CP = NT, CK = 2 * NT, CV = 3 * NT, CD = CV + DV, CR = CD + DV, CL = CR + 1;
     constexpr int ROW = SV ? CL + NT : CR + 1;
     __shared__ float sIn[kTB * ROW];
-    __shared__ float sLP[NT];   // SV: lam of the token before the block
+    __shared__ float sLP[NT];          // SV: lam of the token before the block
+    __shared__ float2 sFK[kTB][NT];    // SV: F and r k of every (token, slot) of the block
+    static_assert(!SV || kThreads == kTB * NT, "one (token, slot) gate per thread");
 
     const T_* k = static_cast<const T_*>(g.k);
     const T_* v = static_cast<const T_*>(g.v);
@@ -306,6 +308,13 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     const bool ou = g.ou_a != nullptr;
     float oa = 0.f, op = 0.f;
     if (ou) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], oa, op);
+    // SV: the gate phase's slot is tid % NT
+    const int gsl = tid % NT, gj = tid / NT;
+    float goa = 0.f, gop = 0.f;
+    if (SV && ou) {
+        const int gn = ktile * NT + gsl;
+        ou_gates(g.ou_a[h * DK + gn], g.ou_p[h * DK + gn], g.ou_d[h * DK + gn], goa, gop);
+    }
 
     Part<kTB, NT> xa, xp, xk, xl;
     Part<kTB, DV> xv, xdy;
@@ -358,18 +367,33 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     for (int blk = 0; blk < nblk; ++blk) {
         const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
         float olam = 0.f, odqt = 0.f;
+        if constexpr (SV) {   // the gates of every (token, slot) from the saved lam_{t-1}, in parallel
+            const float* row = sIn + gj * ROW;
+            const float ra = row[CA + gsl], rp = row[CP + gsl];
+            const float at = ou ? goa : ra, pt = ou ? gop : rp;
+            const float lp = gj > 0 ? row[CL + gsl - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[gsl]);
+            const float rho = rcp(at * at + pt * lp);
+            sFK[gj][gsl] = make_float2(at * rho, row[CR] * row[CK + gsl]);
+            barrier_lds();
+        }
 #pragma unroll
         for (int j = 0; j < kTB; ++j) {   // no branch: rows past nt only reach selects
             const bool live = j < nt;
             const float* row = sIn + j * ROW;
-            const float ra = row[CA + nl], rp = row[CP + nl];
-            const float at = ou ? oa : ra, pt = ou ? op : rp;
-            const float kt = row[CK + nl], rt = row[CR];
-            if constexpr (SV)   // lam_{t-1} from the saved trajectory
-                lam = j > 0 ? row[CL + nl - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[nl]);
-            const float rho = rcp(at * at + pt * lam);
-            const float F = at * rho, kh = rt * kt;
-            if constexpr (!SV) lam = live ? rho * lam + kt * kt * rt : lam;
+            float F, kh;
+            if constexpr (SV) {
+                const float2 fk = sFK[j][nl];
+                F = fk.x;
+                kh = fk.y;
+            } else {
+                const float ra = row[CA + nl], rp = row[CP + nl];
+                const float at = ou ? oa : ra, pt = ou ? op : rp;
+                const float kt = row[CK + nl], rt = row[CR];
+                const float rho = rcp(at * at + pt * lam);
+                F = at * rho;
+                kh = rt * kt;
+                lam = live ? rho * lam + kt * kt * rt : lam;
+            }
             float acc = 0.f;
 #pragma unroll
             for (int i = 0; i < DPER; ++i) {
