@@ -2,11 +2,13 @@
 //
 // These walk the filter one token at a time (Theorem 1 gate view for the
 // precision, Theorem 2 for the information state, Algorithm 1 readout), with
-// the d_k x d_v state held in registers across the token loop.  They are the
-// reference HIP path of the library and the decode step's implementation.
-// With OU parameters (ou_a set) every token of a head shares the gates of its
-// key slot, formed once per lane; the backward then sums the gate gradients of
-// a lane over its tokens into one part per batch row.
+// the d_k x d_v state held in registers across the token loop.  They take fp32
+// inputs and the widths the chunked MFMA path does not, and implement the
+// decode step.  With OU parameters (ou_a set) every token of a head shares the
+// gates of its key slot; the backward then sums the gate gradients of a slot
+// over its tokens into one part per batch row.  The forward can save the
+// precision after every token, which the backward then reads instead of
+// walking it again.
 #include "kla_buf.hpp"
 #include "kla_device.hpp"
 #include "kla_internal.hpp"
