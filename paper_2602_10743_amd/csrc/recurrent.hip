@@ -86,15 +86,19 @@ __device__ __forceinline__ float group_sum_all(float x) {
 // several workgroups (each walks the precision of the head itself)
 template <int DV>
 constexpr int kFwdDVT = DV < 16 ? DV : 16;
-// threads per forward workgroup: 512 (two waves per SIMD) where the key width fills
-// them and the LDS fits
+// threads per forward workgroup and tokens per staged block: blocks of 32 tokens
+// (half the barriers per token) where the LDS holds them, two waves per SIMD at
+// dk = 64 (measured at the state-tracking shape, dk = 32: 256 threads and blocks
+// of 32 tokens beat 512 threads and blocks of 16)
 template <int DK>
-constexpr int kFwdThreads = (DK >= 32 && DK <= 64) ? 512 : 256;
+constexpr int kFwdThreads = DK == 64 ? 512 : 256;
+template <int DK>
+constexpr int kFwdTB = DK <= 32 ? 32 : 16;
 
 // ----------------------------------------------------------------------------
 // Forward.  One workgroup per (b, h, value tile of DVT channels).  Threads
 // tid < DK own the precision lane n = tid; every thread owns H[n, d] for
-// n = ng + i*NG and one channel d = d0 + dl.  Per block of kTB tokens: the
+// n = ng + i*NG and one channel d = d0 + dl.  Per block of TBF tokens: the
 // precision lanes walk the block and leave F, r k, q / lam and q^2 / lam in the
 // staged rows; then every thread updates its state entries over the block and
 // the readout partials are summed.
@@ -102,6 +106,7 @@ template <typename S, int DK, int DV>
 __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s, FwdArgs g, float* saved_lam) {
     using T_ = typename storage<S>::type;
     constexpr int NTH = kFwdThreads<DK>;
+    constexpr int TBF = kFwdTB<DK>;   // tokens per staged block
     constexpr int DVT = kFwdDVT<DV>;
     constexpr int NTILE = DV / DVT;
     constexpr int NG = NTH / DVT;
@@ -109,10 +114,10 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
     static_assert(DK % NG == 0 || NG > DK, "key width must be a multiple of the n-groups");
     // staged row of a token: abar, pbar, k, q [DK] each, this tile's v [DVT], r
     constexpr int CA = 0, CP = DK, CK = 2 * DK, CQ = 3 * DK, CV = 4 * DK, CR = CV + DVT, ROW = CR + 1;
-    constexpr int NY = (kTB * DVT + NTH - 1) / NTH;   // outputs per thread and block
+    constexpr int NY = (TBF * DVT + NTH - 1) / NTH;   // outputs per thread and block
 
-    __shared__ float sIn[kTB * ROW];
-    __shared__ float sRed[kTB][NG][DVT];
+    __shared__ float sIn[TBF * ROW];
+    __shared__ float sRed[TBF][NG][DVT];
 
     const T_* q = static_cast<const T_*>(g.q);
     const T_* k = static_cast<const T_*>(g.k);
@@ -143,14 +148,14 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
     float oa = 0.f, op = 0.f;
     if (ou && tid < DK) ou_gates(g.ou_a[h * DK + tid], g.ou_p[h * DK + tid], g.ou_d[h * DK + tid], oa, op);
 
-    Part<kTB, DK, NTH> xa, xp, xk, xq;
-    Part<kTB, DVT, NTH> xv;
-    Part<kTB, 1, NTH> xr;
+    Part<TBF, DK, NTH> xa, xp, xk, xq;
+    Part<TBF, DVT, NTH> xv;
+    Part<TBF, 1, NTH> xr;
     // with OU gates the abar / pbar columns are filled from k and not used
     const T_* ga = ou ? k : a;
     const T_* gp = ou ? k : p;
     auto fetch = [&](int t) {
-        const int nt = min(kTB, s.T - t);
+        const int nt = min(TBF, s.T - t);
         const size_t o = (row0 + t) * s.H + h;
         xa.fetch(ga + o * DK, s.H * DK, nt);
         xp.fetch(gp + o * DK, s.H * DK, nt);
@@ -175,22 +180,22 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
     // store reads waits for that store, and with the loads issued after the stores such a
     // wait does not also wait for the prefetch.  Fetches past the end fetch the last block
     // again (unused), so they stay unconditional.
-    const int nblk = (s.T + kTB - 1) / kTB;
+    const int nblk = (s.T + TBF - 1) / TBF;
     wait_vm_all();   // the initial state is in: no first-use wait inside the loop
     if (nblk > 0) {
         fetch(0);
         commit();
-        fetch(min(1, nblk - 1) * kTB);
+        fetch(min(1, nblk - 1) * TBF);
     }
     barrier_lds();
     for (int blk = 0; blk < nblk; ++blk) {
-        const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
-        float lsv[kTB];   // lam after each token of the block (the saved context)
+        const int t0 = blk * TBF, nt = min(TBF, s.T - t0);
+        float lsv[TBF];   // lam after each token of the block (the saved context)
         // Token loops carry no branch: rows past nt (the ragged last block) are worked on
         // as well, from the repeated last row, and only selects keep them out of the state.
         if (tid < DK) {
 #pragma unroll
-            for (int j = 0; j < kTB; ++j) {
+            for (int j = 0; j < TBF; ++j) {
                 float* row = sIn + j * ROW;
                 const float ra = row[CA + tid], rp = row[CP + tid];
                 const float at = ou ? oa : ra, pt = ou ? op : rp;
@@ -208,7 +213,7 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
         }
         barrier_lds();
 #pragma unroll
-        for (int j = 0; j < kTB; ++j) {
+        for (int j = 0; j < TBF; ++j) {
             const float* row = sIn + j * ROW;
             const float vd = row[CV + dl];
             float acc = 0.f;
@@ -237,7 +242,7 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
             }
             yo[u] = acc;
         }
-        const int jv = tid - (NTH - kTB);   // the token whose readout variance this thread sums
+        const int jv = tid - (NTH - TBF);   // the token whose readout variance this thread sums
         const bool wv = tile == 0 && g.yvar && jv >= 0 && jv < nt;
         if (wv) {
 #pragma unroll
@@ -253,10 +258,10 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
         if (wv) g.yvar[(row0 + t0 + jv) * s.H + h] = yvo;
         if (saved_lam && tile == 0 && tid < DK) {
 #pragma unroll
-            for (int j = 0; j < kTB; ++j)
+            for (int j = 0; j < TBF; ++j)
                 if (j < nt) saved_lam[((row0 + t0 + j) * s.H + h) * DK + tid] = lsv[j];
         }
-        fetch(min(blk + 2, nblk - 1) * kTB);
+        fetch(min(blk + 2, nblk - 1) * TBF);
         barrier_lds();
     }
     if (tile == 0 && g.lamT && tid < DK) g.lamT[(size_t)bh * DK + tid] = lam;
