@@ -96,7 +96,12 @@ size_t kla_backward_workspace(const kla_desc* desc, int with_saved) {
         }
         return bytes;
     }
-    return kAlign + round_up(kla::backward_recurrent_workspace(s));
+    size_t bytes = kAlign + round_up(kla::backward_recurrent_workspace(s));
+    if (!with_saved) {  // the precision trajectory is recomputed by the forward, plus a scratch output
+        const size_t elt = s.bf16 ? 2 : 4;
+        bytes += round_up(kla::recurrent_saved_bytes(s)) + round_up((size_t)s.B * s.T * s.H * s.dv * elt);
+    }
+    return bytes;
 }
 
 }  // extern "C"
@@ -174,6 +179,15 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
         }
         e = kla::launch_backward_chunked(s, a, saved, work, stream);
     } else {
+        if (!saved) {   // the same forward kernel fills the context, so both ways agree bit for bit
+            char* ctx = work + round_up(kla::backward_recurrent_workspace(s));
+            void* yscratch = ctx + round_up(kla::recurrent_saved_bytes(s));
+            kla::FwdArgs f{a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, yscratch, nullptr, nullptr, nullptr,
+                           a.ou_a, a.ou_p, a.ou_d};
+            e = kla::launch_forward_recurrent(s, f, reinterpret_cast<float*>(ctx), stream);
+            if (e != hipSuccess) return KLA_ERR_HIP;
+            saved = ctx;
+        }
         e = kla::launch_backward_recurrent(s, a, static_cast<const float*>(saved), work, stream);
     }
     if (e == hipSuccess && ou)

@@ -45,7 +45,8 @@ struct DecodeArgs {
 };
 
 // Token-recurrent kernels.  Their saved context is the precision trajectory
-// lam_t [B, T, H, dk] fp32 (saved_lam: NULL, or recurrent_saved_bytes(s) bytes).
+// lam_t [B, T, H, dk] fp32 (recurrent_saved_bytes(s) bytes): optional for the
+// forward, required by the backward.
 size_t recurrent_saved_bytes(const Shape& s);
 hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st);
 size_t backward_recurrent_workspace(const Shape& s);

@@ -9,6 +9,8 @@
 // over its tokens into one part per batch row.  The forward can save the
 // precision after every token, which the backward then reads instead of
 // walking it again.
+#include <type_traits>
+
 #include "kla_buf.hpp"
 #include "kla_device.hpp"
 #include "kla_internal.hpp"
@@ -72,6 +74,13 @@ __device__ __forceinline__ float group_sum(float x) {
     return x;
 }
 
+// x of the lane D below within its 16-lane row (row_shr; lanes with none read 0)
+template <int D>
+__device__ __forceinline__ float row_shr(float x) {
+    static_assert(D >= 1 && D <= 15, "row shift");
+    return dpp<0x110 + D, 0xf>(x);
+}
+
 // Sum over groups of W consecutive lanes (W = 16 or 32), held by every lane of the
 // group: W = 32 exchanges the two row sums with a swizzle (lane l reads lane l ^ 16).
 template <int W>
@@ -96,12 +105,18 @@ template <int DK>
 constexpr int kFwdTB = DK <= 32 ? 32 : 16;
 
 // ----------------------------------------------------------------------------
-// Forward.  One workgroup per (b, h, value tile of DVT channels).  Threads
-// tid < DK own the precision lane n = tid; every thread owns H[n, d] for
-// n = ng + i*NG and one channel d = d0 + dl.  Per block of TBF tokens: the
-// precision lanes walk the block and leave F, r k, q / lam and q^2 / lam in the
-// staged rows; then every thread updates its state entries over the block and
-// the readout partials are summed.
+// Forward.  One workgroup per (b, h, value tile of DVT channels); every thread
+// owns H[n, d] for n = ng + i*NG and one channel d = d0 + dl.  Per block of TBF
+// tokens the precision walk is spread over all threads: GPS consecutive lanes per
+// key slot, lane group g taking tokens g TPG .. g TPG + TPG - 1.  A lane composes
+// the Moebius matrices of its tokens (Theorem 1 in homogeneous form:
+// (x, z) -> ((1 + phi pbar) x + phi abar^2 z, pbar x + abar^2 z), lam = x / z,
+// phi = k^2 r); an inclusive scan of these products over the slot's lanes (DPP,
+// each product scaled by its largest entry: the map is projective) gives the
+// product of every token before the lane's group, which applied to the block's
+// starting lam starts the lane's own walk over its tokens.  The walk leaves F,
+// r k, q / lam and q^2 / lam in the staged rows; then every thread updates its
+// state entries over the block and the readout partials are summed.
 template <typename S, int DK, int DV>
 __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s, FwdArgs g, float* saved_lam) {
     using T_ = typename storage<S>::type;
@@ -115,6 +130,9 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
     // staged row of a token: abar, pbar, k, q [DK] each, this tile's v [DVT], r
     constexpr int CA = 0, CP = DK, CK = 2 * DK, CQ = 3 * DK, CV = 4 * DK, CR = CV + DVT, ROW = CR + 1;
     constexpr int NY = (TBF * DVT + NTH - 1) / NTH;   // outputs per thread and block
+    constexpr int GPS = NTH / DK, TPG = TBF / GPS;       // walk lanes per key slot, tokens per lane
+    static_assert(GPS * DK == NTH && TPG * GPS == TBF && GPS <= 16 && (GPS & (GPS - 1)) == 0,
+                  "the walk lanes of a slot split the block evenly within a DPP row");
 
     __shared__ float sIn[TBF * ROW];
     __shared__ float sRed[TBF][NG][DVT];
@@ -142,11 +160,11 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
         int n = ng + i * NG;
         Hs[i] = (owns && g.eta0) ? g.eta0[((size_t)bh * DK + n) * DV + d] : 0.f;
     }
-    float lam = 1.f;
-    if (tid < DK && g.lam0) lam = g.lam0[(size_t)bh * DK + tid];
+    const int wn = tid / GPS, wg = tid % GPS;   // walk: key slot and token group of this lane
+    float lam = g.lam0 ? g.lam0[(size_t)bh * DK + wn] : 1.f;   // lam before the block, in every lane of slot wn
     const bool ou = g.ou_a != nullptr;
     float oa = 0.f, op = 0.f;
-    if (ou && tid < DK) ou_gates(g.ou_a[h * DK + tid], g.ou_p[h * DK + tid], g.ou_d[h * DK + tid], oa, op);
+    if (ou) ou_gates(g.ou_a[h * DK + wn], g.ou_p[h * DK + wn], g.ou_d[h * DK + wn], oa, op);
 
     Part<TBF, DK, NTH> xa, xp, xk, xq;
     Part<TBF, DVT, NTH> xv;
@@ -190,26 +208,79 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
     barrier_lds();
     for (int blk = 0; blk < nblk; ++blk) {
         const int t0 = blk * TBF, nt = min(TBF, s.T - t0);
-        float lsv[TBF];   // lam after each token of the block (the saved context)
+        float lsv[TPG];   // lam after each of this lane's tokens (the saved context)
         // Token loops carry no branch: rows past nt (the ragged last block) are worked on
         // as well, from the repeated last row, and only selects keep them out of the state.
-        if (tid < DK) {
+        {
+            float ta[TPG], tp[TPG], tk[TPG], tq[TPG], tr[TPG];
 #pragma unroll
-            for (int j = 0; j < TBF; ++j) {
-                float* row = sIn + j * ROW;
-                const float ra = row[CA + tid], rp = row[CP + tid];
-                const float at = ou ? oa : ra, pt = ou ? op : rp;
-                const float kt = row[CK + tid], qt = row[CQ + tid], rt = row[CR];
-                const float rho = rcp(at * at + pt * lam);
-                const float ln = rho * lam + kt * kt * rt;
-                lam = j < nt ? ln : lam;
-                lsv[j] = ln;
-                const float inv = rcp(ln);
-                row[CA + tid] = at * rho;
-                row[CP + tid] = rt * kt;
-                row[CK + tid] = qt * inv;
-                row[CQ + tid] = qt * qt * inv;
+            for (int u = 0; u < TPG; ++u) {
+                const float* row = sIn + (wg * TPG + u) * ROW;
+                const float ra = row[CA + wn], rp = row[CP + wn];
+                ta[u] = ou ? oa : ra;
+                tp[u] = ou ? op : rp;
+                tk[u] = row[CK + wn];
+                tq[u] = row[CQ + wn];
+                tr[u] = row[CR];
             }
+            // this lane's product M_last ... M_first (tokens past nt: identity), scaled
+            float m00 = 1.f, m01 = 0.f, m10 = 0.f, m11 = 1.f;
+#pragma unroll
+            for (int u = 0; u < TPG; ++u) {
+                const float a2 = ta[u] * ta[u], phi = tk[u] * tk[u] * tr[u];
+                const float z0 = fmaf(tp[u], m00, a2 * m10), z1 = fmaf(tp[u], m01, a2 * m11);
+                const bool ok = wg * TPG + u < nt;
+                m00 = ok ? fmaf(phi, z0, m00) : m00;
+                m01 = ok ? fmaf(phi, z1, m01) : m01;
+                m10 = ok ? z0 : m10;
+                m11 = ok ? z1 : m11;
+            }
+            {
+                const float sc = rcp(fmaxf(fmaxf(m00, m01), fmaxf(m10, m11)));
+                m00 *= sc; m01 *= sc; m10 *= sc; m11 *= sc;
+            }
+            // inclusive scan over the slot's lanes: P_g = M_g ... M_0
+            auto scan_step = [&](auto dd) {
+                constexpr int D = decltype(dd)::value;
+                if constexpr (D < GPS) {
+                    const float b00 = row_shr<D>(m00), b01 = row_shr<D>(m01);
+                    const float b10 = row_shr<D>(m10), b11 = row_shr<D>(m11);
+                    const float c00 = fmaf(m00, b00, m01 * b10), c01 = fmaf(m00, b01, m01 * b11);
+                    const float c10 = fmaf(m10, b00, m11 * b10), c11 = fmaf(m10, b01, m11 * b11);
+                    const float sc = rcp(fmaxf(fmaxf(c00, c01), fmaxf(c10, c11)));
+                    const bool take = wg >= D;
+                    m00 = take ? c00 * sc : m00;
+                    m01 = take ? c01 * sc : m01;
+                    m10 = take ? c10 * sc : m10;
+                    m11 = take ? c11 * sc : m11;
+                }
+            };
+            scan_step(std::integral_constant<int, 1>{});
+            scan_step(std::integral_constant<int, 2>{});
+            scan_step(std::integral_constant<int, 4>{});
+            scan_step(std::integral_constant<int, 8>{});
+            // the product of the groups before this one (identity for group 0) applied to lam
+            const float e00 = row_shr<1>(m00), e01 = row_shr<1>(m01);
+            const float e10 = row_shr<1>(m10), e11 = row_shr<1>(m11);
+            float lw = lam;
+            if (wg > 0) lw = fmaf(e00, lam, e01) * rcp(fmaf(e10, lam, e11));
+            // walk this lane's tokens
+#pragma unroll
+            for (int u = 0; u < TPG; ++u) {
+                const int j = wg * TPG + u;
+                float* row = sIn + j * ROW;
+                const float rho = rcp(ta[u] * ta[u] + tp[u] * lw);
+                const float ln = rho * lw + tk[u] * tk[u] * tr[u];
+                lw = j < nt ? ln : lw;
+                lsv[u] = ln;
+                const float inv = rcp(ln);
+                row[CA + wn] = ta[u] * rho;
+                row[CP + wn] = tr[u] * tk[u];
+                row[CK + wn] = tq[u] * inv;
+                row[CQ + wn] = tq[u] * tq[u] * inv;
+            }
+            // lam after the block: the last group's, in every lane of the slot
+            lam = __shfl(lw, (tid & 63 & ~(GPS - 1)) + GPS - 1, 64);
         }
         barrier_lds();
 #pragma unroll
@@ -256,15 +327,17 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
             if (j < nt) st(y, ((row0 + t0 + j) * s.H + h) * DV + tile * DVT + dd, yo[u]);
         }
         if (wv) g.yvar[(row0 + t0 + jv) * s.H + h] = yvo;
-        if (saved_lam && tile == 0 && tid < DK) {
+        if (saved_lam && tile == 0) {
 #pragma unroll
-            for (int j = 0; j < TBF; ++j)
-                if (j < nt) saved_lam[((row0 + t0 + j) * s.H + h) * DK + tid] = lsv[j];
+            for (int u = 0; u < TPG; ++u) {
+                const int j = wg * TPG + u;
+                if (j < nt) saved_lam[((row0 + t0 + j) * s.H + h) * DK + wn] = lsv[u];
+            }
         }
         fetch(min(blk + 2, nblk - 1) * TBF);
         barrier_lds();
     }
-    if (tile == 0 && g.lamT && tid < DK) g.lamT[(size_t)bh * DK + tid] = lam;
+    if (tile == 0 && g.lamT && wg == 0) g.lamT[(size_t)bh * DK + wn] = lam;
     if (g.etaT && owns) {
 #pragma unroll
         for (int i = 0; i < NPER; ++i) g.etaT[((size_t)bh * DK + ng + i * NG) * DV + d] = Hs[i];
@@ -272,26 +345,25 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
 }
 
 // ----------------------------------------------------------------------------
-// Backward, sweep 1 (forward in time).  Re-runs the filter and stores the
-// precision trajectory lam_t and dqt_t = H_t dy_t (the gradient of the
-// effective query q/lam_t), plus PT[n] = sum_d detaT[n,d] H_T[n,d].
-// One workgroup per (b, h, 16 key slots); 16 lanes split the value channels.
-// SV: the forward saved lam_t (slam); every token's gates then follow from lam_{t-1}
-// without the serial precision walk, and lam_t is not written again.
-template <typename S, int DK, int DV, bool SV>
-__global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g, const float* slam, float* wlam,
-                                                               float* wdqt, float* wPT) {
+// Backward, sweep 1 (forward in time).  From the precision trajectory lam_t that
+// the forward saved, re-runs the information state and stores dqt_t = H_t dy_t
+// (the gradient of the effective query q/lam_t), plus PT[n] = sum_d detaT[n,d]
+// H_T[n,d].  One workgroup per (b, h, 16 key slots); 16 lanes split the value
+// channels.  Every token's gates follow from the saved lam_{t-1}, for all
+// (token, slot) pairs of a block in one parallel phase.
+template <typename S, int DK, int DV>
+__global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g, const float* slam, float* wdqt,
+                                                               float* wPT) {
     using T_ = typename storage<S>::type;
     constexpr int NT = 16, DL = 16, DPER = DV / DL;
     static_assert(DL == kTB, "lane j of a slot's row holds token j of the block");
-    // staged row of a token: abar, pbar, k of this workgroup's NT key slots, v [DV], dy [DV], r, and
-    // with SV the saved lam of the NT slots
-    constexpr int CA = 0, CP = NT, CK = 2 * NT, CV = 3 * NT, CD = CV + DV, CR = CD + DV, CL = CR + 1;
-    constexpr int ROW = SV ? CL + NT : CR + 1;
+    static_assert(kThreads == kTB * NT, "one (token, slot) gate per thread");
+    // staged row of a token: abar, pbar, k, saved lam of this workgroup's NT key slots, v [DV], dy [DV], r
+    constexpr int CA = 0, CP = NT, CK = 2 * NT, CL = 3 * NT, CV = 4 * NT, CD = CV + DV, CR = CD + DV;
+    constexpr int ROW = CR + 1;
     __shared__ float sIn[kTB * ROW];
-    __shared__ float sLP[NT];          // SV: lam of the token before the block
-    __shared__ float2 sFK[kTB][NT];    // SV: F and r k of every (token, slot) of the block
-    static_assert(!SV || kThreads == kTB * NT, "one (token, slot) gate per thread");
+    __shared__ float sLP[NT];          // lam of the token before the block
+    __shared__ float2 sFK[kTB][NT];    // F and r k of every (token, slot) of the block
 
     const T_* k = static_cast<const T_*>(g.k);
     const T_* v = static_cast<const T_*>(g.v);
@@ -311,14 +383,11 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
 #pragma unroll
     for (int i = 0; i < DPER; ++i)
         Hs[i] = g.eta0 ? g.eta0[((size_t)bh * DK + n) * DV + dl + i * DL] : 0.f;
-    float lam = g.lam0 ? g.lam0[(size_t)bh * DK + n] : 1.f;
-    const bool ou = g.ou_a != nullptr;
-    float oa = 0.f, op = 0.f;
-    if (ou) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], oa, op);
-    // SV: the gate phase's slot is tid % NT
+    // the gate phase's (token, slot) pair of this thread
     const int gsl = tid % NT, gj = tid / NT;
+    const bool ou = g.ou_a != nullptr;
     float goa = 0.f, gop = 0.f;
-    if (SV && ou) {
+    if (ou) {
         const int gn = ktile * NT + gsl;
         ou_gates(g.ou_a[h * DK + gn], g.ou_p[h * DK + gn], g.ou_d[h * DK + gn], goa, gop);
     }
@@ -327,8 +396,8 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     Part<kTB, DV> xv, xdy;
     Part<kTB, 1> xr;
     Part<1, NT> xlp;
-    // with OU gates the abar / pbar columns are filled from k and not used; with SV and no
-    // initial precision, token 0's lam_{t-1} is read from the saved lam and replaced by 1
+    // with OU gates the abar / pbar columns are filled from k and not used; with no initial
+    // precision, token 0's lam_{t-1} is read from the saved lam and replaced by 1
     const T_* ga = ou ? k : a;
     const T_* gp = ou ? k : p;
     const bool lam0_one = g.lam0 == nullptr;
@@ -338,28 +407,23 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
         xa.fetch(ga + o * DK + ktile * NT, s.H * DK, nt);
         xp.fetch(gp + o * DK + ktile * NT, s.H * DK, nt);
         xk.fetch(k + o * DK + ktile * NT, s.H * DK, nt);
+        xl.fetch(slam + o * DK + ktile * NT, s.H * DK, nt);
         xv.fetch(v + o * DV, s.H * DV, nt);
         xdy.fetch(dy + o * DV, s.H * DV, nt);
         xr.fetch(r + o, s.H, nt);
-        if constexpr (SV) {
-            xl.fetch(slam + o * DK + ktile * NT, s.H * DK, nt);
-            const float* lp0 = t > 0 ? slam + (o - s.H) * DK
-                                     : (lam0_one ? slam + o * DK : g.lam0 + (size_t)bh * DK);
-            xlp.fetch(lp0 + ktile * NT, 0, 1);
-        }
+        const float* lp0 = t > 0 ? slam + (o - s.H) * DK : (lam0_one ? slam + o * DK : g.lam0 + (size_t)bh * DK);
+        xlp.fetch(lp0 + ktile * NT, 0, 1);
     };
     auto commit = [&]() {
         wait_vm_all();   // the prefetch has landed (and stores issued before it are done)
         xa.template commit<ROW>(sIn, CA);
         xp.template commit<ROW>(sIn, CP);
         xk.template commit<ROW>(sIn, CK);
+        xl.template commit<ROW>(sIn, CL);
         xv.template commit<ROW>(sIn, CV);
         xdy.template commit<ROW>(sIn, CD);
         xr.template commit<ROW>(sIn, CR);
-        if constexpr (SV) {
-            xl.template commit<ROW>(sIn, CL);
-            xlp.template commit<NT>(sLP, 0);
-        }
+        xlp.template commit<NT>(sLP, 0);
     };
 
     // blocks staged as in the forward: blk from LDS, blk + 1 in registers
@@ -373,54 +437,34 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     barrier_lds();
     for (int blk = 0; blk < nblk; ++blk) {
         const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
-        float olam = 0.f, odqt = 0.f;
-        if constexpr (SV) {   // the gates of every (token, slot) from the saved lam_{t-1}, in parallel
+        {   // the gates of every (token, slot) from the saved lam_{t-1}, in parallel
             const float* row = sIn + gj * ROW;
             const float ra = row[CA + gsl], rp = row[CP + gsl];
             const float at = ou ? goa : ra, pt = ou ? gop : rp;
             const float lp = gj > 0 ? row[CL + gsl - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[gsl]);
             const float rho = rcp(at * at + pt * lp);
             sFK[gj][gsl] = make_float2(at * rho, row[CR] * row[CK + gsl]);
-            barrier_lds();
         }
+        barrier_lds();
+        float odqt = 0.f;
 #pragma unroll
         for (int j = 0; j < kTB; ++j) {   // no branch: rows past nt only reach selects
             const bool live = j < nt;
             const float* row = sIn + j * ROW;
-            float F, kh;
-            if constexpr (SV) {
-                const float2 fk = sFK[j][nl];
-                F = fk.x;
-                kh = fk.y;
-            } else {
-                const float ra = row[CA + nl], rp = row[CP + nl];
-                const float at = ou ? oa : ra, pt = ou ? op : rp;
-                const float kt = row[CK + nl], rt = row[CR];
-                const float rho = rcp(at * at + pt * lam);
-                F = at * rho;
-                kh = rt * kt;
-                lam = live ? rho * lam + kt * kt * rt : lam;
-            }
+            const float2 fk = sFK[j][nl];   // F, r k
             float acc = 0.f;
 #pragma unroll
             for (int i = 0; i < DPER; ++i) {
-                const float hn = F * Hs[i] + kh * row[CV + dl + i * DL];
+                const float hn = fk.x * Hs[i] + fk.y * row[CV + dl + i * DL];
                 Hs[i] = live ? hn : Hs[i];
                 acc += hn * row[CD + dl + i * DL];
             }
             acc = group_sum<16>(acc);
-            if (dl == j) {   // lane j of the slot's row keeps token j's results
-                olam = lam;
-                odqt = acc;
-            }
+            if (dl == j) odqt = acc;   // lane j of the slot's row keeps token j's result
         }
         barrier_lds();
         commit();
-        if (dl < nt) {
-            const size_t o = ((row0 + t0 + dl) * s.H + h) * DK + n;
-            if constexpr (!SV) wlam[o] = olam;
-            wdqt[o] = odqt;
-        }
+        if (dl < nt) wdqt[((row0 + t0 + dl) * s.H + h) * DK + n] = odqt;
         fetch(min(blk + 2, nblk - 1) * kTB);
         barrier_lds();
     }
@@ -883,18 +927,13 @@ struct FwdL {
 template <typename S, int DK, int DV>
 struct BwdL {
     static hipError_t run(const Shape& s, const BwdArgs& a, const float* saved_lam, void* ws, hipStream_t st) {
+        if (!saved_lam) return hipErrorInvalidValue;
         const size_t ntok = (size_t)s.B * s.T * s.H * DK;
-        float* wlam = static_cast<float*>(ws);
-        float* wdqt = wlam + ntok;
+        float* wdqt = static_cast<float*>(ws);
         float* wPT = wdqt + ntok;
-        const dim3 grid1(s.B * s.H * (DK / 16));
-        if (saved_lam)
-            hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV, true>), grid1, dim3(kThreads), 0, st, s, a, saved_lam,
-                               wlam, wdqt, wPT);
-        else
-            hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV, false>), grid1, dim3(kThreads), 0, st, s, a, nullptr,
-                               wlam, wdqt, wPT);
-        const float* lam_t = saved_lam ? saved_lam : wlam;
+        hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV>), dim3(s.B * s.H * (DK / 16)), dim3(kThreads), 0, st, s, a,
+                           saved_lam, wdqt, wPT);
+        const float* lam_t = saved_lam;
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         auto kern = bwd_sweep2_kernel<S, DK, DV>;
@@ -927,9 +966,10 @@ hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, float* sav
 // one part per batch row: the recurrent backward walks a whole (b, h) in one workgroup
 int recurrent_ou_parts(const Shape& s) { return s.B; }
 
+// dqt_t [B, T, H, dk] and PT [B, H, dk]
 size_t backward_recurrent_workspace(const Shape& s) {
     const size_t ntok = (size_t)s.B * s.T * s.H * s.dk;
-    return (2 * ntok + (size_t)s.B * s.H * s.dk) * sizeof(float);
+    return (ntok + (size_t)s.B * s.H * s.dk) * sizeof(float);
 }
 
 hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, const float* saved_lam, void* ws,
