@@ -19,7 +19,7 @@ namespace kla {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTB = 16;  // tokens per staged block (forward, sweep 1)
+constexpr int kTB = 16;  // tokens per staged block of sweep 1
 
 // Per-token inputs reach the kernels in blocks of ROWS tokens, staged in LDS as
 // rows of floats.  A Part is one tensor's W values per token: each thread
