@@ -60,17 +60,12 @@ struct Part {
 // sequence would lengthen the per-token precision chain several times over.
 __device__ __forceinline__ float rcp(float x) { return __builtin_amdgcn_rcpf(x); }
 
-// Sum over groups of W consecutive lanes with DPP moves.  W = 16: every lane of
-// a 16-lane row holds the row sum.  W = 32: the sum of each half wave lands in
-// its upper 16 lanes (16..31, 48..63).
-template <int W>
-__device__ __forceinline__ float group_sum(float x) {
-    static_assert(W == 16 || W == 32, "group width");
+// Sum over each 16-lane row with DPP moves, held by every lane of the row.
+__device__ __forceinline__ float row_sum16(float x) {
     x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
     x += dpp<0x4E, 0xf>(x);    // quad_perm [2,3,0,1]
     x += dpp<0x141, 0xf>(x);   // row_half_mirror
     x += dpp<0x140, 0xf>(x);   // row_mirror
-    if constexpr (W == 32) x += dpp<0x142, 0xa>(x);   // row_bcast:15 into rows 1 and 3
     return x;
 }
 
@@ -85,7 +80,8 @@ __device__ __forceinline__ float row_shr(float x) {
 // group: W = 32 exchanges the two row sums with a swizzle (lane l reads lane l ^ 16).
 template <int W>
 __device__ __forceinline__ float group_sum_all(float x) {
-    x = group_sum<16>(x);
+    static_assert(W == 16 || W == 32, "group width");
+    x = row_sum16(x);
     if constexpr (W == 32)
         x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
     return x;
@@ -459,7 +455,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
                 Hs[i] = live ? hn : Hs[i];
                 acc += hn * row[CD + dl + i * DL];
             }
-            acc = group_sum<16>(acc);
+            acc = row_sum16(acc);
             if (dl == j) odqt = acc;   // lane j of the slot's row keeps token j's result
         }
         barrier_lds();
@@ -473,7 +469,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
 #pragma unroll
         for (int i = 0; i < DPER; ++i) acc += g.detaT[((size_t)bh * DK + n) * DV + dl + i * DL] * Hs[i];
     }
-    acc = group_sum<16>(acc);
+    acc = row_sum16(acc);
     if (dl == 0) wPT[(size_t)bh * DK + n] = acc;
 }
 
