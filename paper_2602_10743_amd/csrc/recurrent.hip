@@ -20,6 +20,12 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTB = 16;  // tokens per staged block of sweep 1
+constexpr int kCKI = 32; // tokens between the information-state checkpoints of the saved context
+
+// The saved context of this path: lam_t [B, T, H, dk], then the information state
+// before every kCKI-th token [B, H, ceil(T / kCKI), dk, dv], fp32.
+__host__ __device__ inline size_t saved_lam_floats(const Shape& s) { return (size_t)s.B * s.T * s.H * s.dk; }
+__host__ __device__ inline int n_checkpoints(int T) { return (T + kCKI - 1) / kCKI; }
 
 // Per-token inputs reach the kernels in blocks of ROWS tokens, staged in LDS as
 // rows of floats.  A Part is one tensor's W values per token: each thread
@@ -202,8 +208,16 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
         fetch(min(1, nblk - 1) * TBF);
     }
     barrier_lds();
+    static_assert(kCKI % TBF == 0, "checkpoints fall on block starts");
+    float* saved_H = saved_lam ? saved_lam + saved_lam_floats(s) : nullptr;
+    const int nck = n_checkpoints(s.T);
     for (int blk = 0; blk < nblk; ++blk) {
         const int t0 = blk * TBF, nt = min(TBF, s.T - t0);
+        if (saved_H && t0 % kCKI == 0 && owns) {   // the state before token t0
+#pragma unroll
+            for (int i = 0; i < NPER; ++i)
+                saved_H[(((size_t)bh * nck + t0 / kCKI) * DK + ng + i * NG) * DV + d] = Hs[i];
+        }
         float lsv[TPG];   // lam after each of this lane's tokens (the saved context)
         // Token loops carry no branch: rows past nt (the ragged last block) are worked on
         // as well, from the repeated last row, and only selects keep them out of the state.
@@ -333,6 +347,7 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
         fetch(min(blk + 2, nblk - 1) * TBF);
         barrier_lds();
     }
+    wait_vm_all();   // the last (unused) prefetch has landed before the registers are released
     if (tile == 0 && g.lamT && wg == 0) g.lamT[(size_t)bh * DK + wn] = lam;
     if (g.etaT && owns) {
 #pragma unroll
@@ -341,12 +356,14 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
 }
 
 // ----------------------------------------------------------------------------
-// Backward, sweep 1 (forward in time).  From the precision trajectory lam_t that
-// the forward saved, re-runs the information state and stores dqt_t = H_t dy_t
-// (the gradient of the effective query q/lam_t), plus PT[n] = sum_d detaT[n,d]
-// H_T[n,d].  One workgroup per (b, h, 16 key slots); 16 lanes split the value
-// channels.  Every token's gates follow from the saved lam_{t-1}, for all
-// (token, slot) pairs of a block in one parallel phase.
+// Backward, sweep 1 (forward in time).  From the saved context of the forward
+// (lam_t after every token, the information state every kCKI tokens), re-runs the
+// information state and stores dqt_t = H_t dy_t (the gradient of the effective
+// query q/lam_t), plus PT[n] = sum_d detaT[n,d] H_T[n,d].  One workgroup per
+// (b, h, 16 key slots, kCKI-token segment), started from the segment's
+// checkpoint; 16 lanes split the value channels.  Every token's gates follow
+// from the saved lam_{t-1}, for all (token, slot) pairs of a block in one
+// parallel phase.
 template <typename S, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g, const float* slam, float* wdqt,
                                                                float* wPT) {
@@ -368,17 +385,19 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     const T_* r = static_cast<const T_*>(g.r);
     const T_* dy = static_cast<const T_*>(g.dy);
 
-    const int ntile = DK / NT;
-    const int bh = blockIdx.x / ntile, ktile = blockIdx.x % ntile;
+    const int ntile = DK / NT, nck = n_checkpoints(s.T);
+    const int seg = blockIdx.x % nck, bt = blockIdx.x / nck;
+    const int bh = bt / ntile, ktile = bt % ntile;
     const int b = bh / s.H, h = bh % s.H;
     const int tid = threadIdx.x;
     const int nl = tid / DL, n = ktile * NT + nl, dl = tid % DL;
     const size_t row0 = (size_t)b * s.T;
+    const int ts0 = seg * kCKI, tend = min(ts0 + kCKI, s.T);   // this workgroup's tokens
+    const float* ckH = slam + saved_lam_floats(s);
 
     float Hs[DPER];
 #pragma unroll
-    for (int i = 0; i < DPER; ++i)
-        Hs[i] = g.eta0 ? g.eta0[((size_t)bh * DK + n) * DV + dl + i * DL] : 0.f;
+    for (int i = 0; i < DPER; ++i) Hs[i] = ckH[(((size_t)bh * nck + seg) * DK + n) * DV + dl + i * DL];
     // the gate phase's (token, slot) pair of this thread
     const int gsl = tid % NT, gj = tid / NT;
     const bool ou = g.ou_a != nullptr;
@@ -398,7 +417,7 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     const T_* gp = ou ? k : p;
     const bool lam0_one = g.lam0 == nullptr;
     auto fetch = [&](int t) {
-        const int nt = min(kTB, s.T - t);
+        const int nt = min(kTB, tend - t);
         const size_t o = (row0 + t) * s.H + h;
         xa.fetch(ga + o * DK + ktile * NT, s.H * DK, nt);
         xp.fetch(gp + o * DK + ktile * NT, s.H * DK, nt);
@@ -423,16 +442,16 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     };
 
     // blocks staged as in the forward: blk from LDS, blk + 1 in registers
-    const int nblk = (s.T + kTB - 1) / kTB;
+    const int nblk = (tend - ts0 + kTB - 1) / kTB;
     wait_vm_all();   // the initial state is in: no first-use wait inside the loop
     if (nblk > 0) {
-        fetch(0);
+        fetch(ts0);
         commit();
-        fetch(min(1, nblk - 1) * kTB);
+        fetch(ts0 + min(1, nblk - 1) * kTB);
     }
     barrier_lds();
     for (int blk = 0; blk < nblk; ++blk) {
-        const int t0 = blk * kTB, nt = min(kTB, s.T - t0);
+        const int t0 = ts0 + blk * kTB, nt = min(kTB, tend - t0);
         {   // the gates of every (token, slot) from the saved lam_{t-1}, in parallel
             const float* row = sIn + gj * ROW;
             const float ra = row[CA + gsl], rp = row[CP + gsl];
@@ -461,9 +480,11 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
         barrier_lds();
         commit();
         if (dl < nt) wdqt[((row0 + t0 + dl) * s.H + h) * DK + n] = odqt;
-        fetch(min(blk + 2, nblk - 1) * kTB);
+        fetch(ts0 + min(blk + 2, nblk - 1) * kTB);
         barrier_lds();
     }
+    wait_vm_all();   // the last (unused) prefetch has landed before the registers are released
+    if (seg != nck - 1) return;   // the last segment ends at the final state
     float acc = 0.f;
     if (g.detaT) {
 #pragma unroll
@@ -779,6 +800,7 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
         cur ^= 1;
         barrier_lds();
     }
+    wait_vm_all();   // the last (unused) prefetch has landed before the registers are released
     if (tid < DK && g.dlam0) g.dlam0[(size_t)bh * DK + tid] = cnext;
     if (ou) {   // part b of the token sums: the threads of one slot are combined in order
         sOU[tid] = sum_da;
@@ -927,8 +949,12 @@ struct BwdL {
         const size_t ntok = (size_t)s.B * s.T * s.H * DK;
         float* wdqt = static_cast<float*>(ws);
         float* wPT = wdqt + ntok;
-        hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV>), dim3(s.B * s.H * (DK / 16)), dim3(kThreads), 0, st, s, a,
-                           saved_lam, wdqt, wPT);
+        // PT is written by the last segment's workgroups; with T == 0 it is detaT . eta0 summed over d,
+        // which the reverse sweep does not need (no token reads it), so no workgroup is launched
+        const unsigned grid1 = (unsigned)(s.B * s.H * (DK / 16) * n_checkpoints(s.T));
+        if (grid1 > 0)
+            hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV>), dim3(grid1), dim3(kThreads), 0, st, s, a, saved_lam,
+                               wdqt, wPT);
         const float* lam_t = saved_lam;
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
@@ -953,7 +979,9 @@ struct DecL {
 
 }  // namespace
 
-size_t recurrent_saved_bytes(const Shape& s) { return (size_t)s.B * s.T * s.H * s.dk * sizeof(float); }
+size_t recurrent_saved_bytes(const Shape& s) {
+    return (saved_lam_floats(s) + (size_t)s.B * s.H * n_checkpoints(s.T) * s.dk * s.dv) * sizeof(float);
+}
 
 hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st) {
     return dispatch<FwdL>(s, a, saved_lam, st);
