@@ -684,8 +684,15 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
         }
         barrier_lds();
         // ---- B
+        // tokens latest first, in runs of UB unrolled tokens: the whole block for small heads,
+        // shorter runs where a thread holds many dH entries (keeps the loads in registers)
+        constexpr int UB = NPER * DPER <= 2 ? TB : NPER * DPER <= 4 ? 8 : NPER * DPER <= 16 ? 4 : 2;
+        static_assert(TB % UB == 0, "runs split the block");
+#pragma unroll 1
+        for (int jb = TB - UB; jb >= 0; jb -= UB)
 #pragma unroll
-        for (int j = TB - 1; j >= 0; --j) {   // no branch: rows past nt only reach selects
+        for (int jj = UB - 1; jj >= 0; --jj) {   // no branch: rows past nt only reach selects
+            const int j = jb + jj;
             const bool live = j < nt;
             const float* row = sIn + j * ROW;
             float dyd[DPER], vd[DPER], pv[DPER];
