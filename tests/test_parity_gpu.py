@@ -137,6 +137,39 @@ def test_backward_default_belief_ragged(kla, dk, dv):
     log("  " + " ".join(rep))
 
 
+@pytest.mark.parametrize("T", [15, 16, 31, 32, 33, 64, 65])
+def test_recurrent_block_boundaries(kla, T):
+    """fp32 token-recurrent path around its block (16 / 32 tokens) and state-checkpoint
+    (32 tokens) boundaries: forward with a saved context, backward from it and from a
+    recomputed one (bitwise equal), against the oracle."""
+    B, H, dk, dv = 2, 3, 32, 32
+    case = K.random_case(B, T, H, dk, dv, "f32", seed=T + 101, dist="c0")
+    lam0, eta0 = _random_belief(B, H, dk, dv, T + 7)
+    g = np.random.default_rng(T + 5)
+    dlamT = g.standard_normal((B, H, dk)).astype(np.float32).astype(np.float64)
+    detaT = g.standard_normal((B, H, dk, dv)).astype(np.float32).astype(np.float64)
+    log(f"recurrent boundaries B{B} T{T} H{H} dk{dk} dv{dv} f32")
+    x = _dev_inputs(case, "f32")
+    f32 = lambda a: torch.tensor(a, dtype=torch.float32, device=DEV)
+    out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), want_var=True,
+                          save=True)
+    gr = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), x["dy"],
+                          f32(dlamT), f32(detaT), saved=out["saved"])
+    gr2 = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), x["dy"],
+                           f32(dlamT), f32(detaT))
+    torch.cuda.synchronize()
+    ref = oracle.forward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0)
+    rg = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0, case["dy"],
+                         dlamT, detaT)
+    rep = []
+    for n in ("y", "yvar", "lamT", "etaT"):
+        _check(n, to_np(out[n]), ref[n], TOL["f32"], rep)
+    for n in ("dq", "dk", "dv", "da", "dp", "dr", "dlam0", "deta0"):
+        _check(n, to_np(gr[n]), rg[n], TOL["f32"], rep)
+        assert torch.equal(gr[n], gr2[n]), f"{n} differs between saved and recomputed context"
+    log("  " + " ".join(rep))
+
+
 def test_empty_and_single_token(kla):
     for T in (0, 1):
         case = K.random_case(2, T, 2, 32, 16, "f32", seed=5)
