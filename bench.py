@@ -294,6 +294,14 @@ def bench_a5(args, dev):
     x = {n: torch.from_numpy(np.ascontiguousarray(bits[n])).to(dev) for n in bits}
     del bits
     stream = torch.cuda.current_stream(dev)
+    if args.copy_calibration:
+        from paper_2602_10743_amd.traffic import COPY_BYTES
+        src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(2):
+            torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     def step(ev=None):
         if ev is not None:
@@ -321,6 +329,8 @@ def bench_a5(args, dev):
     fwd_b, bwd_b = algorithmic_bytes(w, 4)
     dom, ms, nbytes = ("kla_backward", bwd_ms, bwd_b * th) if bwd_ms >= fwd_ms else ("kla_forward", fwd_ms, fwd_b * th)
     achieved = nbytes / (ms * 1e-3) / 1e9
+    from paper_2602_10743_amd.traffic import DIGEST_SOURCES_A5, load_summary
+    measured = load_summary(os.path.join(ROOT, "profiles", "a5_state_tracking_traffic.md"), DIGEST_SOURCES_A5)
     res = {
         "metric": METRIC, "value": th / (wall / args.steps), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps,
@@ -328,7 +338,8 @@ def bench_a5(args, dev):
         "config": {"workload": w.name, "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv, "pass": "fwd+bwd",
                    "tokens_counted": "B*T*H"},
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "algorithmic_bytes_per_call": nbytes,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured.get(dom) if measured else None,
+                     "traffic_unit": "bytes per call", "algorithmic_bytes_per_call": nbytes,
                      "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
                      "note": "token-recurrent kernels (fp32 inputs)"},
     }

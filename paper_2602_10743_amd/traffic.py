@@ -18,6 +18,10 @@ Run from the repository root on the GPU machine (TMPDIR=/tmp):
 With OU gates: the same two runs with `bench.py ... --ou`, then
   python -m paper_2602_10743_amd.traffic D/fetch D/write --ou > profiles/lm_layer_ou_traffic.md
 
+The state-tracking workload (fp32, token-recurrent kernels): the same two runs with
+`bench.py --a5 --steps 2 --warmup 1 --copy-calibration`, then
+  python -m paper_2602_10743_amd.traffic D/fetch D/write --a5 > profiles/a5_state_tracking_traffic.md
+
 MFMA and VALU utilisation per kernel come from a third run:
   rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU \\
       GRBM_GUI_ACTIVE --output-format csv -d D/util -o run -- \\
@@ -42,6 +46,10 @@ CALLS_OU = {
     "kla_forward_ou": ("fwd_chunk_kernel",),
     "kla_backward_ou": ("bwd_dv_kernel", "bwd_dk_kernel", "dr_combine_kernel", "ou_param_grads_kernel"),
 }
+CALLS_A5 = {
+    "kla_forward": ("fwd_recurrent_kernel",),
+    "kla_backward": ("bwd_sweep1_kernel", "bwd_sweep2_kernel"),
+}
 SUMMARY_KEY = "traffic_bytes_per_call"
 
 
@@ -50,12 +58,15 @@ SUMMARY_KEY = "traffic_bytes_per_call"
 DIGEST_SOURCES = ("kla_api.cpp", "kla_internal.hpp", "kla_device.hpp", "kla_buf.hpp", "kla_mfma.hpp",
                   "kla_chunk.hpp", "chunk_fwd.hip", "chunk_bwd_dv.hip", "chunk_bwd_dk.hip", "ou.hip",
                   "validate.hip")
+# ... and of the token-recurrent kernels (the state-tracking workload)
+DIGEST_SOURCES_A5 = ("kla_api.cpp", "kla_internal.hpp", "kla_device.hpp", "kla_buf.hpp", "recurrent.hip",
+                     "validate.hip")
 
 
-def sources_digest() -> str:
+def sources_digest(names=DIGEST_SOURCES) -> str:
     """sha256 over the sources of the measured kernels, in name order."""
     h = hashlib.sha256()
-    for name in sorted(DIGEST_SOURCES):
+    for name in sorted(names):
         h.update(name.encode())
         with open(os.path.join(HERE, "csrc", name), "rb") as f:
             h.update(f.read())
@@ -95,9 +106,10 @@ def _per_call(vals: dict, scale: float, calls: dict) -> dict:
     return out
 
 
-def summarise(fetch_dir: str, write_dir: str, ou: bool = False) -> str:
-    calls = CALLS_OU if ou else CALLS
-    flag = " --ou" if ou else ""
+def summarise(fetch_dir: str, write_dir: str, ou: bool = False, a5: bool = False) -> str:
+    calls = CALLS_A5 if a5 else CALLS_OU if ou else CALLS
+    flag = " --a5" if a5 else " --ou" if ou else ""
+    names = DIGEST_SOURCES_A5 if a5 else DIGEST_SOURCES
     fetch = _counter(fetch_dir, "FETCH_SIZE")
     write = _counter(write_dir, "WRITE_SIZE")
     kla_names = tuple(k for ks in calls.values() for k in ks)
@@ -109,12 +121,14 @@ def summarise(fetch_dir: str, write_dir: str, ou: bool = False) -> str:
     f_write = COPY_BYTES / max(write[copy])
     rd = _per_call(fetch, f_fetch, calls)
     wr = _per_call(write, f_write, calls)
+    title = ("state-tracking workload (B=64, T=512, H=4, d=32, fp32)" if a5 else
+             "lm-layer workload (B=8, T=2048, H=16, d=128, bf16" + (", OU gates)" if ou else ")"))
     lines = [
-        "# HBM traffic per call, lm-layer workload (B=8, T=2048, H=16, d=128, bf16"
-        + (", OU gates)" if ou else ")"),
+        "# HBM traffic per call, " + title,
         "",
         "Counters: FETCH_SIZE and WRITE_SIZE from two separate `rocprofv3 --pmc` runs of",
-        f"`python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration{flag}`, scaled by",
+        ("`python bench.py --a5 --steps 2 --warmup 1 --copy-calibration`, scaled by" if a5 else
+         f"`python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration{flag}`, scaled by"),
         f"the calibration copy kernel `{copy}` ({COPY_BYTES} bytes read and written):",
         f"fetch scale {f_fetch:.4f} bytes/unit, write scale {f_write:.4f} bytes/unit.",
         "",
@@ -125,16 +139,16 @@ def summarise(fetch_dir: str, write_dir: str, ou: bool = False) -> str:
         lines.append(f"| {call} | {rd[call]:.4g} | {wr[call]:.4g} | {rd[call] + wr[call]:.4g} |")
     lines += [
         "",
-        f"sources: {sources_digest()}",
+        f"sources: {sources_digest(names)}",
         f"{SUMMARY_KEY}: " + ", ".join(f"{c}={rd[c] + wr[c]:.6g}" for c in calls),
         "",
     ]
     return "\n".join(lines)
 
 
-def load_summary(path: str):
+def load_summary(path: str, names=DIGEST_SOURCES):
     """{call: bytes} from a summary written by summarise(), or None when the file
-    is missing or was taken from different kernel sources."""
+    is missing or was taken from different kernel sources (names: the digest's sources)."""
     if not os.path.exists(path):
         return None
     digest, values = None, None
@@ -146,7 +160,7 @@ def load_summary(path: str):
             for item in line.split(":", 1)[1].split(","):
                 k, v = item.strip().split("=")
                 values[k] = float(v)
-    if digest != sources_digest() or values is None:
+    if digest != sources_digest(names) or values is None:
         return None
     return values
 
@@ -215,8 +229,9 @@ if __name__ == "__main__":
         print(summarise_util(sys.argv[2]))
         sys.exit(0)
     ou = "--ou" in sys.argv[1:]
-    args = [a for a in sys.argv[1:] if a != "--ou"]
+    a5 = "--a5" in sys.argv[1:]
+    args = [a for a in sys.argv[1:] if a not in ("--ou", "--a5")]
     if len(args) != 2:
         print(__doc__, file=sys.stderr)
         sys.exit(2)
-    print(summarise(args[0], args[1], ou=ou))
+    print(summarise(args[0], args[1], ou=ou, a5=a5))
