@@ -196,10 +196,8 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
 
     // Block blk is worked on from LDS while block blk + 1 is in registers; after its
     // outputs are formed, block blk + 1 goes to LDS, the outputs are stored and block
-    // blk + 2 is fetched.  The fetch comes last: rewriting a register that an in-flight
-    // store reads waits for that store, and with the loads issued after the stores such a
-    // wait does not also wait for the prefetch.  Fetches past the end fetch the last block
-    // again (unused), so they stay unconditional.
+    // blk + 2 is fetched, a whole block ahead of its commit.  Fetches past the end fetch
+    // the last block again (unused), so they stay unconditional.
     const int nblk = (s.T + TBF - 1) / TBF;
     wait_vm_all();   // the initial state is in: no first-use wait inside the loop
     if (nblk > 0) {
