@@ -112,6 +112,35 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(int B, int T, int C, cons
             for (int e = 0; e < V; ++e) f[e] = 0.f;
         }
     };
+    if (t1 - t0 == kTT) {
+        // a full run: every load of the run unconditional (history before token 0 read from
+        // token 0 and replaced by zeros), so the unrolled loop can issue them all up front
+        const size_t r0 = (size_t)b * T * C + c0;
+        auto hist = [&](int t, float* f) {
+            Vec<S>::load(x, r0 + (size_t)max(t, 0) * C, f);
+#pragma unroll
+            for (int e = 0; e < V; ++e) f[e] = t >= 0 ? f[e] : 0.f;
+        };
+        hist(t0 - 3, h3);
+        hist(t0 - 2, h2);
+        hist(t0 - 1, h1);
+#pragma unroll
+        for (int i = 0; i < kTT; ++i) {
+            const int t = t0 + i;
+            float cur[V], out[V];
+            Vec<S>::load(x, r0 + (size_t)t * C, cur);
+#pragma unroll
+            for (int e = 0; e < V; ++e) {
+                const float s = fmaf(wk[3][e], cur[e], fmaf(wk[2][e], h1[e], fmaf(wk[1][e], h2[e], fmaf(wk[0][e], h3[e], bs[e]))));
+                out[e] = s * sigm(s);
+                h3[e] = h2[e];
+                h2[e] = h1[e];
+                h1[e] = cur[e];
+            }
+            Vec<S>::store(u, r0 + (size_t)t * C, out);
+        }
+        return;
+    }
     load_or_zero(t0 - 3, h3);
     load_or_zero(t0 - 2, h2);
     load_or_zero(t0 - 1, h1);
@@ -169,40 +198,88 @@ __global__ __launch_bounds__(256) void conv_bwd_kernel(int B, int T, int C, cons
         const int ts = min(T - 1, t1 + 2);   // the last token whose ds reaches this tile's dx
         // x window for token t: x[t], x[t-1], x[t-2], x[t-3]; ds of tokens t+1, t+2, t+3
         float x0[V], x1[V], x2[V], x3[V], d1[V], d2[V], d3[V];
-        load_or_zero(x, ts, x0);
-        load_or_zero(x, ts - 1, x1);
-        load_or_zero(x, ts - 2, x2);
-        load_or_zero(x, ts - 3, x3);
+        if (t1 - t0 == kTT && t1 + 3 <= T) {
+            // a full run with its 3 halo tokens inside the sequence: the unrolled loop has
+            // no branch (x before token 0 is read from token 0 and replaced by zeros), so
+            // every load of the run can be issued up front
+            const size_t r0 = (size_t)b * T * C + c0;
+            auto xat = [&](int t, float* f) {
+                Vec<S>::load(x, r0 + (size_t)max(t, 0) * C, f);
 #pragma unroll
-        for (int e = 0; e < V; ++e) d1[e] = d2[e] = d3[e] = 0.f;
-        for (int t = ts; t >= t0; --t) {
-            float g[V], ds[V], xn[V];
-            load_or_zero(du, t, g);
-            load_or_zero(x, t - 4, xn);
-            const bool own = t < t1;
-            float dxo[V];
+                for (int e = 0; e < V; ++e) f[e] = t >= 0 ? f[e] : 0.f;
+            };
+            xat(ts, x0);
+            xat(ts - 1, x1);
+            xat(ts - 2, x2);
+            xat(ts - 3, x3);
 #pragma unroll
-            for (int e = 0; e < V; ++e) {
-                const float s = fmaf(wk[3][e], x0[e], fmaf(wk[2][e], x1[e], fmaf(wk[1][e], x2[e], fmaf(wk[0][e], x3[e], bs[e]))));
-                const float sg = sigm(s);
-                ds[e] = g[e] * sg * fmaf(s, 1.f - sg, 1.f);
-                dxo[e] = fmaf(wk[3][e], ds[e], fmaf(wk[2][e], d1[e], fmaf(wk[1][e], d2[e], wk[0][e] * d3[e])));
-                if (own) {
-                    gw[3][e] = fmaf(ds[e], x0[e], gw[3][e]);
-                    gw[2][e] = fmaf(ds[e], x1[e], gw[2][e]);
-                    gw[1][e] = fmaf(ds[e], x2[e], gw[1][e]);
-                    gw[0][e] = fmaf(ds[e], x3[e], gw[0][e]);
-                    gb[e] += ds[e];
+            for (int e = 0; e < V; ++e) d1[e] = d2[e] = d3[e] = 0.f;
+#pragma unroll
+            for (int i = 0; i < kTT + 3; ++i) {
+                const int t = ts - i;
+                constexpr int kHalo = 3;
+                float g[V], ds[V], xn[V], dxo[V];
+                Vec<S>::load(du, r0 + (size_t)t * C, g);
+                xat(t - 4, xn);
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    const float s = fmaf(wk[3][e], x0[e], fmaf(wk[2][e], x1[e], fmaf(wk[1][e], x2[e], fmaf(wk[0][e], x3[e], bs[e]))));
+                    const float sg = sigm(s);
+                    ds[e] = g[e] * sg * fmaf(s, 1.f - sg, 1.f);
+                    dxo[e] = fmaf(wk[3][e], ds[e], fmaf(wk[2][e], d1[e], fmaf(wk[1][e], d2[e], wk[0][e] * d3[e])));
+                    if (i >= kHalo) {   // the run's own tokens
+                        gw[3][e] = fmaf(ds[e], x0[e], gw[3][e]);
+                        gw[2][e] = fmaf(ds[e], x1[e], gw[2][e]);
+                        gw[1][e] = fmaf(ds[e], x2[e], gw[1][e]);
+                        gw[0][e] = fmaf(ds[e], x3[e], gw[0][e]);
+                        gb[e] += ds[e];
+                    }
+                    d3[e] = d2[e];
+                    d2[e] = d1[e];
+                    d1[e] = ds[e];
+                    x0[e] = x1[e];
+                    x1[e] = x2[e];
+                    x2[e] = x3[e];
+                    x3[e] = xn[e];
                 }
-                d3[e] = d2[e];
-                d2[e] = d1[e];
-                d1[e] = ds[e];
-                x0[e] = x1[e];
-                x1[e] = x2[e];
-                x2[e] = x3[e];
-                x3[e] = xn[e];
+                if (i >= kHalo) Vec<S>::store(dx, r0 + (size_t)t * C, dxo);
             }
-            if (own) Vec<S>::store(dx, ((size_t)b * T + t) * C + c0, dxo);
+        } else {
+            load_or_zero(x, ts, x0);
+            load_or_zero(x, ts - 1, x1);
+            load_or_zero(x, ts - 2, x2);
+            load_or_zero(x, ts - 3, x3);
+#pragma unroll
+            for (int e = 0; e < V; ++e) d1[e] = d2[e] = d3[e] = 0.f;
+            for (int t = ts; t >= t0; --t) {
+                float g[V], ds[V], xn[V];
+                load_or_zero(du, t, g);
+                load_or_zero(x, t - 4, xn);
+                const bool own = t < t1;
+                float dxo[V];
+#pragma unroll
+                for (int e = 0; e < V; ++e) {
+                    const float s = fmaf(wk[3][e], x0[e], fmaf(wk[2][e], x1[e], fmaf(wk[1][e], x2[e], fmaf(wk[0][e], x3[e], bs[e]))));
+                    const float sg = sigm(s);
+                    ds[e] = g[e] * sg * fmaf(s, 1.f - sg, 1.f);
+                    dxo[e] = fmaf(wk[3][e], ds[e], fmaf(wk[2][e], d1[e], fmaf(wk[1][e], d2[e], wk[0][e] * d3[e])));
+                    if (own) {
+                        gw[3][e] = fmaf(ds[e], x0[e], gw[3][e]);
+                        gw[2][e] = fmaf(ds[e], x1[e], gw[2][e]);
+                        gw[1][e] = fmaf(ds[e], x2[e], gw[1][e]);
+                        gw[0][e] = fmaf(ds[e], x3[e], gw[0][e]);
+                        gb[e] += ds[e];
+                    }
+                    d3[e] = d2[e];
+                    d2[e] = d1[e];
+                    d1[e] = ds[e];
+                    x0[e] = x1[e];
+                    x1[e] = x2[e];
+                    x2[e] = x3[e];
+                    x3[e] = xn[e];
+                }
+                if (own) Vec<S>::store(dx, ((size_t)b * T + t) * C + c0, dxo);
+            }
         }
     }
 #pragma unroll
