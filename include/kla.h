@@ -79,7 +79,7 @@ size_t kla_forward_workspace(const kla_desc* desc);
 /* Bytes of the optional saved context that kla_forward can fill for
  * kla_backward: the precision and information state at every chunk start
  * (chunked path: bf16 inputs with dk >= 32), else the precision after every
- * token and the information state before every 32nd token. */
+ * token and the information state before every 64th token. */
 size_t kla_saved_bytes(const kla_desc* desc);
 
 /* Bytes of device workspace kla_backward needs when it is given a saved

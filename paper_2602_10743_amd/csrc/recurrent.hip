@@ -20,7 +20,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTB = 16;  // tokens per staged block of sweep 1
-constexpr int kCKI = 32; // tokens between the information-state checkpoints of the saved context
+constexpr int kCKI = 64; // tokens between the information-state checkpoints of the saved context
 
 // The saved context of this path: lam_t [B, T, H, dk], then the information state
 // before every kCKI-th token [B, H, ceil(T / kCKI), dk, dv], fp32.

@@ -140,7 +140,7 @@ def test_backward_default_belief_ragged(kla, dk, dv):
 @pytest.mark.parametrize("T", [15, 16, 31, 32, 33, 64, 65])
 def test_recurrent_block_boundaries(kla, T):
     """fp32 token-recurrent path around its block (16 / 32 tokens) and state-checkpoint
-    (32 tokens) boundaries: forward with a saved context, backward from it and from a
+    (64 tokens) boundaries: forward with a saved context, backward from it and from a
     recomputed one (bitwise equal), against the oracle."""
     B, H, dk, dv = 2, 3, 32, 32
     case = K.random_case(B, T, H, dk, dv, "f32", seed=T + 101, dist="c0")
