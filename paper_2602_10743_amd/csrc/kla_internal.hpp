@@ -44,9 +44,10 @@ struct DecodeArgs {
     const float *ou_a = nullptr, *ou_p = nullptr, *ou_d = nullptr;
 };
 
-// Token-recurrent kernels.  Their saved context is the precision trajectory
-// lam_t [B, T, H, dk] fp32 (recurrent_saved_bytes(s) bytes): optional for the
-// forward, required by the backward.
+// Token-recurrent kernels.  Their saved context (recurrent_saved_bytes(s) bytes,
+// fp32) is the precision after every token, lam_t [B, T, H, dk], followed by the
+// information state before every 64th token, [B, H, ceil(T / 64), dk, dv]:
+// optional for the forward, required by the backward.
 size_t recurrent_saved_bytes(const Shape& s);
 hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st);
 size_t backward_recurrent_workspace(const Shape& s);

@@ -63,13 +63,23 @@ DIGEST_SOURCES_A5 = ("kla_api.cpp", "kla_internal.hpp", "kla_device.hpp", "kla_b
                      "validate.hip")
 
 
+def code_text(text: str) -> str:
+    """The source without its comments and with whitespace runs collapsed, so
+    that an edit of comments alone leaves the digest as it was (the sources
+    hold no comment markers inside string literals)."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def sources_digest(names=DIGEST_SOURCES) -> str:
-    """sha256 over the sources of the measured kernels, in name order."""
+    """sha256 over the code (comments stripped) of the measured kernels'
+    sources, in name order."""
     h = hashlib.sha256()
     for name in sorted(names):
         h.update(name.encode())
-        with open(os.path.join(HERE, "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(HERE, "csrc", name), encoding="utf-8") as f:
+            h.update(code_text(f.read()).encode())
     return h.hexdigest()
 
 

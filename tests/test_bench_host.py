@@ -69,3 +69,10 @@ def test_digest_sources_exist(names):
     for name in names:
         assert os.path.exists(os.path.join(ROOT, "paper_2602_10743_amd", "csrc", name)), name
     assert "recurrent.hip" in traffic.DIGEST_SOURCES_A5 and "recurrent.hip" not in traffic.DIGEST_SOURCES
+
+
+def test_digest_ignores_comments_only():
+    a = "int f(int x) { // doubles\n  return 2 * x; /* twice */ }\n"
+    b = "/* header */\nint f(int x) {\n    return 2 * x;\n}\n"
+    assert traffic.code_text(a) == traffic.code_text(b)
+    assert traffic.code_text(a) != traffic.code_text(a.replace("2 * x", "3 * x"))
