@@ -254,11 +254,13 @@ struct FwdPc {
 // Backward.  One workgroup per (b, h, CB value channels: 32, 16 at dk = 128); LPC lanes per channel
 // (32, or 16 at dk = 16), lane l owning key slots l % LPC + LPC i of channel
 // l / LPC.  Segments of kCK tokens are taken last to first: stage the segment's
-// inputs, recompute lam and H of its tokens from the checkpoint into registers,
-// then walk its tokens in reverse.  Per token the channel sums (dv, dr) are
-// completed by DPP over the LPC lanes of a channel; the key-slot sums (dq, dk,
-// dabar, dpbar) are added over the channels of a wave by lane shuffles and over
-// the waves through a double-buffered LDS slot, and stored as this tile's part.
+// inputs (fetched into registers one segment ahead), recompute lam and H of its
+// tokens from the checkpoint into registers, then walk its tokens in reverse.
+// Per token the channel sums (dv, dr) are completed by DPP over the LPC lanes of
+// a channel; for the key-slot sums (dq, dk, dabar, dpbar) every channel writes
+// its values to its own row of a double-buffered LDS slot, and after one barrier
+// the rows are added in channel order and stored as this tile's part (no
+// cross-lane shuffles, and the writes need no lane mask).
 // At dk = 128 a lane's 4 elements keep 72 trajectory values in registers, so the
 // workgroup takes 16 channels (2 waves per SIMD, room for them) instead of 32.
 template <int DK, int DV>
@@ -276,12 +278,12 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
     using T_ = typename storage<S>::type;
     constexpr int LPC = PcLanes<DK, DV>::LPC, NPER = PcLanes<DK, DV>::NPER;
     constexpr int CB = PcLanes<DK, DV>::CB;
-    constexpr int NTHR = LPC * CB, NW = NTHR / 64;
+    constexpr int NTHR = LPC * CB;
     static_assert(NTHR % 64 == 0 && (LPC == 16 || LPC == 32), "lane layout");
     __shared__ float4 s_k[kCK][DK];        // abar, pbar, k, q
     __shared__ float4 s_c[kCK][CB];        // r, v, dy, dyvar
     __shared__ float2 s_o[kCK][CB];        // dv, dr
-    __shared__ float s_red[2][NW][4][DK];  // per-wave key-slot sums of dq, dk, dabar, dpbar
+    __shared__ float s_red[2][CB][4][DK];  // per-channel key-slot values of dq, dk, dabar, dpbar
 
     const T_ *q = static_cast<const T_*>(g.q), *k = static_cast<const T_*>(g.k), *v = static_cast<const T_*>(g.v);
     const T_ *a = static_cast<const T_*>(g.a), *p = static_cast<const T_*>(g.p), *r = static_cast<const T_*>(g.r);
@@ -291,7 +293,7 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
     const int ntile = DV / CB;
     const int bh = blockIdx.x / ntile, tile = blockIdx.x % ntile, d0 = tile * CB;
     const int b = bh / s.H, h = bh % s.H;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x;
     const int ln = tid % LPC, c = tid / LPC, d = d0 + c;
     const int T = s.T, nseg = (T + kCK - 1) / kCK;
     const size_t nck = (size_t)s.B * s.H * nseg * DK * DV;
@@ -304,29 +306,57 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
         ge[i] = g.detaT ? g.detaT[o] : 0.f;
         gl[i] = g.dlamT ? g.dlamT[o] : 0.f;
     }
+    // The inputs of a segment and its checkpoint are fetched into registers one segment
+    // ahead (indices clamped to the segment's last token, so every load is issued) and
+    // written to LDS at the start of the segment.
+    constexpr int KPT = (kCK * DK + NTHR - 1) / NTHR, CPT = (kCK * CB + NTHR - 1) / NTHR;
+    float4 nk[KPT], nc[CPT];
+    float nl0[NPER], ne0[NPER];
+    auto fetch = [&](int sg) {
+        const int t0 = sg * kCK, tl = min(kCK, T - t0) - 1;
+#pragma unroll
+        for (int m = 0; m < KPT; ++m) {
+            const int idx = min(tid + NTHR * m, kCK * DK - 1), t = min(idx / DK, tl), n = idx % DK;
+            const size_t o = (((size_t)b * T + t0 + t) * s.H + h) * DK + n;
+            nk[m] = make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
+        }
+#pragma unroll
+        for (int m = 0; m < CPT; ++m) {
+            const int idx = min(tid + NTHR * m, kCK * CB - 1), t = min(idx / CB, tl), cc = idx % CB;
+            const size_t o = (((size_t)b * T + t0 + t) * s.H + h) * DV + d0 + cc;
+            nc[m] = make_float4(ld(r, o), ld(v, o), ld(dy, o), g.dyvar ? g.dyvar[o] : 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < NPER; ++i) {
+            const size_t o = (((size_t)bh * nseg + sg) * DK + ln + LPC * i) * DV + d;
+            nl0[i] = ck[o];
+            ne0[i] = ck[nck + o];
+        }
+    };
+    wait_vm_all();   // the carries are complete before the segment loop
+    if (nseg > 0) fetch(nseg - 1);
     for (int sg = nseg - 1; sg >= 0; --sg) {
         const int t0 = sg * kCK, nt = min(kCK, T - t0);
-        __syncthreads();   // the previous segment's staging and outputs are no longer read
-        for (int idx = tid; idx < nt * DK; idx += NTHR) {
-            const int t = idx / DK, n = idx % DK;
-            const size_t o = (((size_t)b * T + t0 + t) * s.H + h) * DK + n;
-            s_k[t][n] = make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
+        barrier_lds();   // the previous segment's staging and outputs are no longer read
+#pragma unroll
+        for (int m = 0; m < KPT; ++m) {
+            const int idx = tid + NTHR * m;
+            if (KPT * NTHR == kCK * DK || idx < kCK * DK) s_k[idx / DK][idx % DK] = nk[m];
         }
-        for (int idx = tid; idx < nt * CB; idx += NTHR) {
-            const int t = idx / CB, cc = idx % CB;
-            const size_t tok = ((size_t)b * T + t0 + t) * s.H + h;
-            const size_t o = tok * DV + d0 + cc;
-            s_c[t][cc] = make_float4(ld(r, o), ld(v, o), ld(dy, o), g.dyvar ? g.dyvar[o] : 0.f);
+#pragma unroll
+        for (int m = 0; m < CPT; ++m) {
+            const int idx = tid + NTHR * m;
+            if (CPT * NTHR == kCK * CB || idx < kCK * CB) s_c[idx / CB][idx % CB] = nc[m];
         }
         // lam and H before each token of the segment and after its last
         float lt[kCK + 1][NPER], et[kCK + 1][NPER];
 #pragma unroll
         for (int i = 0; i < NPER; ++i) {
-            const size_t o = (((size_t)bh * nseg + sg) * DK + ln + LPC * i) * DV + d;
-            lt[0][i] = ck[o];
-            et[0][i] = ck[nck + o];
+            lt[0][i] = nl0[i];
+            et[0][i] = ne0[i];
         }
-        __syncthreads();
+        barrier_lds();   // the segment's inputs are in
+        fetch(sg > 0 ? sg - 1 : 0);
 #pragma unroll
         for (int j = 0; j < kCK; ++j) {
             const bool ok = j < nt;
@@ -390,28 +420,28 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
                 cdr += dpp<0x140, 0xf>(cdr);
             }
             if (ln == LPC - 1) s_o[j][c] = make_float2(cdv, cdr);
-            // key-slot sums: over the channels of this wave, then through LDS over the waves
-            float* slot = &s_red[j & 1][wave][0][0];
+            // key-slot sums over the channels of the workgroup: every channel's values go to
+            // its own LDS row, summed in a fixed order after the barrier
+            float* slot = &s_red[j & 1][c][0][0];
 #pragma unroll
             for (int qi = 0; qi < 4; ++qi)
 #pragma unroll
-                for (int i = 0; i < NPER; ++i) {
-                    float x = kq[qi][i];
-#pragma unroll
-                    for (int m = LPC; m < 64; m *= 2) x += __shfl_xor(x, m, 64);
-                    if (lane < LPC) slot[qi * DK + ln + LPC * i] = x;
-                }
-            __syncthreads();
+                for (int i = 0; i < NPER; ++i) slot[qi * DK + ln + LPC * i] = kq[qi][i];
+            barrier_lds();   // the channels' key-slot values of token j are in
             const size_t tk = ((size_t)b * T + t0 + j) * s.H + h;
-            for (int idx = tid; idx < 4 * DK; idx += NTHR) {
+            constexpr int RPT = (4 * DK + NTHR - 1) / NTHR;
+#pragma unroll
+            for (int m = 0; m < RPT; ++m) {
+                const int idx = tid + NTHR * m;
+                if (RPT * NTHR != 4 * DK && idx >= 4 * DK) continue;
                 float acc = 0.f;
 #pragma unroll
-                for (int w = 0; w < NW; ++w) acc += (&s_red[j & 1][w][0][0])[idx];
+                for (int cc = 0; cc < CB; ++cc) acc += (&s_red[j & 1][cc][0][0])[idx];
                 const int qi = idx / DK, n = idx % DK;
                 kpart[((size_t)tile * 4 + qi) * nkey + tk * DK + n] = acc;
             }
         }
-        __syncthreads();
+        barrier_lds();   // the channel sums of the segment are in
         for (int idx = tid; idx < nt * CB; idx += NTHR) {
             const int t = idx / CB, cc = idx % CB;
             const size_t o = (((size_t)b * T + t0 + t) * s.H + h) * DV + d0 + cc;
