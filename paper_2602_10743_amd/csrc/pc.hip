@@ -32,6 +32,8 @@
 // channels; the sums over d (dq, dk, dabar, dpbar) inside the workgroup over
 // its channels, then across the channel tiles by pc_key_combine_kernel, in a
 // fixed order (the results are bitwise reproducible).
+#include <type_traits>
+
 #include "kla_buf.hpp"
 #include "kla_device.hpp"
 #include "kla_internal.hpp"
@@ -42,6 +44,12 @@ namespace {
 constexpr int kNG = 8;    // lanes sharing one value channel, each with every 8th key slot
 constexpr int kTB = 16;   // tokens per staged block
 constexpr int kCK = 8;    // tokens between checkpoints of the belief (saved context)
+// The key-slot parts of the backward, [tile][4][B T H dk] fp32, lie part_stride(n)
+// floats apart: n = B T H dk is a multiple of a large power of two at the usual
+// shapes, and the combine kernel's streams that far apart would all fall on the
+// same HBM channels; the pad (1280 bytes) spreads them.
+constexpr int kKPad = 320;
+__host__ __device__ inline size_t part_stride(size_t n) { return n + kKPad; }
 
 __device__ __forceinline__ float sum8(float x) {   // over the 8 lanes of a channel
     x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
@@ -297,7 +305,7 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
     const int ln = tid % LPC, c = tid / LPC, d = d0 + c;
     const int T = s.T, nseg = (T + kCK - 1) / kCK;
     const size_t nck = (size_t)s.B * s.H * nseg * DK * DV;
-    const size_t nkey = (size_t)s.B * T * s.H * DK;
+    const size_t nkey = part_stride((size_t)s.B * T * s.H * DK);
 
     float ge[NPER], gl[NPER];
 #pragma unroll
@@ -457,19 +465,34 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
     }
 }
 
-// dq, dk, dabar, dpbar = sums of the channel tiles' parts, in the input dtype
-template <typename S>
-__global__ __launch_bounds__(256) void pc_key_combine_kernel(const float* __restrict__ kpart, int ntile, size_t n,
-                                                             BwdArgs g) {
-    using T_ = typename storage<S>::type;
-    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+// dq, dk, dabar, dpbar = sums of the NT channel tiles' parts (in tile order), in the
+// input dtype.  A thread takes 4 consecutive elements (n is a multiple of 4; every
+// array is 16-byte aligned) and issues all of its 4 NT part loads before the sums.
+template <typename S, int NT>
+__global__ __launch_bounds__(256) void pc_key_combine_kernel(const float* __restrict__ kpart, size_t n, BwdArgs g) {
+    const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4, ns = part_stride(n);
     if (i >= n) return;
-    T_* out[4] = {static_cast<T_*>(g.dq), static_cast<T_*>(g.dk), static_cast<T_*>(g.da), static_cast<T_*>(g.dp)};
+    void* out[4] = {g.dq, g.dk, g.da, g.dp};
+    float4 x[4][NT];
+#pragma unroll
+    for (int qi = 0; qi < 4; ++qi)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) x[qi][t] = *reinterpret_cast<const float4*>(kpart + ((size_t)t * 4 + qi) * ns + i);
 #pragma unroll
     for (int qi = 0; qi < 4; ++qi) {
-        float acc = 0.f;
-        for (int t = 0; t < ntile; ++t) acc += kpart[((size_t)t * 4 + qi) * n + i];
-        st(out[qi], i, acc);
+        float4 acc = x[qi][0];
+#pragma unroll
+        for (int t = 1; t < NT; ++t) {
+            acc.x += x[qi][t].x;
+            acc.y += x[qi][t].y;
+            acc.z += x[qi][t].z;
+            acc.w += x[qi][t].w;
+        }
+        if constexpr (std::is_same<S, bf16_t>::value)
+            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(out[qi]) + i) =
+                make_uint2(cvt_pk_bf16(acc.x, acc.y), cvt_pk_bf16(acc.z, acc.w));
+        else
+            *reinterpret_cast<float4*>(static_cast<float*>(out[qi]) + i) = acc;
     }
 }
 
@@ -481,10 +504,12 @@ struct BwdPc {
         hipLaunchKernelGGL((bwd_pc_kernel<S, DK, DV>), dim3((unsigned)(s.B * s.H * (DV / CB))), dim3(NTHR), 0, st,
                            s, a, ck, kpart);
         hipError_t e = hipGetLastError();
-        const size_t n = (size_t)s.B * s.T * s.H * DK;
+        const size_t n = (size_t)s.B * s.T * s.H * DK;   // dk is a multiple of 16, n of 4
         if (e != hipSuccess || n == 0) return e;
-        hipLaunchKernelGGL(pc_key_combine_kernel<S>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, kpart,
-                           DV / CB, n, a);
+        constexpr int NT = DV / CB;
+        static_assert(DK % 4 == 0 && (NT == 1 || NT == 2 || NT == 4 || NT == 8), "combine layout");
+        hipLaunchKernelGGL((pc_key_combine_kernel<S, NT>), dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, st,
+                           kpart, n, a);
         return hipGetLastError();
     }
 };
@@ -511,7 +536,7 @@ size_t pc_saved_bytes(const Shape& s) {
 size_t pc_bwd_workspace(const Shape& s) {
     const int cbmax = s.dk == 128 ? 16 : 32;
     const int cb = s.dv < cbmax ? s.dv : cbmax;
-    return (size_t)(s.dv / cb) * 4 * s.B * s.T * s.H * s.dk * sizeof(float);
+    return (size_t)(s.dv / cb) * 4 * part_stride((size_t)s.B * s.T * s.H * s.dk) * sizeof(float);
 }
 
 hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const float* ck, float* kpart, hipStream_t st) {
