@@ -72,6 +72,7 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
     __shared__ float4 s_k[kTB][DK];
     __shared__ float2 s_v[kTB][CT];
     __shared__ float s_y[kTB][CT], s_w[kTB][CT];
+    __shared__ float s_junk[2][NTHR];   // the writes of the lanes that do not hold a channel's sum
 
     const T_ *q = static_cast<const T_*>(g.q), *k = static_cast<const T_*>(g.k), *v = static_cast<const T_*>(g.v);
     const T_ *a = static_cast<const T_*>(g.a), *p = static_cast<const T_*>(g.p), *r = static_cast<const T_*>(g.r);
@@ -131,10 +132,9 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
             }
             ya = sum8(ya);
             wa = sum8(wa);
-            if (ng == 0) {
-                s_y[t][c] = ya;
-                s_w[t][c] = wa;
-            }
+            // every lane writes (no lane mask): the channel's lane 0 its sums, the others a junk slot
+            *(ng == 0 ? &s_y[t][c] : &s_junk[0][tid]) = ya;
+            *(ng == 0 ? &s_w[t][c] : &s_junk[1][tid]) = wa;
         }
         __syncthreads();
         for (int idx = tid; idx < nt * CT; idx += NTHR) {
