@@ -289,15 +289,28 @@ def forward_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, nthreads: Optional
 
 
 def backward_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=None,
-                nthreads: Optional[int] = None, dyvar=None) -> dict:
+                nthreads: Optional[int] = None, dyvar=None, with_mass: bool = False) -> dict:
     """Gradient of ``forward_ou``: dq, dk, dv, dr, dlam0, deta0 as in ``backward``, and
-    da, dp, ddelta [H, dk] for the OU parameters."""
+    da, dp, ddelta [H, dk] for the OU parameters.
+
+    Each parameter gradient is a sum over (b, t) of per-token terms (the gate
+    gradients of a token taken through the discretisation).  ``with_mass`` also
+    returns ``mass_da``, ``mass_dp``, ``mass_ddelta``: the sum over (b, t) of the
+    absolute values of those terms, the scale against which the rounding of such a
+    sum is measured (test infrastructure)."""
     B, T = np.shape(k)[:2]
     abar, pbar = _ou_tokens(a, p, delta, B, T)
     out = backward(q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT, detaT, nthreads=nthreads, dyvar=dyvar)
-    g_abar = out.pop("da").sum(axis=(0, 1))
-    g_pbar = out.pop("dp").sum(axis=(0, 1))
+    ga_tok = out.pop("da")
+    gp_tok = out.pop("dp")
+    g_abar = ga_tok.sum(axis=(0, 1))
+    g_pbar = gp_tok.sum(axis=(0, 1))
     out["da"], out["dp"], out["ddelta"] = ou_discretise_vjp(a, p, delta, g_abar, g_pbar)
+    if with_mass:
+        for name, (ca, cp) in zip(("mass_da", "mass_dp", "mass_ddelta"),
+                                  zip(*(ou_discretise_vjp(a, p, delta, np.ones_like(g_abar) * (i == 0),
+                                                          np.ones_like(g_pbar) * (i == 1)) for i in (0, 1)))):
+            out[name] = np.abs(ga_tok * ca + gp_tok * cp).sum(axis=(0, 1))
     return out
 
 

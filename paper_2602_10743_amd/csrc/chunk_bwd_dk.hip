@@ -11,7 +11,12 @@
 //   Y    = M(B)^T Qp + V Gs^T    dkh = Y / P (gradient of kh = r k)
 //   G'   = Qp^T dY + Gs                          (carried into the previous chunk)
 // The adjoint of log F_t is the reverse running sum S_t of qt dqt - kh dkh (plus
-// the final-state term sum_d detaT H_T), and the adjoint c of lam follows
+// the final-state term sum_d detaT H_T).  Over a whole chunk the attention parts of
+// X and Y cancel exactly: the chunk's total of qt dqt - kh dkh is
+// sum_t Qp_t (dY H0^T)_t - sum_j Kn_j (V Gs^T)_j, and S is carried from chunk to
+// chunk by that total (per token, only within the chunk, by the running sum);
+// summed token by token, the rounding of the large attention terms would add up
+// over the sequence.  The adjoint c of lam follows
 //   g_t = c_t - q_t dqt_t / lam_t^2,    c_T = dlamT,
 //   c_{t-1} = abar_t^2 rho_t^2 g_t - pbar_t rho_t S_t,
 // from which the input gradients follow by the chain rule through rho, lam, F
@@ -83,7 +88,8 @@ struct DkCfg {
     static constexpr int XT = KL + kC * LQ2 * 2, YT = XT + kC * LX * 4;   // X, Y fp32 [kC][LX]
     static constexpr int QS = YT + kC * LX * 4;                     // group maps [NG][5][16] fp32
     static constexpr int PC = QS + NG * 5 * 16 * 4;                 // chunk decay P_C [16] fp32
-    static constexpr int PAIR = (PC + 16 * 4 + 15) / 16 * 16;
+    static constexpr int WT = PC + 16 * 4;                          // chunk totals of the state parts [2][16]
+    static constexpr int PAIR = (WT + 2 * 16 * 4 + 15) / 16 * 16;
     static constexpr int BYTES = PAIR0 + NP * PAIR;   // dynamic part
     // The gradient tiles dq, dk, dabar, dpbar [4][kC][16] bf16 and the dr terms
     // [kC][17] fp32 of each pair live in separate static arrays: they are read
@@ -124,6 +130,15 @@ __device__ __forceinline__ bf16x8 lds_tr8_swz(const uint16_t* tile, int rowA, in
     const bf16x4 a = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)swz<DV>(tile, rowA + (s >> 2), col));
     const bf16x4 b = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4_t*)swz<DV>(tile, rowB + (s >> 2), col));
     return __builtin_shufflevector(a, b, 0, 1, 2, 3, 4, 5, 6, 7);
+}
+
+// sum over each 16-lane row, held by every lane of the row
+__device__ __forceinline__ float row_sum16f(float x) {
+    x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
+    x += dpp<0x4E, 0xf>(x);    // quad_perm [2,3,0,1]
+    x += dpp<0x141, 0xf>(x);   // row_half_mirror
+    x += dpp<0x140, 0xf>(x);   // row_mirror
+    return x;
 }
 
 __device__ __forceinline__ void buf_st128(uint4 v, rsrc_t r, uint32_t voff) {
@@ -287,6 +302,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             float* sX = reinterpret_cast<float*>(wb + Cfg::XT);
             float* sY = reinterpret_cast<float*>(wb + Cfg::YT);
             float* sPC = reinterpret_cast<float*>(wb + Cfg::PC);
+            float* sWT = reinterpret_cast<float*>(wb + Cfg::WT);   // [2][16]: sum_t Qp X0, sum_j Kn Yg
             float* qs = reinterpret_cast<float*>(wb + Cfg::QS);
             auto in_a = [&](int t) {
                 return TI ? ca : __uint_as_float((uint32_t)stg[(0 * kC + t) * 16 + nl] << 16);
@@ -441,6 +457,23 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                     for (int tt = 0; tt < 2; ++tt)
                         xacc[tt] = mfma2a(hh, hl, lds8_swz<DV>(sDY, 16 * tt + l16, 32 * ks + 8 * g4), xacc[tt]);
                 }
+                {   // chunk total of Qp X0 per slot n = 4 g4 + rr (tokens past the end have Qp = 0)
+                    float w[4];
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr) {
+                        w[rr] = 0.f;
+#pragma unroll
+                        for (int tt = 0; tt < 2; ++tt) {
+                            const int o = (16 * tt + l16) * LQ2 + 4 * g4 + rr;
+                            const float qp = __uint_as_float((uint32_t)sQH[o] << 16) + __uint_as_float((uint32_t)sQL[o] << 16);
+                            w[rr] = fmaf(qp, xacc[tt][rr], w[rr]);
+                        }
+                        w[rr] = row_sum16f(w[rr]);
+                    }
+                    if (l16 == 0)
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) sWT[4 * g4 + rr] = w[rr];
+                }
                 const bf16x8 knh = lds_tr8(sKH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
                 const bf16x8 knl = lds_tr8(sKL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
 #pragma unroll
@@ -450,12 +483,9 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                         float4{xacc[tt][0], xacc[tt][1], xacc[tt][2], xacc[tt][3]};
                 }
             } else {
-                // Y^T[n, j] = sum_t Qp^T[n, t] B[t, j] + sum_d Gs[n, d] V^T[d, j]
-                f32x4 yacc[2];
-                const bf16x8 qth = lds_tr8(sQH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
-                const bf16x8 qtl = lds_tr8(sQL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
-#pragma unroll
-                for (int jt = 0; jt < 2; ++jt) yacc[jt] = mfma3(qth, qtl, boh[jt], bol[jt], zero4());
+                // Y^T[n, j] = sum_d Gs[n, d] V^T[d, j] + sum_t Qp^T[n, t] B[t, j]: the state part
+                // first, whose chunk total is taken before the attention part is added
+                f32x4 yacc[2] = {zero4(), zero4()};
                 const float pcn = sPC[l16];
 #pragma unroll
                 for (int rd = 0; rd < NRD; ++rd)
@@ -471,6 +501,27 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                         yacc[jt] = mfma2a(gh, gl, vb, yacc[jt]);
                     }
                 }
+                {   // chunk total of Kn Yg per slot n = 4 g4 + rr (tokens past the end have Kn = 0)
+                    float w[4];
+#pragma unroll
+                    for (int rr = 0; rr < 4; ++rr) {
+                        w[rr] = 0.f;
+#pragma unroll
+                        for (int jt = 0; jt < 2; ++jt) {
+                            const int o = (16 * jt + l16) * LQ2 + 4 * g4 + rr;
+                            const float kn = __uint_as_float((uint32_t)sKH[o] << 16) + __uint_as_float((uint32_t)sKL[o] << 16);
+                            w[rr] = fmaf(kn, yacc[jt][rr], w[rr]);
+                        }
+                        w[rr] = row_sum16f(w[rr]);
+                    }
+                    if (l16 == 0)
+#pragma unroll
+                        for (int rr = 0; rr < 4; ++rr) sWT[16 + 4 * g4 + rr] = w[rr];
+                }
+                const bf16x8 qth = lds_tr8(sQH, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+                const bf16x8 qtl = lds_tr8(sQL, LQ2, 4 * g4, 16 + 4 * g4, 0, l16);
+#pragma unroll
+                for (int jt = 0; jt < 2; ++jt) yacc[jt] = mfma3(qth, qtl, boh[jt], bol[jt], yacc[jt]);
 #pragma unroll
                 for (int jt = 0; jt < 2; ++jt)
                     *reinterpret_cast<float4*>(sY + (16 * jt + l16) * LX + 4 * g4) =
@@ -541,7 +592,9 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             barrier_lds();   // the group summaries are in
 
             // ================================================================ phase 5
-            // carries into this group (through the later groups) and out of the chunk
+            // carries into this group (through the later groups) and out of the chunk; S leaves
+            // the chunk with the chunk's exact total, not the sum of its tokens' terms
+            const float S_out = ST + (sWT[nl] - sWT[16 + nl]);
             float c_in = 0.f, S_in = 0.f;
 #pragma unroll
             for (int q2 = NG - 1; q2 >= 0; --q2) {
@@ -555,6 +608,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 ST += D2;
                 cT = cn;
             }
+            ST = S_out;
             // pass 2: gradients of the group's tokens
             uint16_t* so = s_out + pr * 4 * kC * 16;
             float* drc = s_drc + pr * kC * 17;
@@ -636,8 +690,9 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
         if (g4 == 0) {
             const size_t np = (size_t)2 * s.B * H * DK;
             const size_t o = ((size_t)(e * s.B + b) * H + h) * DK + n0w + nl;
-            g.ou_part[o] = sum_da;
-            g.ou_part[np + o] = sum_dp;
+            float* part = static_cast<float*>(g.ou_part);
+            part[o] = sum_da;
+            part[np + o] = sum_dp;
         }
     }
 }

@@ -31,6 +31,10 @@ kla_status check_desc(const kla_desc* d) {
 
 kla::Shape shape_of(const kla_desc* d) { return kla::Shape{d->B, d->T, d->H, d->dk, d->dv, d->dtype == KLA_BF16}; }
 
+// One predicate decides the saved-context layout on both sides: the context is in
+// the chunked layout exactly when the chunked backward will consume it.
+bool saves_chunked(const kla::Shape& s) { return kla::chunked_bwd_supported(s); }
+
 bool check_mode() {
     const char* e = getenv("KLA_CHECK");
     return e && e[0] == '1';
@@ -82,7 +86,7 @@ size_t kla_forward_workspace(const kla_desc* desc) {
 size_t kla_saved_bytes(const kla_desc* desc) {
     if (check_desc(desc) != KLA_OK) return 0;
     const kla::Shape s = shape_of(desc);
-    return kla::chunked_supported(s) ? kla::chunked_saved_bytes(s) : kla::recurrent_saved_bytes(s);
+    return saves_chunked(s) ? kla::chunked_saved_bytes(s) : kla::recurrent_saved_bytes(s);
 }
 
 size_t kla_backward_workspace(const kla_desc* desc, int with_saved) {
@@ -128,16 +132,25 @@ kla_status forward_impl(const kla_desc* desc, const kla::FwdArgs& a, bool ou, vo
         if (st != KLA_OK) return st;
     }
     hipError_t e;
+    // without a saved context any forward kernel may run; with one, the kernel whose
+    // layout the backward reads (saves_chunked)
+    const bool chunked = saved ? saves_chunked(s) : kla::chunked_supported(s);
     if (!saved && !ou && kla::forward_segments(s) > 1)
         e = kla::launch_forward_segmented(s, a, static_cast<char*>(ws) + kAlign, stream);
     else
-        e = kla::chunked_supported(s) ? kla::launch_forward_chunked(s, a, saved, stream)
-                                      : kla::launch_forward_recurrent(s, a, static_cast<float*>(saved), stream);
+        e = chunked ? kla::launch_forward_chunked(s, a, saved, stream)
+                    : kla::launch_forward_recurrent(s, a, saved, stream);
     return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 
 int ou_parts(const kla::Shape& s) {
     return kla::chunked_bwd_supported(s) ? kla::chunked_ou_parts(s) : kla::recurrent_ou_parts(s);
+}
+
+// bytes per OU part element: fp32 from the chunked backward, the arithmetic type from the
+// token-recurrent one
+size_t ou_part_bytes(const kla::Shape& s) {
+    return kla::chunked_bwd_supported(s) ? sizeof(float) : kla::recurrent_ou_part_bytes(s);
 }
 
 // The backward behind both gate forms.  With OU parameters the gate gradients
@@ -164,7 +177,7 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
         st = validate(s, s.T, a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, ws, stream, a.ou_a, a.ou_p, a.ou_d);
         if (st != KLA_OK) return st;
     }
-    if (ou) a.ou_part = reinterpret_cast<float*>(static_cast<char*>(ws) + kla_backward_workspace(desc, saved != nullptr));
+    if (ou) a.ou_part = static_cast<char*>(ws) + kla_backward_workspace(desc, saved != nullptr);
     char* work = static_cast<char*>(ws) + kAlign;
     hipError_t e;
     if (kla::chunked_bwd_supported(s)) {
@@ -184,14 +197,15 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
             void* yscratch = ctx + round_up(kla::recurrent_saved_bytes(s));
             kla::FwdArgs f{a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, yscratch, nullptr, nullptr, nullptr,
                            a.ou_a, a.ou_p, a.ou_d};
-            e = kla::launch_forward_recurrent(s, f, reinterpret_cast<float*>(ctx), stream);
+            e = kla::launch_forward_recurrent(s, f, ctx, stream);
             if (e != hipSuccess) return KLA_ERR_HIP;
             saved = ctx;
         }
-        e = kla::launch_backward_recurrent(s, a, static_cast<const float*>(saved), work, stream);
+        e = kla::launch_backward_recurrent(s, a, saved, work, stream);
     }
     if (e == hipSuccess && ou)
-        e = kla::launch_ou_param_grads(s.H, s.dk, ou_parts(s), a.ou_part, a.ou_a, a.ou_p, a.ou_d, da, dp, dd, stream);
+        e = kla::launch_ou_param_grads(s.H, s.dk, ou_parts(s), a.ou_part, ou_part_bytes(s) == sizeof(double), a.ou_a,
+                                       a.ou_p, a.ou_d, da, dp, dd, stream);
     return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 
@@ -243,7 +257,7 @@ kla_status kla_backward(const kla_desc* desc, const void* q, const void* k, cons
 size_t kla_backward_ou_workspace(const kla_desc* desc, int with_saved) {
     if (check_desc(desc) != KLA_OK) return 0;
     const kla::Shape s = shape_of(desc);
-    return kla_backward_workspace(desc, with_saved) + round_up((size_t)2 * ou_parts(s) * s.H * s.dk * sizeof(float));
+    return kla_backward_workspace(desc, with_saved) + round_up((size_t)2 * ou_parts(s) * s.H * s.dk * ou_part_bytes(s));
 }
 
 kla_status kla_backward_ou(const kla_desc* desc, const void* q, const void* k, const void* v, const float* a,
@@ -293,7 +307,7 @@ kla_status kla_forward_pc(const kla_desc* desc, const void* q, const void* k, co
         if (st != KLA_OK) return st;
     }
     const kla::FwdArgs a{q, k, v, abar, pbar, r, lam0, eta0, y, yvar, lamT, etaT};
-    return kla::launch_forward_pc(s, a, static_cast<float*>(saved), stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+    return kla::launch_forward_pc(s, a, saved, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
 }
 
 kla_status kla_backward_pc(const kla_desc* desc, const void* q, const void* k, const void* v, const void* abar,
@@ -322,13 +336,13 @@ kla_status kla_backward_pc(const kla_desc* desc, const void* q, const void* k, c
         char* ctx = work + round_up(kla::pc_bwd_workspace(s));
         void* yscratch = ctx + round_up(kla::pc_saved_bytes(s));
         const kla::FwdArgs f{q, k, v, abar, pbar, r, lam0, eta0, yscratch, nullptr, nullptr, nullptr};
-        if (kla::launch_forward_pc(s, f, reinterpret_cast<float*>(ctx), stream) != hipSuccess) return KLA_ERR_HIP;
+        if (kla::launch_forward_pc(s, f, ctx, stream) != hipSuccess) return KLA_ERR_HIP;
         saved = ctx;
     }
     kla::BwdArgs a{q,  k,  v,  abar,  pbar,  r,  lam0, eta0,  dy, dlamT,
                    detaT, dq, dk, dv, dabar, dpbar, dr, dlam0, deta0};
     a.dyvar = dyvar;
-    return kla::launch_backward_pc(s, a, static_cast<const float*>(saved), kpart, stream) == hipSuccess ? KLA_OK
+    return kla::launch_backward_pc(s, a, saved, kpart, stream) == hipSuccess ? KLA_OK
                                                                                                       : KLA_ERR_HIP;
 }
 

@@ -83,9 +83,19 @@ __device__ __forceinline__ float dpp(float x) {
                                                                  0xf, false));
 }
 
+// dpp<> on a double: the same move applied to both 32-bit halves.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp(double x) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, x);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, ROW_MASK, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, ROW_MASK, 0xf, false);
+    return __builtin_bit_cast(double, (uint64_t)(uint32_t)lo | ((uint64_t)(uint32_t)hi << 32));
+}
+
 // Sums over the 32 lanes of each half of a wave (lanes 0..31 and 32..63) with
 // DPP moves; the total of a half lands in its upper 16 lanes (16..31, 48..63).
-__device__ __forceinline__ float half_sum(float x) {
+template <typename A>
+__device__ __forceinline__ A half_sum(A x) {
     x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
     x += dpp<0x4E, 0xf>(x);    // quad_perm [2,3,0,1]
     x += dpp<0x141, 0xf>(x);   // row_half_mirror

@@ -41,9 +41,31 @@ __device__ __forceinline__ void ou_gates(float a, float p, float delta, float& a
     pbar = (float)((double)p * (double)p * -expm1(-2.0 * ad) / (2.0 * (double)a));
 }
 
+// Same gates left in fp64 (the fp32-input paths carry their filter arithmetic in fp64).
+__device__ __forceinline__ void ou_gates(float a, float p, float delta, double& abar, double& pbar) {
+    const double ad = (double)a * (double)delta;
+    abar = exp(-ad);
+    pbar = (double)p * (double)p * -expm1(-2.0 * ad) / (2.0 * (double)a);
+}
+
+// Arithmetic type of the token-recurrent and per-channel kernels for a storage type:
+// fp32 inputs are filtered in fp64, so that the rounding accumulated over long
+// recursions and reverse sums stays far below the single rounding of the outputs;
+// bf16 inputs in fp32.
+template <typename S> struct acc { using type = float; };
+template <> struct acc<f32_t> { using type = double; };
+
 __device__ __forceinline__ float ld(const float* p, size_t i) { return p[i]; }
+__device__ __forceinline__ double ld(const double* p, size_t i) { return p[i]; }
 __device__ __forceinline__ float ld(const uint16_t* p, size_t i) { return bf16_to_f32(p[i]); }
 __device__ __forceinline__ void st(float* p, size_t i, float x) { p[i] = x; }
 __device__ __forceinline__ void st(uint16_t* p, size_t i, float x) { p[i] = f32_to_bf16(x); }
+__device__ __forceinline__ void st(float* p, size_t i, double x) { p[i] = (float)x; }
+__device__ __forceinline__ void st(uint16_t* p, size_t i, double x) { p[i] = f32_to_bf16((float)x); }
+
+// Reciprocal in the arithmetic type: v_rcp_f32 (about 1 ulp) for fp32, the correctly
+// rounded division for fp64.
+__device__ __forceinline__ float rcpa(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ double rcpa(double x) { return 1.0 / x; }
 
 }  // namespace kla

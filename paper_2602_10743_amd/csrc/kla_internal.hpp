@@ -31,8 +31,9 @@ struct BwdArgs {
     float *dlam0, *deta0;
     const float *ou_a = nullptr, *ou_p = nullptr, *ou_d = nullptr;
     // OU gates: per-part sums over tokens of the abar and pbar gradients,
-    // [2][nparts][H][dk] fp32 (da, dp unused)
-    float* ou_part = nullptr;
+    // [2][nparts][H][dk], fp32 from the chunked path, the arithmetic type from the
+    // token-recurrent one (da, dp unused)
+    void* ou_part = nullptr;
     const float* dyvar = nullptr;   // upstream gradient of yvar [B, T, H] fp32, or none
 };
 
@@ -44,15 +45,18 @@ struct DecodeArgs {
     const float *ou_a = nullptr, *ou_p = nullptr, *ou_d = nullptr;
 };
 
-// Token-recurrent kernels.  Their saved context (recurrent_saved_bytes(s) bytes,
-// fp32) is the precision after every token, lam_t [B, T, H, dk], followed by the
-// information state before every 64th token, [B, H, ceil(T / 64), dk, dv]:
-// optional for the forward, required by the backward.
+// Token-recurrent kernels.  They compute in fp64 for fp32 inputs and in fp32 for
+// bf16 inputs (the arithmetic type).  Their saved context (recurrent_saved_bytes(s)
+// bytes, in the arithmetic type) is the precision after every token, lam_t
+// [B, T, H, dk], followed by the information state before every 64th token,
+// [B, H, ceil(T / 64), dk, dv]: optional for the forward, required by the backward.
 size_t recurrent_saved_bytes(const Shape& s);
-hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st);
+hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st);
 size_t backward_recurrent_workspace(const Shape& s);
-hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, const float* saved_lam, void* ws,
+hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, const void* saved, void* ws,
                                      hipStream_t st);
+// bytes per element of the recurrent backward's OU parts (the arithmetic type)
+size_t recurrent_ou_part_bytes(const Shape& s);
 hipError_t launch_decode_step(const Shape& s, const DecodeArgs& a, hipStream_t st);
 
 // Chunked MFMA path (bf16 storage, dk >= 32).
@@ -75,10 +79,11 @@ int recurrent_ou_parts(const Shape& s);
 
 // Per-channel precision (r [B, T, H, dv], beliefs [B, H, dk, dv]): elementwise scan and decode.
 // ck: NULL or pc_saved_bytes of belief checkpoints for launch_backward_pc; kpart: pc_bwd_workspace bytes
-hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, float* ck, hipStream_t st);
+// The checkpoints are in the arithmetic type (fp64 for fp32 inputs, fp32 for bf16).
+hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, void* ck, hipStream_t st);
 size_t pc_saved_bytes(const Shape& s);
 size_t pc_bwd_workspace(const Shape& s);
-hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const float* ck, float* kpart, hipStream_t st);
+hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const void* ck, float* kpart, hipStream_t st);
 hipError_t launch_decode_pc(const Shape& s, const DecodeArgs& a, hipStream_t st);
 
 // Block scaffolding: causal conv1d (k = 4) + SiLU, RMS QK-norm, SiLU gate.
@@ -97,8 +102,9 @@ hipError_t launch_gate_fwd(size_t n, bool bf16, const void* y, const void* z, vo
 hipError_t launch_gate_bwd(size_t n, bool bf16, const void* y, const void* z, const void* dout, void* dy, void* dz,
                            hipStream_t st);
 
-// OU gates: gradients of the parameters from the per-part gate-gradient sums
-hipError_t launch_ou_param_grads(int H, int dk, int nparts, const float* part, const float* a, const float* p,
-                                 const float* d, float* da, float* dp, float* dd, hipStream_t st);
+// OU gates: gradients of the parameters from the per-part gate-gradient sums (fp32
+// parts, or fp64 when part_f64)
+hipError_t launch_ou_param_grads(int H, int dk, int nparts, const void* part, bool part_f64, const float* a,
+                                 const float* p, const float* d, float* da, float* dp, float* dd, hipStream_t st);
 
 }  // namespace kla

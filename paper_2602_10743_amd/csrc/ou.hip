@@ -15,7 +15,8 @@
 namespace kla {
 namespace {
 
-__global__ __launch_bounds__(256) void ou_param_grads_kernel(int n, int nparts, const float* __restrict__ part,
+template <typename P>
+__global__ __launch_bounds__(256) void ou_param_grads_kernel(int n, int nparts, const P* __restrict__ part,
                                                              const float* __restrict__ a, const float* __restrict__ p,
                                                              const float* __restrict__ d, float* __restrict__ da,
                                                              float* __restrict__ dp, float* __restrict__ dd) {
@@ -36,11 +37,16 @@ __global__ __launch_bounds__(256) void ou_param_grads_kernel(int n, int nparts, 
 
 }  // namespace
 
-hipError_t launch_ou_param_grads(int H, int dk, int nparts, const float* part, const float* a, const float* p,
-                                 const float* d, float* da, float* dp, float* dd, hipStream_t st) {
+hipError_t launch_ou_param_grads(int H, int dk, int nparts, const void* part, bool part_f64, const float* a,
+                                 const float* p, const float* d, float* da, float* dp, float* dd, hipStream_t st) {
     const int n = H * dk;
-    hipLaunchKernelGGL(ou_param_grads_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, n, nparts, part, a,
-                       p, d, da, dp, dd);
+    const dim3 grid((unsigned)((n + 255) / 256));
+    if (part_f64)
+        hipLaunchKernelGGL(ou_param_grads_kernel<double>, grid, dim3(256), 0, st, n, nparts,
+                           static_cast<const double*>(part), a, p, d, da, dp, dd);
+    else
+        hipLaunchKernelGGL(ou_param_grads_kernel<float>, grid, dim3(256), 0, st, n, nparts,
+                           static_cast<const float*>(part), a, p, d, da, dp, dd);
     return hipGetLastError();
 }
 

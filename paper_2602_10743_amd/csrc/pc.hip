@@ -27,7 +27,11 @@
 //   drho = df abar + gl lam_{t-1},  dden = -drho rho^2
 //   dabar[n] += df rho + 2 abar dden,  dpbar[n] += dden lam_{t-1}
 //   ge <- f ge,  gl <- gl rho + pbar dden
-// and after the first token dlam0 = gl, deta0 = ge.  The sums over n (dv, dr)
+// and after the first token dlam0 = gl, deta0 = ge.
+//
+// Arithmetic type A (acc<S>): fp64 for fp32 inputs, fp32 for bf16 inputs; the
+// per-element precision and state, their checkpoints and adjoints, and the partial
+// sums up to their single rounding into an output are held in A.  The sums over n (dv, dr)
 // are completed inside the workgroup, which holds every key slot of its
 // channels; the sums over d (dq, dk, dabar, dpbar) inside the workgroup over
 // its channels, then across the channel tiles by pc_key_combine_kernel, in a
@@ -51,7 +55,8 @@ constexpr int kCK = 8;    // tokens between checkpoints of the belief (saved con
 constexpr int kKPad = 320;
 __host__ __device__ inline size_t part_stride(size_t n) { return n + kKPad; }
 
-__device__ __forceinline__ float sum8(float x) {   // over the 8 lanes of a channel
+template <typename A>
+__device__ __forceinline__ A sum8(A x) {   // over the 8 lanes of a channel
     x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
     x += dpp<0x4E, 0xf>(x);    // quad_perm [2,3,0,1]
     x += dpp<0x141, 0xf>(x);   // row_half_mirror
@@ -64,8 +69,10 @@ __device__ __forceinline__ float sum8(float x) {   // over the 8 lanes of a chan
 // (r, v as [t][c]) are staged in LDS, the elements are updated, the partial
 // readouts summed over the 8 lanes of a channel and y, yvar written from LDS.
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s, FwdArgs g, float* ck) {
+__global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s, FwdArgs g,
+                                                                       typename acc<S>::type* ck) {
     using T_ = typename storage<S>::type;
+    using A = typename acc<S>::type;
     constexpr int CT = DV < 32 ? DV : 32;
     constexpr int NTHR = kNG * CT;
     constexpr int NPER = DK / kNG;
@@ -82,17 +89,17 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
     const int b = bh / s.H, h = bh % s.H;
     const int tid = threadIdx.x, ng = tid % kNG, c = tid / kNG, d = d0 + c;
 
-    float lam[NPER], eta[NPER];
+    A lam[NPER], eta[NPER];
 #pragma unroll
     for (int i = 0; i < NPER; ++i) {
         const size_t o = ((size_t)bh * DK + ng + kNG * i) * DV + d;
-        lam[i] = g.lam0 ? g.lam0[o] : 1.f;
-        eta[i] = g.eta0 ? g.eta0[o] : 0.f;
+        lam[i] = g.lam0 ? (A)g.lam0[o] : A(1);
+        eta[i] = g.eta0 ? (A)g.eta0[o] : A(0);
     }
     // checkpoints: the belief before tokens 0, kCK, 2 kCK, ... as lam [BH][nseg][DK][DV] then eta
     const int nseg = (s.T + kCK - 1) / kCK;
-    float* ck_lam = ck;
-    float* ck_eta = ck ? ck + (size_t)s.B * s.H * nseg * DK * DV : nullptr;
+    A* ck_lam = ck;
+    A* ck_eta = ck ? ck + (size_t)s.B * s.H * nseg * DK * DV : nullptr;
     for (int t0 = 0; t0 < s.T; t0 += kTB) {
         const int nt = min(kTB, s.T - t0);
         for (int idx = tid; idx < nt * DK; idx += NTHR) {
@@ -116,25 +123,26 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
                 }
             }
             const float2 rv = s_v[t][c];
-            const float krv_s = rv.x * rv.y;   // r v: the evidence k r v over k
-            float ya = 0.f, wa = 0.f;
+            const A rc = rv.x, krv_s = (A)rv.x * (A)rv.y;   // r v: the evidence k r v over k
+            A ya = 0, wa = 0;
 #pragma unroll
             for (int i = 0; i < NPER; ++i) {
                 const float4 in = s_k[t][ng + kNG * i];   // abar, pbar, k, q
-                const float den = fmaf(in.y, lam[i], in.x * in.x);
-                const float num = fmaf(in.z * in.z * rv.x, den, lam[i]);
-                const float R = __builtin_amdgcn_rcpf(den * num);
-                const float iden = num * R, ilam = den * (den * R);
+                const A ax = in.x, py = in.y, kz = in.z, qw = in.w;
+                const A den = fma(py, lam[i], ax * ax);
+                const A num = fma(kz * kz * rc, den, lam[i]);
+                const A R = rcpa(den * num);
+                const A iden = num * R, ilam = den * (den * R);
                 lam[i] = num * iden;
-                eta[i] = fmaf(in.x * iden, eta[i], in.z * krv_s);
-                ya = fmaf(in.w, eta[i] * ilam, ya);
-                wa = fmaf(in.w * in.w, ilam, wa);
+                eta[i] = fma(ax * iden, eta[i], kz * krv_s);
+                ya = fma(qw, eta[i] * ilam, ya);
+                wa = fma(qw * qw, ilam, wa);
             }
             ya = sum8(ya);
             wa = sum8(wa);
             // every lane writes (no lane mask): the channel's lane 0 its sums, the others a junk slot
-            *(ng == 0 ? &s_y[t][c] : &s_junk[0][tid]) = ya;
-            *(ng == 0 ? &s_w[t][c] : &s_junk[1][tid]) = wa;
+            *(ng == 0 ? &s_y[t][c] : &s_junk[0][tid]) = (float)ya;
+            *(ng == 0 ? &s_w[t][c] : &s_junk[1][tid]) = (float)wa;
         }
         __syncthreads();
         for (int idx = tid; idx < nt * CT; idx += NTHR) {
@@ -150,10 +158,15 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
 #pragma unroll
     for (int i = 0; i < NPER; ++i) {
         const size_t o = ((size_t)bh * DK + ng + kNG * i) * DV + d;
-        if (g.lamT) g.lamT[o] = lam[i];
-        if (g.etaT) g.etaT[o] = eta[i];
+        if (g.lamT) g.lamT[o] = (float)lam[i];
+        if (g.etaT) g.etaT[o] = (float)eta[i];
     }
 }
+
+template <typename A>
+struct alignas(4 * sizeof(A)) A4p {
+    A x, y, z, w;
+};
 
 // Decode: one token for S sequences, belief [S, H, dk, dv] updated in place.
 // One workgroup per (sequence, head); a thread owns 4 consecutive channels
@@ -161,12 +174,13 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
 template <typename S, int DK, int DV>
 __global__ __launch_bounds__(256) void decode_pc_kernel(int H, DecodeArgs g) {
     using T_ = typename storage<S>::type;
+    using A = typename acc<S>::type;
     constexpr int DV4 = DV / 4;
     constexpr int NG = (256 / DV4) < DK ? (256 / DV4) : DK;
     constexpr int NPER = DK / NG;
     __shared__ float4 s_k[DK];
     __shared__ float4 s_r[DV4], s_v[DV4];
-    __shared__ float4 s_y[NG][DV4], s_w[NG][DV4];
+    __shared__ A4p<A> s_y[NG][DV4], s_w[NG][DV4];
 
     const T_ *q = static_cast<const T_*>(g.q), *k = static_cast<const T_*>(g.k), *v = static_cast<const T_*>(g.v);
     const T_ *a = static_cast<const T_*>(g.a), *p = static_cast<const T_*>(g.p), *r = static_cast<const T_*>(g.r);
@@ -186,39 +200,40 @@ __global__ __launch_bounds__(256) void decode_pc_kernel(int H, DecodeArgs g) {
     const int d4 = tid % DV4, ng = tid / DV4;
     if (ng < NG) {
         const float4 rr = s_r[d4], vv = s_v[d4];
-        const float rc[4] = {rr.x, rr.y, rr.z, rr.w};
-        const float rv[4] = {rr.x * vv.x, rr.y * vv.y, rr.z * vv.z, rr.w * vv.w};
-        float ya[4] = {0.f, 0.f, 0.f, 0.f}, wa[4] = {0.f, 0.f, 0.f, 0.f};
+        const A rc[4] = {rr.x, rr.y, rr.z, rr.w};
+        const A rv[4] = {(A)rr.x * vv.x, (A)rr.y * vv.y, (A)rr.z * vv.z, (A)rr.w * vv.w};
+        A ya[4] = {0, 0, 0, 0}, wa[4] = {0, 0, 0, 0};
         float4* lam4 = reinterpret_cast<float4*>(g.lam + sh * DK * DV);
         float4* eta4 = reinterpret_cast<float4*>(g.eta + sh * DK * DV);
 #pragma unroll 2
         for (int i = 0; i < NPER; ++i) {
             const int n = ng + NG * i;
             const float4 in = s_k[n];
+            const A ax = in.x, py = in.y, kz = in.z, qw = in.w;
             const float4 l4 = lam4[n * DV4 + d4], e4 = eta4[n * DV4 + d4];
-            float lp[4] = {l4.x, l4.y, l4.z, l4.w}, ep[4] = {e4.x, e4.y, e4.z, e4.w};
+            A lp[4] = {l4.x, l4.y, l4.z, l4.w}, ep[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const float den = fmaf(in.y, lp[j], in.x * in.x);
-                const float num = fmaf(in.z * in.z * rc[j], den, lp[j]);
-                const float R = __builtin_amdgcn_rcpf(den * num);
-                const float iden = num * R, ilam = den * (den * R);
+                const A den = fma(py, lp[j], ax * ax);
+                const A num = fma(kz * kz * rc[j], den, lp[j]);
+                const A R = rcpa(den * num);
+                const A iden = num * R, ilam = den * (den * R);
                 lp[j] = num * iden;
-                ep[j] = fmaf(in.x * iden, ep[j], in.z * rv[j]);
-                ya[j] = fmaf(in.w, ep[j] * ilam, ya[j]);
-                wa[j] = fmaf(in.w * in.w, ilam, wa[j]);
+                ep[j] = fma(ax * iden, ep[j], kz * rv[j]);
+                ya[j] = fma(qw, ep[j] * ilam, ya[j]);
+                wa[j] = fma(qw * qw, ilam, wa[j]);
             }
-            lam4[n * DV4 + d4] = make_float4(lp[0], lp[1], lp[2], lp[3]);
-            eta4[n * DV4 + d4] = make_float4(ep[0], ep[1], ep[2], ep[3]);
+            lam4[n * DV4 + d4] = make_float4((float)lp[0], (float)lp[1], (float)lp[2], (float)lp[3]);
+            eta4[n * DV4 + d4] = make_float4((float)ep[0], (float)ep[1], (float)ep[2], (float)ep[3]);
         }
-        s_y[ng][d4] = make_float4(ya[0], ya[1], ya[2], ya[3]);
-        s_w[ng][d4] = make_float4(wa[0], wa[1], wa[2], wa[3]);
+        s_y[ng][d4] = A4p<A>{ya[0], ya[1], ya[2], ya[3]};
+        s_w[ng][d4] = A4p<A>{wa[0], wa[1], wa[2], wa[3]};
     }
     __syncthreads();
     for (int j = tid; j < DV4; j += 256) {
-        float4 ys = s_y[0][j], ws = s_w[0][j];
+        A4p<A> ys = s_y[0][j], ws = s_w[0][j];
         for (int gi = 1; gi < NG; ++gi) {
-            const float4 y2 = s_y[gi][j], w2 = s_w[gi][j];
+            const A4p<A> y2 = s_y[gi][j], w2 = s_w[gi][j];
             ys.x += y2.x; ys.y += y2.y; ys.z += y2.z; ys.w += y2.w;
             ws.x += w2.x; ws.y += w2.y; ws.z += w2.z; ws.w += w2.w;
         }
@@ -228,10 +243,10 @@ __global__ __launch_bounds__(256) void decode_pc_kernel(int H, DecodeArgs g) {
         st(y, o + 2, ys.z);
         st(y, o + 3, ys.w);
         if (g.yvar) {
-            g.yvar[o] = ws.x;
-            g.yvar[o + 1] = ws.y;
-            g.yvar[o + 2] = ws.z;
-            g.yvar[o + 3] = ws.w;
+            g.yvar[o] = (float)ws.x;
+            g.yvar[o + 1] = (float)ws.y;
+            g.yvar[o + 2] = (float)ws.z;
+            g.yvar[o + 3] = (float)ws.w;
         }
     }
 }
@@ -250,10 +265,10 @@ hipError_t dispatch_pc(const Shape& s, A&&... args) {
 
 template <typename S, int DK, int DV>
 struct FwdPc {
-    static hipError_t run(const Shape& s, const FwdArgs& a, float* ck, hipStream_t st) {
+    static hipError_t run(const Shape& s, const FwdArgs& a, void* ck, hipStream_t st) {
         constexpr int CT = DV < 32 ? DV : 32;
         hipLaunchKernelGGL((fwd_pc_kernel<S, DK, DV>), dim3((unsigned)(s.B * s.H * (DV / CT))), dim3(kNG * CT), 0,
-                           st, s, a, ck);
+                           st, s, a, static_cast<typename acc<S>::type*>(ck));
         return hipGetLastError();
     }
 };
@@ -271,21 +286,25 @@ struct FwdPc {
 // cross-lane shuffles, and the writes need no lane mask).
 // At dk = 128 a lane's 4 elements keep 72 trajectory values in registers, so the
 // workgroup takes 16 channels (2 waves per SIMD, room for them) instead of 32.
-template <int DK, int DV>
+template <int DK, int DV, typename A = float>
 struct PcLanes {
     static constexpr int LPC = DK < 32 ? DK : 32;
     static constexpr int NPER = DK / LPC;
-    static constexpr int CBMAX = DK == 128 ? 16 : 32;
+    // fp64 arithmetic doubles the trajectory registers: 16 channels from dk = 64 on
+    static constexpr int CBMAX = DK == 128 || (DK == 64 && sizeof(A) == 8) ? 16 : 32;
     static constexpr int CB = DV < CBMAX ? DV : CBMAX;
     static constexpr int NTHR = LPC * CB;
 };
 
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s, BwdArgs g, const float* ck,
+__global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) void bwd_pc_kernel(Shape s, BwdArgs g,
+                                                                        const typename acc<S>::type* ck,
                                                                         float* kpart) {
     using T_ = typename storage<S>::type;
-    constexpr int LPC = PcLanes<DK, DV>::LPC, NPER = PcLanes<DK, DV>::NPER;
-    constexpr int CB = PcLanes<DK, DV>::CB;
+    using A = typename acc<S>::type;
+    using PL = PcLanes<DK, DV, A>;
+    constexpr int LPC = PL::LPC, NPER = PL::NPER;
+    constexpr int CB = PL::CB;
     constexpr int NTHR = LPC * CB;
     static_assert(NTHR % 64 == 0 && (LPC == 16 || LPC == 32), "lane layout");
     __shared__ float4 s_k[kCK][DK];        // abar, pbar, k, q
@@ -307,19 +326,19 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
     const size_t nck = (size_t)s.B * s.H * nseg * DK * DV;
     const size_t nkey = part_stride((size_t)s.B * T * s.H * DK);
 
-    float ge[NPER], gl[NPER];
+    A ge[NPER], gl[NPER];
 #pragma unroll
     for (int i = 0; i < NPER; ++i) {
         const size_t o = ((size_t)bh * DK + ln + LPC * i) * DV + d;
-        ge[i] = g.detaT ? g.detaT[o] : 0.f;
-        gl[i] = g.dlamT ? g.dlamT[o] : 0.f;
+        ge[i] = g.detaT ? (A)g.detaT[o] : A(0);
+        gl[i] = g.dlamT ? (A)g.dlamT[o] : A(0);
     }
     // The inputs of a segment and its checkpoint are fetched into registers one segment
     // ahead (indices clamped to the segment's last token, so every load is issued) and
     // written to LDS at the start of the segment.
     constexpr int KPT = (kCK * DK + NTHR - 1) / NTHR, CPT = (kCK * CB + NTHR - 1) / NTHR;
     float4 nk[KPT], nc[CPT];
-    float nl0[NPER], ne0[NPER];
+    A nl0[NPER], ne0[NPER];
     auto fetch = [&](int sg) {
         const int t0 = sg * kCK, tl = min(kCK, T - t0) - 1;
 #pragma unroll
@@ -357,7 +376,7 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
             if (CPT * NTHR == kCK * CB || idx < kCK * CB) s_c[idx / CB][idx % CB] = nc[m];
         }
         // lam and H before each token of the segment and after its last
-        float lt[kCK + 1][NPER], et[kCK + 1][NPER];
+        A lt[kCK + 1][NPER], et[kCK + 1][NPER];
 #pragma unroll
         for (int i = 0; i < NPER; ++i) {
             lt[0][i] = nl0[i];
@@ -369,16 +388,17 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
         for (int j = 0; j < kCK; ++j) {
             const bool ok = j < nt;
             const float4 cv = s_c[ok ? j : 0][c];
-            const float krv = cv.x * cv.y;
+            const A rc = cv.x, krv = (A)cv.x * (A)cv.y;
 #pragma unroll
             for (int i = 0; i < NPER; ++i) {
                 const float4 in = s_k[ok ? j : 0][ln + LPC * i];
-                const float den = fmaf(in.y, lt[j][i], in.x * in.x);
-                const float num = fmaf(in.z * in.z * cv.x, den, lt[j][i]);
-                const float R = __builtin_amdgcn_rcpf(den * num);
-                const float iden = num * R;
+                const A ax = in.x, py = in.y, kz = in.z;
+                const A den = fma(py, lt[j][i], ax * ax);
+                const A num = fma(kz * kz * rc, den, lt[j][i]);
+                const A R = rcpa(den * num);
+                const A iden = num * R;
                 lt[j + 1][i] = ok ? num * iden : lt[j][i];
-                et[j + 1][i] = ok ? fmaf(in.x * iden, et[j][i], in.z * krv) : et[j][i];
+                et[j + 1][i] = ok ? fma(ax * iden, et[j][i], kz * krv) : et[j][i];
             }
         }
         // reverse over the segment's tokens
@@ -386,32 +406,33 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
         for (int j = kCK - 1; j >= 0; --j) {
             if (j >= nt) continue;   // uniform: the tail of the last segment
             const float4 cv = s_c[j][c];   // r, v, gy, gv
+            const A cr = cv.x, cvv = cv.y, gy = cv.z, gv = cv.w;
             float kq[4][NPER];             // this lane's dq, dk, dabar, dpbar of token j
-            float cdv = 0.f, cdr = 0.f;
+            A cdv = 0, cdr = 0;
 #pragma unroll
             for (int i = 0; i < NPER; ++i) {
                 const float4 in = s_k[j][ln + LPC * i];   // abar, pbar, k, q
-                const float av = in.x, pv = in.y, kv = in.z, qv = in.w;
-                const float lp = lt[j][i], lc = lt[j + 1][i], ep = et[j][i], ec = et[j + 1][i];
-                const float den = fmaf(pv, lp, av * av);
-                const float R = __builtin_amdgcn_rcpf(lc * den);
-                const float ilc = den * R, rho = lc * R;
-                const float mu = ec * ilc;
-                const float qgy = qv * cv.z;
-                kq[0][i] = fmaf(mu, cv.z, 2.f * qv * cv.w * ilc);
-                float gei = fmaf(qgy, ilc, ge[i]);
-                float gli = gl[i] - fmaf(qgy, mu, qv * qv * cv.w * ilc) * ilc;
-                const float df = gei * ep;
-                const float kr = kv * cv.x;
-                kq[1][i] = fmaf(gei, cv.x * cv.y, 2.f * gli * kr);
-                cdr = fmaf(gei, kv * cv.y, fmaf(gli, kv * kv, cdr));
-                cdv = fmaf(gei, kr, cdv);
-                const float drho = fmaf(df, av, gli * lp);
-                const float dden = -drho * rho * rho;
-                kq[2][i] = fmaf(df, rho, 2.f * av * dden);
-                kq[3][i] = dden * lp;
+                const A av = in.x, pv = in.y, kv = in.z, qv = in.w;
+                const A lp = lt[j][i], lc = lt[j + 1][i], ep = et[j][i], ec = et[j + 1][i];
+                const A den = fma(pv, lp, av * av);
+                const A R = rcpa(lc * den);
+                const A ilc = den * R, rho = lc * R;
+                const A mu = ec * ilc;
+                const A qgy = qv * gy;
+                kq[0][i] = (float)fma(mu, gy, A(2) * qv * gv * ilc);
+                const A gei = fma(qgy, ilc, ge[i]);
+                const A gli = gl[i] - fma(qgy, mu, qv * qv * gv * ilc) * ilc;
+                const A df = gei * ep;
+                const A kr = kv * cr;
+                kq[1][i] = (float)fma(gei, cr * cvv, A(2) * gli * kr);
+                cdr = fma(gei, kv * cvv, fma(gli, kv * kv, cdr));
+                cdv = fma(gei, kr, cdv);
+                const A drho = fma(df, av, gli * lp);
+                const A dden = -drho * rho * rho;
+                kq[2][i] = (float)fma(df, rho, A(2) * av * dden);
+                kq[3][i] = (float)(dden * lp);
                 ge[i] = av * rho * gei;
-                gl[i] = fmaf(gli, rho, pv * dden);
+                gl[i] = fma(gli, rho, pv * dden);
             }
             // channel sums over the LPC lanes of the channel
             if constexpr (LPC == 32) {
@@ -427,7 +448,7 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
                 cdr += dpp<0x141, 0xf>(cdr);
                 cdr += dpp<0x140, 0xf>(cdr);
             }
-            if (ln == LPC - 1) s_o[j][c] = make_float2(cdv, cdr);
+            if (ln == LPC - 1) s_o[j][c] = make_float2((float)cdv, (float)cdr);
             // key-slot sums over the channels of the workgroup: every channel's values go to
             // its own LDS row, summed in a fixed order after the barrier
             float* slot = &s_red[j & 1][c][0][0];
@@ -460,8 +481,8 @@ __global__ __launch_bounds__((PcLanes<DK, DV>::NTHR)) void bwd_pc_kernel(Shape s
 #pragma unroll
     for (int i = 0; i < NPER; ++i) {
         const size_t o = ((size_t)bh * DK + ln + LPC * i) * DV + d;
-        if (g.dlam0) g.dlam0[o] = gl[i];
-        if (g.deta0) g.deta0[o] = ge[i];
+        if (g.dlam0) g.dlam0[o] = (float)gl[i];
+        if (g.deta0) g.deta0[o] = (float)ge[i];
     }
 }
 
@@ -498,11 +519,12 @@ __global__ __launch_bounds__(256) void pc_key_combine_kernel(const float* __rest
 
 template <typename S, int DK, int DV>
 struct BwdPc {
-    static hipError_t run(const Shape& s, const BwdArgs& a, const float* ck, float* kpart, hipStream_t st) {
-        constexpr int CB = PcLanes<DK, DV>::CB;
-        constexpr int NTHR = PcLanes<DK, DV>::NTHR;
+    static hipError_t run(const Shape& s, const BwdArgs& a, const void* ck, float* kpart, hipStream_t st) {
+        using PL = PcLanes<DK, DV, typename acc<S>::type>;
+        constexpr int CB = PL::CB;
+        constexpr int NTHR = PL::NTHR;
         hipLaunchKernelGGL((bwd_pc_kernel<S, DK, DV>), dim3((unsigned)(s.B * s.H * (DV / CB))), dim3(NTHR), 0, st,
-                           s, a, ck, kpart);
+                           s, a, static_cast<const typename acc<S>::type*>(ck), kpart);
         hipError_t e = hipGetLastError();
         const size_t n = (size_t)s.B * s.T * s.H * DK;   // dk is a multiple of 16, n of 4
         if (e != hipSuccess || n == 0) return e;
@@ -524,22 +546,22 @@ struct DecPc {
 
 }  // namespace
 
-hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, float* ck, hipStream_t st) {
+hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, void* ck, hipStream_t st) {
     return dispatch_pc<FwdPc>(s, a, ck, st);
 }
 
 size_t pc_saved_bytes(const Shape& s) {
     const size_t nseg = (size_t)(s.T + kCK - 1) / kCK;
-    return 2 * (size_t)s.B * s.H * nseg * s.dk * s.dv * sizeof(float);
+    return 2 * (size_t)s.B * s.H * nseg * s.dk * s.dv * (s.bf16 ? sizeof(float) : sizeof(double));
 }
 
 size_t pc_bwd_workspace(const Shape& s) {
-    const int cbmax = s.dk == 128 ? 16 : 32;
+    const int cbmax = s.dk == 128 || (s.dk == 64 && !s.bf16) ? 16 : 32;   // as PcLanes
     const int cb = s.dv < cbmax ? s.dv : cbmax;
     return (size_t)(s.dv / cb) * 4 * part_stride((size_t)s.B * s.T * s.H * s.dk) * sizeof(float);
 }
 
-hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const float* ck, float* kpart, hipStream_t st) {
+hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const void* ck, float* kpart, hipStream_t st) {
     return dispatch_pc<BwdPc>(s, a, ck, kpart, st);
 }
 

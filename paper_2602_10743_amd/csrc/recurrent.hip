@@ -9,6 +9,16 @@
 // over its tokens into one part per batch row.  The forward can save the
 // precision after every token, which the backward then reads instead of
 // walking it again.
+//
+// Arithmetic type A (acc<S>): fp64 for fp32 inputs, fp32 for bf16 inputs.  Every
+// quantity that a recursion or a sum over tokens carries -- the precision walk,
+// the forget gates, the information state and its adjoint, dqt, the log-gate and
+// precision adjoints, and the saved context and workspace that hand them from
+// kernel to kernel -- is held in A.  Only values used once per token (q / lam,
+// q^2 / lam, partial sums that are rounded once into an output) pass through
+// fp32.  With fp32 arithmetic the rounding accumulated along a 512-token adjoint
+// chain alone exceeds the fp32 tolerance by a factor of four on the gate
+// gradients; in fp64 it is negligible next to the final rounding of the outputs.
 #include <type_traits>
 
 #include "kla_buf.hpp"
@@ -22,22 +32,23 @@ constexpr int kThreads = 256;
 constexpr int kTB = 16;  // tokens per staged block of sweep 1
 constexpr int kCKI = 64; // tokens between the information-state checkpoints of the saved context
 
-// The saved context of this path: lam_t [B, T, H, dk], then the information state
-// before every kCKI-th token [B, H, ceil(T / kCKI), dk, dv], fp32.
-__host__ __device__ inline size_t saved_lam_floats(const Shape& s) { return (size_t)s.B * s.T * s.H * s.dk; }
+// The saved context of this path, in the arithmetic type: lam_t [B, T, H, dk], then
+// the information state before every kCKI-th token [B, H, ceil(T / kCKI), dk, dv].
+__host__ __device__ inline size_t saved_lam_elems(const Shape& s) { return (size_t)s.B * s.T * s.H * s.dk; }
 __host__ __device__ inline int n_checkpoints(int T) { return (T + kCKI - 1) / kCKI; }
+__host__ __device__ inline size_t acc_bytes(const Shape& s) { return s.bf16 ? sizeof(float) : sizeof(double); }
 
 // Per-token inputs reach the kernels in blocks of ROWS tokens, staged in LDS as
-// rows of floats.  A Part is one tensor's W values per token: each thread
-// fetches elements tid + kThreads m of the next block into registers while the
-// current block is worked on, and writes them to their LDS columns once that
-// block is done, so a token's loads never wait in its recursion.  The kernels
-// synchronise with barrier_lds (LDS ordering only): a full __syncthreads would
-// wait for the prefetch at the first barrier after it is issued.
-template <int ROWS, int W, int NT = kThreads>
+// rows of V.  A Part is one tensor's W values per token: each thread fetches
+// elements tid + NT m of the next block into registers while the current block
+// is worked on, and writes them to their LDS columns once that block is done,
+// so a token's loads never wait in its recursion.  The kernels synchronise with
+// barrier_lds (LDS ordering only): a full __syncthreads would wait for the
+// prefetch at the first barrier after it is issued.
+template <int ROWS, int W, int NT = kThreads, typename V = float>
 struct Part {
     static constexpr int N = (ROWS * W + NT - 1) / NT;
-    float x[N];
+    V x[N];
     // rows j < nt (nt >= 1): element c of row j at x0[j * ts + c].  Rows past nt and
     // elements past the block re-read the last valid element: they are never used,
     // and the loads stay unconditional, so nothing waits for them before the commit.
@@ -47,12 +58,12 @@ struct Part {
         for (int m = 0; m < N; ++m) {
             const int e = min((int)threadIdx.x + NT * m, ROWS * W - 1);
             const int j = min(e / W, nt - 1), c = e % W;
-            x[m] = ld(x0, (size_t)(j * ts + c));
+            x[m] = (V)ld(x0, (size_t)(j * ts + c));
         }
     }
     // row j of the block into dst[j * ROW + c0 + c]
     template <int ROW>
-    __device__ __forceinline__ void commit(float* dst, int c0) const {
+    __device__ __forceinline__ void commit(V* dst, int c0) const {
 #pragma unroll
         for (int m = 0; m < N; ++m) {
             const int e = (int)threadIdx.x + NT * m;
@@ -62,12 +73,9 @@ struct Part {
     }
 };
 
-// Reciprocal on v_rcp_f32 (about 1 ulp), as in the chunked kernels: the IEEE division
-// sequence would lengthen the per-token precision chain several times over.
-__device__ __forceinline__ float rcp(float x) { return __builtin_amdgcn_rcpf(x); }
-
 // Sum over each 16-lane row with DPP moves, held by every lane of the row.
-__device__ __forceinline__ float row_sum16(float x) {
+template <typename A>
+__device__ __forceinline__ A row_sum16(A x) {
     x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
     x += dpp<0x4E, 0xf>(x);    // quad_perm [2,3,0,1]
     x += dpp<0x141, 0xf>(x);   // row_half_mirror
@@ -76,22 +84,35 @@ __device__ __forceinline__ float row_sum16(float x) {
 }
 
 // x of the lane D below within its 16-lane row (row_shr; lanes with none read 0)
-template <int D>
-__device__ __forceinline__ float row_shr(float x) {
+template <int D, typename A>
+__device__ __forceinline__ A row_shr(A x) {
     static_assert(D >= 1 && D <= 15, "row shift");
     return dpp<0x110 + D, 0xf>(x);
 }
 
+// lane l reads lane l ^ 16 (ds_swizzle, bitmask mode)
+__device__ __forceinline__ float swz16(float x) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+}
+__device__ __forceinline__ double swz16(double x) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, x);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_ds_swizzle((int)(uint32_t)u, 0x401F);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_ds_swizzle((int)(uint32_t)(u >> 32), 0x401F);
+    return __builtin_bit_cast(double, (uint64_t)lo | ((uint64_t)hi << 32));
+}
+
 // Sum over groups of W consecutive lanes (W = 16 or 32), held by every lane of the
 // group: W = 32 exchanges the two row sums with a swizzle (lane l reads lane l ^ 16).
-template <int W>
-__device__ __forceinline__ float group_sum_all(float x) {
+template <int W, typename A>
+__device__ __forceinline__ A group_sum_all(A x) {
     static_assert(W == 16 || W == 32, "group width");
     x = row_sum16(x);
-    if constexpr (W == 32)
-        x += __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+    if constexpr (W == 32) x += swz16(x);
     return x;
 }
+
+template <typename A>
+__device__ __forceinline__ A amax(A x, A y) { return x > y ? x : y; }
 
 // value channels per forward workgroup: 16, so that even a small head spreads over
 // several workgroups (each walks the precision of the head itself)
@@ -100,11 +121,12 @@ constexpr int kFwdDVT = DV < 16 ? DV : 16;
 // threads per forward workgroup and tokens per staged block: blocks of 32 tokens
 // (half the barriers per token) where the LDS holds them, two waves per SIMD at
 // dk = 64 (measured at the state-tracking shape, dk = 32: 256 threads and blocks
-// of 32 tokens beat 512 threads and blocks of 16)
+// of 32 tokens beat 512 threads and blocks of 16); fp64 arithmetic at dk = 128
+// takes blocks of 8 tokens, within the LDS of a workgroup
 template <int DK>
 constexpr int kFwdThreads = DK == 64 ? 512 : 256;
-template <int DK>
-constexpr int kFwdTB = DK <= 32 ? 32 : 16;
+template <typename A, int DK>
+constexpr int kFwdTB = DK <= 32 ? 32 : (DK == 128 && sizeof(A) == 8) ? 8 : 16;
 
 // ----------------------------------------------------------------------------
 // Forward.  One workgroup per (b, h, value tile of DVT channels); every thread
@@ -116,28 +138,46 @@ constexpr int kFwdTB = DK <= 32 ? 32 : 16;
 // phi = k^2 r); an inclusive scan of these products over the slot's lanes (DPP,
 // each product scaled by its largest entry: the map is projective) gives the
 // product of every token before the lane's group, which applied to the block's
-// starting lam starts the lane's own walk over its tokens.  The walk leaves F,
-// r k, q / lam and q^2 / lam in the staged rows; then every thread updates its
-// state entries over the block and the readout partials are summed.
+// starting lam starts the lane's own walk over its tokens.  The walk leaves F
+// (arithmetic type), q / lam and q^2 / lam; then every thread updates its state
+// entries over the block and the readout partials are summed.
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s, FwdArgs g, float* saved_lam) {
+struct FwdLay {
+    using A = typename acc<S>::type;
+    static constexpr int NTH = kFwdThreads<DK>;
+    static constexpr int TBF = kFwdTB<A, DK>;   // tokens per staged block
+    static constexpr int DVT = kFwdDVT<DV>;
+    static constexpr int NG = NTH / DVT;
+    // staged row of a token: abar, pbar, k, q [DK] each, this tile's v [DVT], r; after the
+    // walk the abar column holds q / lam and the pbar column q^2 / lam
+    static constexpr int CA = 0, CP = DK, CK = 2 * DK, CQ = 3 * DK, CV = 4 * DK, CR = CV + DVT, ROW = CR + 1;
+    // LDS (bytes): staged rows (fp32), forget gates [TBF][DK] (A), readout partials [TBF][NG][DVT] (fp32)
+    static constexpr int L_IN = 0, L_F = (TBF * ROW * 4 + 15) / 16 * 16;
+    static constexpr int L_RED = L_F + TBF * DK * (int)sizeof(A);
+    static constexpr int BYTES = L_RED + TBF * NG * DVT * 4;
+    static_assert(BYTES <= 160 * 1024, "LDS budget of one workgroup");
+};
+
+template <typename S, int DK, int DV>
+__global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s, FwdArgs g,
+                                                                        typename acc<S>::type* saved_lam) {
     using T_ = typename storage<S>::type;
-    constexpr int NTH = kFwdThreads<DK>;
-    constexpr int TBF = kFwdTB<DK>;   // tokens per staged block
-    constexpr int DVT = kFwdDVT<DV>;
+    using A = typename acc<S>::type;
+    using L = FwdLay<S, DK, DV>;
+    constexpr int NTH = L::NTH, TBF = L::TBF, DVT = L::DVT, NG = L::NG;
     constexpr int NTILE = DV / DVT;
-    constexpr int NG = NTH / DVT;
     constexpr int NPER = DK / NG > 0 ? DK / NG : 1;
     static_assert(DK % NG == 0 || NG > DK, "key width must be a multiple of the n-groups");
-    // staged row of a token: abar, pbar, k, q [DK] each, this tile's v [DVT], r
-    constexpr int CA = 0, CP = DK, CK = 2 * DK, CQ = 3 * DK, CV = 4 * DK, CR = CV + DVT, ROW = CR + 1;
+    constexpr int CA = L::CA, CP = L::CP, CK = L::CK, CQ = L::CQ, CV = L::CV, CR = L::CR, ROW = L::ROW;
     constexpr int NY = (TBF * DVT + NTH - 1) / NTH;   // outputs per thread and block
     constexpr int GPS = NTH / DK, TPG = TBF / GPS;       // walk lanes per key slot, tokens per lane
     static_assert(GPS * DK == NTH && TPG * GPS == TBF && GPS <= 16 && (GPS & (GPS - 1)) == 0,
                   "the walk lanes of a slot split the block evenly within a DPP row");
 
-    __shared__ float sIn[TBF * ROW];
-    __shared__ float sRed[TBF][NG][DVT];
+    extern __shared__ __align__(16) unsigned char smem[];
+    float* sIn = reinterpret_cast<float*>(smem + L::L_IN);
+    A* sF = reinterpret_cast<A*>(smem + L::L_F);
+    float* sRed = reinterpret_cast<float*>(smem + L::L_RED);   // [TBF][NG][DVT]
 
     const T_* q = static_cast<const T_*>(g.q);
     const T_* k = static_cast<const T_*>(g.k);
@@ -156,16 +196,16 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
     const bool owns = ng < DK;  // with NG > DK some n-groups are idle
     const size_t row0 = (size_t)b * s.T;
 
-    float Hs[NPER];
+    A Hs[NPER];
 #pragma unroll
     for (int i = 0; i < NPER; ++i) {
         int n = ng + i * NG;
-        Hs[i] = (owns && g.eta0) ? g.eta0[((size_t)bh * DK + n) * DV + d] : 0.f;
+        Hs[i] = (owns && g.eta0) ? (A)g.eta0[((size_t)bh * DK + n) * DV + d] : A(0);
     }
     const int wn = tid / GPS, wg = tid % GPS;   // walk: key slot and token group of this lane
-    float lam = g.lam0 ? g.lam0[(size_t)bh * DK + wn] : 1.f;   // lam before the block, in every lane of slot wn
+    A lam = g.lam0 ? (A)g.lam0[(size_t)bh * DK + wn] : A(1);   // lam before the block, in every lane of slot wn
     const bool ou = g.ou_a != nullptr;
-    float oa = 0.f, op = 0.f;
+    A oa = 0, op = 0;
     if (ou) ou_gates(g.ou_a[h * DK + wn], g.ou_p[h * DK + wn], g.ou_d[h * DK + wn], oa, op);
 
     Part<TBF, DK, NTH> xa, xp, xk, xq;
@@ -207,7 +247,7 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
     }
     barrier_lds();
     static_assert(kCKI % TBF == 0, "checkpoints fall on block starts");
-    float* saved_H = saved_lam ? saved_lam + saved_lam_floats(s) : nullptr;
+    A* saved_H = saved_lam ? saved_lam + saved_lam_elems(s) : nullptr;
     const int nck = n_checkpoints(s.T);
     for (int blk = 0; blk < nblk; ++blk) {
         const int t0 = blk * TBF, nt = min(TBF, s.T - t0);
@@ -216,15 +256,15 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
             for (int i = 0; i < NPER; ++i)
                 saved_H[(((size_t)bh * nck + t0 / kCKI) * DK + ng + i * NG) * DV + d] = Hs[i];
         }
-        float lsv[TPG];   // lam after each of this lane's tokens (the saved context)
+        A lsv[TPG];   // lam after each of this lane's tokens (the saved context)
         // Token loops carry no branch: rows past nt (the ragged last block) are worked on
         // as well, from the repeated last row, and only selects keep them out of the state.
         {
-            float ta[TPG], tp[TPG], tk[TPG], tq[TPG], tr[TPG];
+            A ta[TPG], tp[TPG], tk[TPG], tq[TPG], tr[TPG];
 #pragma unroll
             for (int u = 0; u < TPG; ++u) {
                 const float* row = sIn + (wg * TPG + u) * ROW;
-                const float ra = row[CA + wn], rp = row[CP + wn];
+                const A ra = row[CA + wn], rp = row[CP + wn];
                 ta[u] = ou ? oa : ra;
                 tp[u] = ou ? op : rp;
                 tk[u] = row[CK + wn];
@@ -232,30 +272,30 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
                 tr[u] = row[CR];
             }
             // this lane's product M_last ... M_first (tokens past nt: identity), scaled
-            float m00 = 1.f, m01 = 0.f, m10 = 0.f, m11 = 1.f;
+            A m00 = 1, m01 = 0, m10 = 0, m11 = 1;
 #pragma unroll
             for (int u = 0; u < TPG; ++u) {
-                const float a2 = ta[u] * ta[u], phi = tk[u] * tk[u] * tr[u];
-                const float z0 = fmaf(tp[u], m00, a2 * m10), z1 = fmaf(tp[u], m01, a2 * m11);
+                const A a2 = ta[u] * ta[u], phi = tk[u] * tk[u] * tr[u];
+                const A z0 = fma(tp[u], m00, a2 * m10), z1 = fma(tp[u], m01, a2 * m11);
                 const bool ok = wg * TPG + u < nt;
-                m00 = ok ? fmaf(phi, z0, m00) : m00;
-                m01 = ok ? fmaf(phi, z1, m01) : m01;
+                m00 = ok ? fma(phi, z0, m00) : m00;
+                m01 = ok ? fma(phi, z1, m01) : m01;
                 m10 = ok ? z0 : m10;
                 m11 = ok ? z1 : m11;
             }
             {
-                const float sc = rcp(fmaxf(fmaxf(m00, m01), fmaxf(m10, m11)));
+                const A sc = rcpa(amax(amax(m00, m01), amax(m10, m11)));
                 m00 *= sc; m01 *= sc; m10 *= sc; m11 *= sc;
             }
             // inclusive scan over the slot's lanes: P_g = M_g ... M_0
             auto scan_step = [&](auto dd) {
                 constexpr int D = decltype(dd)::value;
                 if constexpr (D < GPS) {
-                    const float b00 = row_shr<D>(m00), b01 = row_shr<D>(m01);
-                    const float b10 = row_shr<D>(m10), b11 = row_shr<D>(m11);
-                    const float c00 = fmaf(m00, b00, m01 * b10), c01 = fmaf(m00, b01, m01 * b11);
-                    const float c10 = fmaf(m10, b00, m11 * b10), c11 = fmaf(m10, b01, m11 * b11);
-                    const float sc = rcp(fmaxf(fmaxf(c00, c01), fmaxf(c10, c11)));
+                    const A b00 = row_shr<D>(m00), b01 = row_shr<D>(m01);
+                    const A b10 = row_shr<D>(m10), b11 = row_shr<D>(m11);
+                    const A c00 = fma(m00, b00, m01 * b10), c01 = fma(m00, b01, m01 * b11);
+                    const A c10 = fma(m10, b00, m11 * b10), c11 = fma(m10, b01, m11 * b11);
+                    const A sc = rcpa(amax(amax(c00, c01), amax(c10, c11)));
                     const bool take = wg >= D;
                     m00 = take ? c00 * sc : m00;
                     m01 = take ? c01 * sc : m01;
@@ -268,24 +308,23 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
             scan_step(std::integral_constant<int, 4>{});
             scan_step(std::integral_constant<int, 8>{});
             // the product of the groups before this one (identity for group 0) applied to lam
-            const float e00 = row_shr<1>(m00), e01 = row_shr<1>(m01);
-            const float e10 = row_shr<1>(m10), e11 = row_shr<1>(m11);
-            float lw = lam;
-            if (wg > 0) lw = fmaf(e00, lam, e01) * rcp(fmaf(e10, lam, e11));
+            const A e00 = row_shr<1>(m00), e01 = row_shr<1>(m01);
+            const A e10 = row_shr<1>(m10), e11 = row_shr<1>(m11);
+            A lw = lam;
+            if (wg > 0) lw = fma(e00, lam, e01) * rcpa(fma(e10, lam, e11));
             // walk this lane's tokens
 #pragma unroll
             for (int u = 0; u < TPG; ++u) {
                 const int j = wg * TPG + u;
                 float* row = sIn + j * ROW;
-                const float rho = rcp(ta[u] * ta[u] + tp[u] * lw);
-                const float ln = rho * lw + tk[u] * tk[u] * tr[u];
+                const A rho = rcpa(ta[u] * ta[u] + tp[u] * lw);
+                const A ln = rho * lw + tk[u] * tk[u] * tr[u];
                 lw = j < nt ? ln : lw;
                 lsv[u] = ln;
-                const float inv = rcp(ln);
-                row[CA + wn] = ta[u] * rho;
-                row[CP + wn] = tr[u] * tk[u];
-                row[CK + wn] = tq[u] * inv;
-                row[CQ + wn] = tq[u] * tq[u] * inv;
+                const A inv = rcpa(ln);
+                sF[j * DK + wn] = ta[u] * rho;
+                row[CA + wn] = (float)(tq[u] * inv);
+                row[CP + wn] = (float)(tq[u] * tq[u] * inv);
             }
             // lam after the block: the last group's, in every lane of the slot
             lam = __shfl(lw, (tid & 63 & ~(GPS - 1)) + GPS - 1, 64);
@@ -294,30 +333,30 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
 #pragma unroll
         for (int j = 0; j < TBF; ++j) {
             const float* row = sIn + j * ROW;
-            const float vd = row[CV + dl];
-            float acc = 0.f;
+            const A vr = (A)row[CV + dl] * (A)row[CR];   // v_d r
+            A acc = 0;
 #pragma unroll
             for (int i = 0; i < NPER; ++i) {
                 const int n = ng + i * NG;
                 if (NG <= DK || owns) {
-                    const float hn = row[CA + n] * Hs[i] + row[CP + n] * vd;
+                    const A hn = fma(sF[j * DK + n], Hs[i], (A)row[CK + n] * vr);
                     Hs[i] = j < nt ? hn : Hs[i];
-                    acc += row[CK + n] * hn;
+                    acc = fma((A)row[CA + n], hn, acc);
                 }
             }
-            sRed[j][ng][dl] = acc;
+            sRed[(j * NG + ng) * DVT + dl] = (float)acc;
         }
         barrier_lds();
         // the block's outputs are formed in registers and stored after the commit, whose wait
         // then covers the prefetch only
-        float yo[NY], yvo = 0.f;
+        A yo[NY], yvo = 0;
 #pragma unroll
         for (int u = 0; u < NY; ++u) {
             const int idx = tid + NTH * u, j = idx / DVT, dd = idx % DVT;
-            float acc = 0.f;
+            A acc = 0;
             if (j < nt) {
 #pragma unroll
-                for (int gi = 0; gi < NG; ++gi) acc += sRed[j][gi][dd];
+                for (int gi = 0; gi < NG; ++gi) acc += sRed[(j * NG + gi) * DVT + dd];
             }
             yo[u] = acc;
         }
@@ -325,7 +364,7 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
         const bool wv = tile == 0 && g.yvar && jv >= 0 && jv < nt;
         if (wv) {
 #pragma unroll
-            for (int n = 0; n < DK; ++n) yvo += sIn[jv * ROW + CQ + n];
+            for (int n = 0; n < DK; ++n) yvo += sIn[jv * ROW + CP + n];
         }
         barrier_lds();
         commit();
@@ -334,7 +373,7 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
             const int idx = tid + NTH * u, j = idx / DVT, dd = idx % DVT;
             if (j < nt) st(y, ((row0 + t0 + j) * s.H + h) * DV + tile * DVT + dd, yo[u]);
         }
-        if (wv) g.yvar[(row0 + t0 + jv) * s.H + h] = yvo;
+        if (wv) g.yvar[(row0 + t0 + jv) * s.H + h] = (float)yvo;
         if (saved_lam && tile == 0) {
 #pragma unroll
             for (int u = 0; u < TPG; ++u) {
@@ -346,10 +385,10 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
         barrier_lds();
     }
     wait_vm_all();   // the last (unused) prefetch has landed before the registers are released
-    if (tile == 0 && g.lamT && wg == 0) g.lamT[(size_t)bh * DK + wn] = lam;
+    if (tile == 0 && g.lamT && wg == 0) g.lamT[(size_t)bh * DK + wn] = (float)lam;
     if (g.etaT && owns) {
 #pragma unroll
-        for (int i = 0; i < NPER; ++i) g.etaT[((size_t)bh * DK + ng + i * NG) * DV + d] = Hs[i];
+        for (int i = 0; i < NPER; ++i) g.etaT[((size_t)bh * DK + ng + i * NG) * DV + d] = (float)Hs[i];
     }
 }
 
@@ -363,18 +402,22 @@ __global__ __launch_bounds__(kFwdThreads<DK>) void fwd_recurrent_kernel(Shape s,
 // from the saved lam_{t-1}, for all (token, slot) pairs of a block in one
 // parallel phase.
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g, const float* slam, float* wdqt,
-                                                               float* wPT) {
+__global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g, const typename acc<S>::type* slam,
+                                                               typename acc<S>::type* wdqt,
+                                                               typename acc<S>::type* wPT) {
     using T_ = typename storage<S>::type;
+    using A = typename acc<S>::type;
     constexpr int NT = 16, DL = 16, DPER = DV / DL;
     static_assert(DL == kTB, "lane j of a slot's row holds token j of the block");
     static_assert(kThreads == kTB * NT, "one (token, slot) gate per thread");
-    // staged row of a token: abar, pbar, k, saved lam of this workgroup's NT key slots, v [DV], dy [DV], r
-    constexpr int CA = 0, CP = NT, CK = 2 * NT, CL = 3 * NT, CV = 4 * NT, CD = CV + DV, CR = CD + DV;
+    // staged row of a token: abar, pbar, k of this workgroup's NT key slots, v [DV], dy [DV], r
+    constexpr int CA = 0, CP = NT, CK = 2 * NT, CV = 3 * NT, CD = CV + DV, CR = CD + DV;
     constexpr int ROW = CR + 1;
     __shared__ float sIn[kTB * ROW];
-    __shared__ float sLP[NT];          // lam of the token before the block
-    __shared__ float2 sFK[kTB][NT];    // F and r k of every (token, slot) of the block
+    __shared__ A sL[kTB * NT];          // saved lam_t of the block's tokens
+    __shared__ A sLP[NT];               // lam of the token before the block
+    __shared__ A sF[kTB][NT];           // F of every (token, slot) of the block
+    __shared__ A sK[kTB][NT];           // r k
 
     const T_* k = static_cast<const T_*>(g.k);
     const T_* v = static_cast<const T_*>(g.v);
@@ -391,24 +434,25 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     const int nl = tid / DL, n = ktile * NT + nl, dl = tid % DL;
     const size_t row0 = (size_t)b * s.T;
     const int ts0 = seg * kCKI, tend = min(ts0 + kCKI, s.T);   // this workgroup's tokens
-    const float* ckH = slam + saved_lam_floats(s);
+    const A* ckH = slam + saved_lam_elems(s);
 
-    float Hs[DPER];
+    A Hs[DPER];
 #pragma unroll
     for (int i = 0; i < DPER; ++i) Hs[i] = ckH[(((size_t)bh * nck + seg) * DK + n) * DV + dl + i * DL];
     // the gate phase's (token, slot) pair of this thread
     const int gsl = tid % NT, gj = tid / NT;
     const bool ou = g.ou_a != nullptr;
-    float goa = 0.f, gop = 0.f;
+    A goa = 0, gop = 0;
     if (ou) {
         const int gn = ktile * NT + gsl;
         ou_gates(g.ou_a[h * DK + gn], g.ou_p[h * DK + gn], g.ou_d[h * DK + gn], goa, gop);
     }
 
-    Part<kTB, NT> xa, xp, xk, xl;
+    Part<kTB, NT> xa, xp, xk;
+    Part<kTB, NT, kThreads, A> xl;
     Part<kTB, DV> xv, xdy;
     Part<kTB, 1> xr;
-    Part<1, NT> xlp;
+    Part<1, NT, kThreads, A> xlp;
     // with OU gates the abar / pbar columns are filled from k and not used; with no initial
     // precision, token 0's lam_{t-1} is read from the saved lam and replaced by 1
     const T_* ga = ou ? k : a;
@@ -424,15 +468,17 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
         xv.fetch(v + o * DV, s.H * DV, nt);
         xdy.fetch(dy + o * DV, s.H * DV, nt);
         xr.fetch(r + o, s.H, nt);
-        const float* lp0 = t > 0 ? slam + (o - s.H) * DK : (lam0_one ? slam + o * DK : g.lam0 + (size_t)bh * DK);
-        xlp.fetch(lp0 + ktile * NT, 0, 1);
+        if (t > 0 || lam0_one)
+            xlp.fetch(slam + (t > 0 ? o - s.H : o) * DK + ktile * NT, 0, 1);
+        else
+            xlp.fetch(g.lam0 + (size_t)bh * DK + ktile * NT, 0, 1);
     };
     auto commit = [&]() {
         wait_vm_all();   // the prefetch has landed (and stores issued before it are done)
         xa.template commit<ROW>(sIn, CA);
         xp.template commit<ROW>(sIn, CP);
         xk.template commit<ROW>(sIn, CK);
-        xl.template commit<ROW>(sIn, CL);
+        xl.template commit<NT>(sL, 0);
         xv.template commit<ROW>(sIn, CV);
         xdy.template commit<ROW>(sIn, CD);
         xr.template commit<ROW>(sIn, CR);
@@ -452,25 +498,26 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
         const int t0 = ts0 + blk * kTB, nt = min(kTB, tend - t0);
         {   // the gates of every (token, slot) from the saved lam_{t-1}, in parallel
             const float* row = sIn + gj * ROW;
-            const float ra = row[CA + gsl], rp = row[CP + gsl];
-            const float at = ou ? goa : ra, pt = ou ? gop : rp;
-            const float lp = gj > 0 ? row[CL + gsl - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[gsl]);
-            const float rho = rcp(at * at + pt * lp);
-            sFK[gj][gsl] = make_float2(at * rho, row[CR] * row[CK + gsl]);
+            const A ra = row[CA + gsl], rp = row[CP + gsl];
+            const A at = ou ? goa : ra, pt = ou ? gop : rp;
+            const A lp = gj > 0 ? sL[(gj - 1) * NT + gsl] : (t0 == 0 && lam0_one ? A(1) : sLP[gsl]);
+            const A rho = rcpa(at * at + pt * lp);
+            sF[gj][gsl] = at * rho;
+            sK[gj][gsl] = (A)row[CR] * (A)row[CK + gsl];
         }
         barrier_lds();
-        float odqt = 0.f;
+        A odqt = 0;
 #pragma unroll
         for (int j = 0; j < kTB; ++j) {   // no branch: rows past nt only reach selects
             const bool live = j < nt;
             const float* row = sIn + j * ROW;
-            const float2 fk = sFK[j][nl];   // F, r k
-            float acc = 0.f;
+            const A F = sF[j][nl], kh = sK[j][nl];
+            A acc = 0;
 #pragma unroll
             for (int i = 0; i < DPER; ++i) {
-                const float hn = fk.x * Hs[i] + fk.y * row[CV + dl + i * DL];
+                const A hn = fma(F, Hs[i], kh * (A)row[CV + dl + i * DL]);
                 Hs[i] = live ? hn : Hs[i];
-                acc += hn * row[CD + dl + i * DL];
+                acc = fma(hn, (A)row[CD + dl + i * DL], acc);
             }
             acc = row_sum16(acc);
             if (dl == j) odqt = acc;   // lane j of the slot's row keeps token j's result
@@ -483,10 +530,10 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
     }
     wait_vm_all();   // the last (unused) prefetch has landed before the registers are released
     if (seg != nck - 1) return;   // the last segment ends at the final state
-    float acc = 0.f;
+    A acc = 0;
     if (g.detaT) {
 #pragma unroll
-        for (int i = 0; i < DPER; ++i) acc += g.detaT[((size_t)bh * DK + n) * DV + dl + i * DL] * Hs[i];
+        for (int i = 0; i < DPER; ++i) acc = fma((A)g.detaT[((size_t)bh * DK + n) * DV + dl + i * DL], Hs[i], acc);
     }
     acc = row_sum16(acc);
     if (dl == 0) wPT[(size_t)bh * DK + n] = acc;
@@ -511,54 +558,81 @@ __global__ __launch_bounds__(kThreads) void bwd_sweep1_kernel(Shape s, BwdArgs g
 //   C  one lane per slot: the dG / g / c recursion over the block;
 //   D  every (token, slot): dq, dk, dabar, dpbar and the dr terms; dv sums;
 //   E  dr sums, and the next block's inputs go to LDS.
-template <int DK, int DV, int NTH_>
+template <typename A>
+struct alignas(4 * sizeof(A)) A4 {
+    A x, y, z, w;
+};
+template <typename A>
+struct alignas(2 * sizeof(A)) A2 {
+    A x, y;
+};
+
+template <int DK, int DV, int NTH_, int TB_, typename A>
 struct Sweep2Lay {
-    static constexpr int NTH = NTH_;
+    static constexpr int NTH = NTH_, TB = TB_;
     static constexpr int DVT = DV < 32 ? DV : 32, NG = NTH / DVT;
     static constexpr int NPER = DK / NG > 0 ? DK / NG : 1, DPER = DV / DVT;
-    // staged row of token t: lam_t, dqt_t, q, k, abar, pbar [DK] each; v, dy [DV]; r; the
-    // upstream gradient of the readout variance
-    static constexpr int CL = 0, CDQ = DK, CQ = 2 * DK, CK = 3 * DK, CA = 4 * DK, CP = 5 * DK;
-    static constexpr int CV = 6 * DK, CD = CV + DV, CR = CD + DV, CG = CR + 1, ROW = CG + 1;
-    static constexpr int TB = ROW * 16 * 4 <= 48 * 1024 ? 16 : 8;
-    // LDS, in floats: staged rows, then lam of the token before the block; {F_{t+1}, qt, kh,
-    // rho} and {(abar rho)^2, pbar rho, q (dqt + q gv) / lam^2, qt dqt} per (token, slot);
-    // dkh; dv partials per n-group; {dG, g} per (token, slot); dr terms; the carried forget
-    // gate (two buffers); per-thread OU sums
-    static constexpr int L_LP = TB * ROW, L_C0 = (L_LP + DK + 3) / 4 * 4, L_C1 = L_C0 + 4 * TB * DK;
-    static constexpr int L_PK = L_C1 + 4 * TB * DK, L_PV = L_PK + TB * DK, L_SG = L_PV + TB * NG * DV;
-    static constexpr int L_DR = L_SG + 2 * TB * DK, L_FC = L_DR + TB * DK, L_OU = L_FC + 2 * DK;
-    static constexpr size_t BYTES = (size_t)(L_OU + 2 * NTH) * sizeof(float);
+    // staged row of token t (fp32): q, k, abar, pbar [DK] each; v, dy [DV]; r; the upstream
+    // gradient of the readout variance.  Staged in the arithmetic type: lam_t and dqt_t [DK] each.
+    static constexpr int CQ = 0, CK = DK, CA = 2 * DK, CP = 3 * DK;
+    static constexpr int CV = 4 * DK, CD = CV + DV, CR = CD + DV, CG = CR + 1, ROW = CG + 1;
+    static constexpr int WL = 0, WDQ = DK, WROW = 2 * DK;
+    static constexpr int SA = (int)sizeof(A);
+    // LDS (bytes): {F_{t+1}, qt, kh, rho} and {(abar rho)^2, pbar rho, q (dqt + q gv) / lam^2,
+    // qt dqt} per (token, slot); the staged A rows; lam of the token before the block; dkh;
+    // {dG, g} per (token, slot); the carried forget gate (two buffers); per-thread OU sums;
+    // the staged fp32 rows; dv partials per n-group; dr terms
+    static constexpr int L_C0 = 0, L_C1 = L_C0 + 4 * TB * DK * SA, L_W = L_C1 + 4 * TB * DK * SA;
+    static constexpr int L_LP = L_W + TB * WROW * SA, L_PK = L_LP + DK * SA, L_SG = L_PK + TB * DK * SA;
+    static constexpr int L_FC = L_SG + 2 * TB * DK * SA, L_OU = L_FC + 2 * DK * SA;
+    static constexpr int L_IN = L_OU + 2 * NTH * SA, L_PV = L_IN + (TB * ROW * 4 + 15) / 16 * 16;
+    static constexpr int L_DR = L_PV + TB * NG * DV * 4;
+    static constexpr size_t BYTES = (size_t)L_DR + TB * DK * 4;
     static constexpr bool fits = NG <= DK && DK % NG == 0 && (TB * DK) % NTH == 0 && BYTES <= 160 * 1024;
 };
 
+// tokens per staged block: 16 where the LDS holds them, else 8, else 4
+template <int DK, int DV, int NTH, typename A>
+constexpr int sweep2_tb() {
+    return Sweep2Lay<DK, DV, NTH, 16, A>::fits ? 16 : Sweep2Lay<DK, DV, NTH, 8, A>::fits ? 8 : 4;
+}
+
 // 512 threads (two waves per SIMD, half the dH entries per thread) for heads of up to
 // 64 x 64 where the shape splits evenly over them and the LDS fits, else 256
-template <int DK, int DV>
-struct Sweep2Cfg : Sweep2Lay<DK, DV, (DK * DV <= 64 * 64 && Sweep2Lay<DK, DV, 512>::fits) ? 512 : 256> {
-    static_assert(Sweep2Lay<DK, DV, Sweep2Cfg::NTH>::fits, "every thread owns dH entries; LDS budget");
+template <int DK, int DV, typename A>
+constexpr int sweep2_nth() {
+    return (DK * DV <= 64 * 64 && Sweep2Lay<DK, DV, 512, sweep2_tb<DK, DV, 512, A>(), A>::fits) ? 512 : 256;
+}
+
+template <int DK, int DV, typename A>
+struct Sweep2Cfg : Sweep2Lay<DK, DV, sweep2_nth<DK, DV, A>(), sweep2_tb<DK, DV, sweep2_nth<DK, DV, A>(), A>(), A> {
+    static_assert(Sweep2Cfg::fits, "every thread owns dH entries; LDS budget");
 };
 
 template <typename S, int DK, int DV>
-__global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Shape s, BwdArgs g, const float* wlam,
-                                                               const float* wdqt, const float* wPT) {
+__global__ __launch_bounds__((Sweep2Cfg<DK, DV, typename acc<S>::type>::NTH)) void bwd_sweep2_kernel(
+    Shape s, BwdArgs g, const typename acc<S>::type* wlam, const typename acc<S>::type* wdqt,
+    const typename acc<S>::type* wPT, typename acc<S>::type* ou_part) {
     using T_ = typename storage<S>::type;
-    using C = Sweep2Cfg<DK, DV>;
+    using A = typename acc<S>::type;
+    using C = Sweep2Cfg<DK, DV, A>;
     constexpr int DVT = C::DVT, NG = C::NG, NPER = C::NPER, DPER = C::DPER, TB = C::TB, ROW = C::ROW;
+    constexpr int WROW = C::WROW;
     constexpr int NTH = C::NTH;
     constexpr int ND = TB * DK / NTH, NDV = (TB * DV + NTH - 1) / NTH;   // items per thread
     static_assert(ND * NTH == TB * DK, "(token, slot) items split evenly over the threads");
-    extern __shared__ __align__(16) float sm[];
-    float* sIn = sm;
-    float* sLP = sm + C::L_LP;    // [DK]
-    float* sC0 = sm + C::L_C0;    // [TB][DK][4]
-    float* sC1 = sm + C::L_C1;    // [TB][DK][4]
-    float* sPK = sm + C::L_PK;    // [TB][DK]
-    float* sPV = sm + C::L_PV;    // [TB][NG][DV]
-    float* sSG = sm + C::L_SG;    // [TB][DK][2]
-    float* sDR = sm + C::L_DR;    // [TB][DK]
-    float* sFC = sm + C::L_FC;    // [2][DK]
-    float* sOU = sm + C::L_OU;    // [2][NTH]
+    extern __shared__ __align__(16) unsigned char smem[];
+    A4<A>* sC0 = reinterpret_cast<A4<A>*>(smem + C::L_C0);   // [TB][DK]
+    A4<A>* sC1 = reinterpret_cast<A4<A>*>(smem + C::L_C1);   // [TB][DK]
+    A* sW = reinterpret_cast<A*>(smem + C::L_W);              // [TB][WROW]
+    A* sLP = reinterpret_cast<A*>(smem + C::L_LP);            // [DK]
+    A* sPK = reinterpret_cast<A*>(smem + C::L_PK);            // [TB][DK]
+    A2<A>* sSG = reinterpret_cast<A2<A>*>(smem + C::L_SG);   // [TB][DK]
+    A* sFC = reinterpret_cast<A*>(smem + C::L_FC);            // [2][DK]
+    A* sOU = reinterpret_cast<A*>(smem + C::L_OU);            // [2][NTH]
+    float* sIn = reinterpret_cast<float*>(smem + C::L_IN);    // [TB][ROW]
+    float* sPV = reinterpret_cast<float*>(smem + C::L_PV);    // [TB][NG][DV]
+    float* sDR = reinterpret_cast<float*>(smem + C::L_DR);    // [TB][DK]
 
     const T_* q = static_cast<const T_*>(g.q);
     const T_* k = static_cast<const T_*>(g.k);
@@ -581,37 +655,36 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
     const int nme = tid % DK;   // the key slot of this thread's (token, slot) items
     const size_t row0 = (size_t)b * s.T;
 
-    float dH[NPER][DPER];
+    A dH[NPER][DPER];
 #pragma unroll
     for (int i = 0; i < NPER; ++i)
 #pragma unroll
         for (int j = 0; j < DPER; ++j)
-            dH[i][j] = g.detaT ? g.detaT[((size_t)bh * DK + ng + i * NG) * DV + dl + j * DVT] : 0.f;
+            dH[i][j] = g.detaT ? (A)g.detaT[((size_t)bh * DK + ng + i * NG) * DV + dl + j * DVT] : A(0);
 
     // the dG / c recursion lives in threads tid < DK
-    float cnext = 0.f, Sg = 0.f;
+    A cnext = 0, Sg = 0;
     if (tid < DK) {
-        cnext = g.dlamT ? g.dlamT[(size_t)bh * DK + tid] : 0.f;
+        cnext = g.dlamT ? (A)g.dlamT[(size_t)bh * DK + tid] : A(0);
         Sg = wPT[(size_t)bh * DK + tid];
-        sFC[DK + tid] = 1.f;   // no forget gate after the last token
+        sFC[DK + tid] = 1;   // no forget gate after the last token
     }
     const bool ou = g.ou_a != nullptr;
-    float oa = 0.f, op = 0.f, sum_da = 0.f, sum_dp = 0.f;
+    A oa = 0, op = 0, sum_da = 0, sum_dp = 0;
     if (ou) ou_gates(g.ou_a[h * DK + nme], g.ou_p[h * DK + nme], g.ou_d[h * DK + nme], oa, op);
 
-    Part<TB, DK, NTH> xl, xdq, xq, xk, xa, xp;
+    Part<TB, DK, NTH> xq, xk, xa, xp;
+    Part<TB, DK, NTH, A> xl, xdq;
     Part<TB, DV, NTH> xv, xdy;
     Part<TB, 1, NTH> xr, xg;
-    Part<1, DK, NTH> xlp;
+    Part<1, DK, NTH, A> xlp;
     // Loads stay unconditional: absent tensors are replaced by present ones whose values
     // are not used (OU gates: abar / pbar columns from k; no readout-variance gradient:
-    // its column from lam, scaled by zero; no initial precision: token 0's lam_{t-1}
-    // from lam_0, replaced by 1 where it is read).
+    // its column from r, scaled by zero; no initial precision: token 0's lam_{t-1}
+    // from the saved lam, replaced by 1 where it is read).
     const T_* ga = ou ? k : a;
     const T_* gp = ou ? k : p;
-    const float* gvar = g.dyvar ? g.dyvar : wlam;
-    const float gscale = g.dyvar ? 1.f : 0.f;
-    const float* glam0 = g.lam0 ? g.lam0 + (size_t)bh * DK : wlam + (row0 * s.H + h) * DK;
+    const A gscale = g.dyvar ? A(1) : A(0);
     const bool lam0_one = g.lam0 == nullptr;
     auto fetch = [&](int t) {
         const int nt = min(TB, s.T - t);
@@ -626,13 +699,19 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
         xv.fetch(v + o * DV, s.H * DV, nt);
         xdy.fetch(dy + o * DV, s.H * DV, nt);
         xr.fetch(r + o, s.H, nt);
-        xg.fetch(gvar + (g.dyvar ? o : o * DK), g.dyvar ? s.H : ts, nt);
-        xlp.fetch(t > 0 ? wlam + (o - s.H) * DK : glam0, 0, 1);
+        if (g.dyvar)
+            xg.fetch(g.dyvar + o, s.H, nt);
+        else
+            xg.fetch(r + o, s.H, nt);
+        if (t > 0 || lam0_one)
+            xlp.fetch(wlam + (t > 0 ? o - s.H : o) * DK, 0, 1);
+        else
+            xlp.fetch(g.lam0 + (size_t)bh * DK, 0, 1);
     };
     auto commit = [&]() {
         wait_vm_all();   // the prefetch has landed (and stores issued before it are done)
-        xl.template commit<ROW>(sIn, C::CL);
-        xdq.template commit<ROW>(sIn, C::CDQ);
+        xl.template commit<WROW>(sW, C::WL);
+        xdq.template commit<WROW>(sW, C::WDQ);
         xq.template commit<ROW>(sIn, C::CQ);
         xk.template commit<ROW>(sIn, C::CK);
         xa.template commit<ROW>(sIn, C::CA);
@@ -661,30 +740,31 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
             const int j = idx / DK, n = idx % DK;
             if (j < nt) {
                 const float* row = sIn + j * ROW;
-                const float lam = row[C::CL + n];
-                const float lp = j > 0 ? row[C::CL + n - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[n]);
-                const float dqt = row[C::CDQ + n], qv = row[C::CQ + n], kv = row[C::CK + n];
-                const float ra = row[C::CA + n], rp = row[C::CP + n];
-                const float at = ou ? oa : ra, pt = ou ? op : rp;
-                const float rt = row[C::CR], gv = gscale * row[C::CG];
-                const float rho = rcp(at * at + pt * lp);
-                const float il = rcp(lam), qtl = qv * il, F = at * rho;
-                float* c0 = sC0 + 4 * (j * DK + n);
-                c0[1] = qtl;
-                c0[2] = rt * kv;
-                c0[3] = rho;
-                if (j > 0) sC0[4 * ((j - 1) * DK + n)] = F;
+                const A* wrow = sW + j * WROW;
+                const A lam = wrow[C::WL + n];
+                const A lp = j > 0 ? wrow[C::WL + n - WROW] : (t0 == 0 && lam0_one ? A(1) : sLP[n]);
+                const A dqt = wrow[C::WDQ + n], qv = row[C::CQ + n], kv = row[C::CK + n];
+                const A ra = row[C::CA + n], rp = row[C::CP + n];
+                const A at = ou ? oa : ra, pt = ou ? op : rp;
+                const A rt = row[C::CR], gv = gscale * (A)row[C::CG];
+                const A rho = rcpa(at * at + pt * lp);
+                const A il = rcpa(lam), qtl = qv * il, F = at * rho;
+                A4<A>& c0 = sC0[j * DK + n];
+                c0.y = qtl;
+                c0.z = rt * kv;
+                c0.w = rho;
+                if (j > 0) sC0[(j - 1) * DK + n].x = F;
                 else sFC[(cur ^ 1) * DK + n] = F;
-                if (j == nt - 1) c0[0] = sFC[cur * DK + n];
-                *reinterpret_cast<float4*>(sC1 + 4 * (j * DK + n)) =
-                    make_float4(F * F, pt * rho, qv * (dqt + qv * gv) * il * il, qtl * dqt);
+                if (j == nt - 1) c0.x = sFC[cur * DK + n];
+                sC1[j * DK + n] = A4<A>{F * F, pt * rho, qv * (dqt + qv * gv) * il * il, qtl * dqt};
             }
         }
         barrier_lds();
         // ---- B
         // tokens latest first, in runs of UB unrolled tokens: the whole block for small heads,
         // shorter runs where a thread holds many dH entries (keeps the loads in registers)
-        constexpr int UB = NPER * DPER <= 2 ? TB : NPER * DPER <= 4 ? 8 : NPER * DPER <= 16 ? 4 : 2;
+        constexpr int UB0 = NPER * DPER <= 2 ? TB : NPER * DPER <= 4 ? 8 : NPER * DPER <= 16 ? 4 : 2;
+        constexpr int UB = UB0 < TB ? UB0 : TB;
         static_assert(TB % UB == 0, "runs split the block");
 #pragma unroll 1
         for (int jb = TB - UB; jb >= 0; jb -= UB)
@@ -693,29 +773,29 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
             const int j = jb + jj;
             const bool live = j < nt;
             const float* row = sIn + j * ROW;
-            float dyd[DPER], vd[DPER], pv[DPER];
+            A dyd[DPER], vd[DPER], pv[DPER];
 #pragma unroll
             for (int jd = 0; jd < DPER; ++jd) {
                 dyd[jd] = row[C::CD + dl + jd * DVT];
                 vd[jd] = row[C::CV + dl + jd * DVT];
-                pv[jd] = 0.f;
+                pv[jd] = 0;
             }
 #pragma unroll
             for (int i = 0; i < NPER; ++i) {
                 const int n = ng + i * NG;
-                const float4 co = *reinterpret_cast<const float4*>(sC0 + 4 * (j * DK + n));
-                float pk = 0.f;
+                const A4<A> co = sC0[j * DK + n];
+                A pk = 0;
 #pragma unroll
                 for (int jd = 0; jd < DPER; ++jd) {
-                    const float hn = co.x * dH[i][jd] + co.y * dyd[jd];
+                    const A hn = fma(co.x, dH[i][jd], co.y * dyd[jd]);
                     dH[i][jd] = live ? hn : dH[i][jd];
-                    pk += hn * vd[jd];
-                    pv[jd] += hn * co.z;
+                    pk = fma(hn, vd[jd], pk);
+                    pv[jd] = fma(hn, co.z, pv[jd]);
                 }
                 sPK[j * DK + n] = group_sum_all<DVT>(pk);   // the same value from every lane of the group
             }
 #pragma unroll
-            for (int jd = 0; jd < DPER; ++jd) sPV[(j * NG + ng) * DV + dl + jd * DVT] = pv[jd];
+            for (int jd = 0; jd < DPER; ++jd) sPV[(j * NG + ng) * DV + dl + jd * DVT] = (float)pv[jd];
         }
         barrier_lds();
         // ---- C
@@ -723,12 +803,12 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
 #pragma unroll
             for (int j = TB - 1; j >= 0; --j) {   // no branch: rows past nt only reach selects
                 const bool live = j < nt;
-                const float kh = sC0[4 * (j * DK + tid) + 2];
-                const float4 c1 = *reinterpret_cast<const float4*>(sC1 + 4 * (j * DK + tid));
-                const float dkh = sPK[j * DK + tid];
-                const float sg = Sg + (c1.w - kh * dkh);   // dG_t
-                const float gl = cnext - c1.z;              // g_t
-                *reinterpret_cast<float2*>(sSG + 2 * (j * DK + tid)) = make_float2(sg, gl);
+                const A kh = sC0[j * DK + tid].z;
+                const A4<A> c1 = sC1[j * DK + tid];
+                const A dkh = sPK[j * DK + tid];
+                const A sg = Sg + (c1.w - kh * dkh);   // dG_t
+                const A gl = cnext - c1.z;              // g_t
+                sSG[j * DK + tid] = A2<A>{sg, gl};
                 Sg = live ? sg : Sg;
                 cnext = live ? c1.x * gl - c1.y * sg : cnext;
             }
@@ -736,38 +816,39 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
         barrier_lds();
         // ---- D (results in registers: they are stored after the commit, whose wait then
         // covers the prefetch only)
-        float o_dq[ND], o_dk[ND], o_da[ND], o_dp[ND], o_dv[NDV];
+        A o_dq[ND], o_dk[ND], o_da[ND], o_dp[ND], o_dv[NDV];
 #pragma unroll
         for (int u = 0; u < ND; ++u) {
             const int idx = tid + NTH * u, j = idx / DK, n = idx % DK;
             const float* row = sIn + j * ROW;
-            const float lam = row[C::CL + n];
-            const float lp = j > 0 ? row[C::CL + n - ROW] : (t0 == 0 && lam0_one ? 1.f : sLP[n]);
-            const float dqt = row[C::CDQ + n], qv = row[C::CQ + n], kv = row[C::CK + n];
-            const float ra = row[C::CA + n], rp = row[C::CP + n];
-            const float at = ou ? oa : ra, pt = ou ? op : rp;
-            const float rt = row[C::CR], gv = gscale * row[C::CG];
-            const float rho = sC0[4 * (j * DK + n) + 3];
-            const float dkh = sPK[j * DK + n];
-            const float2 sg = *reinterpret_cast<const float2*>(sSG + 2 * (j * DK + n));
-            const float qg = qv * gv;
-            const float drho = sg.y * lp + sg.x * (at * at + pt * lp);
-            o_dq[u] = (dqt + 2.f * qg) * rcp(lam);
-            o_dk[u] = rt * dkh + 2.f * kv * rt * sg.y;
-            o_da[u] = sg.x * rcp(at) - 2.f * at * rho * rho * drho;
+            const A* wrow = sW + j * WROW;
+            const A lam = wrow[C::WL + n];
+            const A lp = j > 0 ? wrow[C::WL + n - WROW] : (t0 == 0 && lam0_one ? A(1) : sLP[n]);
+            const A dqt = wrow[C::WDQ + n], qv = row[C::CQ + n], kv = row[C::CK + n];
+            const A ra = row[C::CA + n], rp = row[C::CP + n];
+            const A at = ou ? oa : ra, pt = ou ? op : rp;
+            const A rt = row[C::CR], gv = gscale * (A)row[C::CG];
+            const A rho = sC0[j * DK + n].w;
+            const A dkh = sPK[j * DK + n];
+            const A2<A> sg = sSG[j * DK + n];
+            const A qg = qv * gv;
+            const A drho = sg.y * lp + sg.x * (at * at + pt * lp);
+            o_dq[u] = (dqt + A(2) * qg) * rcpa(lam);
+            o_dk[u] = rt * dkh + A(2) * kv * rt * sg.y;
+            o_da[u] = sg.x * rcpa(at) - A(2) * at * rho * rho * drho;
             o_dp[u] = -lp * rho * rho * drho;
             if (j < nt) {
                 if (ou) {
                     sum_da += o_da[u];
                     sum_dp += o_dp[u];
                 }
-                sDR[j * DK + n] = kv * dkh + kv * kv * sg.y;
+                sDR[j * DK + n] = (float)(kv * dkh + kv * kv * sg.y);
             }
         }
 #pragma unroll
         for (int u = 0; u < NDV; ++u) {
             const int idx = tid + NTH * u, j = idx / DV, dd = idx % DV;
-            float acc = 0.f;
+            A acc = 0;
             if (j < nt) {
 #pragma unroll
                 for (int gi = 0; gi < NG; ++gi) acc += sPV[(j * NG + gi) * DV + dd];
@@ -796,7 +877,7 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
             if (j < nt && idx < TB * DV) st(dv, ((row0 + t0 + j) * s.H + h) * DV + dd, o_dv[u]);
         }
         if (tid < nt) {
-            float acc = 0.f;
+            A acc = 0;
 #pragma unroll
             for (int n = 0; n < DK; ++n) acc += sDR[tid * DK + n];
             st(dr, (row0 + t0 + tid) * s.H + h, acc);
@@ -806,20 +887,20 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
         barrier_lds();
     }
     wait_vm_all();   // the last (unused) prefetch has landed before the registers are released
-    if (tid < DK && g.dlam0) g.dlam0[(size_t)bh * DK + tid] = cnext;
+    if (tid < DK && g.dlam0) g.dlam0[(size_t)bh * DK + tid] = (float)cnext;
     if (ou) {   // part b of the token sums: the threads of one slot are combined in order
         sOU[tid] = sum_da;
         sOU[NTH + tid] = sum_dp;
         barrier_lds();
         if (tid < DK) {
-            float sa = 0.f, sp = 0.f;
+            A sa = 0, sp = 0;
             for (int i = tid; i < NTH; i += DK) {
                 sa += sOU[i];
                 sp += sOU[NTH + i];
             }
             const size_t np = (size_t)s.B * s.H * DK;
-            g.ou_part[(size_t)bh * DK + tid] = sa;
-            g.ou_part[np + (size_t)bh * DK + tid] = sp;
+            ou_part[(size_t)bh * DK + tid] = sa;
+            ou_part[np + (size_t)bh * DK + tid] = sp;
         }
     }
     if (g.deta0) {   // sFC[cur] holds F of token 0
@@ -828,7 +909,7 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
 #pragma unroll
             for (int j = 0; j < DPER; ++j) {
                 const int n = ng + i * NG;
-                g.deta0[((size_t)bh * DK + n) * DV + dl + j * DVT] = sFC[cur * DK + n] * dH[i][j];
+                g.deta0[((size_t)bh * DK + n) * DV + dl + j * DVT] = (float)(sFC[cur * DK + n] * dH[i][j]);
             }
     }
 }
@@ -839,11 +920,12 @@ __global__ __launch_bounds__((Sweep2Cfg<DK, DV>::NTH)) void bwd_sweep2_kernel(Sh
 template <typename S, int DK, int DV>
 __global__ __launch_bounds__(kThreads) void decode_kernel(int H, DecodeArgs g) {
     using T_ = typename storage<S>::type;
+    using A = typename acc<S>::type;
     constexpr int DV4 = DV / 4;
     constexpr int NG = (kThreads / DV4) < DK ? (kThreads / DV4) : DK;
     constexpr int NPER = DK / NG;
-    __shared__ float sF[DK], sKh[DK], sQt[DK], sW[DK], sV[DV];
-    __shared__ float4 sRed[NG][DV4];
+    __shared__ A sF[DK], sKh[DK], sQt[DK], sW[DK], sV[DV];
+    __shared__ A4<A> sRed[NG][DV4];
 
     const T_* q = static_cast<const T_*>(g.q);
     const T_* k = static_cast<const T_*>(g.k);
@@ -857,7 +939,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(int H, DecodeArgs g) {
     const int tid = threadIdx.x;
     if (tid < DK) {
         const size_t o = sh * DK + tid;
-        float at, pt;
+        A at, pt;
         if (g.ou_a) {
             const int oh = (int)(sh % H) * DK + tid;
             ou_gates(g.ou_a[oh], g.ou_p[oh], g.ou_d[oh], at, pt);
@@ -865,12 +947,12 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(int H, DecodeArgs g) {
             at = ld(a, o);
             pt = ld(p, o);
         }
-        const float kt = ld(k, o), qt = ld(q, o), rt = ld(r, sh);
-        const float lam = g.lam[o];
-        const float rho = 1.f / (at * at + pt * lam);
-        const float ln = rho * lam + kt * kt * rt;
-        g.lam[o] = ln;
-        const float inv = 1.f / ln;
+        const A kt = ld(k, o), qt = ld(q, o), rt = ld(r, sh);
+        const A lam = g.lam[o];
+        const A rho = A(1) / (at * at + pt * lam);
+        const A ln = rho * lam + kt * kt * rt;
+        g.lam[o] = (float)ln;
+        const A inv = A(1) / ln;
         sF[tid] = at * rho;
         sKh[tid] = rt * kt;
         sQt[tid] = qt * inv;
@@ -880,31 +962,29 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(int H, DecodeArgs g) {
     __syncthreads();
     const int d4 = tid % DV4, ng = tid / DV4;
     if (ng < NG) {
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        const float4 vv = make_float4(sV[4 * d4], sV[4 * d4 + 1], sV[4 * d4 + 2], sV[4 * d4 + 3]);
+        A4<A> acc{0, 0, 0, 0};
+        const A4<A> vv{sV[4 * d4], sV[4 * d4 + 1], sV[4 * d4 + 2], sV[4 * d4 + 3]};
         float4* eta4 = reinterpret_cast<float4*>(g.eta + sh * DK * DV);
 #pragma unroll 4
         for (int i = 0; i < NPER; ++i) {
             const int n = ng + i * NG;
-            float4 e = eta4[n * DV4 + d4];
-            const float F = sF[n], kh = sKh[n], qt = sQt[n];
-            e.x = F * e.x + kh * vv.x;
-            e.y = F * e.y + kh * vv.y;
-            e.z = F * e.z + kh * vv.z;
-            e.w = F * e.w + kh * vv.w;
-            eta4[n * DV4 + d4] = e;
-            acc.x += qt * e.x;
-            acc.y += qt * e.y;
-            acc.z += qt * e.z;
-            acc.w += qt * e.w;
+            const float4 e = eta4[n * DV4 + d4];
+            const A F = sF[n], kh = sKh[n], qt = sQt[n];
+            const A ex = fma(F, (A)e.x, kh * vv.x), ey = fma(F, (A)e.y, kh * vv.y);
+            const A ez = fma(F, (A)e.z, kh * vv.z), ew = fma(F, (A)e.w, kh * vv.w);
+            eta4[n * DV4 + d4] = make_float4((float)ex, (float)ey, (float)ez, (float)ew);
+            acc.x = fma(qt, ex, acc.x);
+            acc.y = fma(qt, ey, acc.y);
+            acc.z = fma(qt, ez, acc.z);
+            acc.w = fma(qt, ew, acc.w);
         }
         sRed[ng][d4] = acc;
     }
     __syncthreads();
     if (tid < DV4) {
-        float4 acc = sRed[0][tid];
+        A4<A> acc = sRed[0][tid];
         for (int gi = 1; gi < NG; ++gi) {
-            const float4 x = sRed[gi][tid];
+            const A4<A> x = sRed[gi][tid];
             acc.x += x.x;
             acc.y += x.y;
             acc.z += x.z;
@@ -916,9 +996,9 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(int H, DecodeArgs g) {
         st(y, sh * DV + 4 * tid + 3, acc.w);
     }
     if (g.yvar && tid == kThreads - 1) {
-        float acc = 0.f;
+        A acc = 0;
         for (int n = 0; n < DK; ++n) acc += sW[n];
-        g.yvar[sh] = acc;
+        g.yvar[sh] = (float)acc;
     }
 }
 
@@ -936,40 +1016,50 @@ hipError_t dispatch(const Shape& s, A&&... args) {
     return hipErrorInvalidValue;
 }
 
+// more than 64 KiB of LDS must be opted into once per kernel (thread-safe static init at the caller)
+template <typename K>
+hipError_t allow_lds(K kern, size_t bytes) {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)bytes);
+}
+
 template <typename S, int DK, int DV>
 struct FwdL {
-    static hipError_t run(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st) {
-        constexpr int DVT = kFwdDVT<DV>;
-        const unsigned grid = (unsigned)(s.B * s.H * (DV / DVT));
-        hipLaunchKernelGGL((fwd_recurrent_kernel<S, DK, DV>), dim3(grid), dim3(kFwdThreads<DK>), 0, st, s, a,
-                           saved_lam);
+    static hipError_t run(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st) {
+        using A = typename acc<S>::type;
+        using L = FwdLay<S, DK, DV>;
+        auto kern = fwd_recurrent_kernel<S, DK, DV>;
+        static const hipError_t attr = allow_lds(kern, L::BYTES);
+        if (attr != hipSuccess) return attr;
+        const unsigned grid = (unsigned)(s.B * s.H * (DV / L::DVT));
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(L::NTH), L::BYTES, st, s, a, static_cast<A*>(saved));
         return hipGetLastError();
     }
 };
 
 template <typename S, int DK, int DV>
 struct BwdL {
-    static hipError_t run(const Shape& s, const BwdArgs& a, const float* saved_lam, void* ws, hipStream_t st) {
-        if (!saved_lam) return hipErrorInvalidValue;
+    static hipError_t run(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st) {
+        using A = typename acc<S>::type;
+        if (!saved) return hipErrorInvalidValue;
+        const A* slam = static_cast<const A*>(saved);
         const size_t ntok = (size_t)s.B * s.T * s.H * DK;
-        float* wdqt = static_cast<float*>(ws);
-        float* wPT = wdqt + ntok;
+        A* wdqt = static_cast<A*>(ws);
+        A* wPT = wdqt + ntok;
         // PT is written by the last segment's workgroups; with T == 0 it is detaT . eta0 summed over d,
         // which the reverse sweep does not need (no token reads it), so no workgroup is launched
         const unsigned grid1 = (unsigned)(s.B * s.H * (DK / 16) * n_checkpoints(s.T));
         if (grid1 > 0)
-            hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV>), dim3(grid1), dim3(kThreads), 0, st, s, a, saved_lam,
-                               wdqt, wPT);
-        const float* lam_t = saved_lam;
+            hipLaunchKernelGGL((bwd_sweep1_kernel<S, DK, DV>), dim3(grid1), dim3(kThreads), 0, st, s, a, slam, wdqt,
+                               wPT);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
+        using C = Sweep2Cfg<DK, DV, A>;
         auto kern = bwd_sweep2_kernel<S, DK, DV>;
-        constexpr size_t bytes = Sweep2Cfg<DK, DV>::BYTES;
-        // more than 64 KiB of LDS must be opted into once per kernel (thread-safe static init)
-        static const hipError_t attr =
-            hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+        static const hipError_t attr = allow_lds(kern, C::BYTES);
         if (attr != hipSuccess) return attr;
-        hipLaunchKernelGGL(kern, dim3(s.B * s.H), dim3(Sweep2Cfg<DK, DV>::NTH), bytes, st, s, a, lam_t, wdqt, wPT);
+        hipLaunchKernelGGL(kern, dim3(s.B * s.H), dim3(C::NTH), C::BYTES, st, s, a, slam, wdqt, wPT,
+                           static_cast<A*>(a.ou_part));
         return hipGetLastError();
     }
 };
@@ -985,25 +1075,26 @@ struct DecL {
 }  // namespace
 
 size_t recurrent_saved_bytes(const Shape& s) {
-    return (saved_lam_floats(s) + (size_t)s.B * s.H * n_checkpoints(s.T) * s.dk * s.dv) * sizeof(float);
+    return (saved_lam_elems(s) + (size_t)s.B * s.H * n_checkpoints(s.T) * s.dk * s.dv) * acc_bytes(s);
 }
 
-hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, float* saved_lam, hipStream_t st) {
-    return dispatch<FwdL>(s, a, saved_lam, st);
+hipError_t launch_forward_recurrent(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st) {
+    return dispatch<FwdL>(s, a, saved, st);
 }
 
 // one part per batch row: the recurrent backward walks a whole (b, h) in one workgroup
 int recurrent_ou_parts(const Shape& s) { return s.B; }
+size_t recurrent_ou_part_bytes(const Shape& s) { return acc_bytes(s); }
 
-// dqt_t [B, T, H, dk] and PT [B, H, dk]
+// dqt_t [B, T, H, dk] and PT [B, H, dk], in the arithmetic type
 size_t backward_recurrent_workspace(const Shape& s) {
     const size_t ntok = (size_t)s.B * s.T * s.H * s.dk;
-    return (ntok + (size_t)s.B * s.H * s.dk) * sizeof(float);
+    return (ntok + (size_t)s.B * s.H * s.dk) * acc_bytes(s);
 }
 
-hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, const float* saved_lam, void* ws,
+hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, const void* saved, void* ws,
                                      hipStream_t st) {
-    return dispatch<BwdL>(s, a, saved_lam, ws, st);
+    return dispatch<BwdL>(s, a, saved, ws, st);
 }
 
 hipError_t launch_decode_step(const Shape& s, const DecodeArgs& a, hipStream_t st) {

@@ -8,13 +8,14 @@ import numpy as np
 TOL = {"f32": 1e-4, "bf16": 2e-2}
 
 
-def rel_err(x, ref, floor_frac: float = 1.0) -> float:
+def rel_err(x, ref, floor_frac: float = 0.01) -> float:
     """max_i |x_i - r_i| / max(|r_i|, floor_frac * rms(r)).
 
-    The gate uses floor_frac = 1: an element at least as large as the tensor's
-    rms is judged relative to itself, a smaller one (the result of cancellation
-    between terms of rms size, whose rounding error scales with the rms) relative
-    to the rms.  floor_frac = 0.01 gives the stricter figure also reported."""
+    The gate uses floor_frac = 0.01: an element is judged relative to itself
+    unless it is smaller than 1% of the tensor's rms, where the floor stands in
+    for it (a near-zero element is the result of cancellation between terms of
+    rms size, whose rounding error scales with the rms).  floor_frac = 1 gives
+    the rms-relative figure also reported."""
     x = np.asarray(x, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert x.shape == ref.shape, (x.shape, ref.shape)
@@ -22,6 +23,24 @@ def rel_err(x, ref, floor_frac: float = 1.0) -> float:
         return 0.0
     rms = np.sqrt(np.mean(ref * ref))
     floor = max(floor_frac * rms, 1e-300)
+    return float(np.max(np.abs(x - ref) / np.maximum(np.abs(ref), floor)))
+
+
+def rel_err_sum(x, ref, mass, floor_frac: float = 0.01) -> float:
+    """rel_err for a tensor each of whose elements is a sum over (b, t) of per-token
+    terms (the gradient of a parameter shared by every token): the error of an
+    element is judged against max(|r_i|, floor_frac * rms(r), mass_i), where mass_i is
+    the sum of the absolute values of its terms.  A sum of terms each accurate to a
+    relative delta is accurate to delta * mass; with heavy cancellation (|r_i| much
+    smaller than mass_i) that, and not |r_i|, is the scale of its rounding."""
+    x = np.asarray(x, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    mass = np.asarray(mass, dtype=np.float64)
+    assert x.shape == ref.shape == mass.shape, (x.shape, ref.shape, mass.shape)
+    if ref.size == 0:
+        return 0.0
+    rms = np.sqrt(np.mean(ref * ref))
+    floor = np.maximum(max(floor_frac * rms, 1e-300), mass)
     return float(np.max(np.abs(x - ref) / np.maximum(np.abs(ref), floor)))
 
 

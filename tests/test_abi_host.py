@@ -151,8 +151,11 @@ def test_per_channel_entry_points(lib):
               "kla_backward_pc_workspace"):
         assert n in names
     d = _desc(B=2, T=20, H=3, dk=32, dv=16)
-    # the saved context holds lam and eta at every 8th token: 3 checkpoints of [B, H, dk, dv]
-    assert lib.kla_saved_pc_bytes(ctypes.byref(d)) == 2 * 2 * 3 * 3 * 32 * 16 * 4
+    # the saved context holds lam and eta at every 8th token: 3 checkpoints of [B, H, dk, dv],
+    # in the arithmetic type (fp64 for fp32 inputs, fp32 for bf16 inputs)
+    assert lib.kla_saved_pc_bytes(ctypes.byref(d)) == 2 * 2 * 3 * 3 * 32 * 16 * 8
+    assert lib.kla_saved_pc_bytes(ctypes.byref(_desc(B=2, T=20, H=3, dk=32, dv=16, dtype=1))) == \
+        2 * 2 * 3 * 3 * 32 * 16 * 4
     assert lib.kla_backward_pc_workspace(ctypes.byref(d), 0) > lib.kla_backward_pc_workspace(ctypes.byref(d), 1)
     fake = ctypes.c_void_p(0x10000)
     # q k v a p r lam0 eta0 y yvar lamT etaT saved ws
@@ -188,3 +191,17 @@ def test_block_scaffolding_entry_points(lib):
     assert lib.kla_qk_norm_backward(10, 32, 1, fake, fake, fake, fake, fake, fake, fake, 0, None) == 5
     assert lib.kla_gate_forward(12, 1, fake, fake, fake, None) == 2                       # n % 8 for bf16
     assert lib.kla_gate_backward(16, 1, fake, fake, None, fake, fake, None) == 1
+
+
+def test_saved_context_layout_follows_the_backward(lib):
+    """The forward fills the saved context in the layout of the backward that will read
+    it: bf16 with dk >= 32 but dv = 16 runs the token-recurrent backward, so its context
+    is the per-token precision plus a state checkpoint every 64 tokens, not the chunked one."""
+    import paper_2602_10743_amd as K
+    B, T, H, dk = 2, 64, 3, 64
+    nck = (T + 63) // 64
+    rec = (B * T * H * dk + B * H * nck * dk * 16) * 4   # bf16 inputs: fp32 arithmetic
+    assert K.kla_saved_bytes(_desc(B, T, H, dk, 16, 1)) == rec
+    nchunk = (T + 31) // 32
+    chunked = B * H * dk * (nchunk + (nchunk + 1) * 32) * 4
+    assert K.kla_saved_bytes(_desc(B, T, H, dk, 32, 1)) == chunked

@@ -16,7 +16,7 @@ import pytest
 
 import kla_inputs as K
 import oracle
-from kla_testutil import TOL, bits_to_torch, log, rel_err, to_np, to_torch
+from kla_testutil import TOL, bits_to_torch, log, rel_err, rel_err_sum, to_np, to_torch
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -36,7 +36,15 @@ def kla():
 
 def _check(name, got, ref, tol, report):
     e = rel_err(got, ref)
-    report.append(f"{name}={e:.2e}(1%floor {rel_err(got, ref, 0.01):.1e})")
+    report.append(f"{name}={e:.2e}(rms-rel {rel_err(got, ref, 1.0):.1e})")
+    assert np.all(np.isfinite(got)), f"{name} has non-finite values"
+    assert e <= tol, f"{name}: rel err {e:.3e} > {tol:.0e}"
+
+
+def _check_sum(name, got, ref, mass, tol, report):
+    """Parameter gradients: sums over (b, t), judged against the mass of their terms."""
+    e = rel_err_sum(got, ref, mass)
+    report.append(f"{name}={e:.2e}(plain {rel_err(got, ref):.1e})")
     assert np.all(np.isfinite(got)), f"{name} has non-finite values"
     assert e <= tol, f"{name}: rel err {e:.3e} > {tol:.0e}"
 
@@ -91,15 +99,17 @@ def test_ou_forward_backward_small(kla, B, T, H, dk, dv, dtype, dist):
     torch.cuda.synchronize()
     ref = oracle.forward_ou(case["q"], case["k"], case["v"], Pd["a"], Pd["p"], Pd["delta"], case["r"], lam0, eta0)
     rg = oracle.backward_ou(case["q"], case["k"], case["v"], Pd["a"], Pd["p"], Pd["delta"], case["r"], lam0, eta0,
-                            case["dy"], dlamT, detaT, dyvar=dyvar)
+                            case["dy"], dlamT, detaT, dyvar=dyvar, with_mass=True)
     tol = TOL[dtype]
     rep = []
     _check("y", to_np(out["y"]), K.quantise(ref["y"], dtype), tol, rep)
     _check("yvar", to_np(out["yvar"]), ref["yvar"], TOL["f32"], rep)
     _check("lamT", to_np(out["lamT"]), ref["lamT"], TOL["f32"], rep)
     _check("etaT", to_np(out["etaT"]), ref["etaT"], tol if dtype == "bf16" else TOL["f32"], rep)
-    for n in ("dq", "dk", "dv", "dr", "dlam0", "deta0", "da", "dp", "ddelta"):
+    for n in ("dq", "dk", "dv", "dr", "dlam0", "deta0"):
         _check(n, to_np(gr[n]), rg[n], tol, rep)
+    for n in ("da", "dp", "ddelta"):
+        _check_sum(n, to_np(gr[n]), rg[n], rg["mass_" + n], tol, rep)
     for n in ("dq", "dk", "dv", "dr", "da", "dp", "ddelta"):
         assert torch.equal(gr[n], gr2[n]), f"{n} differs between saved and recomputed context"
     assert np.all(to_np(out["lamT"]) > 0) and np.all(to_np(out["yvar"]) > 0)
@@ -205,14 +215,14 @@ def test_ou_lm_layer_full_size(kla):
         hp = {n: Pd[n][h:h + 1] for n in Pd}
         ref = oracle.forward_ou(sl["q"], sl["k"], sl["v"], hp["a"], hp["p"], hp["delta"], sl["r"])
         rg = oracle.backward_ou(sl["q"], sl["k"], sl["v"], hp["a"], hp["p"], hp["delta"], sl["r"], None, None,
-                                sl["dy"])
+                                sl["dy"], with_mass=True)
         bi = list(range(w.B))
         _check(f"y[h{h}]", to_np(out["y"][bi, :, h]), K.quantise(ref["y"][:, :, 0], w.dtype), tol, rep)
         _check(f"yvar[h{h}]", to_np(out["yvar"][bi, :, h]), ref["yvar"][:, :, 0], tol, rep)
         for n in ("dq", "dk", "dv", "dr"):
             _check(f"{n}[h{h}]", to_np(gr[n][bi, :, h]), rg[n][:, :, 0], tol, rep)
         for n in ("da", "dp", "ddelta"):
-            _check(f"{n}[h{h}]", to_np(gr[n][h:h + 1]), rg[n], tol, rep)
+            _check_sum(f"{n}[h{h}]", to_np(gr[n][h:h + 1]), rg[n], rg["mass_" + n], tol, rep)
     for n in ("dq", "dk", "dv", "dr", "da", "dp", "ddelta"):
         assert torch.isfinite(gr[n].float()).all(), n
     assert torch.all(out["lamT"] > 0) and torch.all(out["yvar"] > 0)

@@ -31,7 +31,7 @@ def kla():
 
 def _check(name, got, ref, tol, report):
     e = rel_err(got, ref)
-    report.append(f"{name}={e:.2e}(1%floor {rel_err(got, ref, 0.01):.1e})")
+    report.append(f"{name}={e:.2e}(rms-rel {rel_err(got, ref, 1.0):.1e})")
     assert np.all(np.isfinite(got)), f"{name} has non-finite values"
     assert e <= tol, f"{name}: rel err {e:.3e} > {tol:.0e}"
 
