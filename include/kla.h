@@ -22,7 +22,8 @@
  *              r is [B, T, H], yvar is [B, T, H]; beliefs are lam [B, H, dk],
  *              eta = H [B, H, dk, dv].
  *   Memory   : every pointer is a device pointer owned by the caller.  The
- *              library never allocates, frees or synchronises; all work is
+ *              library never allocates, frees or synchronises (KLA_CHECK=1 aside);
+ *              all work is
  *              enqueued asynchronously on `stream` (0 = the null stream).
  *              Inputs are read-only; outputs must not alias inputs (except the
  *              in-place belief of kla_decode_step).  Base pointers must be
@@ -39,8 +40,9 @@
  *              belief is then the initial one and its gradients pass through.
  *   Errors   : return codes only; on any error nothing has been enqueued
  *              (except KLA_ERR_HIP, reported when a launch fails).
- *   Threads  : no global mutable state; calls are thread-safe.  Results are
- *              bitwise reproducible for a given descriptor.
+ *   Threads  : no global mutable state (except the per-GPU workspace of
+ *              kla_backward_noalloc, see there); calls are thread-safe.  Results
+ *              are bitwise reproducible for a given descriptor.
  */
 #ifndef KLA_H
 #define KLA_H
@@ -131,6 +133,30 @@ kla_status kla_backward(const kla_desc* desc,
                         void* dq, void* dk, void* dv, void* dabar, void* dpbar, void* dr,
                         float* dlam0, float* deta0,
                         void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * kla_backward_noalloc -- kla_backward for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid allocation).  Arguments and results are those of kla_backward, minus the
+ * workspace: the library keeps one workspace of KLA_NOALLOC_SCRATCH_BYTES per GPU
+ * for the life of the process (a file-scope device array; nothing is allocated,
+ * freed or synchronised per call).
+ *
+ *   saved: required (T > 0): the context is read, never recomputed here.
+ *   Returns KLA_ERR_WORKSPACE when kla_backward_workspace(desc, 1) exceeds
+ *   KLA_NOALLOC_SCRATCH_BYTES (64 MiB: the LM-layer shape B8 T2048 H16 d128 bf16
+ *   needs 8 MiB, the state-tracking shape B64 T512 H4 d32 fp32 34 MiB).
+ *   Calls that overlap on one GPU share its workspace and race: order them on one
+ *   stream.  With KLA_CHECK=1 the call synchronises, which graph capture forbids.
+ */
+#define KLA_NOALLOC_SCRATCH_BYTES (64u << 20)
+kla_status kla_backward_noalloc(const kla_desc* desc,
+                                const void* q, const void* k, const void* v,
+                                const void* abar, const void* pbar, const void* r,
+                                const float* lam0, const float* eta0, const void* saved,
+                                const void* dy, const float* dyvar, const float* dlamT, const float* detaT,
+                                void* dq, void* dk, void* dv, void* dabar, void* dpbar, void* dr,
+                                float* dlam0, float* deta0, hipStream_t stream);
 
 /*
  * kla_decode_step -- one recurrent token for S independent sequences (the

@@ -17,7 +17,7 @@ from typing import Optional
 
 import torch
 
-__all__ = ["kla_forward", "kla_backward", "kla_decode_step", "kla_status_string",
+__all__ = ["kla_forward", "kla_backward", "kla_backward_noalloc", "kla_decode_step", "kla_status_string",
            "kla_forward_workspace", "kla_backward_workspace", "kla_saved_bytes",
            "kla_forward_ou", "kla_backward_ou", "kla_decode_step_ou", "kla_backward_ou_workspace",
            "kla_forward_pc", "kla_backward_pc", "kla_decode_step_pc",
@@ -66,6 +66,8 @@ def _load():
     lib.kla_forward.restype = ctypes.c_int
     lib.kla_backward.argtypes = [D] + [_VP] * 22 + [ctypes.c_size_t, _VP]
     lib.kla_backward.restype = ctypes.c_int
+    lib.kla_backward_noalloc.argtypes = [D] + [_VP] * 22
+    lib.kla_backward_noalloc.restype = ctypes.c_int
     lib.kla_decode_step.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
     lib.kla_decode_step.restype = ctypes.c_int
     lib.kla_backward_ou_workspace.argtypes = [D, ctypes.c_int]
@@ -224,6 +226,38 @@ def kla_backward(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None, *, sa
                           _stream(dev))
     if st != 0:
         raise KLAError(st, "kla_backward")
+    out["dlam0"] = dlam0
+    out["deta0"] = deta0
+    return out
+
+
+def kla_backward_noalloc(q, k, v, a, p, r, lam0, eta0, dy, dlamT=None, detaT=None, *, saved,
+                         want_init_grads: bool = True, dyvar=None) -> dict:
+    """kla_backward through the library's per-GPU static workspace (the entry point for
+    callers that cannot allocate; only the outputs are allocated here, by torch).  A saved
+    context from kla_forward(save=True) is required."""
+    lib = _load()
+    _check_inputs(q, k, v, a, p, r)
+    dev = q.device
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    lam0 = _f32(lam0, (B, H, dk), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    dlamT = _f32(dlamT, (B, H, dk), dev, "dlamT")
+    detaT = _f32(detaT, (B, H, dk, dv), dev, "detaT")
+    dyvar = _f32(dyvar, (B, T, H), dev, "dyvar")
+    if tuple(dy.shape) != (B, T, H, dv) or dy.dtype != q.dtype or not dy.is_contiguous():
+        raise ValueError("dy must be a contiguous [B, T, H, dv] tensor in the input dtype")
+    desc = _desc(q, v)
+    out = {n: torch.empty_like(x) for n, x in (("dq", q), ("dk", k), ("dv", v), ("da", a), ("dp", p), ("dr", r))}
+    dlam0 = torch.empty((B, H, dk), dtype=torch.float32, device=dev) if want_init_grads else None
+    deta0 = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_init_grads else None
+    st = lib.kla_backward_noalloc(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(r), _p(lam0), _p(eta0),
+                                  _p(saved), _p(dy), _p(dyvar), _p(dlamT), _p(detaT), _p(out["dq"]), _p(out["dk"]),
+                                  _p(out["dv"]), _p(out["da"]), _p(out["dp"]), _p(out["dr"]), _p(dlam0), _p(deta0),
+                                  _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_backward_noalloc")
     out["dlam0"] = dlam0
     out["deta0"] = deta0
     return out
