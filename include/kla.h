@@ -301,6 +301,42 @@ kla_status kla_gate_forward(int64_t n, int32_t dtype, const void* y, const void*
 kla_status kla_gate_backward(int64_t n, int32_t dtype, const void* y, const void* z, const void* dout,
                              void* dy, void* dz, hipStream_t stream);
 
+/*
+ * Monte Carlo readout of KLA+ (the log-marginal-likelihood training loss of the
+ * paper's appendix, eqs. nmll_integral and nmll_logsumexp).  The readout of
+ * channel d is Gaussian under the posterior, with mean ymu = y of kla_forward and
+ * variance yvar (one per token and head, the slots being independent a
+ * posteriori), so S draws are
+ *
+ *   ys[s, b, t, h, d] = ymu[b, t, h, d] + sqrt(yvar[b, t, h]) eps[s, b, t, h, d]
+ *
+ * with eps standard normal, drawn by the counter-based generator Philox4x64-10
+ * (Salmon et al., "Parallel random numbers: as easy as 1, 2, 3", SC 2011) and the
+ * Box-Muller transform: for the flat index e of [S, B, T, H, dv], Philox block
+ * j = e / 8 (counter (j, 0, 0, 0), key (seed, 0)) gives four 64-bit words, i.e. eight
+ * 32-bit halves u_0..u_7 (low half first); each pair gives
+ * r = sqrt(-2 ln(((u_2p >> 8) + 1) 2^-24)), a = (u_2p+1 >> 8) 2^-23 and the normals
+ * eps_2p = r cos(pi a), eps_2p+1 = r sin(pi a); element e takes eps_(e mod 8).  Nothing
+ * is stored between the draws and their backward, which draws eps again.
+ *
+ * The decoder p(o | y) belongs to the model; the loss takes its log-probabilities
+ * of the target tokens, logp [S, n] fp32, and returns per token
+ *   nll[i] = -logsumexp_s(logp[s, i]) + log S        (cross-entropy when S = 1).
+ *
+ *   ymu, dymu [B, T, H, dv] and ys, dys [S, B, T, H, dv]: dtype; yvar, dyvar [B, T, H]
+ *   fp32 (yvar > 0).  dv in {16, 32, 64, 128}.  The backward of the draws returns
+ *   dymu = sum_s dys and dyvar = sum_{s,d} dys eps / (2 sqrt(yvar)); that of the loss
+ *   dlogp[s, i] = -dnll[i] softmax_s(logp[., i]).  Every output is overwritten.
+ */
+kla_status kla_mc_sample(int32_t S, int32_t B, int32_t T, int32_t H, int32_t dv, int32_t dtype, uint64_t seed,
+                         const void* ymu, const float* yvar, void* ys, hipStream_t stream);
+kla_status kla_mc_sample_backward(int32_t S, int32_t B, int32_t T, int32_t H, int32_t dv, int32_t dtype,
+                                  uint64_t seed, const float* yvar, const void* dys, void* dymu, float* dyvar,
+                                  hipStream_t stream);
+kla_status kla_mc_nll(int32_t S, int64_t n, const float* logp, float* nll, hipStream_t stream);
+kla_status kla_mc_nll_backward(int32_t S, int64_t n, const float* logp, const float* dnll, float* dlogp,
+                               hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char* kla_status_string(kla_status status);
 

@@ -23,6 +23,8 @@ __all__ = ["kla_forward", "kla_backward", "kla_backward_noalloc", "kla_decode_st
            "kla_forward_pc", "kla_backward_pc", "kla_decode_step_pc",
            "kla_conv_silu_forward", "kla_conv_silu_backward", "kla_qk_norm_forward", "kla_qk_norm_backward",
            "kla_gate_forward", "kla_gate_backward",
+           "kla_mc_sample", "kla_mc_sample_backward", "kla_mc_nll", "kla_mc_nll_backward", "KLAMCSample",
+           "KLAMCNLL", "kla_mc_nll_loss",
            "KLAError", "KLAFilter", "kla_filter", "KLAFilterOU", "kla_filter_ou", "library_path"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -102,6 +104,13 @@ def _load():
         getattr(lib, fn).restype = ctypes.c_int
     lib.kla_decode_step_pc.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
     lib.kla_decode_step_pc.restype = ctypes.c_int
+    u64 = ctypes.c_uint64
+    lib.kla_mc_sample.argtypes = [i32] * 6 + [u64] + [_VP] * 4
+    lib.kla_mc_sample_backward.argtypes = [i32] * 6 + [u64] + [_VP] * 5
+    lib.kla_mc_nll.argtypes = [i32, i64] + [_VP] * 3
+    lib.kla_mc_nll_backward.argtypes = [i32, i64] + [_VP] * 4
+    for fn in ("kla_mc_sample", "kla_mc_sample_backward", "kla_mc_nll", "kla_mc_nll_backward"):
+        getattr(lib, fn).restype = ctypes.c_int
     lib.kla_status_string.argtypes = [ctypes.c_int]
     lib.kla_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -685,3 +694,110 @@ def kla_gate_backward(y, z, dout):
     if st != 0:
         raise KLAError(st, "kla_gate_backward")
     return dy, dz
+
+
+# ------------------------------------------------------------------ Monte Carlo readout (KLA+)
+def _check_mc(ymu, yvar):
+    if not ymu.is_cuda or ymu.dtype not in _DTYPES or ymu.dim() != 4 or not ymu.is_contiguous():
+        raise ValueError("ymu must be a contiguous [B, T, H, dv] fp32/bf16 GPU tensor")
+    B, T, H, dv = ymu.shape
+    _f32(yvar, (B, T, H), ymu.device, "yvar")
+    return B, T, H, dv
+
+
+def kla_mc_sample(ymu, yvar, S: int, seed: int):
+    """S draws ymu + sqrt(yvar) eps of the posterior readout: [S, B, T, H, dv] in ymu's dtype."""
+    lib = _load()
+    B, T, H, dv = _check_mc(ymu, yvar)
+    ys = torch.empty((S, B, T, H, dv), dtype=ymu.dtype, device=ymu.device)
+    st = lib.kla_mc_sample(S, B, T, H, dv, _DTYPES[ymu.dtype], int(seed) & (2**64 - 1), _p(ymu), _p(yvar), _p(ys),
+                           _stream(ymu.device))
+    if st != 0:
+        raise KLAError(st, "kla_mc_sample")
+    return ys
+
+
+def kla_mc_sample_backward(yvar, dys, seed: int):
+    """(dymu, dyvar) of kla_mc_sample for the gradient dys [S, B, T, H, dv] of the draws."""
+    lib = _load()
+    if not dys.is_cuda or dys.dtype not in _DTYPES or dys.dim() != 5 or not dys.is_contiguous():
+        raise ValueError("dys must be a contiguous [S, B, T, H, dv] fp32/bf16 GPU tensor")
+    S, B, T, H, dv = dys.shape
+    _f32(yvar, (B, T, H), dys.device, "yvar")
+    dymu = torch.empty((B, T, H, dv), dtype=dys.dtype, device=dys.device)
+    dyvar = torch.empty((B, T, H), dtype=torch.float32, device=dys.device)
+    st = lib.kla_mc_sample_backward(S, B, T, H, dv, _DTYPES[dys.dtype], int(seed) & (2**64 - 1), _p(yvar), _p(dys),
+                                    _p(dymu), _p(dyvar), _stream(dys.device))
+    if st != 0:
+        raise KLAError(st, "kla_mc_sample_backward")
+    return dymu, dyvar
+
+
+def kla_mc_nll(logp):
+    """-logsumexp_s(logp[s]) + log S per token, logp [S, n] fp32 (the decoder's log-probabilities of
+    the target tokens under each draw)."""
+    lib = _load()
+    _dense(logp, "logp", torch.float32)
+    S = logp.shape[0]
+    n = logp.numel() // S
+    nll = torch.empty(logp.shape[1:], dtype=torch.float32, device=logp.device)
+    st = lib.kla_mc_nll(S, n, _p(logp), _p(nll), _stream(logp.device))
+    if st != 0:
+        raise KLAError(st, "kla_mc_nll")
+    return nll
+
+
+def kla_mc_nll_backward(logp, dnll):
+    """dlogp = -dnll softmax over the draws, [S, n] fp32."""
+    lib = _load()
+    _dense(logp, "logp", torch.float32)
+    _dense(dnll, "dnll", torch.float32)
+    S = logp.shape[0]
+    n = logp.numel() // S
+    if dnll.numel() != n:
+        raise ValueError("dnll must hold one value per token")
+    dlogp = torch.empty_like(logp)
+    st = lib.kla_mc_nll_backward(S, n, _p(logp), _p(dnll), _p(dlogp), _stream(logp.device))
+    if st != 0:
+        raise KLAError(st, "kla_mc_nll_backward")
+    return dlogp
+
+
+class KLAMCSample(torch.autograd.Function):
+    """Autograd wrapper: ys = draws(ymu, yvar); the seed selects the draws."""
+
+    @staticmethod
+    def forward(ctx, ymu, yvar, S, seed):
+        ymu_c, yvar_c = ymu.contiguous(), yvar.contiguous()
+        ctx.save_for_backward(yvar_c)
+        ctx.seed = seed
+        return kla_mc_sample(ymu_c, yvar_c, S, seed)
+
+    @staticmethod
+    def backward(ctx, dys):
+        (yvar,) = ctx.saved_tensors
+        dymu, dyvar = kla_mc_sample_backward(yvar, dys.contiguous(), ctx.seed)
+        return dymu, dyvar, None, None
+
+
+class KLAMCNLL(torch.autograd.Function):
+    """Autograd wrapper: nll = -logsumexp_s(logp) + log S."""
+
+    @staticmethod
+    def forward(ctx, logp):
+        logp_c = logp.contiguous()
+        ctx.save_for_backward(logp_c)
+        return kla_mc_nll(logp_c)
+
+    @staticmethod
+    def backward(ctx, dnll):
+        (logp,) = ctx.saved_tensors
+        return kla_mc_nll_backward(logp, dnll.contiguous())
+
+
+def kla_mc_nll_loss(ymu, yvar, decoder_logp, S: int = 10, seed: int = 0):
+    """The KLA+ objective per token: draws of the readout, the decoder's log-probability of
+    the targets under each draw (decoder_logp: a function of [S, B, T, H, dv] draws returning
+    [S, ...] fp32 log-probabilities, part of the model), and -logsumexp over the draws + log S."""
+    ys = KLAMCSample.apply(ymu, yvar, S, seed)
+    return KLAMCNLL.apply(decoder_logp(ys))

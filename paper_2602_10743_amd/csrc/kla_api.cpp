@@ -448,6 +448,57 @@ kla_status kla_gate_backward(int64_t n, int32_t dtype, const void* y, const void
                                                                                                       : KLA_ERR_HIP;
 }
 
+// ---------------------------------------------------------------- Monte Carlo readout
+
+namespace {
+kla_status mc_shape(int32_t S, int32_t B, int32_t T, int32_t H, int32_t dv, int32_t dtype) {
+    if (dtype != KLA_F32 && dtype != KLA_BF16) return KLA_ERR_DTYPE;
+    if (S < 1 || B < 1 || T < 0 || H < 1 || !width_ok(dv)) return KLA_ERR_SHAPE;
+    if ((double)S * B * T * H * dv > 9.0e18) return KLA_ERR_SHAPE;
+    return KLA_OK;
+}
+}  // namespace
+
+kla_status kla_mc_sample(int32_t S, int32_t B, int32_t T, int32_t H, int32_t dv, int32_t dtype, uint64_t seed,
+                         const void* ymu, const float* yvar, void* ys, hipStream_t stream) {
+    const kla_status st = mc_shape(S, B, T, H, dv, dtype);
+    if (st != KLA_OK) return st;
+    if (T > 0 && (!ymu || !yvar || !ys)) return KLA_ERR_NULL;
+    if (!all_aligned(ymu, (const void*)yvar, ys)) return KLA_ERR_ALIGN;
+    return kla::launch_mc_sample(S, (size_t)B * T * H, dv, dtype == KLA_BF16, seed, ymu, yvar, ys, stream) ==
+                   hipSuccess
+               ? KLA_OK
+               : KLA_ERR_HIP;
+}
+
+kla_status kla_mc_sample_backward(int32_t S, int32_t B, int32_t T, int32_t H, int32_t dv, int32_t dtype,
+                                  uint64_t seed, const float* yvar, const void* dys, void* dymu, float* dyvar,
+                                  hipStream_t stream) {
+    const kla_status st = mc_shape(S, B, T, H, dv, dtype);
+    if (st != KLA_OK) return st;
+    if (T > 0 && (!yvar || !dys || !dymu || !dyvar)) return KLA_ERR_NULL;
+    if (!all_aligned((const void*)yvar, dys, dymu, (void*)dyvar)) return KLA_ERR_ALIGN;
+    return kla::launch_mc_sample_bwd(S, (size_t)B * T * H, dv, dtype == KLA_BF16, seed, yvar, dys, dymu, dyvar,
+                                     stream) == hipSuccess
+               ? KLA_OK
+               : KLA_ERR_HIP;
+}
+
+kla_status kla_mc_nll(int32_t S, int64_t n, const float* logp, float* nll, hipStream_t stream) {
+    if (S < 1 || n < 0) return KLA_ERR_SHAPE;
+    if (n > 0 && (!logp || !nll)) return KLA_ERR_NULL;
+    if (!all_aligned((const void*)logp, (void*)nll)) return KLA_ERR_ALIGN;
+    return kla::launch_mc_nll(S, (size_t)n, logp, nll, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+kla_status kla_mc_nll_backward(int32_t S, int64_t n, const float* logp, const float* dnll, float* dlogp,
+                               hipStream_t stream) {
+    if (S < 1 || n < 0) return KLA_ERR_SHAPE;
+    if (n > 0 && (!logp || !dnll || !dlogp)) return KLA_ERR_NULL;
+    if (!all_aligned((const void*)logp, (const void*)dnll, (void*)dlogp)) return KLA_ERR_ALIGN;
+    return kla::launch_mc_nll_bwd(S, (size_t)n, logp, dnll, dlogp, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
 const char* kla_status_string(kla_status s) {
     switch (s) {
         case KLA_OK: return "KLA_OK";

@@ -102,6 +102,15 @@ hipError_t launch_gate_fwd(size_t n, bool bf16, const void* y, const void* z, vo
 hipError_t launch_gate_bwd(size_t n, bool bf16, const void* y, const void* z, const void* dout, void* dy, void* dz,
                            hipStream_t st);
 
+// Monte Carlo readout (KLA+): draws y = ymu + sqrt(yvar) eps over nrow = B T H rows of dv
+// channels, their backward, and the logsumexp-over-samples loss and its backward.
+hipError_t launch_mc_sample(int S, size_t nrow, int dv, bool bf16, uint64_t seed, const void* ymu, const float* yvar,
+                            void* ys, hipStream_t st);
+hipError_t launch_mc_sample_bwd(int S, size_t nrow, int dv, bool bf16, uint64_t seed, const float* yvar,
+                                const void* dys, void* dymu, float* dyvar, hipStream_t st);
+hipError_t launch_mc_nll(int S, size_t n, const float* logp, float* nll, hipStream_t st);
+hipError_t launch_mc_nll_bwd(int S, size_t n, const float* logp, const float* dnll, float* dlogp, hipStream_t st);
+
 // OU gates: gradients of the parameters from the per-part gate-gradient sums (fp32
 // parts, or fp64 when part_f64)
 hipError_t launch_ou_param_grads(int H, int dk, int nparts, const void* part, bool part_f64, const float* a,
