@@ -52,13 +52,16 @@ def _load():
     lib.kla_oracle_forward.argtypes = [_I] * 5 + [_D] * 12 + [_I]
     lib.kla_oracle_backward.argtypes = [_I] * 5 + [_D] * 20 + [_I]
     lib.kla_oracle_decode_step.argtypes = [_I] * 4 + [_D] * 10
+    lib.kla_oracle_forward_nd.argtypes = [_I] * 5 + [_D] * 12 + [_I]
+    lib.kla_oracle_backward_nd.argtypes = [_I] * 5 + [_D] * 23 + [_I]
     lib.kla_oracle_trace.argtypes = [_I] * 3 + [_D] * 9
     lib.kla_oracle_mobius_matrix.argtypes = [ctypes.c_double] * 4 + [_D]
     lib.kla_oracle_mobius_compose.argtypes = [_D] * 3
     lib.kla_oracle_mobius_apply.argtypes = [_D, ctypes.c_double]
     lib.kla_oracle_mobius_apply.restype = ctypes.c_double
     lib.kla_oracle_affine_compose.argtypes = [_I] + [_D] * 6
-    for fn in ("kla_oracle_forward", "kla_oracle_backward", "kla_oracle_decode_step",
+    for fn in ("kla_oracle_forward", "kla_oracle_backward", "kla_oracle_decode_step", "kla_oracle_forward_nd",
+               "kla_oracle_backward_nd",
                "kla_oracle_trace", "kla_oracle_mobius_matrix", "kla_oracle_mobius_compose",
                "kla_oracle_affine_compose"):
         getattr(lib, fn).restype = None
@@ -320,3 +323,82 @@ def decode_step_ou(q, k, v, a, p, delta, r, lam, eta) -> dict:
     S = np.shape(k)[0]
     shape = (S,) + abar.shape
     return decode_step(q, k, v, np.broadcast_to(abar, shape), np.broadcast_to(pbar, shape), r, lam, eta)
+
+
+# --------------------------------------------------------------------------------------
+# Gates per (key slot, value channel): Algorithm 1 gives A, P, Delta (and so abar, pbar)
+# the shape (N, D), time-invariant, per head: [H, dk, dv].  With the observation
+# precision per value channel (r [B, T, H, dv]) every element (n, d) of a head is its
+# own scalar filter with its own gates.
+
+def forward_nd(q, k, v, abar, pbar, r, lam0=None, eta0=None, nthreads: Optional[int] = None) -> dict:
+    """The filter with gates abar, pbar [H, dk, dv] (the same for every token); r [B, T, H, dv].
+    Returns y, yvar [B, T, H, dv], lamT, etaT [B, H, dk, dv]."""
+    lib = _load()
+    q, k, v, r, abar, pbar = (_c(x) for x in (q, k, v, r, abar, pbar))
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    lam0 = None if lam0 is None else _c(lam0)
+    eta0 = None if eta0 is None else _c(eta0)
+    y = np.empty((B, T, H, dv))
+    yvar = np.empty((B, T, H, dv))
+    lamT = np.empty((B, H, dk, dv))
+    etaT = np.empty((B, H, dk, dv))
+    lib.kla_oracle_forward_nd(B, T, H, dk, dv, _ptr(q), _ptr(k), _ptr(v), _ptr(abar), _ptr(pbar), _ptr(r),
+                              _ptr(lam0), _ptr(eta0), _ptr(y), _ptr(yvar), _ptr(lamT), _ptr(etaT),
+                              nthreads or default_threads())
+    return {"y": y, "yvar": yvar, "lamT": lamT, "etaT": etaT}
+
+
+def backward_nd(q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT=None, detaT=None, dyvar=None,
+                coef=None, nthreads: Optional[int] = None) -> dict:
+    """Gradient of ``forward_nd``: dq, dk [B, T, H, dk], dv, dr [B, T, H, dv], dlam0, deta0
+    [B, H, dk, dv], and the gate gradients g_abar, g_pbar [H, dk, dv] (sums over (b, t)).
+    ``coef`` = (ca, cp), each [3, H, dk, dv]: also return ``mass`` [3, H, dk, dv], the sums
+    over (b, t) of |ca[j] dabar_t + cp[j] dpbar_t|."""
+    lib = _load()
+    q, k, v, r, abar, pbar, dy = (_c(x) for x in (q, k, v, r, abar, pbar, dy))
+    B, T, H, dk = k.shape
+    dv = v.shape[-1]
+    lam0, eta0, dlamT, detaT, dyvar = (None if x is None else _c(x) for x in (lam0, eta0, dlamT, detaT, dyvar))
+    ca, cp = (np.zeros((3, H, dk, dv)), np.zeros((3, H, dk, dv))) if coef is None else (_c(coef[0]), _c(coef[1]))
+    out = {"dq": np.empty((B, T, H, dk)), "dk": np.empty((B, T, H, dk)), "dv": np.empty((B, T, H, dv)),
+           "dr": np.empty((B, T, H, dv)), "dlam0": np.empty((B, H, dk, dv)), "deta0": np.empty((B, H, dk, dv))}
+    ga = np.empty((B, H, dk, dv))
+    gp = np.empty((B, H, dk, dv))
+    mass = np.empty((3, B, H, dk, dv))
+    lib.kla_oracle_backward_nd(B, T, H, dk, dv, _ptr(q), _ptr(k), _ptr(v), _ptr(abar), _ptr(pbar), _ptr(r),
+                               _ptr(lam0), _ptr(eta0), _ptr(dy), _ptr(dyvar), _ptr(dlamT), _ptr(detaT),
+                               _ptr(out["dq"]), _ptr(out["dk"]), _ptr(out["dv"]), _ptr(out["dr"]),
+                               _ptr(out["dlam0"]), _ptr(out["deta0"]), _ptr(ca), _ptr(cp), _ptr(ga), _ptr(gp),
+                               _ptr(mass), nthreads or default_threads())
+    out["g_abar"] = ga.sum(axis=0)
+    out["g_pbar"] = gp.sum(axis=0)
+    if coef is not None:
+        out["mass"] = mass.sum(axis=1)
+    return out
+
+
+def forward_ou_nd(q, k, v, a, p, delta, r, lam0=None, eta0=None, nthreads: Optional[int] = None) -> dict:
+    """``forward_nd`` with the gates of OU parameters a, p, delta [H, dk, dv]."""
+    abar, pbar = ou_discretise(a, p, delta)
+    return forward_nd(q, k, v, abar, pbar, r, lam0, eta0, nthreads=nthreads)
+
+
+def backward_ou_nd(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=None, dyvar=None,
+                   nthreads: Optional[int] = None) -> dict:
+    """Gradient of ``forward_ou_nd``: as ``backward_nd`` for the per-token tensors and the
+    initial belief, and da, dp, ddelta [H, dk, dv] with the masses mass_da, mass_dp,
+    mass_ddelta of their terms (sums over (b, t) of the absolute per-token terms)."""
+    a, p, delta = (_c(x) for x in (a, p, delta))
+    abar, pbar = ou_discretise(a, p, delta)
+    one, zero = np.ones_like(a), np.zeros_like(a)
+    ca = np.stack(ou_discretise_vjp(a, p, delta, one, zero))    # d(da, dp, ddelta) / d g_abar
+    cp = np.stack(ou_discretise_vjp(a, p, delta, zero, one))    # ... / d g_pbar
+    out = backward_nd(q, k, v, abar, pbar, r, lam0, eta0, dy, dlamT, detaT, dyvar, coef=(ca, cp),
+                      nthreads=nthreads)
+    ga, gp = out.pop("g_abar"), out.pop("g_pbar")
+    out["da"], out["dp"], out["ddelta"] = ou_discretise_vjp(a, p, delta, ga, gp)
+    m = out.pop("mass")
+    out["mass_da"], out["mass_dp"], out["mass_ddelta"] = m[0], m[1], m[2]
+    return out

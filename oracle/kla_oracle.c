@@ -41,6 +41,15 @@
  * Layouts (all row-major, contiguous, double):
  *   q, k, a, p  [B, T, H, dk]       v, Lv, y, yvar, dy   [B, T, H, dv]
  *   lam0, eta0, lamT, etaT, dlamT, detaT, dlam0, deta0    [B, H, dk, dv]
+ *
+ * Gates per (n, d) (the *_nd entry points): Algorithm 1 gives the decay and the
+ * process noise the shape (N, D), time-invariant: abar[n,d], pbar[n,d] per head,
+ * [H, dk, dv].  The recursion is the same with abar_t[n] -> abar[h,n,d]; the
+ * gate gradients are then sums over (b, t), returned per (b, h) (summed over t)
+ * together with the sum over t of the absolute values of up to three linear
+ * combinations c_a dabar_t + c_p dpbar_t of the per-token terms (the caller's
+ * coefficients, [3][H, dk, dv]): the scale against which the rounding of such
+ * sums is measured.
  */
 #include <math.h>
 #include <pthread.h>
@@ -56,6 +65,11 @@ typedef struct {
     /* backward only */
     const double *dy, *dyvar, *dlamT, *detaT;
     double *dq, *dk_, *dv_, *da, *dp, *dr, *dlam0, *deta0;
+    /* gates per (n, d): abar, pbar [H, dk, dv]; sums over t of the gate gradients and of
+       |ca[j] dabar_t + cp[j] dpbar_t|, per (b, h): ga, gp [B, H, dk, dv], mass [3][B, H, dk, dv] */
+    int gate_nd;
+    const double *ca, *cp;
+    double *ga, *gp, *mass;
     /* work distribution */
     int next;                 /* next (b,h) pair to take */
     pthread_mutex_t lock;
@@ -66,6 +80,12 @@ static size_t tok(const job_t* J, int b, int t, int h, int width) {
 }
 static size_t bel(const job_t* J, int b, int h) {
     return ((size_t)b * J->H + h) * (size_t)J->dk * J->dv;
+}
+
+/* index of the gate of (b, t, h, n, d) */
+static size_t gate(const job_t* J, int b, int t, int h, int n, int d) {
+    if (J->gate_nd) return ((size_t)h * J->dk + n) * J->dv + d;
+    return tok(J, b, t, h, J->dk) + n;
 }
 
 static int take(job_t* J) {
@@ -87,8 +107,8 @@ static void forward_pair(const job_t* J, int b, int h, double* lam, double* eta)
     for (int t = 0; t < J->T; ++t) {
         const double* qt = J->q + tok(J, b, t, h, dk);
         const double* kt = J->k + tok(J, b, t, h, dk);
-        const double* at = J->a + tok(J, b, t, h, dk);
-        const double* pt = J->p + tok(J, b, t, h, dk);
+        const double* at = J->gate_nd ? NULL : J->a + tok(J, b, t, h, dk);
+        const double* pt = J->gate_nd ? NULL : J->p + tok(J, b, t, h, dk);
         const double* vt = J->v + tok(J, b, t, h, dv);
         const double* rt = J->r + tok(J, b, t, h, dv);
         double* yt = J->y ? J->y + tok(J, b, t, h, dv) : NULL;
@@ -101,9 +121,11 @@ static void forward_pair(const job_t* J, int b, int h, double* lam, double* eta)
             for (int d = 0; d < dv; ++d) {
                 double* L = &lam[n * dv + d];
                 double* E = &eta[n * dv + d];
+                const size_t ig = gate(J, b, t, h, n, d);
+                const double an = J->gate_nd ? J->a[ig] : at[n], pn = J->gate_nd ? J->p[ig] : pt[n];
                 /* predict + update, Theorem 1 (gate view) and Theorem 2 */
-                double rho = 1.0 / (at[n] * at[n] + pt[n] * (*L));
-                double f = at[n] * rho;
+                double rho = 1.0 / (an * an + pn * (*L));
+                double f = an * rho;
                 *L = rho * (*L) + kt[n] * kt[n] * rt[d];
                 *E = f * (*E) + kt[n] * rt[d] * vt[d];
                 /* readout of the posterior mean (and variance) with the query */
@@ -138,17 +160,18 @@ static void backward_filter(const job_t* J, int b, int h, int n, int d, double* 
     lt[0] = J->lam0 ? J->lam0[s0] : 1.0;
     et[0] = J->eta0 ? J->eta0[s0] : 0.0;
     for (int t = 0; t < T; ++t) {
-        size_t ik = tok(J, b, t, h, dk) + n, iv = tok(J, b, t, h, dv) + d;
-        double a = J->a[ik], p = J->p[ik], k = J->k[ik], r = J->r[iv], v = J->v[iv];
+        size_t ik = tok(J, b, t, h, dk) + n, iv = tok(J, b, t, h, dv) + d, ig = gate(J, b, t, h, n, d);
+        double a = J->a[ig], p = J->p[ig], k = J->k[ik], r = J->r[iv], v = J->v[iv];
         double rho = 1.0 / (a * a + p * lt[t]);
         lt[t + 1] = rho * lt[t] + k * k * r;
         et[t + 1] = a * rho * et[t] + k * r * v;
     }
     double gl = J->dlamT ? J->dlamT[s0] : 0.0;   /* adjoint of lam_t */
     double ge = J->detaT ? J->detaT[s0] : 0.0;   /* adjoint of eta_t */
+    double sa = 0.0, sp = 0.0, sm[3] = {0.0, 0.0, 0.0};   /* gates per (n, d): sums over t */
     for (int t = T - 1; t >= 0; --t) {
-        size_t ik = tok(J, b, t, h, dk) + n, iv = tok(J, b, t, h, dv) + d;
-        double a = J->a[ik], p = J->p[ik], k = J->k[ik], q = J->q[ik];
+        size_t ik = tok(J, b, t, h, dk) + n, iv = tok(J, b, t, h, dv) + d, ig = gate(J, b, t, h, n, d);
+        double a = J->a[ig], p = J->p[ig], k = J->k[ik], q = J->q[ik];
         double r = J->r[iv], v = J->v[iv], g = J->dy[iv];
         double lp = lt[t], ep = et[t], lc = lt[t + 1], ec = et[t + 1];
         /* readout y_t[d] += q * eta / lam */
@@ -170,7 +193,7 @@ static void backward_filter(const job_t* J, int b, int h, int n, int d, double* 
         J->dr[iv] += ge * k * v;
         J->dv_[iv] += ge * k * r;
         double ge_prev = f * ge;
-        J->da[ik] += df * rho;
+        double dat = df * rho;   /* this token's gradients of abar and pbar */
         double drho = df * a;
         /* lam_t = rho * lam_{t-1} + k^2 r */
         drho += gl * lp;
@@ -179,14 +202,29 @@ static void backward_filter(const job_t* J, int b, int h, int n, int d, double* 
         J->dr[iv] += gl * k * k;
         /* rho = 1 / (a^2 + p lam_{t-1}) */
         double dden = -drho * rho * rho;
-        J->da[ik] += dden * 2.0 * a;
-        J->dp[ik] += dden * lp;
+        dat += dden * 2.0 * a;
+        double dpt = dden * lp;
+        if (J->gate_nd) {
+            sa += dat;
+            sp += dpt;
+            for (int j = 0; j < 3; ++j) sm[j] += fabs(J->ca[j * (size_t)J->H * dk * dv + ig] * dat +
+                                                      J->cp[j * (size_t)J->H * dk * dv + ig] * dpt);
+        } else {
+            J->da[ik] += dat;
+            J->dp[ik] += dpt;
+        }
         gl_prev += dden * p;
         gl = gl_prev;
         ge = ge_prev;
     }
     if (J->dlam0) J->dlam0[s0] = gl;
     if (J->deta0) J->deta0[s0] = ge;
+    if (J->gate_nd) {
+        const size_t nb = (size_t)J->B * J->H * dk * dv;
+        J->ga[s0] = sa;
+        J->gp[s0] = sp;
+        for (int j = 0; j < 3; ++j) J->mass[j * nb + s0] = sm[j];
+    }
 }
 
 static void* backward_worker(void* arg) {
@@ -252,6 +290,47 @@ void kla_oracle_backward(int B, int T, int H, int dk, int dv,
     memset(dk_, 0, sizeof(double) * nk);
     memset(da, 0, sizeof(double) * nk);
     memset(dp, 0, sizeof(double) * nk);
+    memset(dv_, 0, sizeof(double) * nv);
+    memset(dr, 0, sizeof(double) * nv);
+    run(&J, backward_worker, nthreads);
+}
+
+/* The forward with gates per (n, d): a, p [H, dk, dv], time-invariant. */
+void kla_oracle_forward_nd(int B, int T, int H, int dk, int dv,
+                           const double* q, const double* k, const double* v,
+                           const double* a, const double* p, const double* r,
+                           const double* lam0, const double* eta0,
+                           double* y, double* yvar, double* lamT, double* etaT, int nthreads) {
+    job_t J;
+    memset(&J, 0, sizeof J);
+    J.B = B; J.T = T; J.H = H; J.dk = dk; J.dv = dv; J.gate_nd = 1;
+    J.q = q; J.k = k; J.v = v; J.a = a; J.p = p; J.r = r;
+    J.lam0 = lam0; J.eta0 = eta0; J.y = y; J.yvar = yvar; J.lamT = lamT; J.etaT = etaT;
+    run(&J, forward_worker, nthreads);
+}
+
+/* The backward with gates per (n, d): dq, dk, dv, dr, dlam0, deta0 as in
+ * kla_oracle_backward; ga, gp [B, H, dk, dv] receive the sums over t of the gradients
+ * of abar and pbar, mass [3][B, H, dk, dv] the sums over t of
+ * |ca[j] dabar_t + cp[j] dpbar_t| (ca, cp [3][H, dk, dv]). */
+void kla_oracle_backward_nd(int B, int T, int H, int dk, int dv,
+                            const double* q, const double* k, const double* v,
+                            const double* a, const double* p, const double* r,
+                            const double* lam0, const double* eta0,
+                            const double* dy, const double* dyvar, const double* dlamT, const double* detaT,
+                            double* dq, double* dk_, double* dv_, double* dr, double* dlam0, double* deta0,
+                            const double* ca, const double* cp, double* ga, double* gp, double* mass,
+                            int nthreads) {
+    job_t J;
+    memset(&J, 0, sizeof J);
+    J.B = B; J.T = T; J.H = H; J.dk = dk; J.dv = dv; J.gate_nd = 1;
+    J.q = q; J.k = k; J.v = v; J.a = a; J.p = p; J.r = r;
+    J.lam0 = lam0; J.eta0 = eta0; J.dy = dy; J.dyvar = dyvar; J.dlamT = dlamT; J.detaT = detaT;
+    J.dq = dq; J.dk_ = dk_; J.dv_ = dv_; J.dr = dr; J.dlam0 = dlam0; J.deta0 = deta0;
+    J.ca = ca; J.cp = cp; J.ga = ga; J.gp = gp; J.mass = mass;
+    size_t nk = (size_t)B * T * H * dk, nv = (size_t)B * T * H * dv;
+    memset(dq, 0, sizeof(double) * nk);
+    memset(dk_, 0, sizeof(double) * nk);
     memset(dv_, 0, sizeof(double) * nv);
     memset(dr, 0, sizeof(double) * nv);
     run(&J, backward_worker, nthreads);

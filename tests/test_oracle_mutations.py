@@ -18,18 +18,24 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "kla_oracle.c")
 
 MUTATIONS = {
-    "drop_process_noise": ("1.0 / (at[n] * at[n] + pt[n] * (*L));", "1.0 / (at[n] * at[n] + 0.0 * (*L));"),
-    "forget_gate_without_decay": ("double f = at[n] * rho;", "double f = rho;"),
+    "drop_process_noise": ("1.0 / (an * an + pn * (*L));", "1.0 / (an * an + 0.0 * (*L));"),
+    "forget_gate_without_decay": ("double f = an * rho;", "double f = rho;"),
     "precision_wrong_channel": ("*L = rho * (*L) + kt[n] * kt[n] * rt[d];", "*L = rho * (*L) + kt[n] * kt[n] * rt[0];"),
     "evidence_missing_key": ("*E = f * (*E) + kt[n] * rt[d] * vt[d];", "*E = f * (*E) + rt[d] * vt[d];"),
     "readout_without_precision": ("yt[d] += qt[n] * (*E) * inv;", "yt[d] += qt[n] * (*E);"),
     "variance_query_not_squared": ("wt[d] += qt[n] * qt[n] * inv;", "wt[d] += qt[n] * inv;"),
     "bwd_mean_adjoint_sign": ("gl -= dmu * ec / (lc * lc);", "gl += dmu * ec / (lc * lc);"),
-    "bwd_noise_grad_wrong_index": ("J->dp[ik] += dden * lp;", "J->dp[ik] += dden * lc;"),
+    "bwd_noise_grad_wrong_index": ("double dpt = dden * lp;", "double dpt = dden * lc;"),
     "bwd_key_grad_missing_factor": ("J->dk_[ik] += gl * 2.0 * k * r;", "J->dk_[ik] += gl * k * r;"),
     "bwd_gate_adjoint_dropped": ("gl_prev += dden * p;", "gl_prev += 0.0;"),
     "bwd_variance_query_factor": ("J->dq[ik] += 2.0 * q * gv / lc;", "J->dq[ik] += q * gv / lc;"),
     "bwd_variance_precision_power": ("gl -= q * q * gv / (lc * lc);", "gl -= q * q * gv / lc;"),
+    # gates per (key slot, value channel)
+    "nd_gate_transposed": ("if (J->gate_nd) return ((size_t)h * J->dk + n) * J->dv + d;",
+                           "if (J->gate_nd) return ((size_t)h * J->dv + d) * J->dk + n;"),
+    "nd_gate_of_slot_only": ("if (J->gate_nd) return ((size_t)h * J->dk + n) * J->dv + d;",
+                             "if (J->gate_nd) return ((size_t)h * J->dk + n) * J->dv;"),
+    "nd_gate_grad_sum_dropped": ("            sa += dat;\n", "            sa += 0.0 * dat;\n"),
 }
 
 
@@ -115,12 +121,47 @@ def _fd_battery(orc) -> bool:
     return bool(ok)
 
 
+def _nd_battery(orc) -> bool:
+    """Gates per (n, d): the textbook covariance-form filter per element, and central
+    differences of the gate gradients."""
+    g = np.random.default_rng(2)
+    B, T, H, dk, dv = 1, 7, 1, 3, 2
+    q, k = g.standard_normal((2, B, T, H, dk))
+    v = g.standard_normal((B, T, H, dv))
+    r = 0.2 + g.random((B, T, H, dv))
+    a = 0.3 + 0.6 * g.random((H, dk, dv))
+    p = 0.05 + g.random((H, dk, dv))
+    out = orc.forward_nd(q, k, v, a, p, r)
+    Sig, mu, ok = np.ones((dk, dv)), np.zeros((dk, dv)), True
+    for t in range(T):
+        kt = k[0, t, 0][:, None]
+        mp = a[0] * mu
+        Sp = a[0] ** 2 * Sig + p[0]
+        K = Sp * kt / (kt * kt * Sp + 1.0 / r[0, t, 0][None, :])
+        mu = mp + K * (v[0, t, 0][None, :] - kt * mp)
+        Sig = (1.0 - K * kt) * Sp
+        ok &= np.allclose(out["y"][0, t, 0], (q[0, t, 0][:, None] * mu).sum(0), rtol=1e-9, atol=1e-12)
+    dy = g.standard_normal((B, T, H, dv))
+    gr = orc.backward_nd(q, k, v, a, p, r, None, None, dy)
+    loss = lambda aa, pp: float((orc.forward_nd(q, k, v, aa, pp, r)["y"] * dy).sum())
+    for x, gname in ((a, "g_abar"), (p, "g_pbar")):
+        for idx in np.ndindex(x.shape):
+            old = x[idx]
+            x[idx] = old + 1e-6
+            lp = loss(a, p)
+            x[idx] = old - 1e-6
+            lm = loss(a, p)
+            x[idx] = old
+            ok &= abs((lp - lm) / 2e-6 - gr[gname][idx]) < 1e-5 * max(1.0, abs(gr[gname][idx]))
+    return bool(ok)
+
+
 def test_unmutated_copy_passes_battery(tmp_path):
     import oracle
-    assert _kf_battery(oracle) and _fd_battery(oracle)
+    assert _kf_battery(oracle) and _fd_battery(oracle) and _nd_battery(oracle)
 
 
 @pytest.mark.parametrize("name", sorted(MUTATIONS))
 def test_planted_mistake_is_caught(tmp_path, name):
     orc = _load_mutant(tmp_path, name)
-    assert not (_kf_battery(orc) and _fd_battery(orc)), f"mutation {name} went unnoticed"
+    assert not (_kf_battery(orc) and _fd_battery(orc) and _nd_battery(orc)), f"mutation {name} went unnoticed"
