@@ -265,6 +265,45 @@ kla_status kla_decode_step_pc(int32_t S, int32_t H, int32_t dk, int32_t dv, int3
                               float* lam, float* eta, void* y, float* yvar, hipStream_t stream);
 
 /*
+ * Gates per (key slot, value channel): Algorithm 1 as written, with the decay and
+ * process noise of shape (N, D) per head, time-invariant, from OU parameters
+ * A, P, Delta : (N, D) by the exact discretisation (Sec. 4.1, eq. discretisation),
+ * together with the per-channel observation precision above:
+ *
+ *   abar[h,n,d] = exp(-a delta),  pbar[h,n,d] = p^2 (1 - exp(-2 a delta)) / (2 a)
+ *   rho_t[n,d] = 1 / (abar[n,d]^2 + pbar[n,d] lam_{t-1}[n,d]),  lam_t = rho_t lam_{t-1} + k^2 r_t[d]
+ *   H_t[n,d]   = abar[n,d] rho_t[n,d] H_{t-1}[n,d] + k_t[n] r_t[d] v_t[d],  readouts as above
+ *
+ * a, p, delta, da, dp, ddelta are [H, dk, dv] fp32 (formed in the arithmetic type
+ * of the per-channel kernels: fp64 for fp32 inputs, fp32 for bf16); every other
+ * argument is as in the per-channel entry point of the same name.  The parameter
+ * gradients are the per-token gate gradients summed over (b, t) and taken through
+ * the discretisation in fp64.  Domain under KLA_CHECK=1: a > 0, delta > 0, p finite.
+ */
+size_t kla_backward_pc_ou_workspace(const kla_desc* desc, int with_saved);
+
+kla_status kla_forward_pc_ou(const kla_desc* desc,
+                             const void* q, const void* k, const void* v,
+                             const float* a, const float* p, const float* delta, const void* r,
+                             const float* lam0, const float* eta0,
+                             void* y, float* yvar, float* lamT, float* etaT,
+                             void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
+
+kla_status kla_backward_pc_ou(const kla_desc* desc,
+                              const void* q, const void* k, const void* v,
+                              const float* a, const float* p, const float* delta, const void* r,
+                              const float* lam0, const float* eta0, const void* saved,
+                              const void* dy, const float* dyvar, const float* dlamT, const float* detaT,
+                              void* dq, void* dk, void* dv, float* da, float* dp, float* ddelta, void* dr,
+                              float* dlam0, float* deta0,
+                              void* ws, size_t ws_bytes, hipStream_t stream);
+
+kla_status kla_decode_step_pc_ou(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype,
+                                 const void* q, const void* k, const void* v,
+                                 const float* a, const float* p, const float* delta, const void* r,
+                                 float* lam, float* eta, void* y, float* yvar, hipStream_t stream);
+
+/*
  * Block scaffolding around the layer (the Mamba-style block of Sec. 4.4 and
  * Appendix A): a causal depthwise 1D convolution of kernel size 4 fused with
  * SiLU, QK-norm, and the SiLU output gate.  The paper fixes no details beyond

@@ -264,22 +264,24 @@ def decode_inputs(w: Workload, seed: Optional[int] = None, as_bits: bool = False
 OU_TENSOR_ID = {"a": 7, "p": 8, "delta": 9}
 
 
-def ou_params(H: int, dk: int, seed: int = 0) -> dict:
-    """Time-invariant OU parameters [H, dk] as float32 (the storage form; the
-    oracle widens them): step size delta log-uniform on [1e-3, 1e-1], mean
-    reversion a uniform on [1, 16], diffusion scale p = softplus(N(2, 1)).  The
-    resulting decays exp(-a delta) span about (0.2, 0.999), centred near 0.92."""
+def ou_params(H: int, dk: int, seed: int = 0, dv: Optional[int] = None) -> dict:
+    """Time-invariant OU parameters [H, dk] (or [H, dk, dv] when dv is given: one per
+    key slot and value channel) as float32 (the storage form; the oracle widens
+    them): step size delta log-uniform on [1e-3, 1e-1], mean reversion a uniform on
+    [1, 16], diffusion scale p = softplus(N(2, 1)).  The resulting decays
+    exp(-a delta) span about (0.2, 0.999), centred near 0.92."""
     out = {}
+    shape = (dk,) if dv is None else (dk, dv)
     for name, tid in OU_TENSOR_ID.items():
         rows = []
         for h in range(H):
-            g = _rng(seed, tid, 0, h)
+            g = _rng(seed, tid + (0 if dv is None else 10), 0, h)
             if name == "delta":
-                x = np.exp(g.uniform(np.log(1e-3), np.log(1e-1), dk))
+                x = np.exp(g.uniform(np.log(1e-3), np.log(1e-1), shape))
             elif name == "a":
-                x = g.uniform(1.0, 16.0, dk)
+                x = g.uniform(1.0, 16.0, shape)
             else:
-                x = softplus(g.standard_normal(dk) + 2.0)
+                x = softplus(g.standard_normal(shape) + 2.0)
             rows.append(x)
         out[name] = to_f32(np.stack(rows))
     return out

@@ -21,6 +21,7 @@ __all__ = ["kla_forward", "kla_backward", "kla_backward_noalloc", "kla_decode_st
            "kla_forward_workspace", "kla_backward_workspace", "kla_saved_bytes",
            "kla_forward_ou", "kla_backward_ou", "kla_decode_step_ou", "kla_backward_ou_workspace",
            "kla_forward_pc", "kla_backward_pc", "kla_decode_step_pc",
+           "kla_forward_pc_ou", "kla_backward_pc_ou", "kla_decode_step_pc_ou", "KLAFilterPcOU", "kla_filter_pc_ou",
            "kla_conv_silu_forward", "kla_conv_silu_backward", "kla_qk_norm_forward", "kla_qk_norm_backward",
            "kla_gate_forward", "kla_gate_backward",
            "kla_mc_sample", "kla_mc_sample_backward", "kla_mc_nll", "kla_mc_nll_backward", "KLAMCSample",
@@ -102,6 +103,14 @@ def _load():
     for fn in ("kla_conv_silu_forward", "kla_conv_silu_backward", "kla_qk_norm_forward", "kla_qk_norm_backward",
                "kla_gate_forward", "kla_gate_backward"):
         getattr(lib, fn).restype = ctypes.c_int
+    lib.kla_backward_pc_ou_workspace.argtypes = [D, ctypes.c_int]
+    lib.kla_backward_pc_ou_workspace.restype = ctypes.c_size_t
+    lib.kla_forward_pc_ou.argtypes = [D] + [_VP] * 15 + [ctypes.c_size_t, _VP]
+    lib.kla_forward_pc_ou.restype = ctypes.c_int
+    lib.kla_backward_pc_ou.argtypes = [D] + [_VP] * 24 + [ctypes.c_size_t, _VP]
+    lib.kla_backward_pc_ou.restype = ctypes.c_int
+    lib.kla_decode_step_pc_ou.argtypes = [ctypes.c_int32] * 5 + [_VP] * 12
+    lib.kla_decode_step_pc_ou.restype = ctypes.c_int
     lib.kla_decode_step_pc.argtypes = [ctypes.c_int32] * 5 + [_VP] * 11
     lib.kla_decode_step_pc.restype = ctypes.c_int
     u64 = ctypes.c_uint64
@@ -801,3 +810,127 @@ def kla_mc_nll_loss(ymu, yvar, decoder_logp, S: int = 10, seed: int = 0):
     [S, ...] fp32 log-probabilities, part of the model), and -logsumexp over the draws + log S."""
     ys = KLAMCSample.apply(ymu, yvar, S, seed)
     return KLAMCNLL.apply(decoder_logp(ys))
+
+
+# ------------------------------------------------------------------ gates per (key slot, value channel)
+def _check_pc_ou(q, k, v, r, a, p, delta):
+    if not q.is_cuda or q.dtype not in _DTYPES:
+        raise ValueError("inputs must be fp32/bf16 GPU tensors")
+    B, T, H, dk = q.shape
+    dv = v.shape[-1]
+    for name, t, shape in (("k", k, (B, T, H, dk)), ("v", v, (B, T, H, dv)), ("r", r, (B, T, H, dv))):
+        if tuple(t.shape) != shape or t.dtype != q.dtype or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {shape} tensor in q's dtype")
+    if not q.is_contiguous():
+        raise ValueError("q must be contiguous")
+    for name, t in (("a", a), ("p", p), ("delta", delta)):
+        _f32(t, (H, dk, dv), q.device, name)
+    return B, T, H, dk, dv
+
+
+def kla_forward_pc_ou(q, k, v, a, p, delta, r, lam0=None, eta0=None, *, want_var: bool = False,
+                      want_state: bool = True, save: bool = False) -> dict:
+    """Filter with gates per (key slot, value channel) from OU parameters a, p, delta
+    [H, dk, dv] fp32 and one observation precision per value channel r [B, T, H, dv]
+    (Algorithm 1's shapes).  Returns as kla_forward_pc."""
+    lib = _load()
+    B, T, H, dk, dv = _check_pc_ou(q, k, v, r, a, p, delta)
+    dev = q.device
+    lam0 = _f32(lam0, (B, H, dk, dv), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    desc = _desc(q, v)
+    y = torch.empty((B, T, H, dv), dtype=q.dtype, device=dev)
+    yvar = torch.empty((B, T, H, dv), dtype=torch.float32, device=dev) if want_var else None
+    lamT = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_state else None
+    etaT = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_state else None
+    nsaved = int(lib.kla_saved_pc_bytes(ctypes.byref(desc))) if save else 0
+    saved = torch.empty(max(nsaved, 1), dtype=torch.uint8, device=dev) if save else None
+    nws = kla_forward_workspace(desc)
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    st = lib.kla_forward_pc_ou(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(delta), _p(r), _p(lam0),
+                               _p(eta0), _p(y), _p(yvar), _p(lamT), _p(etaT), _p(saved if nsaved else None), _p(ws),
+                               nws, _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_forward_pc_ou")
+    return {"y": y, "yvar": yvar, "lamT": lamT, "etaT": etaT, "saved": saved if nsaved else None}
+
+
+def kla_backward_pc_ou(q, k, v, a, p, delta, r, lam0, eta0, dy, dlamT=None, detaT=None, *, saved=None,
+                       want_init_grads: bool = True, dyvar=None) -> dict:
+    """Gradients of kla_forward_pc_ou: dq, dk [B, T, H, dk] and dv, dr [B, T, H, dv] in the
+    input dtype; da, dp, ddelta [H, dk, dv] fp32; dlam0, deta0 [B, H, dk, dv] when asked."""
+    lib = _load()
+    B, T, H, dk, dv = _check_pc_ou(q, k, v, r, a, p, delta)
+    dev = q.device
+    lam0 = _f32(lam0, (B, H, dk, dv), dev, "lam0")
+    eta0 = _f32(eta0, (B, H, dk, dv), dev, "eta0")
+    dlamT = _f32(dlamT, (B, H, dk, dv), dev, "dlamT")
+    detaT = _f32(detaT, (B, H, dk, dv), dev, "detaT")
+    dyvar = _f32(dyvar, (B, T, H, dv), dev, "dyvar")
+    if tuple(dy.shape) != (B, T, H, dv) or dy.dtype != q.dtype or not dy.is_contiguous():
+        raise ValueError("dy must be a contiguous [B, T, H, dv] tensor in the input dtype")
+    desc = _desc(q, v)
+    out = {n: torch.empty_like(x) for n, x in (("dq", q), ("dk", k), ("dv", v), ("dr", r))}
+    for n in ("da", "dp", "ddelta"):
+        out[n] = torch.empty((H, dk, dv), dtype=torch.float32, device=dev)
+    dlam0 = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_init_grads else None
+    deta0 = torch.empty((B, H, dk, dv), dtype=torch.float32, device=dev) if want_init_grads else None
+    nws = int(lib.kla_backward_pc_ou_workspace(ctypes.byref(desc), int(saved is not None)))
+    ws = torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    st = lib.kla_backward_pc_ou(ctypes.byref(desc), _p(q), _p(k), _p(v), _p(a), _p(p), _p(delta), _p(r), _p(lam0),
+                                _p(eta0), _p(saved), _p(dy), _p(dyvar), _p(dlamT), _p(detaT), _p(out["dq"]),
+                                _p(out["dk"]), _p(out["dv"]), _p(out["da"]), _p(out["dp"]), _p(out["ddelta"]),
+                                _p(out["dr"]), _p(dlam0), _p(deta0), _p(ws), nws, _stream(dev))
+    if st != 0:
+        raise KLAError(st, "kla_backward_pc_ou")
+    out["dlam0"] = dlam0
+    out["deta0"] = deta0
+    return out
+
+
+def kla_decode_step_pc_ou(q, k, v, a, p, delta, r, lam, eta, *, want_var: bool = False, y=None) -> dict:
+    """One token for S sequences with gates per (key slot, value channel): q, k [S, H, dk];
+    v, r [S, H, dv]; a, p, delta [H, dk, dv]; lam, eta [S, H, dk, dv] fp32 updated in place."""
+    lib = _load()
+    S, H, dk = q.shape
+    dv = v.shape[-1]
+    for name, t, shape in (("k", k, (S, H, dk)), ("v", v, (S, H, dv)), ("r", r, (S, H, dv))):
+        if tuple(t.shape) != shape or t.dtype != q.dtype or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {shape} tensor in q's dtype")
+    for name, t in (("a", a), ("p", p), ("delta", delta)):
+        _f32(t, (H, dk, dv), q.device, name)
+    _f32(lam, (S, H, dk, dv), q.device, "lam")
+    _f32(eta, (S, H, dk, dv), q.device, "eta")
+    if y is None:
+        y = torch.empty((S, H, dv), dtype=q.dtype, device=q.device)
+    yvar = torch.empty((S, H, dv), dtype=torch.float32, device=q.device) if want_var else None
+    st = lib.kla_decode_step_pc_ou(S, H, dk, dv, _DTYPES[q.dtype], _p(q), _p(k), _p(v), _p(a), _p(p), _p(delta),
+                                   _p(r), _p(lam), _p(eta), _p(y), _p(yvar), _stream(q.device))
+    if st != 0:
+        raise KLAError(st, "kla_decode_step_pc_ou")
+    return {"y": y, "yvar": yvar, "lam": lam, "eta": eta}
+
+
+class KLAFilterPcOU(torch.autograd.Function):
+    """Autograd wrapper: y, lamT, etaT = filter(q, k, v, a, p, delta, r) with gates per
+    (key slot, value channel) from OU parameters [H, dk, dv]."""
+
+    @staticmethod
+    def forward(ctx, q, k, v, a, p, delta, r):
+        out = kla_forward_pc_ou(q, k, v, a, p, delta, r, save=True)
+        ctx.save_for_backward(q, k, v, a, p, delta, r, out["saved"])
+        return out["y"], out["lamT"], out["etaT"]
+
+    @staticmethod
+    def backward(ctx, dy, dlamT, detaT):
+        q, k, v, a, p, delta, r, saved = ctx.saved_tensors
+        c = lambda t: None if t is None else t.contiguous()
+        dy = torch.zeros_like(q[..., :1].expand(*q.shape[:3], v.shape[-1])).contiguous() if dy is None \
+            else dy.contiguous()
+        g = kla_backward_pc_ou(q, k, v, a, p, delta, r, None, None, dy, c(dlamT), c(detaT), saved=saved,
+                               want_init_grads=False)
+        return g["dq"], g["dk"], g["dv"], g["da"], g["dp"], g["ddelta"], g["dr"]
+
+
+def kla_filter_pc_ou(q, k, v, a, p, delta, r):
+    return KLAFilterPcOU.apply(q, k, v, a, p, delta, r)

@@ -346,6 +346,92 @@ kla_status kla_backward_pc(const kla_desc* desc, const void* q, const void* k, c
                                                                                                       : KLA_ERR_HIP;
 }
 
+size_t kla_backward_pc_ou_workspace(const kla_desc* desc, int with_saved) {
+    if (check_desc(desc) != KLA_OK) return 0;
+    return kla_backward_pc_workspace(desc, with_saved) + round_up(kla::pc_ou_part_bytes(shape_of(desc)));
+}
+
+kla_status kla_forward_pc_ou(const kla_desc* desc, const void* q, const void* k, const void* v, const float* a,
+                             const float* p, const float* delta, const void* r, const float* lam0, const float* eta0,
+                             void* y, float* yvar, float* lamT, float* etaT, void* saved, void* ws, size_t ws_bytes,
+                             hipStream_t stream) {
+    kla_status st = check_desc(desc);
+    if (st != KLA_OK) return st;
+    if (!a || !p || !delta) return KLA_ERR_NULL;
+    if (desc->T > 0 && (!q || !k || !v || !r || !y)) return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, (const void*)a, (const void*)p, (const void*)delta, r, (const void*)lam0,
+                     (const void*)eta0, y, (void*)yvar, (void*)lamT, (void*)etaT, saved, ws))
+        return KLA_ERR_ALIGN;
+    if (!ws || ws_bytes < kla_forward_workspace(desc)) return KLA_ERR_WORKSPACE;
+    const kla::Shape s = shape_of(desc);
+    if (check_mode()) {
+        st = validate(s, s.T, q, k, v, nullptr, nullptr, r, lam0, eta0, ws, stream, a, p, delta, true);
+        if (st != KLA_OK) return st;
+    }
+    const kla::FwdArgs f{q, k, v, nullptr, nullptr, r, lam0, eta0, y, yvar, lamT, etaT, a, p, delta};
+    return kla::launch_forward_pc(s, f, saved, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
+kla_status kla_backward_pc_ou(const kla_desc* desc, const void* q, const void* k, const void* v, const float* a,
+                              const float* p, const float* delta, const void* r, const float* lam0,
+                              const float* eta0, const void* saved, const void* dy, const float* dyvar,
+                              const float* dlamT, const float* detaT, void* dq, void* dk, void* dv, float* da,
+                              float* dp, float* ddelta, void* dr, float* dlam0, float* deta0, void* ws,
+                              size_t ws_bytes, hipStream_t stream) {
+    kla_status st = check_desc(desc);
+    if (st != KLA_OK) return st;
+    if (!a || !p || !delta || !da || !dp || !ddelta) return KLA_ERR_NULL;
+    if (desc->T > 0 && (!q || !k || !v || !r || !dy || !dq || !dk || !dv || !dr)) return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, (const void*)a, (const void*)p, (const void*)delta, r, (const void*)lam0,
+                     (const void*)eta0, saved, dy, (const void*)dyvar, (const void*)dlamT, (const void*)detaT, dq,
+                     dk, dv, (void*)da, (void*)dp, (void*)ddelta, dr, (void*)dlam0, (void*)deta0, ws))
+        return KLA_ERR_ALIGN;
+    if (!ws || ws_bytes < kla_backward_pc_ou_workspace(desc, saved != nullptr)) return KLA_ERR_WORKSPACE;
+    const kla::Shape s = shape_of(desc);
+    if (check_mode()) {
+        st = validate(s, s.T, q, k, v, nullptr, nullptr, r, lam0, eta0, ws, stream, a, p, delta, true);
+        if (st != KLA_OK) return st;
+    }
+    char* work = static_cast<char*>(ws) + kAlign;
+    float* kpart = reinterpret_cast<float*>(work);
+    void* ou_part = static_cast<char*>(ws) + kla_backward_pc_workspace(desc, saved != nullptr);
+    if (!saved) {
+        char* ctx = work + round_up(kla::pc_bwd_workspace(s));
+        void* yscratch = ctx + round_up(kla::pc_saved_bytes(s));
+        const kla::FwdArgs f{q, k, v, nullptr, nullptr, r, lam0, eta0, yscratch, nullptr, nullptr, nullptr, a, p,
+                             delta};
+        if (kla::launch_forward_pc(s, f, ctx, stream) != hipSuccess) return KLA_ERR_HIP;
+        saved = ctx;
+    }
+    kla::BwdArgs g{q,  k,  v,  nullptr, nullptr, r,  lam0, eta0,  dy, dlamT,
+                   detaT, dq, dk, dv, nullptr, nullptr, dr, dlam0, deta0};
+    g.ou_a = a;
+    g.ou_p = p;
+    g.ou_d = delta;
+    g.ou_part = ou_part;
+    g.dyvar = dyvar;
+    if (kla::launch_backward_pc(s, g, saved, kpart, stream) != hipSuccess) return KLA_ERR_HIP;
+    // the parameters are per (head, key slot, value channel): H dk dv of them, one part per batch row
+    return kla::launch_ou_param_grads(s.H, s.dk * s.dv, s.B, ou_part, !s.bf16, a, p, delta, da, dp, ddelta,
+                                      stream) == hipSuccess
+               ? KLA_OK
+               : KLA_ERR_HIP;
+}
+
+kla_status kla_decode_step_pc_ou(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,
+                                 const void* k, const void* v, const float* a, const float* p, const float* delta,
+                                 const void* r, float* lam, float* eta, void* y, float* yvar, hipStream_t stream) {
+    kla_desc d{S, 1, H, dk, dv, dtype};
+    kla_status st = check_desc(&d);
+    if (st != KLA_OK) return st;
+    if (!q || !k || !v || !a || !p || !delta || !r || !lam || !eta || !y) return KLA_ERR_NULL;
+    if (!all_aligned(q, k, v, (const void*)a, (const void*)p, (const void*)delta, r, (void*)lam, (void*)eta, y,
+                     (void*)yvar))
+        return KLA_ERR_ALIGN;
+    const kla::DecodeArgs g{q, k, v, nullptr, nullptr, r, lam, eta, y, yvar, a, p, delta};
+    return kla::launch_decode_pc(shape_of(&d), g, stream) == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+}
+
 kla_status kla_decode_step_pc(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const void* q,
                               const void* k, const void* v, const void* abar, const void* pbar, const void* r,
                               float* lam, float* eta, void* y, float* yvar, hipStream_t stream) {

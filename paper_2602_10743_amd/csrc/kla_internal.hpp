@@ -83,6 +83,9 @@ int recurrent_ou_parts(const Shape& s);
 hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, void* ck, hipStream_t st);
 size_t pc_saved_bytes(const Shape& s);
 size_t pc_bwd_workspace(const Shape& s);
+// OU parameters per (key slot, value channel), [H, dk, dv] (ou_a set in the arguments): the
+// backward leaves per-batch-row parts of the gate-gradient sums in the arithmetic type
+size_t pc_ou_part_bytes(const Shape& s);
 hipError_t launch_backward_pc(const Shape& s, const BwdArgs& a, const void* ck, float* kpart, hipStream_t st);
 hipError_t launch_decode_pc(const Shape& s, const DecodeArgs& a, hipStream_t st);
 

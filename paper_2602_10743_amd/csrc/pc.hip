@@ -29,6 +29,12 @@
 //   ge <- f ge,  gl <- gl rho + pbar dden
 // and after the first token dlam0 = gl, deta0 = ge.
 //
+// Gates per (key slot, value channel) (TI instantiations): Algorithm 1's
+// Abar, Pbar : (N, D), time-invariant, from OU parameters a, p, delta [H, dk, dv]
+// by the exact discretisation of Sec. 4.1; every lane forms the gates of its
+// elements once, the gates are not staged, and the backward sums each element's
+// gate gradients over its tokens (one part per batch row) instead of storing them.
+//
 // Arithmetic type A (acc<S>): fp64 for fp32 inputs, fp32 for bf16 inputs; the
 // per-element precision and state, their checkpoints and adjoints, and the partial
 // sums up to their single rounding into an output are held in A.  The sums over n (dv, dr)
@@ -68,7 +74,7 @@ __device__ __forceinline__ A sum8(A x) {   // over the 8 lanes of a channel
 // key-side inputs (abar, pbar, k, q as fp32 [t][n]) and the channel inputs
 // (r, v as [t][c]) are staged in LDS, the elements are updated, the partial
 // readouts summed over the 8 lanes of a channel and y, yvar written from LDS.
-template <typename S, int DK, int DV>
+template <typename S, int DK, int DV, bool TI>
 __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s, FwdArgs g,
                                                                        typename acc<S>::type* ck) {
     using T_ = typename storage<S>::type;
@@ -89,12 +95,16 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
     const int b = bh / s.H, h = bh % s.H;
     const int tid = threadIdx.x, ng = tid % kNG, c = tid / kNG, d = d0 + c;
 
-    A lam[NPER], eta[NPER];
+    A lam[NPER], eta[NPER], ga[NPER], gp[NPER];
 #pragma unroll
     for (int i = 0; i < NPER; ++i) {
         const size_t o = ((size_t)bh * DK + ng + kNG * i) * DV + d;
         lam[i] = g.lam0 ? (A)g.lam0[o] : A(1);
         eta[i] = g.eta0 ? (A)g.eta0[o] : A(0);
+        if constexpr (TI) {
+            const size_t og = ((size_t)h * DK + ng + kNG * i) * DV + d;
+            ou_gates(g.ou_a[og], g.ou_p[og], g.ou_d[og], ga[i], gp[i]);
+        }
     }
     // checkpoints: the belief before tokens 0, kCK, 2 kCK, ... as lam [BH][nseg][DK][DV] then eta
     const int nseg = (s.T + kCK - 1) / kCK;
@@ -105,7 +115,7 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
         for (int idx = tid; idx < nt * DK; idx += NTHR) {
             const int t = idx / DK, n = idx % DK;
             const size_t o = (((size_t)b * s.T + t0 + t) * s.H + h) * DK + n;
-            s_k[t][n] = make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
+            s_k[t][n] = TI ? make_float4(0.f, 0.f, ld(k, o), ld(q, o)) : make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
         }
         for (int idx = tid; idx < nt * CT; idx += NTHR) {
             const int t = idx / CT, cc = idx % CT;
@@ -128,7 +138,7 @@ __global__ __launch_bounds__(8 * (DV < 32 ? DV : 32)) void fwd_pc_kernel(Shape s
 #pragma unroll
             for (int i = 0; i < NPER; ++i) {
                 const float4 in = s_k[t][ng + kNG * i];   // abar, pbar, k, q
-                const A ax = in.x, py = in.y, kz = in.z, qw = in.w;
+                const A ax = TI ? ga[i] : (A)in.x, py = TI ? gp[i] : (A)in.y, kz = in.z, qw = in.w;
                 const A den = fma(py, lam[i], ax * ax);
                 const A num = fma(kz * kz * rc, den, lam[i]);
                 const A R = rcpa(den * num);
@@ -171,7 +181,7 @@ struct alignas(4 * sizeof(A)) A4p {
 // Decode: one token for S sequences, belief [S, H, dk, dv] updated in place.
 // One workgroup per (sequence, head); a thread owns 4 consecutive channels
 // (16-byte accesses of lam and eta) of every NG-th key slot.
-template <typename S, int DK, int DV>
+template <typename S, int DK, int DV, bool TI>
 __global__ __launch_bounds__(256) void decode_pc_kernel(int H, DecodeArgs g) {
     using T_ = typename storage<S>::type;
     using A = typename acc<S>::type;
@@ -189,7 +199,7 @@ __global__ __launch_bounds__(256) void decode_pc_kernel(int H, DecodeArgs g) {
     const int tid = threadIdx.x;
     for (int n = tid; n < DK; n += 256) {
         const size_t o = sh * DK + n;
-        s_k[n] = make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
+        s_k[n] = TI ? make_float4(0.f, 0.f, ld(k, o), ld(q, o)) : make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
     }
     for (int j = tid; j < DV4; j += 256) {
         const size_t o = sh * DV + 4 * j;
@@ -209,11 +219,16 @@ __global__ __launch_bounds__(256) void decode_pc_kernel(int H, DecodeArgs g) {
         for (int i = 0; i < NPER; ++i) {
             const int n = ng + NG * i;
             const float4 in = s_k[n];
-            const A ax = in.x, py = in.y, kz = in.z, qw = in.w;
+            const A kz = in.z, qw = in.w;
             const float4 l4 = lam4[n * DV4 + d4], e4 = eta4[n * DV4 + d4];
             A lp[4] = {l4.x, l4.y, l4.z, l4.w}, ep[4] = {e4.x, e4.y, e4.z, e4.w};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
+                A ax = in.x, py = in.y;
+                if constexpr (TI) {
+                    const size_t og = ((size_t)(sh % H) * DK + n) * DV + 4 * d4 + j;
+                    ou_gates(g.ou_a[og], g.ou_p[og], g.ou_d[og], ax, py);
+                }
                 const A den = fma(py, lp[j], ax * ax);
                 const A num = fma(kz * kz * rc[j], den, lp[j]);
                 const A R = rcpa(den * num);
@@ -267,8 +282,12 @@ template <typename S, int DK, int DV>
 struct FwdPc {
     static hipError_t run(const Shape& s, const FwdArgs& a, void* ck, hipStream_t st) {
         constexpr int CT = DV < 32 ? DV : 32;
-        hipLaunchKernelGGL((fwd_pc_kernel<S, DK, DV>), dim3((unsigned)(s.B * s.H * (DV / CT))), dim3(kNG * CT), 0,
-                           st, s, a, static_cast<typename acc<S>::type*>(ck));
+        const dim3 grid((unsigned)(s.B * s.H * (DV / CT))), block(kNG * CT);
+        auto* c = static_cast<typename acc<S>::type*>(ck);
+        if (a.ou_a)
+            hipLaunchKernelGGL((fwd_pc_kernel<S, DK, DV, true>), grid, block, 0, st, s, a, c);
+        else
+            hipLaunchKernelGGL((fwd_pc_kernel<S, DK, DV, false>), grid, block, 0, st, s, a, c);
         return hipGetLastError();
     }
 };
@@ -296,7 +315,7 @@ struct PcLanes {
     static constexpr int NTHR = LPC * CB;
 };
 
-template <typename S, int DK, int DV>
+template <typename S, int DK, int DV, bool TI>
 __global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) void bwd_pc_kernel(Shape s, BwdArgs g,
                                                                         const typename acc<S>::type* ck,
                                                                         float* kpart) {
@@ -326,12 +345,18 @@ __global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) voi
     const size_t nck = (size_t)s.B * s.H * nseg * DK * DV;
     const size_t nkey = part_stride((size_t)s.B * T * s.H * DK);
 
-    A ge[NPER], gl[NPER];
+    constexpr int NQ = TI ? 2 : 4;   // key-slot sums per token: dq, dk (, dabar, dpbar)
+    A ge[NPER], gl[NPER], ga[NPER], gp[NPER], sum_da[NPER], sum_dp[NPER];
 #pragma unroll
     for (int i = 0; i < NPER; ++i) {
         const size_t o = ((size_t)bh * DK + ln + LPC * i) * DV + d;
         ge[i] = g.detaT ? (A)g.detaT[o] : A(0);
         gl[i] = g.dlamT ? (A)g.dlamT[o] : A(0);
+        sum_da[i] = sum_dp[i] = 0;
+        if constexpr (TI) {
+            const size_t og = ((size_t)h * DK + ln + LPC * i) * DV + d;
+            ou_gates(g.ou_a[og], g.ou_p[og], g.ou_d[og], ga[i], gp[i]);
+        }
     }
     // The inputs of a segment and its checkpoint are fetched into registers one segment
     // ahead (indices clamped to the segment's last token, so every load is issued) and
@@ -345,7 +370,7 @@ __global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) voi
         for (int m = 0; m < KPT; ++m) {
             const int idx = min(tid + NTHR * m, kCK * DK - 1), t = min(idx / DK, tl), n = idx % DK;
             const size_t o = (((size_t)b * T + t0 + t) * s.H + h) * DK + n;
-            nk[m] = make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
+            nk[m] = TI ? make_float4(0.f, 0.f, ld(k, o), ld(q, o)) : make_float4(ld(a, o), ld(p, o), ld(k, o), ld(q, o));
         }
 #pragma unroll
         for (int m = 0; m < CPT; ++m) {
@@ -392,7 +417,7 @@ __global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) voi
 #pragma unroll
             for (int i = 0; i < NPER; ++i) {
                 const float4 in = s_k[ok ? j : 0][ln + LPC * i];
-                const A ax = in.x, py = in.y, kz = in.z;
+                const A ax = TI ? ga[i] : (A)in.x, py = TI ? gp[i] : (A)in.y, kz = in.z;
                 const A den = fma(py, lt[j][i], ax * ax);
                 const A num = fma(kz * kz * rc, den, lt[j][i]);
                 const A R = rcpa(den * num);
@@ -412,7 +437,7 @@ __global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) voi
 #pragma unroll
             for (int i = 0; i < NPER; ++i) {
                 const float4 in = s_k[j][ln + LPC * i];   // abar, pbar, k, q
-                const A av = in.x, pv = in.y, kv = in.z, qv = in.w;
+                const A av = TI ? ga[i] : (A)in.x, pv = TI ? gp[i] : (A)in.y, kv = in.z, qv = in.w;
                 const A lp = lt[j][i], lc = lt[j + 1][i], ep = et[j][i], ec = et[j + 1][i];
                 const A den = fma(pv, lp, av * av);
                 const A R = rcpa(lc * den);
@@ -429,8 +454,13 @@ __global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) voi
                 cdv = fma(gei, kr, cdv);
                 const A drho = fma(df, av, gli * lp);
                 const A dden = -drho * rho * rho;
-                kq[2][i] = (float)fma(df, rho, A(2) * av * dden);
-                kq[3][i] = (float)(dden * lp);
+                if constexpr (TI) {
+                    sum_da[i] += fma(df, rho, A(2) * av * dden);
+                    sum_dp[i] += dden * lp;
+                } else {
+                    kq[2][i] = (float)fma(df, rho, A(2) * av * dden);
+                    kq[3][i] = (float)(dden * lp);
+                }
                 ge[i] = av * rho * gei;
                 gl[i] = fma(gli, rho, pv * dden);
             }
@@ -453,16 +483,16 @@ __global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) voi
             // its own LDS row, summed in a fixed order after the barrier
             float* slot = &s_red[j & 1][c][0][0];
 #pragma unroll
-            for (int qi = 0; qi < 4; ++qi)
+            for (int qi = 0; qi < NQ; ++qi)
 #pragma unroll
                 for (int i = 0; i < NPER; ++i) slot[qi * DK + ln + LPC * i] = kq[qi][i];
             barrier_lds();   // the channels' key-slot values of token j are in
             const size_t tk = ((size_t)b * T + t0 + j) * s.H + h;
-            constexpr int RPT = (4 * DK + NTHR - 1) / NTHR;
+            constexpr int RPT = (NQ * DK + NTHR - 1) / NTHR;
 #pragma unroll
             for (int m = 0; m < RPT; ++m) {
                 const int idx = tid + NTHR * m;
-                if (RPT * NTHR != 4 * DK && idx >= 4 * DK) continue;
+                if (RPT * NTHR != NQ * DK && idx >= NQ * DK) continue;
                 float acc = 0.f;
 #pragma unroll
                 for (int cc = 0; cc < CB; ++cc) acc += (&s_red[j & 1][cc][0][0])[idx];
@@ -483,24 +513,30 @@ __global__ __launch_bounds__((PcLanes<DK, DV, typename acc<S>::type>::NTHR)) voi
         const size_t o = ((size_t)bh * DK + ln + LPC * i) * DV + d;
         if (g.dlam0) g.dlam0[o] = (float)gl[i];
         if (g.deta0) g.deta0[o] = (float)ge[i];
+        if constexpr (TI) {   // part b of the gate-gradient sums, [2][B][H][DK][DV]
+            A* part = static_cast<A*>(g.ou_part);
+            const size_t np = (size_t)s.B * s.H * DK * DV;
+            part[o] = sum_da[i];
+            part[np + o] = sum_dp[i];
+        }
     }
 }
 
 // dq, dk, dabar, dpbar = sums of the NT channel tiles' parts (in tile order), in the
 // input dtype.  A thread takes 4 consecutive elements (n is a multiple of 4; every
 // array is 16-byte aligned) and issues all of its 4 NT part loads before the sums.
-template <typename S, int NT>
+template <typename S, int NT, int NQ>
 __global__ __launch_bounds__(256) void pc_key_combine_kernel(const float* __restrict__ kpart, size_t n, BwdArgs g) {
     const size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * 4, ns = part_stride(n);
     if (i >= n) return;
     void* out[4] = {g.dq, g.dk, g.da, g.dp};
-    float4 x[4][NT];
+    float4 x[NQ][NT];
 #pragma unroll
-    for (int qi = 0; qi < 4; ++qi)
+    for (int qi = 0; qi < NQ; ++qi)
 #pragma unroll
         for (int t = 0; t < NT; ++t) x[qi][t] = *reinterpret_cast<const float4*>(kpart + ((size_t)t * 4 + qi) * ns + i);
 #pragma unroll
-    for (int qi = 0; qi < 4; ++qi) {
+    for (int qi = 0; qi < NQ; ++qi) {
         float4 acc = x[qi][0];
 #pragma unroll
         for (int t = 1; t < NT; ++t) {
@@ -523,15 +559,22 @@ struct BwdPc {
         using PL = PcLanes<DK, DV, typename acc<S>::type>;
         constexpr int CB = PL::CB;
         constexpr int NTHR = PL::NTHR;
-        hipLaunchKernelGGL((bwd_pc_kernel<S, DK, DV>), dim3((unsigned)(s.B * s.H * (DV / CB))), dim3(NTHR), 0, st,
-                           s, a, static_cast<const typename acc<S>::type*>(ck), kpart);
+        const dim3 grid((unsigned)(s.B * s.H * (DV / CB))), block(NTHR);
+        auto* c = static_cast<const typename acc<S>::type*>(ck);
+        if (a.ou_a)
+            hipLaunchKernelGGL((bwd_pc_kernel<S, DK, DV, true>), grid, block, 0, st, s, a, c, kpart);
+        else
+            hipLaunchKernelGGL((bwd_pc_kernel<S, DK, DV, false>), grid, block, 0, st, s, a, c, kpart);
         hipError_t e = hipGetLastError();
         const size_t n = (size_t)s.B * s.T * s.H * DK;   // dk is a multiple of 16, n of 4
         if (e != hipSuccess || n == 0) return e;
         constexpr int NT = DV / CB;
         static_assert(DK % 4 == 0 && (NT == 1 || NT == 2 || NT == 4 || NT == 8), "combine layout");
-        hipLaunchKernelGGL((pc_key_combine_kernel<S, NT>), dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, st,
-                           kpart, n, a);
+        const dim3 cgrid((unsigned)((n / 4 + 255) / 256));
+        if (a.ou_a)   // the gate gradients went to the parameter parts
+            hipLaunchKernelGGL((pc_key_combine_kernel<S, NT, 2>), cgrid, dim3(256), 0, st, kpart, n, a);
+        else
+            hipLaunchKernelGGL((pc_key_combine_kernel<S, NT, 4>), cgrid, dim3(256), 0, st, kpart, n, a);
         return hipGetLastError();
     }
 };
@@ -539,7 +582,12 @@ struct BwdPc {
 template <typename S, int DK, int DV>
 struct DecPc {
     static hipError_t run(const Shape& s, const DecodeArgs& a, hipStream_t st) {
-        hipLaunchKernelGGL((decode_pc_kernel<S, DK, DV>), dim3((unsigned)(s.B * s.H)), dim3(256), 0, st, s.H, a);
+        if (a.ou_a)
+            hipLaunchKernelGGL((decode_pc_kernel<S, DK, DV, true>), dim3((unsigned)(s.B * s.H)), dim3(256), 0, st,
+                               s.H, a);
+        else
+            hipLaunchKernelGGL((decode_pc_kernel<S, DK, DV, false>), dim3((unsigned)(s.B * s.H)), dim3(256), 0, st,
+                               s.H, a);
         return hipGetLastError();
     }
 };
@@ -553,6 +601,11 @@ hipError_t launch_forward_pc(const Shape& s, const FwdArgs& a, void* ck, hipStre
 size_t pc_saved_bytes(const Shape& s) {
     const size_t nseg = (size_t)(s.T + kCK - 1) / kCK;
     return 2 * (size_t)s.B * s.H * nseg * s.dk * s.dv * (s.bf16 ? sizeof(float) : sizeof(double));
+}
+
+// the per-batch-row parts of the gate-gradient sums of the OU entry points: [2][B][H][dk][dv]
+size_t pc_ou_part_bytes(const Shape& s) {
+    return 2 * (size_t)s.B * s.H * s.dk * s.dv * (s.bf16 ? sizeof(float) : sizeof(double));
 }
 
 size_t pc_bwd_workspace(const Shape& s) {

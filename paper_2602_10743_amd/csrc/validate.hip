@@ -60,7 +60,9 @@ hipError_t launch_validate(const Shape& s, const void* q, const void* k, const v
     const size_t nk = tok * s.dk, nv = tok * s.dv, ne = (size_t)s.B * s.H * s.dk * s.dv;
     // per-channel precision: r [B, T, H, dv] and lam0 [B, H, dk, dv]
     const size_t nr = per_channel ? nv : tok, nb = per_channel ? ne : (size_t)s.B * s.H * s.dk;
-    const size_t nou = (size_t)s.H * s.dk;
+    // OU parameters: [H, dk], or [H, dk, dv] (gates per key slot and value channel) with the
+    // per-channel precision
+    const size_t nou = (size_t)s.H * s.dk * (per_channel ? s.dv : 1);
     const unsigned grid = 1024;
     if (s.bf16)
         hipLaunchKernelGGL(validate_kernel<bf16_t>, dim3(grid), dim3(256), 0, st, nk, nv, nr, nb, ne, q, k, v, a,
