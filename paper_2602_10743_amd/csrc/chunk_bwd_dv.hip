@@ -98,7 +98,7 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void bwd_dv_kernel(Shape 
             f32x4 A00 = zero4(), A10 = zero4(), A11 = zero4();
 #pragma unroll
             for (int ks = 0; ks < KSN; ++ks) {
-                const int o0 = l16 * LQ + 32 * ks + 8 * g4, o1 = o0 + 16 * LQ;
+                const int o0 = l16 * LQ + 32 * ks + 8 * g4, o1 = o0 + 16 * LQ + kQPad;
                 const bf16x8 q0h = lds8(sQH + o0), q0l = lds8(sQL + o0);
                 const bf16x8 q1h = lds8(sQH + o1), q1l = lds8(sQL + o1);
                 const bf16x8 k0h = lds8(sKH + o0), k0l = lds8(sKL + o0);
@@ -132,7 +132,7 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void bwd_dv_kernel(Shape 
                 bf16x8 kbh[2], kbl[2];
 #pragma unroll
                 for (int jt = 0; jt < 2; ++jt) {
-                    const int ko = (16 * jt + l16) * LQ + 32 * ks + 4 * g4;
+                    const int ko = (16 * jt + l16) * LQ + jt * kQPad + 32 * ks + 4 * g4;
                     kbh[jt] = lds4x2(sKH + ko, sKH + ko + 16);
                     kbl[jt] = lds4x2(sKL + ko, sKL + ko + 16);
                 }
@@ -159,14 +159,15 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void bwd_dv_kernel(Shape 
             }
 
             // ---- G <- Qp^T dY + Gs
+            const int tpad = g4 >= 2 ? kQPad : 0;   // tile rows 8 g4 .. 8 g4 + 7 past row 16
             bf16x8 yb[NDT];   // dY rows t = 8 g4 .. 8 g4 + 7 of column d
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) yb[dt] = lds_tr8(sDY, DVT, 8 * g4, 8 * g4 + 4, dl0 + 16 * dt, l16);
 #pragma unroll
             for (int rt = 0; rt < NRT; ++rt) {
                 // Qp^T rows n = 16 rt + l16, tokens 8 g4 .. 8 g4 + 7
-                const bf16x8 qth = lds_tr8(sQH, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
-                const bf16x8 qtl = lds_tr8(sQL, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
+                const bf16x8 qth = lds_tr8(sQH + tpad, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
+                const bf16x8 qtl = lds_tr8(sQL + tpad, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
 #pragma unroll
                 for (int dt = 0; dt < NDT; ++dt) G[rt][dt] = mfma2a(qth, qtl, yb[dt], G[rt][dt]);
             }

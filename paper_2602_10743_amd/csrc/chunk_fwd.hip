@@ -98,7 +98,7 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
                     f32x4 S00 = zero4(), S01 = zero4(), S11 = zero4();
 #pragma unroll
                     for (int ks = 0; ks < KSN; ++ks) {
-                        const int o0 = l16 * LQ + 32 * ks + 8 * g4, o1 = o0 + 16 * LQ;
+                        const int o0 = l16 * LQ + 32 * ks + 8 * g4, o1 = o0 + 16 * LQ + kQPad;
                         const bf16x8 k0h = lds8(sKH + o0), k0l = lds8(sKL + o0);
                         const bf16x8 k1h = lds8(sKH + o1), k1l = lds8(sKL + o1);
                         const bf16x8 q0h = lds8(sQH + o0), q0l = lds8(sQL + o0);
@@ -132,7 +132,7 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
                         bf16x8 qbh[2], qbl[2];
 #pragma unroll
                         for (int it = 0; it < 2; ++it) {
-                            const int qo = (16 * it + l16) * LQ + 32 * ks + 4 * g4;
+                            const int qo = (16 * it + l16) * LQ + it * kQPad + 32 * ks + 4 * g4;
                             qbh[it] = lds4x2(sQH + qo, sQH + qo + 16);
                             qbl[it] = lds4x2(sQL + qo, sQL + qo + 16);
                         }
@@ -166,14 +166,15 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
                 }
 
                 // ---- state: H <- diag(P_C) (H + Kn^T V)
+                const int tpad = g4 >= 2 ? kQPad : 0;   // tile rows 8 g4 .. 8 g4 + 7 past row 16
                 bf16x8 vb[NDT];   // V rows t = 8 g4 .. 8 g4 + 7 of column d
 #pragma unroll
                 for (int dt = 0; dt < NDT; ++dt) vb[dt] = lds_tr8(sVS, DVT, 8 * g4, 8 * g4 + 4, dl0 + 16 * dt, l16);
 #pragma unroll
                 for (int rt = 0; rt < NRT; ++rt) {
                     // Kn^T rows n = 16 rt + l16, tokens 8 g4 .. 8 g4 + 7
-                    const bf16x8 kth = lds_tr8(sKH, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
-                    const bf16x8 ktl = lds_tr8(sKL, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
+                    const bf16x8 kth = lds_tr8(sKH + tpad, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
+                    const bf16x8 ktl = lds_tr8(sKL + tpad, LQ, 8 * g4, 8 * g4 + 4, 16 * rt, l16);
                     const float4 dec = *reinterpret_cast<const float4*>(sDec + 16 * rt + 4 * g4);
 #pragma unroll
                     for (int dt = 0; dt < NDT; ++dt) {

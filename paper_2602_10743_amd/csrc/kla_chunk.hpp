@@ -50,6 +50,26 @@ namespace kla {
 
 constexpr int kC = 32;   // tokens per chunk
 
+// LDS placement of the per-chunk [t][...] tiles written by the two halves of a scan
+// wave.  Lane l of a wave works on token rows of half l / 32; the rows 16 apart would
+// otherwise fall on the same LDS banks, so the second 16 rows of every tile start
+// 64 bytes (16 banks) further on: Qp / Kn tiles after kQPad extra halfwords, the
+// staged inputs one spare row of SW = 32 slots later (kSR rows per input).
+constexpr int kQPad = 32;
+constexpr int kSR = kC + 1;
+__device__ __forceinline__ constexpr int srow(int t) { return t + (t >> 4); }
+
+// x of lane l ^ 32, as seen by the lanes of one half: hi32 is valid in lanes 32..63
+// (the partner's value from lanes 0..31), lo32 in lanes 0..31.  One lane-swap
+// instruction, no LDS round trip.
+struct Swap32 {
+    float hi32, lo32;
+};
+__device__ __forceinline__ Swap32 swap32(float x) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return {__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+
 template <int DK_, int DV_>
 struct ChunkCfg {
     static constexpr int DK = DK_, DV = DV_;
@@ -64,18 +84,20 @@ struct ChunkCfg {
     static constexpr int NRT = DK / 16;
     static constexpr int KSN = DK / 32;
     static constexpr int LQ = DK + 8;                // row stride of [t][n] tiles (halfwords)
+    static constexpr int QPAD = kQPad;               // extra halfwords before row 16 of a tile
+    static constexpr int QT = kC * LQ + QPAD;        // one [t][n] tile (halfwords)
     // one exchange buffer (byte offsets)
-    static constexpr int QH = 0, QL = QH + kC * LQ * 2, KH = QL + kC * LQ * 2, KL = KH + kC * LQ * 2;
-    static constexpr int DEC = KL + kC * LQ * 2;     // P_C [DK] fp32
+    static constexpr int QH = 0, QL = QH + QT * 2, KH = QL + QT * 2, KL = KH + QT * 2;
+    static constexpr int DEC = KL + QT * 2;          // P_C [DK] fp32
     static constexpr int YVP = DEC + DK * 4;         // variance partials [NSW][kC] fp32
     static constexpr int VS = (YVP + NSW * kC * 4 + 15) / 16 * 16;   // value tile [kC][DVT] bf16
     static constexpr int BUF = VS + kC * DVT * 2;
     static constexpr int NVL = kC * DVT * 2 / 1024;  // 1 KiB wave loads of the value tile
     static constexpr int TPV = kC / NVL;             // tokens per value-tile load
-    // per scan wave: abar, pbar, k, q [2 buffers][4][kC][SW] bf16, then r [2][64] and the
-    // chunk-start lam [2][64] as words
+    // per scan wave: abar, pbar, k, q [2 buffers][4][kSR][SW] bf16 (token t in row
+    // t + t / 16), then r [2][64] and the chunk-start lam [2][64] as words
     static constexpr int STG = 2 * BUF;
-    static constexpr int STG_IN = 4 * kC * SW * 2;   // one buffer of staged inputs
+    static constexpr int STG_IN = 4 * kSR * SW * 2;  // one buffer of staged inputs
     static constexpr int STG_R = 2 * STG_IN, STG_L = STG_R + 2 * 64 * 4;
     static constexpr int STG_WAVE = STG_L + 2 * 64 * 4;
     static constexpr int BYTES = STG + NSW * STG_WAVE;
@@ -115,12 +137,13 @@ __device__ __forceinline__ void read_group(ScanGroup& gr, const uint16_t* __rest
                                            const uint32_t* __restrict__ rw, int sl, int t8) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
+        const int row = srow(t8 + e);
         if constexpr (!TI) {
-            gr.a[e] = stg[(0 * kC + t8 + e) * SW + sl];
-            gr.p[e] = stg[(1 * kC + t8 + e) * SW + sl];
+            gr.a[e] = stg[(0 * kSR + row) * SW + sl];
+            gr.p[e] = stg[(1 * kSR + row) * SW + sl];
         }
-        gr.k[e] = stg[(2 * kC + t8 + e) * SW + sl];
-        if constexpr (!NOQ) gr.q[e] = stg[(3 * kC + t8 + e) * SW + sl];
+        gr.k[e] = stg[(2 * kSR + row) * SW + sl];
+        if constexpr (!NOQ) gr.q[e] = stg[(3 * kSR + row) * SW + sl];
     }
     gr.r[0] = *reinterpret_cast<const uint4*>(rw + t8);
     gr.r[1] = *reinterpret_cast<const uint4*>(rw + t8 + 4);
@@ -145,9 +168,9 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const int t = 8 * hf + j;
-            ta[j] = TI ? ca : bf16w(stg[(0 * kC + t) * SW + sl]);
-            tp[j] = TI ? cp : bf16w(stg[(1 * kC + t) * SW + sl]);
-            tk[j] = bf16w(stg[(2 * kC + t) * SW + sl]);
+            ta[j] = TI ? ca : bf16w(stg[(0 * kSR + t) * SW + sl]);
+            tp[j] = TI ? cp : bf16w(stg[(1 * kSR + t) * SW + sl]);
+            tk[j] = bf16w(stg[(2 * kSR + t) * SW + sl]);
             tr[j] = bf16w(rw[t]);
         }
 #pragma unroll
@@ -165,9 +188,9 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
     }
     // ---- the start of this lane's half: (lam, 1, 1) in half 0; in half 1 the partner's
     // product (tokens 0..7) and then its own (8..15) applied to (lam, 1)
-    const float p00 = __shfl_xor(m00, 32, 64), p10 = __shfl_xor(m10, 32, 64);
-    const float p01 = __shfl_xor(m01, 32, 64), p11 = __shfl_xor(m11, 32, 64);
-    const float pa = __shfl_xor(aq, 32, 64);
+    const float p00 = swap32(m00).hi32, p10 = swap32(m10).hi32;   // used by half 1 only
+    const float p01 = swap32(m01).hi32, p11 = swap32(m11).hi32;
+    const float pa = swap32(aq).hi32;
     const float x8 = fmaf(p00, x, p01), z8 = fmaf(p10, x, p11);
     float xw = hf ? fmaf(m00, x8, m01 * z8) : x;
     float zw = hf ? fmaf(m10, x8, m11 * z8) : 1.f;
@@ -213,23 +236,24 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
             if constexpr (!NOQ) split2(qp2[0], qp2[1], qh, ql);
             split2(kn2[0], kn2[1], kh, kl);
             const int t = tb + 8 * g + 2 * j2;
+            const int e0 = t * LQ + hf * kQPad + n, e1 = e0 + LQ;   // rows t, t + 1
             if constexpr (!NOQ) {
-                o.qh[t * LQ + n] = static_cast<uint16_t>(qh);
-                o.qh[(t + 1) * LQ + n] = static_cast<uint16_t>(qh >> 16);
-                o.ql[t * LQ + n] = static_cast<uint16_t>(ql);
-                o.ql[(t + 1) * LQ + n] = static_cast<uint16_t>(ql >> 16);
+                o.qh[e0] = static_cast<uint16_t>(qh);
+                o.qh[e1] = static_cast<uint16_t>(qh >> 16);
+                o.ql[e0] = static_cast<uint16_t>(ql);
+                o.ql[e1] = static_cast<uint16_t>(ql >> 16);
             }
-            o.kh[t * LQ + n] = static_cast<uint16_t>(kh);
-            o.kh[(t + 1) * LQ + n] = static_cast<uint16_t>(kh >> 16);
-            o.kl[t * LQ + n] = static_cast<uint16_t>(kl);
-            o.kl[(t + 1) * LQ + n] = static_cast<uint16_t>(kl >> 16);
+            o.kh[e0] = static_cast<uint16_t>(kh);
+            o.kh[e1] = static_cast<uint16_t>(kh >> 16);
+            o.kl[e0] = static_cast<uint16_t>(kl);
+            o.kl[e1] = static_cast<uint16_t>(kl >> 16);
         }
     }
     // ---- the half-1 lanes stand at the chunk end; their lam goes to both halves
     const float iz = fast_rcp(zw);
     const float lam_end = xw * iz;
     if (hf) o.dec[n] = Aw * iz;
-    const float other = __shfl_xor(lam_end, 32, 64);
+    const float other = swap32(lam_end).lo32;   // half 1's lam, in half 0
     return hf ? lam_end : other;
 }
 
@@ -279,11 +303,11 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
         const int t0 = in ? cn * kC : 0, nt = in ? min(kC, T - t0) : 0;
         const size_t e0 = ((sc.seq0 + t0) * H + h) * DK + wave * SW;
         const uint32_t bytes = nt > 0 ? (uint32_t)((nt - 1) * H * DK + SW) * 2 : 0u;
-        uint16_t* stg = reinterpret_cast<uint16_t*>(stw) + bb * 4 * kC * SW;
+        uint16_t* stg = reinterpret_cast<uint16_t*>(stw) + bb * 4 * kSR * SW;
         auto one = [&](const uint16_t* src, int ti) {
             const rsrc_t rs = make_rsrc(src + e0, bytes);
-            buf_ld128_lds(rs, stg + ti * kC * SW, in_voff);
-            buf_ld128_lds(rs, stg + (ti * kC + 16) * SW, in_voff + 16 * tok_bytes);
+            buf_ld128_lds(rs, stg + ti * kSR * SW, in_voff);
+            buf_ld128_lds(rs, stg + (ti * kSR + srow(16)) * SW, in_voff + 16 * tok_bytes);
         };
         if constexpr (!TI) {
             one(sc.a, 0);
@@ -336,7 +360,7 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             o.kl = reinterpret_cast<uint16_t*>(buf + Cfg::KL);
             o.dec = reinterpret_cast<float*>(buf + Cfg::DEC);
             o.yv = reinterpret_cast<float*>(buf + Cfg::YVP) + wave * kC;
-            const uint16_t* stg = reinterpret_cast<const uint16_t*>(stw) + bb * 4 * kC * SW;
+            const uint16_t* stg = reinterpret_cast<const uint16_t*>(stw) + bb * 4 * kSR * SW;
             const uint32_t* rwc = rw + bb * 64;
             if (nt == kC)
                 x = scan_chunk<SW, Cfg::LQ, YV, true, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
