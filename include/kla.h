@@ -36,6 +36,19 @@
  *              checked unless the environment sets KLA_CHECK=1, in which case
  *              a validation kernel runs first and the call synchronises and
  *              returns KLA_ERR_NUMERIC on a violation.
+ *   Range    : the chunked path (bf16 inputs, see kla_forward) walks Theorem
+ *              1's precision update over 32-token chunks and forms, per key
+ *              slot, P_t / lam_t and 1 / P_t with P_t the product of the forget
+ *              gates F = abar rho from the chunk start to token t (Theorem 2).
+ *              Both must be finite in fp32: roughly, the geometric mean of F
+ *              over any 32 consecutive tokens must lie in about [0.07, 15]
+ *              (P_C within 2^+-126 over a chunk; e.g. abar = 0.03 with pbar =
+ *              0.05 for a whole chunk is outside).  Outside that range y and
+ *              the gradients are not finite.  Under KLA_CHECK=1 the walks of
+ *              the chunked forward and backward record whether any Qp or Kn
+ *              was not finite, and the call synchronises and returns
+ *              KLA_ERR_RANGE.  The token-recurrent path (fp32 inputs) and the
+ *              per-channel entry points have no such limit.
  *   Empty    : with T == 0 the per-token pointers may be NULL; the final
  *              belief is then the initial one and its gradients pass through.
  *   Errors   : return codes only; on any error nothing has been enqueued
@@ -66,7 +79,8 @@ typedef enum {
     KLA_ERR_ALIGN = 4,      /* a pointer is not 16-byte aligned                   */
     KLA_ERR_WORKSPACE = 5,  /* workspace missing or smaller than required         */
     KLA_ERR_NUMERIC = 6,    /* KLA_CHECK=1 found an input outside the domain      */
-    KLA_ERR_HIP = 7         /* a HIP launch or runtime call failed                */
+    KLA_ERR_HIP = 7,        /* a HIP launch or runtime call failed                */
+    KLA_ERR_RANGE = 8       /* KLA_CHECK=1: a chunk's gate products left fp32 range */
 } kla_status;
 
 /* Problem descriptor: batch, sequence length, heads, key width, value width, dtype. */

@@ -198,6 +198,9 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
     }
     ST += __shfl_xor(ST, 16, 64);
     ST += __shfl_xor(ST, 32, 64);
+    // range check of the walk: Qp Kn (= q r k / lam) summed over the lane's tokens stays
+    // finite exactly while every Qp and Kn is
+    float chk = 0.f;
     // time-invariant gates of the slot and the lane's sums of their gradients
     float ca = 0.f, cp = 0.f, sum_da = 0.f, sum_dp = 0.f;
     if constexpr (TI) {
@@ -416,6 +419,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                     const bool ok = FULL || t < nt;
                     qp2[e2] = ok ? (qv * An) * AR : 0.f;
                     kn2[e2] = ok ? (kr * zn) * XR : 0.f;
+                    chk = fmaf(qp2[e2], kn2[e2], chk);
                     lam_r[j] = xn * iz;
                     P_r[j] = An * iz;
                     iP_r[j] = zn * XR;
@@ -681,6 +685,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
         }
     }
     wait_vm_all();   // the requests for the chunk before the first have landed before exit
+    if (g.range_flag && !(fabsf(chk) <= 3.0e38f)) *g.range_flag = 1;
     if (g.dlam0 && e == 0 && g4 == 0) g.dlam0[(size_t)bh * DK + n0w + nl] = cT;
     if constexpr (TI) {   // part e * B + b of the token sums: the wave's four token groups added
         sum_da += __shfl_xor(sum_da, 16, 64);

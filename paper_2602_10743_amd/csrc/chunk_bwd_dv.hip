@@ -46,7 +46,8 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void bwd_dv_kernel(Shape 
         const ScanSrc sc{static_cast<const uint16_t*>(g.a), static_cast<const uint16_t*>(g.p),
                          static_cast<const uint16_t*>(g.k), static_cast<const uint16_t*>(g.q),
                          static_cast<const uint16_t*>(g.r), static_cast<const uint16_t*>(g.dy),
-                         tile * DVT, seq0, H, h, T, nchunk, bh, g.ou_a, g.ou_p, g.ou_d};
+                         tile * DVT, seq0, H, h, T, nchunk, bh, g.ou_a, g.ou_p, g.ou_d,
+                         g.range_flag};
         scan_wave<Cfg, false, true, TI>(smem, wave, lane, sc, saved_lam, nullptr);
         return;
     }

@@ -51,7 +51,7 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
 
     if (wave < NSW) {
         // ================================================================ scan waves
-        const ScanSrc sc{a, p, k, q, r, v, tile * DVT, seq0, H, h, T, nchunk, bh, g.ou_a, g.ou_p, g.ou_d};
+        const ScanSrc sc{a, p, k, q, r, v, tile * DVT, seq0, H, h, T, nchunk, bh, g.ou_a, g.ou_p, g.ou_d, g.range_flag};
         const float x = scan_wave<Cfg, YV, false, TI, NOY>(smem, wave, lane, sc, g.lam0, saved_lam);
         if (g.lamT && lane < SW && tile == 0) g.lamT[(size_t)bh * DK + wave * SW + lane] = x;
     } else {

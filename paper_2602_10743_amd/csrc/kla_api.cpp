@@ -73,6 +73,15 @@ kla_status validate(const kla::Shape& s, int T, const void* q, const void* k, co
     return host ? KLA_ERR_NUMERIC : KLA_OK;
 }
 
+// After a chunked call under KLA_CHECK=1: the walks set the flag (zeroed by validate)
+// when a chunk's in-chunk gate products left fp32 range.  Synchronous.
+kla_status range_status(const void* flag_ws, hipStream_t st) {
+    int host = 0;
+    if (hipMemcpyAsync(&host, flag_ws, sizeof(int), hipMemcpyDeviceToHost, st) != hipSuccess) return KLA_ERR_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return KLA_ERR_HIP;
+    return host ? KLA_ERR_RANGE : KLA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -127,20 +136,24 @@ kla_status forward_impl(const kla_desc* desc, const kla::FwdArgs& a, bool ou, vo
         return KLA_ERR_ALIGN;
     if (!ws || ws_bytes < kla_forward_workspace(desc)) return KLA_ERR_WORKSPACE;
     const kla::Shape s = shape_of(desc);
-    if (check_mode()) {
+    const bool check = check_mode();
+    kla::FwdArgs fa = a;
+    if (check) {
         st = validate(s, s.T, a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, ws, stream, a.ou_a, a.ou_p, a.ou_d);
         if (st != KLA_OK) return st;
+        fa.range_flag = static_cast<int*>(ws);
     }
     hipError_t e;
     // without a saved context any forward kernel may run; with one, the kernel whose
     // layout the backward reads (saves_chunked)
     const bool chunked = saved ? saves_chunked(s) : kla::chunked_supported(s);
     if (!saved && !ou && kla::forward_segments(s) > 1)
-        e = kla::launch_forward_segmented(s, a, static_cast<char*>(ws) + kAlign, stream);
+        e = kla::launch_forward_segmented(s, fa, static_cast<char*>(ws) + kAlign, stream);
     else
-        e = chunked ? kla::launch_forward_chunked(s, a, saved, stream)
-                    : kla::launch_forward_recurrent(s, a, saved, stream);
-    return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+        e = chunked ? kla::launch_forward_chunked(s, fa, saved, stream)
+                    : kla::launch_forward_recurrent(s, fa, saved, stream);
+    if (e != hipSuccess) return KLA_ERR_HIP;
+    return check && chunked ? range_status(ws, stream) : KLA_OK;
 }
 
 int ou_parts(const kla::Shape& s) {
@@ -173,9 +186,11 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
                            : kla_backward_workspace(desc, saved != nullptr);
     if (!ws || ws_bytes < need) return KLA_ERR_WORKSPACE;
     const kla::Shape s = shape_of(desc);
-    if (check_mode()) {
+    const bool check = check_mode();
+    if (check) {
         st = validate(s, s.T, a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, ws, stream, a.ou_a, a.ou_p, a.ou_d);
         if (st != KLA_OK) return st;
+        a.range_flag = static_cast<int*>(ws);
     }
     if (ou) a.ou_part = static_cast<char*>(ws) + kla_backward_workspace(desc, saved != nullptr);
     char* work = static_cast<char*>(ws) + kAlign;
@@ -185,7 +200,7 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
             char* ctx = work + round_up(kla::chunked_bwd_workspace(s));
             void* yscratch = ctx + round_up(kla::chunked_saved_bytes(s));
             kla::FwdArgs f{a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, yscratch, nullptr, nullptr, nullptr,
-                           a.ou_a, a.ou_p, a.ou_d};
+                           a.ou_a, a.ou_p, a.ou_d, a.range_flag};
             e = kla::launch_forward_chunked(s, f, ctx, stream);
             if (e != hipSuccess) return KLA_ERR_HIP;
             saved = ctx;
@@ -206,7 +221,8 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
     if (e == hipSuccess && ou)
         e = kla::launch_ou_param_grads(s.H, s.dk, ou_parts(s), a.ou_part, ou_part_bytes(s) == sizeof(double), a.ou_a,
                                        a.ou_p, a.ou_d, da, dp, dd, stream);
-    return e == hipSuccess ? KLA_OK : KLA_ERR_HIP;
+    if (e != hipSuccess) return KLA_ERR_HIP;
+    return check && kla::chunked_bwd_supported(s) ? range_status(ws, stream) : KLA_OK;
 }
 
 kla_status decode_impl(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const kla::DecodeArgs& a,
@@ -595,6 +611,8 @@ const char* kla_status_string(kla_status s) {
         case KLA_ERR_WORKSPACE: return "KLA_ERR_WORKSPACE: workspace missing or too small";
         case KLA_ERR_NUMERIC: return "KLA_ERR_NUMERIC: an input lies outside the filter's domain";
         case KLA_ERR_HIP: return "KLA_ERR_HIP: a HIP launch or runtime call failed";
+        case KLA_ERR_RANGE:
+            return "KLA_ERR_RANGE: the gate products inside a 32-token chunk left fp32 range";
     }
     return "KLA_ERR_UNKNOWN";
 }

@@ -155,11 +155,12 @@ __device__ __forceinline__ float bf16w(uint32_t w) { return __uint_as_float(w <<
 // inputs (stg: [4][kC][SW] bf16; rw: r as words [kC]), starting from the chunk-
 // start lam x.  FULL: all kC tokens are valid (no per-token guards).  TI: the
 // gates are the lane's ca, cp for every token.  Returns the lam at the chunk end
-// in every lane.
+// in every lane.  chk accumulates Qp Kn (= q r k / lam, of modest size) over the
+// lane's tokens (NOQ: 0 Kn): it stays finite exactly while every Qp and Kn is.
 template <int SW, int LQ, bool YV, bool FULL, bool TI, bool NOQ>
 __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, const uint32_t* __restrict__ rw,
                                             int sl, int hf, int n, int nt, float x, const ScanOut& o, float ca,
-                                            float cp) {
+                                            float cp, float& chk) {
     // ---- the 2x2 product of this lane's 8 tokens 8 hf .. 8 hf + 7, as the images of
     // (1, 0) and (0, 1), with the product of abar
     float m00 = 1.f, m10 = 0.f, m01 = 0.f, m11 = 1.f, aq = 1.f;
@@ -223,6 +224,7 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
                 const bool ok = FULL || t < nt;
                 qp2[e] = ok ? (qv * An) * AR : 0.f;
                 kn2[e] = ok ? (kr * zn) * (xn * R) : 0.f;
+                chk = fmaf(NOQ ? 0.f : qp2[e], kn2[e], chk);
                 xw = ok ? xn : xw;
                 zw = ok ? zn : zw;
                 Aw = ok ? An : Aw;
@@ -265,6 +267,7 @@ struct ScanSrc {
     size_t seq0;                          // b * T
     int H, h, T, nchunk, bh;
     const float *oa = nullptr, *op = nullptr, *od = nullptr;   // OU parameters [H, DK] (TI)
+    int* range_flag = nullptr;   // set to 1 when the walk leaves fp32 range, or none
 };
 
 // The scan-wave loop: nchunk + 1 rounds, each ended by barrier_lds().  The walk
@@ -284,6 +287,7 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
     const int sl = lane % SW, hf = lane / SW;   // key slot within the wave, half of the chunk
     const int n = wave * SW + sl;
     float x = 1.f;                              // lam at the chunk start
+    float chk = 0.f;                            // range check of the walk (scan_chunk)
     if (!REV && lam_in) x = lam_in[(size_t)sc.bh * DK + n];
     float ca = 0.f, cp = 0.f;                   // time-invariant gates of slot n
     if constexpr (TI) ou_gates(sc.oa[h * DK + n], sc.op[h * DK + n], sc.od[h * DK + n], ca, cp);
@@ -363,15 +367,16 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             const uint16_t* stg = reinterpret_cast<const uint16_t*>(stw) + bb * 4 * kSR * SW;
             const uint32_t* rwc = rw + bb * 64;
             if (nt == kC)
-                x = scan_chunk<SW, Cfg::LQ, YV, true, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
+                x = scan_chunk<SW, Cfg::LQ, YV, true, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp, chk);
             else
-                x = scan_chunk<SW, Cfg::LQ, YV, false, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp);
+                x = scan_chunk<SW, Cfg::LQ, YV, false, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp, chk);
             // the value tile has landed (younger: the NI + 1 + NL staging loads)
             wait_vm_le<NI + 1 + NL>();
         }
         barrier_lds();
     }
     wait_vm_all();   // the requests for the chunk past the end have landed before exit
+    if (sc.range_flag && !(fabsf(chk) <= 3.0e38f)) *sc.range_flag = 1;   // NaN fails the test too
     return x;
 }
 

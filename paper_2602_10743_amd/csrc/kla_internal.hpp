@@ -20,6 +20,8 @@ struct FwdArgs {
     void* y;
     float *yvar, *lamT, *etaT;
     const float *ou_a = nullptr, *ou_p = nullptr, *ou_d = nullptr;
+    // chunked path: set to 1 when a chunk's walk leaves fp32 range (Qp or Kn not finite), or none
+    int* range_flag = nullptr;
 };
 
 struct BwdArgs {
@@ -35,6 +37,7 @@ struct BwdArgs {
     // token-recurrent one (da, dp unused)
     void* ou_part = nullptr;
     const float* dyvar = nullptr;   // upstream gradient of yvar [B, T, H] fp32, or none
+    int* range_flag = nullptr;        // as in FwdArgs
 };
 
 struct DecodeArgs {
