@@ -37,18 +37,21 @@
  *              a validation kernel runs first and the call synchronises and
  *              returns KLA_ERR_NUMERIC on a violation.
  *   Range    : the chunked path (bf16 inputs, see kla_forward) walks Theorem
- *              1's precision update over 32-token chunks and forms, per key
- *              slot, P_t / lam_t and 1 / P_t with P_t the product of the forget
- *              gates F = abar rho from the chunk start to token t (Theorem 2).
- *              Both must be finite in fp32: roughly, the geometric mean of F
- *              over any 32 consecutive tokens must lie in about [0.07, 15]
- *              (P_C within 2^+-126 over a chunk; e.g. abar = 0.03 with pbar =
- *              0.05 for a whole chunk is outside).  Outside that range y and
- *              the gradients are not finite.  Under KLA_CHECK=1 the walks of
- *              the chunked forward and backward record whether any Qp or Kn
- *              was not finite, and the call synchronises and returns
- *              KLA_ERR_RANGE.  The token-recurrent path (fp32 inputs) and the
- *              per-channel entry points have no such limit.
+ *              1's precision update over 32-token chunks in homogeneous
+ *              coordinates: per key slot it carries, from the chunk start to
+ *              token t, A_t = prod abar and z_t = prod (abar^2 + pbar lam_{t-1})
+ *              (so lam_t = x_t / z_t and the product of the forget gates of
+ *              Theorem 2 is P_t = A_t / z_t) and forms q P_t / lam_t and
+ *              r k / P_t.  A_t, z_t and lam_t z_t must stay inside fp32's normal
+ *              range over every chunk: roughly, the geometric mean of abar over
+ *              32 consecutive tokens above 0.066 and that of abar^2 + pbar lam
+ *              below 16 (abar = 0.03 over a whole chunk is outside: A underflows).
+ *              Outside that range y and the gradients are not finite.  Under
+ *              KLA_CHECK=1 the walks of the chunked forward and backward record
+ *              whether any of those products was not finite, and the call
+ *              synchronises and returns KLA_ERR_RANGE.  The token-recurrent
+ *              path (fp32 inputs) and the per-channel entry points have no
+ *              such limit.
  *   Empty    : with T == 0 the per-token pointers may be NULL; the final
  *              belief is then the initial one and its gradients pass through.
  *   Errors   : return codes only; on any error nothing has been enqueued
@@ -94,8 +97,11 @@ size_t kla_forward_workspace(const kla_desc* desc);
 
 /* Bytes of the optional saved context that kla_forward can fill for
  * kla_backward: the precision and information state at every chunk start
- * (chunked path: bf16 inputs with dk >= 32), else the precision after every
- * token and the information state before every 64th token. */
+ * (chunked layout: bf16 inputs with dk >= 32 and dv >= 32, the shapes whose
+ * backward is chunked), else the precision after every token and the
+ * information state before every 64th token (fp32; fp64 for fp32 inputs, whose
+ * token-recurrent kernels accumulate in fp64).  Both calls pick the layout by
+ * the same rule, so a context from kla_forward always fits kla_backward. */
 size_t kla_saved_bytes(const kla_desc* desc);
 
 /* Bytes of device workspace kla_backward needs when it is given a saved
