@@ -10,9 +10,9 @@ traffic only while the sources still match it.
 
 Run from the repository root on the GPU machine (TMPDIR=/tmp):
   rocprofv3 --pmc FETCH_SIZE --output-format csv -d D/fetch -o run -- \\
-      python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration
+      python bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-configs --copy-calibration
   rocprofv3 --pmc WRITE_SIZE --output-format csv -d D/write -o run -- \\
-      python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration
+      python bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-configs --copy-calibration
   python -m paper_2602_10743_amd.traffic D/fetch D/write > profiles/lm_layer_traffic.md
 
 With OU gates: the same two runs with `bench.py ... --ou`, then
@@ -25,7 +25,7 @@ The state-tracking workload (fp32, token-recurrent kernels): the same two runs w
 MFMA and VALU utilisation per kernel come from a third run:
   rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU \\
       GRBM_GUI_ACTIVE --output-format csv -d D/util -o run -- \\
-      python bench.py --steps 2 --warmup 1 --no-cpu-baseline
+      python bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-configs
   python -m paper_2602_10743_amd.traffic --util D/util > profiles/lm_layer_mfma_valu.md
 """
 import csv
@@ -138,7 +138,7 @@ def summarise(fetch_dir: str, write_dir: str, ou: bool = False, a5: bool = False
         "",
         "Counters: FETCH_SIZE and WRITE_SIZE from two separate `rocprofv3 --pmc` runs of",
         ("`python bench.py --a5 --steps 2 --warmup 1 --copy-calibration`, scaled by" if a5 else
-         f"`python bench.py --steps 2 --warmup 1 --no-cpu-baseline --copy-calibration{flag}`, scaled by"),
+         f"`python bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-configs --copy-calibration{flag}`, scaled by"),
         f"the calibration copy kernel `{copy}` ({COPY_BYTES} bytes read and written):",
         f"fetch scale {f_fetch:.4f} bytes/unit, write scale {f_write:.4f} bytes/unit.",
         "",
@@ -208,7 +208,7 @@ def summarise_util(run_dir: str) -> str:
         "Command (repository root, one MI355X, TMPDIR=/tmp):",
         "",
         "    rocprofv3 --pmc " + " ".join(UTIL_COUNTERS) + " --output-format csv -d D/util -o run -- "
-        "python bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+        "python bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-configs",
         "    python -m paper_2602_10743_amd.traffic --util D/util",
         "",
         "Durations come from the dispatch timestamps of the same run.  MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / ",
