@@ -35,6 +35,9 @@ sequences to spread over the chip.
 With --a5 it times forward + backward of the state-tracking workload (B = 64,
 H = 4, T = 512, d = 32, fp32 inputs: the token-recurrent kernels).
 
+With --mc it times the Monte Carlo readout of KLA+ at the same shape with S = 10
+draws: kla_mc_sample, kla_mc_sample_backward, kla_mc_nll and kla_mc_nll_backward.
+
 With --block it times the block scaffolding around the layer at the same shape,
 forward + backward: the causal conv1d + SiLU over the C = H dk channels, the
 RMS QK-norm of q and of k (rows of dk) and the SiLU gate of the output, all
@@ -402,6 +405,74 @@ def bench_long(args, dev, emit=True):
     return res
 
 
+def bench_mc(args, dev):
+    """The Monte Carlo readout of KLA+ at the LM-layer shape with S = 10 draws: kla_mc_sample,
+    its backward, and the logsumexp loss with its backward, inputs resident in HBM.  The
+    draws (and their gradient, in the backward) are S copies of the bf16 readout, so the
+    calls are priced on HBM bytes; the Philox rounds make the draw kernels VALU-heavy."""
+    import torch
+    import kla_inputs as K
+    import paper_2602_10743_amd as kla
+    w = K.WORKLOADS[2]
+    B, T, H, dv, S, seed = w.B, w.T, w.H, w.dv, 10, 2026
+    g = torch.Generator(device=dev).manual_seed(0)
+    ymu = torch.randn((B, T, H, dv), generator=g, device=dev).to(torch.bfloat16)
+    yvar = 0.05 + torch.rand((B, T, H), generator=g, device=dev)
+    dys = torch.randn((S, B, T, H, dv), generator=g, device=dev).to(torch.bfloat16)
+    n = B * T * H
+    logp = -4.0 * torch.rand((S, n), generator=g, device=dev)
+    dnll = torch.randn(n, generator=g, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    names = ("kla_mc_sample", "kla_mc_sample_backward", "kla_mc_nll", "kla_mc_nll_backward")
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        kla.kla_mc_sample(ymu, yvar, S, seed)
+        if ev is not None:
+            ev[1].record(stream)
+        kla.kla_mc_sample_backward(yvar, dys, seed)
+        if ev is not None:
+            ev[2].record(stream)
+        kla.kla_mc_nll(logp)
+        if ev is not None:
+            ev[3].record(stream)
+        kla.kla_mc_nll_backward(logp, dnll)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = [float(np.mean([e[k].elapsed_time(e[k + 1]) for e in evs])) for k in range(4)]
+    el = B * T * H * dv
+    # algorithmic bytes per call: read ymu, yvar, write S draws; read yvar, S gradients, write
+    # dymu, dyvar; read logp, write nll; read logp, dnll, write dlogp
+    nbytes = [2 * el + 4 * n + 2 * S * el, 4 * n + 2 * S * el + 2 * el + 4 * n, 4 * S * n + 4 * n,
+              4 * S * n + 4 * n + 4 * S * n]
+    calls = {nm: {"ms": m, "bytes": b, "hbm_frac": b / (m * 1e-3) / 1e9 / HBM_PEAK_GBS}
+             for nm, m, b in zip(names, ms, nbytes)}
+    dom = max(range(4), key=lambda k: ms[k])
+    achieved = nbytes[dom] / (ms[dom] * 1e-3) / 1e9
+    res = {
+        "metric": METRIC, "value": n / (wall / args.steps), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": wall * 1e3 / args.steps, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.name + "_mc", "B": B, "T": T, "H": H, "dv": dv, "S": S,
+                   "pass": "draws + loss, forward and backward", "tokens_counted": "B*T*H"},
+        "roofline": {"bound": "hbm", "kernel": names[dom], "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "algorithmic_bytes_per_call": nbytes[dom], "calls": calls},
+    }
+    print(json.dumps(res), flush=True)
+
+
 def calls_per_step(name):
     return 2 if name.startswith("norm") else 1
 
@@ -468,6 +539,8 @@ def main():
                     help="decode step on the decode workload (with --pc: per-channel precision)")
     ap.add_argument("--long", action="store_true", help="forward of the long-context workload")
     ap.add_argument("--a5", action="store_true", help="fwd+bwd of the state-tracking workload (fp32)")
+    ap.add_argument("--mc", action="store_true",
+                    help="Monte Carlo readout (draws, logsumexp loss, their backward) at the LM-layer shape")
     ap.add_argument("--block", action="store_true",
                     help="block scaffolding around the layer (conv + SiLU, QK-norm, gate), forward + backward")
     args = ap.parse_args()
@@ -491,6 +564,9 @@ def main():
         return
     if args.a5:
         bench_a5(args, dev)
+        return
+    if args.mc:
+        bench_mc(args, dev)
         return
     if args.pc:
         bench_pc(args, w, dev)

@@ -26,12 +26,26 @@ namespace {
 constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;   // round multipliers
 constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;   // key increments
 
+// The 128-bit product m x (m a constant) as its high and low 64-bit halves, from four
+// 32 x 32 -> 64 partial products (v_mad_u64_u32) shared by both halves.
+template <uint64_t M>
+__device__ __forceinline__ void mul128(uint64_t x, uint64_t& hi, uint64_t& lo) {
+    constexpr uint32_t m0 = (uint32_t)M, m1 = (uint32_t)(M >> 32);
+    const uint32_t x0 = (uint32_t)x, x1 = (uint32_t)(x >> 32);
+    const uint64_t p00 = (uint64_t)m0 * x0;                           // bits 0..63
+    const uint64_t p01 = (uint64_t)m0 * x1 + (p00 >> 32);             // bits 32..95, no overflow
+    const uint64_t p10 = (uint64_t)m1 * x0 + (uint32_t)p01;           // bits 32..95, no overflow
+    hi = (uint64_t)m1 * x1 + (p01 >> 32) + (p10 >> 32);
+    lo = (p10 << 32) | (uint32_t)p00;
+}
+
 __device__ __forceinline__ void philox4x64_10(uint64_t c0, uint64_t key, uint64_t w[4]) {
     uint64_t x0 = c0, x1 = 0, x2 = 0, x3 = 0, k0 = key, k1 = 0;
 #pragma unroll
     for (int i = 0; i < 10; ++i) {
-        const uint64_t hi0 = __umul64hi(kM0, x0), lo0 = kM0 * x0;
-        const uint64_t hi1 = __umul64hi(kM1, x2), lo1 = kM1 * x2;
+        uint64_t hi0, lo0, hi1, lo1;
+        mul128<kM0>(x0, hi0, lo0);
+        mul128<kM1>(x2, hi1, lo1);
         const uint64_t y0 = hi1 ^ x1 ^ k0, y2 = hi0 ^ x3 ^ k1;
         x0 = y0;
         x1 = lo1;
@@ -46,19 +60,21 @@ __device__ __forceinline__ void philox4x64_10(uint64_t c0, uint64_t key, uint64_
     w[3] = x3;
 }
 
-// the 8 normals of Philox block j
+// the 8 normals of Philox block j.  The transcendentals are the hardware ones
+// (v_log_f32, v_sqrt_f32, v_sin_f32 / v_cos_f32 in revolutions, each within a few
+// ulp or 2^-20 absolute): the uniforms are exact multiples of 2^-24, the angle
+// pi a with a in [0, 2) is a / 2 revolutions.
 __device__ __forceinline__ void normals8(uint64_t j, uint64_t seed, float z[8]) {
     uint64_t w[4];
     philox4x64_10(j, seed, w);
 #pragma unroll
     for (int p = 0; p < 4; ++p) {
         const uint32_t ur = (uint32_t)w[p], ua = (uint32_t)(w[p] >> 32);
-        const float u = (float)((ur >> 8) + 1u) * 0x1p-24f;   // (0, 1], exact
-        const float r = sqrtf(-2.f * logf(u));
-        float s, c;
-        sincospif((float)(ua >> 8) * 0x1p-23f, &s, &c);
-        z[2 * p] = r * c;
-        z[2 * p + 1] = r * s;
+        const float u = (float)((ur >> 8) + 1u) * 0x1p-24f;                 // (0, 1], exact
+        const float r = __builtin_amdgcn_sqrtf(-2.f * 0.69314718055994531f * __builtin_amdgcn_logf(u));
+        const float rev = (float)(ua >> 8) * 0x1p-24f;                      // a / 2, exact
+        z[2 * p] = r * __builtin_amdgcn_cosf(rev);
+        z[2 * p + 1] = r * __builtin_amdgcn_sinf(rev);
     }
 }
 
