@@ -103,26 +103,40 @@ def cpu_baseline_pc(w):
 
 
 def bench_pc(args, w, dev):
-    """Forward of the per-channel-precision variant at the LM-layer shape."""
+    """Forward + backward of the per-channel-precision variant at the LM-layer shape; with
+    --ou its gates per (key slot, value channel) come from OU parameters [H, dk, dv]
+    (kla_forward_pc_ou / kla_backward_pc_ou, Algorithm 1's shapes)."""
     import torch
     import kla_inputs as K
     import paper_2602_10743_amd as kla
-    names = ("q", "k", "v", "a", "p", "rc", "dy")
+    names = ("q", "k", "v", "rc", "dy") if args.ou else ("q", "k", "v", "a", "p", "rc", "dy")
     bits = K.full(w, names=names, as_bits=True)
     x = {n: torch.from_numpy(np.ascontiguousarray(bits[n].view(np.int16))).view(torch.bfloat16).to(dev)
          for n in bits}
     del bits
+    ou = None
+    if args.ou:
+        ou = {n: torch.from_numpy(v).to(dev) for n, v in K.ou_params(w.H, w.dk, seed=w.cid, dv=w.dv).items()}
     stream = torch.cuda.current_stream(dev)
     y = torch.empty_like(x["v"])
 
     def step(ev=None):
         if ev is not None:
             ev[0].record(stream)
-        out = kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], want_state=False, save=True, y=y)
+        if ou is None:
+            out = kla.kla_forward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], want_state=False, save=True,
+                                     y=y)
+        else:
+            out = kla.kla_forward_pc_ou(x["q"], x["k"], x["v"], ou["a"], ou["p"], ou["delta"], x["rc"],
+                                        want_state=False, save=True)
         if ev is not None:
             ev[1].record(stream)
-        kla.kla_backward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], None, None, x["dy"],
-                            saved=out["saved"], want_init_grads=False)
+        if ou is None:
+            kla.kla_backward_pc(x["q"], x["k"], x["v"], x["a"], x["p"], x["rc"], None, None, x["dy"],
+                                saved=out["saved"], want_init_grads=False)
+        else:
+            kla.kla_backward_pc_ou(x["q"], x["k"], x["v"], ou["a"], ou["p"], ou["delta"], x["rc"], None, None,
+                                   x["dy"], saved=out["saved"], want_init_grads=False)
         if ev is not None:
             ev[2].record(stream)
 
@@ -145,17 +159,19 @@ def bench_pc(args, w, dev):
         "metric": METRIC, "value": th / (ms_per_step * 1e-3), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": w.name + "_pc", "B": w.B, "T": w.T, "H": w.H, "dk": w.dk, "dv": w.dv,
-                   "pass": "fwd+bwd", "precision": "per value channel (bf16 inputs, fp32 scan)",
+        "config": {"workload": w.name + ("_pc_ou" if ou else "_pc"), "B": w.B, "T": w.T, "H": w.H, "dk": w.dk,
+                   "dv": w.dv, "pass": "fwd+bwd", "precision": "per value channel (bf16 inputs, fp32 scan)",
+                   "gates": "ou (a, p, delta per head, key slot and value channel)" if ou else "per token",
                    "tokens_counted": "B*T*H"},
-        "roofline": {"bound": "alu", "kernel": "kla_backward_pc", "achieved": achieved / 1e12,
+        "roofline": {"bound": "alu", "kernel": "kla_backward_pc_ou" if ou else "kla_backward_pc",
+                     "achieved": achieved / 1e12,
                      "peak": VALU_LANE_OPS / 1e12, "unit": "T lane-ops/s",
                      "frac": achieved / VALU_LANE_OPS, "traffic": None,
                      "element_updates_per_call": elements, "slots_per_element": ALU_SLOTS_BWD_PER_ELEMENT,
                      "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
                      "fwd_frac": elements * ALU_SLOTS_PER_ELEMENT / (fwd_ms * 1e-3) / VALU_LANE_OPS},
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and ou is None:
         res["cpu_baseline"] = cpu_baseline_pc(w)
     print(json.dumps(res), flush=True)
 
