@@ -96,9 +96,10 @@ typedef struct {
 size_t kla_forward_workspace(const kla_desc* desc);
 
 /* Bytes of the optional saved context that kla_forward can fill for
- * kla_backward: the precision and information state at every chunk start
- * (chunked layout: bf16 inputs with dk >= 32 and dv >= 32, the shapes whose
- * backward is chunked), else the precision after every token and the
+ * kla_backward: the precision and information state at every chunk start, and
+ * the precision walk's state after the chunk's first 16 tokens (chunked layout:
+ * bf16 inputs with dk >= 32 and dv >= 32, the shapes whose backward is
+ * chunked), else the precision after every token and the
  * information state before every 64th token (fp32; fp64 for fp32 inputs, whose
  * token-recurrent kernels accumulate in fp64).  Both calls pick the layout by
  * the same rule, so a context from kla_forward always fits kla_backward. */

@@ -1,7 +1,7 @@
 // Chunked backward, key side: dq, dk, dabar, dpbar, dr and dlam0.
 //
 // Notation per chunk of kC = 32 tokens (local t), with P_t, Qp, Kn from the
-// precision walk (kla_chunk.hpp) redone from the saved chunk-start lam:
+// precision walk (kla_chunk.hpp) redone from the saved walk state:
 //   H_t  = P_t (H0 + sum_{j<=t} Kn_j v_j^T)          (state rows, H0 = saved chunk-start state)
 //   G    = adjoint of the chunk's last state from later tokens (detaT for the
 //          last chunk), Gs = diag(P_C) G
@@ -33,10 +33,11 @@
 // a pair takes the tokens 16 e .. 16 e + 15 of each chunk in the walks:
 //   walk   lanes = (slot nl = lane % 16, group g = lane / 16 of 4 tokens): each
 //          lane forms its group's transfer -- the 2x2 map of (x, z) of
-//          Theorem 1 over 4 tokens, with prod abar --, the eight groups of the
-//          chunk are chained through LDS, and each lane walks its 4 tokens from
-//          the group start, writing Qp and Kn ([t][16], split bf16) and keeping
-//          lam_t, P_t and the reciprocals the adjoint walk needs;
+//          Theorem 1 over 4 tokens, with prod abar --, the four groups of each
+//          half are chained through LDS from the saved state at the start of
+//          the half (lam_0, or lam_16 and P_16), and each lane walks its 4
+//          tokens from the group start, writing Qp and Kn ([t][16], split bf16)
+//          and keeping lam_t, P_t and the reciprocals the adjoint walk needs;
 //   MFMA   split by operand instead: wave 0 forms B^T and X^T (with the chunk's
 //          saved start state H0 in registers), wave 1 forms B and Y^T and
 //          carries G^T[dv, 16] in registers;
@@ -81,7 +82,7 @@ struct DkCfg {
     // per pair (offsets from the pair's base)
     static constexpr int STG = 0;                                   // [2][4][kC][16] bf16: abar, pbar, k, q
     static constexpr int RW = STG + 2 * 4 * kC * 16 * 2;            // [2][64] r words
-    static constexpr int LW = RW + 2 * 64 * 4;                      // [2][64] chunk-start lam (lanes < 16)
+    static constexpr int LW = RW + 2 * 64 * 4;                      // [2][64] walk state: lam_0, lam_16, P_16 [3][16]
     static constexpr int GV = LW + 2 * 64 * 4;                      // [2][64] yvar gradient (fp32)
     static constexpr int QH = GV + 2 * 64 * 4;                      // Qp, Kn split bf16 [kC][LQ2]
     static constexpr int QL = QH + kC * LQ2 * 2, KH = QL + kC * LQ2 * 2, KL = KH + kC * LQ2 * 2;
@@ -245,9 +246,10 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                 const rsrc_t rv = make_rsrc(g.dyvar + tok0 * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 4 : 0u);
                 buf_ld32_lds(rv, wb + Cfg::GV + bb * 256, (uint32_t)lane * H * 4);
             } else {
-                const rsrc_t rl =
-                    make_rsrc(saved_lam + ((size_t)bh * nchunk + (in ? cn : 0)) * DK + n0w, in ? 64u : 0u);
-                buf_ld32_lds(rl, wb + Cfg::LW + bb * 256, (uint32_t)lane * 4);
+                // lanes 16 i + l: row i of the saved walk state (lam_0, lam_16, P_16) for slot n0w + l
+                const rsrc_t rl = make_rsrc(saved_lam + ((size_t)bh * nchunk + (in ? cn : 0)) * kLamRows * DK + n0w,
+                                            in ? (uint32_t)(2 * DK + 16) * 4 : 0u);
+                buf_ld32_lds(rl, wb + Cfg::LW + bb * 256, (uint32_t)((lane >> 4) * DK + (lane & 15)) * 4);
             }
         } else if (part < nparts) {
             const int m = (part - nin) >> 1, i = wave + NW * m, sel = (part - nin) & 1;
@@ -384,14 +386,17 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             barrier_lds();   // the group transfers of the chunk are in
 
             // ================================================================ phase 2
-            // chain the earlier groups from the chunk start (x, z, A) = (lam, 1, 1)
-            float x = reinterpret_cast<const float*>(wb + Cfg::LW)[bb * 64 + nl], z = 1.f, A = 1.f;
+            // chain the wave's earlier groups from the saved state at the start of its half:
+            // (x, z, A) = (lam_0, 1, 1) for tokens 0..15, (lam_16, 1, P_16) for 16..31
+            const float* lws = reinterpret_cast<const float*>(wb + Cfg::LW) + bb * 64;
+            float x = lws[16 * E + nl], z = 1.f, A = E == 0 ? 1.f : lws[32 + nl];
 #pragma unroll
-            for (int q2 = 0; q2 < NG - 1; ++q2) {
-                const float m00 = qs[(q2 * 5 + 0) * 16 + nl], m10 = qs[(q2 * 5 + 1) * 16 + nl];
-                const float m01 = qs[(q2 * 5 + 2) * 16 + nl], m11 = qs[(q2 * 5 + 3) * 16 + nl];
-                const float aq = qs[(q2 * 5 + 4) * 16 + nl];
-                const bool use = q2 < gg;
+            for (int q2 = 0; q2 < NG / 2 - 1; ++q2) {
+                const int q3 = 4 * E + q2;
+                const float m00 = qs[(q3 * 5 + 0) * 16 + nl], m10 = qs[(q3 * 5 + 1) * 16 + nl];
+                const float m01 = qs[(q3 * 5 + 2) * 16 + nl], m11 = qs[(q3 * 5 + 3) * 16 + nl];
+                const float aq = qs[(q3 * 5 + 4) * 16 + nl];
+                const bool use = q2 < g4;
                 const float xn = fmaf(m00, x, m01 * z), zn = fmaf(m10, x, m11 * z);
                 x = use ? xn : x;
                 z = use ? zn : z;
@@ -747,7 +752,7 @@ size_t chunked_bwd_workspace(const Shape& s) { return (size_t)(s.dk / 16) * s.B 
 hipError_t launch_backward_chunked(const Shape& s, const BwdArgs& a, const void* saved, void* ws, hipStream_t st) {
     const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
     const float* saved_lam = static_cast<const float*>(saved);
-    const float* saved_H = saved_lam + (size_t)s.B * s.H * nchunk * s.dk;
+    const float* saved_H = saved_lam + (size_t)s.B * s.H * nchunk * kLamRows * s.dk;
     float* dr_part = static_cast<float*>(ws);
 #define KLA_DK_CASE(DK_, DV_)                                                    \
     if (s.dk == DK_ && s.dv == DV_) {                                            \

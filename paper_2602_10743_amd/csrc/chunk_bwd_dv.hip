@@ -11,8 +11,8 @@
 // the gradient of the initial state eta0.
 //
 // One workgroup per (batch, head, value tile of up to 64 channels).  The scan
-// waves redo the precision walk of each chunk from its saved start lam and
-// stage the chunk's dY tile; the MFMA waves (16 value channels each, G[dk, 16]
+// waves redo the precision walk of each chunk, each half of it from its saved
+// start state (lam_0; lam_16 and P_16), and stage the chunk's dY tile; the MFMA waves (16 value channels each, G[dk, 16]
 // in registers) consume the previous round's chunk:
 //   dV^T[d, j] = sum_i dY^T[d, i] A[i, j] + sum_n Gs^T[d, n] Kn^T[n, j]
 //   G[n, d]   += sum_t Qp^T[n, t] dY[t, d]
@@ -48,7 +48,7 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void bwd_dv_kernel(Shape 
                          static_cast<const uint16_t*>(g.r), static_cast<const uint16_t*>(g.dy),
                          tile * DVT, seq0, H, h, T, nchunk, bh, g.ou_a, g.ou_p, g.ou_d,
                          g.range_flag};
-        scan_wave<Cfg, false, true, TI>(smem, wave, lane, sc, saved_lam, nullptr);
+        scan_wave<Cfg, false, true, TI>(smem, wave, lane, sc, saved_lam, false);
         return;
     }
 

@@ -52,7 +52,7 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
     if (wave < NSW) {
         // ================================================================ scan waves
         const ScanSrc sc{a, p, k, q, r, v, tile * DVT, seq0, H, h, T, nchunk, bh, g.ou_a, g.ou_p, g.ou_d, g.range_flag};
-        const float x = scan_wave<Cfg, YV, false, TI, NOY>(smem, wave, lane, sc, g.lam0, saved_lam);
+        const float x = scan_wave<Cfg, YV, false, TI, NOY>(smem, wave, lane, sc, g.lam0, saved_lam != nullptr);
         if (g.lamT && lane < SW && tile == 0) g.lamT[(size_t)bh * DK + wave * SW + lane] = x;
     } else {
         // ================================================================ MFMA waves
@@ -186,6 +186,14 @@ __global__ __launch_bounds__((ChunkCfg<DK, DV>::NTHR)) void fwd_chunk_kernel(Sha
                     }
                 }
 
+                // the chunk's walk state goes to the saved context (one value tile stores it)
+                if (saved_lam && tile == 0) {
+                    constexpr int NV4 = kLamRows * DK / 4;
+                    const float4* src = reinterpret_cast<const float4*>(buf + Cfg::MIDS);
+                    float4* dst = reinterpret_cast<float4*>(saved_lam + ((size_t)bh * nchunk + cc) * kLamRows * DK);
+                    for (int i = m * 64 + lane; i < NV4; i += Cfg::NMW * 64) dst[i] = src[i];
+                }
+
                 if (YV && tile == 0 && m == 0 && lane < nt) {
                     const float* yv = reinterpret_cast<const float*>(buf + Cfg::YVP);
                     float acc = 0.f;
@@ -242,12 +250,13 @@ hipError_t launch_fwd(const Shape& s, const FwdArgs& a, float* saved_lam, float*
 
 bool chunked_supported(const Shape& s) { return s.bf16 && s.dk >= 32; }
 
-// Saved context: lam at every chunk start [BH][nchunk][dk], then the
+// Saved context: the precision walk's state of every chunk [BH][nchunk][kLamRows][dk]
+// (lam at the chunk start, lam_16 and P_16 after its first 16 tokens), then the
 // information state at every chunk start and after the last token
 // [BH][nchunk+1][dk][dv].
 size_t chunked_saved_bytes(const Shape& s) {
     const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
-    return (size_t)s.B * s.H * s.dk * (nchunk + (nchunk + 1) * (size_t)s.dv) * sizeof(float);
+    return (size_t)s.B * s.H * s.dk * (kLamRows * nchunk + (nchunk + 1) * (size_t)s.dv) * sizeof(float);
 }
 
 hipError_t launch_forward_chunked(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st) {
@@ -256,7 +265,7 @@ hipError_t launch_forward_chunked(const Shape& s, const FwdArgs& a, void* saved,
     if (saved) {
         const size_t nchunk = (size_t)(s.T + kC - 1) / kC;
         saved_lam = static_cast<float*>(saved);
-        saved_H = saved_lam + (size_t)s.B * s.H * nchunk * s.dk;
+        saved_H = saved_lam + (size_t)s.B * s.H * nchunk * kLamRows * s.dk;
     }
 #define KLA_FWD_CASE(DK_, DV_) \
     if (s.dk == DK_ && s.dv == DV_) return launch_fwd<DK_, DV_>(s, a, saved_lam, saved_H, st);

@@ -58,6 +58,7 @@ constexpr int kC = 32;   // tokens per chunk
 constexpr int kQPad = 32;
 constexpr int kSR = kC + 1;
 __device__ __forceinline__ constexpr int srow(int t) { return t + (t >> 4); }
+constexpr int kLamRows = 3;   // saved walk state per chunk and key slot: lam_0, lam_16, P_16
 
 // x of lane l ^ 32, as seen by the lanes of one half: hi32 is valid in lanes 32..63
 // (the partner's value from lanes 0..31), lo32 in lanes 0..31.  One lane-swap
@@ -89,17 +90,18 @@ struct ChunkCfg {
     // one exchange buffer (byte offsets)
     static constexpr int QH = 0, QL = QH + QT * 2, KH = QL + QT * 2, KL = KH + QT * 2;
     static constexpr int DEC = KL + QT * 2;          // P_C [DK] fp32
-    static constexpr int YVP = DEC + DK * 4;         // variance partials [NSW][kC] fp32
+    static constexpr int MIDS = DEC + DK * 4;        // walk state [kLamRows][DK] fp32
+    static constexpr int YVP = MIDS + kLamRows * DK * 4;   // variance partials [NSW][kC] fp32
     static constexpr int VS = (YVP + NSW * kC * 4 + 15) / 16 * 16;   // value tile [kC][DVT] bf16
     static constexpr int BUF = VS + kC * DVT * 2;
     static constexpr int NVL = kC * DVT * 2 / 1024;  // 1 KiB wave loads of the value tile
     static constexpr int TPV = kC / NVL;             // tokens per value-tile load
     // per scan wave: abar, pbar, k, q [2 buffers][4][kSR][SW] bf16 (token t in row
-    // t + t / 16), then r [2][64] and the chunk-start lam [2][64] as words
+    // t + t / 16), then r [2][64] and the saved walk state [2][2][64] as words
     static constexpr int STG = 2 * BUF;
     static constexpr int STG_IN = 4 * kSR * SW * 2;  // one buffer of staged inputs
     static constexpr int STG_R = 2 * STG_IN, STG_L = STG_R + 2 * 64 * 4;
-    static constexpr int STG_WAVE = STG_L + 2 * 64 * 4;
+    static constexpr int STG_WAVE = STG_L + 2 * 128 * 4;
     static constexpr int BYTES = STG + NSW * STG_WAVE;
     static_assert(DK >= 32 && DK % 32 == 0, "chunked path needs dk >= 32");
     static_assert(DVT % 16 == 0 && NVL >= 1 && NVL * TPV == kC, "value tile sizes");
@@ -123,6 +125,7 @@ struct ScanOut {
     uint16_t *qh, *ql, *kh, *kl;   // [t][n]
     float* dec;                    // P_C [n]
     float* yv;                     // per-token sums of q^2 / lam over this wave's slots
+    float* mid;                    // the chunk's walk state [kLamRows][n] (see scan_wave)
 };
 
 // Staged inputs of 8 consecutive tokens for one key slot (raw bf16 / r words;
@@ -157,45 +160,62 @@ __device__ __forceinline__ float bf16w(uint32_t w) { return __uint_as_float(w <<
 // gates are the lane's ca, cp for every token.  Returns the lam at the chunk end
 // in every lane.  chk accumulates Qp Kn (= q r k / lam, of modest size) over the
 // lane's tokens (NOQ: 0 Kn): it stays finite exactly while every Qp and Kn is.
-template <int SW, int LQ, bool YV, bool FULL, bool TI, bool NOQ>
+// lm, pm: the walk's state after token 15 in half 1, as lam_16 and P_16 = A_16 /
+// z_16 (the state (x, z, A) scaled by 1 / z_16, which leaves every Qp, Kn, lam
+// and P of the later tokens unchanged).  MID: the walk starts from such a saved
+// state instead, x = lam_0 in half 0 and lam_16 in half 1, pm = P_16 in half 1,
+// so neither the 8-token products nor the exchanges between the halves are
+// needed; the return value is then the half's own end lam (the chunk end in
+// half 1 only).
+template <int SW, int LQ, bool YV, bool FULL, bool TI, bool NOQ, bool MID = false>
 __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, const uint32_t* __restrict__ rw,
                                             int sl, int hf, int n, int nt, float x, const ScanOut& o, float ca,
-                                            float cp, float& chk) {
-    // ---- the 2x2 product of this lane's 8 tokens 8 hf .. 8 hf + 7, as the images of
-    // (1, 0) and (0, 1), with the product of abar
-    float m00 = 1.f, m10 = 0.f, m01 = 0.f, m11 = 1.f, aq = 1.f;
-    {
-        float ta[8], tp[8], tk[8], tr[8];
+                                            float cp, float& chk, float& lm, float& pm) {
+    float xw, zw, Aw;
+    if constexpr (MID) {
+        xw = x;
+        zw = 1.f;
+        Aw = hf ? pm : 1.f;
+    } else {
+        // ---- the 2x2 product of this lane's 8 tokens 8 hf .. 8 hf + 7, as the images of
+        // (1, 0) and (0, 1), with the product of abar
+        float m00 = 1.f, m10 = 0.f, m01 = 0.f, m11 = 1.f, aq = 1.f;
+        {
+            float ta[8], tp[8], tk[8], tr[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int t = 8 * hf + j;
-            ta[j] = TI ? ca : bf16w(stg[(0 * kSR + t) * SW + sl]);
-            tp[j] = TI ? cp : bf16w(stg[(1 * kSR + t) * SW + sl]);
-            tk[j] = bf16w(stg[(2 * kSR + t) * SW + sl]);
-            tr[j] = bf16w(rw[t]);
-        }
+            for (int j = 0; j < 8; ++j) {
+                const int t = 8 * hf + j;
+                ta[j] = TI ? ca : bf16w(stg[(0 * kSR + t) * SW + sl]);
+                tp[j] = TI ? cp : bf16w(stg[(1 * kSR + t) * SW + sl]);
+                tk[j] = bf16w(stg[(2 * kSR + t) * SW + sl]);
+                tr[j] = bf16w(rw[t]);
+            }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const float a2 = ta[j] * ta[j], phi = tk[j] * tk[j] * tr[j];
-            const float z0 = fmaf(tp[j], m00, a2 * m10), z1 = fmaf(tp[j], m01, a2 * m11);
-            const float x0 = fmaf(phi, z0, m00), x1 = fmaf(phi, z1, m01);
-            const bool ok = FULL || 8 * hf + j < nt;
-            m00 = ok ? x0 : m00;
-            m10 = ok ? z0 : m10;
-            m01 = ok ? x1 : m01;
-            m11 = ok ? z1 : m11;
-            aq = ok ? aq * ta[j] : aq;
+            for (int j = 0; j < 8; ++j) {
+                const float a2 = ta[j] * ta[j], phi = tk[j] * tk[j] * tr[j];
+                const float z0 = fmaf(tp[j], m00, a2 * m10), z1 = fmaf(tp[j], m01, a2 * m11);
+                const float x0 = fmaf(phi, z0, m00), x1 = fmaf(phi, z1, m01);
+                const bool ok = FULL || 8 * hf + j < nt;
+                m00 = ok ? x0 : m00;
+                m10 = ok ? z0 : m10;
+                m01 = ok ? x1 : m01;
+                m11 = ok ? z1 : m11;
+                aq = ok ? aq * ta[j] : aq;
+            }
         }
+        // ---- the start of this lane's half: (lam, 1, 1) in half 0; in half 1 the partner's
+        // product (tokens 0..7) and then its own (8..15) applied to (lam, 1)
+        const float p00 = swap32(m00).hi32, p10 = swap32(m10).hi32;   // used by half 1 only
+        const float p01 = swap32(m01).hi32, p11 = swap32(m11).hi32;
+        const float pa = swap32(aq).hi32;
+        const float x8 = fmaf(p00, x, p01), z8 = fmaf(p10, x, p11);
+        xw = hf ? fmaf(m00, x8, m01 * z8) : x;
+        zw = hf ? fmaf(m10, x8, m11 * z8) : 1.f;
+        Aw = hf ? aq * pa : 1.f;
+        const float iz16 = fast_rcp(zw);
+        lm = xw * iz16;
+        pm = Aw * iz16;
     }
-    // ---- the start of this lane's half: (lam, 1, 1) in half 0; in half 1 the partner's
-    // product (tokens 0..7) and then its own (8..15) applied to (lam, 1)
-    const float p00 = swap32(m00).hi32, p10 = swap32(m10).hi32;   // used by half 1 only
-    const float p01 = swap32(m01).hi32, p11 = swap32(m11).hi32;
-    const float pa = swap32(aq).hi32;
-    const float x8 = fmaf(p00, x, p01), z8 = fmaf(p10, x, p11);
-    float xw = hf ? fmaf(m00, x8, m01 * z8) : x;
-    float zw = hf ? fmaf(m10, x8, m11 * z8) : 1.f;
-    float Aw = hf ? aq * pa : 1.f;
 
     // ---- walk tokens 16 hf .. 16 hf + 15 (inputs of the next 8 read before the current 8)
     const int tb = 16 * hf;
@@ -255,8 +275,12 @@ __device__ __forceinline__ float scan_chunk(const uint16_t* __restrict__ stg, co
     const float iz = fast_rcp(zw);
     const float lam_end = xw * iz;
     if (hf) o.dec[n] = Aw * iz;
-    const float other = swap32(lam_end).lo32;   // half 1's lam, in half 0
-    return hf ? lam_end : other;
+    if constexpr (MID) {
+        return lam_end;
+    } else {
+        const float other = swap32(lam_end).lo32;   // half 1's lam, in half 0
+        return hf ? lam_end : other;
+    }
 }
 
 // Sequence and tensors of one scan-wave loop.
@@ -271,15 +295,18 @@ struct ScanSrc {
 };
 
 // The scan-wave loop: nchunk + 1 rounds, each ended by barrier_lds().  The walk
-// order is c = 0 .. nchunk-1 (REV = false: lam carried from lam_in, the
-// chunk-start lam stored to save_lam when given) or c = nchunk-1 .. 0 (REV:
-// the chunk-start lam read from lam_in [BH][nchunk][DK]).  Returns the lam
-// after the last walked token (forward order) for key slot wave * SW + lane % SW.
+// order is c = 0 .. nchunk-1 (REV = false: lam carried from lam_in, and with
+// save the chunk's walk state written to the exchange buffer's mid region, which
+// the MFMA waves store) or c = nchunk-1 .. 0 (REV: the walk state read from
+// lam_in).  The walk state of a chunk is [kLamRows][DK]: lam at the chunk start,
+// lam_16 and P_16 after its first 16 tokens (the valid ones when fewer); the
+// saved sequence holds it as [BH][nchunk][kLamRows][DK].  Returns, walking
+// forwards, the lam after the last token for key slot wave * SW + lane % SW.
 template <class Cfg, bool YV, bool REV, bool TI, bool NOQ = false>
 __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int lane, const ScanSrc& sc,
-                                           const float* __restrict__ lam_in, float* __restrict__ save_lam) {
+                                           const float* __restrict__ lam_in, bool save) {
     constexpr int DK = Cfg::DK, DV = Cfg::DV, DVT = Cfg::DVT, SW = Cfg::SW, NSW = Cfg::NSW;
-    constexpr int NL = REV ? 1 : 0;    // chunk-start lam requests per round
+    constexpr int NL = REV ? 2 : 0;    // walk-state requests per round
     // staging loads of the per-token key-side inputs per round: two per staged tensor
     constexpr int NI = 2 * ((TI ? 0 : 2) + 1 + (NOQ ? 0 : 1));
     static_assert(!(NOQ && YV), "the readout variance needs the query");
@@ -288,20 +315,22 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
     const int n = wave * SW + sl;
     float x = 1.f;                              // lam at the chunk start
     float chk = 0.f;                            // range check of the walk (scan_chunk)
+    float lm = 0.f, pm = 0.f;                   // half 1: lam_16, P_16 of the chunk walked last
     if (!REV && lam_in) x = lam_in[(size_t)sc.bh * DK + n];
     float ca = 0.f, cp = 0.f;                   // time-invariant gates of slot n
     if constexpr (TI) ou_gates(sc.oa[h * DK + n], sc.op[h * DK + n], sc.od[h * DK + n], ca, cp);
     unsigned char* stw = smem + Cfg::STG + wave * Cfg::STG_WAVE;
     uint32_t* rw = reinterpret_cast<uint32_t*>(stw + Cfg::STG_R);   // [2][64]
-    float* lw = reinterpret_cast<float*>(stw + Cfg::STG_L);         // [2][64]
+    float* lw = reinterpret_cast<float*>(stw + Cfg::STG_L);         // [2][2][64]
     const uint32_t tok_bytes = (uint32_t)H * DK * 2;
     // lane -> (token lane / 4, 8 slots); a load of 16 tokens lands as [t][SW] rows
     const uint32_t in_voff = (uint32_t)(lane >> 2) * tok_bytes + (lane & 3) * 16;
     auto chunk_of = [&](int it) { return REV ? nchunk - 1 - it : it; };
 
     // every input of chunk cn into staging buffer bb: abar, pbar, k, q (two loads of 16
-    // tokens each), r and, walking backwards, the chunk-start lam.  Chunks outside the
-    // sequence get empty descriptors, whose loads write zeros.
+    // tokens each), r and, walking backwards, the saved walk state (lane l: lam_0 of
+    // slot l, or lam_16 of slot l - 32, then P_16).  Chunks outside the sequence get
+    // empty descriptors, whose loads write zeros.
     auto issue_inputs = [&](int cn, int bb) {
         const bool in = cn >= 0 && cn < nchunk;
         const int t0 = in ? cn * kC : 0, nt = in ? min(kC, T - t0) : 0;
@@ -322,9 +351,10 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
         const rsrc_t rr = make_rsrc(sc.r + (sc.seq0 + t0) * H + h, nt > 0 ? (uint32_t)((nt - 1) * H + 1) * 2 : 0u);
         buf_ld16_lds(rr, rw + bb * 64, (uint32_t)lane * H * 2);
         if constexpr (REV) {
-            const rsrc_t rl = make_rsrc(lam_in + ((size_t)sc.bh * nchunk + (in ? cn : 0)) * DK + wave * SW,
-                                        in ? (uint32_t)SW * 4 : 0u);
-            buf_ld32_lds(rl, lw + bb * 64, (uint32_t)lane * 4);
+            const rsrc_t rl = make_rsrc(lam_in + ((size_t)sc.bh * nchunk + (in ? cn : 0)) * kLamRows * DK + wave * SW,
+                                        in ? (uint32_t)(2 * DK + SW) * 4 : 0u);
+            buf_ld32_lds(rl, lw + bb * 128, (uint32_t)(hf * DK + sl) * 4);
+            buf_ld32_lds(rl, lw + bb * 128 + 64, (uint32_t)(2 * DK + sl) * 4);
         }
     };
     // this wave's share of the value-tile loads (loads i = wave, wave + NSW, ...)
@@ -338,8 +368,6 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
         for (int i = wave; i < Cfg::NVL; i += NSW)
             buf_ld128_lds(rv, vs + i * 1024, v_voff + (uint32_t)(i * Cfg::TPV) * H * DV * 2);
     };
-    // the chunk-start lam goes to save_lam (one store per round, issued by the whole wave)
-    const bool sl_store = !REV && save_lam != nullptr;
     wait_vm_all();   // the carried lam is complete before the prefetch loop starts
     if (nchunk > 0) issue_inputs(chunk_of(0), 0);
 
@@ -347,14 +375,15 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
         if (it < nchunk) {
             const int c = chunk_of(it), bb = it & 1;
             const int nt = min(kC, T - c * kC);
-            if (sl_store) save_lam[((size_t)sc.bh * nchunk + c) * DK + n] = x;
             issue_tile(c, it);
             issue_inputs(chunk_of(it + 1), bb ^ 1);
             // this chunk's inputs, requested one round earlier, have landed: younger are the
-            // requests just issued (the saved-lam store, the value-tile loads, NI + 1 + NL
-            // staging loads)
-            wait_vm_le_rt<NI + 1 + NL>(nvw + (sl_store ? 1 : 0));
-            if constexpr (REV) x = lw[bb * 64 + sl];
+            // requests just issued (the value-tile loads, NI + 1 + NL staging loads)
+            wait_vm_le_rt<NI + 1 + NL>(nvw);
+            if constexpr (REV) {
+                x = lw[bb * 128 + lane];
+                pm = lw[bb * 128 + 64 + lane];
+            }
 
             unsigned char* buf = smem + (it & 1) * Cfg::BUF;
             ScanOut o;
@@ -364,12 +393,24 @@ __device__ __forceinline__ float scan_wave(unsigned char* smem, int wave, int la
             o.kl = reinterpret_cast<uint16_t*>(buf + Cfg::KL);
             o.dec = reinterpret_cast<float*>(buf + Cfg::DEC);
             o.yv = reinterpret_cast<float*>(buf + Cfg::YVP) + wave * kC;
+            o.mid = reinterpret_cast<float*>(buf + Cfg::MIDS);
+            const float x0 = x;
             const uint16_t* stg = reinterpret_cast<const uint16_t*>(stw) + bb * 4 * kSR * SW;
             const uint32_t* rwc = rw + bb * 64;
             if (nt == kC)
-                x = scan_chunk<SW, Cfg::LQ, YV, true, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp, chk);
+                x = scan_chunk<SW, Cfg::LQ, YV, true, TI, NOQ, REV>(stg, rwc, sl, hf, n, nt, x, o, ca, cp, chk, lm,
+                                                                  pm);
             else
-                x = scan_chunk<SW, Cfg::LQ, YV, false, TI, NOQ>(stg, rwc, sl, hf, n, nt, x, o, ca, cp, chk);
+                x = scan_chunk<SW, Cfg::LQ, YV, false, TI, NOQ, REV>(stg, rwc, sl, hf, n, nt, x, o, ca, cp, chk, lm,
+                                                                   pm);
+            if (!REV && save) {
+                if (hf) {
+                    o.mid[DK + n] = lm;
+                    o.mid[2 * DK + n] = pm;
+                } else {
+                    o.mid[n] = x0;
+                }
+            }
             // the value tile has landed (younger: the NI + 1 + NL staging loads)
             wait_vm_le<NI + 1 + NL>();
         }

@@ -203,5 +203,5 @@ def test_saved_context_layout_follows_the_backward(lib):
     rec = (B * T * H * dk + B * H * nck * dk * 16) * 4   # bf16 inputs: fp32 arithmetic
     assert K.kla_saved_bytes(_desc(B, T, H, dk, 16, 1)) == rec
     nchunk = (T + 31) // 32
-    chunked = B * H * dk * (nchunk + (nchunk + 1) * 32) * 4
+    chunked = B * H * dk * (3 * nchunk + (nchunk + 1) * 32) * 4   # walk state (3 rows), then states
     assert K.kla_saved_bytes(_desc(B, T, H, dk, 32, 1)) == chunked
