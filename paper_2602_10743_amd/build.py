@@ -25,7 +25,7 @@ FLAGS = [
     "-I", INCLUDE, "-I", CSRC, "-Wall", "-Wno-unused-function",
 ]
 SOURCES = ["kla_api.cpp", "recurrent.hip", "validate.hip", "ou.hip", "pc.hip", "block.hip", "chunk_fwd.hip",
-           "chunk_seg.hip", "chunk_bwd_dv.hip", "chunk_bwd_dk.hip", "noalloc.hip", "mc.hip"]
+           "chunk_seg.hip", "chunk_bwd_dv.hip", "chunk_bwd_dk.hip", "chunk64.hip", "noalloc.hip", "mc.hip"]
 
 
 def _hipcc() -> str:

@@ -1,0 +1,698 @@
+// Chunked forward and backward of the KLA filter for fp32 inputs, in fp64.
+//
+// The chunk form of the bf16 path (chunk_fwd.hip, chunk_bwd_dv.hip,
+// chunk_bwd_dk.hip) with every quantity in fp64.  Per chunk of kC64 = 32 tokens
+// and key slot n, the precision walk (Theorem 1 in homogeneous coordinates:
+// z' = pbar x + abar^2 z, x' = x + k^2 r z', from (x, z) = (lam_0, 1), A the
+// running product of abar) gives
+//   lam_t = x_t / z_t,   P_t = A_t / z_t   (the product of the forget gates
+//                                           F = abar rho over the chunk),
+//   Qp[t, n] = q / lam_t * P_t = q A_t / x_t,   Kn[t, n] = k r / P_t = k r z_t / A_t,
+// and the readout and state update of Algorithm 1 over the chunk are
+//   y = M(Qp Kn^T) V + Qp H0,   H_C = diag(P_C) (H0 + Kn^T V)   (M: j <= t).
+// The backward is their reverse-mode counterpart, chunk by chunk from the last:
+//   S = M(Qp Kn^T),  B = M(dY V^T),  Gs = diag(P_C) G   (G: adjoint of the chunk's
+//   last state from later tokens, detaT for the last chunk)
+//   dV = S^T dY + Kn Gs,  X = dY H0^T + B Kn,  Y = B^T Qp + V Gs^T,
+//   G' = Qp^T dY + Gs   (carried into the previous chunk; after the first, deta0),
+// dqt = P X (gradient of qt = q / lam_t) and dkh = Y / P (gradient of kh = k r),
+// then the adjoint walk of the precision, per slot over the chunk's tokens in
+// reverse: with u_t = qt dqt - kh dkh summed from the end into S (the adjoint of
+// log F, started at sum_d detaT H_T), g_t = c_t - q (dqt + q gv) / lam_t^2 and
+// c_{t-1} = abar^2 rho^2 g_t - pbar rho S_t (c_T = dlamT, gv the upstream
+// gradient of yvar), the input gradients
+//   dq = (dqt + 2 q gv) / lam,  dk = r dkh + 2 k r g,  dr = sum_n (k dkh + k^2 g),
+//   drho = g lam_{t-1} + S / rho,  dabar = S / abar - 2 abar rho^2 drho,
+//   dpbar = -lam_{t-1} rho^2 drho,  dlam0 = c after the first token.
+//
+// Why fp64 in chunks: the fp32-input path is held to 1e-4 on every gradient, which
+// its long adjoint chains only meet in fp64, and the token-recurrent fp64 kernels
+// are bound by one dependent step per token; here the dependent steps are per
+// chunk (the walk over 32 tokens, spread over token groups as in chunk_bwd_dk.hip),
+// and the contractions run on v_mfma_f64_16x16x4_f64.
+//
+// One workgroup of 256 threads per (b, h), dk and dv in {16, 32}.  The walk
+// lanes are (slot n = tid % dk, token group gq = tid / dk of TPG tokens); each
+// lane forms its group's 2x2 transfer, the groups are chained through LDS from
+// the chunk-start lam, and each lane then walks its own tokens.  Tokens past the
+// sequence end enter with abar = 1, pbar = k = q = r = 0, which the walk, the
+// contractions and the adjoint pass through unchanged.  The 16x16 tiles of the
+// state (forward) or its adjoint (backward) live in the registers of one wave
+// each.
+//
+// Saved context (c64_saved_bytes): lam at every chunk start [BH][nchunk][dk], then
+// the information state at every chunk start and after the last token
+// [BH][nchunk+1][dk][dv], fp64.
+#include "kla_device.hpp"
+#include "kla_internal.hpp"
+
+namespace kla {
+namespace {
+
+constexpr int kC64 = 32;    // tokens per chunk
+constexpr int kNT64 = 256;  // threads per workgroup
+
+typedef double d4 __attribute__((ext_vector_type(4)));
+
+// D += A B over four columns of A (v_mfma_f64_16x16x4_f64): lane l supplies
+// A[l % 16][l / 16] and B[l / 16][l % 16]; D[i][j] is component i / 4 of lane
+// j + 16 (i % 4).
+__device__ __forceinline__ d4 mfma64(double a, double b, d4 c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ d4 zero_d4() { return d4{0.0, 0.0, 0.0, 0.0}; }
+
+// acc += sum_{k < K} A(i, k) B(k, j) for the 16x16 tile whose A rows start at pa and
+// B columns at pb (LDS), A(i, k) = pa[i AI + k AK], B(k, j) = pb[k BK + j BJ].  The
+// triangular products run over the whole chunk: the tile above the diagonal of the
+// masked matrices is stored as zeros.
+template <int K, int AI, int AK, int BK, int BJ>
+__device__ __forceinline__ d4 tile_mm(d4 acc, const double* pa, const double* pb, int lane) {
+    const int li = lane & 15, lk = lane >> 4;
+    double av[K / 4], bv[K / 4];
+#pragma unroll
+    for (int s = 0; s < K / 4; ++s) {
+        av[s] = pa[li * AI + (4 * s + lk) * AK];
+        bv[s] = pb[(4 * s + lk) * BK + li * BJ];
+    }
+#pragma unroll
+    for (int s = 0; s < K / 4; ++s) acc = mfma64(av[s], bv[s], acc);
+    return acc;
+}
+
+// row of component r of a D tile, relative to the tile (its column is lane % 16)
+__device__ __forceinline__ int drow(int r, int lane) { return 4 * r + (lane >> 4); }
+
+// Per-token inputs of a walk lane, slot n, tokens t0 .. t0 + TPG - 1 of a chunk
+// (t0 = gq TPG), as loaded (fp32); tokens past the sequence end (j >= nv) read as
+// the identity step.  The loads are unconditional, at token 0 for those tokens, so
+// that they can all be in flight at once.
+template <int DK, int TPG, bool TI>
+struct WalkIn {
+    float a[TPG], p[TPG], k[TPG], q[TPG], r[TPG];
+    int nv;
+    double ca, cp;   // time-invariant gates (TI)
+    __device__ void load(const float* ga, const float* gp, const float* gk, const float* gq, const float* gr,
+                         size_t tok0, int H, int h, int n, int t0, int nt) {
+        nv = min(max(nt - t0, 0), TPG);
+#pragma unroll
+        for (int j = 0; j < TPG; ++j) {
+            const int ts = t0 + j < nt ? t0 + j : 0;
+            const size_t e = ((tok0 + ts) * H + h) * DK + n;
+            if constexpr (!TI) {
+                a[j] = ga[e];
+                p[j] = gp[e];
+            }
+            k[j] = gk[e];
+            q[j] = gq[e];
+            r[j] = gr[(tok0 + ts) * H + h];
+        }
+    }
+    __device__ double A(int j) const { return j < nv ? (TI ? ca : (double)a[j]) : 1.0; }
+    __device__ double P(int j) const { return j < nv ? (TI ? cp : (double)p[j]) : 0.0; }
+    __device__ double K(int j) const { return j < nv ? (double)k[j] : 0.0; }
+    __device__ double Q(int j) const { return j < nv ? (double)q[j] : 0.0; }
+    __device__ double R(int j) const { return j < nv ? (double)r[j] : 0.0; }
+};
+
+// The 2x2 transfer of a lane's tokens (the images of (1, 0) and (0, 1) under the
+// homogeneous precision map) and the product of abar, into qs[gq][5][DK].
+template <int DK, int TPG, bool TI>
+__device__ __forceinline__ void group_transfer(const WalkIn<DK, TPG, TI>& in, double* qs, int gq, int n) {
+    double m00 = 1.0, m10 = 0.0, m01 = 0.0, m11 = 1.0, aq = 1.0;
+#pragma unroll
+    for (int j = 0; j < TPG; ++j) {
+        const double av = in.A(j), kv = in.K(j);
+        const double a2 = av * av, phi = kv * kv * in.R(j);
+        const double z0 = fma(in.P(j), m00, a2 * m10), z1 = fma(in.P(j), m01, a2 * m11);
+        m00 = fma(phi, z0, m00);
+        m01 = fma(phi, z1, m01);
+        m10 = z0;
+        m11 = z1;
+        aq *= av;
+    }
+    qs[(gq * 5 + 0) * DK + n] = m00;
+    qs[(gq * 5 + 1) * DK + n] = m10;
+    qs[(gq * 5 + 2) * DK + n] = m01;
+    qs[(gq * 5 + 3) * DK + n] = m11;
+    qs[(gq * 5 + 4) * DK + n] = aq;
+}
+
+// (x, z, A) before the lane's first token: the transfers of the earlier groups
+// applied to the chunk start (lam, 1, 1).
+template <int DK>
+__device__ __forceinline__ void chain_start(const double* qs, int gq, int n, double lam, double& x, double& z,
+                                            double& A) {
+    x = lam;
+    z = 1.0;
+    A = 1.0;
+    for (int g2 = 0; g2 < gq; ++g2) {
+        const double m00 = qs[(g2 * 5 + 0) * DK + n], m10 = qs[(g2 * 5 + 1) * DK + n];
+        const double m01 = qs[(g2 * 5 + 2) * DK + n], m11 = qs[(g2 * 5 + 3) * DK + n];
+        const double xn = fma(m00, x, m01 * z), zn = fma(m10, x, m11 * z);
+        x = xn;
+        z = zn;
+        A *= qs[(g2 * 5 + 4) * DK + n];
+    }
+}
+
+// ============================================================================ forward
+template <int DK, int DV, bool TI>
+__global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double* saved_lam, double* saved_H) {
+    constexpr int C = kC64, G = kNT64 / DK, TPG = C / G;
+    constexpr int PQ = DK + 1, PV = DV + 1, PS = C + 1;
+    constexpr int NTD = DV / 16, NTN = DK / 16, NTT = C / 16;
+    constexpr int NVE = C * DV / kNT64;   // value elements per thread and chunk
+    __shared__ double sQp[C * PQ], sKn[C * PQ], sV[C * PV], sS[C * PS], sH[DK * PV], sW[C * PQ];
+    __shared__ double qs[G * 5 * DK];
+    __shared__ double sLam[2 * DK], sPC[DK];
+
+    const int bh = blockIdx.x, b = bh / s.H, h = bh % s.H, H = s.H, T = s.T;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = tid % DK, gq = tid / DK;
+    const int nchunk = (T + C - 1) / C;
+    const size_t seq0 = (size_t)b * T;
+    const float* fq = static_cast<const float*>(g.q);
+    const float* fk = static_cast<const float*>(g.k);
+    const float* fv = static_cast<const float*>(g.v);
+    const float* fa = static_cast<const float*>(g.a);
+    const float* fp = static_cast<const float*>(g.p);
+    const float* fr = static_cast<const float*>(g.r);
+    float* fy = static_cast<float*>(g.y);
+
+    double ca = 0.0, cp = 0.0;   // time-invariant gates of slot n
+    if constexpr (TI) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], ca, cp);
+
+    // this wave's state tile (tn, td) = H[16 tn .. + 15][16 td .. + 15], if any
+    const bool hown = wave < NTN * NTD;
+    const int tn = wave / NTD, td = wave % NTD;
+    d4 Hs = zero_d4();
+    if (hown && g.eta0)
+        for (int r = 0; r < 4; ++r)
+            Hs[r] = g.eta0[((size_t)bh * DK + 16 * tn + drow(r, lane)) * DV + 16 * td + (lane & 15)];
+    // the readout tile (ti, tdy) of this wave, if any
+    const bool yown = wave < NTT * NTD;
+    const int ti = wave / NTD, tdy = wave % NTD;
+
+    if (tid < DK) sLam[tid] = g.lam0 ? (double)g.lam0[(size_t)bh * DK + tid] : 1.0;
+    double chk = 0.0;   // range check: sum of Qp Kn over the lane's tokens
+
+    // a chunk's inputs, fetched one chunk ahead
+    struct Pre {
+        WalkIn<DK, TPG, TI> w;
+        float v[NVE];
+    };
+    auto fetch = [&](Pre& P, int cn) {
+        const int nt = min(C, T - cn * C);
+        const size_t tok0 = seq0 + (size_t)cn * C;
+        P.w.load(fa, fp, fk, fq, fr, tok0, H, h, n, gq * TPG, nt);
+#pragma unroll
+        for (int m = 0; m < NVE; ++m) {
+            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
+            P.v[m] = fv[((tok0 + (t < nt ? t : 0)) * H + h) * DV + d];
+        }
+    };
+
+    auto round = [&](int c, Pre& cur, Pre& nxt) {
+        const int nt = min(C, T - c * C);
+        const size_t tok0 = seq0 + (size_t)c * C;
+        const double* lam_s = sLam + (c & 1) * DK;
+        cur.w.ca = ca;
+        cur.w.cp = cp;
+        // ---- this chunk's values and its start state into LDS (the state also into the
+        // saved context), the walk lanes' transfers; then the next chunk's fetch
+#pragma unroll
+        for (int m = 0; m < NVE; ++m) {
+            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
+            sV[t * PV + d] = t < nt ? (double)cur.v[m] : 0.0;
+        }
+        if (hown)
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * tn + drow(r, lane), col = 16 * td + (lane & 15);
+                sH[row * PV + col] = Hs[r];
+                if (saved_H) saved_H[(((size_t)bh * (nchunk + 1) + c) * DK + row) * DV + col] = Hs[r];
+            }
+        group_transfer(cur.w, qs, gq, n);
+        if (c + 1 < nchunk) fetch(nxt, c + 1);
+        __syncthreads();   // transfers, values, state in; lam_s visible
+
+        // ---- the lane's own tokens from the chained start
+        const double lam0c = lam_s[n];
+        if (saved_lam && gq == 0) saved_lam[((size_t)bh * nchunk + c) * DK + n] = lam0c;
+        double x, z, A;
+        chain_start<DK>(qs, gq, n, lam0c, x, z, A);
+#pragma unroll
+        for (int j = 0; j < TPG; ++j) {
+            const int t = gq * TPG + j;
+            const double av = cur.w.A(j), kv = cur.w.K(j), qv = cur.w.Q(j);
+            const double kr = kv * cur.w.R(j);
+            const double zn = fma(cur.w.P(j), x, av * av * z);
+            const double xn = fma(kr * kv, zn, x);
+            const double An = A * av;
+            const double R = rcpa(xn * An);
+            const double AR = An * R;            // 1 / x_t
+            const double qp = qv * An * AR;      // q A_t / x_t
+            const double kn = kr * zn * (xn * R);   // k r z_t / A_t
+            chk = fma(qp, kn, chk);
+            sQp[t * PQ + n] = qp;
+            sKn[t * PQ + n] = kn;
+            sW[t * PQ + n] = qv * qv * zn * AR;   // q^2 / lam_t
+            x = xn;
+            z = zn;
+            A = An;
+        }
+        if (gq == G - 1) {   // the last group ends at the chunk end
+            const double iz = rcpa(z);
+            sLam[((c + 1) & 1) * DK + n] = x * iz;
+            sPC[n] = A * iz;
+        }
+        __syncthreads();   // Qp, Kn, q^2 / lam, P_C in
+
+        // ---- S = M(Qp Kn^T): tiles (0,0), (1,0), (1,1) on waves 0..2, wave 1 also the zero tile
+        if (wave < 3) {
+            const int si = wave == 0 ? 0 : 1, sj = wave == 2 ? 1 : 0;
+            d4 acc = tile_mm<DK, PQ, 1, 1, PQ>(zero_d4(), sQp + 16 * si * PQ, sKn + 16 * sj * PQ, lane);
+            for (int r = 0; r < 4; ++r) {
+                const int i = drow(r, lane), j = lane & 15;
+                sS[(16 * si + i) * PS + 16 * sj + j] = (si == sj && j > i) ? 0.0 : acc[r];
+            }
+            if (si != sj)
+                for (int r = 0; r < 4; ++r) sS[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
+        }
+        // ---- the readout's state part, Qp H0, and the state update, diag(P_C) (H0 + Kn^T V)
+        d4 yacc = zero_d4();
+        if (yown) yacc = tile_mm<DK, PQ, 1, PV, 1>(yacc, sQp + 16 * ti * PQ, sH + 16 * tdy, lane);
+        if (hown) {
+            Hs = tile_mm<C, 1, PQ, PV, 1>(Hs, sKn + 16 * tn, sV + 16 * td, lane);
+            for (int r = 0; r < 4; ++r) Hs[r] *= sPC[16 * tn + drow(r, lane)];
+        }
+        __syncthreads();   // S in
+
+        // ---- y = S V + Qp H0, and yvar
+        if (yown) {
+            yacc = tile_mm<C, PS, 1, PV, 1>(yacc, sS + 16 * ti * PS, sV + 16 * tdy, lane);
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * ti + drow(r, lane);
+                if (t < nt) fy[((tok0 + t) * H + h) * DV + 16 * tdy + (lane & 15)] = (float)yacc[r];
+            }
+        }
+        if (g.yvar && tid < nt) {
+            double acc = 0.0;
+#pragma unroll
+            for (int m = 0; m < DK; ++m) acc += sW[tid * PQ + m];
+            g.yvar[(tok0 + tid) * H + h] = (float)acc;
+        }
+        __syncthreads();   // LDS free for the next chunk
+    };
+
+    Pre P0, P1;
+    if (nchunk > 0) fetch(P0, 0);
+    for (int c = 0; c < nchunk; c += 2) {
+        round(c, P0, P1);
+        if (c + 1 < nchunk) round(c + 1, P1, P0);
+    }
+
+    // ---- the final belief
+    const double* lam_e = sLam + (nchunk & 1) * DK;
+    if (g.lamT && tid < DK) g.lamT[(size_t)bh * DK + tid] = (float)lam_e[tid];
+    if (hown)
+        for (int r = 0; r < 4; ++r) {
+            const int row = 16 * tn + drow(r, lane), col = 16 * td + (lane & 15);
+            if (g.etaT) g.etaT[((size_t)bh * DK + row) * DV + col] = (float)Hs[r];
+            if (saved_H) saved_H[(((size_t)bh * (nchunk + 1) + nchunk) * DK + row) * DV + col] = Hs[r];
+        }
+    if (g.range_flag && !(fabs(chk) <= 1.0e300)) *g.range_flag = 1;
+}
+
+// ============================================================================ backward
+template <int DK, int DV, bool TI>
+__global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const double* saved_lam,
+                                                      const double* saved_H) {
+    constexpr int C = kC64, G = kNT64 / DK, TPG = C / G;
+    constexpr int PQ = DK + 1, PV = DV + 1, PS = C + 1;
+    constexpr int NTD = DV / 16, NTN = DK / 16, NTT = C / 16;
+    constexpr int NVE = C * DV / kNT64, NHE = DK * DV / kNT64;
+    __shared__ double sQp[C * PQ], sKn[C * PQ], sV[C * PV], sDY[C * PV], sS[C * PS], sB[C * PS];
+    __shared__ double sH0[DK * PV], sGs[DK * PV], sX[C * PQ], sY[C * PQ], sDR[C * PQ];
+    __shared__ double qs[G * 5 * DK];
+    __shared__ double sLam[DK], sPC[DK], sCar[2 * 2 * DK];   // carries (c, S) by round parity
+
+    const int bh = blockIdx.x, b = bh / s.H, h = bh % s.H, H = s.H, T = s.T;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = tid % DK, gq = tid / DK;
+    const int nchunk = (T + C - 1) / C;
+    const size_t seq0 = (size_t)b * T;
+    const float* fq = static_cast<const float*>(g.q);
+    const float* fk = static_cast<const float*>(g.k);
+    const float* fv = static_cast<const float*>(g.v);
+    const float* fa = static_cast<const float*>(g.a);
+    const float* fp = static_cast<const float*>(g.p);
+    const float* fr = static_cast<const float*>(g.r);
+    const float* fdy = static_cast<const float*>(g.dy);
+    float* gdq = static_cast<float*>(g.dq);
+    float* gdk = static_cast<float*>(g.dk);
+    float* gdv = static_cast<float*>(g.dv);
+    float* gda = static_cast<float*>(g.da);
+    float* gdp = static_cast<float*>(g.dp);
+    float* gdr = static_cast<float*>(g.dr);
+
+    double ca = 0.0, cp = 0.0;
+    if constexpr (TI) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], ca, cp);
+    double sum_da = 0.0, sum_dp = 0.0;   // OU gates: the lane's sums of the gate gradients
+
+    // this wave's adjoint tile (tn, td) of G, if any
+    const bool gown = wave < NTN * NTD;
+    const int tn = wave / NTD, td = wave % NTD;
+    d4 Gt = zero_d4();
+    if (gown && g.detaT)
+        for (int r = 0; r < 4; ++r)
+            Gt[r] = g.detaT[((size_t)bh * DK + 16 * tn + drow(r, lane)) * DV + 16 * td + (lane & 15)];
+    // carries at the sequence end: c = dlamT, S = sum_d detaT H_T
+    if (tid < DK) {
+        double st = 0.0;
+        if (g.detaT) {
+            const double* HT = saved_H + (((size_t)bh * (nchunk + 1) + nchunk) * DK + tid) * DV;
+            const float* dT = g.detaT + ((size_t)bh * DK + tid) * DV;
+            for (int d = 0; d < DV; ++d) st = fma((double)dT[d], HT[d], st);
+        }
+        sCar[(nchunk & 1) * 2 * DK + tid] = g.dlamT ? (double)g.dlamT[(size_t)bh * DK + tid] : 0.0;
+        sCar[(nchunk & 1) * 2 * DK + DK + tid] = st;
+    }
+    double chk = 0.0;
+
+    // a chunk's inputs, output gradients and saved start (lam, state), fetched one chunk ahead
+    struct Pre {
+        WalkIn<DK, TPG, TI> w;
+        float gv[TPG], v[NVE], dy[NVE];
+        double h0[NHE], lam;
+    };
+    auto fetch = [&](Pre& P, int cn) {
+        const int nt = min(C, T - cn * C);
+        const size_t tok0 = seq0 + (size_t)cn * C;
+        P.w.load(fa, fp, fk, fq, fr, tok0, H, h, n, gq * TPG, nt);
+#pragma unroll
+        for (int j = 0; j < TPG; ++j) {
+            const int t = gq * TPG + j;
+            P.gv[j] = g.dyvar ? g.dyvar[(tok0 + (t < nt ? t : 0)) * H + h] : 0.f;
+        }
+#pragma unroll
+        for (int m = 0; m < NVE; ++m) {
+            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
+            const size_t gi = ((tok0 + (t < nt ? t : 0)) * H + h) * DV + d;
+            P.v[m] = fv[gi];
+            P.dy[m] = fdy[gi];
+        }
+#pragma unroll
+        for (int m = 0; m < NHE; ++m) P.h0[m] = saved_H[((size_t)bh * (nchunk + 1) + cn) * DK * DV + tid + kNT64 * m];
+        P.lam = saved_lam[((size_t)bh * nchunk + cn) * DK + n];
+    };
+
+    auto round = [&](int c, Pre& cur, Pre& nxt) {
+        const int nt = min(C, T - c * C);
+        const size_t tok0 = seq0 + (size_t)c * C;
+        cur.w.ca = ca;
+        cur.w.cp = cp;
+        // ---- stage the chunk into LDS, the walk lanes' transfers; then the previous chunk's fetch
+#pragma unroll
+        for (int m = 0; m < NVE; ++m) {
+            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
+            sV[t * PV + d] = t < nt ? (double)cur.v[m] : 0.0;
+            sDY[t * PV + d] = t < nt ? (double)cur.dy[m] : 0.0;
+        }
+#pragma unroll
+        for (int m = 0; m < NHE; ++m) {
+            const int e = tid + kNT64 * m;
+            sH0[(e / DV) * PV + e % DV] = cur.h0[m];
+        }
+        if (tid < DK) sLam[tid] = cur.lam;
+        double gv[TPG];
+#pragma unroll
+        for (int j = 0; j < TPG; ++j) gv[j] = gq * TPG + j < nt ? (double)cur.gv[j] : 0.0;
+        group_transfer(cur.w, qs, gq, n);
+        if (c >= 1) fetch(nxt, c - 1);
+        __syncthreads();
+
+        // ---- the walk over the lane's tokens: Qp, Kn, and what the adjoint walk needs
+        double lam_p[TPG], P_t[TPG], iP_t[TPG], il_t[TPG], rho[TPG], irho[TPG], ia[TPG];
+        {
+            double x, z, A;
+            chain_start<DK>(qs, gq, n, sLam[n], x, z, A);
+            double izp = rcpa(z);
+#pragma unroll
+            for (int j = 0; j < TPG; ++j) {
+                const int t = gq * TPG + j;
+                const double av = cur.w.A(j), kv = cur.w.K(j);
+                const double kr = kv * cur.w.R(j);
+                const double zn = fma(cur.w.P(j), x, av * av * z);
+                const double xn = fma(kr * kv, zn, x);
+                const double An = A * av;
+                const double R = rcpa(xn * An), iz = rcpa(zn);
+                const double AR = An * R, XR = xn * R;   // 1 / x_t, 1 / A_t
+                const double qp = cur.w.Q(j) * An * AR, kn = kr * zn * XR;
+                chk = fma(qp, kn, chk);
+                sQp[t * PQ + n] = qp;
+                sKn[t * PQ + n] = kn;
+                lam_p[j] = x * izp;
+                P_t[j] = An * iz;
+                iP_t[j] = zn * XR;
+                il_t[j] = zn * AR;
+                rho[j] = z * iz;
+                irho[j] = zn * izp;
+                ia[j] = A * XR;
+                izp = iz;
+                x = xn;
+                z = zn;
+                A = An;
+            }
+            if (gq == G - 1) sPC[n] = A * rcpa(z);
+        }
+        __syncthreads();   // Qp, Kn, P_C in
+
+        // ---- S = M(Qp Kn^T) and B = M(dY V^T): six tiles over the four waves (the tiles (1,0)
+        // also write the zero tile above the diagonal); Gs = diag(P_C) G
+        for (int job = wave; job < 6; job += 4) {
+            const int kind = job / 3, tt = job % 3;   // kind 0: S, 1: B; tiles (0,0), (1,0), (1,1)
+            const int si = tt == 0 ? 0 : 1, sj = tt == 2 ? 1 : 0;
+            d4 acc = kind == 0 ? tile_mm<DK, PQ, 1, 1, PQ>(zero_d4(), sQp + 16 * si * PQ, sKn + 16 * sj * PQ, lane)
+                               : tile_mm<DV, PV, 1, 1, PV>(zero_d4(), sDY + 16 * si * PV, sV + 16 * sj * PV, lane);
+            double* dst = kind == 0 ? sS : sB;
+            for (int r = 0; r < 4; ++r) {
+                const int i = drow(r, lane), j = lane & 15;
+                dst[(16 * si + i) * PS + 16 * sj + j] = (si == sj && j > i) ? 0.0 : acc[r];
+            }
+            if (si != sj)
+                for (int r = 0; r < 4; ++r) dst[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
+        }
+        if (gown)
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * tn + drow(r, lane);
+                Gt[r] *= sPC[row];
+                sGs[row * PV + 16 * td + (lane & 15)] = Gt[r];
+            }
+        __syncthreads();   // S, B, Gs in
+
+        // ---- dV = S^T dY + Kn Gs (tiles (tj, td)); X = dY H0^T + B Kn and Y = B^T Qp + V Gs^T
+        // (tiles (t, tn)); G' = Qp^T dY + Gs (this wave's tile)
+        for (int job = wave; job < NTT * NTD; job += 4) {
+            const int tj = job / NTD, dd = job % NTD;
+            d4 acc = tile_mm<C, 1, PS, PV, 1>(zero_d4(), sS + 16 * tj, sDY + 16 * dd, lane);
+            acc = tile_mm<DK, PQ, 1, PV, 1>(acc, sKn + 16 * tj * PQ, sGs + 16 * dd, lane);
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * tj + drow(r, lane);
+                if (t < nt) gdv[((tok0 + t) * H + h) * DV + 16 * dd + (lane & 15)] = (float)acc[r];
+            }
+        }
+        for (int job = wave; job < NTT * NTN; job += 4) {
+            const int tq = job / NTN, nn = job % NTN;
+            d4 xa = tile_mm<DV, PV, 1, 1, PV>(zero_d4(), sDY + 16 * tq * PV, sH0 + 16 * nn * PV, lane);
+            xa = tile_mm<C, PS, 1, PQ, 1>(xa, sB + 16 * tq * PS, sKn + 16 * nn, lane);
+            d4 ya = tile_mm<C, 1, PS, PQ, 1>(zero_d4(), sB + 16 * tq, sQp + 16 * nn, lane);
+            ya = tile_mm<DV, PV, 1, 1, PV>(ya, sV + 16 * tq * PV, sGs + 16 * nn * PV, lane);
+            for (int r = 0; r < 4; ++r) {
+                const int t = 16 * tq + drow(r, lane), col = 16 * nn + (lane & 15);
+                sX[t * PQ + col] = xa[r];
+                sY[t * PQ + col] = ya[r];
+            }
+        }
+        if (gown) Gt = tile_mm<C, 1, PQ, PV, 1>(Gt, sQp + 16 * tn, sDY + 16 * td, lane);
+        __syncthreads();   // X, Y in
+
+        // ---- adjoint pass 1: the lane's tokens in reverse, each the affine step
+        //   (c, S) -> (alpha (c - w) - beta (S + u), S + u),
+        // composed into c_out = Am c_in + Bm S_in + Cm, S_out = S_in + Dm
+        double u_[TPG], w_[TPG], al_[TPG], be_[TPG], dqt_[TPG], dkh_[TPG];
+        double Am = 1.0, Bm = 0.0, Cm = 0.0, Dm = 0.0;
+#pragma unroll
+        for (int j = TPG - 1; j >= 0; --j) {
+            const int t = gq * TPG + j;
+            const double dqt = P_t[j] * sX[t * PQ + n], dkh = sY[t * PQ + n] * iP_t[j];
+            const double qv = cur.w.Q(j), av = cur.w.A(j);
+            const double kh = cur.w.K(j) * cur.w.R(j);
+            const double qi = qv * il_t[j];
+            const double u = qi * dqt - kh * dkh;
+            const double w = qi * fma(qv, gv[j], dqt) * il_t[j];
+            const double al = av * av * rho[j] * rho[j], be = cur.w.P(j) * rho[j];
+            u_[j] = u;
+            w_[j] = w;
+            al_[j] = al;
+            be_[j] = be;
+            dqt_[j] = dqt;
+            dkh_[j] = dkh;
+            Cm = al * Cm - be * Dm - (al * w + be * u);
+            Bm = al * Bm - be;
+            Am = al * Am;
+            Dm = Dm + u;
+        }
+        qs[(gq * 4 + 0) * DK + n] = Am;   // the transfers were last read before two barriers
+        qs[(gq * 4 + 1) * DK + n] = Bm;
+        qs[(gq * 4 + 2) * DK + n] = Cm;
+        qs[(gq * 4 + 3) * DK + n] = Dm;
+        __syncthreads();
+
+        // ---- pass 2: carries into the lane's group (through the later groups) and out of the
+        // chunk, then the gradients of its tokens
+        double cc, SS;
+        {
+            const double* car = sCar + ((c + 1) & 1) * 2 * DK;
+            double cT = car[n], ST = car[DK + n];
+            cc = cT;
+            SS = ST;
+            for (int g2 = G - 1; g2 >= 0; --g2) {
+                if (g2 == gq) {
+                    cc = cT;
+                    SS = ST;
+                }
+                const double A2 = qs[(g2 * 4 + 0) * DK + n], B2 = qs[(g2 * 4 + 1) * DK + n];
+                const double C2 = qs[(g2 * 4 + 2) * DK + n], D2 = qs[(g2 * 4 + 3) * DK + n];
+                const double cn = fma(A2, cT, fma(B2, ST, C2));
+                ST += D2;
+                cT = cn;
+            }
+            if (gq == 0) {
+                sCar[(c & 1) * 2 * DK + n] = cT;
+                sCar[(c & 1) * 2 * DK + DK + n] = ST;
+            }
+        }
+#pragma unroll
+        for (int j = TPG - 1; j >= 0; --j) {
+            const int t = gq * TPG + j;
+            SS += u_[j];
+            const double gl = cc - w_[j];
+            const double kv = cur.w.K(j), rv = cur.w.R(j), av = cur.w.A(j), qv = cur.w.Q(j);
+            const double r2 = rho[j] * rho[j];
+            const double dkv = fma(2.0 * kv * rv, gl, rv * dkh_[j]);
+            const double drho = fma(gl, lam_p[j], SS * irho[j]);
+            const double dav = fma(-2.0 * av * r2, drho, SS * ia[j]);
+            const double dpv = -lam_p[j] * r2 * drho;
+            const double dqv = fma(2.0 * qv, gv[j], dqt_[j]) * il_t[j];
+            sDR[t * PQ + n] = fma(kv * kv, gl, kv * dkh_[j]);
+            cc = fma(al_[j], gl, -be_[j] * SS);
+            if (t < nt) {
+                const size_t e = ((tok0 + t) * H + h) * DK + n;
+                gdq[e] = (float)dqv;
+                gdk[e] = (float)dkv;
+                if constexpr (TI) {
+                    sum_da += dav;
+                    sum_dp += dpv;
+                } else {
+                    gda[e] = (float)dav;
+                    gdp[e] = (float)dpv;
+                }
+            }
+        }
+        __syncthreads();   // dr terms in
+        if (tid < nt) {
+            double acc = 0.0;
+#pragma unroll
+            for (int m = 0; m < DK; ++m) acc += sDR[tid * PQ + m];
+            gdr[(tok0 + tid) * H + h] = (float)acc;
+        }
+    };
+
+    Pre P0, P1;
+    if (nchunk > 0) fetch(P0, nchunk - 1);
+    for (int c = nchunk - 1; c >= 0; c -= 2) {
+        round(c, P0, P1);
+        if (c >= 1) round(c - 1, P1, P0);
+    }
+
+    // ---- gradients of the initial belief, and the OU gate sums
+    if (g.dlam0 && tid < DK) g.dlam0[(size_t)bh * DK + tid] = (float)sCar[tid];
+    if (g.deta0 && gown)
+        for (int r = 0; r < 4; ++r)
+            g.deta0[((size_t)bh * DK + 16 * tn + drow(r, lane)) * DV + 16 * td + (lane & 15)] = (float)Gt[r];
+    if constexpr (TI) {
+        double* part = static_cast<double*>(g.ou_part);
+        const size_t np = (size_t)s.B * s.H * DK;
+        // the slot's sum over all token groups (tids n, n + DK, ...), through LDS
+        __syncthreads();
+        sDR[gq * PQ + n] = sum_da;
+        sX[gq * PQ + n] = sum_dp;
+        __syncthreads();
+        if (tid < DK) {
+            double sa = 0.0, sp = 0.0;
+            for (int g2 = 0; g2 < G; ++g2) {
+                sa += sDR[g2 * PQ + tid];
+                sp += sX[g2 * PQ + tid];
+            }
+            part[(size_t)bh * DK + tid] = sa;
+            part[np + (size_t)bh * DK + tid] = sp;
+        }
+    }
+    if (g.range_flag && !(fabs(chk) <= 1.0e300)) *g.range_flag = 1;
+}
+
+template <int DK, int DV>
+hipError_t launch_fwd64(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st) {
+    double* slam = static_cast<double*>(saved);
+    double* sH = slam ? slam + (size_t)s.B * s.H * ((s.T + kC64 - 1) / kC64) * DK : nullptr;
+    const dim3 grid((unsigned)(s.B * s.H));
+    if (a.ou_a)
+        hipLaunchKernelGGL((fwd64_kernel<DK, DV, true>), grid, dim3(kNT64), 0, st, s, a, slam, sH);
+    else
+        hipLaunchKernelGGL((fwd64_kernel<DK, DV, false>), grid, dim3(kNT64), 0, st, s, a, slam, sH);
+    return hipGetLastError();
+}
+
+template <int DK, int DV>
+hipError_t launch_bwd64(const Shape& s, const BwdArgs& a, const void* saved, hipStream_t st) {
+    if (!saved) return hipErrorInvalidValue;
+    const double* slam = static_cast<const double*>(saved);
+    const double* sH = slam + (size_t)s.B * s.H * ((s.T + kC64 - 1) / kC64) * DK;
+    const dim3 grid((unsigned)(s.B * s.H));
+    if (a.ou_a)
+        hipLaunchKernelGGL((bwd64_kernel<DK, DV, true>), grid, dim3(kNT64), 0, st, s, a, slam, sH);
+    else
+        hipLaunchKernelGGL((bwd64_kernel<DK, DV, false>), grid, dim3(kNT64), 0, st, s, a, slam, sH);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+bool c64_supported(const Shape& s) { return !s.bf16 && (s.dk == 16 || s.dk == 32) && (s.dv == 16 || s.dv == 32); }
+
+size_t c64_saved_bytes(const Shape& s) {
+    const size_t nchunk = (size_t)(s.T + kC64 - 1) / kC64;
+    return (size_t)s.B * s.H * s.dk * (nchunk + (nchunk + 1) * (size_t)s.dv) * sizeof(double);
+}
+
+#define KLA_C64_CASES(F, ...)                                    \
+    if (s.dk == 16 && s.dv == 16) return F<16, 16>(__VA_ARGS__); \
+    if (s.dk == 16 && s.dv == 32) return F<16, 32>(__VA_ARGS__); \
+    if (s.dk == 32 && s.dv == 16) return F<32, 16>(__VA_ARGS__); \
+    if (s.dk == 32 && s.dv == 32) return F<32, 32>(__VA_ARGS__);
+
+hipError_t launch_forward_c64(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st) {
+    KLA_C64_CASES(launch_fwd64, s, a, saved, st)
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_backward_c64(const Shape& s, const BwdArgs& a, const void* saved, hipStream_t st) {
+    KLA_C64_CASES(launch_bwd64, s, a, saved, st)
+    return hipErrorInvalidValue;
+}
+
+}  // namespace kla

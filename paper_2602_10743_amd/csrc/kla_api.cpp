@@ -95,7 +95,8 @@ size_t kla_forward_workspace(const kla_desc* desc) {
 size_t kla_saved_bytes(const kla_desc* desc) {
     if (check_desc(desc) != KLA_OK) return 0;
     const kla::Shape s = shape_of(desc);
-    return saves_chunked(s) ? kla::chunked_saved_bytes(s) : kla::recurrent_saved_bytes(s);
+    if (saves_chunked(s)) return kla::chunked_saved_bytes(s);
+    return kla::c64_supported(s) ? kla::c64_saved_bytes(s) : kla::recurrent_saved_bytes(s);
 }
 
 size_t kla_backward_workspace(const kla_desc* desc, int with_saved) {
@@ -107,6 +108,12 @@ size_t kla_backward_workspace(const kla_desc* desc, int with_saved) {
             const size_t elt = s.bf16 ? 2 : 4;
             bytes += round_up(kla::chunked_saved_bytes(s)) + round_up((size_t)s.B * s.T * s.H * s.dv * elt);
         }
+        return bytes;
+    }
+    if (kla::c64_supported(s)) {
+        size_t bytes = kAlign;
+        if (!with_saved)   // the context is recomputed: saved states plus a scratch output
+            bytes += round_up(kla::c64_saved_bytes(s)) + round_up((size_t)s.B * s.T * s.H * s.dv * sizeof(float));
         return bytes;
     }
     size_t bytes = kAlign + round_up(kla::backward_recurrent_workspace(s));
@@ -147,13 +154,17 @@ kla_status forward_impl(const kla_desc* desc, const kla::FwdArgs& a, bool ou, vo
     // without a saved context any forward kernel may run; with one, the kernel whose
     // layout the backward reads (saves_chunked)
     const bool chunked = saved ? saves_chunked(s) : kla::chunked_supported(s);
+    const bool c64 = kla::c64_supported(s);
     if (!saved && !ou && kla::forward_segments(s) > 1)
         e = kla::launch_forward_segmented(s, fa, static_cast<char*>(ws) + kAlign, stream);
+    else if (chunked)
+        e = kla::launch_forward_chunked(s, fa, saved, stream);
+    else if (c64)
+        e = kla::launch_forward_c64(s, fa, saved, stream);
     else
-        e = chunked ? kla::launch_forward_chunked(s, fa, saved, stream)
-                    : kla::launch_forward_recurrent(s, fa, saved, stream);
+        e = kla::launch_forward_recurrent(s, fa, saved, stream);
     if (e != hipSuccess) return KLA_ERR_HIP;
-    return check && chunked ? range_status(ws, stream) : KLA_OK;
+    return check && (chunked || c64) ? range_status(ws, stream) : KLA_OK;
 }
 
 int ou_parts(const kla::Shape& s) {
@@ -206,6 +217,17 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
             saved = ctx;
         }
         e = kla::launch_backward_chunked(s, a, saved, work, stream);
+    } else if (kla::c64_supported(s)) {
+        if (!saved) {
+            char* ctx = work;
+            void* yscratch = ctx + round_up(kla::c64_saved_bytes(s));
+            kla::FwdArgs f{a.q, a.k, a.v, a.a, a.p, a.r, a.lam0, a.eta0, yscratch, nullptr, nullptr, nullptr,
+                           a.ou_a, a.ou_p, a.ou_d, a.range_flag};
+            e = kla::launch_forward_c64(s, f, ctx, stream);
+            if (e != hipSuccess) return KLA_ERR_HIP;
+            saved = ctx;
+        }
+        e = kla::launch_backward_c64(s, a, saved, stream);
     } else {
         if (!saved) {   // the same forward kernel fills the context, so both ways agree bit for bit
             char* ctx = work + round_up(kla::backward_recurrent_workspace(s));
@@ -222,7 +244,7 @@ kla_status backward_impl(const kla_desc* desc, kla::BwdArgs a, bool ou, const vo
         e = kla::launch_ou_param_grads(s.H, s.dk, ou_parts(s), a.ou_part, ou_part_bytes(s) == sizeof(double), a.ou_a,
                                        a.ou_p, a.ou_d, da, dp, dd, stream);
     if (e != hipSuccess) return KLA_ERR_HIP;
-    return check && kla::chunked_bwd_supported(s) ? range_status(ws, stream) : KLA_OK;
+    return check && (kla::chunked_bwd_supported(s) || kla::c64_supported(s)) ? range_status(ws, stream) : KLA_OK;
 }
 
 kla_status decode_impl(int32_t S, int32_t H, int32_t dk, int32_t dv, int32_t dtype, const kla::DecodeArgs& a,

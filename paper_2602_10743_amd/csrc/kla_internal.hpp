@@ -62,6 +62,16 @@ hipError_t launch_backward_recurrent(const Shape& s, const BwdArgs& a, const voi
 size_t recurrent_ou_part_bytes(const Shape& s);
 hipError_t launch_decode_step(const Shape& s, const DecodeArgs& a, hipStream_t st);
 
+// Chunked fp64 path for fp32 storage with dk, dv in {16, 32}: the chunk form on fp64
+// MFMA.  Its saved context (c64_saved_bytes, fp64) is lam at every 32-token chunk
+// start [B*H][nchunk][dk], then the information state at every chunk start and after
+// the last token [B*H][nchunk+1][dk][dv]; the backward needs no other workspace and
+// leaves the OU parts as the token-recurrent one does (per batch row, fp64).
+bool c64_supported(const Shape& s);
+size_t c64_saved_bytes(const Shape& s);
+hipError_t launch_forward_c64(const Shape& s, const FwdArgs& a, void* saved, hipStream_t st);
+hipError_t launch_backward_c64(const Shape& s, const BwdArgs& a, const void* saved, hipStream_t st);
+
 // Chunked MFMA path (bf16 storage, dk >= 32).
 bool chunked_supported(const Shape& s);
 size_t chunked_saved_bytes(const Shape& s);

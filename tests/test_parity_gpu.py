@@ -65,6 +65,11 @@ SMALL = [  # B, T, H, dk, dv, dtype, dist
     # bf16 with dk >= 32 and dv = 16: chunked forward without a saved context, token-recurrent
     # backward (and forward, when the context is saved)
     (2, 70, 2, 64, 16, "bf16", "lm"),
+    # chunked fp64 path (fp32 inputs, dk and dv in {16, 32}): whole and partial chunks, one token
+    (2, 95, 2, 32, 32, "f32", "lm"),
+    (1, 64, 3, 32, 16, "f32", "c0"),
+    (2, 33, 1, 16, 32, "f32", "lm"),
+    (1, 1, 2, 32, 32, "f32", "c0"),
 ]
 
 
