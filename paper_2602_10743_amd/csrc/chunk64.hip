@@ -43,6 +43,7 @@
 // Saved context (c64_saved_bytes): lam at every chunk start [BH][nchunk][dk], then
 // the information state at every chunk start and after the last token
 // [BH][nchunk+1][dk][dv], fp64.
+#include "kla_buf.hpp"
 #include "kla_device.hpp"
 #include "kla_internal.hpp"
 
@@ -81,39 +82,82 @@ __device__ __forceinline__ d4 tile_mm(d4 acc, const double* pa, const double* pb
     return acc;
 }
 
+// Sum over the DK lanes of one walk group (DK = 32: a half wave, DK = 16: a DPP row),
+// valid in the group's last lane (n = DK - 1).
+template <int DK>
+__device__ __forceinline__ double slot_sum(double x) {
+    if constexpr (DK == 32) {
+        return half_sum(x);
+    } else {
+        x += dpp<0xB1, 0xf>(x);    // quad_perm [1,0,3,2]
+        x += dpp<0x4E, 0xf>(x);    // quad_perm [2,3,0,1]
+        x += dpp<0x141, 0xf>(x);   // row_half_mirror
+        x += dpp<0x140, 0xf>(x);   // row_mirror
+        return x;
+    }
+}
+
 // row of component r of a D tile, relative to the tile (its column is lane % 16)
 __device__ __forceinline__ int drow(int r, int lane) { return 4 * r + (lane >> 4); }
 
+__device__ __forceinline__ float bld32(rsrc_t r, uint32_t voff) {
+    return __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, voff, 0, 0));
+}
+
+// Stores through a buffer: a lane whose offset lies past the end stores nothing.
+__device__ __forceinline__ void bst32(rsrc_t r, uint32_t voff, float x) {
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, voff, 0, 0);
+}
+
+__device__ __forceinline__ void bst64(rsrc_t r, uint32_t voff, double x) {
+    typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+    __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, x), r, voff, 0, 0);
+}
+
+// Buffers over one chunk's rows of the per-token tensors of head h: [t][H][DK] rows
+// (abar, pbar, k, q) and [t][H] (r), each ending at the chunk's last valid token, so
+// that tokens past the sequence end read as zero.
+struct ChunkBufs {
+    rsrc_t a, p, k, q, r;
+    __device__ ChunkBufs(const float* ga, const float* gp, const float* gk, const float* gq, const float* gr,
+                         size_t tok0, int H, int h, int DK, int nt) {
+        const size_t e0 = (tok0 * H + h) * DK;
+        const uint32_t bytes = (uint32_t)((nt - 1) * H * DK + DK) * 4;
+        a = make_rsrc(ga ? ga + e0 : gk, ga ? bytes : 0u);
+        p = make_rsrc(gp ? gp + e0 : gk, gp ? bytes : 0u);
+        k = make_rsrc(gk + e0, bytes);
+        q = make_rsrc(gq + e0, bytes);
+        r = make_rsrc(gr + tok0 * H + h, (uint32_t)((nt - 1) * H + 1) * 4);
+    }
+};
+
 // Per-token inputs of a walk lane, slot n, tokens t0 .. t0 + TPG - 1 of a chunk
-// (t0 = gq TPG), as loaded (fp32); tokens past the sequence end (j >= nv) read as
-// the identity step.  The loads are unconditional, at token 0 for those tokens, so
-// that they can all be in flight at once.
+// (t0 = gq TPG), as loaded (fp32).  Tokens past the sequence end (j >= nv) read as
+// zeros, and abar as 1: the identity step.
 template <int DK, int TPG, bool TI>
 struct WalkIn {
     float a[TPG], p[TPG], k[TPG], q[TPG], r[TPG];
     int nv;
     double ca, cp;   // time-invariant gates (TI)
-    __device__ void load(const float* ga, const float* gp, const float* gk, const float* gq, const float* gr,
-                         size_t tok0, int H, int h, int n, int t0, int nt) {
+    __device__ void load(const ChunkBufs& cb, int H, int n, int t0, int nt) {
         nv = min(max(nt - t0, 0), TPG);
 #pragma unroll
         for (int j = 0; j < TPG; ++j) {
-            const int ts = t0 + j < nt ? t0 + j : 0;
-            const size_t e = ((tok0 + ts) * H + h) * DK + n;
+            const uint32_t vo = (uint32_t)((t0 + j) * H * DK + n) * 4;
             if constexpr (!TI) {
-                a[j] = ga[e];
-                p[j] = gp[e];
+                a[j] = bld32(cb.a, vo);
+                p[j] = bld32(cb.p, vo);
             }
-            k[j] = gk[e];
-            q[j] = gq[e];
-            r[j] = gr[(tok0 + ts) * H + h];
+            k[j] = bld32(cb.k, vo);
+            q[j] = bld32(cb.q, vo);
+            r[j] = bld32(cb.r, (uint32_t)((t0 + j) * H) * 4);
         }
     }
     __device__ double A(int j) const { return j < nv ? (TI ? ca : (double)a[j]) : 1.0; }
-    __device__ double P(int j) const { return j < nv ? (TI ? cp : (double)p[j]) : 0.0; }
-    __device__ double K(int j) const { return j < nv ? (double)k[j] : 0.0; }
-    __device__ double Q(int j) const { return j < nv ? (double)q[j] : 0.0; }
-    __device__ double R(int j) const { return j < nv ? (double)r[j] : 0.0; }
+    __device__ double P(int j) const { return TI ? (j < nv ? cp : 0.0) : (double)p[j]; }
+    __device__ double K(int j) const { return (double)k[j]; }
+    __device__ double Q(int j) const { return (double)q[j]; }
+    __device__ double R(int j) const { return (double)r[j]; }
 };
 
 // The 2x2 transfer of a lane's tokens (the images of (1, 0) and (0, 1) under the
@@ -141,19 +185,22 @@ __device__ __forceinline__ void group_transfer(const WalkIn<DK, TPG, TI>& in, do
 
 // (x, z, A) before the lane's first token: the transfers of the earlier groups
 // applied to the chunk start (lam, 1, 1).
-template <int DK>
+template <int DK, int G>
 __device__ __forceinline__ void chain_start(const double* qs, int gq, int n, double lam, double& x, double& z,
                                             double& A) {
     x = lam;
     z = 1.0;
     A = 1.0;
-    for (int g2 = 0; g2 < gq; ++g2) {
+#pragma unroll
+    for (int g2 = 0; g2 < G - 1; ++g2) {   // every lane the same steps, applied while g2 < gq
         const double m00 = qs[(g2 * 5 + 0) * DK + n], m10 = qs[(g2 * 5 + 1) * DK + n];
         const double m01 = qs[(g2 * 5 + 2) * DK + n], m11 = qs[(g2 * 5 + 3) * DK + n];
+        const double aq = qs[(g2 * 5 + 4) * DK + n];
+        const bool use = g2 < gq;
         const double xn = fma(m00, x, m01 * z), zn = fma(m10, x, m11 * z);
-        x = xn;
-        z = zn;
-        A *= qs[(g2 * 5 + 4) * DK + n];
+        x = use ? xn : x;
+        z = use ? zn : z;
+        A = use ? A * aq : A;
     }
 }
 
@@ -164,7 +211,7 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
     constexpr int PQ = DK + 1, PV = DV + 1, PS = C + 1;
     constexpr int NTD = DV / 16, NTN = DK / 16, NTT = C / 16;
     constexpr int NVE = C * DV / kNT64;   // value elements per thread and chunk
-    __shared__ double sQp[C * PQ], sKn[C * PQ], sV[C * PV], sS[C * PS], sH[DK * PV], sW[C * PQ];
+    __shared__ double sQp[C * PQ], sKn[C * PQ], sV[C * PV], sS[C * PS], sH[DK * PV];
     __shared__ double qs[G * 5 * DK];
     __shared__ double sLam[2 * DK], sPC[DK];
 
@@ -185,15 +232,17 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
     double ca = 0.0, cp = 0.0;   // time-invariant gates of slot n
     if constexpr (TI) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], ca, cp);
 
-    // this wave's state tile (tn, td) = H[16 tn .. + 15][16 td .. + 15], if any
-    const bool hown = wave < NTN * NTD;
+    // this wave's state tile (tn, td) = H[16 tn .. + 15][16 td .. + 15], if any (at
+    // dk = dv = 32 every wave owns one state tile and one readout tile, known at compile time)
+    constexpr bool FULL = NTN * NTD == 4 && NTT * NTD == 4;
+    const bool hown = FULL || wave < NTN * NTD;
     const int tn = wave / NTD, td = wave % NTD;
     d4 Hs = zero_d4();
     if (hown && g.eta0)
         for (int r = 0; r < 4; ++r)
             Hs[r] = g.eta0[((size_t)bh * DK + 16 * tn + drow(r, lane)) * DV + 16 * td + (lane & 15)];
     // the readout tile (ti, tdy) of this wave, if any
-    const bool yown = wave < NTT * NTD;
+    const bool yown = FULL || wave < NTT * NTD;
     const int ti = wave / NTD, tdy = wave % NTD;
 
     if (tid < DK) sLam[tid] = g.lam0 ? (double)g.lam0[(size_t)bh * DK + tid] : 1.0;
@@ -207,32 +256,58 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
     auto fetch = [&](Pre& P, int cn) {
         const int nt = min(C, T - cn * C);
         const size_t tok0 = seq0 + (size_t)cn * C;
-        P.w.load(fa, fp, fk, fq, fr, tok0, H, h, n, gq * TPG, nt);
+        P.w.load(ChunkBufs(TI ? nullptr : fa, TI ? nullptr : fp, fk, fq, fr, tok0, H, h, DK, nt), H, n, gq * TPG, nt);
+        const rsrc_t rv = make_rsrc(fv + (tok0 * H + h) * DV, (uint32_t)((nt - 1) * H * DV + DV) * 4);
 #pragma unroll
         for (int m = 0; m < NVE; ++m) {
             const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
-            P.v[m] = fv[((tok0 + (t < nt ? t : 0)) * H + h) * DV + d];
+            P.v[m] = bld32(rv, (uint32_t)(t * H * DV + d) * 4);
+        }
+    };
+
+    // The outputs of a round (its y tile and yvar) are stored at the start of the next
+    // one, before that round's fetch: no store is then younger than a fetch, and the
+    // wait for a fetched chunk does not also wait for the stores of the round before.
+    float oy[4] = {0.f, 0.f, 0.f, 0.f}, oyv[TPG];   // oyv: yvar of the lane's tokens (lane n = DK - 1)
+    int oc = -1;   // the chunk they belong to (none: -1)
+    auto flush = [&]() {
+        if (oc < 0) return;
+        const int nt = min(C, T - oc * C);
+        const size_t tok0 = seq0 + (size_t)oc * C;
+        if (yown) {
+            const rsrc_t ry = make_rsrc(fy + (tok0 * H + h) * DV, (uint32_t)((nt - 1) * H * DV + DV) * 4);
+            for (int r = 0; r < 4; ++r)
+                bst32(ry, (uint32_t)((16 * ti + drow(r, lane)) * H * DV + 16 * tdy + (lane & 15)) * 4, oy[r]);
+        }
+        if (g.yvar) {   // tokens past the chunk's last one, and the other lanes, fall outside the buffer
+            const rsrc_t rw = make_rsrc(g.yvar + tok0 * H + h, (uint32_t)((nt - 1) * H + 1) * 4);
+#pragma unroll
+            for (int j = 0; j < TPG; ++j)
+                bst32(rw, n == DK - 1 ? (uint32_t)((gq * TPG + j) * H) * 4 : 0x7ffffff0u, oyv[j]);
         }
     };
 
     auto round = [&](int c, Pre& cur, Pre& nxt) {
         const int nt = min(C, T - c * C);
-        const size_t tok0 = seq0 + (size_t)c * C;
         const double* lam_s = sLam + (c & 1) * DK;
         cur.w.ca = ca;
         cur.w.cp = cp;
+        flush();
+        if (saved_lam && tid < DK) saved_lam[((size_t)bh * nchunk + c) * DK + tid] = lam_s[tid];
         // ---- this chunk's values and its start state into LDS (the state also into the
         // saved context), the walk lanes' transfers; then the next chunk's fetch
 #pragma unroll
         for (int m = 0; m < NVE; ++m) {
             const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
-            sV[t * PV + d] = t < nt ? (double)cur.v[m] : 0.0;
+            sV[t * PV + d] = (double)cur.v[m];
         }
         if (hown)
             for (int r = 0; r < 4; ++r) {
                 const int row = 16 * tn + drow(r, lane), col = 16 * td + (lane & 15);
                 sH[row * PV + col] = Hs[r];
-                if (saved_H) saved_H[(((size_t)bh * (nchunk + 1) + c) * DK + row) * DV + col] = Hs[r];
+                if (saved_H)
+                    bst64(make_rsrc(saved_H + ((size_t)bh * (nchunk + 1) + c) * DK * DV, DK * DV * 8),
+                          (uint32_t)(row * DV + col) * 8, Hs[r]);
             }
         group_transfer(cur.w, qs, gq, n);
         if (c + 1 < nchunk) fetch(nxt, c + 1);
@@ -240,9 +315,9 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
 
         // ---- the lane's own tokens from the chained start
         const double lam0c = lam_s[n];
-        if (saved_lam && gq == 0) saved_lam[((size_t)bh * nchunk + c) * DK + n] = lam0c;
         double x, z, A;
-        chain_start<DK>(qs, gq, n, lam0c, x, z, A);
+        chain_start<DK, G>(qs, gq, n, lam0c, x, z, A);
+        double wv[TPG];   // q^2 / lam_t
 #pragma unroll
         for (int j = 0; j < TPG; ++j) {
             const int t = gq * TPG + j;
@@ -258,7 +333,7 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
             chk = fma(qp, kn, chk);
             sQp[t * PQ + n] = qp;
             sKn[t * PQ + n] = kn;
-            sW[t * PQ + n] = qv * qv * zn * AR;   // q^2 / lam_t
+            wv[j] = qv * qv * zn * AR;
             x = xn;
             z = zn;
             A = An;
@@ -270,17 +345,6 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
         }
         __syncthreads();   // Qp, Kn, q^2 / lam, P_C in
 
-        // ---- S = M(Qp Kn^T): tiles (0,0), (1,0), (1,1) on waves 0..2, wave 1 also the zero tile
-        if (wave < 3) {
-            const int si = wave == 0 ? 0 : 1, sj = wave == 2 ? 1 : 0;
-            d4 acc = tile_mm<DK, PQ, 1, 1, PQ>(zero_d4(), sQp + 16 * si * PQ, sKn + 16 * sj * PQ, lane);
-            for (int r = 0; r < 4; ++r) {
-                const int i = drow(r, lane), j = lane & 15;
-                sS[(16 * si + i) * PS + 16 * sj + j] = (si == sj && j > i) ? 0.0 : acc[r];
-            }
-            if (si != sj)
-                for (int r = 0; r < 4; ++r) sS[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
-        }
         // ---- the readout's state part, Qp H0, and the state update, diag(P_C) (H0 + Kn^T V)
         d4 yacc = zero_d4();
         if (yown) yacc = tile_mm<DK, PQ, 1, PV, 1>(yacc, sQp + 16 * ti * PQ, sH + 16 * tdy, lane);
@@ -288,22 +352,32 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
             Hs = tile_mm<C, 1, PQ, PV, 1>(Hs, sKn + 16 * tn, sV + 16 * td, lane);
             for (int r = 0; r < 4; ++r) Hs[r] *= sPC[16 * tn + drow(r, lane)];
         }
+        // ---- S = M(Qp Kn^T): tiles (0,0), (1,0), (1,1) from waves 0..2 (wave 3 repeats the
+        // last, unstored, so that every wave runs the same code), wave 1 also the zero tile
+        {
+            const int st = wave < 3 ? wave : 2;
+            const int si = st == 0 ? 0 : 1, sj = st == 2 ? 1 : 0;
+            const d4 acc = tile_mm<DK, PQ, 1, 1, PQ>(zero_d4(), sQp + 16 * si * PQ, sKn + 16 * sj * PQ, lane);
+            if (wave < 3) {
+                for (int r = 0; r < 4; ++r) {
+                    const int i = drow(r, lane), j = lane & 15;
+                    sS[(16 * si + i) * PS + 16 * sj + j] = (si == sj && j > i) ? 0.0 : acc[r];
+                }
+                if (si != sj)
+                    for (int r = 0; r < 4; ++r) sS[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
+            }
+        }
         __syncthreads();   // S in
 
         // ---- y = S V + Qp H0, and yvar
         if (yown) {
             yacc = tile_mm<C, PS, 1, PV, 1>(yacc, sS + 16 * ti * PS, sV + 16 * tdy, lane);
-            for (int r = 0; r < 4; ++r) {
-                const int t = 16 * ti + drow(r, lane);
-                if (t < nt) fy[((tok0 + t) * H + h) * DV + 16 * tdy + (lane & 15)] = (float)yacc[r];
-            }
+            for (int r = 0; r < 4; ++r) oy[r] = (float)yacc[r];
         }
-        if (g.yvar && tid < nt) {
-            double acc = 0.0;
+        if (g.yvar)
 #pragma unroll
-            for (int m = 0; m < DK; ++m) acc += sW[tid * PQ + m];
-            g.yvar[(tok0 + tid) * H + h] = (float)acc;
-        }
+            for (int j = 0; j < TPG; ++j) oyv[j] = (float)slot_sum<DK>(wv[j]);
+        oc = c;
         __syncthreads();   // LDS free for the next chunk
     };
 
@@ -313,6 +387,7 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
         round(c, P0, P1);
         if (c + 1 < nchunk) round(c + 1, P1, P0);
     }
+    flush();
 
     // ---- the final belief
     const double* lam_e = sLam + (nchunk & 1) * DK;
@@ -333,9 +408,9 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
     constexpr int C = kC64, G = kNT64 / DK, TPG = C / G;
     constexpr int PQ = DK + 1, PV = DV + 1, PS = C + 1;
     constexpr int NTD = DV / 16, NTN = DK / 16, NTT = C / 16;
-    constexpr int NVE = C * DV / kNT64, NHE = DK * DV / kNT64;
+    constexpr int NVE = C * DV / kNT64, NHE = (DK * DV + kNT64 - 1) / kNT64;
     __shared__ double sQp[C * PQ], sKn[C * PQ], sV[C * PV], sDY[C * PV], sS[C * PS], sB[C * PS];
-    __shared__ double sH0[DK * PV], sGs[DK * PV], sX[C * PQ], sY[C * PQ], sDR[C * PQ];
+    __shared__ double sH0[DK * PV], sGs[DK * PV], sX[C * PQ], sY[C * PQ];
     __shared__ double qs[G * 5 * DK];
     __shared__ double sLam[DK], sPC[DK], sCar[2 * 2 * DK];   // carries (c, S) by round parity
 
@@ -363,8 +438,10 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
     if constexpr (TI) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], ca, cp);
     double sum_da = 0.0, sum_dp = 0.0;   // OU gates: the lane's sums of the gate gradients
 
-    // this wave's adjoint tile (tn, td) of G, if any
-    const bool gown = wave < NTN * NTD;
+    // this wave's adjoint tile (tn, td) of G, if any (at dk = dv = 32 every wave owns one
+    // tile of G, dV, X and Y, known at compile time)
+    constexpr bool FULL = NTN * NTD == 4 && NTT * NTD == 4 && NTT * NTN == 4;
+    const bool gown = FULL || wave < NTN * NTD;
     const int tn = wave / NTD, td = wave % NTD;
     d4 Gt = zero_d4();
     if (gown && g.detaT)
@@ -392,54 +469,100 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
     auto fetch = [&](Pre& P, int cn) {
         const int nt = min(C, T - cn * C);
         const size_t tok0 = seq0 + (size_t)cn * C;
-        P.w.load(fa, fp, fk, fq, fr, tok0, H, h, n, gq * TPG, nt);
+        P.w.load(ChunkBufs(TI ? nullptr : fa, TI ? nullptr : fp, fk, fq, fr, tok0, H, h, DK, nt), H, n, gq * TPG, nt);
+        const rsrc_t rg = make_rsrc(g.dyvar ? g.dyvar + tok0 * H + h : fr, g.dyvar ? (uint32_t)((nt - 1) * H + 1) * 4 : 0u);
 #pragma unroll
-        for (int j = 0; j < TPG; ++j) {
-            const int t = gq * TPG + j;
-            P.gv[j] = g.dyvar ? g.dyvar[(tok0 + (t < nt ? t : 0)) * H + h] : 0.f;
-        }
-#pragma unroll
-        for (int m = 0; m < NVE; ++m) {
-            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
-            const size_t gi = ((tok0 + (t < nt ? t : 0)) * H + h) * DV + d;
-            P.v[m] = fv[gi];
-            P.dy[m] = fdy[gi];
-        }
-#pragma unroll
-        for (int m = 0; m < NHE; ++m) P.h0[m] = saved_H[((size_t)bh * (nchunk + 1) + cn) * DK * DV + tid + kNT64 * m];
-        P.lam = saved_lam[((size_t)bh * nchunk + cn) * DK + n];
-    };
-
-    auto round = [&](int c, Pre& cur, Pre& nxt) {
-        const int nt = min(C, T - c * C);
-        const size_t tok0 = seq0 + (size_t)c * C;
-        cur.w.ca = ca;
-        cur.w.cp = cp;
-        // ---- stage the chunk into LDS, the walk lanes' transfers; then the previous chunk's fetch
+        for (int j = 0; j < TPG; ++j) P.gv[j] = bld32(rg, (uint32_t)((gq * TPG + j) * H) * 4);
+        const size_t v0 = (tok0 * H + h) * DV;
+        const uint32_t vbytes = (uint32_t)((nt - 1) * H * DV + DV) * 4;
+        const rsrc_t rv = make_rsrc(fv + v0, vbytes), rdy = make_rsrc(fdy + v0, vbytes);
 #pragma unroll
         for (int m = 0; m < NVE; ++m) {
             const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
-            sV[t * PV + d] = t < nt ? (double)cur.v[m] : 0.0;
-            sDY[t * PV + d] = t < nt ? (double)cur.dy[m] : 0.0;
+            const uint32_t vo = (uint32_t)(t * H * DV + d) * 4;
+            P.v[m] = bld32(rv, vo);
+            P.dy[m] = bld32(rdy, vo);
         }
 #pragma unroll
         for (int m = 0; m < NHE; ++m) {
             const int e = tid + kNT64 * m;
-            sH0[(e / DV) * PV + e % DV] = cur.h0[m];
+            P.h0[m] = e < DK * DV ? saved_H[((size_t)bh * (nchunk + 1) + cn) * DK * DV + e] : 0.0;
+        }
+        P.lam = saved_lam[((size_t)bh * nchunk + cn) * DK + n];
+    };
+
+    // The gradients of a round are stored at the start of the next one, before that
+    // round's fetch (as in the forward): dV of this wave's tile, dq, dk, dabar, dpbar of
+    // the lane's tokens, dr of token tid.
+    const bool dvown = FULL || wave < NTT * NTD;
+    const int tj = wave / NTD, dd = wave % NTD;   // this wave's dV tile
+    float odv[4] = {0.f, 0.f, 0.f, 0.f}, odq[TPG], odk[TPG], oda[TPG], odp[TPG], odr[TPG];   // odr: lane n = DK - 1
+    int oc = -1;
+    auto flush = [&]() {
+        if (oc < 0) return;
+        const int nt = min(C, T - oc * C);
+        const size_t tok0 = seq0 + (size_t)oc * C;
+        // buffers end at the chunk's last valid token: stores past it are dropped
+        if (dvown) {
+            const rsrc_t rv = make_rsrc(gdv + (tok0 * H + h) * DV, (uint32_t)((nt - 1) * H * DV + DV) * 4);
+            for (int r = 0; r < 4; ++r)
+                bst32(rv, (uint32_t)((16 * tj + drow(r, lane)) * H * DV + 16 * dd + (lane & 15)) * 4, odv[r]);
+        }
+        const size_t k0 = (tok0 * H + h) * DK;
+        const uint32_t kbytes = (uint32_t)((nt - 1) * H * DK + DK) * 4;
+        const rsrc_t rq = make_rsrc(gdq + k0, kbytes), rk = make_rsrc(gdk + k0, kbytes);
+#pragma unroll
+        for (int j = 0; j < TPG; ++j) {
+            const uint32_t vo = (uint32_t)((gq * TPG + j) * H * DK + n) * 4;
+            bst32(rq, vo, odq[j]);
+            bst32(rk, vo, odk[j]);
+        }
+        if constexpr (!TI) {
+            const rsrc_t ra = make_rsrc(gda + k0, kbytes), rp = make_rsrc(gdp + k0, kbytes);
+#pragma unroll
+            for (int j = 0; j < TPG; ++j) {
+                const uint32_t vo = (uint32_t)((gq * TPG + j) * H * DK + n) * 4;
+                bst32(ra, vo, oda[j]);
+                bst32(rp, vo, odp[j]);
+            }
+        }
+        const rsrc_t rr = make_rsrc(gdr + tok0 * H + h, (uint32_t)((nt - 1) * H + 1) * 4);
+#pragma unroll
+        for (int j = 0; j < TPG; ++j) bst32(rr, n == DK - 1 ? (uint32_t)((gq * TPG + j) * H) * 4 : 0x7ffffff0u, odr[j]);
+    };
+
+    auto round = [&](int c, Pre& cur, Pre& nxt) {
+        const int nt = min(C, T - c * C);
+        cur.w.ca = ca;
+        cur.w.cp = cp;
+        flush();
+        // ---- stage the chunk into LDS, the walk lanes' transfers; then the previous chunk's fetch
+#pragma unroll
+        for (int m = 0; m < NVE; ++m) {
+            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
+            sV[t * PV + d] = (double)cur.v[m];
+            sDY[t * PV + d] = (double)cur.dy[m];
+        }
+#pragma unroll
+        for (int m = 0; m < NHE; ++m) {
+            const int e = tid + kNT64 * m;
+            if (e < DK * DV) sH0[(e / DV) * PV + e % DV] = cur.h0[m];
         }
         if (tid < DK) sLam[tid] = cur.lam;
         double gv[TPG];
 #pragma unroll
-        for (int j = 0; j < TPG; ++j) gv[j] = gq * TPG + j < nt ? (double)cur.gv[j] : 0.0;
+        for (int j = 0; j < TPG; ++j) gv[j] = (double)cur.gv[j];
         group_transfer(cur.w, qs, gq, n);
         if (c >= 1) fetch(nxt, c - 1);
         __syncthreads();
 
         // ---- the walk over the lane's tokens: Qp, Kn, and what the adjoint walk needs
-        double lam_p[TPG], P_t[TPG], iP_t[TPG], il_t[TPG], rho[TPG], irho[TPG], ia[TPG];
+        // (kept across the contractions: lam_{t-1}, P_t, 1 / lam_t, rho_t; the reciprocals and
+        // coefficients of the adjoint walk are formed again from them where used)
+        double lam_p[TPG], P_t[TPG], il_t[TPG], rho[TPG];
         {
             double x, z, A;
-            chain_start<DK>(qs, gq, n, sLam[n], x, z, A);
+            chain_start<DK, G>(qs, gq, n, sLam[n], x, z, A);
             double izp = rcpa(z);
 #pragma unroll
             for (int j = 0; j < TPG; ++j) {
@@ -457,11 +580,8 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
                 sKn[t * PQ + n] = kn;
                 lam_p[j] = x * izp;
                 P_t[j] = An * iz;
-                iP_t[j] = zn * XR;
                 il_t[j] = zn * AR;
                 rho[j] = z * iz;
-                irho[j] = zn * izp;
-                ia[j] = A * XR;
                 izp = iz;
                 x = xn;
                 z = zn;
@@ -471,20 +591,27 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         }
         __syncthreads();   // Qp, Kn, P_C in
 
-        // ---- S = M(Qp Kn^T) and B = M(dY V^T): six tiles over the four waves (the tiles (1,0)
-        // also write the zero tile above the diagonal); Gs = diag(P_C) G
-        for (int job = wave; job < 6; job += 4) {
-            const int kind = job / 3, tt = job % 3;   // kind 0: S, 1: B; tiles (0,0), (1,0), (1,1)
-            const int si = tt == 0 ? 0 : 1, sj = tt == 2 ? 1 : 0;
-            d4 acc = kind == 0 ? tile_mm<DK, PQ, 1, 1, PQ>(zero_d4(), sQp + 16 * si * PQ, sKn + 16 * sj * PQ, lane)
-                               : tile_mm<DV, PV, 1, 1, PV>(zero_d4(), sDY + 16 * si * PV, sV + 16 * sj * PV, lane);
-            double* dst = kind == 0 ? sS : sB;
-            for (int r = 0; r < 4; ++r) {
-                const int i = drow(r, lane), j = lane & 15;
-                dst[(16 * si + i) * PS + 16 * sj + j] = (si == sj && j > i) ? 0.0 : acc[r];
+        // ---- S = M(Qp Kn^T) and B = M(dY V^T): tiles (0,0), (1,0), (1,1) of each from waves
+        // 0..2 (wave 3 repeats the last, unstored); the tiles (1,0) also write the zero tile above
+        // the diagonal.  Gs = diag(P_C) G
+        {
+            const int st = wave < 3 ? wave : 2;
+            const int si = st == 0 ? 0 : 1, sj = st == 2 ? 1 : 0;
+            const d4 sa = tile_mm<DK, PQ, 1, 1, PQ>(zero_d4(), sQp + 16 * si * PQ, sKn + 16 * sj * PQ, lane);
+            const d4 ba = tile_mm<DV, PV, 1, 1, PV>(zero_d4(), sDY + 16 * si * PV, sV + 16 * sj * PV, lane);
+            if (wave < 3) {
+                for (int r = 0; r < 4; ++r) {
+                    const int i = drow(r, lane), j = lane & 15;
+                    const bool up = si == sj && j > i;
+                    sS[(16 * si + i) * PS + 16 * sj + j] = up ? 0.0 : sa[r];
+                    sB[(16 * si + i) * PS + 16 * sj + j] = up ? 0.0 : ba[r];
+                }
+                if (si != sj)
+                    for (int r = 0; r < 4; ++r) {
+                        sS[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
+                        sB[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
+                    }
             }
-            if (si != sj)
-                for (int r = 0; r < 4; ++r) dst[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
         }
         if (gown)
             for (int r = 0; r < 4; ++r) {
@@ -496,17 +623,14 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
 
         // ---- dV = S^T dY + Kn Gs (tiles (tj, td)); X = dY H0^T + B Kn and Y = B^T Qp + V Gs^T
         // (tiles (t, tn)); G' = Qp^T dY + Gs (this wave's tile)
-        for (int job = wave; job < NTT * NTD; job += 4) {
-            const int tj = job / NTD, dd = job % NTD;
+        if (dvown) {
             d4 acc = tile_mm<C, 1, PS, PV, 1>(zero_d4(), sS + 16 * tj, sDY + 16 * dd, lane);
             acc = tile_mm<DK, PQ, 1, PV, 1>(acc, sKn + 16 * tj * PQ, sGs + 16 * dd, lane);
-            for (int r = 0; r < 4; ++r) {
-                const int t = 16 * tj + drow(r, lane);
-                if (t < nt) gdv[((tok0 + t) * H + h) * DV + 16 * dd + (lane & 15)] = (float)acc[r];
-            }
+            for (int r = 0; r < 4; ++r) odv[r] = (float)acc[r];
         }
-        for (int job = wave; job < NTT * NTN; job += 4) {
-            const int tq = job / NTN, nn = job % NTN;
+        __builtin_amdgcn_sched_barrier(0);   // one job's operands in registers at a time
+        if (FULL || wave < NTT * NTN) {
+            const int tq = wave / NTN, nn = wave % NTN;
             d4 xa = tile_mm<DV, PV, 1, 1, PV>(zero_d4(), sDY + 16 * tq * PV, sH0 + 16 * nn * PV, lane);
             xa = tile_mm<C, PS, 1, PQ, 1>(xa, sB + 16 * tq * PS, sKn + 16 * nn, lane);
             d4 ya = tile_mm<C, 1, PS, PQ, 1>(zero_d4(), sB + 16 * tq, sQp + 16 * nn, lane);
@@ -517,30 +641,31 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
                 sY[t * PQ + col] = ya[r];
             }
         }
+        __builtin_amdgcn_sched_barrier(0);
         if (gown) Gt = tile_mm<C, 1, PQ, PV, 1>(Gt, sQp + 16 * tn, sDY + 16 * td, lane);
         __syncthreads();   // X, Y in
 
         // ---- adjoint pass 1: the lane's tokens in reverse, each the affine step
         //   (c, S) -> (alpha (c - w) - beta (S + u), S + u),
         // composed into c_out = Am c_in + Bm S_in + Cm, S_out = S_in + Dm
-        double u_[TPG], w_[TPG], al_[TPG], be_[TPG], dqt_[TPG], dkh_[TPG];
+        // per token of the lane: u, w and the step coefficients alpha = abar^2 rho^2, beta = pbar rho
+        double dqt_[TPG], dkh_[TPG];
+        auto coef = [&](int j, double& u, double& w, double& al, double& be) {
+            const double qv = cur.w.Q(j), av = cur.w.A(j);
+            const double qi = qv * il_t[j];
+            u = qi * dqt_[j] - cur.w.K(j) * cur.w.R(j) * dkh_[j];
+            w = qi * fma(qv, gv[j], dqt_[j]) * il_t[j];
+            al = av * av * rho[j] * rho[j];
+            be = cur.w.P(j) * rho[j];
+        };
         double Am = 1.0, Bm = 0.0, Cm = 0.0, Dm = 0.0;
 #pragma unroll
         for (int j = TPG - 1; j >= 0; --j) {
             const int t = gq * TPG + j;
-            const double dqt = P_t[j] * sX[t * PQ + n], dkh = sY[t * PQ + n] * iP_t[j];
-            const double qv = cur.w.Q(j), av = cur.w.A(j);
-            const double kh = cur.w.K(j) * cur.w.R(j);
-            const double qi = qv * il_t[j];
-            const double u = qi * dqt - kh * dkh;
-            const double w = qi * fma(qv, gv[j], dqt) * il_t[j];
-            const double al = av * av * rho[j] * rho[j], be = cur.w.P(j) * rho[j];
-            u_[j] = u;
-            w_[j] = w;
-            al_[j] = al;
-            be_[j] = be;
-            dqt_[j] = dqt;
-            dkh_[j] = dkh;
+            dqt_[j] = P_t[j] * sX[t * PQ + n];
+            dkh_[j] = sY[t * PQ + n] * rcpa(P_t[j]);
+            double u, w, al, be;
+            coef(j, u, w, al, be);
             Cm = al * Cm - be * Dm - (al * w + be * u);
             Bm = al * Bm - be;
             Am = al * Am;
@@ -554,7 +679,7 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
 
         // ---- pass 2: carries into the lane's group (through the later groups) and out of the
         // chunk, then the gradients of its tokens
-        double cc, SS;
+        double cc, SS, drt[TPG];
         {
             const double* car = sCar + ((c + 1) & 1) * 2 * DK;
             double cT = car[n], ST = car[DK + n];
@@ -579,37 +704,32 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
 #pragma unroll
         for (int j = TPG - 1; j >= 0; --j) {
             const int t = gq * TPG + j;
-            SS += u_[j];
-            const double gl = cc - w_[j];
+            double u, w, al, be;
+            coef(j, u, w, al, be);
+            SS += u;
+            const double gl = cc - w;
             const double kv = cur.w.K(j), rv = cur.w.R(j), av = cur.w.A(j), qv = cur.w.Q(j);
             const double r2 = rho[j] * rho[j];
             const double dkv = fma(2.0 * kv * rv, gl, rv * dkh_[j]);
-            const double drho = fma(gl, lam_p[j], SS * irho[j]);
-            const double dav = fma(-2.0 * av * r2, drho, SS * ia[j]);
+            const double drho = fma(gl, lam_p[j], SS * rcpa(rho[j]));
+            const double dav = fma(-2.0 * av * r2, drho, SS * rcpa(av));
             const double dpv = -lam_p[j] * r2 * drho;
             const double dqv = fma(2.0 * qv, gv[j], dqt_[j]) * il_t[j];
-            sDR[t * PQ + n] = fma(kv * kv, gl, kv * dkh_[j]);
-            cc = fma(al_[j], gl, -be_[j] * SS);
-            if (t < nt) {
-                const size_t e = ((tok0 + t) * H + h) * DK + n;
-                gdq[e] = (float)dqv;
-                gdk[e] = (float)dkv;
-                if constexpr (TI) {
-                    sum_da += dav;
-                    sum_dp += dpv;
-                } else {
-                    gda[e] = (float)dav;
-                    gdp[e] = (float)dpv;
-                }
+            drt[j] = fma(kv * kv, gl, kv * dkh_[j]);
+            cc = fma(al, gl, -be * SS);
+            odq[j] = (float)dqv;
+            odk[j] = (float)dkv;
+            oda[j] = (float)dav;
+            odp[j] = (float)dpv;
+            if (TI && t < nt) {
+                sum_da += dav;
+                sum_dp += dpv;
             }
         }
-        __syncthreads();   // dr terms in
-        if (tid < nt) {
-            double acc = 0.0;
 #pragma unroll
-            for (int m = 0; m < DK; ++m) acc += sDR[tid * PQ + m];
-            gdr[(tok0 + tid) * H + h] = (float)acc;
-        }
+        for (int j = 0; j < TPG; ++j) odr[j] = (float)slot_sum<DK>(drt[j]);   // dr: the sum over the slots
+        oc = c;
+        __syncthreads();   // qs free for the next chunk's transfers
     };
 
     Pre P0, P1;
@@ -618,6 +738,7 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         round(c, P0, P1);
         if (c >= 1) round(c - 1, P1, P0);
     }
+    flush();
 
     // ---- gradients of the initial belief, and the OU gate sums
     if (g.dlam0 && tid < DK) g.dlam0[(size_t)bh * DK + tid] = (float)sCar[tid];
@@ -629,14 +750,14 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         const size_t np = (size_t)s.B * s.H * DK;
         // the slot's sum over all token groups (tids n, n + DK, ...), through LDS
         __syncthreads();
-        sDR[gq * PQ + n] = sum_da;
-        sX[gq * PQ + n] = sum_dp;
+        sX[gq * PQ + n] = sum_da;
+        sY[gq * PQ + n] = sum_dp;
         __syncthreads();
         if (tid < DK) {
             double sa = 0.0, sp = 0.0;
             for (int g2 = 0; g2 < G; ++g2) {
-                sa += sDR[g2 * PQ + tid];
-                sp += sX[g2 * PQ + tid];
+                sa += sX[g2 * PQ + tid];
+                sp += sY[g2 * PQ + tid];
             }
             part[(size_t)bh * DK + tid] = sa;
             part[np + (size_t)bh * DK + tid] = sp;

@@ -4,17 +4,19 @@ oracle's own belief for a decode continuation, and the range guard of the chunke
 
 * pbar = 0 with a time-invariant abar per key slot: lam and the state have closed forms
   (the appendix theorem with the initial-belief terms and sums from s = 1, reading R8),
-  on the chunked path (bf16) and the token-recurrent path (fp32).
+  on the chunked path (bf16) and the chunked fp64 path (fp32, dk = 32, dv = 16).
 * abar = 1 exactly, and small abar with tiny pbar (the gate F = abar rho then exceeds 1
-  for the first tokens), against the oracle on both paths.
+  for the first tokens), against the oracle on the three paths (bf16 chunked, fp32
+  token-recurrent at dk = 64, fp32 chunked fp64 at dk = dv = 32).
 * Split-sequence resume: two forwards chained through the final belief equal one
   forward over the whole sequence; the cut at token 45 is not a multiple of the 32-token
   chunk, so the chunk boundaries of the second part move by 13 tokens (the results do
   not depend on where chunks start).
 * Decode seeded with the oracle's belief after a 1024-token prewarm, compared step by
   step with the oracle's continuation.
-* KLA_CHECK=1 reports KLA_ERR_RANGE when the gate products of a chunk leave fp32 range
-  (abar = 0.03 over whole chunks: the product of abar underflows), and passes in range.
+* KLA_CHECK=1 reports KLA_ERR_RANGE when the gate products of a chunk leave the walk's
+  range (bf16 inputs: abar = 0.03 over whole chunks underflows fp32; fp32 inputs:
+  abar = 1e-12 underflows fp64), and passes in range.
 """
 import numpy as np
 import pytest
@@ -104,7 +106,7 @@ def _gates(kind, B, T, H, dk, g):
 
 
 @pytest.mark.parametrize("kind", ["abar_one", "small_abar_tiny_pbar"])
-@pytest.mark.parametrize("dtype,dk,dv", [("bf16", 128, 64), ("f32", 64, 32)])
+@pytest.mark.parametrize("dtype,dk,dv", [("bf16", 128, 64), ("f32", 64, 32), ("f32", 32, 32)])
 def test_boundary_gates_against_oracle(kla, kind, dtype, dk, dv):
     B, T, H = 2, 75, 2
     case = K.random_case(B, T, H, dk, dv, dtype, seed=91, dist="lm")
@@ -129,7 +131,7 @@ def test_boundary_gates_against_oracle(kla, kind, dtype, dk, dv):
     log("  " + " ".join(rep))
 
 
-@pytest.mark.parametrize("dtype,dk,dv", [("bf16", 128, 128), ("f32", 64, 32)])
+@pytest.mark.parametrize("dtype,dk,dv", [("bf16", 128, 128), ("f32", 64, 32), ("f32", 32, 32)])
 def test_split_sequence_resume(kla, dtype, dk, dv):
     B, T, H, cut = 2, 100, 2, 45
     case = K.random_case(B, T, H, dk, dv, dtype, seed=101, dist="lm")
@@ -188,15 +190,18 @@ def test_decode_from_oracle_belief(kla):
     log("  " + " ".join(rep))
 
 
-def test_chunk_range_guard(kla, monkeypatch):
-    B, T, H, dk, dv = 1, 96, 2, 64, 32
-    case = K.random_case(B, T, H, dk, dv, "bf16", seed=111, dist="lm")
-    good = _dev(case, "bf16", K.NAMES + ("dy",))
+# abar whose product over a 32-token chunk leaves the walk's range: fp32 arithmetic for bf16
+# inputs (0.03^32 ~ 2e-49), fp64 for fp32 inputs (1e-12 per token leaves fp64 after 26 tokens)
+@pytest.mark.parametrize("dtype,dk,dv,abar", [("bf16", 64, 32, 0.03), ("f32", 32, 32, 1e-12)])
+def test_chunk_range_guard(kla, monkeypatch, dtype, dk, dv, abar):
+    B, T, H = 1, 96, 2
+    case = K.random_case(B, T, H, dk, dv, dtype, seed=111, dist="lm")
+    good = _dev(case, dtype, K.NAMES + ("dy",))
     bad_case = dict(case)
-    bad_case["a"] = K.quantise(np.full((B, T, H, dk), 0.03), "bf16")
-    bad_case["p"] = K.quantise(np.full((B, T, H, dk), 0.05), "bf16")
-    bad = _dev(bad_case, "bf16", K.NAMES + ("dy",))
-    log("chunk range guard")
+    bad_case["a"] = K.quantise(np.full((B, T, H, dk), abar), dtype)
+    bad_case["p"] = K.quantise(np.full((B, T, H, dk), 0.05), dtype)
+    bad = _dev(bad_case, dtype, K.NAMES + ("dy",))
+    log(f"chunk range guard {dtype} dk{dk} dv{dv} abar={abar}")
     monkeypatch.setenv("KLA_CHECK", "1")
     with pytest.raises(kla.KLAError) as ei:
         kla.kla_forward(bad["q"], bad["k"], bad["v"], bad["a"], bad["p"], bad["r"])
@@ -210,4 +215,4 @@ def test_chunk_range_guard(kla, monkeypatch):
                      saved=out["saved"])
     torch.cuda.synchronize()
     ref = oracle.forward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"])
-    assert rel_err(to_np(out["y"]), ref["y"]) <= TOL["bf16"]
+    assert rel_err(to_np(out["y"]), ref["y"]) <= TOL[dtype]
