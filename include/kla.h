@@ -29,8 +29,9 @@
  *              in-place belief of kla_decode_step).  Base pointers must be
  *              16-byte aligned.
  *   dtype    : q, k, v, abar, pbar, r, y, dy and the input gradients share
- *              `dtype` (fp32 or bf16).  Beliefs, yvar, states and every
- *              accumulation are fp32.
+ *              `dtype` (fp32 or bf16).  Beliefs and yvar are fp32 at the
+ *              boundary.  The arithmetic is fp32 for bf16 inputs and fp64 for
+ *              fp32 inputs (their 1e-4 gradients need fp64 adjoint carries).
  *   Shapes   : B, H >= 1, T >= 0, dk and dv each in {16, 32, 64, 128}.
  *   Domain   : abar in (0, 1], pbar >= 0, r > 0, lam0 > 0, all finite.  Not
  *              checked unless the environment sets KLA_CHECK=1, in which case
@@ -46,12 +47,15 @@
  *              range over every chunk: roughly, the geometric mean of abar over
  *              32 consecutive tokens above 0.066 and that of abar^2 + pbar lam
  *              below 16 (abar = 0.03 over a whole chunk is outside: A underflows).
- *              Outside that range y and the gradients are not finite.  Under
- *              KLA_CHECK=1 the walks of the chunked forward and backward record
- *              whether any of those products was not finite, and the call
- *              synchronises and returns KLA_ERR_RANGE.  The token-recurrent
- *              path (fp32 inputs) and the per-channel entry points have no
- *              such limit.
+ *              Outside that range y and the gradients are not finite.  fp32
+ *              inputs with dk and dv in {16, 32} take the same chunk walk in
+ *              fp64, whose range is far wider (the geometric mean of abar over
+ *              32 tokens above about 1e-9; abar = 1e-12 over a chunk is
+ *              outside).  Under KLA_CHECK=1 the walks of the chunked forward
+ *              and backward record whether any of those products was not
+ *              finite, and the call synchronises and returns KLA_ERR_RANGE.
+ *              The token-recurrent path (fp32 inputs at dk or dv of 64 or 128)
+ *              and the per-channel entry points have no such limit.
  *   Empty    : with T == 0 the per-token pointers may be NULL; the final
  *              belief is then the initial one and its gradients pass through.
  *   Errors   : return codes only; on any error nothing has been enqueued
@@ -83,7 +87,7 @@ typedef enum {
     KLA_ERR_WORKSPACE = 5,  /* workspace missing or smaller than required         */
     KLA_ERR_NUMERIC = 6,    /* KLA_CHECK=1 found an input outside the domain      */
     KLA_ERR_HIP = 7,        /* a HIP launch or runtime call failed                */
-    KLA_ERR_RANGE = 8       /* KLA_CHECK=1: a chunk's gate products left fp32 range */
+    KLA_ERR_RANGE = 8       /* KLA_CHECK=1: a chunk's gate products left the walk's range */
 } kla_status;
 
 /* Problem descriptor: batch, sequence length, heads, key width, value width, dtype. */
@@ -99,10 +103,12 @@ size_t kla_forward_workspace(const kla_desc* desc);
  * kla_backward: the precision and information state at every chunk start, and
  * the precision walk's state after the chunk's first 16 tokens (chunked layout:
  * bf16 inputs with dk >= 32 and dv >= 32, the shapes whose backward is
- * chunked), else the precision after every token and the
- * information state before every 64th token (fp32; fp64 for fp32 inputs, whose
- * token-recurrent kernels accumulate in fp64).  Both calls pick the layout by
- * the same rule, so a context from kla_forward always fits kla_backward. */
+ * chunked); the precision and information state at every chunk start in fp64
+ * (fp32 inputs with dk and dv in {16, 32}, the chunked fp64 path); else the
+ * precision after every token and the information state before every 64th
+ * token (fp32; fp64 for fp32 inputs, whose token-recurrent kernels accumulate
+ * in fp64).  Both calls pick the layout by the same rule, so a context from
+ * kla_forward always fits kla_backward. */
 size_t kla_saved_bytes(const kla_desc* desc);
 
 /* Bytes of device workspace kla_backward needs when it is given a saved
