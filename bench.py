@@ -33,7 +33,7 @@ T = 65536, d = 128, bf16; heads 8..15 with slow decay), which has only 16
 sequences to spread over the chip.
 
 With --a5 it times forward + backward of the state-tracking workload (B = 64,
-H = 4, T = 512, d = 32, fp32 inputs: the token-recurrent kernels).
+H = 4, T = 512, d = 32, fp32 inputs: the chunked fp64 kernels).
 
 With --mc it times the Monte Carlo readout of KLA+ at the same shape with S = 10
 draws: kla_mc_sample, kla_mc_sample_backward, kla_mc_nll and kla_mc_nll_backward.
@@ -368,7 +368,7 @@ def bench_a5(args, dev, emit=True):
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured.get(dom) if measured else None,
                      "traffic_unit": "bytes per call", "algorithmic_bytes_per_call": nbytes,
                      "fwd_ms": fwd_ms, "bwd_ms": bwd_ms,
-                     "note": "token-recurrent kernels (fp32 inputs); Infinity Cache flushed between steps"},
+                     "note": "chunked fp64 kernels (fp32 inputs, fp64 MFMA); Infinity Cache flushed between steps"},
     }
     if emit:
         print(json.dumps(res), flush=True)
@@ -683,7 +683,7 @@ def main():
 
 def other_configs(args, dev):
     """The other workloads, each in its own pass and timing: the state-tracking fwd+bwd
-    step (fp32, token-recurrent kernels), the long-context forward and the decode step,
+    step (fp32, chunked fp64 kernels), the long-context forward and the decode step,
     with their HBM-roofline fractions on their algorithmic bytes."""
     import torch
     sub = argparse.Namespace(**vars(args))

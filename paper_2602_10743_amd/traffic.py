@@ -18,7 +18,7 @@ Run from the repository root on the GPU machine (TMPDIR=/tmp):
 With OU gates: the same two runs with `bench.py ... --ou`, then
   python -m paper_2602_10743_amd.traffic D/fetch D/write --ou > profiles/lm_layer_ou_traffic.md
 
-The state-tracking workload (fp32, token-recurrent kernels): the same two runs with
+The state-tracking workload (fp32, chunked fp64 kernels): the same two runs with
 `bench.py --a5 --steps 2 --warmup 1 --copy-calibration`, then
   python -m paper_2602_10743_amd.traffic D/fetch D/write --a5 > profiles/a5_state_tracking_traffic.md
 
@@ -47,8 +47,8 @@ CALLS_OU = {
     "kla_backward_ou": ("bwd_dv_kernel", "bwd_dk_kernel", "dr_combine_kernel", "ou_param_grads_kernel"),
 }
 CALLS_A5 = {
-    "kla_forward": ("fwd_recurrent_kernel",),
-    "kla_backward": ("bwd_sweep1_kernel", "bwd_sweep2_kernel"),
+    "kla_forward": ("fwd64_kernel",),
+    "kla_backward": ("bwd64_kernel",),
 }
 SUMMARY_KEY = "traffic_bytes_per_call"
 
@@ -59,7 +59,7 @@ DIGEST_SOURCES = ("kla_api.cpp", "kla_internal.hpp", "kla_device.hpp", "kla_buf.
                   "kla_chunk.hpp", "chunk_fwd.hip", "chunk_bwd_dv.hip", "chunk_bwd_dk.hip", "ou.hip",
                   "validate.hip")
 # ... and of the token-recurrent kernels (the state-tracking workload)
-DIGEST_SOURCES_A5 = ("kla_api.cpp", "kla_internal.hpp", "kla_device.hpp", "kla_buf.hpp", "recurrent.hip",
+DIGEST_SOURCES_A5 = ("kla_api.cpp", "kla_internal.hpp", "kla_device.hpp", "kla_buf.hpp", "chunk64.hip",
                      "validate.hip")
 
 
@@ -176,6 +176,9 @@ def load_summary(path: str, names=DIGEST_SOURCES):
 
 
 UTIL_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU", "GRBM_GUI_ACTIVE")
+# the state-tracking workload (fp32 inputs) runs fp64 MFMAs
+UTIL_COUNTERS_A5 = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_F64", "SQ_INSTS_VALU", "GRBM_GUI_ACTIVE")
+F64_PEAK = 78.6e12       # fp64 flop/s (matrix and vector alike)
 NUM_SIMD = 1024          # 256 CUs x 4 SIMDs
 NUM_XCD = 8              # GRBM_GUI_ACTIVE comes summed over the accelerator dies
 BF16_PEAK = 2.5e15       # dense bf16 MFMA flop/s
@@ -190,34 +193,45 @@ def _rows(run_dir: str):
         yield from csv.DictReader(open(f))
 
 
-def summarise_util(run_dir: str) -> str:
-    """MFMA busy fraction, bf16 MFMA flop rate and VALU issue per kernel from one
-    counter run with UTIL_COUNTERS; durations from the dispatch timestamps."""
+def summarise_util(run_dir: str, a5: bool = False) -> str:
+    """MFMA busy fraction, MFMA flop rate (bf16; fp64 for the state-tracking
+    workload) and VALU issue per kernel from one counter run with UTIL_COUNTERS
+    (UTIL_COUNTERS_A5); durations from the dispatch timestamps."""
     acc = defaultdict(lambda: defaultdict(float))   # kernel -> counter -> sum over dispatches
     dur = defaultdict(dict)                          # kernel -> dispatch -> ns
+    tables = [CALLS_A5] if a5 else [CALLS, CALLS_OU]
     for r in _rows(run_dir):
         k = _short(r["Kernel_Name"])
-        if not k.startswith(tuple(n for ns in list(CALLS.values()) + list(CALLS_OU.values()) for n in ns)):
+        if not k.startswith(tuple(n for t in tables for ns in t.values() for n in ns)):
             continue
         d = r.get("Dispatch_Id") or r.get("Correlation_Id")
         acc[k][r["Counter_Name"]] += float(r["Counter_Value"])
         dur[k][d] = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+    mops, peak, kind = (("SQ_INSTS_VALU_MFMA_MOPS_F64", F64_PEAK, "fp64") if a5 else
+                        ("SQ_INSTS_VALU_MFMA_MOPS_BF16", BF16_PEAK, "bf16"))
+    title = ("state-tracking workload (B=64, T=512, H=4, d=32, fp32 inputs, fp64 arithmetic)" if a5 else
+             "lm-layer workload (B=8, T=2048, H=16, d=128, bf16)")
+    cmd = ("python bench.py --a5 --steps 2 --warmup 1 --no-cpu-baseline" if a5 else
+           "python bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-configs")
     lines = [
-        "# MFMA and VALU utilisation per kernel, lm-layer workload (B=8, T=2048, H=16, d=128, bf16)",
+        f"# MFMA and VALU utilisation per kernel, {title}",
         "",
         "Command (repository root, one MI355X, TMPDIR=/tmp):",
         "",
-        "    rocprofv3 --pmc " + " ".join(UTIL_COUNTERS) + " --output-format csv -d D/util -o run -- "
-        "python bench.py --steps 2 --warmup 1 --no-cpu-baseline --no-configs",
-        "    python -m paper_2602_10743_amd.traffic --util D/util",
+        "    rocprofv3 --pmc " + " ".join(UTIL_COUNTERS_A5 if a5 else UTIL_COUNTERS) +
+        " --output-format csv -d D/util -o run -- " + cmd,
+        "    python -m paper_2602_10743_amd.traffic " + ("--util-a5" if a5 else "--util") + " D/util",
         "",
         "Durations come from the dispatch timestamps of the same run.  MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / ",
-        f"{NUM_XCD} dies x {NUM_SIMD} SIMDs); bf16 rate = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16 / duration against",
-        f"{BF16_PEAK / 1e15:.1f} PFLOP/s; VALU issue = SQ_INSTS_VALU / duration against one wave64",
-        "instruction per 4 cycles per SIMD at 2.4 GHz.  The split-bf16 products count 2-3 MFMAs",
-        "per fp32-accurate product.",
+        f"{NUM_XCD} dies x {NUM_SIMD} SIMDs); {kind} rate = 512 x {mops} / duration against",
+        f"{peak / 1e12:.1f} TFLOP/s; VALU issue = SQ_INSTS_VALU / duration against one wave64",
+        "instruction per 4 cycles per SIMD at 2.4 GHz." + ("" if a5 else "  The split-bf16 products count 2-3 MFMAs"),
+    ]
+    if not a5:
+        lines.append("per fp32-accurate product.")
+    lines += [
         "",
-        "| kernel | dispatches | avg us | MFMA busy | bf16 MFMA TFLOP/s | of peak | VALU Ginst/s | of peak |",
+        f"| kernel | dispatches | avg us | MFMA busy | {kind} MFMA TFLOP/s | of peak | VALU Ginst/s | of peak |",
         "|---|---|---|---|---|---|---|---|",
     ]
     for k in sorted(acc):
@@ -226,17 +240,17 @@ def summarise_util(run_dir: str) -> str:
         c = {name: v / n for name, v in acc[k].items()}
         active = c.get("GRBM_GUI_ACTIVE", 1.0) / NUM_XCD
         busy = c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / max(active * NUM_SIMD, 1.0)
-        flops = 512.0 * c.get("SQ_INSTS_VALU_MFMA_MOPS_BF16", 0.0) / t
+        flops = 512.0 * c.get(mops, 0.0) / t
         valu = c.get("SQ_INSTS_VALU", 0.0) / t
         lines.append(f"| {k} | {n} | {t * 1e6:.1f} | {100 * busy:.1f}% | {flops / 1e12:.1f} | "
-                     f"{100 * flops / BF16_PEAK:.1f}% | {valu / 1e9:.1f} | {100 * valu / VALU_PEAK_INSTS:.1f}% |")
+                     f"{100 * flops / peak:.1f}% | {valu / 1e9:.1f} | {100 * valu / VALU_PEAK_INSTS:.1f}% |")
     lines.append("")
     return "\n".join(lines)
 
 
 if __name__ == "__main__":
-    if len(sys.argv) == 3 and sys.argv[1] == "--util":
-        print(summarise_util(sys.argv[2]))
+    if len(sys.argv) == 3 and sys.argv[1] in ("--util", "--util-a5"):
+        print(summarise_util(sys.argv[2], a5=sys.argv[1] == "--util-a5"))
         sys.exit(0)
     ou = "--ou" in sys.argv[1:]
     a5 = "--a5" in sys.argv[1:]
