@@ -375,17 +375,17 @@ def test_workload0_tiny_forward(kla):
 
 
 def test_workload1_state_tracking_fwd_bwd(kla):
-    _workload_parity(kla, 1, 4, backward=True)
+    _workload_parity(kla, 1, 12, backward=True)
 
 
 def test_workload2_lm_layer_fwd_bwd(kla):
-    _workload_parity(kla, 2, 3, backward=True)
+    _workload_parity(kla, 2, 6, backward=True)
 
 
 def test_workload3_long_context_forward(kla):
     w = K.WORKLOADS[3]
-    # one normal-gate head and one near-one-gate head, plus the corner pair
-    _workload_parity(kla, 3, 2, backward=False)
+    # the corner pairs (heads 0 and 15: a normal-gate head and a near-one-gate head) and two more
+    _workload_parity(kla, 3, 4, backward=False)
 
 
 def test_workload4_decode(kla):
