@@ -34,17 +34,18 @@
 //   walk   lanes = (slot nl = lane % 16, group g = lane / 16 of 4 tokens): each
 //          lane forms its group's transfer -- the 2x2 map of (x, z) of
 //          Theorem 1 over 4 tokens, with prod abar --, the four groups of each
-//          half are chained through LDS from the saved state at the start of
-//          the half (lam_0, or lam_16 and P_16), and each lane walks its 4
-//          tokens from the group start, writing Qp and Kn ([t][16], split bf16)
-//          and keeping lam_t, P_t and the reciprocals the adjoint walk needs;
+//          half (the wave's four 16-lane rows) are chained by lane swaps from
+//          the saved state at the start of the half (lam_0, or lam_16 and
+//          P_16), and each lane walks its 4 tokens from the group start,
+//          writing Qp and Kn ([t][16], split bf16) and keeping lam_t, P_t and
+//          the reciprocals the adjoint walk needs;
 //   MFMA   split by operand instead: wave 0 forms B^T and X^T (with the chunk's
 //          saved start state H0 in registers), wave 1 forms B and Y^T and
 //          carries G^T[dv, 16] in registers;
 //   adjoint per lane: its group's tokens in reverse, once to summarise the
 //          group as an affine map of the incoming (c, S), then -- the groups
 //          chained through LDS -- once more for the gradients.
-// The chunks are walked last to first, five LDS barriers per chunk separating
+// The chunks are walked last to first, four LDS barriers per chunk separating
 // the phases.  The next chunk's inputs go straight into LDS, requested during
 // the first pass of a round's adjoint walk; the chunk's saved state rows come
 // into wave 0's registers at the start of its round.
@@ -87,8 +88,8 @@ struct DkCfg {
     static constexpr int QH = GV + 2 * 64 * 4;                      // Qp, Kn split bf16 [kC][LQ2]
     static constexpr int QL = QH + kC * LQ2 * 2, KH = QL + kC * LQ2 * 2, KL = KH + kC * LQ2 * 2;
     static constexpr int XT = KL + kC * LQ2 * 2, YT = XT + kC * LX * 4;   // X, Y fp32 [kC][LX]
-    static constexpr int QS = YT + kC * LX * 4;                     // group maps [NG][5][16] fp32
-    static constexpr int PC = QS + NG * 5 * 16 * 4;                 // chunk decay P_C [16] fp32
+    static constexpr int QS = YT + kC * LX * 4;                     // adjoint group summaries [NG][4][16] fp32
+    static constexpr int PC = QS + NG * 4 * 16 * 4;                 // chunk decay P_C [16] fp32
     static constexpr int WT = PC + 16 * 4;                          // chunk totals of the state parts [2][16]
     static constexpr int PAIR = (WT + 2 * 16 * 4 + 15) / 16 * 16;
     static constexpr int BYTES = PAIR0 + NP * PAIR;   // dynamic part
@@ -362,6 +363,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
             }
             // the transfer of this lane's group: (x, z) -> M (x, z) over its valid tokens, as the
             // images of (1, 0) and (0, 1), and the product of abar
+            float tr[5];
             {
                 float x0 = 1.f, z0 = 0.f, x1 = 0.f, z1 = 1.f, Aq = 1.f;
 #pragma unroll
@@ -377,25 +379,25 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                     z1 = ok ? z1n : z1;
                     Aq = ok ? Aq * av : Aq;
                 }
-                qs[(gg * 5 + 0) * 16 + nl] = x0;
-                qs[(gg * 5 + 1) * 16 + nl] = z0;
-                qs[(gg * 5 + 2) * 16 + nl] = x1;
-                qs[(gg * 5 + 3) * 16 + nl] = z1;
-                qs[(gg * 5 + 4) * 16 + nl] = Aq;
+                tr[0] = x0;
+                tr[1] = z0;
+                tr[2] = x1;
+                tr[3] = z1;
+                tr[4] = Aq;
             }
-            barrier_lds();   // the group transfers of the chunk are in
+            __builtin_amdgcn_sched_barrier(0);   // keep the phases apart in the schedule (register pressure)
 
             // ================================================================ phase 2
             // chain the wave's earlier groups from the saved state at the start of its half:
-            // (x, z, A) = (lam_0, 1, 1) for tokens 0..15, (lam_16, 1, P_16) for 16..31
+            // (x, z, A) = (lam_0, 1, 1) for tokens 0..15, (lam_16, 1, P_16) for 16..31.  A
+            // wave's four groups are its four 16-lane rows, so the transfers of the earlier rows
+            // are read across lanes (ds_bpermute), with no LDS store and no barrier.
             const float* lws = reinterpret_cast<const float*>(wb + Cfg::LW) + bb * 64;
             float x = lws[16 * E + nl], z = 1.f, A = E == 0 ? 1.f : lws[32 + nl];
 #pragma unroll
             for (int q2 = 0; q2 < NG / 2 - 1; ++q2) {
-                const int q3 = 4 * E + q2;
-                const float m00 = qs[(q3 * 5 + 0) * 16 + nl], m10 = qs[(q3 * 5 + 1) * 16 + nl];
-                const float m01 = qs[(q3 * 5 + 2) * 16 + nl], m11 = qs[(q3 * 5 + 3) * 16 + nl];
-                const float aq = qs[(q3 * 5 + 4) * 16 + nl];
+                auto pick = [&](int i) { return __shfl(tr[i], 16 * q2 + nl, 64); };   // row q2, same column
+                const float m00 = pick(0), m10 = pick(1), m01 = pick(2), m11 = pick(3), aq = pick(4);
                 const bool use = q2 < g4;
                 const float xn = fmaf(m00, x, m01 * z), zn = fmaf(m10, x, m11 * z);
                 x = use ? xn : x;
@@ -594,7 +596,7 @@ __global__ __launch_bounds__((DkCfg<DK, DV>::NTHR)) void bwd_dk_kernel(Shape s, 
                     GT[rd] = mfma2b(yt, qbh, qbl, GT[rd]);
                 }
             }
-            qs[(gg * 4 + 0) * 16 + nl] = Am;   // the group transfers were read before the last barrier
+            qs[(gg * 4 + 0) * 16 + nl] = Am;   // the last chunk's summaries were read before two barriers
             qs[(gg * 4 + 1) * 16 + nl] = Bm;
             qs[(gg * 4 + 2) * 16 + nl] = Cm;
             qs[(gg * 4 + 3) * 16 + nl] = Dm;
