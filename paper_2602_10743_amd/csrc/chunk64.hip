@@ -288,10 +288,7 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
     };
 
     auto round = [&](int c, Pre& cur, Pre& nxt) {
-        const int nt = min(C, T - c * C);
         const double* lam_s = sLam + (c & 1) * DK;
-        cur.w.ca = ca;
-        cur.w.cp = cp;
         flush();
         if (saved_lam && tid < DK) saved_lam[((size_t)bh * nchunk + c) * DK + tid] = lam_s[tid];
         // ---- this chunk's values and its start state into LDS (the state also into the
@@ -382,6 +379,8 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
     };
 
     Pre P0, P1;
+    P0.w.ca = P1.w.ca = ca;
+    P0.w.cp = P1.w.cp = cp;
     if (nchunk > 0) fetch(P0, 0);
     for (int c = 0; c < nchunk; c += 2) {
         round(c, P0, P1);
@@ -533,8 +532,6 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
 
     auto round = [&](int c, Pre& cur, Pre& nxt) {
         const int nt = min(C, T - c * C);
-        cur.w.ca = ca;
-        cur.w.cp = cp;
         flush();
         // ---- stage the chunk into LDS, the walk lanes' transfers; then the previous chunk's fetch
 #pragma unroll
@@ -733,6 +730,8 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
     };
 
     Pre P0, P1;
+    P0.w.ca = P1.w.ca = ca;
+    P0.w.cp = P1.w.cp = cp;
     if (nchunk > 0) fetch(P0, nchunk - 1);
     for (int c = nchunk - 1; c >= 0; c -= 2) {
         round(c, P0, P1);
