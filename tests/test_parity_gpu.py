@@ -126,8 +126,9 @@ def test_backward_small(kla, B, T, H, dk, dv, dtype, dist, with_saved):
 
 @pytest.mark.parametrize("dk,dv", [(32, 32), (128, 16)])
 def test_backward_default_belief_ragged(kla, dk, dv):
-    """Token-recurrent path without an initial belief, final-belief gradients or a
-    variance gradient, at a length that leaves a partial block."""
+    """fp32 paths (dk = dv = 32: the chunked fp64 one; dk = 128: the token-recurrent one)
+    without an initial belief, final-belief gradients or a variance gradient, at a length
+    that leaves a partial chunk or block."""
     B, T, H = 2, 37, 3
     case = K.random_case(B, T, H, dk, dv, "f32", seed=dk + dv, dist="c0")
     log(f"backward defaults B{B} T{T} H{H} dk{dk} dv{dv} f32")
@@ -146,11 +147,13 @@ def test_backward_default_belief_ragged(kla, dk, dv):
 
 
 @pytest.mark.parametrize("T", [15, 16, 31, 32, 33, 64, 65])
-def test_recurrent_block_boundaries(kla, T):
-    """fp32 token-recurrent path around its block (16 / 32 tokens) and state-checkpoint
-    (64 tokens) boundaries: forward with a saved context, backward from it and from a
-    recomputed one (bitwise equal), against the oracle."""
-    B, H, dk, dv = 2, 3, 32, 32
+@pytest.mark.parametrize("dk,dv", [(32, 32), (64, 32)])
+def test_recurrent_block_boundaries(kla, T, dk, dv):
+    """The fp32 paths around their boundaries: the chunked fp64 path at dk = dv = 32
+    (32-token chunks) and the token-recurrent path at dk = 64 (blocks of 16 / 32 tokens,
+    state checkpoints every 64): forward with a saved context, backward from it and from
+    a recomputed one (bitwise equal), against the oracle."""
+    B, H = 2, 3
     case = K.random_case(B, T, H, dk, dv, "f32", seed=T + 101, dist="c0")
     lam0, eta0 = _random_belief(B, H, dk, dv, T + 7)
     g = np.random.default_rng(T + 5)
@@ -178,20 +181,21 @@ def test_recurrent_block_boundaries(kla, T):
     log("  " + " ".join(rep))
 
 
-def test_empty_and_single_token(kla):
+@pytest.mark.parametrize("dk", [32, 64])   # fp32: the chunked fp64 path, the token-recurrent one
+def test_empty_and_single_token(kla, dk):
     for T in (0, 1):
-        case = K.random_case(2, T, 2, 32, 16, "f32", seed=5)
-        lam0, eta0 = _random_belief(2, 2, 32, 16, 3)
-        log(f"edge T={T}")
+        case = K.random_case(2, T, 2, dk, 16, "f32", seed=5)
+        lam0, eta0 = _random_belief(2, 2, dk, 16, 3)
+        log(f"edge T={T} dk={dk}")
         x = _dev_inputs(case, "f32")
         f32 = lambda a: torch.tensor(a, dtype=torch.float32, device=DEV)
         out = kla.kla_forward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), want_var=True)
         gr = kla.kla_backward(x["q"], x["k"], x["v"], x["a"], x["p"], x["r"], f32(lam0), f32(eta0), x["dy"],
-                              f32(np.ones((2, 2, 32))), f32(np.ones((2, 2, 32, 16))))
+                              f32(np.ones((2, 2, dk))), f32(np.ones((2, 2, dk, 16))))
         torch.cuda.synchronize()
         ref = oracle.forward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0)
         rg = oracle.backward(case["q"], case["k"], case["v"], case["a"], case["p"], case["r"], lam0, eta0,
-                             case["dy"], np.ones((2, 2, 32)), np.ones((2, 2, 32, 16)))
+                             case["dy"], np.ones((2, 2, dk)), np.ones((2, 2, dk, 16)))
         np.testing.assert_allclose(to_np(out["lamT"]), ref["lamT"], rtol=1e-6)
         np.testing.assert_allclose(to_np(out["etaT"]), ref["etaT"], rtol=1e-6, atol=1e-7)
         np.testing.assert_allclose(to_np(gr["dlam0"]), rg["dlam0"], rtol=1e-5, atol=1e-6)
