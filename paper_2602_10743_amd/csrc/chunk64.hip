@@ -205,20 +205,31 @@ __device__ __forceinline__ void chain_start(const double* qs, int gq, int n, dou
 }
 
 // ============================================================================ forward
+// Eight waves: waves 0..3 walk chunk c (stage, group transfers, walk: Qp, Kn, P_C
+// and the next chunk-start lam into the LDS set of c's parity) while waves 4..7
+// run the contractions of chunk c - 1 from the other set, each owning one state
+// tile and one readout tile.  Two barriers per round: between the walk's group
+// transfers and their chaining (the MFMA waves then go from S to the products
+// that read it), and at the round's end.
+constexpr int kWT = 256;   // walk threads of the forward (waves 0..3); waves 4..7 are MFMA waves
+
 template <int DK, int DV, bool TI>
-__global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double* saved_lam, double* saved_H) {
-    constexpr int C = kC64, G = kNT64 / DK, TPG = C / G;
+__global__ __launch_bounds__(2 * kWT) void fwd64_kernel(Shape s, FwdArgs g, double* saved_lam, double* saved_H) {
+    constexpr int C = kC64, G = kWT / DK, TPG = C / G;
     constexpr int PQ = DK + 1, PV = DV + 1, PS = C + 1;
     constexpr int NTD = DV / 16, NTN = DK / 16, NTT = C / 16;
-    constexpr int NVE = C * DV / kNT64;   // value elements per thread and chunk
-    __shared__ double sQp[C * PQ], sKn[C * PQ], sV[C * PV], sS[C * PS], sH[DK * PV];
-    __shared__ double qs[G * 5 * DK];
-    __shared__ double sLam[2 * DK], sPC[DK];
+    constexpr int NVE = C * DV / kWT;   // value elements per walk thread and chunk
+    // chunk c's walk results, in the set c & 1 (written by the walk waves in round c,
+    // read by the MFMA waves in round c + 1)
+    __shared__ double sQp[2][C * PQ], sKn[2][C * PQ], sV[2][C * PV], sPC[2][DK];
+    __shared__ double sS[C * PS], sH[DK * PV];   // MFMA waves
+    __shared__ double qs[G * 5 * DK], sLam[2 * DK];   // walk waves
 
     const int bh = blockIdx.x, b = bh / s.H, h = bh % s.H, H = s.H, T = s.T;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int n = tid % DK, gq = tid / DK;
+    const bool walker = wave < 4;
+    const int n = tid % DK, gq = (tid % kWT) / DK;   // walk lanes: slot, token group
     const int nchunk = (T + C - 1) / C;
     const size_t seq0 = (size_t)b * T;
     const float* fq = static_cast<const float*>(g.q);
@@ -230,25 +241,25 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
     float* fy = static_cast<float*>(g.y);
 
     double ca = 0.0, cp = 0.0;   // time-invariant gates of slot n
-    if constexpr (TI) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], ca, cp);
+    if constexpr (TI)
+        if (walker) ou_gates(g.ou_a[h * DK + n], g.ou_p[h * DK + n], g.ou_d[h * DK + n], ca, cp);
 
-    // this wave's state tile (tn, td) = H[16 tn .. + 15][16 td .. + 15], if any (at
-    // dk = dv = 32 every wave owns one state tile and one readout tile, known at compile time)
+    // MFMA wave mw's state tile (tn, td) = H[16 tn .. + 15][16 td .. + 15] and readout tile
+    // (ti, tdy), if any (at dk = dv = 32 every MFMA wave owns one of each, known at compile time)
     constexpr bool FULL = NTN * NTD == 4 && NTT * NTD == 4;
-    const bool hown = FULL || wave < NTN * NTD;
-    const int tn = wave / NTD, td = wave % NTD;
+    const int mw = wave - 4;
+    const bool hown = !walker && (FULL || mw < NTN * NTD);
+    const bool yown = !walker && (FULL || mw < NTT * NTD);
+    const int tn = mw / NTD, td = mw % NTD, ti = mw / NTD, tdy = mw % NTD;
     d4 Hs = zero_d4();
     if (hown && g.eta0)
         for (int r = 0; r < 4; ++r)
             Hs[r] = g.eta0[((size_t)bh * DK + 16 * tn + drow(r, lane)) * DV + 16 * td + (lane & 15)];
-    // the readout tile (ti, tdy) of this wave, if any
-    const bool yown = FULL || wave < NTT * NTD;
-    const int ti = wave / NTD, tdy = wave % NTD;
 
     if (tid < DK) sLam[tid] = g.lam0 ? (double)g.lam0[(size_t)bh * DK + tid] : 1.0;
     double chk = 0.0;   // range check: sum of Qp Kn over the lane's tokens
 
-    // a chunk's inputs, fetched one chunk ahead
+    // a chunk's inputs, fetched by the walk waves one chunk ahead
     struct Pre {
         WalkIn<DK, TPG, TI> w;
         float v[NVE];
@@ -260,60 +271,45 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
         const rsrc_t rv = make_rsrc(fv + (tok0 * H + h) * DV, (uint32_t)((nt - 1) * H * DV + DV) * 4);
 #pragma unroll
         for (int m = 0; m < NVE; ++m) {
-            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
+            const int e = tid + kWT * m, t = e / DV, d = e % DV;
             P.v[m] = bld32(rv, (uint32_t)(t * H * DV + d) * 4);
         }
     };
 
-    // The outputs of a round (its y tile and yvar) are stored at the start of the next
-    // one, before that round's fetch: no store is then younger than a fetch, and the
-    // wait for a fetched chunk does not also wait for the stores of the round before.
-    float oy[4] = {0.f, 0.f, 0.f, 0.f}, oyv[TPG];   // oyv: yvar of the lane's tokens (lane n = DK - 1)
-    int oc = -1;   // the chunk they belong to (none: -1)
+    // The walk waves' outputs of a round (yvar of its chunk) are stored at the start of
+    // their next round, before that round's fetch: no store is then younger than a fetch,
+    // and the wait for a fetched chunk does not also wait for the stores of the round before.
+    float oyv[TPG];   // yvar of the lane's tokens (lane n = DK - 1)
+    int oc = -1;      // the chunk they belong to (none: -1)
     auto flush = [&]() {
-        if (oc < 0) return;
+        if (oc < 0 || !g.yvar) return;
         const int nt = min(C, T - oc * C);
-        const size_t tok0 = seq0 + (size_t)oc * C;
-        if (yown) {
-            const rsrc_t ry = make_rsrc(fy + (tok0 * H + h) * DV, (uint32_t)((nt - 1) * H * DV + DV) * 4);
-            for (int r = 0; r < 4; ++r)
-                bst32(ry, (uint32_t)((16 * ti + drow(r, lane)) * H * DV + 16 * tdy + (lane & 15)) * 4, oy[r]);
-        }
-        if (g.yvar) {   // tokens past the chunk's last one, and the other lanes, fall outside the buffer
-            const rsrc_t rw = make_rsrc(g.yvar + tok0 * H + h, (uint32_t)((nt - 1) * H + 1) * 4);
+        const rsrc_t rw = make_rsrc(g.yvar + (seq0 + (size_t)oc * C) * H + h, (uint32_t)((nt - 1) * H + 1) * 4);
 #pragma unroll
-            for (int j = 0; j < TPG; ++j)
-                bst32(rw, n == DK - 1 ? (uint32_t)((gq * TPG + j) * H) * 4 : 0x7ffffff0u, oyv[j]);
-        }
+        for (int j = 0; j < TPG; ++j)   // tokens past the chunk's last one, and the other lanes, fall outside
+            bst32(rw, n == DK - 1 ? (uint32_t)((gq * TPG + j) * H) * 4 : 0x7ffffff0u, oyv[j]);
     };
 
-    auto round = [&](int c, Pre& cur, Pre& nxt) {
-        const double* lam_s = sLam + (c & 1) * DK;
+    // ---- walk waves, chunk c: stage and group transfers, then the next chunk's fetch
+    auto walk1 = [&](int c, Pre& cur, Pre& nxt) {
         flush();
+        const double* lam_s = sLam + (c & 1) * DK;
         if (saved_lam && tid < DK) saved_lam[((size_t)bh * nchunk + c) * DK + tid] = lam_s[tid];
-        // ---- this chunk's values and its start state into LDS (the state also into the
-        // saved context), the walk lanes' transfers; then the next chunk's fetch
+        double* V = sV[c & 1];
 #pragma unroll
         for (int m = 0; m < NVE; ++m) {
-            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
-            sV[t * PV + d] = (double)cur.v[m];
+            const int e = tid + kWT * m, t = e / DV, d = e % DV;
+            V[t * PV + d] = (double)cur.v[m];
         }
-        if (hown)
-            for (int r = 0; r < 4; ++r) {
-                const int row = 16 * tn + drow(r, lane), col = 16 * td + (lane & 15);
-                sH[row * PV + col] = Hs[r];
-                if (saved_H)
-                    bst64(make_rsrc(saved_H + ((size_t)bh * (nchunk + 1) + c) * DK * DV, DK * DV * 8),
-                          (uint32_t)(row * DV + col) * 8, Hs[r]);
-            }
         group_transfer(cur.w, qs, gq, n);
         if (c + 1 < nchunk) fetch(nxt, c + 1);
-        __syncthreads();   // transfers, values, state in; lam_s visible
-
-        // ---- the lane's own tokens from the chained start
-        const double lam0c = lam_s[n];
+    };
+    // ---- walk waves, chunk c: the lane's own tokens from the chained start
+    auto walk2 = [&](int c, Pre& cur) {
+        double* Qp = sQp[c & 1];
+        double* Kn = sKn[c & 1];
         double x, z, A;
-        chain_start<DK, G>(qs, gq, n, lam0c, x, z, A);
+        chain_start<DK, G>(qs, gq, n, sLam[(c & 1) * DK + n], x, z, A);
         double wv[TPG];   // q^2 / lam_t
 #pragma unroll
         for (int j = 0; j < TPG; ++j) {
@@ -324,12 +320,12 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
             const double xn = fma(kr * kv, zn, x);
             const double An = A * av;
             const double R = rcpa(xn * An);
-            const double AR = An * R;            // 1 / x_t
-            const double qp = qv * An * AR;      // q A_t / x_t
+            const double AR = An * R;               // 1 / x_t
+            const double qp = qv * An * AR;         // q A_t / x_t
             const double kn = kr * zn * (xn * R);   // k r z_t / A_t
             chk = fma(qp, kn, chk);
-            sQp[t * PQ + n] = qp;
-            sKn[t * PQ + n] = kn;
+            Qp[t * PQ + n] = qp;
+            Kn[t * PQ + n] = kn;
             wv[j] = qv * qv * zn * AR;
             x = xn;
             z = zn;
@@ -338,66 +334,92 @@ __global__ __launch_bounds__(kNT64) void fwd64_kernel(Shape s, FwdArgs g, double
         if (gq == G - 1) {   // the last group ends at the chunk end
             const double iz = rcpa(z);
             sLam[((c + 1) & 1) * DK + n] = x * iz;
-            sPC[n] = A * iz;
-        }
-        __syncthreads();   // Qp, Kn, q^2 / lam, P_C in
-
-        // ---- the readout's state part, Qp H0, and the state update, diag(P_C) (H0 + Kn^T V)
-        d4 yacc = zero_d4();
-        if (yown) yacc = tile_mm<DK, PQ, 1, PV, 1>(yacc, sQp + 16 * ti * PQ, sH + 16 * tdy, lane);
-        if (hown) {
-            Hs = tile_mm<C, 1, PQ, PV, 1>(Hs, sKn + 16 * tn, sV + 16 * td, lane);
-            for (int r = 0; r < 4; ++r) Hs[r] *= sPC[16 * tn + drow(r, lane)];
-        }
-        // ---- S = M(Qp Kn^T): tiles (0,0), (1,0), (1,1) from waves 0..2 (wave 3 repeats the
-        // last, unstored, so that every wave runs the same code), wave 1 also the zero tile
-        {
-            const int st = wave < 3 ? wave : 2;
-            const int si = st == 0 ? 0 : 1, sj = st == 2 ? 1 : 0;
-            const d4 acc = tile_mm<DK, PQ, 1, 1, PQ>(zero_d4(), sQp + 16 * si * PQ, sKn + 16 * sj * PQ, lane);
-            if (wave < 3) {
-                for (int r = 0; r < 4; ++r) {
-                    const int i = drow(r, lane), j = lane & 15;
-                    sS[(16 * si + i) * PS + 16 * sj + j] = (si == sj && j > i) ? 0.0 : acc[r];
-                }
-                if (si != sj)
-                    for (int r = 0; r < 4; ++r) sS[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
-            }
-        }
-        __syncthreads();   // S in
-
-        // ---- y = S V + Qp H0, and yvar
-        if (yown) {
-            yacc = tile_mm<C, PS, 1, PV, 1>(yacc, sS + 16 * ti * PS, sV + 16 * tdy, lane);
-            for (int r = 0; r < 4; ++r) oy[r] = (float)yacc[r];
+            sPC[c & 1][n] = A * iz;
         }
         if (g.yvar)
 #pragma unroll
             for (int j = 0; j < TPG; ++j) oyv[j] = (float)slot_sum<DK>(wv[j]);
         oc = c;
-        __syncthreads();   // LDS free for the next chunk
+    };
+    // ---- MFMA waves, chunk c: the chunk-start state into LDS (and the saved context), S =
+    // M(Qp Kn^T) (tiles (0,0), (1,0), (1,1) from waves 4..6, wave 7 repeating the last,
+    // unstored; wave 5 also writes the zero tile above the diagonal)
+    auto mfma1 = [&](int c) {
+        if (hown)
+            for (int r = 0; r < 4; ++r) {
+                const int row = 16 * tn + drow(r, lane), col = 16 * td + (lane & 15);
+                sH[row * PV + col] = Hs[r];
+                if (saved_H)
+                    bst64(make_rsrc(saved_H + ((size_t)bh * (nchunk + 1) + c) * DK * DV, DK * DV * 8),
+                          (uint32_t)(row * DV + col) * 8, Hs[r]);
+            }
+        const int st = mw < 3 ? mw : 2;
+        const int si = st == 0 ? 0 : 1, sj = st == 2 ? 1 : 0;
+        const d4 acc = tile_mm<DK, PQ, 1, 1, PQ>(zero_d4(), sQp[c & 1] + 16 * si * PQ, sKn[c & 1] + 16 * sj * PQ, lane);
+        if (mw < 3) {
+            for (int r = 0; r < 4; ++r) {
+                const int i = drow(r, lane), j = lane & 15;
+                sS[(16 * si + i) * PS + 16 * sj + j] = (si == sj && j > i) ? 0.0 : acc[r];
+            }
+            if (si != sj)
+                for (int r = 0; r < 4; ++r) sS[drow(r, lane) * PS + 16 + (lane & 15)] = 0.0;
+        }
+    };
+    // ---- MFMA waves, chunk c: y = S V + Qp H0 and the state update diag(P_C) (H0 + Kn^T V)
+    auto mfma2 = [&](int c) {
+        const double* Qp = sQp[c & 1];
+        const double* V = sV[c & 1];
+        if (yown) {
+            d4 yacc = tile_mm<DK, PQ, 1, PV, 1>(zero_d4(), Qp + 16 * ti * PQ, sH + 16 * tdy, lane);
+            yacc = tile_mm<C, PS, 1, PV, 1>(yacc, sS + 16 * ti * PS, V + 16 * tdy, lane);
+            const int nt = min(C, T - c * C);
+            const rsrc_t ry = make_rsrc(fy + ((seq0 + (size_t)c * C) * H + h) * DV, (uint32_t)((nt - 1) * H * DV + DV) * 4);
+            for (int r = 0; r < 4; ++r)   // rows past the chunk's last token fall outside the buffer
+                bst32(ry, (uint32_t)((16 * ti + drow(r, lane)) * H * DV + 16 * tdy + (lane & 15)) * 4, (float)yacc[r]);
+        }
+        if (hown) {
+            Hs = tile_mm<C, 1, PQ, PV, 1>(Hs, sKn[c & 1] + 16 * tn, V + 16 * td, lane);
+            for (int r = 0; r < 4; ++r) Hs[r] *= sPC[c & 1][16 * tn + drow(r, lane)];
+        }
+    };
+
+    // round r: the walk waves take chunk r, the MFMA waves chunk r - 1
+    auto round = [&](int r, Pre& cur, Pre& nxt) {
+        if (walker) {
+            if (r < nchunk) walk1(r, cur, nxt);
+        } else if (r >= 1) {
+            mfma1(r - 1);
+        }
+        __syncthreads();   // group transfers in; S and the chunk-start state in
+        if (walker) {
+            if (r < nchunk) walk2(r, cur);
+        } else if (r >= 1) {
+            mfma2(r - 1);
+        }
+        __syncthreads();   // chunk r's walk results in; chunk r - 1's LDS set free
     };
 
     Pre P0, P1;
     P0.w.ca = P1.w.ca = ca;
     P0.w.cp = P1.w.cp = cp;
-    if (nchunk > 0) fetch(P0, 0);
-    for (int c = 0; c < nchunk; c += 2) {
-        round(c, P0, P1);
-        if (c + 1 < nchunk) round(c + 1, P1, P0);
+    if (walker && nchunk > 0) fetch(P0, 0);
+    for (int r = 0; r <= nchunk; r += 2) {
+        round(r, P0, P1);
+        if (r + 1 <= nchunk) round(r + 1, P1, P0);
     }
-    flush();
 
     // ---- the final belief
-    const double* lam_e = sLam + (nchunk & 1) * DK;
-    if (g.lamT && tid < DK) g.lamT[(size_t)bh * DK + tid] = (float)lam_e[tid];
-    if (hown)
+    if (walker) {
+        flush();
+        if (g.lamT && tid < DK) g.lamT[(size_t)bh * DK + tid] = (float)sLam[(nchunk & 1) * DK + tid];
+        if (g.range_flag && !(fabs(chk) <= 1.0e300)) *g.range_flag = 1;
+    } else if (hown) {
         for (int r = 0; r < 4; ++r) {
             const int row = 16 * tn + drow(r, lane), col = 16 * td + (lane & 15);
             if (g.etaT) g.etaT[((size_t)bh * DK + row) * DV + col] = (float)Hs[r];
             if (saved_H) saved_H[(((size_t)bh * (nchunk + 1) + nchunk) * DK + row) * DV + col] = Hs[r];
         }
-    if (g.range_flag && !(fabs(chk) <= 1.0e300)) *g.range_flag = 1;
+    }
 }
 
 // ============================================================================ backward
@@ -771,9 +793,9 @@ hipError_t launch_fwd64(const Shape& s, const FwdArgs& a, void* saved, hipStream
     double* sH = slam ? slam + (size_t)s.B * s.H * ((s.T + kC64 - 1) / kC64) * DK : nullptr;
     const dim3 grid((unsigned)(s.B * s.H));
     if (a.ou_a)
-        hipLaunchKernelGGL((fwd64_kernel<DK, DV, true>), grid, dim3(kNT64), 0, st, s, a, slam, sH);
+        hipLaunchKernelGGL((fwd64_kernel<DK, DV, true>), grid, dim3(2 * kWT), 0, st, s, a, slam, sH);
     else
-        hipLaunchKernelGGL((fwd64_kernel<DK, DV, false>), grid, dim3(kNT64), 0, st, s, a, slam, sH);
+        hipLaunchKernelGGL((fwd64_kernel<DK, DV, false>), grid, dim3(2 * kWT), 0, st, s, a, slam, sH);
     return hipGetLastError();
 }
 
