@@ -31,8 +31,9 @@
 // chunk (the walk over 32 tokens, spread over token groups as in chunk_bwd_dk.hip),
 // and the contractions run on v_mfma_f64_16x16x4_f64.
 //
-// One workgroup of 256 threads per (b, h), dk and dv in {16, 32}.  The walk
-// lanes are (slot n = tid % dk, token group gq = tid / dk of TPG tokens); each
+// One workgroup per (b, h), dk and dv in {16, 32}: 512 threads in the forward
+// (walk waves and MFMA waves, see there), 256 in the backward.  The walk lanes
+// are 256 threads (slot n = tid % dk, token group gq = tid / dk of TPG tokens); each
 // lane forms its group's 2x2 transfer, the groups are chained through LDS from
 // the chunk-start lam, and each lane then walks its own tokens.  Tokens past the
 // sequence end enter with abar = 1, pbar = k = q = r = 0, which the walk, the
@@ -51,7 +52,7 @@ namespace kla {
 namespace {
 
 constexpr int kC64 = 32;    // tokens per chunk
-constexpr int kNT64 = 256;  // threads per workgroup
+constexpr int kNT64 = 256;  // threads per backward workgroup
 
 typedef double d4 __attribute__((ext_vector_type(4)));
 
