@@ -68,7 +68,7 @@ def test_traffic_summary_requires_matching_sources(tmp_path):
 def test_digest_sources_exist(names):
     for name in names:
         assert os.path.exists(os.path.join(ROOT, "paper_2602_10743_amd", "csrc", name)), name
-    assert "recurrent.hip" in traffic.DIGEST_SOURCES_A5 and "recurrent.hip" not in traffic.DIGEST_SOURCES
+    assert "chunk64.hip" in traffic.DIGEST_SOURCES_A5 and "chunk64.hip" not in traffic.DIGEST_SOURCES
 
 
 def test_digest_ignores_comments_only():
