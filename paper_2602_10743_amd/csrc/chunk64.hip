@@ -110,9 +110,40 @@ __device__ __forceinline__ void bst32(rsrc_t r, uint32_t voff, float x) {
     __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(x), r, voff, 0, 0);
 }
 
+typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
+typedef __attribute__((__vector_size__(4 * sizeof(uint32_t)))) uint32_t u32x4;
+
 __device__ __forceinline__ void bst64(rsrc_t r, uint32_t voff, double x) {
-    typedef __attribute__((__vector_size__(2 * sizeof(uint32_t)))) uint32_t u32x2;
     __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, x), r, voff, 0, 0);
+}
+
+// N (2 or 4) consecutive floats through a buffer in one load (offset aligned to 4 N bytes)
+template <int N>
+__device__ __forceinline__ void bldN(rsrc_t r, uint32_t voff, float* out) {
+    if constexpr (N == 4) {
+        const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) out[i] = __uint_as_float(v[i]);
+    } else {
+        static_assert(N == 2, "2 or 4 floats");
+        const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, 0, 0);
+        out[0] = __uint_as_float(v[0]);
+        out[1] = __uint_as_float(v[1]);
+    }
+}
+
+// N (2 or 4) consecutive floats from LDS (aligned to 4 N bytes) stored through a buffer in one store
+template <int N>
+__device__ __forceinline__ void bstN_lds(rsrc_t r, uint32_t voff, const float* src) {
+    if constexpr (N == 4) {
+        const float4 v = *reinterpret_cast<const float4*>(src);
+        __builtin_amdgcn_raw_buffer_store_b128(
+            u32x4{__float_as_uint(v.x), __float_as_uint(v.y), __float_as_uint(v.z), __float_as_uint(v.w)}, r, voff, 0, 0);
+    } else {
+        static_assert(N == 2, "2 or 4 floats");
+        const float2 v = *reinterpret_cast<const float2*>(src);
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{__float_as_uint(v.x), __float_as_uint(v.y)}, r, voff, 0, 0);
+    }
 }
 
 // Buffers over one chunk's rows of the per-token tensors of head h: [t][H][DK] rows
@@ -391,13 +422,13 @@ __global__ __launch_bounds__(2 * kWT) void fwd64_kernel(Shape s, FwdArgs g, doub
         } else if (r >= 1) {
             mfma1(r - 1);
         }
-        __syncthreads();   // group transfers in; S and the chunk-start state in
+        barrier_lds();   // group transfers in; S and the chunk-start state in
         if (walker) {
             if (r < nchunk) walk2(r, cur);
         } else if (r >= 1) {
             mfma2(r - 1);
         }
-        __syncthreads();   // chunk r's walk results in; chunk r - 1's LDS set free
+        barrier_lds();   // chunk r's walk results in; chunk r - 1's LDS set free
     };
 
     Pre P0, P1;
@@ -430,11 +461,21 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
     constexpr int C = kC64, G = kNT64 / DK, TPG = C / G;
     constexpr int PQ = DK + 1, PV = DV + 1, PS = C + 1;
     constexpr int NTD = DV / 16, NTN = DK / 16, NTT = C / 16;
-    constexpr int NVE = C * DV / kNT64, NHE = (DK * DV + kNT64 - 1) / kNT64;
+    // values per thread of a chunk's [C][DV] and [C][DK] rows and of a [DK][DV] state
+    constexpr int NVE = C * DV / kNT64, NKE = C * DK / kNT64, NHE = DK * DV / kNT64;
+    constexpr int NIN = TI ? 2 : 4;    // staged input rows: abar, pbar (per-token gates only), k, q
+    constexpr int NOUT = TI ? 2 : 4;   // staged gradient rows: dq, dk, dabar, dpbar (per-token gates only)
+    constexpr int NINB = NIN * C * DK * 4 / 1024;   // 1 KiB direct loads of the input rows per chunk
+    static_assert(NINB % 4 == 0 && (NVE == 2 || NVE == 4) && (NKE == 2 || NKE == 4), "staging shapes");
+    // row strides of the staged gradients: the walk lanes' writes (rows TPG apart within a
+    // wave) fall in distinct banks, and every row starts on 16 bytes
+    constexpr int SO = 40, SVD = DV == 32 ? 48 : 16;
     __shared__ double sQp[C * PQ], sKn[C * PQ], sV[C * PV], sDY[C * PV], sS[C * PS], sB[C * PS];
     __shared__ double sH0[DK * PV], sGs[DK * PV], sX[C * PQ], sY[C * PQ];
     __shared__ double qs[G * 5 * DK];
-    __shared__ double sLam[DK], sPC[DK], sCar[2 * 2 * DK];   // carries (c, S) by round parity
+    __shared__ double sPC[DK], sCar[2 * 2 * DK];   // carries (c, S) by round parity
+    __shared__ __attribute__((aligned(16))) float sIn[NIN * C * DK];   // [NIN][C][DK]
+    __shared__ __attribute__((aligned(16))) float sOut[NOUT * C * SO], sDv[C * SVD], sDr[C];
 
     const int bh = blockIdx.x, b = bh / s.H, h = bh % s.H, H = s.H, T = s.T;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -482,99 +523,125 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
     }
     double chk = 0.0;
 
-    // a chunk's inputs, output gradients and saved start (lam, state), fetched one chunk ahead
-    struct Pre {
-        WalkIn<DK, TPG, TI> w;
-        float gv[TPG], v[NVE], dy[NVE];
-        double h0[NHE], lam;
-    };
-    auto fetch = [&](Pre& P, int cn) {
+    // Chunk cn's inputs, fetched during the round before its own: abar, pbar, k, q by 16-byte
+    // direct loads into sIn (row-major [C][DK] each), the rest into registers: v and dy (NVE
+    // consecutive values of thread tid), the saved state (NHE consecutive values), r and gv of
+    // token lane % 32, and lam of slot n.  Tokens past the sequence end read as zeros.
+    float pv[NVE], pdy[NVE], pr, pgv;
+    double ph0[NHE], plam;
+    auto prefetch = [&](int cn) {
         const int nt = min(C, T - cn * C);
         const size_t tok0 = seq0 + (size_t)cn * C;
-        P.w.load(ChunkBufs(TI ? nullptr : fa, TI ? nullptr : fp, fk, fq, fr, tok0, H, h, DK, nt), H, n, gq * TPG, nt);
-        const rsrc_t rg = make_rsrc(g.dyvar ? g.dyvar + tok0 * H + h : fr, g.dyvar ? (uint32_t)((nt - 1) * H + 1) * 4 : 0u);
+        const ChunkBufs cb(TI ? nullptr : fa, TI ? nullptr : fp, fk, fq, fr, tok0, H, h, DK, nt);
 #pragma unroll
-        for (int j = 0; j < TPG; ++j) P.gv[j] = bld32(rg, (uint32_t)((gq * TPG + j) * H) * 4);
+        for (int m = 0; m < NINB / 4; ++m) {
+            const int blk = 4 * m + wave;                            // 1 KiB block of sIn
+            const int x = blk * 1024 / (C * DK * 4);                 // its input row set
+            const int o = blk * 1024 % (C * DK * 4) + 16 * lane;     // this lane's byte within the set
+            const int t = o / (DK * 4), col = o % (DK * 4) / 4;
+            const rsrc_t rs = TI ? (x == 0 ? cb.k : cb.q) : (x == 0 ? cb.a : x == 1 ? cb.p : x == 2 ? cb.k : cb.q);
+            buf_ld128_lds(rs, sIn + blk * 256, (uint32_t)(t * H * DK + col) * 4);
+        }
+        pr = bld32(cb.r, (uint32_t)((lane & 31) * H) * 4);
+        if (g.dyvar) {
+            const rsrc_t rg = make_rsrc(g.dyvar + tok0 * H + h, (uint32_t)((nt - 1) * H + 1) * 4);
+            pgv = bld32(rg, (uint32_t)((lane & 31) * H) * 4);
+        } else {
+            pgv = 0.f;
+        }
         const size_t v0 = (tok0 * H + h) * DV;
         const uint32_t vbytes = (uint32_t)((nt - 1) * H * DV + DV) * 4;
-        const rsrc_t rv = make_rsrc(fv + v0, vbytes), rdy = make_rsrc(fdy + v0, vbytes);
+        const int t = NVE * tid / DV, d = NVE * tid % DV;
+        bldN<NVE>(make_rsrc(fv + v0, vbytes), (uint32_t)(t * H * DV + d) * 4, pv);
+        bldN<NVE>(make_rsrc(fdy + v0, vbytes), (uint32_t)(t * H * DV + d) * 4, pdy);
+        const double* hs = saved_H + ((size_t)bh * (nchunk + 1) + cn) * DK * DV + NHE * tid;
+        if constexpr (NHE == 1) {
+            ph0[0] = hs[0];
+        } else {
 #pragma unroll
-        for (int m = 0; m < NVE; ++m) {
-            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
-            const uint32_t vo = (uint32_t)(t * H * DV + d) * 4;
-            P.v[m] = bld32(rv, vo);
-            P.dy[m] = bld32(rdy, vo);
+            for (int i = 0; i < NHE / 2; ++i) {
+                const double2 hv = reinterpret_cast<const double2*>(hs)[i];
+                ph0[2 * i] = hv.x;
+                ph0[2 * i + 1] = hv.y;
+            }
         }
+        plam = saved_lam[((size_t)bh * nchunk + cn) * DK + n];
+    };
+    // the fetched chunk becomes the next one: v, dy and the saved state into their fp64 tiles,
+    // the per-lane values into the carried registers (after the wait for this wave's loads;
+    // a barrier then publishes sIn and the tiles)
+    double lam_c = 1.0;
+    float rc = 0.f, gvc = 0.f;
+    auto take = [&]() {
+        wait_vm_le<0>();
+        const int t = NVE * tid / DV, d = NVE * tid % DV;
 #pragma unroll
-        for (int m = 0; m < NHE; ++m) {
-            const int e = tid + kNT64 * m;
-            P.h0[m] = e < DK * DV ? saved_H[((size_t)bh * (nchunk + 1) + cn) * DK * DV + e] : 0.0;
+        for (int i = 0; i < NVE; ++i) {
+            sV[t * PV + d + i] = (double)pv[i];
+            sDY[t * PV + d + i] = (double)pdy[i];
         }
-        P.lam = saved_lam[((size_t)bh * nchunk + cn) * DK + n];
+        const int hr = NHE * tid / DV, hc = NHE * tid % DV;
+#pragma unroll
+        for (int i = 0; i < NHE; ++i) sH0[hr * PV + hc + i] = ph0[i];
+        lam_c = plam;
+        rc = pr;
+        gvc = pgv;
     };
 
-    // The gradients of a round are stored at the start of the next one, before that
-    // round's fetch (as in the forward): dV of this wave's tile, dq, dk, dabar, dpbar of
-    // the lane's tokens, dr of token tid.
+    // A round's gradients are staged in LDS (dV by the MFMA waves, the rest by the walk lanes,
+    // dr by the last lane of each group) and stored at the start of the next round, 16 or 8
+    // bytes per thread and row set, through buffers that drop the tokens past the end.
     const bool dvown = FULL || wave < NTT * NTD;
     const int tj = wave / NTD, dd = wave % NTD;   // this wave's dV tile
-    float odv[4] = {0.f, 0.f, 0.f, 0.f}, odq[TPG], odk[TPG], oda[TPG], odp[TPG], odr[TPG];   // odr: lane n = DK - 1
     int oc = -1;
     auto flush = [&]() {
         if (oc < 0) return;
         const int nt = min(C, T - oc * C);
         const size_t tok0 = seq0 + (size_t)oc * C;
-        // buffers end at the chunk's last valid token: stores past it are dropped
-        if (dvown) {
+        {
+            const int t = NVE * tid / DV, d = NVE * tid % DV;
             const rsrc_t rv = make_rsrc(gdv + (tok0 * H + h) * DV, (uint32_t)((nt - 1) * H * DV + DV) * 4);
-            for (int r = 0; r < 4; ++r)
-                bst32(rv, (uint32_t)((16 * tj + drow(r, lane)) * H * DV + 16 * dd + (lane & 15)) * 4, odv[r]);
+            bstN_lds<NVE>(rv, (uint32_t)(t * H * DV + d) * 4, sDv + t * SVD + d);
         }
         const size_t k0 = (tok0 * H + h) * DK;
         const uint32_t kbytes = (uint32_t)((nt - 1) * H * DK + DK) * 4;
-        const rsrc_t rq = make_rsrc(gdq + k0, kbytes), rk = make_rsrc(gdk + k0, kbytes);
-#pragma unroll
-        for (int j = 0; j < TPG; ++j) {
-            const uint32_t vo = (uint32_t)((gq * TPG + j) * H * DK + n) * 4;
-            bst32(rq, vo, odq[j]);
-            bst32(rk, vo, odk[j]);
-        }
+        const int t = NKE * tid / DK, col = NKE * tid % DK;
+        const uint32_t vo = (uint32_t)(t * H * DK + col) * 4;
+        bstN_lds<NKE>(make_rsrc(gdq + k0, kbytes), vo, sOut + t * SO + col);
+        bstN_lds<NKE>(make_rsrc(gdk + k0, kbytes), vo, sOut + C * SO + t * SO + col);
         if constexpr (!TI) {
-            const rsrc_t ra = make_rsrc(gda + k0, kbytes), rp = make_rsrc(gdp + k0, kbytes);
-#pragma unroll
-            for (int j = 0; j < TPG; ++j) {
-                const uint32_t vo = (uint32_t)((gq * TPG + j) * H * DK + n) * 4;
-                bst32(ra, vo, oda[j]);
-                bst32(rp, vo, odp[j]);
-            }
+            bstN_lds<NKE>(make_rsrc(gda + k0, kbytes), vo, sOut + 2 * C * SO + t * SO + col);
+            bstN_lds<NKE>(make_rsrc(gdp + k0, kbytes), vo, sOut + 3 * C * SO + t * SO + col);
         }
-        const rsrc_t rr = make_rsrc(gdr + tok0 * H + h, (uint32_t)((nt - 1) * H + 1) * 4);
-#pragma unroll
-        for (int j = 0; j < TPG; ++j) bst32(rr, n == DK - 1 ? (uint32_t)((gq * TPG + j) * H) * 4 : 0x7ffffff0u, odr[j]);
+        if (tid < C)
+            bst32(make_rsrc(gdr + tok0 * H + h, (uint32_t)((nt - 1) * H + 1) * 4), (uint32_t)(tid * H) * 4, sDr[tid]);
     };
 
-    auto round = [&](int c, Pre& cur, Pre& nxt) {
+    auto round = [&](int c) {
         const int nt = min(C, T - c * C);
         flush();
-        // ---- stage the chunk into LDS, the walk lanes' transfers; then the previous chunk's fetch
-#pragma unroll
-        for (int m = 0; m < NVE; ++m) {
-            const int e = tid + kNT64 * m, t = e / DV, d = e % DV;
-            sV[t * PV + d] = (double)cur.v[m];
-            sDY[t * PV + d] = (double)cur.dy[m];
-        }
-#pragma unroll
-        for (int m = 0; m < NHE; ++m) {
-            const int e = tid + kNT64 * m;
-            if (e < DK * DV) sH0[(e / DV) * PV + e % DV] = cur.h0[m];
-        }
-        if (tid < DK) sLam[tid] = cur.lam;
+        // ---- the lane's tokens from the staged rows, and their group transfer; then the fetch of
+        // the previous chunk (sIn is free once every lane has read it)
+        WalkIn<DK, TPG, TI> wi;
+        wi.ca = ca;
+        wi.cp = cp;
+        wi.nv = min(max(nt - gq * TPG, 0), TPG);
         double gv[TPG];
 #pragma unroll
-        for (int j = 0; j < TPG; ++j) gv[j] = (double)cur.gv[j];
-        group_transfer(cur.w, qs, gq, n);
-        if (c >= 1) fetch(nxt, c - 1);
-        __syncthreads();
+        for (int j = 0; j < TPG; ++j) {
+            const int t = gq * TPG + j;
+            if constexpr (!TI) {
+                wi.a[j] = sIn[t * DK + n];
+                wi.p[j] = sIn[C * DK + t * DK + n];
+            }
+            wi.k[j] = sIn[(NIN - 2) * C * DK + t * DK + n];
+            wi.q[j] = sIn[(NIN - 1) * C * DK + t * DK + n];
+            wi.r[j] = __shfl(rc, t, 64);
+            gv[j] = (double)__shfl(gvc, t, 64);
+        }
+        group_transfer(wi, qs, gq, n);
+        barrier_lds();
+        if (c >= 1) prefetch(c - 1);
 
         // ---- the walk over the lane's tokens: Qp, Kn, and what the adjoint walk needs
         // (kept across the contractions: lam_{t-1}, P_t, 1 / lam_t, rho_t; the reciprocals and
@@ -582,19 +649,19 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         double lam_p[TPG], P_t[TPG], il_t[TPG], rho[TPG];
         {
             double x, z, A;
-            chain_start<DK, G>(qs, gq, n, sLam[n], x, z, A);
+            chain_start<DK, G>(qs, gq, n, lam_c, x, z, A);
             double izp = rcpa(z);
 #pragma unroll
             for (int j = 0; j < TPG; ++j) {
                 const int t = gq * TPG + j;
-                const double av = cur.w.A(j), kv = cur.w.K(j);
-                const double kr = kv * cur.w.R(j);
-                const double zn = fma(cur.w.P(j), x, av * av * z);
+                const double av = wi.A(j), kv = wi.K(j);
+                const double kr = kv * wi.R(j);
+                const double zn = fma(wi.P(j), x, av * av * z);
                 const double xn = fma(kr * kv, zn, x);
                 const double An = A * av;
                 const double R = rcpa(xn * An), iz = rcpa(zn);
                 const double AR = An * R, XR = xn * R;   // 1 / x_t, 1 / A_t
-                const double qp = cur.w.Q(j) * An * AR, kn = kr * zn * XR;
+                const double qp = wi.Q(j) * An * AR, kn = kr * zn * XR;
                 chk = fma(qp, kn, chk);
                 sQp[t * PQ + n] = qp;
                 sKn[t * PQ + n] = kn;
@@ -609,7 +676,7 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
             }
             if (gq == G - 1) sPC[n] = A * rcpa(z);
         }
-        __syncthreads();   // Qp, Kn, P_C in
+        barrier_lds();   // Qp, Kn, P_C in
 
         // ---- S = M(Qp Kn^T) and B = M(dY V^T): tiles (0,0), (1,0), (1,1) of each from waves
         // 0..2 (wave 3 repeats the last, unstored); the tiles (1,0) also write the zero tile above
@@ -639,14 +706,14 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
                 Gt[r] *= sPC[row];
                 sGs[row * PV + 16 * td + (lane & 15)] = Gt[r];
             }
-        __syncthreads();   // S, B, Gs in
+        barrier_lds();   // S, B, Gs in
 
         // ---- dV = S^T dY + Kn Gs (tiles (tj, td)); X = dY H0^T + B Kn and Y = B^T Qp + V Gs^T
         // (tiles (t, tn)); G' = Qp^T dY + Gs (this wave's tile)
         if (dvown) {
             d4 acc = tile_mm<C, 1, PS, PV, 1>(zero_d4(), sS + 16 * tj, sDY + 16 * dd, lane);
             acc = tile_mm<DK, PQ, 1, PV, 1>(acc, sKn + 16 * tj * PQ, sGs + 16 * dd, lane);
-            for (int r = 0; r < 4; ++r) odv[r] = (float)acc[r];
+            for (int r = 0; r < 4; ++r) sDv[(16 * tj + drow(r, lane)) * SVD + 16 * dd + (lane & 15)] = (float)acc[r];
         }
         __builtin_amdgcn_sched_barrier(0);   // one job's operands in registers at a time
         if (FULL || wave < NTT * NTN) {
@@ -663,7 +730,7 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         }
         __builtin_amdgcn_sched_barrier(0);
         if (gown) Gt = tile_mm<C, 1, PQ, PV, 1>(Gt, sQp + 16 * tn, sDY + 16 * td, lane);
-        __syncthreads();   // X, Y in
+        barrier_lds();   // X, Y in
 
         // ---- adjoint pass 1: the lane's tokens in reverse, each the affine step
         //   (c, S) -> (alpha (c - w) - beta (S + u), S + u),
@@ -671,12 +738,12 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         // per token of the lane: u, w and the step coefficients alpha = abar^2 rho^2, beta = pbar rho
         double dqt_[TPG], dkh_[TPG];
         auto coef = [&](int j, double& u, double& w, double& al, double& be) {
-            const double qv = cur.w.Q(j), av = cur.w.A(j);
+            const double qv = wi.Q(j), av = wi.A(j);
             const double qi = qv * il_t[j];
-            u = qi * dqt_[j] - cur.w.K(j) * cur.w.R(j) * dkh_[j];
+            u = qi * dqt_[j] - wi.K(j) * wi.R(j) * dkh_[j];
             w = qi * fma(qv, gv[j], dqt_[j]) * il_t[j];
             al = av * av * rho[j] * rho[j];
-            be = cur.w.P(j) * rho[j];
+            be = wi.P(j) * rho[j];
         };
         double Am = 1.0, Bm = 0.0, Cm = 0.0, Dm = 0.0;
 #pragma unroll
@@ -695,7 +762,7 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         qs[(gq * 4 + 1) * DK + n] = Bm;
         qs[(gq * 4 + 2) * DK + n] = Cm;
         qs[(gq * 4 + 3) * DK + n] = Dm;
-        __syncthreads();
+        barrier_lds();
 
         // ---- pass 2: carries into the lane's group (through the later groups) and out of the
         // chunk, then the gradients of its tokens
@@ -728,7 +795,7 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
             coef(j, u, w, al, be);
             SS += u;
             const double gl = cc - w;
-            const double kv = cur.w.K(j), rv = cur.w.R(j), av = cur.w.A(j), qv = cur.w.Q(j);
+            const double kv = wi.K(j), rv = wi.R(j), av = wi.A(j), qv = wi.Q(j);
             const double r2 = rho[j] * rho[j];
             const double dkv = fma(2.0 * kv * rv, gl, rv * dkh_[j]);
             const double drho = fma(gl, lam_p[j], SS * rcpa(rho[j]));
@@ -737,29 +804,33 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
             const double dqv = fma(2.0 * qv, gv[j], dqt_[j]) * il_t[j];
             drt[j] = fma(kv * kv, gl, kv * dkh_[j]);
             cc = fma(al, gl, -be * SS);
-            odq[j] = (float)dqv;
-            odk[j] = (float)dkv;
-            oda[j] = (float)dav;
-            odp[j] = (float)dpv;
+            sOut[t * SO + n] = (float)dqv;
+            sOut[C * SO + t * SO + n] = (float)dkv;
+            if constexpr (!TI) {
+                sOut[2 * C * SO + t * SO + n] = (float)dav;
+                sOut[3 * C * SO + t * SO + n] = (float)dpv;
+            }
             if (TI && t < nt) {
                 sum_da += dav;
                 sum_dp += dpv;
             }
         }
 #pragma unroll
-        for (int j = 0; j < TPG; ++j) odr[j] = (float)slot_sum<DK>(drt[j]);   // dr: the sum over the slots
+        for (int j = 0; j < TPG; ++j) {   // dr: the sum over the slots
+            const double dr = slot_sum<DK>(drt[j]);
+            if (n == DK - 1) sDr[gq * TPG + j] = (float)dr;
+        }
         oc = c;
-        __syncthreads();   // qs free for the next chunk's transfers
+        if (c >= 1) take();
+        barrier_lds();   // qs free for the next chunk's transfers; the next chunk staged
     };
 
-    Pre P0, P1;
-    P0.w.ca = P1.w.ca = ca;
-    P0.w.cp = P1.w.cp = cp;
-    if (nchunk > 0) fetch(P0, nchunk - 1);
-    for (int c = nchunk - 1; c >= 0; c -= 2) {
-        round(c, P0, P1);
-        if (c >= 1) round(c - 1, P1, P0);
+    if (nchunk > 0) {
+        prefetch(nchunk - 1);
+        take();
     }
+    barrier_lds();
+    for (int c = nchunk - 1; c >= 0; --c) round(c);
     flush();
 
     // ---- gradients of the initial belief, and the OU gate sums
@@ -771,10 +842,10 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         double* part = static_cast<double*>(g.ou_part);
         const size_t np = (size_t)s.B * s.H * DK;
         // the slot's sum over all token groups (tids n, n + DK, ...), through LDS
-        __syncthreads();
+        barrier_lds();
         sX[gq * PQ + n] = sum_da;
         sY[gq * PQ + n] = sum_dp;
-        __syncthreads();
+        barrier_lds();
         if (tid < DK) {
             double sa = 0.0, sp = 0.0;
             for (int g2 = 0; g2 < G; ++g2) {

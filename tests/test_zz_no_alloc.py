@@ -43,11 +43,17 @@ def _one(kla, B, T, H, dk, dv, dtype, dist, seed):
         assert torch.equal(got[n], ref[n]), f"{n} differs from kla_backward (B{B} T{T} H{H} d{dk}/{dv} {dtype})"
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_noalloc_matches_backward_twice(kla, dtype):
-    log(f"noalloc {dtype}: B2 T300 H4 d128, then B1 T70 H2 d64/32")
-    _one(kla, 2, 300, 4, 128, 128, dtype, "lm", seed=11)
-    _one(kla, 1, 70, 2, 64, 32, dtype, "lm", seed=12)
+# bf16 at these shapes runs the chunked kernels; fp32 the token-recurrent ones (d128, 64/32)
+# and the chunked fp64 ones (32/32, 32/16)
+@pytest.mark.parametrize("dtype,first,second", [
+    ("bf16", (2, 300, 4, 128, 128), (1, 70, 2, 64, 32)),
+    ("f32", (2, 300, 4, 128, 128), (1, 70, 2, 64, 32)),
+    ("f32", (2, 300, 4, 32, 32), (1, 45, 2, 32, 16)),
+])
+def test_noalloc_matches_backward_twice(kla, dtype, first, second):
+    log(f"noalloc {dtype}: B T H dk dv {first}, then {second}")
+    _one(kla, *first, dtype, "lm", seed=11)
+    _one(kla, *second, dtype, "lm", seed=12)
 
 
 def test_noalloc_rejects_oversize_and_missing_context(kla):
