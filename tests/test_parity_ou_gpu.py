@@ -71,6 +71,8 @@ OU_SMALL = [  # B, T, H, dk, dv, dtype, dist
     (2, 100, 3, 16, 16, "f32", "c0"),
     (1, 77, 2, 32, 64, "f32", "lm"),
     (2, 95, 2, 32, 32, "f32", "lm"),
+    (1, 64, 3, 32, 16, "f32", "c0"),
+    (2, 33, 1, 16, 32, "f32", "lm"),
     (1, 33, 2, 16, 128, "bf16", "c0"),
     (2, 130, 2, 64, 32, "bf16", "lm"),
     (1, 200, 2, 128, 128, "bf16", "lm"),
