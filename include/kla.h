@@ -172,7 +172,7 @@ kla_status kla_backward(const kla_desc* desc,
  *   saved: required (T > 0): the context is read, never recomputed here.
  *   Returns KLA_ERR_WORKSPACE when kla_backward_workspace(desc, 1) exceeds
  *   KLA_NOALLOC_SCRATCH_BYTES (64 MiB: the LM-layer shape B8 T2048 H16 d128 bf16
- *   needs 8 MiB, the state-tracking shape B64 T512 H4 d32 fp32 34 MiB).
+ *   needs 8 MiB, the state-tracking shape B64 T512 H4 d32 fp32 256 bytes).
  *   Calls that overlap on one GPU share its workspace and race: order them on one
  *   stream.  With KLA_CHECK=1 the call synchronises, which graph capture forbids.
  */
