@@ -455,6 +455,13 @@ __global__ __launch_bounds__(2 * kWT) void fwd64_kernel(Shape s, FwdArgs g, doub
 }
 
 // ============================================================================ backward
+// Four waves (one per SIMD) take each chunk, from the last, through every phase, with an
+// LDS barrier after each: the chunk's inputs from the staging area and the group
+// transfers | the walk (Qp, Kn, P_C; the next chunk's fetch issued) | S, B, Gs | dV, X, Y,
+// G' | adjoint pass 1 | adjoint pass 2 (gradients staged; the next chunk's inputs staged).
+// Overlapping the phases on eight waves, as the forward does, was slower: the fp64 walk and
+// adjoint work and the fp64 MFMAs contend for the same units, and the two roles' state does
+// not fit 256 registers per wave.
 template <int DK, int DV, bool TI>
 __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const double* saved_lam,
                                                       const double* saved_H) {
