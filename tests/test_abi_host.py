@@ -205,3 +205,15 @@ def test_saved_context_layout_follows_the_backward(lib):
     nchunk = (T + 31) // 32
     chunked = B * H * dk * (3 * nchunk + (nchunk + 1) * 32) * 4   # walk state (3 rows), then states
     assert K.kla_saved_bytes(_desc(B, T, H, dk, 32, 1)) == chunked
+    # fp32 inputs: the chunked fp64 path at dk, dv <= 32 (lam at every chunk start, then the
+    # states, fp64), the token-recurrent fp64 kernels above
+    for dk2, dv2 in ((32, 32), (32, 16), (16, 32), (16, 16)):
+        c64 = B * H * dk2 * (nchunk + (nchunk + 1) * dv2) * 8
+        assert K.kla_saved_bytes(_desc(B, T, H, dk2, dv2, 0)) == c64
+        # with a saved context the fp64 chunk backward needs only the validation flag's slot;
+        # without one, room for the recomputed context and a scratch output
+        with_ctx = K.kla_backward_workspace(_desc(B, T, H, dk2, dv2, 0), True)
+        assert 0 < with_ctx <= 256
+        assert K.kla_backward_workspace(_desc(B, T, H, dk2, dv2, 0), False) >= with_ctx + c64 + B * T * H * dv2 * 4
+    rec64 = (B * T * H * 64 + B * H * nck * 64 * 32) * 8
+    assert K.kla_saved_bytes(_desc(B, T, H, 64, 32, 0)) == rec64
