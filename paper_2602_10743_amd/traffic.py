@@ -22,6 +22,12 @@ The state-tracking workload (fp32, chunked fp64 kernels): the same two runs with
 `bench.py --a5 --steps 2 --warmup 1 --copy-calibration`, then
   python -m paper_2602_10743_amd.traffic D/fetch D/write --a5 > profiles/a5_state_tracking_traffic.md
 
+The kernel-trace tables of profiles/*_kernel_trace.md come from the stats file of a
+`rocprofv3 --kernel-trace --stats --output-format csv -d D/trace -o bench -- python bench.py ...`
+run:
+  python -m paper_2602_10743_amd.traffic --trace D/trace/bench_kernel_stats.csv [name,name,...]
+(the optional list keeps the kernels whose names contain one of the given parts).
+
 MFMA and VALU utilisation per kernel come from a third run:
   rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_INSTS_VALU \\
       GRBM_GUI_ACTIVE --output-format csv -d D/util -o run -- \\
@@ -248,7 +254,29 @@ def summarise_util(run_dir: str, a5: bool = False) -> str:
     return "\n".join(lines)
 
 
+def trace_table(stats_csv: str, keep=None) -> str:
+    """Markdown table of a rocprofv3 kernel_stats.csv: calls, average, min and max
+    duration (us) and share of the total, longest first."""
+    rows = []
+    with open(stats_csv, newline="") as f:
+        for r in csv.DictReader(f):
+            name = re.sub(r"\(.*\)$", "", r["Name"].replace("void ", "").replace("kla::(anonymous namespace)::", ""))
+            if keep and not any(k in name for k in keep):
+                continue
+            rows.append((name, int(r["Calls"]), float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+                         float(r["MaxNs"]) / 1e3, float(r["TotalDurationNs"])))
+    total = sum(r[5] for r in rows) or 1.0
+    rows.sort(key=lambda r: -r[5])
+    out = ["| kernel | calls | avg us | min us | max us | share |", "|---|---|---|---|---|---|"]
+    for name, calls, avg, lo, hi, tot in rows:
+        out.append(f"| {name} | {calls} | {avg:.1f} | {lo:.1f} | {hi:.1f} | {100 * tot / total:.1f}% |")
+    return "\n".join(out)
+
+
 if __name__ == "__main__":
+    if len(sys.argv) in (3, 4) and sys.argv[1] == "--trace":
+        print(trace_table(sys.argv[2], sys.argv[3].split(",") if len(sys.argv) == 4 else None))
+        sys.exit(0)
     if len(sys.argv) == 3 and sys.argv[1] in ("--util", "--util-a5"):
         print(summarise_util(sys.argv[2], a5=sys.argv[1] == "--util-a5"))
         sys.exit(0)

@@ -76,3 +76,19 @@ def test_digest_ignores_comments_only():
     b = "/* header */\nint f(int x) {\n    return 2 * x;\n}\n"
     assert traffic.code_text(a) == traffic.code_text(b)
     assert traffic.code_text(a) != traffic.code_text(a.replace("2 * x", "3 * x"))
+
+
+def test_trace_table_from_kernel_stats(tmp_path):
+    stats = tmp_path / "bench_kernel_stats.csv"
+    stats.write_text(
+        '"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n'
+        '"void kla::(anonymous namespace)::bwd_dk_kernel<128, 128, false, false>(kla::Shape, kla::BwdArgs)",'
+        '"2","900000","450000","60.0","440000","460000","1"\n'
+        '"void kla::(anonymous namespace)::fwd_chunk_kernel<128, 128, false, false, false>(kla::Shape)",'
+        '"2","600000","300000","40.0","290000","310000","1"\n'
+        '"at::native::fill_kernel(float)","5","100","20","0.0","10","30","1"\n')
+    out = traffic.trace_table(str(stats), ["bwd_dk", "fwd_chunk"]).splitlines()
+    assert out[0].startswith("| kernel | calls | avg us")
+    assert out[2] == "| bwd_dk_kernel<128, 128, false, false> | 2 | 450.0 | 440.0 | 460.0 | 60.0% |"
+    assert out[3] == "| fwd_chunk_kernel<128, 128, false, false, false> | 2 | 300.0 | 290.0 | 310.0 | 40.0% |"
+    assert len(out) == 4   # the fill kernel is left out
