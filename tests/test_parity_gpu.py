@@ -379,11 +379,11 @@ def test_workload0_tiny_forward(kla):
 
 
 def test_workload1_state_tracking_fwd_bwd(kla):
-    _workload_parity(kla, 1, 12, backward=True)
+    _workload_parity(kla, 1, 32, backward=True)
 
 
 def test_workload2_lm_layer_fwd_bwd(kla):
-    _workload_parity(kla, 2, 6, backward=True)
+    _workload_parity(kla, 2, 12, backward=True)
 
 
 def test_workload3_long_context_forward(kla):
@@ -407,7 +407,7 @@ def test_workload4_decode(kla):
     dbits = K.decode_inputs(w, as_bits=True)
     dx = {n: bits_to_torch(dbits[n], DEV) for n in dbits}
     del dbits
-    pairs = _sample_pairs(w, 3)
+    pairs = _sample_pairs(w, 8)
     bi = [b for b, _ in pairs]
     hi = [h for _, h in pairs]
     ys = []
