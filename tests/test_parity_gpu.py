@@ -388,8 +388,8 @@ def test_workload2_lm_layer_fwd_bwd(kla):
 
 def test_workload3_long_context_forward(kla):
     w = K.WORKLOADS[3]
-    # the corner pairs (heads 0 and 15: a normal-gate head and a near-one-gate head) and two more
-    _workload_parity(kla, 3, 4, backward=False)
+    # the corner pairs (heads 0 and 15: a normal-gate head and a near-one-gate head) and six more
+    _workload_parity(kla, 3, 8, backward=False)
 
 
 def test_workload4_decode(kla):
