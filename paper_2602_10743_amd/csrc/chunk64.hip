@@ -651,9 +651,9 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
         if (c >= 1) prefetch(c - 1);
 
         // ---- the walk over the lane's tokens: Qp, Kn, and what the adjoint walk needs
-        // (kept across the contractions: lam_{t-1}, P_t, 1 / lam_t, rho_t; the reciprocals and
-        // coefficients of the adjoint walk are formed again from them where used)
-        double lam_p[TPG], P_t[TPG], il_t[TPG], rho[TPG];
+        // (kept across the contractions: lam_{t-1}, P_t, 1 / lam_t, rho_t and 1 / rho_t; the step
+        // coefficients of the adjoint walk are formed in its first pass and kept for the second)
+        double lam_p[TPG], P_t[TPG], il_t[TPG], rho[TPG], irho[TPG];
         {
             double x, z, A;
             chain_start<DK, G>(qs, gq, n, lam_c, x, z, A);
@@ -676,6 +676,7 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
                 P_t[j] = An * iz;
                 il_t[j] = zn * AR;
                 rho[j] = z * iz;
+                irho[j] = zn * izp;   // 1 / rho_t = z_t / z_{t-1}
                 izp = iz;
                 x = xn;
                 z = zn;
@@ -753,6 +754,7 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
             be = wi.P(j) * rho[j];
         };
         double Am = 1.0, Bm = 0.0, Cm = 0.0, Dm = 0.0;
+        double cu[TPG], cw[TPG], cal[TPG], cbe[TPG];   // the step coefficients, kept for pass 2
 #pragma unroll
         for (int j = TPG - 1; j >= 0; --j) {
             const int t = gq * TPG + j;
@@ -760,6 +762,10 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
             dkh_[j] = sY[t * PQ + n] * rcpa(P_t[j]);
             double u, w, al, be;
             coef(j, u, w, al, be);
+            cu[j] = u;
+            cw[j] = w;
+            cal[j] = al;
+            cbe[j] = be;
             Cm = al * Cm - be * Dm - (al * w + be * u);
             Bm = al * Bm - be;
             Am = al * Am;
@@ -798,14 +804,13 @@ __global__ __launch_bounds__(kNT64) void bwd64_kernel(Shape s, BwdArgs g, const 
 #pragma unroll
         for (int j = TPG - 1; j >= 0; --j) {
             const int t = gq * TPG + j;
-            double u, w, al, be;
-            coef(j, u, w, al, be);
+            const double u = cu[j], w = cw[j], al = cal[j], be = cbe[j];
             SS += u;
             const double gl = cc - w;
             const double kv = wi.K(j), rv = wi.R(j), av = wi.A(j), qv = wi.Q(j);
             const double r2 = rho[j] * rho[j];
             const double dkv = fma(2.0 * kv * rv, gl, rv * dkh_[j]);
-            const double drho = fma(gl, lam_p[j], SS * rcpa(rho[j]));
+            const double drho = fma(gl, lam_p[j], SS * irho[j]);
             const double dav = fma(-2.0 * av * r2, drho, SS * rcpa(av));
             const double dpv = -lam_p[j] * r2 * drho;
             const double dqv = fma(2.0 * qv, gv[j], dqt_[j]) * il_t[j];
